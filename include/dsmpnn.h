@@ -1,0 +1,241 @@
+/*
+ * dsmpnn.h -- C ABI of the MI355X (gfx950) hot path of DS-MPNN
+ * (Kakka et al., "Sampling-based Distributed Training with Message Passing
+ * Neural Network", arXiv 2402.15106).
+ *
+ * The calls follow the paper's statement of the problem:
+ *   sample nodes            (Sec. 2.1; Algorithm 1, node-sampling step)
+ *   build the radius graph  (Sec. 2.1; Algorithm 1, edge-index creation and
+ *                            edge-sampling steps)
+ *   run an edge-conditioned message-passing layer forward and backward
+ *                           (eq. (1), eq. (ii); Algorithm 1, graph-convolution
+ *                            step with residual, and its backpropagation)
+ *
+ * Conventions shared by every call
+ *   - Pointers marked "device" address GPU memory of the handle's device;
+ *     pointers marked "host" address host memory.  The caller owns every
+ *     buffer; the library allocates nothing in any call except dsmp_create.
+ *   - Work is enqueued on the stream bound with dsmp_set_stream (default:
+ *     the null stream) and is asynchronous unless a call says it
+ *     synchronises.
+ *   - Every call returns a dsmp_status.  On failure nothing has been
+ *     enqueued (argument errors are found on the host before any launch),
+ *     except where a call states otherwise; dsmp_last_error(h) then holds a
+ *     message.  The library never aborts the process.
+ *   - Integer index arrays are int32 (sizes beyond 2^31-1 edges or nodes
+ *     are rejected with DSMP_UNSUPPORTED).
+ *   - Results are deterministic: the same inputs give bitwise-identical
+ *     outputs on every run (no floating-point atomics anywhere).
+ */
+#ifndef DSMPNN_H
+#define DSMPNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum dsmp_status {
+  DSMP_OK = 0,
+  DSMP_INVALID_ARG = 1,          /* a null pointer, a size out of range, ... */
+  DSMP_CAPACITY = 2,             /* an output buffer is too small; the needed size is reported */
+  DSMP_HIP_ERROR = 3,            /* the HIP runtime reported an error */
+  DSMP_UNSUPPORTED = 4,          /* a valid request this build does not implement */
+  DSMP_WORKSPACE_TOO_SMALL = 5   /* the workspace passed is smaller than the query said */
+} dsmp_status;
+
+typedef struct dsmp_handle dsmp_handle;
+
+/* Version of this ABI (major*10000 + minor*100 + patch). */
+int dsmp_version(void);
+
+/* Create a handle bound to HIP device `device` (made current for the calls
+ * made through the handle).  *out receives the handle; host memory owned by
+ * the library until dsmp_destroy. */
+dsmp_status dsmp_create(dsmp_handle** out, int device);
+dsmp_status dsmp_destroy(dsmp_handle* h);
+
+/* Bind a hipStream_t (passed as void*; NULL = the null stream). */
+dsmp_status dsmp_set_stream(dsmp_handle* h, void* stream);
+
+/* Message of the last failed call on this handle ("" if none). */
+const char* dsmp_last_error(const dsmp_handle* h);
+
+/* ------------------------------------------------------------------ sampling
+ * Nystrom node sampling (Sec. 2.1: a subset of s nodes drawn at random from
+ * the domain; Algorithm 1, node-sampling step).  Uniform sampling without
+ * replacement: candidate m gets the key
+ *     SplitMix64 output number m+1 after seeding the state with `seed`
+ * (Steele, Lea, Flood, OOPSLA 2014) and the s candidates with the smallest
+ * keys are kept.  Keys are distinct, so the set is unique.
+ *
+ * idx_out : device int32 [s], receives the kept candidates in ascending order.
+ * ws      : device workspace of at least dsmp_sample_workspace(M) bytes.
+ * Errors  : INVALID_ARG if M < 0, s < 0, s > M, or a needed pointer is NULL.
+ *           s == 0 enqueues nothing. */
+dsmp_status dsmp_sample_workspace(int64_t M, size_t* bytes);
+dsmp_status dsmp_sample_nodes(dsmp_handle* h, int64_t M, int64_t s, uint64_t seed,
+                              int32_t* idx_out, void* ws, size_t ws_bytes);
+
+/* Gather rows: dst[i, :] = src[idx[i], :] for i < n.  Rows are row_bytes long
+ * (a multiple of 4).  src: device [n_src_rows, row_bytes]; idx: device
+ * int32 [n]; dst: device [n, row_bytes].  Indices out of [0, n_src_rows)
+ * write a zero row.  Used to pull the sampled nodes' positions, attributes
+ * and features out of the candidate arrays. */
+dsmp_status dsmp_gather_rows(dsmp_handle* h, const void* src, int64_t n_src_rows,
+                             int64_t row_bytes, const int32_t* idx, int64_t n, void* dst);
+
+/* ------------------------------------------------------------- radius graph
+ * Graph kernels of Sec. 2.1: every destination i in [0, n_dst) is joined to
+ * every source j in [0, n_src), j != i, within radius r; when more than `cap`
+ * sources qualify, `cap` of them are kept (Algorithm 1, edge-index creation
+ * then edge sampling).  Sources are owned nodes first (the destinations)
+ * then halo nodes of a sub-domain.
+ *
+ * The radius test is float32 without fused multiply-add, in this order:
+ *     dx_a = p_j[a] - p_i[a];  d2 = ((dx_0*dx_0) + (dx_1*dx_1)) [+ (dx_2*dx_2)]
+ *     keep iff d2 <= r*r      (r*r rounded to float32)
+ * Cap modes: DSMP_CAP_KNN keeps the `cap` smallest (d2, j) pairs;
+ * DSMP_CAP_RANDOM keeps the `cap` smallest (key, j) pairs where key is the
+ * SplitMix64 output number i*n_src + j + 1 after seeding with `seed`, a
+ * uniform random subset (the paper's edge sampling).
+ *
+ * Output (CSR by destination, deterministic): within each row the sources
+ * are ascending.  dst[e] is the row of edge e.  csc_ptr/csc_eid group the
+ * edges by source with ascending edge ids inside each group.
+ */
+enum { DSMP_CAP_KNN = 0, DSMP_CAP_RANDOM = 1 };
+
+typedef struct dsmp_graph_query {
+  const float* pos;   /* device float32 [n_src, dim], row-major */
+  int64_t n_src;      /* >= n_dst */
+  int64_t n_dst;      /* destinations are sources [0, n_dst) */
+  int32_t dim;        /* 2 or 3 */
+  float r;            /* radius, >= 0 */
+  int32_t cap;        /* 0 = keep all, else the maximum edges per destination */
+  int32_t cap_mode;   /* DSMP_CAP_KNN or DSMP_CAP_RANDOM */
+  uint64_t seed;      /* used by DSMP_CAP_RANDOM */
+} dsmp_graph_query;
+
+typedef struct dsmp_graph {
+  int64_t n_dst;
+  int64_t n_src;
+  int64_t n_edges;    /* E */
+  int32_t* row_ptr;   /* device [n_dst+1] */
+  int32_t* col;       /* device [E]  source of each edge */
+  int32_t* dst;       /* device [E]  destination of each edge */
+  int32_t* csc_ptr;   /* device [n_src+1] */
+  int32_t* csc_eid;   /* device [E]  edge ids grouped by source */
+} dsmp_graph;
+
+/* Workspace bytes for count/build of this query. */
+dsmp_status dsmp_radius_graph_workspace(const dsmp_graph_query* q, size_t* bytes);
+
+/* Count the edges.  SYNCHRONISES the stream; *n_edges (host) receives E.
+ * UNSUPPORTED if a destination has more candidate sources than the per-row
+ * limit (4096) or E exceeds 2^31-1. */
+dsmp_status dsmp_radius_graph_count(dsmp_handle* h, const dsmp_graph_query* q, void* ws,
+                                    size_t ws_bytes, int64_t* n_edges);
+
+/* Build the graph into caller buffers (g->row_ptr ... g->csc_eid, sized for
+ * `edge_capacity` edges).  SYNCHRONISES the stream at its end and writes
+ * g->n_dst, g->n_src and g->n_edges.  If E > edge_capacity it returns
+ * DSMP_CAPACITY with g->n_edges = E; then row_ptr is complete, and no edge
+ * array has been written past edge_capacity. */
+dsmp_status dsmp_radius_graph_build(dsmp_handle* h, const dsmp_graph_query* q, void* ws,
+                                    size_t ws_bytes, int64_t edge_capacity, dsmp_graph* g);
+
+/* --------------------------------------------------------------- NNConv layer
+ * The edge-conditioned convolution of eq. (1) / eq. (ii) with the residual
+ * hop update of Algorithm 1.  For edge e = (i <- j) with attributes x_e:
+ *     z1 = ReLU(W1 x_e + b1),  z = ReLU(W2 z1 + b2)
+ *     Theta_e[p][q] = (W3 z + b3)[p*d + q]            (never materialised)
+ *     m_e[q] = sum_p Theta_e[p][q] * h_j[p]
+ *     agg_i = mean of m_e over the edges of i (0 when i has none)
+ *     y_i = agg_i + Wr h_i + br;   out_i = h_i + act(y_i)   (residual on)
+ *                                  out_i = act(y_i)         (residual off)
+ * Edge attributes: DSMP_ATTR_CONCAT  x_e = [p_i, p_j, s_i, s_j]  (de = 2*dim+2)
+ *                  DSMP_ATTR_DIFF    x_e = v_i - v_j             (de = dim+1)
+ * from node_attr rows v = (p, s) of dim+1 floats.
+ *
+ * dtype DSMP_BF16: h_in, W2, W3 and Wr take bfloat16 operands (the values in
+ * the fp32 parameter arrays are rounded to nearest-even when packed) and the
+ * products accumulate in float32; DSMP_F32 is float32 throughout.  Node
+ * attributes, W1, biases, outputs and gradients are float32 in both.
+ * Supported widths: d in {32, 64, 128}; h1, h2 in {32, 64, 128, 256};
+ * dim in {2, 3}; other values give UNSUPPORTED.
+ */
+enum { DSMP_F32 = 0, DSMP_BF16 = 1 };
+enum { DSMP_ACT_IDENTITY = 0, DSMP_ACT_RELU = 1 };
+enum { DSMP_ATTR_CONCAT = 0, DSMP_ATTR_DIFF = 1 };
+enum { DSMP_GRAD_ACCUMULATE = 1 };
+
+typedef struct dsmp_layer_desc {
+  int32_t dim;        /* spatial dimension D */
+  int32_t d;          /* latent width */
+  int32_t h1, h2;     /* kernel-MLP hidden widths */
+  int32_t dtype;      /* DSMP_F32 or DSMP_BF16 */
+  int32_t act;        /* DSMP_ACT_IDENTITY or DSMP_ACT_RELU */
+  int32_t residual;   /* 0 or 1 */
+  int32_t attr_mode;  /* DSMP_ATTR_CONCAT or DSMP_ATTR_DIFF */
+} dsmp_layer_desc;
+
+/* Parameters, device float32, torch Linear layout [out, in]:
+ * W1 [h1, de], b1 [h1], W2 [h2, h1], b2 [h2], W3 [d*d, h2], b3 [d*d],
+ * Wr [d, d], br [d]. */
+typedef struct dsmp_layer_params {
+  const float *W1, *b1, *W2, *b2, *W3, *b3, *Wr, *br;
+} dsmp_layer_params;
+
+/* Gradients, device float32, same layouts as the parameters. */
+typedef struct dsmp_layer_grads {
+  float *dW1, *db1, *dW2, *db2, *dW3, *db3, *dWr, *dbr;
+} dsmp_layer_grads;
+
+/* Bytes of the packed parameter buffer (the layouts the kernels read). */
+dsmp_status dsmp_nnconv_packed_bytes(const dsmp_layer_desc* desc, size_t* bytes);
+
+/* Pack parameters into `packed` (device, dsmp_nnconv_packed_bytes long,
+ * 256-byte aligned).  Asynchronous; the parameters may be freed or changed
+ * once the stream has passed this call. */
+dsmp_status dsmp_nnconv_pack(dsmp_handle* h, const dsmp_layer_desc* desc,
+                             const dsmp_layer_params* params, void* packed);
+
+/* Byte sizes, for a graph with g->n_dst, g->n_src, g->n_edges set:
+ *   saved : written by forward, read by backward (per layer);
+ *   fwd_ws, bwd_ws : scratch of the forward and backward calls. */
+dsmp_status dsmp_nnconv_workspace(const dsmp_layer_desc* desc, const dsmp_graph* g,
+                                  size_t* saved_bytes, size_t* fwd_ws_bytes,
+                                  size_t* bwd_ws_bytes);
+
+/* Forward.  node_attr: device float32 [n_src, dim+1]; h_in: device
+ * [n_src, d] of the layer dtype; h_out: device float32 [n_dst, d];
+ * h_out_lp: NULL or device [n_dst, d] of the layer dtype (a copy of h_out
+ * rounded to the layer dtype, e.g. the owned rows of the next layer's
+ * input); saved / ws: device, sizes from dsmp_nnconv_workspace.  Inputs are
+ * not modified; outputs are overwritten.  Uses g->row_ptr, g->col, g->dst. */
+dsmp_status dsmp_nnconv_forward(dsmp_handle* h, const dsmp_layer_desc* desc, const void* packed,
+                                const dsmp_graph* g, const float* node_attr, const void* h_in,
+                                float* h_out, void* h_out_lp, void* saved, size_t saved_bytes,
+                                void* ws, size_t ws_bytes);
+
+/* Backward of the forward call that filled `saved`.  grad_out: device
+ * float32 [n_dst, d].  grad_h: device float32 [n_src, d]; every row is
+ * written (rows of sources with no edges get only the root and residual
+ * terms, halo rows only their edge terms).  Parameter gradients go to
+ * `grads` (every pointer non-NULL), overwritten, or added to when `flags`
+ * has DSMP_GRAD_ACCUMULATE (layers sharing parameters).  Uses the whole
+ * graph including csc_ptr / csc_eid. */
+dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_desc* desc, const void* packed,
+                                 const dsmp_graph* g, const float* node_attr, const void* h_in,
+                                 const void* saved, size_t saved_bytes, const float* grad_out,
+                                 float* grad_h, const dsmp_layer_grads* grads, int32_t flags,
+                                 void* ws, size_t ws_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DSMPNN_H */

@@ -1,0 +1,12 @@
+"""MI355X (gfx950) hot path of DS-MPNN (arXiv 2402.15106).
+
+Node sampling, radius-graph construction and the edge-conditioned
+message-passing layer (forward and backward) as hand-written HIP kernels
+behind a C ABI (include/dsmpnn.h); this package is the thin Python binding.
+"""
+
+from ._lib import (  # noqa: F401
+    Dsmp, DsmpError, Graph, LayerDesc, layer_desc, load_library, LIB_PATH, EXPORTED,
+    CAP_KNN, CAP_RANDOM, F32, BF16, ACT_IDENTITY, ACT_RELU, ATTR_CONCAT, ATTR_DIFF,
+    GRAD_ACCUMULATE, OK, INVALID_ARG, CAPACITY, HIP_ERROR, UNSUPPORTED, WORKSPACE_TOO_SMALL,
+)

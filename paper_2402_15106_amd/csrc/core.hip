@@ -1,0 +1,299 @@
+// Handle management, scan and fill utilities, node sampling and row gather.
+#include "common.hpp"
+
+#include <new>
+
+using namespace dsmp;
+
+// ------------------------------------------------------------------ scan
+
+namespace {
+
+__device__ __forceinline__ uint32_t block_exclusive_scan_1024(uint32_t v, uint32_t* sh,
+                                                             uint32_t* total) {
+  // 1024 threads = 16 waves; wave scans by shuffles, then a scan of wave sums.
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    uint32_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sh[wid] = x;
+  __syncthreads();
+  if (wid == 0) {
+    uint32_t s = lane < 16 ? sh[lane] : 0u;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      uint32_t y = __shfl_up(s, o, 64);
+      if (lane >= o) s += y;
+    }
+    if (lane < 16) sh[16 + lane] = s;
+  }
+  __syncthreads();
+  uint32_t wave_off = wid > 0 ? sh[16 + wid - 1] : 0u;
+  *total = sh[31];
+  uint32_t r = wave_off + x - v;
+  __syncthreads();
+  return r;
+}
+
+__global__ __launch_bounds__(1024) void k_scan_blocksums(const uint32_t* __restrict__ in,
+                                                         int64_t n, uint32_t* __restrict__ sums) {
+  __shared__ uint32_t sh[32];
+  int64_t i = (int64_t)blockIdx.x * SCAN_BLOCK + threadIdx.x;
+  uint32_t v = i < n ? in[i] : 0u;
+  uint32_t tot;
+  block_exclusive_scan_1024(v, sh, &tot);
+  if (threadIdx.x == 0) sums[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(1024) void k_scan_sums(uint32_t* __restrict__ sums, int nb) {
+  // exclusive scan of nb block sums in place, in chunks of 1024; sums[nb] = total
+  __shared__ uint32_t sh[32];
+  uint32_t carry = 0;
+  for (int base = 0; base < nb; base += SCAN_BLOCK) {
+    int i = base + threadIdx.x;
+    uint32_t v = i < nb ? sums[i] : 0u;
+    uint32_t tot;
+    uint32_t ex = block_exclusive_scan_1024(v, sh, &tot);
+    if (i < nb) sums[i] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) sums[nb] = carry;
+}
+
+__global__ __launch_bounds__(1024) void k_scan_final(const uint32_t* __restrict__ in, int64_t n,
+                                                     const uint32_t* __restrict__ sums,
+                                                     int32_t* __restrict__ out, int nb) {
+  __shared__ uint32_t sh[32];
+  int64_t i = (int64_t)blockIdx.x * SCAN_BLOCK + threadIdx.x;
+  uint32_t v = i < n ? in[i] : 0u;
+  uint32_t tot;
+  uint32_t ex = block_exclusive_scan_1024(v, sh, &tot);
+  if (i < n) out[i] = (int32_t)(sums[blockIdx.x] + ex);
+  if (blockIdx.x == 0 && threadIdx.x == 0) out[n] = (int32_t)sums[nb];
+}
+
+__global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (; i < n; i += stride) p[i] = v;
+}
+
+}  // namespace
+
+namespace dsmp {
+
+dsmp_status exclusive_scan_u32(dsmp_handle* h, const uint32_t* in, int32_t* out, int64_t n,
+                               uint32_t* tmp) {
+  int nb = (int)ceil_div(n, SCAN_BLOCK);
+  if (nb == 0) {
+    hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(1024), 0, h->stream, tmp, 0);
+    hipLaunchKernelGGL(k_scan_final, dim3(1), dim3(1024), 0, h->stream, in, (int64_t)0, tmp, out, 0);
+    DSMP_LAUNCHED(h, "scan");
+    return DSMP_OK;
+  }
+  hipLaunchKernelGGL(k_scan_blocksums, dim3(nb), dim3(1024), 0, h->stream, in, n, tmp);
+  hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(1024), 0, h->stream, tmp, nb);
+  hipLaunchKernelGGL(k_scan_final, dim3(nb), dim3(1024), 0, h->stream, in, n, tmp, out, nb);
+  DSMP_LAUNCHED(h, "scan");
+  return DSMP_OK;
+}
+
+dsmp_status fill_u32(dsmp_handle* h, uint32_t* p, int64_t n, uint32_t v) {
+  if (n <= 0) return DSMP_OK;
+  unsigned g = ceil_div(n, 256);
+  if (g > 4096) g = 4096;
+  hipLaunchKernelGGL(k_fill_u32, dim3(g), dim3(256), 0, h->stream, p, n, v);
+  DSMP_LAUNCHED(h, "fill");
+  return DSMP_OK;
+}
+
+}  // namespace dsmp
+
+// ------------------------------------------------------------------ handle
+
+extern "C" int dsmp_version(void) { return 10000; }
+
+extern "C" dsmp_status dsmp_create(dsmp_handle** out, int device) {
+  if (!out) return DSMP_INVALID_ARG;
+  *out = nullptr;
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || device < 0 || device >= n) return DSMP_INVALID_ARG;
+  if (hipSetDevice(device) != hipSuccess) return DSMP_HIP_ERROR;
+  dsmp_handle* h = new (std::nothrow) dsmp_handle();
+  if (!h) return DSMP_HIP_ERROR;
+  h->device = device;
+  *out = h;
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_destroy(dsmp_handle* h) {
+  delete h;
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_set_stream(dsmp_handle* h, void* stream) {
+  if (!h) return DSMP_INVALID_ARG;
+  h->stream = reinterpret_cast<hipStream_t>(stream);
+  return DSMP_OK;
+}
+
+extern "C" const char* dsmp_last_error(const dsmp_handle* h) { return h ? h->err.c_str() : ""; }
+
+// ------------------------------------------------------------------ sampling
+//
+// Selection of the s smallest SplitMix64 keys out of M by an 8-pass MSB-first
+// radix select over 8-bit digits (the keys are recomputed every pass), then a
+// stable compaction of the candidates whose key is <= the s-th smallest.
+
+namespace {
+
+struct SelState {
+  unsigned long long prefix;   // digits fixed so far
+  unsigned long long rank;     // 1-based rank of the wanted key among the unfixed ones
+};
+
+constexpr int SAMPLE_CHUNK = 1024;   // candidates per block in the compaction
+
+__global__ __launch_bounds__(256) void k_sel_hist(int64_t M, uint64_t seed, const SelState* st,
+                                                  int shift, uint32_t* __restrict__ hist) {
+  __shared__ uint32_t lh[256];
+  lh[threadIdx.x] = 0;
+  __syncthreads();
+  const uint64_t prefix = st->prefix;
+  const uint64_t himask = shift >= 56 ? 0ull : (~0ull << (shift + 8));
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (; i < M; i += stride) {
+    uint64_t k = splitmix64(seed, (uint64_t)i);
+    if ((k & himask) == (prefix & himask)) atomicAdd(&lh[(k >> shift) & 255u], 1u);
+  }
+  __syncthreads();
+  if (lh[threadIdx.x]) atomicAdd(&hist[threadIdx.x], lh[threadIdx.x]);
+}
+
+__global__ void k_sel_pick(SelState* st, int shift, uint32_t* __restrict__ hist) {
+  if (threadIdx.x != 0) return;
+  uint64_t r = st->rank, acc = 0;
+  int dsel = 255;
+  for (int d = 0; d < 256; ++d) {
+    if (acc + hist[d] >= r) { dsel = d; break; }
+    acc += hist[d];
+  }
+  st->rank = r - acc;
+  st->prefix |= (uint64_t)dsel << shift;
+  for (int d = 0; d < 256; ++d) hist[d] = 0;
+}
+
+__global__ void k_sel_init(SelState* st, uint64_t s, uint32_t* hist) {
+  if (threadIdx.x == 0) { st->prefix = 0; st->rank = s; }
+  hist[threadIdx.x] = 0;
+}
+
+__global__ __launch_bounds__(1024) void k_sel_count(int64_t M, uint64_t seed, const SelState* st,
+                                                    uint32_t* __restrict__ cnt) {
+  __shared__ uint32_t sh[32];
+  int64_t i = (int64_t)blockIdx.x * SAMPLE_CHUNK + threadIdx.x;
+  uint32_t f = (i < M && splitmix64(seed, (uint64_t)i) <= st->prefix) ? 1u : 0u;
+  uint32_t tot;
+  block_exclusive_scan_1024(f, sh, &tot);
+  if (threadIdx.x == 0) cnt[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(1024) void k_sel_write(int64_t M, uint64_t seed, const SelState* st,
+                                                    const uint32_t* __restrict__ off,
+                                                    int32_t* __restrict__ out) {
+  __shared__ uint32_t sh[32];
+  int64_t i = (int64_t)blockIdx.x * SAMPLE_CHUNK + threadIdx.x;
+  uint32_t f = (i < M && splitmix64(seed, (uint64_t)i) <= st->prefix) ? 1u : 0u;
+  uint32_t tot;
+  uint32_t ex = block_exclusive_scan_1024(f, sh, &tot);
+  if (f) out[off[blockIdx.x] + ex] = (int32_t)i;
+}
+
+__global__ void k_iota(int32_t* out, int64_t n) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) out[i] = (int32_t)i;
+}
+
+size_t sample_ws(int64_t M) {
+  size_t nb = ceil_div(M, SAMPLE_CHUNK);
+  return 256 + 1024 + 256 * (nb + 2) * 4 / 256 * 4 + (nb + 2) * 4 + 1024;
+}
+
+}  // namespace
+
+extern "C" dsmp_status dsmp_sample_workspace(int64_t M, size_t* bytes) {
+  if (!bytes || M < 0) return DSMP_INVALID_ARG;
+  *bytes = sample_ws(M);
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_sample_nodes(dsmp_handle* h, int64_t M, int64_t s, uint64_t seed,
+                                         int32_t* idx_out, void* ws, size_t ws_bytes) {
+  if (!h) return DSMP_INVALID_ARG;
+  DSMP_CHECK(h, M >= 0 && s >= 0 && s <= M, DSMP_INVALID_ARG, "need 0 <= s <= M (M=%lld s=%lld)",
+             (long long)M, (long long)s);
+  DSMP_CHECK(h, M <= INT32_MAX, DSMP_UNSUPPORTED, "M exceeds int32 range");
+  if (s == 0) return DSMP_OK;
+  DSMP_CHECK(h, idx_out != nullptr, DSMP_INVALID_ARG, "idx_out is NULL");
+  if (s == M) {
+    hipLaunchKernelGGL(k_iota, dim3(ceil_div(M, 256)), dim3(256), 0, h->stream, idx_out, M);
+    DSMP_LAUNCHED(h, "iota");
+    return DSMP_OK;
+  }
+  DSMP_CHECK(h, ws != nullptr && ws_bytes >= sample_ws(M), DSMP_WORKSPACE_TOO_SMALL,
+             "sampling workspace needs %zu bytes", sample_ws(M));
+  Carve c(ws);
+  SelState* st = c.take<SelState>(1);
+  uint32_t* hist = c.take<uint32_t>(256);
+  int nb = (int)ceil_div(M, SAMPLE_CHUNK);
+  uint32_t* cnt = c.take<uint32_t>(nb + 2);
+  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, h->stream, st, (uint64_t)s, hist);
+  unsigned g = ceil_div(M, 256);
+  if (g > 2048) g = 2048;
+  for (int shift = 56; shift >= 0; shift -= 8) {
+    hipLaunchKernelGGL(k_sel_hist, dim3(g), dim3(256), 0, h->stream, M, seed, st, shift, hist);
+    hipLaunchKernelGGL(k_sel_pick, dim3(1), dim3(64), 0, h->stream, st, shift, hist);
+  }
+  hipLaunchKernelGGL(k_sel_count, dim3(nb), dim3(1024), 0, h->stream, M, seed, st, cnt);
+  hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(1024), 0, h->stream, cnt, nb);
+  hipLaunchKernelGGL(k_sel_write, dim3(nb), dim3(1024), 0, h->stream, M, seed, st, cnt, idx_out);
+  DSMP_LAUNCHED(h, "sample");
+  return DSMP_OK;
+}
+
+// ------------------------------------------------------------------ gather
+
+namespace {
+__global__ void k_gather_rows(const uint32_t* __restrict__ src, int64_t n_src_rows, int64_t words,
+                              const int32_t* __restrict__ idx, int64_t n, uint32_t* __restrict__ dst) {
+  int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t total = n * words;
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (; t < total; t += stride) {
+    int64_t r = t / words, w = t - r * words;
+    int32_t s = idx[r];
+    dst[t] = (s >= 0 && s < n_src_rows) ? src[(int64_t)s * words + w] : 0u;
+  }
+}
+}  // namespace
+
+extern "C" dsmp_status dsmp_gather_rows(dsmp_handle* h, const void* src, int64_t n_src_rows,
+                                        int64_t row_bytes, const int32_t* idx, int64_t n, void* dst) {
+  if (!h) return DSMP_INVALID_ARG;
+  DSMP_CHECK(h, n >= 0 && n_src_rows >= 0 && row_bytes > 0 && row_bytes % 4 == 0, DSMP_INVALID_ARG,
+             "bad gather sizes");
+  if (n == 0) return DSMP_OK;
+  DSMP_CHECK(h, src && idx && dst, DSMP_INVALID_ARG, "gather pointer is NULL");
+  int64_t words = row_bytes / 4;
+  unsigned g = ceil_div(n * words, 256);
+  if (g > 8192) g = 8192;
+  hipLaunchKernelGGL(k_gather_rows, dim3(g), dim3(256), 0, h->stream,
+                     static_cast<const uint32_t*>(src), n_src_rows, words, idx, n,
+                     static_cast<uint32_t*>(dst));
+  DSMP_LAUNCHED(h, "gather_rows");
+  return DSMP_OK;
+}

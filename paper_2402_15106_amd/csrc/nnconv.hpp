@@ -1,0 +1,84 @@
+// NNConv layer internals: MFMA fragment traits, packed parameter layout and
+// the shapes each kernel instantiation is compiled for.
+#pragma once
+
+#include "common.hpp"
+
+namespace dsmp {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// One 32x32 output tile per MFMA chain.  Operand layouts (lane l, h = l/32):
+//   A[row = l%32][k = ks*KS + h*EPL + t]   B[k = ks*KS + h*EPL + t][col = l%32]
+//   D[row = 8*(i/4) + 4*h + (i%4)][col = l%32]  for accumulator register i.
+template <typename T>
+struct MT;
+
+template <>
+struct MT<__bf16> {
+  static constexpr int KS = 16, EPL = 8;
+  typedef bf16x8 frag;
+  static __device__ __forceinline__ f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <>
+struct MT<float> {
+  static constexpr int KS = 2, EPL = 1;
+  typedef float frag;
+  static __device__ __forceinline__ f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+};
+
+// A contraction index that comes out of a D tile (rows of the previous
+// product) is consumed as the B operand of the next product straight from
+// registers.  Register order n = 16*c + i of 32-row tile c maps to B element
+// (ks = n / EPL, t = n % EPL); the weights on the A side are stored with
+// their columns permuted to match:  packed column kk = ks*KS + h*EPL + t
+// holds original column  k = 32*c + 8*(i/4) + 4*h + (i%4).
+template <typename T>
+__host__ __device__ __forceinline__ int kperm(int kk) {
+  constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL;
+  int ks = kk / KS, rem = kk % KS, h = rem / EPL, t = rem % EPL;
+  int n = ks * EPL + t, c = n / 16, i = n % 16;
+  return 32 * c + 8 * (i / 4) + 4 * h + (i % 4);
+}
+
+// Byte offsets of the sections of a packed parameter buffer.
+struct PackLayout {
+  size_t w1l, b1l, w2p, b2, w3f, w3q, w3t, b3t, b3n, w2t, wr, br, total;
+};
+
+inline PackLayout pack_layout(int d, int h1, int h2, int esz) {
+  PackLayout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    off = (off + 255) & ~size_t(255);
+    size_t o = off;
+    off += bytes;
+    return o;
+  };
+  L.w1l = take((size_t)h1 * 8 * 4);           // fp32 [2][h1/2][8]
+  L.b1l = take((size_t)h1 * 4);               // fp32 [2][h1/2]
+  L.w2p = take((size_t)h2 * h1 * esz);        // T [h2][h1 permuted]
+  L.b2 = take((size_t)h2 * 4);                // fp32 [h2]
+  L.w3f = take((size_t)d * d * h2 * esz);     // T [p][q][h2 permuted]
+  L.w3q = take((size_t)d * d * h2 * esz);     // T [q][p][h2 permuted]
+  L.w3t = take((size_t)d * h2 * d * esz);     // T [p][k][q]
+  L.b3t = take((size_t)d * d * esz);          // T [q][p]
+  L.b3n = take((size_t)d * d * esz);          // T [p][q]
+  L.w2t = take((size_t)h1 * h2 * esz);        // T [j][h2 permuted]
+  L.wr = take((size_t)d * d * 4);             // fp32 [q][p] (rounded to the layer dtype)
+  L.br = take((size_t)d * 4);                 // fp32 [d]
+  L.total = (off + 255) & ~size_t(255);
+  return L;
+}
+
+// Edges per workgroup tile of the edge kernels (4 waves x 2 tiles x 32).
+constexpr int EDGE_TILE = 256;
+
+}  // namespace dsmp

@@ -1,0 +1,663 @@
+// NNConv layer forward (eq. (1), eq. (ii); Algorithm 1, graph-convolution step
+// with the residual hop update), parameter packing, and the edge contraction
+// that the backward pass reuses for the feature gradient.
+//
+// Edge contraction.  For edge e = (i <- j) the message is
+//     m_e[q] = sum_p h_j[p] * ( sum_k W3[p*d+q][k] z_e[k] + b3[p*d+q] ).
+// The d x d kernel matrix is never formed.  For each p the 32-row blocks of
+// W3[p*d + q][:] (rows q) are the A operand of a bf16 (or fp32) MFMA chain
+// over k, the edge tile's z vectors (held in registers for the whole loop)
+// are the B operand, and the 32x32 product is scaled by h_j[p] (one value per
+// lane: the lane's column is its edge) and accumulated.  The b3 term is one
+// more small MFMA product, B3^T h_j, that initialises the accumulators.  W3
+// is streamed through LDS in double-buffered chunks shared by the four waves
+// of a workgroup, and each A fragment feeds two edge tiles.
+//
+// Segmented mean without atomics: the edges of a workgroup tile are sorted by
+// destination, so the tile's messages go to LDS and one thread per
+// (destination, column) sums its run in edge order.  Destinations that start
+// or end outside the tile leave a partial sum (first and last run of every
+// tile); the node kernel adds those partials in tile order.
+#include "nnconv.hpp"
+
+#include <mutex>
+
+namespace dsmp {
+
+enum { MODE_FWD = 0, MODE_DH = 1 };
+
+struct EdgeArgs {
+  int64_t E, n_dst, n_src;
+  const int32_t* row_ptr;
+  const int32_t* col;
+  const int32_t* dst;
+  const int32_t* csc_ptr;
+  const int32_t* csc_eid;
+  const float* node_attr;
+  int dim, attr_mode;
+  const unsigned char* gath;     // FWD: h_in [n_src][d]; DH: g [n_dst][d]  (layer dtype)
+  const unsigned char* packed;
+  PackLayout L;
+  unsigned char* zE;             // [E][h2] layer dtype: FWD writes (if set), DH reads
+  unsigned char* z1E;            // [E][h1] layer dtype: FWD writes (if set)
+  float* out_direct;             // [segments][d]
+  float* out_part;               // [tiles][2][d]
+};
+
+dsmp_status launch_edge_contract(dsmp_handle* h, const dsmp_layer_desc& desc, int mode,
+                                 const EdgeArgs& a);
+
+}  // namespace dsmp
+
+using namespace dsmp;
+
+namespace {
+
+template <typename T>
+__device__ __forceinline__ void set_el(typename MT<T>::frag& f, int i, float v);
+template <>
+__device__ __forceinline__ void set_el<__bf16>(bf16x8& f, int i, float v) { f[i] = (__bf16)v; }
+template <>
+__device__ __forceinline__ void set_el<float>(float& f, int, float v) { f = v; }
+
+template <typename T>
+__device__ __forceinline__ typename MT<T>::frag ld_frag(const void* p) {
+  return *reinterpret_cast<const typename MT<T>::frag*>(p);
+}
+
+template <typename T>
+__device__ __forceinline__ typename MT<T>::frag zero_frag() {
+  typename MT<T>::frag f;
+  if constexpr (sizeof(f) == 4) f = 0.0f;
+  else for (int i = 0; i < 8; ++i) f[i] = (__bf16)0.0f;
+  return f;
+}
+
+__device__ __forceinline__ float to_f(__bf16 x) { return (float)x; }
+__device__ __forceinline__ float to_f(float x) { return x; }
+
+template <typename T, int DL, int H1, int H2>
+struct Shape {
+  static constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL, NT = 2, TILE = EDGE_TILE;
+  static constexpr int QT = DL / 32, KT = H2 / 32;
+  static constexpr int SK1 = H1 / KS, SK2 = H2 / KS, SKD = DL / KS;
+  static constexpr int ESZ = sizeof(T);
+  static constexpr int ROWB = H2 * ESZ + 16;
+  static constexpr int RCH = (DL * H2 * ESZ <= 32768) ? DL : (32768 / (H2 * ESZ));
+  static constexpr int CPP = DL / RCH, QPC = RCH / 32, NCH = DL * CPP;
+  static constexpr int STAGE = RCH * ROWB;
+  static constexpr int HROWB = DL * ESZ + 16;
+  static constexpr int MSGW = DL + 4;
+  static constexpr int U16 = RCH * H2 * ESZ / 16, UPT = (U16 + 255) / 256, ROW16 = H2 * ESZ / 16;
+  static constexpr int LDS_MAIN = 2 * STAGE + TILE * HROWB;
+  static constexpr int LDS_MSG = TILE * MSGW * 4;
+  static constexpr int LDS = LDS_MAIN > LDS_MSG ? LDS_MAIN : LDS_MSG;
+};
+
+// Edge attributes of edge (i <- j): concat [p_i, p_j, s_i, s_j] or diff v_i - v_j.
+__device__ __forceinline__ void edge_attr(const float* __restrict__ na, int dim, int mode, int i,
+                                          int j, float x[8]) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) x[c] = 0.0f;
+  const float* vi = na + (size_t)i * (dim + 1);
+  const float* vj = na + (size_t)j * (dim + 1);
+  if (dim == 2) {
+    if (mode == DSMP_ATTR_CONCAT) {
+      x[0] = vi[0]; x[1] = vi[1]; x[2] = vj[0]; x[3] = vj[1]; x[4] = vi[2]; x[5] = vj[2];
+    } else {
+      x[0] = vi[0] - vj[0]; x[1] = vi[1] - vj[1]; x[2] = vi[2] - vj[2];
+    }
+  } else {
+    if (mode == DSMP_ATTR_CONCAT) {
+      x[0] = vi[0]; x[1] = vi[1]; x[2] = vi[2]; x[3] = vj[0]; x[4] = vj[1]; x[5] = vj[2];
+      x[6] = vi[3]; x[7] = vj[3];
+    } else {
+      x[0] = vi[0] - vj[0]; x[1] = vi[1] - vj[1]; x[2] = vi[2] - vj[2]; x[3] = vi[3] - vj[3];
+    }
+  }
+}
+
+template <typename T, int DL, int H1, int H2, int MODE>
+__global__ __launch_bounds__(256, 1) void k_edge_contract(EdgeArgs a) {
+  using S = Shape<T, DL, H1, H2>;
+  using M = MT<T>;
+  using frag = typename M::frag;
+  constexpr int KS = S::KS, EPL = S::EPL, NT = S::NT, TILE = S::TILE, ESZ = S::ESZ;
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* stage0 = smem;
+  unsigned char* htile = smem + 2 * S::STAGE;
+  float* msg = reinterpret_cast<float*>(smem);
+
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int64_t tile = blockIdx.x, t0 = tile * TILE;
+  const int64_t tend = t0 + TILE < a.E ? t0 + TILE : a.E;
+  const unsigned char* P = a.packed;
+
+  int64_t eid[NT];
+  int dnode[NT], snode[NT], hrow[NT];
+  bool valid[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    hrow[t] = (wv * NT + t) * 32 + l32;
+    int64_t s = t0 + hrow[t];
+    valid[t] = s < a.E;
+    int64_t e = valid[t] ? (MODE == MODE_FWD ? s : (int64_t)a.csc_eid[s]) : 0;
+    eid[t] = e;
+    dnode[t] = valid[t] ? a.dst[e] : 0;
+    snode[t] = valid[t] ? a.col[e] : 0;
+  }
+
+  // rows gathered for this tile: h_j (forward) or g_i (feature gradient)
+  {
+    constexpr int HU = DL * ESZ / 16;
+    for (int u = tid; u < TILE * HU; u += 256) {
+      int r = u / HU, c = u % HU;
+      int64_t s = t0 + r;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (s < a.E) {
+        int64_t e = MODE == MODE_FWD ? s : (int64_t)a.csc_eid[s];
+        int node = MODE == MODE_FWD ? a.col[e] : a.dst[e];
+        v = reinterpret_cast<const uint4*>(a.gath + (size_t)node * DL * ESZ)[c];
+      }
+      *reinterpret_cast<uint4*>(htile + r * S::HROWB + c * 16) = v;
+    }
+  }
+
+  // B operand of the contraction: z_e, in the permuted register order
+  frag zB[NT][S::SK2];
+  if constexpr (MODE == MODE_FWD) {
+    frag z1B[NT][S::SK1];
+    const float* w1l = reinterpret_cast<const float*>(P + a.L.w1l) + hh * (H1 / 2) * 8;
+    const float* b1l = reinterpret_cast<const float*>(P + a.L.b1l) + hh * (H1 / 2);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      float x[8];
+      edge_attr(a.node_attr, a.dim, a.attr_mode, dnode[t], snode[t], x);
+#pragma unroll
+      for (int n = 0; n < H1 / 2; ++n) {
+        const f32x4 wa = *reinterpret_cast<const f32x4*>(w1l + n * 8);
+        const f32x4 wb = *reinterpret_cast<const f32x4*>(w1l + n * 8 + 4);
+        float v = b1l[n];
+        v += wa[0] * x[0]; v += wa[1] * x[1]; v += wa[2] * x[2]; v += wa[3] * x[3];
+        v += wb[0] * x[4]; v += wb[1] * x[5]; v += wb[2] * x[6]; v += wb[3] * x[7];
+        set_el<T>(z1B[t][n / EPL], n % EPL, v > 0.0f ? v : 0.0f);
+      }
+      if (a.z1E && valid[t]) {
+#pragma unroll
+        for (int s = 0; s < S::SK1; ++s)
+          *reinterpret_cast<frag*>(a.z1E + ((size_t)eid[t] * H1 + s * KS + hh * EPL) * ESZ) = z1B[t][s];
+      }
+    }
+    const unsigned char* w2p = P + a.L.w2p;
+    const float* b2 = reinterpret_cast<const float*>(P + a.L.b2);
+#pragma unroll
+    for (int kt = 0; kt < S::KT; ++kt) {
+      f32x16 C[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) C[t] = f32x16{};
+#pragma unroll
+      for (int s = 0; s < S::SK1; ++s) {
+        frag A = ld_frag<T>(w2p + ((size_t)(kt * 32 + l32) * H1 + s * KS + hh * EPL) * ESZ);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) C[t] = M::mma(A, z1B[t][s], C[t]);
+      }
+      float bb[16];
+#pragma unroll
+      for (int a4 = 0; a4 < 4; ++a4) {
+        f32x4 v = *reinterpret_cast<const f32x4*>(b2 + kt * 32 + 8 * a4 + 4 * hh);
+        bb[4 * a4] = v[0]; bb[4 * a4 + 1] = v[1]; bb[4 * a4 + 2] = v[2]; bb[4 * a4 + 3] = v[3];
+      }
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          float v = C[t][i] + bb[i];
+          const int n = 16 * kt + i;
+          set_el<T>(zB[t][n / EPL], n % EPL, v > 0.0f ? v : 0.0f);
+        }
+    }
+    if (a.zE) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        if (valid[t])
+#pragma unroll
+          for (int s = 0; s < S::SK2; ++s)
+            *reinterpret_cast<frag*>(a.zE + ((size_t)eid[t] * H2 + s * KS + hh * EPL) * ESZ) = zB[t][s];
+    }
+  } else {
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int s = 0; s < S::SK2; ++s)
+        zB[t][s] = valid[t] ? ld_frag<T>(a.zE + ((size_t)eid[t] * H2 + s * KS + hh * EPL) * ESZ)
+                            : zero_frag<T>();
+  }
+  __syncthreads();   // gathered rows are in LDS
+
+  // accumulators start at the bias term  B3^T u  (u = gathered row)
+  f32x16 acc[NT][S::QT];
+  {
+    const unsigned char* bop = P + (MODE == MODE_FWD ? a.L.b3t : a.L.b3n);
+#pragma unroll
+    for (int qt = 0; qt < S::QT; ++qt) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[t][qt] = f32x16{};
+#pragma unroll
+      for (int ps = 0; ps < S::SKD; ++ps) {
+        frag A = ld_frag<T>(bop + ((size_t)(qt * 32 + l32) * DL + ps * KS + hh * EPL) * ESZ);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          frag B = ld_frag<T>(htile + hrow[t] * S::HROWB + (ps * KS + hh * EPL) * ESZ);
+          acc[t][qt] = M::mma(A, B, acc[t][qt]);
+        }
+      }
+    }
+  }
+
+  // main loop over p: W3 rows (p*d + q), chunks of RCH rows, double-buffered
+  const unsigned char* A3 = P + (MODE == MODE_FWD ? a.L.w3f : a.L.w3q);
+  static_assert(S::U16 % 256 == 0, "stage chunk must split evenly over the workgroup");
+  uint4 pre[S::UPT];
+#define DSMP_GLOAD(c_)                                                                          \
+  do {                                                                                         \
+    const uint4* src_ = reinterpret_cast<const uint4*>(                                        \
+        A3 + ((size_t)((c_) / S::CPP) * DL + (size_t)((c_) % S::CPP) * S::RCH) * H2 * ESZ);   \
+    _Pragma("unroll") for (int u = 0; u < S::UPT; ++u) pre[u] = src_[tid + u * 256];           \
+  } while (0)
+#define DSMP_LSTORE(buf_)                                                                      \
+  do {                                                                                         \
+    _Pragma("unroll") for (int u = 0; u < S::UPT; ++u) {                                       \
+      const int idx = tid + u * 256;                                                           \
+      *reinterpret_cast<uint4*>(stage0 + (buf_) * S::STAGE + (idx / S::ROW16) * S::ROWB +      \
+                                (idx % S::ROW16) * 16) = pre[u];                               \
+    }                                                                                          \
+  } while (0)
+  DSMP_GLOAD(0);
+  DSMP_LSTORE(0);
+  __syncthreads();
+  for (int p = 0; p < DL; ++p) {
+    float sc[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      sc[t] = to_f(*reinterpret_cast<const T*>(htile + hrow[t] * S::HROWB + p * ESZ));
+#pragma unroll
+    for (int cc = 0; cc < S::CPP; ++cc) {
+      const int c = p * S::CPP + cc;
+      const int buf = c & 1;
+      const bool more = c + 1 < S::NCH;
+      if (more) DSMP_GLOAD(c + 1);
+      const unsigned char* sb = stage0 + buf * S::STAGE;
+#pragma unroll
+      for (int qq = 0; qq < S::QPC; ++qq) {
+        f32x16 C[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) C[t] = f32x16{};
+#pragma unroll
+        for (int s = 0; s < S::SK2; ++s) {
+          frag A = ld_frag<T>(sb + (qq * 32 + l32) * S::ROWB + (s * KS + hh * EPL) * ESZ);
+#pragma unroll
+          for (int t = 0; t < NT; ++t) C[t] = M::mma(A, zB[t][s], C[t]);
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[t][cc * S::QPC + qq] += sc[t] * C[t];
+      }
+      if (more) DSMP_LSTORE(buf ^ 1);
+      __syncthreads();
+    }
+  }
+#undef DSMP_GLOAD
+#undef DSMP_LSTORE
+
+  // messages to LDS, then per-destination (or per-source) runs
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int qt = 0; qt < S::QT; ++qt)
+#pragma unroll
+      for (int a4 = 0; a4 < 4; ++a4) {
+        f32x4 v = {acc[t][qt][4 * a4], acc[t][qt][4 * a4 + 1], acc[t][qt][4 * a4 + 2],
+                   acc[t][qt][4 * a4 + 3]};
+        *reinterpret_cast<f32x4*>(msg + hrow[t] * S::MSGW + qt * 32 + 8 * a4 + 4 * hh) = v;
+      }
+  __syncthreads();
+  const int32_t* ptr = MODE == MODE_FWD ? a.row_ptr : a.csc_ptr;
+  const int64_t i_first = MODE == MODE_FWD ? a.dst[t0] : a.col[a.csc_eid[t0]];
+  const int64_t i_last = MODE == MODE_FWD ? a.dst[tend - 1] : a.col[a.csc_eid[tend - 1]];
+  constexpr int G = 256 / DL;
+  const int q = tid % DL;
+  for (int64_t i = i_first + tid / DL; i <= i_last; i += G) {
+    const int64_t pa = ptr[i], pb = ptr[i + 1];
+    const int64_t lo = pa > t0 ? pa : t0, hi = pb < tend ? pb : tend;
+    if (lo >= hi) continue;
+    float s = 0.0f;
+    for (int64_t u = lo; u < hi; ++u) s += msg[(u - t0) * S::MSGW + q];
+    if (pa >= t0 && pb <= tend) a.out_direct[i * DL + q] = s;
+    else a.out_part[(tile * 2 + (pa < t0 ? 0 : 1)) * DL + q] = s;
+  }
+}
+
+// Sum of the run of segment i at column q from the tile sums the edge kernel
+// left: one direct value when the run sits in one tile, else the partials of
+// the tiles it crosses, in tile order.
+__device__ __forceinline__ float segment_sum(const int32_t* __restrict__ ptr, int64_t i, int q, int DL,
+                                             const float* __restrict__ direct,
+                                             const float* __restrict__ part) {
+  const int64_t pa = ptr[i], pb = ptr[i + 1];
+  if (pb <= pa) return 0.0f;
+  const int64_t ta = pa / EDGE_TILE, tb = (pb - 1) / EDGE_TILE;
+  if (ta == tb) return direct[i * DL + q];
+  float s = part[(ta * 2 + 1) * DL + q];
+  for (int64_t t = ta + 1; t < tb; ++t) s += part[(t * 2) * DL + q];
+  s += part[(tb * 2) * DL + q];
+  return s;
+}
+
+struct NodeArgs {
+  int64_t n_dst;
+  const int32_t* row_ptr;
+  const unsigned char* h_in;   // [n_src][d] layer dtype
+  const float* direct;
+  const float* part;
+  const float* wr;             // [d][d] fp32
+  const float* br;             // [d]
+  float* h_out;
+  unsigned char* h_out_lp;
+  float* y_saved;
+  int act, residual;
+};
+
+// y_i = mean_i + Wr h_i + br;  out_i = [h_i +] act(y_i)
+template <typename T, int DL>
+__global__ __launch_bounds__(256) void k_fwd_node(NodeArgs a) {
+  constexpr int NPB = 256 / DL;
+  __shared__ float wr[DL][DL + 1];
+  __shared__ float hs[NPB][DL];
+  for (int u = threadIdx.x; u < DL * DL; u += 256) wr[u / DL][u % DL] = a.wr[u];
+  const int li = threadIdx.x / DL, q = threadIdx.x % DL;
+  const T* hin = reinterpret_cast<const T*>(a.h_in);
+  for (int64_t base = (int64_t)blockIdx.x * NPB; base < a.n_dst; base += (int64_t)gridDim.x * NPB) {
+    const int64_t i = base + li;
+    const bool ok = i < a.n_dst;
+    __syncthreads();
+    hs[li][q] = ok ? to_f(hin[i * DL + q]) : 0.0f;
+    __syncthreads();
+    if (!ok) continue;
+    const int32_t deg = a.row_ptr[i + 1] - a.row_ptr[i];
+    float y = 0.0f;
+    if (deg > 0) y = segment_sum(a.row_ptr, i, q, DL, a.direct, a.part) / (float)deg;
+    float r = 0.0f;
+#pragma unroll 8
+    for (int p = 0; p < DL; ++p) r += wr[q][p] * hs[li][p];
+    y += r + a.br[q];
+    const float act = a.act == DSMP_ACT_RELU ? (y > 0.0f ? y : 0.0f) : y;
+    const float out = a.residual ? hs[li][q] + act : act;
+    a.h_out[i * DL + q] = out;
+    if (a.h_out_lp) reinterpret_cast<T*>(a.h_out_lp)[i * DL + q] = (T)out;
+    a.y_saved[i * DL + q] = y;
+  }
+}
+
+// ------------------------------------------------------------------ packing
+
+struct PackArgs {
+  const float *W1, *b1, *W2, *b2, *W3, *b3, *Wr, *br;
+  int d, h1, h2, de;
+  PackLayout L;
+  unsigned char* out;
+};
+
+template <typename T>
+__global__ void k_pack(PackArgs a) {
+  constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL;
+  const int d = a.d, h1 = a.h1, h2 = a.h2;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  float* w1l = reinterpret_cast<float*>(a.out + a.L.w1l);
+  float* b1l = reinterpret_cast<float*>(a.out + a.L.b1l);
+  for (int64_t x = t0; x < (int64_t)h1 * 8; x += stride) {
+    int c = x % 8, hn = x / 8, hh = hn / (h1 / 2), n = hn % (h1 / 2);
+    int j = kperm<T>((n / EPL) * KS + hh * EPL + n % EPL);
+    w1l[x] = c < a.de ? a.W1[j * a.de + c] : 0.0f;
+    if (c == 0) b1l[hn] = a.b1[j];
+  }
+  T* w2p = reinterpret_cast<T*>(a.out + a.L.w2p);
+  T* w2t = reinterpret_cast<T*>(a.out + a.L.w2t);
+  for (int64_t x = t0; x < (int64_t)h2 * h1; x += stride) {
+    int k = x / h1, kk = x % h1;
+    w2p[x] = (T)a.W2[k * h1 + kperm<T>(kk)];
+    int j = x / h2, kk2 = x % h2;
+    w2t[x] = (T)a.W2[kperm<T>(kk2) * h1 + j];
+  }
+  float* b2 = reinterpret_cast<float*>(a.out + a.L.b2);
+  for (int64_t x = t0; x < h2; x += stride) b2[x] = a.b2[x];
+  T* w3f = reinterpret_cast<T*>(a.out + a.L.w3f);
+  T* w3q = reinterpret_cast<T*>(a.out + a.L.w3q);
+  T* w3t = reinterpret_cast<T*>(a.out + a.L.w3t);
+  for (int64_t x = t0; x < (int64_t)d * d * h2; x += stride) {
+    int64_t r = x / h2;
+    int kk = x % h2;
+    int i0 = r / d, i1 = r % d;
+    // w3f[p=i0][q=i1][kk], w3q[q=i0][p=i1][kk]
+    w3f[x] = (T)a.W3[((int64_t)i0 * d + i1) * h2 + kperm<T>(kk)];
+    w3q[x] = (T)a.W3[((int64_t)i1 * d + i0) * h2 + kperm<T>(kk)];
+    // w3t[p][k][q]
+    int p = x / ((int64_t)h2 * d), rem = x % ((int64_t)h2 * d), k = rem / d, q = rem % d;
+    w3t[x] = (T)a.W3[((int64_t)p * d + q) * h2 + k];
+  }
+  T* b3t = reinterpret_cast<T*>(a.out + a.L.b3t);
+  T* b3n = reinterpret_cast<T*>(a.out + a.L.b3n);
+  float* wr = reinterpret_cast<float*>(a.out + a.L.wr);
+  for (int64_t x = t0; x < (int64_t)d * d; x += stride) {
+    int i0 = x / d, i1 = x % d;
+    b3t[x] = (T)a.b3[i1 * d + i0];
+    b3n[x] = (T)a.b3[x];
+    wr[x] = (float)(T)a.Wr[x];
+  }
+  float* br = reinterpret_cast<float*>(a.out + a.L.br);
+  for (int64_t x = t0; x < d; x += stride) br[x] = a.br[x];
+}
+
+template <typename K>
+dsmp_status set_lds(dsmp_handle* h, K kernel, int bytes) {
+  DSMP_HIP(h, hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, bytes));
+  return DSMP_OK;
+}
+
+template <typename T, int DL, int H1, int H2>
+dsmp_status launch_edge_shape(dsmp_handle* h, int mode, const EdgeArgs& a) {
+  using S = Shape<T, DL, H1, H2>;
+  const unsigned grid = ceil_div(mode == MODE_FWD ? a.E : a.E, S::TILE);
+  if (mode == MODE_FWD) {
+    auto kern = k_edge_contract<T, DL, H1, H2, MODE_FWD>;
+    dsmp_status st = set_lds(h, kern, S::LDS);
+    if (st != DSMP_OK) return st;
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), S::LDS, h->stream, a);
+  } else {
+    auto kern = k_edge_contract<T, DL, H1, H2, MODE_DH>;
+    dsmp_status st = set_lds(h, kern, S::LDS);
+    if (st != DSMP_OK) return st;
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), S::LDS, h->stream, a);
+  }
+  DSMP_LAUNCHED(h, "edge contraction");
+  return DSMP_OK;
+}
+
+}  // namespace
+
+namespace dsmp {
+
+bool shape_supported(const dsmp_layer_desc& d) {
+  if (d.dtype == DSMP_F32) return (d.d == 32 && d.h1 == 64 && d.h2 == 64) ||
+                                  (d.d == 64 && d.h1 == 128 && d.h2 == 128);
+  if (d.dtype == DSMP_BF16) return (d.d == 32 && d.h1 == 64 && d.h2 == 64) ||
+                                   (d.d == 64 && d.h1 == 128 && d.h2 == 128) ||
+                                   (d.d == 128 && d.h1 == 256 && d.h2 == 256);
+  return false;
+}
+
+dsmp_status launch_edge_contract(dsmp_handle* h, const dsmp_layer_desc& d, int mode,
+                                 const EdgeArgs& a) {
+  if (a.E == 0) return DSMP_OK;
+  if (d.dtype == DSMP_F32) {
+    if (d.d == 32) return launch_edge_shape<float, 32, 64, 64>(h, mode, a);
+    if (d.d == 64) return launch_edge_shape<float, 64, 128, 128>(h, mode, a);
+  } else {
+    if (d.d == 32) return launch_edge_shape<__bf16, 32, 64, 64>(h, mode, a);
+    if (d.d == 64) return launch_edge_shape<__bf16, 64, 128, 128>(h, mode, a);
+    if (d.d == 128) return launch_edge_shape<__bf16, 128, 256, 256>(h, mode, a);
+  }
+  return fail(h, DSMP_UNSUPPORTED, "unsupported layer shape");
+}
+
+}  // namespace dsmp
+
+// ------------------------------------------------------------------ C ABI
+
+namespace {
+
+int attr_width(const dsmp_layer_desc& d) {
+  return d.attr_mode == DSMP_ATTR_CONCAT ? 2 * d.dim + 2 : d.dim + 1;
+}
+
+dsmp_status check_desc(dsmp_handle* h, const dsmp_layer_desc* d) {
+  DSMP_CHECK(h, d != nullptr, DSMP_INVALID_ARG, "layer descriptor is NULL");
+  DSMP_CHECK(h, d->dim == 2 || d->dim == 3, DSMP_INVALID_ARG, "dim must be 2 or 3");
+  DSMP_CHECK(h, d->dtype == DSMP_F32 || d->dtype == DSMP_BF16, DSMP_INVALID_ARG, "unknown dtype");
+  DSMP_CHECK(h, d->act == DSMP_ACT_IDENTITY || d->act == DSMP_ACT_RELU, DSMP_INVALID_ARG,
+             "unknown activation");
+  DSMP_CHECK(h, d->attr_mode == DSMP_ATTR_CONCAT || d->attr_mode == DSMP_ATTR_DIFF, DSMP_INVALID_ARG,
+             "unknown edge attribute mode");
+  DSMP_CHECK(h, d->residual == 0 || d->residual == 1, DSMP_INVALID_ARG, "residual must be 0 or 1");
+  DSMP_CHECK(h, shape_supported(*d), DSMP_UNSUPPORTED,
+             "unsupported widths d=%d h1=%d h2=%d for this dtype", d->d, d->h1, d->h2);
+  return DSMP_OK;
+}
+
+}  // namespace
+
+namespace dsmp {
+
+dsmp_status check_layer_desc(dsmp_handle* h, const dsmp_layer_desc* d) { return check_desc(h, d); }
+int layer_attr_width(const dsmp_layer_desc& d) { return attr_width(d); }
+
+struct SavedLayout {
+  size_t y, zE, z1E, total;
+};
+
+SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E) {
+  Carve c(nullptr);
+  int esz = d.dtype == DSMP_BF16 ? 2 : 4;
+  SavedLayout s;
+  s.y = (size_t)c.take<float>((size_t)n_dst * d.d) ;
+  s.zE = (size_t)c.take<unsigned char>((size_t)E * d.h2 * esz);
+  s.z1E = (size_t)c.take<unsigned char>((size_t)E * d.h1 * esz);
+  s.total = c.used();
+  return s;
+}
+
+size_t fwd_ws_bytes(const dsmp_layer_desc& d, int64_t n_dst, int64_t E) {
+  Carve c(nullptr);
+  c.take<float>((size_t)n_dst * d.d);
+  c.take<float>((size_t)(ceil_div(E, EDGE_TILE) + 1) * 2 * d.d);
+  return c.used();
+}
+
+dsmp_status check_graph(dsmp_handle* h, const dsmp_graph* g, bool need_csc) {
+  DSMP_CHECK(h, g != nullptr, DSMP_INVALID_ARG, "graph is NULL");
+  DSMP_CHECK(h, g->n_dst >= 0 && g->n_src >= g->n_dst && g->n_edges >= 0, DSMP_INVALID_ARG,
+             "bad graph sizes");
+  DSMP_CHECK(h, g->n_edges <= INT32_MAX && g->n_src <= INT32_MAX, DSMP_UNSUPPORTED,
+             "graph too large for int32 indices");
+  DSMP_CHECK(h, g->row_ptr != nullptr, DSMP_INVALID_ARG, "row_ptr is NULL");
+  DSMP_CHECK(h, g->n_edges == 0 || (g->col && g->dst), DSMP_INVALID_ARG, "col or dst is NULL");
+  if (need_csc)
+    DSMP_CHECK(h, g->csc_ptr && (g->n_edges == 0 || g->csc_eid), DSMP_INVALID_ARG,
+               "csc arrays are NULL");
+  return DSMP_OK;
+}
+
+}  // namespace dsmp
+
+extern "C" dsmp_status dsmp_nnconv_packed_bytes(const dsmp_layer_desc* desc, size_t* bytes) {
+  if (!desc || !bytes) return DSMP_INVALID_ARG;
+  dsmp_status st = check_desc(nullptr, desc);
+  if (st != DSMP_OK) return st;
+  *bytes = pack_layout(desc->d, desc->h1, desc->h2, desc->dtype == DSMP_BF16 ? 2 : 4).total;
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_nnconv_pack(dsmp_handle* h, const dsmp_layer_desc* desc,
+                                        const dsmp_layer_params* p, void* packed) {
+  if (!h) return DSMP_INVALID_ARG;
+  dsmp_status st = check_desc(h, desc);
+  if (st != DSMP_OK) return st;
+  DSMP_CHECK(h, p && p->W1 && p->b1 && p->W2 && p->b2 && p->W3 && p->b3 && p->Wr && p->br && packed,
+             DSMP_INVALID_ARG, "a parameter pointer is NULL");
+  DSMP_CHECK(h, (reinterpret_cast<uintptr_t>(packed) & 255) == 0, DSMP_INVALID_ARG,
+             "packed buffer must be 256-byte aligned");
+  PackArgs a{p->W1, p->b1, p->W2, p->b2, p->W3, p->b3, p->Wr, p->br,
+             desc->d, desc->h1, desc->h2, attr_width(*desc),
+             pack_layout(desc->d, desc->h1, desc->h2, desc->dtype == DSMP_BF16 ? 2 : 4),
+             static_cast<unsigned char*>(packed)};
+  if (desc->dtype == DSMP_BF16)
+    hipLaunchKernelGGL(k_pack<__bf16>, dim3(1024), dim3(256), 0, h->stream, a);
+  else
+    hipLaunchKernelGGL(k_pack<float>, dim3(1024), dim3(256), 0, h->stream, a);
+  DSMP_LAUNCHED(h, "pack");
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_nnconv_forward(dsmp_handle* h, const dsmp_layer_desc* desc,
+                                           const void* packed, const dsmp_graph* g,
+                                           const float* node_attr, const void* h_in, float* h_out,
+                                           void* h_out_lp, void* saved, size_t saved_bytes, void* ws,
+                                           size_t ws_bytes) {
+  if (!h) return DSMP_INVALID_ARG;
+  dsmp_status st = check_desc(h, desc);
+  if (st != DSMP_OK) return st;
+  if ((st = check_graph(h, g, false)) != DSMP_OK) return st;
+  const dsmp_layer_desc& d = *desc;
+  DSMP_CHECK(h, packed && (g->n_src == 0 || (node_attr && h_in)) && (g->n_dst == 0 || h_out),
+             DSMP_INVALID_ARG, "a forward pointer is NULL");
+  SavedLayout sl = saved_layout(d, g->n_dst, g->n_edges);
+  size_t need_ws = fwd_ws_bytes(d, g->n_dst, g->n_edges);
+  DSMP_CHECK(h, saved && saved_bytes >= sl.total, DSMP_WORKSPACE_TOO_SMALL,
+             "saved buffer needs %zu bytes", sl.total);
+  DSMP_CHECK(h, ws && ws_bytes >= need_ws, DSMP_WORKSPACE_TOO_SMALL, "forward workspace needs %zu bytes",
+             need_ws);
+  const int esz = d.dtype == DSMP_BF16 ? 2 : 4;
+  PackLayout L = pack_layout(d.d, d.h1, d.h2, esz);
+  unsigned char* sv = static_cast<unsigned char*>(saved);
+  Carve c(ws);
+  float* direct = c.take<float>((size_t)g->n_dst * d.d);
+  float* part = c.take<float>((size_t)(ceil_div(g->n_edges, EDGE_TILE) + 1) * 2 * d.d);
+  EdgeArgs ea{};
+  ea.E = g->n_edges; ea.n_dst = g->n_dst; ea.n_src = g->n_src;
+  ea.row_ptr = g->row_ptr; ea.col = g->col; ea.dst = g->dst;
+  ea.node_attr = node_attr; ea.dim = d.dim; ea.attr_mode = d.attr_mode;
+  ea.gath = static_cast<const unsigned char*>(h_in);
+  ea.packed = static_cast<const unsigned char*>(packed); ea.L = L;
+  ea.zE = sv + sl.zE; ea.z1E = sv + sl.z1E;
+  ea.out_direct = direct; ea.out_part = part;
+  if ((st = launch_edge_contract(h, d, MODE_FWD, ea)) != DSMP_OK) return st;
+  if (g->n_dst > 0) {
+    NodeArgs na{g->n_dst, g->row_ptr, static_cast<const unsigned char*>(h_in), direct, part,
+                reinterpret_cast<const float*>(ea.packed + L.wr),
+                reinterpret_cast<const float*>(ea.packed + L.br), h_out,
+                static_cast<unsigned char*>(h_out_lp), reinterpret_cast<float*>(sv + sl.y), d.act,
+                d.residual};
+    unsigned grid = ceil_div(g->n_dst, 256 / d.d);
+    if (grid > 2048) grid = 2048;
+    if (d.dtype == DSMP_BF16) {
+      if (d.d == 32) hipLaunchKernelGGL((k_fwd_node<__bf16, 32>), dim3(grid), dim3(256), 0, h->stream, na);
+      if (d.d == 64) hipLaunchKernelGGL((k_fwd_node<__bf16, 64>), dim3(grid), dim3(256), 0, h->stream, na);
+      if (d.d == 128) hipLaunchKernelGGL((k_fwd_node<__bf16, 128>), dim3(grid), dim3(256), 0, h->stream, na);
+    } else {
+      if (d.d == 32) hipLaunchKernelGGL((k_fwd_node<float, 32>), dim3(grid), dim3(256), 0, h->stream, na);
+      if (d.d == 64) hipLaunchKernelGGL((k_fwd_node<float, 64>), dim3(grid), dim3(256), 0, h->stream, na);
+    }
+    DSMP_LAUNCHED(h, "forward node update");
+  }
+  return DSMP_OK;
+}

@@ -1,0 +1,174 @@
+"""GPU parity: the NNConv layer (forward and backward) against the fp64 oracle.
+
+The graph comes from the oracle and is uploaded, so these tests do not depend
+on the GPU graph builder.  Tolerance: max |gpu - oracle| / max |oracle| per
+tensor, 1e-4 for float32 layers and 2e-2 for bf16-operand layers.
+"""
+
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import nnconv as onn
+from oracle import radius_graph as org
+from tests.helpers import TOL, announce, gpu_lib, rel_err
+from workloads import bf16_round, layer_params, make_config
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = {"f32_32": ("f32", 32, 64, 64), "f32_64": ("f32", 64, 128, 128), "bf16_32": ("bf16", 32, 64, 64),
+          "bf16_64": ("bf16", 64, 128, 128), "bf16_128": ("bf16", 128, 256, 256)}
+
+
+@pytest.fixture(scope="module")
+def env():
+    return gpu_lib()
+
+
+class Case:
+    """A layer problem on the host plus its device copies."""
+
+    def __init__(self, env, pos, attr, h, n_dst, r, cap, P, dtype, D, d, h1, h2, act=0, residual=1,
+                 attr_mode=0, G=None, rows=None):
+        dm, lib, torch = env
+        self.dm, self.lib, self.torch = dm, lib, torch
+        dev = torch.device("cuda", 0)
+        self.rp, self.col = org.radius_graph(pos, n_dst, r, cap)
+        rp, col = self.rp, self.col
+        E = col.size
+        cp, ceid = org.transpose(rp, col, pos.shape[0])
+        i32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+        pad = lambda a: np.concatenate([a, np.zeros(1, np.int32)]) if a.size == 0 else a
+        self.g = dm.Graph(n_dst, pos.shape[0], E, i32(rp), i32(pad(col)), i32(pad(org.dst_of_edges(rp))),
+                          i32(cp), i32(pad(ceid)))
+        self.P, self.h, self.attr, self.n_dst = P, h, attr, n_dst
+        self.act, self.residual, self.attr_mode = act, residual, attr_mode
+        self.dtype = dtype
+        tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+        self.desc = dm.layer_desc(D, d, h1, h2, dm.BF16 if dtype == "bf16" else dm.F32, act, residual, attr_mode)
+        self.t_attr = torch.from_numpy(attr).to(dev)
+        self.t_h = torch.from_numpy(h).to(dev).to(tdt)
+        self.packed = lib.dsmp_nnconv_pack(self.desc, {k: torch.from_numpy(v) for k, v in P.items()})
+        self.x = onn.edge_attr(attr, rp, col, "concat" if attr_mode == 0 else "diff")
+        self.G = G
+        self.rows = rows
+
+    def forward(self):
+        out, saved = self.lib.dsmp_nnconv_forward(self.desc, self.packed, self.g, self.t_attr, self.t_h)
+        self.torch.cuda.synchronize()
+        self.saved = saved
+        return out.cpu().numpy()
+
+    def oracle_forward(self):
+        out, _ = onn.forward(self.P, self.x, self.h.astype(np.float64), self.rp, self.col, self.n_dst,
+                             self.act, bool(self.residual), rows=self.rows)
+        return out
+
+    def backward(self):
+        dev = self.torch.device("cuda", 0)
+        gh, grads = self.lib.dsmp_nnconv_backward(self.desc, self.packed, self.g, self.t_attr, self.t_h,
+                                                  self.saved, self.torch.from_numpy(self.G).to(dev))
+        self.torch.cuda.synchronize()
+        return gh.cpu().numpy(), {k: v.cpu().numpy() for k, v in grads.items()}
+
+    def oracle_backward(self):
+        return onn.backward(self.P, self.x, self.h.astype(np.float64), self.rp, self.col, self.n_dst, self.G,
+                            self.act, bool(self.residual), rows=self.rows)
+
+
+def random_case(env, shape, n=900, n_dst=None, D=2, r=None, cap=0, act=0, residual=1, attr_mode=0, seed=0):
+    dtype, d, h1, h2 = SHAPES[shape]
+    g = np.random.default_rng(seed)
+    n_dst = n if n_dst is None else n_dst
+    pos = g.uniform(0, 1, (n, D)).astype(np.float32)
+    attr = np.concatenate([pos, g.uniform(0, 2, (n, 1)).astype(np.float32)], 1)
+    if r is None:
+        r = (30.0 / n / (np.pi if D == 2 else 4.19)) ** (1.0 / D)   # ~30 neighbours
+    h = g.normal(0, 1, (n, d)).astype(np.float32)
+    if dtype == "bf16":
+        h = bf16_round(h)
+    de = 2 * D + 2 if attr_mode == 0 else D + 1
+    P = layer_params(g, d, de, h1, h2, dtype)
+    G = g.normal(0, 1, (n_dst, d)).astype(np.float32)
+    return Case(env, pos, attr, h, n_dst, r, cap, P, dtype, D, d, h1, h2, act, residual, attr_mode, G)
+
+
+FWD_CASES = {
+    "f32_32_2d": dict(shape="f32_32"),
+    "f32_64_3d": dict(shape="f32_64", D=3),
+    "bf16_32_2d": dict(shape="bf16_32"),
+    "bf16_64_2d": dict(shape="bf16_64"),
+    "bf16_64_3d_knn": dict(shape="bf16_64", D=3, cap=12),
+    "bf16_128_3d": dict(shape="bf16_128", D=3, cap=24, n=700),
+    "bf16_64_relu_nores": dict(shape="bf16_64", act=1, residual=0),
+    "bf16_64_diff_attr": dict(shape="bf16_64", attr_mode=1),
+    "f32_32_halo": dict(shape="f32_32", n=1000, n_dst=700),
+    "bf16_64_one_tile_ragged": dict(shape="bf16_64", n=37, r=0.3),
+    "bf16_64_isolated": dict(shape="bf16_64", n=400, r=0.02),
+    "bf16_64_high_degree": dict(shape="bf16_64", n=600, r=0.5),
+}
+
+
+@pytest.mark.parametrize("name", sorted(FWD_CASES))
+def test_forward_parity(env, name):
+    kw = FWD_CASES[name]
+    announce("forward", name)
+    c = random_case(env, seed=zlib.crc32(name.encode()) % 1000, **kw)
+    got = c.forward()
+    ref = c.oracle_forward()
+    err = rel_err(got, ref)
+    print("E=%d err=%.3e" % (c.col.size, err))
+    assert err <= TOL[c.dtype], err
+
+
+def test_forward_no_edges(env):
+    announce("forward no edges")
+    c = random_case(env, "bf16_64", n=50, r=1e-6)
+    assert c.col.size == 0
+    assert rel_err(c.forward(), c.oracle_forward()) <= TOL["bf16"]
+
+
+def test_forward_deterministic(env):
+    c = random_case(env, "bf16_64", n=3000, seed=5)
+    a = c.forward()
+    b = c.forward()
+    assert np.array_equal(a, b)
+
+
+def workload_case(env, k, layer=0, rows=None):
+    w = make_config(k)
+    pos, attr, h = [], [], []
+    for p in w.parts:
+        idx = oracle.sampling.sample_nodes(p.pos.shape[0], p.s, p.seed)
+        pos.append(p.pos[idx]); attr.append(p.attr[idx]); h.append(p.h[idx])
+    pos, attr, h = np.concatenate(pos), np.concatenate(attr), np.concatenate(h)
+    G = np.zeros_like(w.grad_out)
+    if rows is None:
+        G = w.grad_out
+    else:
+        G[rows] = w.grad_out[rows]
+    return Case(env, pos, attr, h, w.n_dst, w.r, w.cap, w.params[layer], w.dtype, w.D, w.d, w.H1, w.H2,
+                G=G, rows=rows)
+
+
+@pytest.mark.parametrize("k", [1, 2])
+def test_forward_workload_full(env, k):
+    announce("forward workload", k)
+    c = workload_case(env, k)
+    err = rel_err(c.forward(), c.oracle_forward())
+    print("E=%d err=%.3e" % (c.col.size, err))
+    assert err <= TOL[c.dtype]
+
+
+@pytest.mark.parametrize("k", [3, 4, 5])
+def test_forward_workload_rows(env, k):
+    announce("forward workload rows", k)
+    rows = np.sort(np.random.default_rng(k).choice(make_config(k).n_dst, 256, replace=False))
+    c = workload_case(env, k, rows=rows)
+    got = c.forward()
+    ref = c.oracle_forward()
+    err = rel_err(got[rows], ref[rows])
+    print("E=%d err=%.3e" % (c.col.size, err))
+    assert err <= TOL[c.dtype]

@@ -79,8 +79,9 @@ def _uniform(rng, shape, fan_in):
 def layer_params(rng, d, de, H1, H2, dtype):
     """One layer's parameters, U(+-1/sqrt(fan_in)), torch Linear layout [out, in].
 
-    For bf16 cases the operands the GPU feeds to bf16 matrix cores (W2, W3,
-    Wr) are rounded to bfloat16 here, so both sides use identical values.
+    For bf16 cases the operands the GPU feeds to bf16 matrix cores (W2, the
+    last-layer matrix W3 with its bias column b3, and Wr) are rounded to
+    bfloat16 here, so both sides use identical values.
     """
     P = {
         "W1": _uniform(rng, (H1, de), de), "b1": _uniform(rng, (H1,), de),
@@ -90,7 +91,7 @@ def layer_params(rng, d, de, H1, H2, dtype):
     }
     P = {k: v.astype(np.float32) for k, v in P.items()}
     if dtype == "bf16":
-        for k in ("W2", "W3", "Wr"):
+        for k in ("W2", "W3", "b3", "Wr"):
             P[k] = bf16_round(P[k])
     return P
 
