@@ -81,4 +81,40 @@ inline PackLayout pack_layout(int d, int h1, int h2, int esz) {
 // Edges per workgroup tile of the edge kernels (4 waves x 2 tiles x 32).
 constexpr int EDGE_TILE = 256;
 
+enum { MODE_FWD = 0, MODE_DH = 1 };
+
+// Arguments of the edge contraction (forward messages, or the feature
+// gradient when run over the edges in source order).
+struct EdgeArgs {
+  int64_t E, n_dst, n_src;
+  const int32_t* row_ptr;
+  const int32_t* col;
+  const int32_t* dst;
+  const int32_t* csc_ptr;
+  const int32_t* csc_eid;
+  const float* node_attr;
+  int dim, attr_mode;
+  const unsigned char* gath;     // FWD: h_in [n_src][d]; DH: g [n_dst][d]  (layer dtype)
+  const unsigned char* packed;
+  PackLayout L;
+  unsigned char* zE;             // [E][h2] layer dtype: FWD writes (if set), DH reads
+  unsigned char* z1E;            // [E][h1] layer dtype: FWD writes (if set)
+  float* out_direct;             // [segments][d]
+  float* out_part;               // [tiles][2][d]
+};
+
+dsmp_status launch_edge_contract(dsmp_handle* h, const dsmp_layer_desc& desc, int mode,
+                                 const EdgeArgs& a);
+
+// Per-layer buffer the forward fills for the backward: y [n_dst][d] fp32,
+// z [E][h2] and z1 [E][h1] in the layer dtype and the permuted order.
+struct SavedLayout {
+  size_t y, zE, z1E, total;
+};
+SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E);
+size_t fwd_ws_bytes(const dsmp_layer_desc& d, int64_t n_dst, int64_t E);
+dsmp_status check_layer_desc(dsmp_handle* h, const dsmp_layer_desc* d);
+dsmp_status check_graph(dsmp_handle* h, const dsmp_graph* g, bool need_csc);
+int layer_attr_width(const dsmp_layer_desc& d);
+
 }  // namespace dsmp

@@ -1,28 +1,912 @@
-// NNConv layer backward (placeholder until the backward kernels land).
+// NNConv layer backward: gradients of the forward in nnconv_fwd.hip with
+// respect to the input features and every parameter (the backpropagation step
+// of Algorithm 1 for one graph-convolution hop).
+//
+// With ybar = G * act'(y) and the per-edge message gradient g_e = ybar_i/deg_i
+// (i the destination of e):
+//   dWr = sum_i ybar_i h_i^T,  dbr = sum_i ybar_i,  dh_i += [G_i] + Wr^T ybar_i
+//   dh_j += sum_{e: j->i} Theta_e g_e        (edge contraction in source order)
+//   dz_e[k] = sum_p h_j[p] sum_q W3[p*d+q][k] g_e[q]   (MFMA, scaled by h_j[p])
+//   dW3[p*d+q][k] = sum_e h_j[p] g_e[q] z_e[k],  db3[p*d+q] = sum_e h_j[p] g_e[q]
+//   da2 = dz * [z > 0]:  dW2 = sum_e da2 z1^T, db2 = sum_e da2, dz1 = W2^T da2
+//   da1 = dz1 * [z1 > 0]: dW1 = sum_e da1 x_e^T, db1 = sum_e da1
+// Every sum over edges or nodes is split into fixed chunks whose partial sums
+// are added in chunk order: no atomics, bitwise-reproducible results.
 #include "nnconv.hpp"
 
-namespace dsmp {
-struct SavedLayout { size_t y, zE, z1E, total; };
-SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E);
-size_t fwd_ws_bytes(const dsmp_layer_desc& d, int64_t n_dst, int64_t E);
-dsmp_status check_layer_desc(dsmp_handle* h, const dsmp_layer_desc* d);
-}
 using namespace dsmp;
+
+namespace {
+
+template <typename T>
+__device__ __forceinline__ void set_el(typename MT<T>::frag& f, int i, float v);
+template <>
+__device__ __forceinline__ void set_el<__bf16>(bf16x8& f, int i, float v) { f[i] = (__bf16)v; }
+template <>
+__device__ __forceinline__ void set_el<float>(float& f, int, float v) { f = v; }
+
+template <typename T>
+__device__ __forceinline__ float get_el(const typename MT<T>::frag& f, int i);
+template <>
+__device__ __forceinline__ float get_el<__bf16>(const bf16x8& f, int i) { return (float)f[i]; }
+template <>
+__device__ __forceinline__ float get_el<float>(const float& f, int) { return f; }
+
+template <typename T>
+__device__ __forceinline__ typename MT<T>::frag ld_frag(const void* p) {
+  return *reinterpret_cast<const typename MT<T>::frag*>(p);
+}
+
+__device__ __forceinline__ float to_f(__bf16 x) { return (float)x; }
+__device__ __forceinline__ float to_f(float x) { return x; }
+
+__device__ __forceinline__ void edge_attr(const float* __restrict__ na, int dim, int mode, int i, int j,
+                                          float x[8]) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) x[c] = 0.0f;
+  const float* vi = na + (size_t)i * (dim + 1);
+  const float* vj = na + (size_t)j * (dim + 1);
+  if (dim == 2) {
+    if (mode == DSMP_ATTR_CONCAT) {
+      x[0] = vi[0]; x[1] = vi[1]; x[2] = vj[0]; x[3] = vj[1]; x[4] = vi[2]; x[5] = vj[2];
+    } else {
+      x[0] = vi[0] - vj[0]; x[1] = vi[1] - vj[1]; x[2] = vi[2] - vj[2];
+    }
+  } else {
+    if (mode == DSMP_ATTR_CONCAT) {
+      x[0] = vi[0]; x[1] = vi[1]; x[2] = vi[2]; x[3] = vj[0]; x[4] = vj[1]; x[5] = vj[2];
+      x[6] = vi[3]; x[7] = vj[3];
+    } else {
+      x[0] = vi[0] - vj[0]; x[1] = vi[1] - vj[1]; x[2] = vi[2] - vj[2]; x[3] = vi[3] - vj[3];
+    }
+  }
+}
+
+// ------------------------------------------------------------ node pre-pass
+
+struct BNodeArgs {
+  int64_t n_dst;
+  const int32_t* row_ptr;
+  const float* G;
+  const float* y;
+  const float* wr;       // [q][p]
+  float* ybar;
+  unsigned char* gT;     // [n_dst][d] layer dtype
+  float* gF;             // [n_dst][d]
+  float* dh_node;
+  int act, residual;
+};
+
+template <typename T, int DL>
+__global__ __launch_bounds__(256) void k_bwd_node(BNodeArgs a) {
+  constexpr int NPB = 256 / DL;
+  __shared__ float wr[DL][DL + 1];
+  __shared__ float yb[NPB][DL];
+  for (int u = threadIdx.x; u < DL * DL; u += 256) wr[u / DL][u % DL] = a.wr[u];
+  const int li = threadIdx.x / DL, c = threadIdx.x % DL;
+  for (int64_t base = (int64_t)blockIdx.x * NPB; base < a.n_dst; base += (int64_t)gridDim.x * NPB) {
+    const int64_t i = base + li;
+    const bool ok = i < a.n_dst;
+    float g = 0.0f, v = 0.0f;
+    if (ok) {
+      g = a.G[i * DL + c];
+      v = a.act == DSMP_ACT_RELU ? (a.y[i * DL + c] > 0.0f ? g : 0.0f) : g;
+    }
+    __syncthreads();
+    yb[li][c] = v;
+    __syncthreads();
+    if (!ok) continue;
+    const int32_t deg = a.row_ptr[i + 1] - a.row_ptr[i];
+    const float gm = deg > 0 ? v / (float)deg : 0.0f;
+    a.ybar[i * DL + c] = v;
+    a.gF[i * DL + c] = gm;
+    reinterpret_cast<T*>(a.gT)[i * DL + c] = (T)gm;
+    float s = a.residual ? g : 0.0f;
+#pragma unroll 8
+    for (int q = 0; q < DL; ++q) s += wr[q][c] * yb[li][q];
+    a.dh_node[i * DL + c] = s;
+  }
+}
+
+// dWr = sum_i ybar_i h_i^T, dbr = sum_i ybar_i over a chunk of nodes.
+template <typename T, int DL>
+__global__ __launch_bounds__(256) void k_bwd_root(int64_t n_dst, int64_t per_block, const float* __restrict__ ybar,
+                                                  const unsigned char* __restrict__ h_in,
+                                                  float* __restrict__ part) {
+  constexpr int PP = DL * DL / 256, NB = 32;
+  __shared__ float ys[NB][DL];
+  __shared__ float hs[NB][DL];
+  const int q = threadIdx.x % DL, p0 = (threadIdx.x / DL) * PP;
+  const T* hin = reinterpret_cast<const T*>(h_in);
+  float acc[PP];
+#pragma unroll
+  for (int u = 0; u < PP; ++u) acc[u] = 0.0f;
+  float accb = 0.0f;
+  const int64_t i0 = (int64_t)blockIdx.x * per_block;
+  const int64_t i1 = i0 + per_block < n_dst ? i0 + per_block : n_dst;
+  for (int64_t b = i0; b < i1; b += NB) {
+    __syncthreads();
+    for (int u = threadIdx.x; u < NB * DL; u += 256) {
+      int64_t i = b + u / DL;
+      bool ok = i < i1;
+      ys[u / DL][u % DL] = ok ? ybar[i * DL + u % DL] : 0.0f;
+      hs[u / DL][u % DL] = ok ? to_f(hin[i * DL + u % DL]) : 0.0f;
+    }
+    __syncthreads();
+    for (int n = 0; n < NB; ++n) {
+      const float yv = ys[n][q];
+#pragma unroll
+      for (int u = 0; u < PP; ++u) acc[u] += yv * hs[n][p0 + u];
+      accb += yv;
+    }
+  }
+  float* out = part + (size_t)blockIdx.x * (DL * DL + DL);
+#pragma unroll
+  for (int u = 0; u < PP; ++u) out[q * DL + p0 + u] = acc[u];
+  if (threadIdx.x < DL) out[DL * DL + q] = accb;
+}
+
+// db3[p*d+q] = sum_i (sum_{e in E_i} h_{src(e)}[p]) g_i[q] over a chunk of destinations.
+template <typename T, int DL>
+__global__ __launch_bounds__(256) void k_bwd_db3(int64_t n_dst, int64_t per_block, const int32_t* __restrict__ row_ptr,
+                                                 const int32_t* __restrict__ col, const unsigned char* __restrict__ h_in,
+                                                 const float* __restrict__ gF, float* __restrict__ part) {
+  constexpr int PP = DL * DL / 256, NB = 16;
+  __shared__ float hsum[NB][DL];
+  __shared__ float gs[NB][DL];
+  const T* hin = reinterpret_cast<const T*>(h_in);
+  const int p = threadIdx.x % DL, q0 = (threadIdx.x / DL) * PP;
+  float acc[PP];
+#pragma unroll
+  for (int u = 0; u < PP; ++u) acc[u] = 0.0f;
+  const int64_t i0 = (int64_t)blockIdx.x * per_block;
+  const int64_t i1 = i0 + per_block < n_dst ? i0 + per_block : n_dst;
+  for (int64_t b = i0; b < i1; b += NB) {
+    __syncthreads();
+    for (int u = threadIdx.x; u < NB * DL; u += 256) {
+      const int64_t i = b + u / DL;
+      const int c = u % DL;
+      float s = 0.0f, gv = 0.0f;
+      if (i < i1) {
+        for (int32_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) s += to_f(hin[(int64_t)col[e] * DL + c]);
+        gv = gF[i * DL + c];
+      }
+      hsum[u / DL][c] = s;
+      gs[u / DL][c] = gv;
+    }
+    __syncthreads();
+    for (int n = 0; n < NB; ++n) {
+      const float hv = hsum[n][p];
+#pragma unroll
+      for (int u = 0; u < PP; ++u) acc[u] += hv * gs[n][q0 + u];
+    }
+  }
+  float* out = part + (size_t)blockIdx.x * DL * DL;
+#pragma unroll
+  for (int u = 0; u < PP; ++u) out[p * DL + q0 + u] = acc[u];
+}
+
+// ------------------------------------------------------------ dz kernel
+
+struct DzArgs {
+  int64_t E;
+  const int32_t* col;
+  const int32_t* dst;
+  const unsigned char* h_in;   // [n_src][d]
+  const unsigned char* gT;     // [n_dst][d]
+  const unsigned char* packed;
+  PackLayout L;
+  const unsigned char* zE;     // [E][h2] permuted order
+  const unsigned char* z1E;    // [E][h1] permuted order
+  unsigned char* da2E;         // [E][h2] permuted order, layer dtype
+  float* da1E;                 // [E][h1] permuted order
+};
+
+template <typename T, int DL, int H1, int H2>
+struct DzShape {
+  static constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL;
+  static constexpr int NT = (H2 <= 64 || (H2 <= 128 && sizeof(T) == 2)) ? 2 : 1, TILE = 4 * NT * 32;
+  static constexpr int KT = H2 / 32, JT = H1 / 32, SKD = DL / KS, SK2 = H2 / KS;
+  static constexpr int ESZ = sizeof(T);
+  static constexpr int ROWB = DL * ESZ + 16;
+  static constexpr int RCH = (H2 * DL * ESZ <= 32768) ? H2 : 32768 / (DL * ESZ);
+  static constexpr int CPP = H2 / RCH, KPC = RCH / 32, NCH = DL * CPP;
+  static constexpr int STAGE = RCH * ROWB, HROWB = DL * ESZ + 16;
+  static constexpr int U16 = RCH * DL * ESZ / 16, UPT = U16 / 256, ROW16 = DL * ESZ / 16;
+  static constexpr int LDS = 2 * STAGE + TILE * HROWB;
+};
+
+template <typename T, int DL, int H1, int H2>
+__global__ __launch_bounds__(256, 1) void k_bwd_dz(DzArgs a) {
+  using S = DzShape<T, DL, H1, H2>;
+  using M = MT<T>;
+  using frag = typename M::frag;
+  constexpr int KS = S::KS, EPL = S::EPL, NT = S::NT, TILE = S::TILE, ESZ = S::ESZ;
+  static_assert(S::U16 % 256 == 0, "chunk must split evenly");
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* stage0 = smem;
+  unsigned char* htile = smem + 2 * S::STAGE;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int64_t t0 = (int64_t)blockIdx.x * TILE;
+  const unsigned char* P = a.packed;
+
+  int64_t eid[NT];
+  int dnode[NT], hrow[NT];
+  bool valid[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    hrow[t] = (wv * NT + t) * 32 + l32;
+    eid[t] = t0 + hrow[t];
+    valid[t] = eid[t] < a.E;
+    dnode[t] = valid[t] ? a.dst[eid[t]] : 0;
+  }
+  {
+    constexpr int HU = DL * ESZ / 16;
+    for (int u = tid; u < TILE * HU; u += 256) {
+      int r = u / HU, c = u % HU;
+      int64_t e = t0 + r;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (e < a.E) v = reinterpret_cast<const uint4*>(a.h_in + (size_t)a.col[e] * DL * ESZ)[c];
+      *reinterpret_cast<uint4*>(htile + r * S::HROWB + c * 16) = v;
+    }
+  }
+  frag gB[NT][S::SKD];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int s = 0; s < S::SKD; ++s)
+      gB[t][s] = ld_frag<T>(a.gT + ((size_t)dnode[t] * DL + s * KS + hh * EPL) * ESZ);
+
+  f32x16 acc[NT][S::KT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int kt = 0; kt < S::KT; ++kt) acc[t][kt] = f32x16{};
+
+  const unsigned char* A3 = P + a.L.w3t;   // [p][k][q]
+  uint4 pre[S::UPT];
+#define DZ_GLOAD(c_)                                                                             \
+  do {                                                                                          \
+    const uint4* src_ = reinterpret_cast<const uint4*>(                                         \
+        A3 + ((size_t)((c_) / S::CPP) * H2 + (size_t)((c_) % S::CPP) * S::RCH) * DL * ESZ);    \
+    _Pragma("unroll") for (int u = 0; u < S::UPT; ++u) pre[u] = src_[tid + u * 256];            \
+  } while (0)
+#define DZ_LSTORE(buf_)                                                                         \
+  do {                                                                                          \
+    _Pragma("unroll") for (int u = 0; u < S::UPT; ++u) {                                        \
+      const int idx = tid + u * 256;                                                            \
+      *reinterpret_cast<uint4*>(stage0 + (buf_) * S::STAGE + (idx / S::ROW16) * S::ROWB +       \
+                                (idx % S::ROW16) * 16) = pre[u];                                \
+    }                                                                                           \
+  } while (0)
+  DZ_GLOAD(0);
+  DZ_LSTORE(0);
+  __syncthreads();
+  for (int p = 0; p < DL; ++p) {
+    float sc[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      sc[t] = to_f(*reinterpret_cast<const T*>(htile + hrow[t] * S::HROWB + p * ESZ));
+#pragma unroll
+    for (int cc = 0; cc < S::CPP; ++cc) {
+      const int c = p * S::CPP + cc;
+      const int buf = c & 1;
+      const bool more = c + 1 < S::NCH;
+      if (more) DZ_GLOAD(c + 1);
+      const unsigned char* sb = stage0 + buf * S::STAGE;
+#pragma unroll
+      for (int kq = 0; kq < S::KPC; ++kq) {
+        f32x16 C[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) C[t] = f32x16{};
+#pragma unroll
+        for (int s = 0; s < S::SKD; ++s) {
+          frag A = ld_frag<T>(sb + (kq * 32 + l32) * S::ROWB + (s * KS + hh * EPL) * ESZ);
+#pragma unroll
+          for (int t = 0; t < NT; ++t) C[t] = M::mma(A, gB[t][s], C[t]);
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[t][cc * S::KPC + kq] += sc[t] * C[t];
+      }
+      if (more) DZ_LSTORE(buf ^ 1);
+      __syncthreads();
+    }
+  }
+#undef DZ_GLOAD
+#undef DZ_LSTORE
+
+  // da2 = dz * [z > 0] in the permuted order, then dz1 = W2^T da2 and da1
+  const unsigned char* w2t = P + a.L.w2t;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const size_t e = valid[t] ? (size_t)eid[t] : 0;
+    frag da2B[S::SK2];
+#pragma unroll
+    for (int s = 0; s < S::SK2; ++s) {
+      const frag zf = ld_frag<T>(a.zE + (e * H2 + s * KS + hh * EPL) * ESZ);
+#pragma unroll
+      for (int u = 0; u < EPL; ++u) {
+        const int n = s * EPL + u;
+        const float v = get_el<T>(zf, u) > 0.0f ? acc[t][n / 16][n % 16] : 0.0f;
+        set_el<T>(da2B[s], u, v);
+      }
+      if (valid[t]) *reinterpret_cast<frag*>(a.da2E + (e * H2 + s * KS + hh * EPL) * ESZ) = da2B[s];
+    }
+#pragma unroll
+    for (int jt = 0; jt < S::JT; ++jt) {
+      f32x16 C = f32x16{};
+#pragma unroll
+      for (int s = 0; s < S::SK2; ++s) {
+        frag A = ld_frag<T>(w2t + ((size_t)(jt * 32 + l32) * H2 + s * KS + hh * EPL) * ESZ);
+        C = M::mma(A, da2B[s], C);
+      }
+      // register i of tile jt is permuted position n = 16*jt + i
+#pragma unroll
+      for (int i = 0; i < 16; i += EPL) {
+        const int n = 16 * jt + i;
+        const int pos = (n / EPL) * KS + hh * EPL;
+        const frag z1f = ld_frag<T>(a.z1E + (e * H1 + pos) * ESZ);
+        float v[EPL];
+#pragma unroll
+        for (int u = 0; u < EPL; ++u) v[u] = get_el<T>(z1f, u) > 0.0f ? C[i + u] : 0.0f;
+        if (valid[t]) {
+          float* dst = a.da1E + e * H1 + pos;
+          if constexpr (EPL == 8) {
+            *reinterpret_cast<f32x4*>(dst) = f32x4{v[0], v[1], v[2], v[3]};
+            *reinterpret_cast<f32x4*>(dst + 4) = f32x4{v[4], v[5], v[6], v[7]};
+          } else {
+            dst[0] = v[0];
+          }
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------ dW3 (split over edges)
+
+struct W3Args {
+  int64_t E;
+  int64_t per_chunk;   // edges per chunk (multiple of 64)
+  int nchunk;
+  const int32_t* col;
+  const int32_t* dst;
+  const unsigned char* h_in;
+  const float* gF;
+  const unsigned char* zE;
+  float* part;         // [nchunk][d*d*h2]
+};
+
+template <typename T, int DL, int H2>
+struct W3Shape {
+  static constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL, ESZ = sizeof(T);
+  static constexpr int QT = DL / 32, KT = H2 / 32;
+  static constexpr int QT_W = QT < 2 ? QT : 2, KT_W = KT < 4 ? KT : 4;
+  static constexpr int WPP = (QT / QT_W) * (KT / KT_W), PB = 4 / WPP;
+  static constexpr int ECH = 64;
+  static constexpr int ZROW = (ECH + 16 / ESZ) * ESZ;   // bytes per k row of the z chunk
+  static constexpr int FROW = ECH + 4;                   // floats per row of g / h chunks
+  static constexpr int LDS = H2 * ZROW + DL * FROW * 4 + PB * FROW * 4;
+  static_assert(WPP * PB == 4, "four waves per workgroup");
+};
+
+template <typename T, int DL, int H2>
+__global__ __launch_bounds__(256, 1) void k_bwd_dW3(W3Args a) {
+  using S = W3Shape<T, DL, H2>;
+  using M = MT<T>;
+  using frag = typename M::frag;
+  constexpr int KS = S::KS, EPL = S::EPL, ESZ = S::ESZ, ECH = S::ECH;
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* zl = smem;
+  float* gl = reinterpret_cast<float*>(smem + H2 * S::ZROW);
+  float* hl = gl + DL * S::FROW;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  // workgroups of one edge chunk sit on one XCD (ids congruent mod 8)
+  constexpr int NPB = DL / S::PB;
+  const int wg = blockIdx.x, xcd = wg & 7, slot = wg >> 3;
+  const int chunk = (slot / NPB) * 8 + xcd, pb = slot % NPB;
+  const int p0 = pb * S::PB, pl = wv / S::WPP, sub = wv % S::WPP;
+  const int qt0 = (sub % (S::QT / S::QT_W)) * S::QT_W, kt0 = (sub / (S::QT / S::QT_W)) * S::KT_W;
+  const T* hin = reinterpret_cast<const T*>(a.h_in);
+  const int64_t e_begin = (int64_t)chunk * a.per_chunk;
+  int64_t e_end = e_begin + a.per_chunk;
+  if (e_end > a.E) e_end = a.E;
+
+  f32x16 acc[S::KT_W][S::QT_W];
+#pragma unroll
+  for (int kk = 0; kk < S::KT_W; ++kk)
+#pragma unroll
+    for (int qq = 0; qq < S::QT_W; ++qq) acc[kk][qq] = f32x16{};
+
+  for (int64_t eb = e_begin; eb < e_end; eb += ECH) {
+    __syncthreads();
+    // z chunk, transposed to [k][e] with the permutation undone
+    constexpr int ZU = H2 * ESZ / 16;   // 16-byte units per edge row
+    for (int u = tid; u < ECH * ZU; u += 256) {
+      const int el = u / ZU, c16 = u % ZU;
+      const int64_t e = eb + el;
+      const uint4 raw = e < e_end ? *reinterpret_cast<const uint4*>(a.zE + ((size_t)e * H2) * ESZ + c16 * 16)
+                                  : make_uint4(0, 0, 0, 0);
+      const T* v = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+      for (int w = 0; w < 16 / ESZ; ++w) {
+        const int k = kperm<T>(c16 * (16 / ESZ) + w);
+        *reinterpret_cast<T*>(zl + k * S::ZROW + el * ESZ) = v[w];
+      }
+    }
+    for (int u = tid; u < ECH * (DL / 4); u += 256) {
+      const int el = u / (DL / 4), q4 = u % (DL / 4);
+      const int64_t e = eb + el;
+      f32x4 v = {0.f, 0.f, 0.f, 0.f};
+      if (e < e_end) v = *reinterpret_cast<const f32x4*>(a.gF + (size_t)a.dst[e] * DL + q4 * 4);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) gl[(q4 * 4 + w) * S::FROW + el] = v[w];
+    }
+    for (int u = tid; u < ECH * S::PB; u += 256) {
+      const int el = u / S::PB, pp = u % S::PB;
+      const int64_t e = eb + el;
+      hl[pp * S::FROW + el] = e < e_end ? to_f(hin[(size_t)a.col[e] * DL + p0 + pp]) : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll 2
+    for (int ks = 0; ks < ECH / KS; ++ks) {
+      const int ec = ks * KS + hh * EPL;
+      frag A[S::KT_W];
+#pragma unroll
+      for (int kk = 0; kk < S::KT_W; ++kk) A[kk] = ld_frag<T>(zl + ((kt0 + kk) * 32 + l32) * S::ZROW + ec * ESZ);
+      float hv[EPL];
+#pragma unroll
+      for (int u = 0; u < EPL; ++u) hv[u] = hl[pl * S::FROW + ec + u];
+#pragma unroll
+      for (int qq = 0; qq < S::QT_W; ++qq) {
+        const float* gr = gl + ((qt0 + qq) * 32 + l32) * S::FROW + ec;
+        frag B;
+#pragma unroll
+        for (int u = 0; u < EPL; ++u) set_el<T>(B, u, hv[u] * gr[u]);
+#pragma unroll
+        for (int kk = 0; kk < S::KT_W; ++kk) acc[kk][qq] = M::mma(A[kk], B, acc[kk][qq]);
+      }
+    }
+  }
+  // tile (k rows, q cols) -> part[chunk][(p*d + q)*h2 + k]
+  float* out = a.part + (size_t)chunk * DL * DL * H2;
+  const int p = p0 + pl;
+#pragma unroll
+  for (int qq = 0; qq < S::QT_W; ++qq) {
+    const int q = (qt0 + qq) * 32 + l32;
+#pragma unroll
+    for (int kk = 0; kk < S::KT_W; ++kk)
+#pragma unroll
+      for (int a4 = 0; a4 < 4; ++a4) {
+        const int k = (kt0 + kk) * 32 + 8 * a4 + 4 * hh;
+        *reinterpret_cast<f32x4*>(out + ((size_t)p * DL + q) * H2 + k) =
+            f32x4{acc[kk][qq][4 * a4], acc[kk][qq][4 * a4 + 1], acc[kk][qq][4 * a4 + 2], acc[kk][qq][4 * a4 + 3]};
+      }
+  }
+}
+
+// ------------------------------------------------------------ dW2 / db2 (split over edges)
+
+struct W2Args {
+  int64_t E;
+  int64_t per_chunk;
+  int nsplit;
+  const unsigned char* da2E;   // [E][h2] permuted
+  const unsigned char* z1E;    // [E][h1] permuted
+  float* part;                 // [nchunk][h2*h1 + h2]
+};
+
+template <typename T, int H1, int H2>
+struct W2Shape {
+  static constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL, ESZ = sizeof(T);
+  static constexpr int KT = H2 / 32, JT = H1 / 32;
+  static constexpr int NSPLIT = KT * JT > 32 ? KT * JT / 32 : 1;
+  static constexpr int JT_WG = JT / NSPLIT;                 // j tiles per workgroup
+  static constexpr int KT_W = KT >= 4 ? KT / 4 : 1;         // k tiles per wave
+  static constexpr int JGRP = KT >= 4 ? 1 : 4 / KT;         // waves sharing one k tile
+  static constexpr int JT_W = JT_WG / JGRP;                 // j tiles per wave
+  static constexpr int ECH = 64;
+  static constexpr int ROW = (ECH + 16 / ESZ) * ESZ;
+  static constexpr int LDS = (H2 + H1) * ROW;
+};
+
+template <typename T, int H1, int H2>
+__global__ __launch_bounds__(256, 1) void k_bwd_dW2(W2Args a) {
+  using S = W2Shape<T, H1, H2>;
+  using M = MT<T>;
+  using frag = typename M::frag;
+  constexpr int KS = S::KS, EPL = S::EPL, ESZ = S::ESZ, ECH = S::ECH;
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* dl = smem;                 // da2 [k][e]
+  unsigned char* zl = smem + H2 * S::ROW;   // z1 [j][e]
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int split = blockIdx.x % S::NSPLIT, chunk = blockIdx.x / S::NSPLIT;
+  const int kt0 = (wv / S::JGRP) * S::KT_W;
+  const int jt0 = split * S::JT_WG + (wv % S::JGRP) * S::JT_W;
+  const int64_t e_begin = (int64_t)chunk * a.per_chunk;
+  int64_t e_end = e_begin + a.per_chunk;
+  if (e_end > a.E) e_end = a.E;
+  f32x16 acc[S::KT_W][S::JT_W];
+#pragma unroll
+  for (int kk = 0; kk < S::KT_W; ++kk)
+#pragma unroll
+    for (int jj = 0; jj < S::JT_W; ++jj) acc[kk][jj] = f32x16{};
+  float bsum = 0.0f;
+  for (int64_t eb = e_begin; eb < e_end; eb += ECH) {
+    __syncthreads();
+    constexpr int DU = H2 * ESZ / 16, ZU = H1 * ESZ / 16;
+    for (int u = tid; u < ECH * (DU + ZU); u += 256) {
+      const bool isd = u < ECH * DU;
+      const int uu = isd ? u : u - ECH * DU;
+      const int W = isd ? DU : ZU;
+      const int el = uu / W, c16 = uu % W;
+      const int64_t e = eb + el;
+      const unsigned char* srcp = isd ? a.da2E + (size_t)e * H2 * ESZ : a.z1E + (size_t)e * H1 * ESZ;
+      const uint4 raw = e < e_end ? *reinterpret_cast<const uint4*>(srcp + c16 * 16) : make_uint4(0, 0, 0, 0);
+      const T* v = reinterpret_cast<const T*>(&raw);
+      unsigned char* base = isd ? dl : zl;
+#pragma unroll
+      for (int w = 0; w < 16 / ESZ; ++w) {
+        const int k = kperm<T>(c16 * (16 / ESZ) + w);
+        *reinterpret_cast<T*>(base + k * S::ROW + el * ESZ) = v[w];
+      }
+    }
+    __syncthreads();
+    if (split == 0 && tid < H2)
+      for (int el = 0; el < ECH; ++el) bsum += to_f(*reinterpret_cast<const T*>(dl + tid * S::ROW + el * ESZ));
+#pragma unroll 2
+    for (int ks = 0; ks < ECH / KS; ++ks) {
+      const int ec = ks * KS + hh * EPL;
+      frag A[S::KT_W];
+#pragma unroll
+      for (int kk = 0; kk < S::KT_W; ++kk) A[kk] = ld_frag<T>(dl + ((kt0 + kk) * 32 + l32) * S::ROW + ec * ESZ);
+#pragma unroll
+      for (int jj = 0; jj < S::JT_W; ++jj) {
+        const frag B = ld_frag<T>(zl + ((jt0 + jj) * 32 + l32) * S::ROW + ec * ESZ);
+#pragma unroll
+        for (int kk = 0; kk < S::KT_W; ++kk) acc[kk][jj] = M::mma(A[kk], B, acc[kk][jj]);
+      }
+    }
+  }
+  float* out = a.part + (size_t)chunk * (H2 * H1 + H2);
+#pragma unroll
+  for (int jj = 0; jj < S::JT_W; ++jj) {
+    const int j = (jt0 + jj) * 32 + l32;
+#pragma unroll
+    for (int kk = 0; kk < S::KT_W; ++kk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int k = (kt0 + kk) * 32 + 8 * (i / 4) + 4 * hh + (i % 4);
+        out[(size_t)k * H1 + j] = acc[kk][jj][i];
+      }
+  }
+  if (split == 0 && tid < H2) out[H2 * H1 + tid] = bsum;
+}
+
+// ------------------------------------------------------------ dW1 / db1 (split over edges)
+
+template <int H1>
+__global__ __launch_bounds__(256) void k_bwd_dW1(int64_t E, int64_t per_chunk, const int32_t* __restrict__ col,
+                                                 const int32_t* __restrict__ dst, const float* __restrict__ node_attr,
+                                                 int dim, int attr_mode, int de, const float* __restrict__ da1E,
+                                                 const int* __restrict__ jof, float* __restrict__ part) {
+  constexpr int SUB = 256 / H1;
+  __shared__ float red[SUB][H1][9];
+  const int kk = threadIdx.x % H1, sub = threadIdx.x / H1;
+  const int64_t e0 = (int64_t)blockIdx.x * per_chunk;
+  int64_t e1 = e0 + per_chunk;
+  if (e1 > E) e1 = E;
+  float acc[9];
+#pragma unroll
+  for (int c = 0; c < 9; ++c) acc[c] = 0.0f;
+  for (int64_t e = e0 + sub; e < e1; e += SUB) {
+    float x[8];
+    edge_attr(node_attr, dim, attr_mode, dst[e], col[e], x);
+    const float v = da1E[e * H1 + kk];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[c] += v * x[c];
+    acc[8] += v;
+  }
+#pragma unroll
+  for (int c = 0; c < 9; ++c) red[sub][kk][c] = acc[c];
+  __syncthreads();
+  if (sub == 0) {
+    for (int s = 1; s < SUB; ++s)
+#pragma unroll
+      for (int c = 0; c < 9; ++c) acc[c] += red[s][kk][c];
+    const int j = jof[kk];
+    float* out = part + (size_t)blockIdx.x * (H1 * de + H1);
+    for (int c = 0; c < de; ++c) out[j * de + c] = acc[c];
+    out[H1 * de + j] = acc[8];
+  }
+}
+
+// ------------------------------------------------------------ reductions and finals
+
+// out[x] = [out[x] +] sum_c part[c*stride + off + x], chunks added in order
+__global__ void k_reduce(const float* __restrict__ part, int nchunk, int64_t stride, int64_t off, int64_t n,
+                         float* __restrict__ out, int accumulate) {
+  for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n; x += (int64_t)gridDim.x * blockDim.x) {
+    float s = 0.0f;
+    for (int c = 0; c < nchunk; ++c) s += part[(int64_t)c * stride + off + x];
+    out[x] = accumulate ? out[x] + s : s;
+  }
+}
+
+__device__ __forceinline__ float segment_sum(const int32_t* __restrict__ ptr, int64_t i, int q, int DL,
+                                             const float* __restrict__ direct, const float* __restrict__ part) {
+  const int64_t pa = ptr[i], pb = ptr[i + 1];
+  if (pb <= pa) return 0.0f;
+  const int64_t ta = pa / EDGE_TILE, tb = (pb - 1) / EDGE_TILE;
+  if (ta == tb) return direct[i * DL + q];
+  float s = part[(ta * 2 + 1) * DL + q];
+  for (int64_t t = ta + 1; t < tb; ++t) s += part[(t * 2) * DL + q];
+  s += part[(tb * 2) * DL + q];
+  return s;
+}
+
+// grad_h[j] = [root/residual terms if j is a destination] + sum over the edges leaving j
+__global__ void k_bwd_dh_final(int64_t n_src, int64_t n_dst, int DL, const int32_t* __restrict__ csc_ptr,
+                               const float* __restrict__ direct, const float* __restrict__ part,
+                               const float* __restrict__ dh_node, float* __restrict__ grad_h) {
+  const int64_t total = n_src * DL;
+  for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < total; x += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t j = x / DL;
+    const int c = (int)(x % DL);
+    float s = segment_sum(csc_ptr, j, c, DL, direct, part);
+    if (j < n_dst) s += dh_node[x];
+    grad_h[x] = s;
+  }
+}
+
+__global__ void k_jof(int* out, int h1, int isbf16) {
+  int kk = blockIdx.x * blockDim.x + threadIdx.x;
+  if (kk < h1) out[kk] = isbf16 ? kperm<__bf16>(kk) : kperm<float>(kk);
+}
+
+// ------------------------------------------------------------ workspace
+
+struct BwdWs {
+  float *ybar, *gF, *dh_node, *dh_direct, *dh_part, *da1E;
+  unsigned char *gT, *da2E;
+  float *p_root, *p_db3, *p_w3, *p_w2, *p_w1;
+  int* jof;
+  int nr, nb3, n3, n2, n1;
+  int64_t pc3, pc2, pc1, pr, pb3;
+  size_t total;
+};
+
+int w3_nchunk(int d, int h2, int64_t E) {
+  int pb = 4;
+  int qt = d / 32, kt = h2 / 32;
+  int qtw = qt < 2 ? qt : 2, ktw = kt < 4 ? kt : 4;
+  int wpp = (qt / qtw) * (kt / ktw);
+  pb = 4 / wpp;
+  int npb = d / pb;
+  int target = 1024 / npb;
+  int n = ((target + 7) / 8) * 8;
+  if (n < 8) n = 8;
+  int64_t maxn = ((E + 63) / 64 + 7) / 8 * 8;
+  if (maxn < 8) maxn = 8;
+  if (n > maxn) n = (int)maxn;
+  return n;
+}
+
+BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t E, void* base) {
+  Carve c(base);
+  BwdWs w;
+  const int esz = d.dtype == DSMP_BF16 ? 2 : 4;
+  const int de = layer_attr_width(d);
+  w.ybar = c.take<float>((size_t)n_dst * d.d);
+  w.gF = c.take<float>((size_t)n_dst * d.d);
+  w.gT = c.take<unsigned char>((size_t)n_dst * d.d * esz);
+  w.dh_node = c.take<float>((size_t)n_dst * d.d);
+  w.dh_direct = c.take<float>((size_t)n_src * d.d);
+  w.dh_part = c.take<float>((size_t)(ceil_div(E, EDGE_TILE) + 1) * 2 * d.d);
+  w.da2E = c.take<unsigned char>((size_t)E * d.h2 * esz);
+  w.da1E = c.take<float>((size_t)E * d.h1);
+  w.nr = (int)(n_dst > 0 ? (ceil_div(n_dst, 512) < 256 ? ceil_div(n_dst, 512) : 256) : 1);
+  w.pr = n_dst > 0 ? ceil_div(n_dst, w.nr) : 1;
+  w.p_root = c.take<float>((size_t)w.nr * (d.d * d.d + d.d));
+  w.nb3 = w.nr;
+  w.pb3 = w.pr;
+  w.p_db3 = c.take<float>((size_t)w.nb3 * d.d * d.d);
+  w.n3 = w3_nchunk(d.d, d.h2, E);
+  w.pc3 = ((E + w.n3 - 1) / w.n3 + 63) / 64 * 64;
+  if (w.pc3 < 64) w.pc3 = 64;
+  w.p_w3 = c.take<float>((size_t)w.n3 * d.d * d.d * d.h2);
+  w.n2 = (int)(E > 0 ? (ceil_div(E, 2048) < 512 ? ceil_div(E, 2048) : 512) : 1);
+  w.pc2 = ((E + w.n2 - 1) / w.n2 + 63) / 64 * 64;
+  if (w.pc2 < 64) w.pc2 = 64;
+  w.p_w2 = c.take<float>((size_t)w.n2 * (d.h2 * d.h1 + d.h2));
+  w.n1 = (int)(E > 0 ? (ceil_div(E, 1024) < 1024 ? ceil_div(E, 1024) : 1024) : 1);
+  w.pc1 = E > 0 ? (E + w.n1 - 1) / w.n1 : 1;
+  w.p_w1 = c.take<float>((size_t)w.n1 * (d.h1 * de + d.h1));
+  w.jof = c.take<int>(d.h1);
+  w.total = c.used();
+  return w;
+}
+
+template <typename K>
+dsmp_status set_lds(dsmp_handle* h, K kernel, int bytes) {
+  DSMP_HIP(h, hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, bytes));
+  return DSMP_OK;
+}
+
+template <typename T, int DL, int H1, int H2>
+dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, const W2Args& w2) {
+  hipStream_t s = h->stream;
+  dsmp_status st;
+  if (dz.E > 0) {
+    using S = DzShape<T, DL, H1, H2>;
+    auto kz = k_bwd_dz<T, DL, H1, H2>;
+    if ((st = set_lds(h, kz, S::LDS)) != DSMP_OK) return st;
+    hipLaunchKernelGGL(kz, dim3(ceil_div(dz.E, S::TILE)), dim3(256), S::LDS, s, dz);
+    DSMP_LAUNCHED(h, "dz");
+  }
+  {
+    using S = W3Shape<T, DL, H2>;
+    auto k3 = k_bwd_dW3<T, DL, H2>;
+    if ((st = set_lds(h, k3, S::LDS)) != DSMP_OK) return st;
+    hipLaunchKernelGGL(k3, dim3((DL / S::PB) * w3.nchunk), dim3(256), S::LDS, s, w3);
+    DSMP_LAUNCHED(h, "dW3");
+  }
+  {
+    using S = W2Shape<T, H1, H2>;
+    auto k2 = k_bwd_dW2<T, H1, H2>;
+    if ((st = set_lds(h, k2, S::LDS)) != DSMP_OK) return st;
+    int nchunk = (int)((w2.E + w2.per_chunk - 1) / w2.per_chunk);
+    if (nchunk < 1) nchunk = 1;
+    hipLaunchKernelGGL(k2, dim3(nchunk * S::NSPLIT), dim3(256), S::LDS, s, w2);
+    DSMP_LAUNCHED(h, "dW2");
+  }
+  return DSMP_OK;
+}
+
+dsmp_status dispatch_edge_grads(dsmp_handle* h, const dsmp_layer_desc& d, const DzArgs& dz, const W3Args& w3,
+                                const W2Args& w2) {
+  if (d.dtype == DSMP_F32) {
+    if (d.d == 32) return run_edge_grads<float, 32, 64, 64>(h, dz, w3, w2);
+    if (d.d == 64) return run_edge_grads<float, 64, 128, 128>(h, dz, w3, w2);
+  } else {
+    if (d.d == 32) return run_edge_grads<__bf16, 32, 64, 64>(h, dz, w3, w2);
+    if (d.d == 64) return run_edge_grads<__bf16, 64, 128, 128>(h, dz, w3, w2);
+    if (d.d == 128) return run_edge_grads<__bf16, 128, 256, 256>(h, dz, w3, w2);
+  }
+  return fail(h, DSMP_UNSUPPORTED, "unsupported layer shape");
+}
+
+template <typename T, int DL>
+void launch_node_kernels(dsmp_handle* h, const BNodeArgs& na, int64_t n_dst, const BwdWs& w,
+                         const unsigned char* h_in, const int32_t* row_ptr, const int32_t* col) {
+  hipStream_t s = h->stream;
+  if (n_dst == 0) return;
+  unsigned grid = ceil_div(n_dst, 256 / DL);
+  if (grid > 2048) grid = 2048;
+  hipLaunchKernelGGL((k_bwd_node<T, DL>), dim3(grid), dim3(256), 0, s, na);
+  hipLaunchKernelGGL((k_bwd_root<T, DL>), dim3(w.nr), dim3(256), 0, s, n_dst, w.pr, w.ybar, h_in, w.p_root);
+  hipLaunchKernelGGL((k_bwd_db3<T, DL>), dim3(w.nb3), dim3(256), 0, s, n_dst, w.pb3, row_ptr, col, h_in, w.gF,
+                     w.p_db3);
+}
+
+}  // namespace
 
 extern "C" dsmp_status dsmp_nnconv_workspace(const dsmp_layer_desc* desc, const dsmp_graph* g,
                                              size_t* saved_bytes, size_t* fwd_ws, size_t* bwd_ws) {
   if (!desc || !g || !saved_bytes || !fwd_ws || !bwd_ws) return DSMP_INVALID_ARG;
   dsmp_status st = check_layer_desc(nullptr, desc);
   if (st != DSMP_OK) return st;
+  if (g->n_dst < 0 || g->n_src < g->n_dst || g->n_edges < 0) return DSMP_INVALID_ARG;
   *saved_bytes = saved_layout(*desc, g->n_dst, g->n_edges).total;
   *fwd_ws = fwd_ws_bytes(*desc, g->n_dst, g->n_edges);
-  *bwd_ws = 256;
+  *bwd_ws = carve_bwd(*desc, g->n_dst, g->n_src, g->n_edges, nullptr).total;
   return DSMP_OK;
 }
 
-extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_desc*, const void*,
-                                            const dsmp_graph*, const float*, const void*, const void*,
-                                            size_t, const float*, float*, const dsmp_layer_grads*,
-                                            int32_t, void*, size_t) {
-  return fail(h, DSMP_UNSUPPORTED, "backward not built yet");
+extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_desc* desc, const void* packed,
+                                            const dsmp_graph* g, const float* node_attr, const void* h_in,
+                                            const void* saved, size_t saved_bytes, const float* grad_out,
+                                            float* grad_h, const dsmp_layer_grads* grads, int32_t flags, void* ws,
+                                            size_t ws_bytes) {
+  if (!h) return DSMP_INVALID_ARG;
+  dsmp_status st = check_layer_desc(h, desc);
+  if (st != DSMP_OK) return st;
+  if ((st = check_graph(h, g, true)) != DSMP_OK) return st;
+  const dsmp_layer_desc& d = *desc;
+  DSMP_CHECK(h, packed && saved && grads, DSMP_INVALID_ARG, "packed, saved or grads is NULL");
+  DSMP_CHECK(h, grads->dW1 && grads->db1 && grads->dW2 && grads->db2 && grads->dW3 && grads->db3 && grads->dWr &&
+                    grads->dbr, DSMP_INVALID_ARG, "a gradient pointer is NULL");
+  DSMP_CHECK(h, (g->n_dst == 0 || grad_out) && (g->n_src == 0 || (grad_h && h_in && node_attr)),
+             DSMP_INVALID_ARG, "a backward pointer is NULL");
+  DSMP_CHECK(h, (flags & ~DSMP_GRAD_ACCUMULATE) == 0, DSMP_INVALID_ARG, "unknown flags");
+  const SavedLayout sl = saved_layout(d, g->n_dst, g->n_edges);
+  DSMP_CHECK(h, saved_bytes >= sl.total, DSMP_WORKSPACE_TOO_SMALL, "saved buffer needs %zu bytes", sl.total);
+  const BwdWs need = carve_bwd(d, g->n_dst, g->n_src, g->n_edges, nullptr);
+  DSMP_CHECK(h, ws && ws_bytes >= need.total, DSMP_WORKSPACE_TOO_SMALL, "backward workspace needs %zu bytes",
+             need.total);
+  const BwdWs w = carve_bwd(d, g->n_dst, g->n_src, g->n_edges, ws);
+  const int esz = d.dtype == DSMP_BF16 ? 2 : 4;
+  const int de = layer_attr_width(d);
+  const PackLayout L = pack_layout(d.d, d.h1, d.h2, esz);
+  const unsigned char* pk = static_cast<const unsigned char*>(packed);
+  const unsigned char* sv = static_cast<const unsigned char*>(saved);
+  const unsigned char* hin = static_cast<const unsigned char*>(h_in);
+  hipStream_t s = h->stream;
+  const int acc = flags & DSMP_GRAD_ACCUMULATE;
+  const int64_t E = g->n_edges, n_dst = g->n_dst, n_src = g->n_src;
+
+  // node pre-pass, root grads, db3 partials
+  BNodeArgs na{n_dst, g->row_ptr, grad_out, reinterpret_cast<const float*>(sv + sl.y),
+               reinterpret_cast<const float*>(pk + L.wr), w.ybar, w.gT, w.gF, w.dh_node, d.act, d.residual};
+  if (d.dtype == DSMP_BF16) {
+    if (d.d == 32) launch_node_kernels<__bf16, 32>(h, na, n_dst, w, hin, g->row_ptr, g->col);
+    if (d.d == 64) launch_node_kernels<__bf16, 64>(h, na, n_dst, w, hin, g->row_ptr, g->col);
+    if (d.d == 128) launch_node_kernels<__bf16, 128>(h, na, n_dst, w, hin, g->row_ptr, g->col);
+  } else {
+    if (d.d == 32) launch_node_kernels<float, 32>(h, na, n_dst, w, hin, g->row_ptr, g->col);
+    if (d.d == 64) launch_node_kernels<float, 64>(h, na, n_dst, w, hin, g->row_ptr, g->col);
+  }
+  DSMP_LAUNCHED(h, "backward node kernels");
+
+  // feature gradient through the edges (edge contraction in source order)
+  EdgeArgs ea{};
+  ea.E = E; ea.n_dst = n_dst; ea.n_src = n_src;
+  ea.row_ptr = g->row_ptr; ea.col = g->col; ea.dst = g->dst; ea.csc_ptr = g->csc_ptr; ea.csc_eid = g->csc_eid;
+  ea.node_attr = node_attr; ea.dim = d.dim; ea.attr_mode = d.attr_mode;
+  ea.gath = w.gT; ea.packed = pk; ea.L = L;
+  ea.zE = const_cast<unsigned char*>(sv + sl.zE);
+  ea.z1E = nullptr;
+  ea.out_direct = w.dh_direct; ea.out_part = w.dh_part;
+  if ((st = launch_edge_contract(h, d, MODE_DH, ea)) != DSMP_OK) return st;
+  if (n_src > 0) {
+    unsigned grid = ceil_div(n_src * d.d, 256);
+    if (grid > 4096) grid = 4096;
+    hipLaunchKernelGGL(k_bwd_dh_final, dim3(grid), dim3(256), 0, s, n_src, n_dst, d.d, g->csc_ptr, w.dh_direct,
+                       w.dh_part, w.dh_node, grad_h);
+    DSMP_LAUNCHED(h, "grad_h");
+  }
+
+  // kernel-MLP gradients
+  if (E > 0) {
+    DzArgs dz{E, g->col, g->dst, hin, w.gT, pk, L, sv + sl.zE, sv + sl.z1E, w.da2E, w.da1E};
+    W3Args w3{E, w.pc3, w.n3, g->col, g->dst, hin, w.gF, sv + sl.zE, w.p_w3};
+    W2Args w2{E, w.pc2, 1, w.da2E, sv + sl.z1E, w.p_w2};
+    if ((st = dispatch_edge_grads(h, d, dz, w3, w2)) != DSMP_OK) return st;
+    hipLaunchKernelGGL(k_jof, dim3(ceil_div(d.h1, 256)), dim3(256), 0, s, w.jof, d.h1, d.dtype == DSMP_BF16);
+    int n1 = (int)((E + w.pc1 - 1) / w.pc1);
+    if (d.h1 == 64)
+      hipLaunchKernelGGL((k_bwd_dW1<64>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr, d.dim,
+                         d.attr_mode, de, w.da1E, w.jof, w.p_w1);
+    else if (d.h1 == 128)
+      hipLaunchKernelGGL((k_bwd_dW1<128>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr, d.dim,
+                         d.attr_mode, de, w.da1E, w.jof, w.p_w1);
+    else
+      hipLaunchKernelGGL((k_bwd_dW1<256>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr, d.dim,
+                         d.attr_mode, de, w.da1E, w.jof, w.p_w1);
+    DSMP_LAUNCHED(h, "dW1");
+  }
+
+  // fixed-order reductions into the caller's gradients
+  auto red = [&](const float* part, int nchunk, int64_t stride, int64_t off, int64_t n, float* out) {
+    unsigned grid = ceil_div(n, 256);
+    if (grid > 2048) grid = 2048;
+    if (grid == 0) return;
+    hipLaunchKernelGGL(k_reduce, dim3(grid), dim3(256), 0, s, part, nchunk, stride, off, n, out, acc);
+  };
+  const int64_t dd = (int64_t)d.d * d.d;
+  const int n3 = E > 0 ? w.n3 : 0;
+  const int n2 = E > 0 ? (int)((E + w.pc2 - 1) / w.pc2) : 0;
+  const int n1 = E > 0 ? (int)((E + w.pc1 - 1) / w.pc1) : 0;
+  const int nr = n_dst > 0 ? w.nr : 0;
+  red(w.p_root, nr, dd + d.d, 0, dd, grads->dWr);
+  red(w.p_root, nr, dd + d.d, dd, d.d, grads->dbr);
+  red(w.p_db3, nr, dd, 0, dd, grads->db3);
+  red(w.p_w3, n3, dd * d.h2, 0, dd * d.h2, grads->dW3);
+  red(w.p_w2, n2, (int64_t)d.h2 * d.h1 + d.h2, 0, (int64_t)d.h2 * d.h1, grads->dW2);
+  red(w.p_w2, n2, (int64_t)d.h2 * d.h1 + d.h2, (int64_t)d.h2 * d.h1, d.h2, grads->db2);
+  red(w.p_w1, n1, (int64_t)d.h1 * de + d.h1, 0, (int64_t)d.h1 * de, grads->dW1);
+  red(w.p_w1, n1, (int64_t)d.h1 * de + d.h1, (int64_t)d.h1 * de, d.h1, grads->db1);
+  DSMP_LAUNCHED(h, "gradient reductions");
+  return DSMP_OK;
 }

@@ -20,34 +20,6 @@
 // tile); the node kernel adds those partials in tile order.
 #include "nnconv.hpp"
 
-#include <mutex>
-
-namespace dsmp {
-
-enum { MODE_FWD = 0, MODE_DH = 1 };
-
-struct EdgeArgs {
-  int64_t E, n_dst, n_src;
-  const int32_t* row_ptr;
-  const int32_t* col;
-  const int32_t* dst;
-  const int32_t* csc_ptr;
-  const int32_t* csc_eid;
-  const float* node_attr;
-  int dim, attr_mode;
-  const unsigned char* gath;     // FWD: h_in [n_src][d]; DH: g [n_dst][d]  (layer dtype)
-  const unsigned char* packed;
-  PackLayout L;
-  unsigned char* zE;             // [E][h2] layer dtype: FWD writes (if set), DH reads
-  unsigned char* z1E;            // [E][h1] layer dtype: FWD writes (if set)
-  float* out_direct;             // [segments][d]
-  float* out_part;               // [tiles][2][d]
-};
-
-dsmp_status launch_edge_contract(dsmp_handle* h, const dsmp_layer_desc& desc, int mode,
-                                 const EdgeArgs& a);
-
-}  // namespace dsmp
 
 using namespace dsmp;
 
@@ -177,9 +149,12 @@ __global__ __launch_bounds__(256, 1) void k_edge_contract(EdgeArgs a) {
       for (int n = 0; n < H1 / 2; ++n) {
         const f32x4 wa = *reinterpret_cast<const f32x4*>(w1l + n * 8);
         const f32x4 wb = *reinterpret_cast<const f32x4*>(w1l + n * 8 + 4);
+        // b1 + W1 x as a chain of fused multiply-adds in attribute order
         float v = b1l[n];
-        v += wa[0] * x[0]; v += wa[1] * x[1]; v += wa[2] * x[2]; v += wa[3] * x[3];
-        v += wb[0] * x[4]; v += wb[1] * x[5]; v += wb[2] * x[6]; v += wb[3] * x[7];
+        v = __builtin_fmaf(wa[0], x[0], v); v = __builtin_fmaf(wa[1], x[1], v);
+        v = __builtin_fmaf(wa[2], x[2], v); v = __builtin_fmaf(wa[3], x[3], v);
+        v = __builtin_fmaf(wb[0], x[4], v); v = __builtin_fmaf(wb[1], x[5], v);
+        v = __builtin_fmaf(wb[2], x[6], v); v = __builtin_fmaf(wb[3], x[7], v);
         set_el<T>(z1B[t][n / EPL], n % EPL, v > 0.0f ? v : 0.0f);
       }
       if (a.z1E && valid[t]) {
@@ -540,10 +515,6 @@ namespace dsmp {
 
 dsmp_status check_layer_desc(dsmp_handle* h, const dsmp_layer_desc* d) { return check_desc(h, d); }
 int layer_attr_width(const dsmp_layer_desc& d) { return attr_width(d); }
-
-struct SavedLayout {
-  size_t y, zE, z1E, total;
-};
 
 SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E) {
   Carve c(nullptr);

@@ -63,8 +63,19 @@ class Case:
 
     def oracle_forward(self):
         out, _ = onn.forward(self.P, self.x, self.h.astype(np.float64), self.rp, self.col, self.n_dst,
-                             self.act, bool(self.residual), rows=self.rows)
+                             self.act, bool(self.residual), rows=self.rows, decide=self.dtype)
         return out
+
+    def clear_ambiguous_outputs(self):
+        """Zero the upstream gradient where ReLU(y) is a decision a float32
+        kernel could take either way (either choice is then correct)."""
+        if self.act != onn.ACT_RELU:
+            return 0
+        _, _, amb = onn.forward(self.P, self.x, self.h.astype(np.float64), self.rp, self.col, self.n_dst,
+                                self.act, bool(self.residual), rows=self.rows, decide=self.dtype,
+                                return_ambiguous=True)
+        self.G = np.where(amb, 0.0, self.G).astype(np.float32)
+        return int(amb.sum())
 
     def backward(self):
         dev = self.torch.device("cuda", 0)
@@ -75,7 +86,7 @@ class Case:
 
     def oracle_backward(self):
         return onn.backward(self.P, self.x, self.h.astype(np.float64), self.rp, self.col, self.n_dst, self.G,
-                            self.act, bool(self.residual), rows=self.rows)
+                            self.act, bool(self.residual), rows=self.rows, decide=self.dtype)
 
 
 def random_case(env, shape, n=900, n_dst=None, D=2, r=None, cap=0, act=0, residual=1, attr_mode=0, seed=0):
@@ -172,3 +183,69 @@ def test_forward_workload_rows(env, k):
     err = rel_err(got[rows], ref[rows])
     print("E=%d err=%.3e" % (c.col.size, err))
     assert err <= TOL[c.dtype]
+
+
+GRAD_KEYS = ("dW1", "db1", "dW2", "db2", "dW3", "db3", "dWr", "dbr")
+
+
+def _check_backward(c, label):
+    namb = c.clear_ambiguous_outputs()
+    c.forward()
+    gh, grads = c.backward()
+    ref = c.oracle_backward()
+    errs = {"grad_h": rel_err(gh, ref["grad_h"])}
+    for k in GRAD_KEYS:
+        errs[k] = rel_err(grads[k], ref[k], ref["allow"].get(k))
+    print(label, "ambiguous-y=%d" % namb, " ".join("%s=%.2e" % kv for kv in errs.items()))
+    for k, e in errs.items():
+        assert e <= TOL[c.dtype], (k, e)
+
+
+@pytest.mark.parametrize("name", sorted(FWD_CASES))
+def test_backward_parity(env, name):
+    kw = FWD_CASES[name]
+    announce("backward", name)
+    c = random_case(env, seed=zlib.crc32(name.encode()) % 1000, **kw)
+    _check_backward(c, "E=%d" % c.col.size)
+
+
+def test_backward_no_edges(env):
+    announce("backward no edges")
+    c = random_case(env, "bf16_64", n=50, r=1e-6)
+    _check_backward(c, "E=0")
+
+
+def test_backward_accumulate_and_determinism(env):
+    announce("backward accumulate")
+    dm, lib, torch = env
+    c = random_case(env, "bf16_64", n=2000, seed=11)
+    c.forward()
+    gh1, g1 = c.backward()
+    gh2, g2 = c.backward()
+    for k in GRAD_KEYS:
+        assert np.array_equal(g1[k], g2[k]), k
+    assert np.array_equal(gh1, gh2)
+    dev = torch.device("cuda", 0)
+    grads = {k: torch.from_numpy(v).to(dev) for k, v in g1.items()}
+    lib.dsmp_nnconv_backward(c.desc, c.packed, c.g, c.t_attr, c.t_h, c.saved, torch.from_numpy(c.G).to(dev),
+                             grads=grads, flags=dm.GRAD_ACCUMULATE)
+    torch.cuda.synchronize()
+    for k in GRAD_KEYS:
+        assert np.array_equal(grads[k].cpu().numpy(), (g1[k] + g1[k]).astype(np.float32)), k
+
+
+@pytest.mark.parametrize("k", [1, 2])
+def test_backward_workload_full(env, k):
+    announce("backward workload", k)
+    c = workload_case(env, k)
+    _check_backward(c, "E=%d" % c.col.size)
+
+
+@pytest.mark.parametrize("k", [3, 4, 5])
+def test_backward_workload_rows(env, k):
+    """Sparse upstream gradient (rows only): every gradient is an exact sum
+    over those rows' edges, while the GPU runs the full-size kernels."""
+    announce("backward workload rows", k)
+    rows = np.sort(np.random.default_rng(k + 10).choice(make_config(k).n_dst, 128, replace=False))
+    c = workload_case(env, k, rows=rows)
+    _check_backward(c, "E=%d" % c.col.size)
