@@ -1,0 +1,251 @@
+"""Benchmark of the DS-MPNN hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic input,
+all inputs resident in HBM before timing starts:
+  sample the nodes (every part of the workload), gather their positions,
+  attributes and latent features, build the radius graph (count, cap, CSR,
+  transpose), then for every layer pack its parameters and run the NNConv
+  forward, then the backward through every layer in reverse (the feature
+  gradient of layer l is the upstream gradient of layer l-1).
+
+Default workload: the Darcy-like case -- 8,192 nodes sampled from a 256x256
+grid, r = 0.04, d = 64, kernel MLP 6->128->128->4096, 4 layers, bf16 operands
+with fp32 accumulation.  Prints one JSON line.
+
+value = edges/s = E * layers / (seconds per step), i.e. edge-layer passes
+(forward + backward) per second, sampling and graph build included.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA (2.5 PFLOP/s published)
+PEAK_FP32_TFLOPS = 157.3       # MI355X fp32 (matrix and vector)
+METRIC = "edges/sec and achieved TFLOP/s per NNConv layer fwd+bwd on 1 MI355X"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=1536,
+                    help="destination rows of the oracle's timed layer sample")
+    return ap.parse_args()
+
+
+def per_edge_flops(w):
+    """Nominal method work per retained edge (one kernel evaluation, eq. (1))."""
+    d, H1, H2, de = w.d, w.H1, w.H2, w.de
+    return {
+        "edge_fwd": 2 * (de * H1 + H1 * H2) + 2 * (H2 + 1) * d * d,
+        "edge_dh": 2 * (H2 + 1) * d * d,
+        "dz": 2 * H2 * d * d + 2 * H1 * H2,
+        "dW3": 2 * H2 * d * d,
+        "dW2": 2 * H1 * H2,
+        "fwd+bwd": (8 * H2 + 6) * d * d + 6 * H1 * H2 + 4 * de * H1,
+    }
+
+
+class Pipeline:
+    def __init__(self, w, lib, dm, torch):
+        self.w, self.lib, self.dm, self.torch = w, lib, dm, torch
+        dev = torch.device("cuda", 0)
+        tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        self.tdt = tdt
+        self.parts = []
+        for p in w.parts:
+            self.parts.append(dict(
+                M=p.pos.shape[0], s=p.s, seed=p.seed,
+                pos=torch.from_numpy(p.pos).to(dev), attr=torch.from_numpy(p.attr).to(dev),
+                h=torch.from_numpy(p.h).to(dev).to(tdt),
+                idx=torch.empty(p.s, dtype=torch.int32, device=dev)))
+        n_src, n_dst, d = w.n_src, w.n_dst, w.d
+        self.pos = torch.empty(n_src, w.D, dtype=torch.float32, device=dev)
+        self.attr = torch.empty(n_src, w.D + 1, dtype=torch.float32, device=dev)
+        self.h = [torch.empty(n_src, d, dtype=tdt, device=dev) for _ in range(w.layers + 1)]
+        self.desc = dm.layer_desc(w.D, d, w.H1, w.H2, dm.BF16 if w.dtype == "bf16" else dm.F32)
+        self.params = [{k: torch.from_numpy(v).to(dev) for k, v in P.items()} for P in w.params]
+        self.G = torch.from_numpy(w.grad_out).to(dev)
+        # size the graph once (E is fixed for this input) and preallocate everything
+        self.sample_and_gather()
+        E = lib.dsmp_radius_graph_count(self.pos, n_dst, w.r, w.cap, w.cap_mode)
+        self.graph = lib.dsmp_radius_graph_build(self.pos, n_dst, w.r, w.cap, w.cap_mode, capacity=E)
+        self.E = E
+        sb, fb, bb = lib.dsmp_nnconv_workspace(self.desc, self.graph)
+        self.saved = [torch.empty(max(sb, 256), dtype=torch.uint8, device=dev) for _ in range(w.layers)]
+        self.fws = torch.empty(max(fb, 256), dtype=torch.uint8, device=dev)
+        self.bws = torch.empty(max(bb, 256), dtype=torch.uint8, device=dev)
+        self.packed = [lib.dsmp_nnconv_pack(self.desc, P) for P in self.params]
+        self.out = [torch.empty(n_dst, d, dtype=torch.float32, device=dev) for _ in range(w.layers)]
+        self.grad_h = [torch.empty(n_src, d, dtype=torch.float32, device=dev) for _ in range(w.layers)]
+        f32 = dict(dtype=torch.float32, device=dev)
+        de, H1, H2 = w.de, w.H1, w.H2
+        self.grads = [{"dW1": torch.empty(H1, de, **f32), "db1": torch.empty(H1, **f32),
+                       "dW2": torch.empty(H2, H1, **f32), "db2": torch.empty(H2, **f32),
+                       "dW3": torch.empty(d * d, H2, **f32), "db3": torch.empty(d * d, **f32),
+                       "dWr": torch.empty(d, d, **f32), "dbr": torch.empty(d, **f32)} for _ in range(w.layers)]
+
+    def sample_and_gather(self):
+        lib = self.lib
+        off = 0
+        for p in self.parts:
+            lib.dsmp_sample_nodes(p["M"], p["s"], p["seed"], out=p["idx"])
+            sl = slice(off, off + p["s"])
+            lib.dsmp_gather_rows(p["pos"], p["idx"], out=self.pos[sl])
+            lib.dsmp_gather_rows(p["attr"], p["idx"], out=self.attr[sl])
+            lib.dsmp_gather_rows(p["h"], p["idx"], out=self.h[0][sl])
+            off += p["s"]
+
+    def step(self):
+        w, lib = self.w, self.lib
+        n_dst = w.n_dst
+        self.sample_and_gather()
+        lib.dsmp_radius_graph_build(self.pos, n_dst, w.r, w.cap, w.cap_mode, capacity=self.E, out=self.graph)
+        for l in range(w.layers):
+            if n_dst < w.n_src:      # halo rows keep their input features at every layer
+                self.h[l + 1][n_dst:].copy_(self.h[0][n_dst:])
+            lib.dsmp_nnconv_pack(self.desc, self.params[l], out=self.packed[l])
+            lib.dsmp_nnconv_forward(self.desc, self.packed[l], self.graph, self.attr, self.h[l],
+                                    h_out=self.out[l], h_out_lp=self.h[l + 1][:n_dst], saved=self.saved[l],
+                                    ws=self.fws)
+        G = self.G
+        for l in reversed(range(w.layers)):
+            lib.dsmp_nnconv_backward(self.desc, self.packed[l], self.graph, self.attr, self.h[l], self.saved[l],
+                                     G, grad_h=self.grad_h[l], grads=self.grads[l], ws=self.bws)
+            G = self.grad_h[l][:n_dst]
+
+
+def cpu_baseline(w, rows_n, E_gpu):
+    """Time the oracle, as it stands, on the host: sampling and the radius
+    graph of the whole workload, and one layer forward+backward on a fixed
+    subset of destination rows (sparse upstream gradient), extrapolated to the
+    step's E * layers."""
+    import numpy as np
+    import oracle
+    from threadpoolctl import threadpool_info
+    t = time.perf_counter()
+    pos, attr, h = [], [], []
+    for p in w.parts:
+        idx = oracle.sampling.sample_nodes(p.pos.shape[0], p.s, p.seed)
+        pos.append(p.pos[idx]); attr.append(p.attr[idx]); h.append(p.h[idx])
+    t_sample = time.perf_counter() - t
+    pos, attr, h = np.concatenate(pos), np.concatenate(attr), np.concatenate(h).astype(np.float64)
+    t = time.perf_counter()
+    rp, col = oracle.radius_graph.radius_graph(pos, w.n_dst, w.r, w.cap, w.cap_mode)
+    t_graph = time.perf_counter() - t
+    rows = np.sort(np.random.default_rng(0).choice(w.n_dst, min(rows_n, w.n_dst), replace=False))
+    E_sub = int(sum(rp[i + 1] - rp[i] for i in rows))
+    G = np.zeros((w.n_dst, w.d))
+    G[rows] = w.grad_out[rows]
+    decide = w.dtype
+    t = time.perf_counter()
+    x = oracle.nnconv.edge_attr(attr, rp, col)
+    oracle.nnconv.forward(w.params[0], x, h, rp, col, w.n_dst, rows=rows, decide=decide)
+    oracle.nnconv.backward(w.params[0], x, h, rp, col, w.n_dst, G, rows=rows, decide=decide)
+    t_layer_sub = time.perf_counter() - t
+    E = int(rp[-1])
+    t_step = t_sample + t_graph + w.layers * t_layer_sub * E / max(E_sub, 1)
+    threads = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
+    return {
+        "value": E * w.layers / t_step, "unit": "edges/s", "cores": int(threads), "kind": "oracle",
+        "sample": ("sampling and radius graph of the whole workload (%.2f s + %.2f s), one layer forward+"
+                   "backward on %d destination rows = %d of %d edges (%.2f s), extrapolated to %d layers; "
+                   "%d BLAS threads, %d cores in affinity; E matches the GPU's: %s"
+                   % (t_sample, t_graph, len(rows), E_sub, E, t_layer_sub, w.layers, threads,
+                      len(os.sched_getaffinity(0)), E == E_gpu)),
+        "seconds": round(t_sample + t_graph + t_layer_sub, 2),
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build runs the hot path on one MI355X "
+              "(one sub-domain's share); --gpus %d is not supported." % max(args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2402_15106_amd as dm
+    from workloads import make_config
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+
+    w = make_config(args.config)
+    lib = dm.Dsmp(0)
+    pipe = Pipeline(w, lib, dm, torch)
+    print("workload %s: n_dst=%d n_src=%d E=%d layers=%d" % (w.name, w.n_dst, w.n_src, pipe.E, w.layers),
+          file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        pipe.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        pipe.step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / args.steps
+    print("timed %d steps: %.3f ms/step" % (args.steps, ms), file=sys.stderr, flush=True)
+
+    # per-kernel durations: HIP events recorded by the library on its stream
+    lib.dsmp_profile_enable(True)
+    lib.dsmp_profile_reset()
+    for _ in range(args.steps):
+        pipe.step()
+    prof = lib.dsmp_profile_read()
+    lib.dsmp_profile_enable(False)
+
+    E, L = pipe.E, w.layers
+    fl = per_edge_flops(w)
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_TFLOPS
+    kernels = {}
+    for name, (tot, n) in prof.items():
+        if n == 0:
+            continue
+        avg = tot / n
+        ent = {"ms_avg": round(avg, 5), "launches_per_step": n / args.steps,
+               "ms_per_step": round(tot / args.steps, 4)}
+        if name in fl:
+            tf = E * fl[name] / (avg * 1e-3) / 1e12
+            ent["tflops"] = round(tf, 2)
+            ent["frac_peak"] = round(tf / peak, 4)
+        kernels[name] = ent
+    mfma = {k: v for k, v in kernels.items() if "tflops" in v}
+    dom = max(mfma, key=lambda k: mfma[k]["ms_per_step"])
+    dk = kernels[dom]
+    achieved = dk["tflops"]
+    flops_step = L * (E * fl["fwd+bwd"] + w.n_dst * 6 * w.d * w.d)
+    res = {
+        "metric": METRIC,
+        "value": round(E * L / (ms * 1e-3), 1),
+        "unit": "edges/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded stand-in for the paper's mesh datasets)",
+        "config": {"workload": "%s: %d nodes sampled from %d candidates, radius %.3g, cap %s, d=%d, kernel MLP "
+                               "%d->%d->%d->%d, %d layers, sample+graph+forward+backward per step"
+                               % (w.name, w.n_dst, sum(p.pos.shape[0] for p in w.parts), w.r, w.cap or "none",
+                                  w.d, w.de, w.H1, w.H2, w.d * w.d, L),
+                   "n_dst": w.n_dst, "n_src": w.n_src, "edges": E, "layers": L, "d": w.d, "h1": w.H1,
+                   "h2": w.H2},
+        "tflops_step": round(flops_step / (ms * 1e-3) / 1e12, 2),
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "flops_per_launch": E * fl[dom], "ms_per_launch": dk["ms_avg"]},
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_rows, E)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

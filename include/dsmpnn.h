@@ -234,6 +234,35 @@ dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_desc* desc, co
                                  float* grad_h, const dsmp_layer_grads* grads, int32_t flags,
                                  void* ws, size_t ws_bytes);
 
+/* ------------------------------------------------------------ kernel timing
+ * Opt-in timing of the library's kernels with HIP events, for benchmarks.
+ * While enabled, every launch (or launch group) of a kernel class below is
+ * bracketed by a pair of hipEvents recorded on the bound stream; the events
+ * are created on first use and owned by the handle.  dsmp_profile_read
+ * SYNCHRONISES on the outstanding events, adds their elapsed times to the
+ * class totals and returns the total milliseconds and the number of
+ * bracketed launches since the last reset.  Disabled (the default) the calls
+ * record nothing. */
+enum {
+  DSMP_K_SAMPLE = 0,    /* dsmp_sample_nodes */
+  DSMP_K_GATHER = 1,    /* dsmp_gather_rows */
+  DSMP_K_GRAPH = 2,     /* dsmp_radius_graph_build (whole call) */
+  DSMP_K_EDGE_FWD = 3,  /* forward edge contraction kernel */
+  DSMP_K_NODE_FWD = 4,  /* forward node update kernel */
+  DSMP_K_NODE_BWD = 5,  /* backward node, root and db3 kernels */
+  DSMP_K_EDGE_DH = 6,   /* feature-gradient edge contraction kernel */
+  DSMP_K_DH_FINAL = 7,  /* feature-gradient assembly kernel */
+  DSMP_K_DZ = 8,        /* dz / da2 / da1 kernel */
+  DSMP_K_DW3 = 9,       /* dW3 split-over-edges kernel */
+  DSMP_K_DW2 = 10,      /* dW2 split-over-edges kernel */
+  DSMP_K_DW1 = 11,      /* dW1 kernel */
+  DSMP_K_REDUCE = 12,   /* fixed-order gradient reductions */
+  DSMP_K_COUNT = 13
+};
+dsmp_status dsmp_profile_enable(dsmp_handle* h, int enable);
+dsmp_status dsmp_profile_reset(dsmp_handle* h);
+dsmp_status dsmp_profile_read(dsmp_handle* h, int kernel_class, double* total_ms, int64_t* launches);
+
 #ifdef __cplusplus
 }
 #endif

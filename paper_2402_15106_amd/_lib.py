@@ -31,7 +31,12 @@ EXPORTED = ["dsmp_version", "dsmp_create", "dsmp_destroy", "dsmp_set_stream", "d
             "dsmp_sample_workspace", "dsmp_sample_nodes", "dsmp_gather_rows",
             "dsmp_radius_graph_workspace", "dsmp_radius_graph_count", "dsmp_radius_graph_build",
             "dsmp_nnconv_packed_bytes", "dsmp_nnconv_pack", "dsmp_nnconv_workspace",
-            "dsmp_nnconv_forward", "dsmp_nnconv_backward"]
+            "dsmp_nnconv_forward", "dsmp_nnconv_backward", "dsmp_profile_enable", "dsmp_profile_reset",
+            "dsmp_profile_read"]
+
+# kernel classes of the opt-in timing (dsmp_profile_*)
+KERNEL_CLASSES = ["sample", "gather", "graph", "edge_fwd", "node_fwd", "node_bwd", "edge_dh", "dh_final",
+                  "dz", "dW3", "dW2", "dW1", "reduce"]
 
 
 class DsmpError(RuntimeError):
@@ -92,6 +97,10 @@ _SIG = {
     "dsmp_nnconv_backward": (ctypes.c_int, [_P, ctypes.POINTER(LayerDesc), _P, ctypes.POINTER(CGraph), _P, _P,
                                             _P, ctypes.c_size_t, _P, _P, ctypes.POINTER(LayerGrads),
                                             ctypes.c_int32, _P, ctypes.c_size_t]),
+    "dsmp_profile_enable": (ctypes.c_int, [_P, ctypes.c_int]),
+    "dsmp_profile_reset": (ctypes.c_int, [_P]),
+    "dsmp_profile_read": (ctypes.c_int, [_P, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                         ctypes.POINTER(ctypes.c_int64)]),
 }
 
 _lib = None
@@ -183,6 +192,22 @@ class Dsmp:
             buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
             self._ws[key] = buf
         return buf
+
+    # ------------------------------------------------------------ timing
+    def dsmp_profile_enable(self, on: bool = True):
+        self._check(self.lib.dsmp_profile_enable(self.h, int(bool(on))), self.h)
+
+    def dsmp_profile_reset(self):
+        self._check(self.lib.dsmp_profile_reset(self.h), self.h)
+
+    def dsmp_profile_read(self) -> dict:
+        """{kernel class: (total ms, launches)} since the last reset (synchronises)."""
+        out = {}
+        for i, name in enumerate(KERNEL_CLASSES):
+            ms, n = ctypes.c_double(), ctypes.c_int64()
+            self._check(self.lib.dsmp_profile_read(self.h, i, ctypes.byref(ms), ctypes.byref(n)), self.h)
+            out[name] = (ms.value, n.value)
+        return out
 
     # ------------------------------------------------------------ sampling
     def dsmp_sample_nodes(self, M: int, s: int, seed: int, out: Optional[torch.Tensor] = None):

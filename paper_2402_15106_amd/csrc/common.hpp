@@ -5,6 +5,7 @@
 #include <stdint.h>
 #include <stddef.h>
 #include <string>
+#include <vector>
 #include <cstdio>
 #include <cstdarg>
 
@@ -14,9 +15,47 @@ struct dsmp_handle {
   int device = 0;
   hipStream_t stream = nullptr;
   std::string err;
+  // kernel timing (opt-in)
+  struct Mark {
+    int cls;
+    hipEvent_t a, b;
+  };
+  bool prof = false;
+  std::vector<Mark> pending;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> pool;
+  double tot_ms[DSMP_K_COUNT] = {};
+  int64_t launches[DSMP_K_COUNT] = {};
 };
 
 namespace dsmp {
+
+// Brackets the launches issued in its scope with a pair of events when the
+// handle's timing is on.
+struct ProfScope {
+  dsmp_handle* h;
+  int idx = -1;
+  ProfScope(dsmp_handle* hh, int cls) : h(hh) {
+    if (!h || !h->prof) return;
+    std::pair<hipEvent_t, hipEvent_t> ev;
+    if (!h->pool.empty()) {
+      ev = h->pool.back();
+      h->pool.pop_back();
+    } else if (hipEventCreate(&ev.first) != hipSuccess || hipEventCreate(&ev.second) != hipSuccess) {
+      return;
+    }
+    if (hipEventRecord(ev.first, h->stream) != hipSuccess) {
+      h->pool.push_back(ev);
+      return;
+    }
+    h->pending.push_back({cls, ev.first, ev.second});
+    idx = (int)h->pending.size() - 1;
+  }
+  void end() {
+    if (idx >= 0) (void)hipEventRecord(h->pending[idx].b, h->stream);
+    idx = -1;
+  }
+  ~ProfScope() { end(); }
+};
 
 inline dsmp_status fail(dsmp_handle* h, dsmp_status st, const char* fmt, ...) {
   char buf[512];

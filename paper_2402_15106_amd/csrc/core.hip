@@ -130,7 +130,47 @@ extern "C" dsmp_status dsmp_create(dsmp_handle** out, int device) {
 }
 
 extern "C" dsmp_status dsmp_destroy(dsmp_handle* h) {
+  if (!h) return DSMP_OK;
+  for (auto& m : h->pending) { (void)hipEventDestroy(m.a); (void)hipEventDestroy(m.b); }
+  for (auto& e : h->pool) { (void)hipEventDestroy(e.first); (void)hipEventDestroy(e.second); }
   delete h;
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_profile_enable(dsmp_handle* h, int enable) {
+  if (!h) return DSMP_INVALID_ARG;
+  h->prof = enable != 0;
+  return DSMP_OK;
+}
+
+static dsmp_status drain_marks(dsmp_handle* h) {
+  for (auto& m : h->pending) {
+    DSMP_HIP(h, hipEventSynchronize(m.b));
+    float ms = 0.0f;
+    DSMP_HIP(h, hipEventElapsedTime(&ms, m.a, m.b));
+    h->tot_ms[m.cls] += ms;
+    h->launches[m.cls] += 1;
+    h->pool.push_back({m.a, m.b});
+  }
+  h->pending.clear();
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_profile_reset(dsmp_handle* h) {
+  if (!h) return DSMP_INVALID_ARG;
+  dsmp_status st = drain_marks(h);
+  for (int k = 0; k < DSMP_K_COUNT; ++k) { h->tot_ms[k] = 0.0; h->launches[k] = 0; }
+  return st;
+}
+
+extern "C" dsmp_status dsmp_profile_read(dsmp_handle* h, int cls, double* total_ms, int64_t* launches) {
+  if (!h) return DSMP_INVALID_ARG;
+  DSMP_CHECK(h, cls >= 0 && cls < DSMP_K_COUNT && total_ms && launches, DSMP_INVALID_ARG,
+             "bad profile query");
+  dsmp_status st = drain_marks(h);
+  if (st != DSMP_OK) return st;
+  *total_ms = h->tot_ms[cls];
+  *launches = h->launches[cls];
   return DSMP_OK;
 }
 
@@ -239,6 +279,7 @@ extern "C" dsmp_status dsmp_sample_nodes(dsmp_handle* h, int64_t M, int64_t s, u
   DSMP_CHECK(h, M <= INT32_MAX, DSMP_UNSUPPORTED, "M exceeds int32 range");
   if (s == 0) return DSMP_OK;
   DSMP_CHECK(h, idx_out != nullptr, DSMP_INVALID_ARG, "idx_out is NULL");
+  ProfScope prof(h, DSMP_K_SAMPLE);
   if (s == M) {
     hipLaunchKernelGGL(k_iota, dim3(ceil_div(M, 256)), dim3(256), 0, h->stream, idx_out, M);
     DSMP_LAUNCHED(h, "iota");
@@ -288,6 +329,7 @@ extern "C" dsmp_status dsmp_gather_rows(dsmp_handle* h, const void* src, int64_t
              "bad gather sizes");
   if (n == 0) return DSMP_OK;
   DSMP_CHECK(h, src && idx && dst, DSMP_INVALID_ARG, "gather pointer is NULL");
+  ProfScope prof(h, DSMP_K_GATHER);
   int64_t words = row_bytes / 4;
   unsigned g = ceil_div(n * words, 256);
   if (g > 8192) g = 8192;

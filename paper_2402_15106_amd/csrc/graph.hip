@@ -485,6 +485,7 @@ extern "C" dsmp_status dsmp_radius_graph_build(dsmp_handle* h, const dsmp_graph_
   GraphWs w = carve_graph_ws(ws, q->n_src, q->n_dst, &need);
   DSMP_CHECK(h, ws != nullptr && ws_bytes >= need, DSMP_WORKSPACE_TOO_SMALL,
              "graph workspace needs %zu bytes", need);
+  ProfScope prof(h, DSMP_K_GRAPH);
   int64_t E;
   uint32_t maxraw;
   st = count_phase(h, q, w, g->row_ptr, &E, &maxraw);

@@ -742,6 +742,7 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
     using S = DzShape<T, DL, H1, H2>;
     auto kz = k_bwd_dz<T, DL, H1, H2>;
     if ((st = set_lds(h, kz, S::LDS)) != DSMP_OK) return st;
+    ProfScope prof(h, DSMP_K_DZ);
     hipLaunchKernelGGL(kz, dim3(ceil_div(dz.E, S::TILE)), dim3(256), S::LDS, s, dz);
     DSMP_LAUNCHED(h, "dz");
   }
@@ -749,6 +750,7 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
     using S = W3Shape<T, DL, H2>;
     auto k3 = k_bwd_dW3<T, DL, H2>;
     if ((st = set_lds(h, k3, S::LDS)) != DSMP_OK) return st;
+    ProfScope prof(h, DSMP_K_DW3);
     hipLaunchKernelGGL(k3, dim3((DL / S::PB) * w3.nchunk), dim3(256), S::LDS, s, w3);
     DSMP_LAUNCHED(h, "dW3");
   }
@@ -758,6 +760,7 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
     if ((st = set_lds(h, k2, S::LDS)) != DSMP_OK) return st;
     int nchunk = (int)((w2.E + w2.per_chunk - 1) / w2.per_chunk);
     if (nchunk < 1) nchunk = 1;
+    ProfScope prof(h, DSMP_K_DW2);
     hipLaunchKernelGGL(k2, dim3(nchunk * S::NSPLIT), dim3(256), S::LDS, s, w2);
     DSMP_LAUNCHED(h, "dW2");
   }
@@ -837,6 +840,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   const int64_t E = g->n_edges, n_dst = g->n_dst, n_src = g->n_src;
 
   // node pre-pass, root grads, db3 partials
+  ProfScope prof_node(h, DSMP_K_NODE_BWD);
   BNodeArgs na{n_dst, g->row_ptr, grad_out, reinterpret_cast<const float*>(sv + sl.y),
                reinterpret_cast<const float*>(pk + L.wr), w.ybar, w.gT, w.gF, w.dh_node, d.act, d.residual};
   if (d.dtype == DSMP_BF16) {
@@ -848,6 +852,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
     if (d.d == 64) launch_node_kernels<float, 64>(h, na, n_dst, w, hin, g->row_ptr, g->col);
   }
   DSMP_LAUNCHED(h, "backward node kernels");
+  prof_node.end();
 
   // feature gradient through the edges (edge contraction in source order)
   EdgeArgs ea{};
@@ -862,6 +867,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   if (n_src > 0) {
     unsigned grid = ceil_div(n_src * d.d, 256);
     if (grid > 4096) grid = 4096;
+    ProfScope prof(h, DSMP_K_DH_FINAL);
     hipLaunchKernelGGL(k_bwd_dh_final, dim3(grid), dim3(256), 0, s, n_src, n_dst, d.d, g->csc_ptr, w.dh_direct,
                        w.dh_part, w.dh_node, grad_h);
     DSMP_LAUNCHED(h, "grad_h");
@@ -875,6 +881,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
     if ((st = dispatch_edge_grads(h, d, dz, w3, w2)) != DSMP_OK) return st;
     hipLaunchKernelGGL(k_jof, dim3(ceil_div(d.h1, 256)), dim3(256), 0, s, w.jof, d.h1, d.dtype == DSMP_BF16);
     int n1 = (int)((E + w.pc1 - 1) / w.pc1);
+    ProfScope prof(h, DSMP_K_DW1);
     if (d.h1 == 64)
       hipLaunchKernelGGL((k_bwd_dW1<64>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr, d.dim,
                          d.attr_mode, de, w.da1E, w.jof, w.p_w1);
@@ -899,6 +906,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   const int n2 = E > 0 ? (int)((E + w.pc2 - 1) / w.pc2) : 0;
   const int n1 = E > 0 ? (int)((E + w.pc1 - 1) / w.pc1) : 0;
   const int nr = n_dst > 0 ? w.nr : 0;
+  ProfScope prof_red(h, DSMP_K_REDUCE);
   red(w.p_root, nr, dd + d.d, 0, dd, grads->dWr);
   red(w.p_root, nr, dd + d.d, dd, d.d, grads->dbr);
   red(w.p_db3, nr, dd, 0, dd, grads->db3);

@@ -447,11 +447,13 @@ dsmp_status launch_edge_shape(dsmp_handle* h, int mode, const EdgeArgs& a) {
     auto kern = k_edge_contract<T, DL, H1, H2, MODE_FWD>;
     dsmp_status st = set_lds(h, kern, S::LDS);
     if (st != DSMP_OK) return st;
+    ProfScope prof(h, DSMP_K_EDGE_FWD);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(256), S::LDS, h->stream, a);
   } else {
     auto kern = k_edge_contract<T, DL, H1, H2, MODE_DH>;
     dsmp_status st = set_lds(h, kern, S::LDS);
     if (st != DSMP_OK) return st;
+    ProfScope prof(h, DSMP_K_EDGE_DH);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(256), S::LDS, h->stream, a);
   }
   DSMP_LAUNCHED(h, "edge contraction");
@@ -620,6 +622,7 @@ extern "C" dsmp_status dsmp_nnconv_forward(dsmp_handle* h, const dsmp_layer_desc
                 d.residual};
     unsigned grid = ceil_div(g->n_dst, 256 / d.d);
     if (grid > 2048) grid = 2048;
+    ProfScope prof(h, DSMP_K_NODE_FWD);
     if (d.dtype == DSMP_BF16) {
       if (d.d == 32) hipLaunchKernelGGL((k_fwd_node<__bf16, 32>), dim3(grid), dim3(256), 0, h->stream, na);
       if (d.d == 64) hipLaunchKernelGGL((k_fwd_node<__bf16, 64>), dim3(grid), dim3(256), 0, h->stream, na);
