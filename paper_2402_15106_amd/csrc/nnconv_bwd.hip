@@ -217,7 +217,7 @@ struct DzShape {
 };
 
 template <typename T, int DL, int H1, int H2>
-__global__ __launch_bounds__(256, 1) void k_bwd_dz(DzArgs a) {
+__global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) void k_bwd_dz(DzArgs a) {
   using S = DzShape<T, DL, H1, H2>;
   using M = MT<T>;
   using frag = typename M::frag;
@@ -363,6 +363,42 @@ __global__ __launch_bounds__(256, 1) void k_bwd_dz(DzArgs a) {
   }
 }
 
+// Copy a chunk of ECH edge rows of a [E][W] array (layer dtype, permuted
+// register order) into LDS transposed to [W][ECH] (rows still in the permuted
+// order), four edges per thread: 8-byte (bf16) or 16-byte (fp32) LDS writes,
+// zero rows past e_end.  ROWB is the LDS row pitch in bytes.
+template <typename T, int W, int ECH, int ROWB>
+__device__ __forceinline__ void stage_transposed(const unsigned char* __restrict__ src, int64_t eb, int64_t e_end,
+                                                 unsigned char* __restrict__ dstl) {
+  constexpr int ESZ = sizeof(T), KPU = 16 / ESZ, EQ = ECH / 4, NU = EQ * (W / KPU);
+  for (int u = threadIdx.x; u < NU; u += 256) {
+    const int eq = u % EQ, kg = u / EQ;
+    uint4 v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t e = eb + 4 * eq + i;
+      v[i] = e < e_end ? *reinterpret_cast<const uint4*>(src + ((size_t)e * W) * ESZ + kg * 16) : make_uint4(0, 0, 0, 0);
+    }
+    const uint32_t* d0 = reinterpret_cast<const uint32_t*>(&v[0]);
+    const uint32_t* d1 = reinterpret_cast<const uint32_t*>(&v[1]);
+    const uint32_t* d2 = reinterpret_cast<const uint32_t*>(&v[2]);
+    const uint32_t* d3 = reinterpret_cast<const uint32_t*>(&v[3]);
+    if constexpr (ESZ == 2) {
+#pragma unroll
+      for (int w = 0; w < 8; ++w) {
+        const int sh = (w & 1) * 16, dw = w >> 1;
+        const uint32_t lo = ((d0[dw] >> sh) & 0xFFFFu) | (((d1[dw] >> sh) & 0xFFFFu) << 16);
+        const uint32_t hi = ((d2[dw] >> sh) & 0xFFFFu) | (((d3[dw] >> sh) & 0xFFFFu) << 16);
+        *reinterpret_cast<uint2*>(dstl + (kg * 8 + w) * ROWB + 4 * eq * ESZ) = make_uint2(lo, hi);
+      }
+    } else {
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        *reinterpret_cast<uint4*>(dstl + (kg * 4 + w) * ROWB + 4 * eq * ESZ) = make_uint4(d0[w], d1[w], d2[w], d3[w]);
+    }
+  }
+}
+
 // ------------------------------------------------------------ dW3 (split over edges)
 
 struct W3Args {
@@ -391,7 +427,7 @@ struct W3Shape {
 };
 
 template <typename T, int DL, int H2>
-__global__ __launch_bounds__(256, 1) void k_bwd_dW3(W3Args a) {
+__global__ __launch_bounds__(256, 2) void k_bwd_dW3(W3Args a) {
   using S = W3Shape<T, DL, H2>;
   using M = MT<T>;
   using frag = typename M::frag;
@@ -420,27 +456,20 @@ __global__ __launch_bounds__(256, 1) void k_bwd_dW3(W3Args a) {
 
   for (int64_t eb = e_begin; eb < e_end; eb += ECH) {
     __syncthreads();
-    // z chunk, transposed to [k][e] with the permutation undone
-    constexpr int ZU = H2 * ESZ / 16;   // 16-byte units per edge row
-    for (int u = tid; u < ECH * ZU; u += 256) {
-      const int el = u / ZU, c16 = u % ZU;
-      const int64_t e = eb + el;
-      const uint4 raw = e < e_end ? *reinterpret_cast<const uint4*>(a.zE + ((size_t)e * H2) * ESZ + c16 * 16)
-                                  : make_uint4(0, 0, 0, 0);
-      const T* v = reinterpret_cast<const T*>(&raw);
+    // z chunk transposed to [kk][e] (kk = stored order; undone at the output)
+    stage_transposed<T, H2, ECH, S::ZROW>(a.zE, eb, e_end, zl);
+    // g chunk transposed to [q][e], four edges x four columns per thread
+    for (int u = tid; u < (ECH / 4) * (DL / 4); u += 256) {
+      const int eq = u % (ECH / 4), q4 = u / (ECH / 4);
+      f32x4 v[4];
 #pragma unroll
-      for (int w = 0; w < 16 / ESZ; ++w) {
-        const int k = kperm<T>(c16 * (16 / ESZ) + w);
-        *reinterpret_cast<T*>(zl + k * S::ZROW + el * ESZ) = v[w];
+      for (int i = 0; i < 4; ++i) {
+        const int64_t e = eb + 4 * eq + i;
+        v[i] = e < e_end ? *reinterpret_cast<const f32x4*>(a.gF + (size_t)a.dst[e] * DL + q4 * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
       }
-    }
-    for (int u = tid; u < ECH * (DL / 4); u += 256) {
-      const int el = u / (DL / 4), q4 = u % (DL / 4);
-      const int64_t e = eb + el;
-      f32x4 v = {0.f, 0.f, 0.f, 0.f};
-      if (e < e_end) v = *reinterpret_cast<const f32x4*>(a.gF + (size_t)a.dst[e] * DL + q4 * 4);
 #pragma unroll
-      for (int w = 0; w < 4; ++w) gl[(q4 * 4 + w) * S::FROW + el] = v[w];
+      for (int w = 0; w < 4; ++w)
+        *reinterpret_cast<f32x4*>(gl + (q4 * 4 + w) * S::FROW + 4 * eq) = f32x4{v[0][w], v[1][w], v[2][w], v[3][w]};
     }
     for (int u = tid; u < ECH * S::PB; u += 256) {
       const int el = u / S::PB, pp = u % S::PB;
@@ -478,9 +507,16 @@ __global__ __launch_bounds__(256, 1) void k_bwd_dW3(W3Args a) {
     for (int kk = 0; kk < S::KT_W; ++kk)
 #pragma unroll
       for (int a4 = 0; a4 < 4; ++a4) {
-        const int k = (kt0 + kk) * 32 + 8 * a4 + 4 * hh;
-        *reinterpret_cast<f32x4*>(out + ((size_t)p * DL + q) * H2 + k) =
-            f32x4{acc[kk][qq][4 * a4], acc[kk][qq][4 * a4 + 1], acc[kk][qq][4 * a4 + 2], acc[kk][qq][4 * a4 + 3]};
+        // tile rows are stored-order positions; map them back to k
+        const int r = (kt0 + kk) * 32 + 8 * a4 + 4 * hh;
+        float* o = out + ((size_t)p * DL + q) * H2;
+        if constexpr (EPL == 8) {
+          *reinterpret_cast<f32x4*>(o + kperm<T>(r)) =
+              f32x4{acc[kk][qq][4 * a4], acc[kk][qq][4 * a4 + 1], acc[kk][qq][4 * a4 + 2], acc[kk][qq][4 * a4 + 3]};
+        } else {
+#pragma unroll
+          for (int b = 0; b < 4; ++b) o[kperm<T>(r + b)] = acc[kk][qq][4 * a4 + b];
+        }
       }
   }
 }
@@ -534,23 +570,8 @@ __global__ __launch_bounds__(256, 1) void k_bwd_dW2(W2Args a) {
   float bsum = 0.0f;
   for (int64_t eb = e_begin; eb < e_end; eb += ECH) {
     __syncthreads();
-    constexpr int DU = H2 * ESZ / 16, ZU = H1 * ESZ / 16;
-    for (int u = tid; u < ECH * (DU + ZU); u += 256) {
-      const bool isd = u < ECH * DU;
-      const int uu = isd ? u : u - ECH * DU;
-      const int W = isd ? DU : ZU;
-      const int el = uu / W, c16 = uu % W;
-      const int64_t e = eb + el;
-      const unsigned char* srcp = isd ? a.da2E + (size_t)e * H2 * ESZ : a.z1E + (size_t)e * H1 * ESZ;
-      const uint4 raw = e < e_end ? *reinterpret_cast<const uint4*>(srcp + c16 * 16) : make_uint4(0, 0, 0, 0);
-      const T* v = reinterpret_cast<const T*>(&raw);
-      unsigned char* base = isd ? dl : zl;
-#pragma unroll
-      for (int w = 0; w < 16 / ESZ; ++w) {
-        const int k = kperm<T>(c16 * (16 / ESZ) + w);
-        *reinterpret_cast<T*>(base + k * S::ROW + el * ESZ) = v[w];
-      }
-    }
+    stage_transposed<T, H2, ECH, S::ROW>(a.da2E, eb, e_end, dl);
+    stage_transposed<T, H1, ECH, S::ROW>(a.z1E, eb, e_end, zl);
     __syncthreads();
     if (split == 0 && tid < H2)
       for (int el = 0; el < ECH; ++el) bsum += to_f(*reinterpret_cast<const T*>(dl + tid * S::ROW + el * ESZ));
@@ -569,18 +590,19 @@ __global__ __launch_bounds__(256, 1) void k_bwd_dW2(W2Args a) {
     }
   }
   float* out = a.part + (size_t)chunk * (H2 * H1 + H2);
+  // tile rows and columns are stored-order positions; map them back to (k, j)
 #pragma unroll
   for (int jj = 0; jj < S::JT_W; ++jj) {
-    const int j = (jt0 + jj) * 32 + l32;
+    const int j = kperm<T>((jt0 + jj) * 32 + l32);
 #pragma unroll
     for (int kk = 0; kk < S::KT_W; ++kk)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int k = (kt0 + kk) * 32 + 8 * (i / 4) + 4 * hh + (i % 4);
+        const int k = kperm<T>((kt0 + kk) * 32 + 8 * (i / 4) + 4 * hh + (i % 4));
         out[(size_t)k * H1 + j] = acc[kk][jj][i];
       }
   }
-  if (split == 0 && tid < H2) out[H2 * H1 + tid] = bsum;
+  if (split == 0 && tid < H2) out[H2 * H1 + kperm<T>(tid)] = bsum;
 }
 
 // ------------------------------------------------------------ dW1 / db1 (split over edges)
@@ -590,7 +612,8 @@ __global__ __launch_bounds__(256) void k_bwd_dW1(int64_t E, int64_t per_chunk, c
                                                  const int32_t* __restrict__ dst, const float* __restrict__ node_attr,
                                                  int dim, int attr_mode, int de, const float* __restrict__ da1E,
                                                  const int* __restrict__ jof, float* __restrict__ part) {
-  constexpr int SUB = 256 / H1;
+  constexpr int SUB = 256 / H1, XB = 256;
+  __shared__ float xs[XB][9];
   __shared__ float red[SUB][H1][9];
   const int kk = threadIdx.x % H1, sub = threadIdx.x / H1;
   const int64_t e0 = (int64_t)blockIdx.x * per_chunk;
@@ -599,13 +622,24 @@ __global__ __launch_bounds__(256) void k_bwd_dW1(int64_t E, int64_t per_chunk, c
   float acc[9];
 #pragma unroll
   for (int c = 0; c < 9; ++c) acc[c] = 0.0f;
-  for (int64_t e = e0 + sub; e < e1; e += SUB) {
-    float x[8];
-    edge_attr(node_attr, dim, attr_mode, dst[e], col[e], x);
-    const float v = da1E[e * H1 + kk];
+  for (int64_t eb = e0; eb < e1; eb += XB) {
+    __syncthreads();
+    {
+      const int64_t e = eb + threadIdx.x;
+      float x[8];
+      if (e < e1) edge_attr(node_attr, dim, attr_mode, dst[e], col[e], x);
 #pragma unroll
-    for (int c = 0; c < 8; ++c) acc[c] += v * x[c];
-    acc[8] += v;
+      for (int c = 0; c < 8; ++c) xs[threadIdx.x][c] = e < e1 ? x[c] : 0.0f;
+      xs[threadIdx.x][8] = e < e1 ? 1.0f : 0.0f;
+    }
+    __syncthreads();
+    const int n = e1 - eb < XB ? (int)(e1 - eb) : XB;
+#pragma unroll 4
+    for (int u = sub; u < n; u += SUB) {
+      const float v = da1E[(eb + u) * H1 + kk];
+#pragma unroll
+      for (int c = 0; c < 9; ++c) acc[c] += v * xs[u][c];
+    }
   }
 #pragma unroll
   for (int c = 0; c < 9; ++c) red[sub][kk][c] = acc[c];
@@ -623,13 +657,28 @@ __global__ __launch_bounds__(256) void k_bwd_dW1(int64_t E, int64_t per_chunk, c
 
 // ------------------------------------------------------------ reductions and finals
 
-// out[x] = [out[x] +] sum_c part[c*stride + off + x], chunks added in order
-__global__ void k_reduce(const float* __restrict__ part, int nchunk, int64_t stride, int64_t off, int64_t n,
-                         float* __restrict__ out, int accumulate) {
-  for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n; x += (int64_t)gridDim.x * blockDim.x) {
+// out[x] = [out[x] +] sum_c part[c*stride + off + x].  A block owns 64
+// consecutive outputs; four thread groups sum the chunks c = g, g+4, ... in
+// order, and the four group sums are added in group order (deterministic).
+__global__ __launch_bounds__(256) void k_reduce(const float* __restrict__ part, int nchunk, int64_t stride,
+                                                int64_t off, int64_t n, float* __restrict__ out, int accumulate) {
+  __shared__ float sh[4][64];
+  const int c0 = threadIdx.x & 63, g = threadIdx.x >> 6;
+  for (int64_t x0 = (int64_t)blockIdx.x * 64; x0 < n; x0 += (int64_t)gridDim.x * 64) {
+    const int64_t x = x0 + c0;
     float s = 0.0f;
-    for (int c = 0; c < nchunk; ++c) s += part[(int64_t)c * stride + off + x];
-    out[x] = accumulate ? out[x] + s : s;
+    if (x < n) {
+      const float* p = part + off + x;
+#pragma unroll 8
+      for (int c = g; c < nchunk; c += 4) s += p[(int64_t)c * stride];
+    }
+    sh[g][c0] = s;
+    __syncthreads();
+    if (g == 0 && x < n) {
+      const float t = ((sh[0][c0] + sh[1][c0]) + sh[2][c0]) + sh[3][c0];
+      out[x] = accumulate ? out[x] + t : t;
+    }
+    __syncthreads();
   }
 }
 
@@ -705,7 +754,7 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   w.dh_part = c.take<float>((size_t)(ceil_div(E, EDGE_TILE) + 1) * 2 * d.d);
   w.da2E = c.take<unsigned char>((size_t)E * d.h2 * esz);
   w.da1E = c.take<float>((size_t)E * d.h1);
-  w.nr = (int)(n_dst > 0 ? (ceil_div(n_dst, 512) < 256 ? ceil_div(n_dst, 512) : 256) : 1);
+  w.nr = (int)(n_dst > 0 ? (ceil_div(n_dst, 32) < 1024 ? ceil_div(n_dst, 32) : 1024) : 1);
   w.pr = n_dst > 0 ? ceil_div(n_dst, w.nr) : 1;
   w.p_root = c.take<float>((size_t)w.nr * (d.d * d.d + d.d));
   w.nb3 = w.nr;
@@ -719,7 +768,7 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   w.pc2 = ((E + w.n2 - 1) / w.n2 + 63) / 64 * 64;
   if (w.pc2 < 64) w.pc2 = 64;
   w.p_w2 = c.take<float>((size_t)w.n2 * (d.h2 * d.h1 + d.h2));
-  w.n1 = (int)(E > 0 ? (ceil_div(E, 1024) < 1024 ? ceil_div(E, 1024) : 1024) : 1);
+  w.n1 = (int)(E > 0 ? (ceil_div(E, 512) < 2048 ? ceil_div(E, 512) : 2048) : 1);
   w.pc1 = E > 0 ? (E + w.n1 - 1) / w.n1 : 1;
   w.p_w1 = c.take<float>((size_t)w.n1 * (d.h1 * de + d.h1));
   w.jof = c.take<int>(d.h1);
@@ -896,8 +945,8 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
 
   // fixed-order reductions into the caller's gradients
   auto red = [&](const float* part, int nchunk, int64_t stride, int64_t off, int64_t n, float* out) {
-    unsigned grid = ceil_div(n, 256);
-    if (grid > 2048) grid = 2048;
+    unsigned grid = ceil_div(n, 64);
+    if (grid > 8192) grid = 8192;
     if (grid == 0) return;
     hipLaunchKernelGGL(k_reduce, dim3(grid), dim3(256), 0, s, part, nchunk, stride, off, n, out, acc);
   };

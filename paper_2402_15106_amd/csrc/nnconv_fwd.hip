@@ -89,8 +89,10 @@ __device__ __forceinline__ void edge_attr(const float* __restrict__ na, int dim,
   }
 }
 
+// Two workgroups per CU when registers and LDS allow (d <= 64), so one
+// workgroup's MFMA chains overlap the other's barriers and epilogues.
 template <typename T, int DL, int H1, int H2, int MODE>
-__global__ __launch_bounds__(256, 1) void k_edge_contract(EdgeArgs a) {
+__global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) void k_edge_contract(EdgeArgs a) {
   using S = Shape<T, DL, H1, H2>;
   using M = MT<T>;
   using frag = typename M::frag;
