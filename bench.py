@@ -42,6 +42,35 @@ def parse():
     return ap.parse_args()
 
 
+TRAFFIC_TABLE = os.path.join(ROOT, "profiles", "darcy256_bf16_traffic.md")
+KERNEL_SOURCES = {
+    "edge_fwd": ["nnconv_fwd.hip", "nnconv.hpp", "common.hpp"],
+    "edge_dh": ["nnconv_fwd.hip", "nnconv.hpp", "common.hpp"],
+    "dz": ["nnconv_bwd.hip", "nnconv.hpp", "common.hpp"],
+    "dW3": ["nnconv_bwd.hip", "nnconv.hpp", "common.hpp"],
+    "dW2": ["nnconv_bwd.hip", "nnconv.hpp", "common.hpp"],
+}
+
+
+def measured_traffic(cls, workload):
+    """HBM bytes per launch of kernel class ``cls`` from the committed
+    rocprofv3 FETCH_SIZE/WRITE_SIZE table, or None when the table covers
+    another workload or the kernel's sources changed since it was taken."""
+    import hashlib
+    if workload != "darcy256-bf16" or cls not in KERNEL_SOURCES or not os.path.exists(TRAFFIC_TABLE):
+        return None
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[cls]:
+        with open(os.path.join(ROOT, "paper_2402_15106_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    digest = h.hexdigest()[:16]
+    for line in open(TRAFFIC_TABLE):
+        cells = [c.strip() for c in line.strip().strip("|").split("|")]
+        if len(cells) == 6 and cells[0] == cls:
+            return int(float(cells[5])) if cells[2] == digest else None
+    return None
+
+
 def per_edge_flops(w):
     """Nominal method work per retained edge (one kernel evaluation, eq. (1))."""
     d, H1, H2, de = w.d, w.H1, w.H2, w.de
@@ -238,7 +267,7 @@ def main():
                    "h2": w.H2},
         "tflops_step": round(flops_step / (ms * 1e-3) / 1e12, 2),
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "frac": round(achieved / peak, 4), "traffic": measured_traffic(dom, w.name),
                      "flops_per_launch": E * fl[dom], "ms_per_launch": dk["ms_avg"]},
         "kernels": kernels,
     }
