@@ -34,6 +34,29 @@ struct MT<float> {
   }
 };
 
+// Eight floats to one bf16x8 fragment with four packed conversions
+// (round to nearest even), or one float to an fp32 fragment.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+template <typename T>
+__device__ __forceinline__ typename MT<T>::frag pack_frag(const float* v);
+
+template <>
+__device__ __forceinline__ bf16x8 pack_frag<__bf16>(const float* v) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bf16x2 b = __builtin_convertvector((f32x2){v[2 * i], v[2 * i + 1]}, bf16x2);
+    w[i] = __builtin_bit_cast(uint32_t, b);
+  }
+  const uint4 u = make_uint4(w[0], w[1], w[2], w[3]);
+  return __builtin_bit_cast(bf16x8, u);
+}
+
+template <>
+__device__ __forceinline__ float pack_frag<float>(const float* v) { return v[0]; }
+
 // A contraction index that comes out of a D tile (rows of the previous
 // product) is consumed as the B operand of the next product straight from
 // registers.  Register order n = 16*c + i of 32-row tile c maps to B element

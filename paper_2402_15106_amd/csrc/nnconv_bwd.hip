@@ -193,7 +193,7 @@ struct DzArgs {
   const int32_t* col;
   const int32_t* dst;
   const unsigned char* h_in;   // [n_src][d]
-  const unsigned char* gT;     // [n_dst][d]
+  const float* gF;             // [n_dst][d] fp32
   const unsigned char* packed;
   PackLayout L;
   const unsigned char* zE;     // [E][h2] permuted order
@@ -216,6 +216,10 @@ struct DzShape {
   static constexpr int LDS = 2 * STAGE + TILE * HROWB;
 };
 
+// dz_e[k] = sum_p h_j[p] sum_q W3[p*d+q][k] g_e[q], accumulated as
+// sum_p W3T[p] (h_j[p] g_e): the scale is folded into the B operand, so the
+// accumulators are touched only by MFMA and the next p's operand is formed
+// while the current products run.
 template <typename T, int DL, int H1, int H2>
 __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) void k_bwd_dz(DzArgs a) {
   using S = DzShape<T, DL, H1, H2>;
@@ -250,12 +254,14 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
       *reinterpret_cast<uint4*>(htile + r * S::HROWB + c * 16) = v;
     }
   }
-  frag gB[NT][S::SKD];
+  // the lane's g_e values (its half of every K step), fp32
+  float gv[NT][S::SKD][EPL];
 #pragma unroll
   for (int t = 0; t < NT; ++t)
 #pragma unroll
     for (int s = 0; s < S::SKD; ++s)
-      gB[t][s] = ld_frag<T>(a.gT + ((size_t)dnode[t] * DL + s * KS + hh * EPL) * ESZ);
+#pragma unroll
+      for (int u = 0; u < EPL; ++u) gv[t][s][u] = a.gF[(size_t)dnode[t] * DL + s * KS + hh * EPL + u];
 
   f32x16 acc[NT][S::KT];
 #pragma unroll
@@ -282,11 +288,30 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
   DZ_GLOAD(0);
   DZ_LSTORE(0);
   __syncthreads();
+  // scaled B operand for p = 0
+  frag Bq[NT][S::SKD];
+  auto form = [&](int p, frag (&B)[NT][S::SKD]) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const float sc = to_f(*reinterpret_cast<const T*>(htile + hrow[t] * S::HROWB + p * ESZ));
+#pragma unroll
+      for (int s = 0; s < S::SKD; ++s) {
+        float v[EPL];
+#pragma unroll
+        for (int u = 0; u < EPL; ++u) v[u] = sc * gv[t][s][u];
+        B[t][s] = pack_frag<T>(v);
+      }
+    }
+  };
+  // Products of W3T[p] (chunk by chunk) against Bq; once a fragment Bq[t][s]
+  // has fed its last product of this p it is re-formed in place for p+1, so
+  // the formation overlaps the remaining products.
+  form(0, Bq);
   for (int p = 0; p < DL; ++p) {
-    float sc[NT];
+    float scn[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t)
-      sc[t] = to_f(*reinterpret_cast<const T*>(htile + hrow[t] * S::HROWB + p * ESZ));
+      scn[t] = p + 1 < DL ? to_f(*reinterpret_cast<const T*>(htile + hrow[t] * S::HROWB + (p + 1) * ESZ)) : 0.0f;
 #pragma unroll
     for (int cc = 0; cc < S::CPP; ++cc) {
       const int c = p * S::CPP + cc;
@@ -295,18 +320,22 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
       if (more) DZ_GLOAD(c + 1);
       const unsigned char* sb = stage0 + buf * S::STAGE;
 #pragma unroll
-      for (int kq = 0; kq < S::KPC; ++kq) {
-        f32x16 C[NT];
+      for (int s = 0; s < S::SKD; ++s) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) C[t] = f32x16{};
-#pragma unroll
-        for (int s = 0; s < S::SKD; ++s) {
+        for (int kq = 0; kq < S::KPC; ++kq) {
           frag A = ld_frag<T>(sb + (kq * 32 + l32) * S::ROWB + (s * KS + hh * EPL) * ESZ);
 #pragma unroll
-          for (int t = 0; t < NT; ++t) C[t] = M::mma(A, gB[t][s], C[t]);
+          for (int t = 0; t < NT; ++t) acc[t][cc * S::KPC + kq] = M::mma(A, Bq[t][s], acc[t][cc * S::KPC + kq]);
         }
+        if (cc == S::CPP - 1) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) acc[t][cc * S::KPC + kq] += sc[t] * C[t];
+          for (int t = 0; t < NT; ++t) {
+            float v[EPL];
+#pragma unroll
+            for (int u = 0; u < EPL; ++u) v[u] = scn[t] * gv[t][s][u];
+            Bq[t][s] = pack_frag<T>(v);
+          }
+        }
       }
       if (more) DZ_LSTORE(buf ^ 1);
       __syncthreads();
@@ -324,12 +353,13 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
 #pragma unroll
     for (int s = 0; s < S::SK2; ++s) {
       const frag zf = ld_frag<T>(a.zE + (e * H2 + s * KS + hh * EPL) * ESZ);
+      float v[EPL];
 #pragma unroll
       for (int u = 0; u < EPL; ++u) {
         const int n = s * EPL + u;
-        const float v = get_el<T>(zf, u) > 0.0f ? acc[t][n / 16][n % 16] : 0.0f;
-        set_el<T>(da2B[s], u, v);
+        v[u] = get_el<T>(zf, u) > 0.0f ? acc[t][n / 16][n % 16] : 0.0f;
       }
+      da2B[s] = pack_frag<T>(v);
       if (valid[t]) *reinterpret_cast<frag*>(a.da2E + (e * H2 + s * KS + hh * EPL) * ESZ) = da2B[s];
     }
 #pragma unroll
@@ -413,25 +443,35 @@ struct W3Args {
   float* part;         // [nchunk][d*d*h2]
 };
 
+// Wave tile of the dW3 product: PW values of p x QTW q-tiles x KTW k-tiles.
+// Small q/k extents give each wave two p's over one q-tile, so one g
+// fragment read from LDS feeds two formed operands.
 template <typename T, int DL, int H2>
 struct W3Shape {
   static constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL, ESZ = sizeof(T);
   static constexpr int QT = DL / 32, KT = H2 / 32;
-  static constexpr int QT_W = QT < 2 ? QT : 2, KT_W = KT < 4 ? KT : 4;
-  static constexpr int WPP = (QT / QT_W) * (KT / KT_W), PB = 4 / WPP;
+  static constexpr int KTW = KT < 4 ? KT : 4;
+  static constexpr bool PAIR = QT * (KT / KTW) <= 2;
+  static constexpr int QTW = PAIR ? 1 : 2, PW = PAIR ? 2 : 1;
+  static constexpr int WPG = (QT / QTW) * (KT / KTW);   // waves per group of PW p's
+  static constexpr int PB = (4 / WPG) * PW;             // p's per workgroup
   static constexpr int ECH = 64;
-  static constexpr int ZROW = (ECH + 16 / ESZ) * ESZ;   // bytes per k row of the z chunk
+  static constexpr int ZROW = (ECH + 16 / ESZ) * ESZ;   // bytes per row of the z chunk
   static constexpr int FROW = ECH + 4;                   // floats per row of g / h chunks
   static constexpr int LDS = H2 * ZROW + DL * FROW * 4 + PB * FROW * 4;
-  static_assert(WPP * PB == 4, "four waves per workgroup");
+  // staging units per thread (rounded up)
+  static constexpr int ZU = ((ECH / 4) * (H2 * ESZ / 16) + 255) / 256;
+  static constexpr int GU = ((ECH / 4) * (DL / 4) + 255) / 256;
+  static constexpr int HU = (ECH * PB + 255) / 256;
+  static_assert(WPG * (PB / PW) == 4, "four waves per workgroup");
 };
 
 template <typename T, int DL, int H2>
-__global__ __launch_bounds__(256, 2) void k_bwd_dW3(W3Args a) {
+__global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) void k_bwd_dW3(W3Args a) {
   using S = W3Shape<T, DL, H2>;
   using M = MT<T>;
   using frag = typename M::frag;
-  constexpr int KS = S::KS, EPL = S::EPL, ESZ = S::ESZ, ECH = S::ECH;
+  constexpr int KS = S::KS, EPL = S::EPL, ESZ = S::ESZ, ECH = S::ECH, EQ = ECH / 4;
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* zl = smem;
   float* gl = reinterpret_cast<float*>(smem + H2 * S::ZROW);
@@ -441,83 +481,150 @@ __global__ __launch_bounds__(256, 2) void k_bwd_dW3(W3Args a) {
   constexpr int NPB = DL / S::PB;
   const int wg = blockIdx.x, xcd = wg & 7, slot = wg >> 3;
   const int chunk = (slot / NPB) * 8 + xcd, pb = slot % NPB;
-  const int p0 = pb * S::PB, pl = wv / S::WPP, sub = wv % S::WPP;
-  const int qt0 = (sub % (S::QT / S::QT_W)) * S::QT_W, kt0 = (sub / (S::QT / S::QT_W)) * S::KT_W;
+  const int p0 = pb * S::PB;
+  const int grp = wv / S::WPG, sub = wv % S::WPG;
+  const int pl0 = grp * S::PW;                                   // first local p of this wave
+  const int qt0 = (sub % (S::QT / S::QTW)) * S::QTW, kt0 = (sub / (S::QT / S::QTW)) * S::KTW;
   const T* hin = reinterpret_cast<const T*>(a.h_in);
   const int64_t e_begin = (int64_t)chunk * a.per_chunk;
   int64_t e_end = e_begin + a.per_chunk;
   if (e_end > a.E) e_end = a.E;
 
-  f32x16 acc[S::KT_W][S::QT_W];
+  f32x16 acc[S::PW][S::KTW][S::QTW];
 #pragma unroll
-  for (int kk = 0; kk < S::KT_W; ++kk)
+  for (int pp = 0; pp < S::PW; ++pp)
 #pragma unroll
-    for (int qq = 0; qq < S::QT_W; ++qq) acc[kk][qq] = f32x16{};
+    for (int kk = 0; kk < S::KTW; ++kk)
+#pragma unroll
+      for (int qq = 0; qq < S::QTW; ++qq) acc[pp][kk][qq] = f32x16{};
 
-  for (int64_t eb = e_begin; eb < e_end; eb += ECH) {
-    __syncthreads();
-    // z chunk transposed to [kk][e] (kk = stored order; undone at the output)
-    stage_transposed<T, H2, ECH, S::ZROW>(a.zE, eb, e_end, zl);
-    // g chunk transposed to [q][e], four edges x four columns per thread
-    for (int u = tid; u < (ECH / 4) * (DL / 4); u += 256) {
-      const int eq = u % (ECH / 4), q4 = u / (ECH / 4);
-      f32x4 v[4];
+  // next chunk held in registers while the current one is multiplied
+  uint4 zr[S::ZU][4];
+  f32x4 gr[S::GU][4];
+  float hr[S::HU];
+  auto fetch = [&](int64_t eb) {
+#pragma unroll
+    for (int x = 0; x < S::ZU; ++x) {
+      const int u = tid + x * 256, eq = u % EQ, kg = u / EQ;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int64_t e = eb + 4 * eq + i;
-        v[i] = e < e_end ? *reinterpret_cast<const f32x4*>(a.gF + (size_t)a.dst[e] * DL + q4 * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+        zr[x][i] = (u < EQ * (H2 * ESZ / 16) && e < e_end)
+                       ? *reinterpret_cast<const uint4*>(a.zE + (size_t)e * H2 * ESZ + kg * 16)
+                       : make_uint4(0, 0, 0, 0);
       }
+    }
+#pragma unroll
+    for (int x = 0; x < S::GU; ++x) {
+      const int u = tid + x * 256, eq = u % EQ, q4 = u / EQ;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t e = eb + 4 * eq + i;
+        gr[x][i] = (u < EQ * (DL / 4) && e < e_end)
+                       ? *reinterpret_cast<const f32x4*>(a.gF + (size_t)a.dst[e] * DL + q4 * 4)
+                       : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+#pragma unroll
+    for (int x = 0; x < S::HU; ++x) {
+      const int u = tid + x * 256, el = u / S::PB, pp = u % S::PB;
+      const int64_t e = eb + el;
+      hr[x] = (u < ECH * S::PB && e < e_end) ? to_f(hin[(size_t)a.col[e] * DL + p0 + pp]) : 0.0f;
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int x = 0; x < S::ZU; ++x) {
+      const int u = tid + x * 256, eq = u % EQ, kg = u / EQ;
+      if (u >= EQ * (H2 * ESZ / 16)) continue;
+      const uint32_t* d0 = reinterpret_cast<const uint32_t*>(&zr[x][0]);
+      const uint32_t* d1 = reinterpret_cast<const uint32_t*>(&zr[x][1]);
+      const uint32_t* d2 = reinterpret_cast<const uint32_t*>(&zr[x][2]);
+      const uint32_t* d3 = reinterpret_cast<const uint32_t*>(&zr[x][3]);
+      if constexpr (ESZ == 2) {
+#pragma unroll
+        for (int w = 0; w < 8; ++w) {
+          const int sh = (w & 1) * 16, dw = w >> 1;
+          const uint32_t lo = ((d0[dw] >> sh) & 0xFFFFu) | (((d1[dw] >> sh) & 0xFFFFu) << 16);
+          const uint32_t hi = ((d2[dw] >> sh) & 0xFFFFu) | (((d3[dw] >> sh) & 0xFFFFu) << 16);
+          *reinterpret_cast<uint2*>(zl + (kg * 8 + w) * S::ZROW + 4 * eq * ESZ) = make_uint2(lo, hi);
+        }
+      } else {
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          *reinterpret_cast<uint4*>(zl + (kg * 4 + w) * S::ZROW + 4 * eq * ESZ) = make_uint4(d0[w], d1[w], d2[w], d3[w]);
+      }
+    }
+#pragma unroll
+    for (int x = 0; x < S::GU; ++x) {
+      const int u = tid + x * 256, eq = u % EQ, q4 = u / EQ;
+      if (u >= EQ * (DL / 4)) continue;
 #pragma unroll
       for (int w = 0; w < 4; ++w)
-        *reinterpret_cast<f32x4*>(gl + (q4 * 4 + w) * S::FROW + 4 * eq) = f32x4{v[0][w], v[1][w], v[2][w], v[3][w]};
+        *reinterpret_cast<f32x4*>(gl + (q4 * 4 + w) * S::FROW + 4 * eq) =
+            f32x4{gr[x][0][w], gr[x][1][w], gr[x][2][w], gr[x][3][w]};
     }
-    for (int u = tid; u < ECH * S::PB; u += 256) {
-      const int el = u / S::PB, pp = u % S::PB;
-      const int64_t e = eb + el;
-      hl[pp * S::FROW + el] = e < e_end ? to_f(hin[(size_t)a.col[e] * DL + p0 + pp]) : 0.0f;
+#pragma unroll
+    for (int x = 0; x < S::HU; ++x) {
+      const int u = tid + x * 256, el = u / S::PB, pp = u % S::PB;
+      if (u < ECH * S::PB) hl[pp * S::FROW + el] = hr[x];
     }
+  };
+
+  if (e_begin < e_end) fetch(e_begin);
+  for (int64_t eb = e_begin; eb < e_end; eb += ECH) {
+    __syncthreads();   // the previous chunk's products are done with LDS
+    store();
     __syncthreads();
+    if (eb + ECH < e_end) fetch(eb + ECH);
 #pragma unroll 2
     for (int ks = 0; ks < ECH / KS; ++ks) {
       const int ec = ks * KS + hh * EPL;
-      frag A[S::KT_W];
+      frag A[S::KTW];
 #pragma unroll
-      for (int kk = 0; kk < S::KT_W; ++kk) A[kk] = ld_frag<T>(zl + ((kt0 + kk) * 32 + l32) * S::ZROW + ec * ESZ);
-      float hv[EPL];
+      for (int kk = 0; kk < S::KTW; ++kk) A[kk] = ld_frag<T>(zl + ((kt0 + kk) * 32 + l32) * S::ZROW + ec * ESZ);
 #pragma unroll
-      for (int u = 0; u < EPL; ++u) hv[u] = hl[pl * S::FROW + ec + u];
+      for (int qq = 0; qq < S::QTW; ++qq) {
+        const float* gp = gl + ((qt0 + qq) * 32 + l32) * S::FROW + ec;
+        float gv[EPL];
 #pragma unroll
-      for (int qq = 0; qq < S::QT_W; ++qq) {
-        const float* gr = gl + ((qt0 + qq) * 32 + l32) * S::FROW + ec;
-        frag B;
+        for (int u = 0; u < EPL; ++u) gv[u] = gp[u];
 #pragma unroll
-        for (int u = 0; u < EPL; ++u) set_el<T>(B, u, hv[u] * gr[u]);
+        for (int pp = 0; pp < S::PW; ++pp) {
+          const float* hp = hl + (pl0 + pp) * S::FROW + ec;
+          float bv[EPL];
 #pragma unroll
-        for (int kk = 0; kk < S::KT_W; ++kk) acc[kk][qq] = M::mma(A[kk], B, acc[kk][qq]);
+          for (int u = 0; u < EPL; ++u) bv[u] = hp[u] * gv[u];
+          const frag B = pack_frag<T>(bv);
+#pragma unroll
+          for (int kk = 0; kk < S::KTW; ++kk) acc[pp][kk][qq] = M::mma(A[kk], B, acc[pp][kk][qq]);
+        }
       }
     }
   }
-  // tile (k rows, q cols) -> part[chunk][(p*d + q)*h2 + k]
+  // tile (rows: stored-order k positions, cols q) -> part[chunk][(p*d + q)*h2 + k]
   float* out = a.part + (size_t)chunk * DL * DL * H2;
-  const int p = p0 + pl;
 #pragma unroll
-  for (int qq = 0; qq < S::QT_W; ++qq) {
-    const int q = (qt0 + qq) * 32 + l32;
+  for (int pp = 0; pp < S::PW; ++pp) {
+    const int p = p0 + pl0 + pp;
 #pragma unroll
-    for (int kk = 0; kk < S::KT_W; ++kk)
+    for (int qq = 0; qq < S::QTW; ++qq) {
+      const int q = (qt0 + qq) * 32 + l32;
+      float* o = out + ((size_t)p * DL + q) * H2;
 #pragma unroll
-      for (int a4 = 0; a4 < 4; ++a4) {
-        // tile rows are stored-order positions; map them back to k
-        const int r = (kt0 + kk) * 32 + 8 * a4 + 4 * hh;
-        float* o = out + ((size_t)p * DL + q) * H2;
-        if constexpr (EPL == 8) {
-          *reinterpret_cast<f32x4*>(o + kperm<T>(r)) =
-              f32x4{acc[kk][qq][4 * a4], acc[kk][qq][4 * a4 + 1], acc[kk][qq][4 * a4 + 2], acc[kk][qq][4 * a4 + 3]};
-        } else {
+      for (int kk = 0; kk < S::KTW; ++kk)
 #pragma unroll
-          for (int b = 0; b < 4; ++b) o[kperm<T>(r + b)] = acc[kk][qq][4 * a4 + b];
+        for (int a4 = 0; a4 < 4; ++a4) {
+          const int r = (kt0 + kk) * 32 + 8 * a4 + 4 * hh;
+          if constexpr (EPL == 8) {
+            *reinterpret_cast<f32x4*>(o + kperm<T>(r)) = f32x4{acc[pp][kk][qq][4 * a4], acc[pp][kk][qq][4 * a4 + 1],
+                                                               acc[pp][kk][qq][4 * a4 + 2], acc[pp][kk][qq][4 * a4 + 3]};
+          } else {
+#pragma unroll
+            for (int b = 0; b < 4; ++b) o[kperm<T>(r + b)] = acc[pp][kk][qq][4 * a4 + b];
+          }
         }
-      }
+    }
   }
 }
 
@@ -725,13 +832,15 @@ struct BwdWs {
   size_t total;
 };
 
+int w3_pb(int d, int h2) {
+  const int qt = d / 32, kt = h2 / 32, ktw = kt < 4 ? kt : 4;
+  const bool pair = qt * (kt / ktw) <= 2;
+  const int qtw = pair ? 1 : 2, pw = pair ? 2 : 1, wpg = (qt / qtw) * (kt / ktw);
+  return (4 / wpg) * pw;
+}
+
 int w3_nchunk(int d, int h2, int64_t E) {
-  int pb = 4;
-  int qt = d / 32, kt = h2 / 32;
-  int qtw = qt < 2 ? qt : 2, ktw = kt < 4 ? kt : 4;
-  int wpp = (qt / qtw) * (kt / ktw);
-  pb = 4 / wpp;
-  int npb = d / pb;
+  int npb = d / w3_pb(d, h2);
   int target = 1024 / npb;
   int n = ((target + 7) / 8) * 8;
   if (n < 8) n = 8;
@@ -924,7 +1033,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
 
   // kernel-MLP gradients
   if (E > 0) {
-    DzArgs dz{E, g->col, g->dst, hin, w.gT, pk, L, sv + sl.zE, sv + sl.z1E, w.da2E, w.da1E};
+    DzArgs dz{E, g->col, g->dst, hin, w.gF, pk, L, sv + sl.zE, sv + sl.z1E, w.da2E, w.da1E};
     W3Args w3{E, w.pc3, w.n3, g->col, g->dst, hin, w.gF, sv + sl.zE, w.p_w3};
     W2Args w2{E, w.pc2, 1, w.da2E, sv + sl.z1E, w.p_w2};
     if ((st = dispatch_edge_grads(h, d, dz, w3, w2)) != DSMP_OK) return st;

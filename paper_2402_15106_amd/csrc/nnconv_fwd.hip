@@ -148,16 +148,22 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
       float x[8];
       edge_attr(a.node_attr, a.dim, a.attr_mode, dnode[t], snode[t], x);
 #pragma unroll
-      for (int n = 0; n < H1 / 2; ++n) {
-        const f32x4 wa = *reinterpret_cast<const f32x4*>(w1l + n * 8);
-        const f32x4 wb = *reinterpret_cast<const f32x4*>(w1l + n * 8 + 4);
-        // b1 + W1 x as a chain of fused multiply-adds in attribute order
-        float v = b1l[n];
-        v = __builtin_fmaf(wa[0], x[0], v); v = __builtin_fmaf(wa[1], x[1], v);
-        v = __builtin_fmaf(wa[2], x[2], v); v = __builtin_fmaf(wa[3], x[3], v);
-        v = __builtin_fmaf(wb[0], x[4], v); v = __builtin_fmaf(wb[1], x[5], v);
-        v = __builtin_fmaf(wb[2], x[6], v); v = __builtin_fmaf(wb[3], x[7], v);
-        set_el<T>(z1B[t][n / EPL], n % EPL, v > 0.0f ? v : 0.0f);
+      for (int s = 0; s < S::SK1; ++s) {
+        float zv[EPL];
+#pragma unroll
+        for (int u = 0; u < EPL; ++u) {
+          const int n = s * EPL + u;
+          const f32x4 wa = *reinterpret_cast<const f32x4*>(w1l + n * 8);
+          const f32x4 wb = *reinterpret_cast<const f32x4*>(w1l + n * 8 + 4);
+          // b1 + W1 x as a chain of fused multiply-adds in attribute order
+          float v = b1l[n];
+          v = __builtin_fmaf(wa[0], x[0], v); v = __builtin_fmaf(wa[1], x[1], v);
+          v = __builtin_fmaf(wa[2], x[2], v); v = __builtin_fmaf(wa[3], x[3], v);
+          v = __builtin_fmaf(wb[0], x[4], v); v = __builtin_fmaf(wb[1], x[5], v);
+          v = __builtin_fmaf(wb[2], x[6], v); v = __builtin_fmaf(wb[3], x[7], v);
+          zv[u] = v > 0.0f ? v : 0.0f;
+        }
+        z1B[t][s] = pack_frag<T>(zv);
       }
       if (a.z1E && valid[t]) {
 #pragma unroll
@@ -187,10 +193,14 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
 #pragma unroll
       for (int t = 0; t < NT; ++t)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          float v = C[t][i] + bb[i];
-          const int n = 16 * kt + i;
-          set_el<T>(zB[t][n / EPL], n % EPL, v > 0.0f ? v : 0.0f);
+        for (int i0 = 0; i0 < 16; i0 += EPL) {
+          float zv[EPL];
+#pragma unroll
+          for (int u = 0; u < EPL; ++u) {
+            const float v = C[t][i0 + u] + bb[i0 + u];
+            zv[u] = v > 0.0f ? v : 0.0f;
+          }
+          zB[t][(16 * kt + i0) / EPL] = pack_frag<T>(zv);
         }
     }
     if (a.zE) {
