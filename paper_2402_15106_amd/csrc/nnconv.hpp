@@ -71,6 +71,62 @@ __host__ __device__ __forceinline__ int kperm(int kk) {
   return 32 * c + 8 * (i / 4) + 4 * h + (i % 4);
 }
 
+// Direct global-to-LDS staging of a weight block (no registers on the way):
+// ROWS rows of RB bytes, contiguous in global memory, land in LDS with a row
+// pitch of RB + 16 bytes, which keeps the 32-row fragment reads free of bank
+// conflicts.  Each wave-wide load fills 64 consecutive 16-byte LDS units; a
+// unit in a row's padding slot re-reads that row's first unit, and lanes past
+// the end of the block are masked off.  The copy is complete for the whole
+// workgroup after stage_wait() and a barrier.
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void gbl_void_t;
+
+template <int ROWS, int RB>
+struct LdsStage {
+  static constexpr int NU = RB / 16, PITCH = NU + 1, UNITS = ROWS * PITCH;
+  static constexpr int PER = (UNITS + 255) / 256;
+  static constexpr int BYTES = ROWS * (RB + 16);
+  static_assert(RB % 16 == 0, "rows are whole 16-byte units");
+  uint32_t off[PER];
+
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int U = i * 256 + (int)threadIdx.x;
+      const int r = U / PITCH, u = U % PITCH;
+      off[i] = (uint32_t)(r * RB + (u < NU ? u : 0) * 16);
+    }
+  }
+  // Start the copy of the block at src into dst (ROWS * (RB + 16) bytes).
+  __device__ __forceinline__ void issue(const unsigned char* src, unsigned char* dst) const {
+    const int wbase = (int)(threadIdx.x & ~63u);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      if (UNITS % 256 == 0 || i + 1 < PER || i * 256 + (int)threadIdx.x < UNITS) {
+        // keep the offset a 32-bit register at the load (scalar base + vector offset)
+        uint32_t o = off[i];
+        asm volatile("" : "+v"(o));
+        __builtin_amdgcn_global_load_lds((gbl_void_t*)(src + o),
+                                         (lds_void_t*)(dst + (size_t)(i * 256 + wbase) * 16), 16, 0, 0);
+      }
+    }
+  }
+};
+
+// Copy n16 contiguous 16-byte units from global memory to contiguous LDS.
+__device__ __forceinline__ void lds_copy_async(const unsigned char* src, unsigned char* dst, int n16) {
+  const int tid = (int)threadIdx.x, wbase = tid & ~63;
+  for (int i = 0; i * 256 < n16; ++i) {
+    const int U = i * 256 + tid;
+    if (U < n16)
+      __builtin_amdgcn_global_load_lds((gbl_void_t*)(src + (size_t)U * 16),
+                                       (lds_void_t*)(dst + (size_t)(i * 256 + wbase) * 16), 16, 0, 0);
+  }
+}
+
+// Wait for this thread's outstanding global loads, the LDS stages included.
+__device__ __forceinline__ void stage_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Byte offsets of the sections of a packed parameter buffer.
 struct PackLayout {
   size_t w1l, b1l, w2p, b2, w3f, w3q, w3t, b3t, b3n, w2t, wr, br, total;

@@ -212,7 +212,6 @@ struct DzShape {
   static constexpr int RCH = (H2 * DL * ESZ <= 32768) ? H2 : 32768 / (DL * ESZ);
   static constexpr int CPP = H2 / RCH, KPC = RCH / 32, NCH = DL * CPP;
   static constexpr int STAGE = RCH * ROWB, HROWB = DL * ESZ + 16;
-  static constexpr int U16 = RCH * DL * ESZ / 16, UPT = U16 / 256, ROW16 = DL * ESZ / 16;
   static constexpr int LDS = 2 * STAGE + TILE * HROWB;
 };
 
@@ -226,7 +225,6 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
   using M = MT<T>;
   using frag = typename M::frag;
   constexpr int KS = S::KS, EPL = S::EPL, NT = S::NT, TILE = S::TILE, ESZ = S::ESZ;
-  static_assert(S::U16 % 256 == 0, "chunk must split evenly");
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* stage0 = smem;
   unsigned char* htile = smem + 2 * S::STAGE;
@@ -270,23 +268,16 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
     for (int kt = 0; kt < S::KT; ++kt) acc[t][kt] = f32x16{};
 
   const unsigned char* A3 = P + a.L.w3t;   // [p][k][q]
-  uint4 pre[S::UPT];
-#define DZ_GLOAD(c_)                                                                             \
-  do {                                                                                          \
-    const uint4* src_ = reinterpret_cast<const uint4*>(                                         \
-        A3 + ((size_t)((c_) / S::CPP) * H2 + (size_t)((c_) % S::CPP) * S::RCH) * DL * ESZ);    \
-    _Pragma("unroll") for (int u = 0; u < S::UPT; ++u) pre[u] = src_[tid + u * 256];            \
-  } while (0)
-#define DZ_LSTORE(buf_)                                                                         \
-  do {                                                                                          \
-    _Pragma("unroll") for (int u = 0; u < S::UPT; ++u) {                                        \
-      const int idx = tid + u * 256;                                                            \
-      *reinterpret_cast<uint4*>(stage0 + (buf_) * S::STAGE + (idx / S::ROW16) * S::ROWB +       \
-                                (idx % S::ROW16) * 16) = pre[u];                                \
-    }                                                                                           \
-  } while (0)
-  DZ_GLOAD(0);
-  DZ_LSTORE(0);
+  // W3T chunks go straight into LDS, one chunk ahead of the products
+  using St = LdsStage<S::RCH, DL * ESZ>;
+  static_assert(St::BYTES == S::STAGE, "stage layout");
+  St stg;
+  stg.init();
+  auto chunk = [&](int c) {
+    return A3 + ((size_t)(c / S::CPP) * H2 + (size_t)(c % S::CPP) * S::RCH) * DL * ESZ;
+  };
+  stg.issue(chunk(0), stage0);
+  stage_wait();
   __syncthreads();
   // scaled B operand for p = 0
   frag Bq[NT][S::SKD];
@@ -316,8 +307,7 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
     for (int cc = 0; cc < S::CPP; ++cc) {
       const int c = p * S::CPP + cc;
       const int buf = c & 1;
-      const bool more = c + 1 < S::NCH;
-      if (more) DZ_GLOAD(c + 1);
+      if (c + 1 < S::NCH) stg.issue(chunk(c + 1), stage0 + (buf ^ 1) * S::STAGE);
       const unsigned char* sb = stage0 + buf * S::STAGE;
 #pragma unroll
       for (int s = 0; s < S::SKD; ++s) {
@@ -337,12 +327,10 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
           }
         }
       }
-      if (more) DZ_LSTORE(buf ^ 1);
+      stage_wait();
       __syncthreads();
     }
   }
-#undef DZ_GLOAD
-#undef DZ_LSTORE
 
   // da2 = dz * [z > 0] in the permuted order, then dz1 = W2^T da2 and da1
   const unsigned char* w2t = P + a.L.w2t;

@@ -60,8 +60,17 @@ struct Shape {
   static constexpr int STAGE = RCH * ROWB;
   static constexpr int HROWB = DL * ESZ + 16;
   static constexpr int MSGW = DL + 4;
-  static constexpr int U16 = RCH * H2 * ESZ / 16, UPT = (U16 + 255) / 256, ROW16 = H2 * ESZ / 16;
-  static constexpr int LDS_MAIN = 2 * STAGE + TILE * HROWB;
+  // The scaling of a q-block's products is deferred past the next block's
+  // MFMA chain when the extra accumulator set fits the register budget.
+  static constexpr bool PIPE = DL <= 64;
+  static constexpr int AD = 4;   // A-fragment read depth of the main loop
+  // W2 staged in the two W3 buffers, in pieces of W2R rows when it is larger
+  static constexpr int W2B = H1 * ESZ + 16;
+  static constexpr int W2R_FIT = (2 * STAGE / W2B) / 32 * 32;
+  static constexpr int W2R = W2R_FIT < H2 ? W2R_FIT : H2, NW2 = H2 / W2R;
+  static_assert(W2R >= 32 && H2 % W2R == 0, "W2 pieces");
+  static constexpr int W1BYTES = H1 * 8 * 4 + H1 * 4;   // W1 [2][H1/2][8], b1 [2][H1/2] (fp32)
+  static constexpr int LDS_MAIN = 2 * STAGE + TILE * HROWB + W1BYTES;
   static constexpr int LDS_MSG = TILE * MSGW * 4;
   static constexpr int LDS = LDS_MAIN > LDS_MSG ? LDS_MAIN : LDS_MSG;
 };
@@ -100,12 +109,52 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* stage0 = smem;
   unsigned char* htile = smem + 2 * S::STAGE;
+  float* w1s = reinterpret_cast<float*>(htile + TILE * S::HROWB);
   float* msg = reinterpret_cast<float*>(smem);
 
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
   const int64_t tile = blockIdx.x, t0 = tile * TILE;
   const int64_t tend = t0 + TILE < a.E ? t0 + TILE : a.E;
   const unsigned char* P = a.packed;
+  const unsigned char* A3 = P + (MODE == MODE_FWD ? a.L.w3f : a.L.w3q);
+  using St = LdsStage<S::RCH, H2 * ESZ>;
+  static_assert(St::BYTES == S::STAGE, "stage layout");
+  auto chunk = [&](int c) {
+    return A3 + ((size_t)(c / S::CPP) * DL + (size_t)(c % S::CPP) * S::RCH) * H2 * ESZ;
+  };
+  St stg;
+  stg.init();
+
+  // Direct-to-LDS loads go out first so their latency overlaps the id and
+  // attribute loads: the tile's gathered rows (h_j in the forward, g_i for
+  // the feature gradient; rows past E take row 0 and are never read back),
+  // then the first-layer weights and W2 (forward) or the first W3 chunk.
+  {
+    constexpr int HU = DL * ESZ / 16, PITCH = HU + 1, UNITS = TILE * PITCH;
+    const int wbase = tid & ~63;
+#pragma unroll
+    for (int i = 0; i < (UNITS + 255) / 256; ++i) {
+      const int U = i * 256 + tid;
+      if (UNITS % 256 == 0 || U < UNITS) {
+        const int r = U / PITCH, c = U % PITCH;
+        const int64_t s = t0 + r;
+        int node = 0;
+        if (s < a.E) node = MODE == MODE_FWD ? a.col[s] : a.dst[a.csc_eid[s]];
+        __builtin_amdgcn_global_load_lds(
+            (gbl_void_t*)(a.gath + (size_t)node * DL * ESZ + (c < HU ? c : 0) * 16),
+            (lds_void_t*)(htile + (size_t)(i * 256 + wbase) * 16), 16, 0, 0);
+      }
+    }
+  }
+  if constexpr (MODE == MODE_FWD) {
+    lds_copy_async(P + a.L.w1l, reinterpret_cast<unsigned char*>(w1s), H1 * 8 * 4 / 16);
+    lds_copy_async(P + a.L.b1l, reinterpret_cast<unsigned char*>(w1s + H1 * 8), H1 * 4 / 16);
+    LdsStage<S::W2R, H1 * ESZ> w2st;
+    w2st.init();
+    w2st.issue(P + a.L.w2p, stage0);
+  } else {
+    stg.issue(chunk(0), stage0);
+  }
 
   int64_t eid[NT];
   int dnode[NT], snode[NT], hrow[NT];
@@ -121,87 +170,90 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
     snode[t] = valid[t] ? a.col[e] : 0;
   }
 
-  // rows gathered for this tile: h_j (forward) or g_i (feature gradient)
-  {
-    constexpr int HU = DL * ESZ / 16;
-    for (int u = tid; u < TILE * HU; u += 256) {
-      int r = u / HU, c = u % HU;
-      int64_t s = t0 + r;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (s < a.E) {
-        int64_t e = MODE == MODE_FWD ? s : (int64_t)a.csc_eid[s];
-        int node = MODE == MODE_FWD ? a.col[e] : a.dst[e];
-        v = reinterpret_cast<const uint4*>(a.gath + (size_t)node * DL * ESZ)[c];
-      }
-      *reinterpret_cast<uint4*>(htile + r * S::HROWB + c * 16) = v;
-    }
-  }
-
   // B operand of the contraction: z_e, in the permuted register order
   frag zB[NT][S::SK2];
   if constexpr (MODE == MODE_FWD) {
+    float x[NT][8];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) edge_attr(a.node_attr, a.dim, a.attr_mode, dnode[t], snode[t], x[t]);
+    stage_wait();
+    __syncthreads();   // rows, W1 and W2 are in LDS
     frag z1B[NT][S::SK1];
-    const float* w1l = reinterpret_cast<const float*>(P + a.L.w1l) + hh * (H1 / 2) * 8;
-    const float* b1l = reinterpret_cast<const float*>(P + a.L.b1l) + hh * (H1 / 2);
+    const float* w1h = w1s + hh * (H1 / 2) * 8;
+    const float* b1h = w1s + H1 * 8 + hh * (H1 / 2);
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      float x[8];
-      edge_attr(a.node_attr, a.dim, a.attr_mode, dnode[t], snode[t], x);
+    for (int s = 0; s < S::SK1; ++s) {
+      float zv[NT][EPL];
 #pragma unroll
-      for (int s = 0; s < S::SK1; ++s) {
-        float zv[EPL];
+      for (int u = 0; u < EPL; ++u) {
+        const int n = s * EPL + u;
+        const f32x4 wa = *reinterpret_cast<const f32x4*>(w1h + n * 8);
+        const f32x4 wb = *reinterpret_cast<const f32x4*>(w1h + n * 8 + 4);
+        const float bn = b1h[n];
 #pragma unroll
-        for (int u = 0; u < EPL; ++u) {
-          const int n = s * EPL + u;
-          const f32x4 wa = *reinterpret_cast<const f32x4*>(w1l + n * 8);
-          const f32x4 wb = *reinterpret_cast<const f32x4*>(w1l + n * 8 + 4);
+        for (int t = 0; t < NT; ++t) {
           // b1 + W1 x as a chain of fused multiply-adds in attribute order
-          float v = b1l[n];
-          v = __builtin_fmaf(wa[0], x[0], v); v = __builtin_fmaf(wa[1], x[1], v);
-          v = __builtin_fmaf(wa[2], x[2], v); v = __builtin_fmaf(wa[3], x[3], v);
-          v = __builtin_fmaf(wb[0], x[4], v); v = __builtin_fmaf(wb[1], x[5], v);
-          v = __builtin_fmaf(wb[2], x[6], v); v = __builtin_fmaf(wb[3], x[7], v);
-          zv[u] = v > 0.0f ? v : 0.0f;
+          float v = bn;
+          v = __builtin_fmaf(wa[0], x[t][0], v); v = __builtin_fmaf(wa[1], x[t][1], v);
+          v = __builtin_fmaf(wa[2], x[t][2], v); v = __builtin_fmaf(wa[3], x[t][3], v);
+          v = __builtin_fmaf(wb[0], x[t][4], v); v = __builtin_fmaf(wb[1], x[t][5], v);
+          v = __builtin_fmaf(wb[2], x[t][6], v); v = __builtin_fmaf(wb[3], x[t][7], v);
+          zv[t][u] = v > 0.0f ? v : 0.0f;
         }
-        z1B[t][s] = pack_frag<T>(zv);
       }
-      if (a.z1E && valid[t]) {
 #pragma unroll
-        for (int s = 0; s < S::SK1; ++s)
-          *reinterpret_cast<frag*>(a.z1E + ((size_t)eid[t] * H1 + s * KS + hh * EPL) * ESZ) = z1B[t][s];
-      }
+      for (int t = 0; t < NT; ++t) z1B[t][s] = pack_frag<T>(zv[t]);
     }
-    const unsigned char* w2p = P + a.L.w2p;
-    const float* b2 = reinterpret_cast<const float*>(P + a.L.b2);
-#pragma unroll
-    for (int kt = 0; kt < S::KT; ++kt) {
-      f32x16 C[NT];
-#pragma unroll
-      for (int t = 0; t < NT; ++t) C[t] = f32x16{};
-#pragma unroll
-      for (int s = 0; s < S::SK1; ++s) {
-        frag A = ld_frag<T>(w2p + ((size_t)(kt * 32 + l32) * H1 + s * KS + hh * EPL) * ESZ);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) C[t] = M::mma(A, z1B[t][s], C[t]);
-      }
-      float bb[16];
-#pragma unroll
-      for (int a4 = 0; a4 < 4; ++a4) {
-        f32x4 v = *reinterpret_cast<const f32x4*>(b2 + kt * 32 + 8 * a4 + 4 * hh);
-        bb[4 * a4] = v[0]; bb[4 * a4 + 1] = v[1]; bb[4 * a4 + 2] = v[2]; bb[4 * a4 + 3] = v[3];
-      }
+    if (a.z1E) {
 #pragma unroll
       for (int t = 0; t < NT; ++t)
+        if (valid[t])
 #pragma unroll
-        for (int i0 = 0; i0 < 16; i0 += EPL) {
-          float zv[EPL];
+          for (int s = 0; s < S::SK1; ++s)
+            *reinterpret_cast<frag*>(a.z1E + ((size_t)eid[t] * H1 + s * KS + hh * EPL) * ESZ) = z1B[t][s];
+    }
+    const float* b2 = reinterpret_cast<const float*>(P + a.L.b2);
 #pragma unroll
-          for (int u = 0; u < EPL; ++u) {
-            const float v = C[t][i0 + u] + bb[i0 + u];
-            zv[u] = v > 0.0f ? v : 0.0f;
-          }
-          zB[t][(16 * kt + i0) / EPL] = pack_frag<T>(zv);
+    for (int piece = 0; piece < S::NW2; ++piece) {
+      if (piece > 0) {
+        __syncthreads();   // every wave is done with the previous piece
+        LdsStage<S::W2R, H1 * ESZ> w2st;
+        w2st.init();
+        w2st.issue(P + a.L.w2p + (size_t)piece * S::W2R * H1 * ESZ, stage0);
+        stage_wait();
+        __syncthreads();
+      }
+#pragma unroll
+      for (int kl = 0; kl < S::W2R / 32; ++kl) {
+        const int kt = piece * (S::W2R / 32) + kl;
+        f32x16 C[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) C[t] = f32x16{};
+#pragma unroll
+        for (int s = 0; s < S::SK1; ++s) {
+          frag A = ld_frag<T>(stage0 + (kl * 32 + l32) * S::W2B + (s * KS + hh * EPL) * ESZ);
+#pragma unroll
+          for (int t = 0; t < NT; ++t) C[t] = M::mma(A, z1B[t][s], C[t]);
         }
+        float bb[16];
+#pragma unroll
+        for (int a4 = 0; a4 < 4; ++a4) {
+          f32x4 v = *reinterpret_cast<const f32x4*>(b2 + kt * 32 + 8 * a4 + 4 * hh);
+          bb[4 * a4] = v[0]; bb[4 * a4 + 1] = v[1]; bb[4 * a4 + 2] = v[2]; bb[4 * a4 + 3] = v[3];
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int i0 = 0; i0 < 16; i0 += EPL) {
+            float zv[EPL];
+#pragma unroll
+            for (int u = 0; u < EPL; ++u) {
+              const float v = C[t][i0 + u] + bb[i0 + u];
+              zv[u] = v > 0.0f ? v : 0.0f;
+            }
+            zB[t][(16 * kt + i0) / EPL] = pack_frag<T>(zv);
+          }
+      }
     }
     if (a.zE) {
 #pragma unroll
@@ -211,6 +263,8 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
           for (int s = 0; s < S::SK2; ++s)
             *reinterpret_cast<frag*>(a.zE + ((size_t)eid[t] * H2 + s * KS + hh * EPL) * ESZ) = zB[t][s];
     }
+    __syncthreads();   // every wave is done with W2: the first W3 chunk takes its place
+    stg.issue(chunk(0), stage0);
   } else {
 #pragma unroll
     for (int t = 0; t < NT; ++t)
@@ -218,8 +272,9 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
       for (int s = 0; s < S::SK2; ++s)
         zB[t][s] = valid[t] ? ld_frag<T>(a.zE + ((size_t)eid[t] * H2 + s * KS + hh * EPL) * ESZ)
                             : zero_frag<T>();
+    stage_wait();
+    __syncthreads();   // gathered rows (and the first W3 chunk) are in LDS
   }
-  __syncthreads();   // gathered rows are in LDS
 
   // accumulators start at the bias term  B3^T u  (u = gathered row)
   f32x16 acc[NT][S::QT];
@@ -240,28 +295,22 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
       }
     }
   }
+  if constexpr (MODE == MODE_FWD) {
+    stage_wait();
+    __syncthreads();   // first W3 chunk is in LDS
+  }
 
   // main loop over p: W3 rows (p*d + q), chunks of RCH rows, double-buffered
-  const unsigned char* A3 = P + (MODE == MODE_FWD ? a.L.w3f : a.L.w3q);
-  static_assert(S::U16 % 256 == 0, "stage chunk must split evenly over the workgroup");
-  uint4 pre[S::UPT];
-#define DSMP_GLOAD(c_)                                                                          \
-  do {                                                                                         \
-    const uint4* src_ = reinterpret_cast<const uint4*>(                                        \
-        A3 + ((size_t)((c_) / S::CPP) * DL + (size_t)((c_) % S::CPP) * S::RCH) * H2 * ESZ);   \
-    _Pragma("unroll") for (int u = 0; u < S::UPT; ++u) pre[u] = src_[tid + u * 256];           \
-  } while (0)
-#define DSMP_LSTORE(buf_)                                                                      \
-  do {                                                                                         \
-    _Pragma("unroll") for (int u = 0; u < S::UPT; ++u) {                                       \
-      const int idx = tid + u * 256;                                                           \
-      *reinterpret_cast<uint4*>(stage0 + (buf_) * S::STAGE + (idx / S::ROW16) * S::ROWB +      \
-                                (idx % S::ROW16) * 16) = pre[u];                               \
-    }                                                                                          \
-  } while (0)
-  DSMP_GLOAD(0);
-  DSMP_LSTORE(0);
-  __syncthreads();
+  // in LDS and fetched one chunk ahead straight into LDS.  The products of
+  // one q-block are scaled into the accumulators after the next block's MFMA
+  // chain has been issued, so the scaling overlaps the matrix work.
+  f32x16 Cp[NT];
+  float scp[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    Cp[t] = f32x16{};
+    scp[t] = 0.0f;
+  }
   for (int p = 0; p < DL; ++p) {
     float sc[NT];
 #pragma unroll
@@ -271,29 +320,61 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
     for (int cc = 0; cc < S::CPP; ++cc) {
       const int c = p * S::CPP + cc;
       const int buf = c & 1;
-      const bool more = c + 1 < S::NCH;
-      if (more) DSMP_GLOAD(c + 1);
+      if (c + 1 < S::NCH) stg.issue(chunk(c + 1), stage0 + (buf ^ 1) * S::STAGE);
       const unsigned char* sb = stage0 + buf * S::STAGE;
+      // A fragments of the chunk, read AD-1 steps ahead of their products
+      constexpr int NS = S::QPC * S::SK2, AD = S::AD;
+      auto a_at = [&](int j) {
+        return sb + ((j / S::SK2) * 32 + l32) * S::ROWB + ((j % S::SK2) * KS + hh * EPL) * ESZ;
+      };
+      frag Ab[AD];
+#pragma unroll
+      for (int j = 0; j < AD - 1; ++j) Ab[j] = ld_frag<T>(a_at(j));
 #pragma unroll
       for (int qq = 0; qq < S::QPC; ++qq) {
         f32x16 C[NT];
 #pragma unroll
         for (int t = 0; t < NT; ++t) C[t] = f32x16{};
+        // retire the previous q-block (block QT-1 of the previous p before
+        // block 0) a few registers per step, between this block's products
+        const int prev = (cc * S::QPC + qq + S::QT - 1) % S::QT;
 #pragma unroll
         for (int s = 0; s < S::SK2; ++s) {
-          frag A = ld_frag<T>(sb + (qq * 32 + l32) * S::ROWB + (s * KS + hh * EPL) * ESZ);
+          const int j = qq * S::SK2 + s;
+          if (j + AD - 1 < NS) Ab[(j + AD - 1) % AD] = ld_frag<T>(a_at(j + AD - 1));
 #pragma unroll
-          for (int t = 0; t < NT; ++t) C[t] = M::mma(A, zB[t][s], C[t]);
+          for (int t = 0; t < NT; ++t) C[t] = M::mma(Ab[j % AD], zB[t][s], C[t]);
+          if constexpr (S::PIPE) {
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+              for (int pq = 0; pq < S::QT; ++pq)
+                if (pq == prev)
+#pragma unroll
+                  for (int r = s * 16 / S::SK2; r < (s + 1) * 16 / S::SK2; ++r) acc[t][pq][r] += scp[t] * Cp[t][r];
+          }
+          // keep the read-ahead and the interleaving in this order
+          __builtin_amdgcn_sched_barrier(0);
         }
+        if constexpr (S::PIPE) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) acc[t][cc * S::QPC + qq] += sc[t] * C[t];
+          for (int t = 0; t < NT; ++t) {
+            Cp[t] = C[t];
+            scp[t] = sc[t];
+          }
+        } else {
+#pragma unroll
+          for (int t = 0; t < NT; ++t) acc[t][cc * S::QPC + qq] += sc[t] * C[t];
+        }
       }
-      if (more) DSMP_LSTORE(buf ^ 1);
+      stage_wait();
       __syncthreads();
     }
   }
-#undef DSMP_GLOAD
-#undef DSMP_LSTORE
+  if constexpr (S::PIPE) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t][S::QT - 1] += scp[t] * Cp[t];
+  }
 
   // messages to LDS, then per-destination (or per-source) runs
 #pragma unroll
