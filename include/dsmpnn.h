@@ -234,6 +234,20 @@ dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_desc* desc, co
                                  float* grad_h, const dsmp_layer_grads* grads, int32_t flags,
                                  void* ws, size_t ws_bytes);
 
+/* How the layer evaluates the edge contraction.  DSMP_EDGE_PER_EDGE forms
+ * each message m_e on MFMA (edge tiles against streamed W3 chunks) and sums
+ * them per destination.  DSMP_EDGE_AGGREGATE uses the linearity of the mean:
+ * the per-destination sums S_i = sum_e [z_e; 1] (x) h_j are formed first and
+ * contracted with W3 and b3 in one GEMM (the feature gradient likewise over
+ * the edges of each source, and dW3 from the same S_i); the result is the
+ * same up to floating-point summation order.  DSMP_EDGE_AUTO (the default)
+ * takes the aggregate form when the mean in-degree times d is at least 512.
+ * The setting applies to later forward and backward calls on the handle; a
+ * backward must run with the algorithm of its forward.  Workspace sizes
+ * cover either algorithm. */
+enum { DSMP_EDGE_AUTO = 0, DSMP_EDGE_PER_EDGE = 1, DSMP_EDGE_AGGREGATE = 2 };
+dsmp_status dsmp_set_edge_algorithm(dsmp_handle* h, int32_t algorithm);
+
 /* ------------------------------------------------------------ kernel timing
  * Opt-in timing of the library's kernels with HIP events, for benchmarks.
  * While enabled, every launch (or launch group) of a kernel class below is
@@ -253,11 +267,16 @@ enum {
   DSMP_K_EDGE_DH = 6,   /* feature-gradient edge contraction kernel */
   DSMP_K_DH_FINAL = 7,  /* feature-gradient assembly kernel */
   DSMP_K_DZ = 8,        /* dz / da2 / da1 kernel */
-  DSMP_K_DW3 = 9,       /* dW3 split-over-edges kernel */
+  DSMP_K_DW3 = 9,       /* dW3 kernels (split over edges, or over S) */
   DSMP_K_DW2 = 10,      /* dW2 split-over-edges kernel */
   DSMP_K_DW1 = 11,      /* dW1 kernel */
   DSMP_K_REDUCE = 12,   /* fixed-order gradient reductions */
-  DSMP_K_COUNT = 13
+  DSMP_K_EDGE_MLP = 13, /* kernel-MLP edge kernel (aggregate form) */
+  DSMP_K_OUTER_FWD = 14,/* per-destination sums S_i (aggregate form) */
+  DSMP_K_GEMM_FWD = 15, /* W3 GEMM over S (aggregate form) */
+  DSMP_K_OUTER_DH = 16, /* per-source sums T_j (aggregate form) */
+  DSMP_K_GEMM_DH = 17,  /* W3 GEMM over T (aggregate form) */
+  DSMP_K_COUNT = 18
 };
 dsmp_status dsmp_profile_enable(dsmp_handle* h, int enable);
 dsmp_status dsmp_profile_reset(dsmp_handle* h);

@@ -8,5 +8,5 @@ behind a C ABI (include/dsmpnn.h); this package is the thin Python binding.
 from ._lib import (  # noqa: F401
     Dsmp, DsmpError, Graph, LayerDesc, layer_desc, load_library, LIB_PATH, EXPORTED, KERNEL_CLASSES,
     CAP_KNN, CAP_RANDOM, F32, BF16, ACT_IDENTITY, ACT_RELU, ATTR_CONCAT, ATTR_DIFF,
-    GRAD_ACCUMULATE, OK, INVALID_ARG, CAPACITY, HIP_ERROR, UNSUPPORTED, WORKSPACE_TOO_SMALL,
+    GRAD_ACCUMULATE, EDGE_AUTO, EDGE_PER_EDGE, EDGE_AGGREGATE, OK, INVALID_ARG, CAPACITY, HIP_ERROR, UNSUPPORTED, WORKSPACE_TOO_SMALL,
 )

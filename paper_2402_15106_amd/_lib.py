@@ -26,17 +26,19 @@ F32, BF16 = 0, 1
 ACT_IDENTITY, ACT_RELU = 0, 1
 ATTR_CONCAT, ATTR_DIFF = 0, 1
 GRAD_ACCUMULATE = 1
+EDGE_AUTO, EDGE_PER_EDGE, EDGE_AGGREGATE = 0, 1, 2
 
 EXPORTED = ["dsmp_version", "dsmp_create", "dsmp_destroy", "dsmp_set_stream", "dsmp_last_error",
             "dsmp_sample_workspace", "dsmp_sample_nodes", "dsmp_gather_rows",
             "dsmp_radius_graph_workspace", "dsmp_radius_graph_count", "dsmp_radius_graph_build",
             "dsmp_nnconv_packed_bytes", "dsmp_nnconv_pack", "dsmp_nnconv_workspace",
             "dsmp_nnconv_forward", "dsmp_nnconv_backward", "dsmp_profile_enable", "dsmp_profile_reset",
-            "dsmp_profile_read"]
+            "dsmp_profile_read", "dsmp_set_edge_algorithm"]
 
 # kernel classes of the opt-in timing (dsmp_profile_*)
 KERNEL_CLASSES = ["sample", "gather", "graph", "edge_fwd", "node_fwd", "node_bwd", "edge_dh", "dh_final",
-                  "dz", "dW3", "dW2", "dW1", "reduce"]
+                  "dz", "dW3", "dW2", "dW1", "reduce", "edge_mlp", "outer_fwd", "gemm_fwd", "outer_dh",
+                  "gemm_dh"]
 
 
 class DsmpError(RuntimeError):
@@ -77,6 +79,7 @@ _SIG = {
     "dsmp_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]),
     "dsmp_destroy": (ctypes.c_int, [_P]),
     "dsmp_set_stream": (ctypes.c_int, [_P, _P]),
+    "dsmp_set_edge_algorithm": (ctypes.c_int, [_P, ctypes.c_int32]),
     "dsmp_last_error": (ctypes.c_char_p, [_P]),
     "dsmp_sample_workspace": (ctypes.c_int, [ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]),
     "dsmp_sample_nodes": (ctypes.c_int, [_P, ctypes.c_int64, ctypes.c_int64, ctypes.c_uint64, _P, _P,
@@ -184,6 +187,10 @@ class Dsmp:
     def _bind(self):
         s = torch.cuda.current_stream(self.device).cuda_stream
         self._check(self.lib.dsmp_set_stream(self.h, ctypes.c_void_p(s)), self.h)
+
+    def dsmp_set_edge_algorithm(self, algorithm: int):
+        """Edge-contraction form for later layer calls (EDGE_AUTO / EDGE_PER_EDGE / EDGE_AGGREGATE)."""
+        self._check(self.lib.dsmp_set_edge_algorithm(self.h, int(algorithm)), self.h)
 
     def workspace(self, key: str, nbytes: int) -> torch.Tensor:
         """A cached uint8 device buffer of at least nbytes for scratch use."""

@@ -14,6 +14,7 @@
 struct dsmp_handle {
   int device = 0;
   hipStream_t stream = nullptr;
+  int edge_algo = 0;   // DSMP_EDGE_AUTO / PER_EDGE / AGGREGATE
   std::string err;
   // kernel timing (opt-in)
   struct Mark {

@@ -180,6 +180,14 @@ extern "C" dsmp_status dsmp_set_stream(dsmp_handle* h, void* stream) {
   return DSMP_OK;
 }
 
+extern "C" dsmp_status dsmp_set_edge_algorithm(dsmp_handle* h, int32_t algorithm) {
+  if (!h) return DSMP_INVALID_ARG;
+  DSMP_CHECK(h, algorithm == DSMP_EDGE_AUTO || algorithm == DSMP_EDGE_PER_EDGE || algorithm == DSMP_EDGE_AGGREGATE,
+             DSMP_INVALID_ARG, "unknown edge algorithm %d", algorithm);
+  h->edge_algo = algorithm;
+  return DSMP_OK;
+}
+
 extern "C" const char* dsmp_last_error(const dsmp_handle* h) { return h ? h->err.c_str() : ""; }
 
 // ------------------------------------------------------------------ sampling

@@ -129,7 +129,7 @@ __device__ __forceinline__ void stage_wait() { __builtin_amdgcn_s_waitcnt(0x0F70
 
 // Byte offsets of the sections of a packed parameter buffer.
 struct PackLayout {
-  size_t w1l, b1l, w2p, b2, w3f, w3q, w3t, b3t, b3n, w2t, wr, br, total;
+  size_t w1l, b1l, w2p, b2, w3f, w3q, w3t, b3t, b3n, w2t, wr, br, wgt, wht, total;
 };
 
 inline PackLayout pack_layout(int d, int h1, int h2, int esz) {
@@ -153,6 +153,9 @@ inline PackLayout pack_layout(int d, int h1, int h2, int esz) {
   L.w2t = take((size_t)h1 * h2 * esz);        // T [j][h2 permuted]
   L.wr = take((size_t)d * d * 4);             // fp32 [q][p] (rounded to the layer dtype)
   L.br = take((size_t)d * 4);                 // fp32 [d]
+  // W3~ for the aggregate form, in the segment-sum K order (K = h2*d + d):
+  L.wgt = take((size_t)d * (h2 + 1) * d * esz);   // T [q][K(k, p)]
+  L.wht = take((size_t)d * (h2 + 1) * d * esz);   // T [p][K(k, q)]
   L.total = (off + 255) & ~size_t(255);
   return L;
 }
@@ -160,7 +163,7 @@ inline PackLayout pack_layout(int d, int h1, int h2, int esz) {
 // Edges per workgroup tile of the edge kernels (4 waves x 2 tiles x 32).
 constexpr int EDGE_TILE = 256;
 
-enum { MODE_FWD = 0, MODE_DH = 1 };
+enum { MODE_FWD = 0, MODE_DH = 1, MODE_MLP = 2 };
 
 // Arguments of the edge contraction (forward messages, or the feature
 // gradient when run over the edges in source order).
@@ -186,14 +189,28 @@ dsmp_status launch_edge_contract(dsmp_handle* h, const dsmp_layer_desc& desc, in
                                  const EdgeArgs& a);
 
 // Per-layer buffer the forward fills for the backward: y [n_dst][d] fp32,
-// z [E][h2] and z1 [E][h1] in the layer dtype and the permuted order.
+// z [E][h2] and z1 [E][h1] in the layer dtype and the permuted order, and
+// the per-destination sums S [n_dst][(h2+1)d] of the aggregate form.
 struct SavedLayout {
-  size_t y, zE, z1E, total;
+  size_t y, zE, z1E, os, total;
 };
 SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E);
 size_t fwd_ws_bytes(const dsmp_layer_desc& d, int64_t n_dst, int64_t E);
 dsmp_status check_layer_desc(dsmp_handle* h, const dsmp_layer_desc* d);
 dsmp_status check_graph(dsmp_handle* h, const dsmp_graph* g, bool need_csc);
 int layer_attr_width(const dsmp_layer_desc& d);
+
+// Aggregate form of the edge contraction (nnconv_agg.hip).
+bool use_aggregate(const dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_dst, int64_t E);
+int64_t agg_ktot(const dsmp_layer_desc& d);
+int agg_gemm_slices(int64_t n_rows, const dsmp_layer_desc& d);
+int agg_dw3_slices(int64_t n_rows);
+dsmp_status launch_outer_sum(dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_seg, const int32_t* seg_ptr,
+                             const int32_t* pos_eid, const int32_t* row_of, const unsigned char* zE,
+                             const unsigned char* u, unsigned char* out);
+dsmp_status launch_w3_gemm(dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_rows, const unsigned char* A,
+                           const unsigned char* BT, int nsl, float* part);
+dsmp_status launch_dw3_agg(dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_rows, const unsigned char* OS,
+                           const unsigned char* G, float* part, float* dW3, int accumulate);
 
 }  // namespace dsmp

@@ -1,0 +1,456 @@
+// Aggregate-first evaluation of the NNConv edge contraction (eq. (1)).
+//
+// The message of edge e = (i <- j) is bilinear in the kernel-MLP output z_e
+// and the source row h_j:
+//     m_e[q] = sum_{k,p} W3[p*d+q][k] z_e[k] h_j[p] + sum_p b3[p*d+q] h_j[p].
+// The mean over the edges of i is linear, so with z~ = [z; 1]
+//     agg_i[q] = (1/deg_i) sum_{k,p} W3~[p*d+q][k] S_i[k][p],
+//     S_i[k][p] = sum_{e in in(i)} z~_e[k] h_j(e)[p],
+// one GEMM over the per-destination sums S (n_dst x (h2+1)d) in place of one
+// product per edge.  The feature gradient has the same form over the edges
+// leaving a source j, with T_j[k][q] = sum_{e in out(j)} z~_e[k] g_e[q] and
+// dh_j[p] = sum_{k,q} W3~[p*d+q][k] T_j[k][q]; the weight gradient is
+// dW3[p*d+q][k] = sum_i g_i[q] S_i[k][p] (g_e = g_i for every edge into i).
+// Neither form writes anything of size E x d x d.
+//
+// K order of a sum row.  The (h2/32) x (d/32) tiles of 32 x 32 are stored in
+// MFMA accumulator order: tile t = kt*(d/32) + ct, lane l, register r at
+// K = 1024 t + 16 l + r holds k = 32 kt + 8 (r/4) + 4 (l/32) + r%4 (the
+// stored, permuted z order) and c = 32 ct + l%32; the d values of the z~ = 1
+// row follow at K = h2*d + c.  The packed W3 matrices (WgT, WhT) use the same
+// K order, so neither side is ever transposed in memory.
+#include "nnconv.hpp"
+
+using namespace dsmp;
+
+namespace {
+
+template <typename T>
+__device__ __forceinline__ typename MT<T>::frag ldf(const void* p) {
+  return *reinterpret_cast<const typename MT<T>::frag*>(p);
+}
+
+// Copy 4 gathered rows (16-byte unit kg of each) into LDS transposed: row
+// (element) kg*KPU + w, columns c0..c0+3.  Null row pointers give zeros.
+template <typename T, int ROWB>
+__device__ __forceinline__ void put4_transposed(const unsigned char* const r[4], int kg, int c0,
+                                                unsigned char* __restrict__ dstl) {
+  constexpr int ESZ = sizeof(T);
+  uint4 v[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    v[i] = r[i] ? *reinterpret_cast<const uint4*>(r[i] + kg * 16) : make_uint4(0, 0, 0, 0);
+  const uint32_t* d0 = reinterpret_cast<const uint32_t*>(&v[0]);
+  const uint32_t* d1 = reinterpret_cast<const uint32_t*>(&v[1]);
+  const uint32_t* d2 = reinterpret_cast<const uint32_t*>(&v[2]);
+  const uint32_t* d3 = reinterpret_cast<const uint32_t*>(&v[3]);
+  if constexpr (ESZ == 2) {
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      const int sh = (w & 1) * 16, dw = w >> 1;
+      const uint32_t lo = ((d0[dw] >> sh) & 0xFFFFu) | (((d1[dw] >> sh) & 0xFFFFu) << 16);
+      const uint32_t hi = ((d2[dw] >> sh) & 0xFFFFu) | (((d3[dw] >> sh) & 0xFFFFu) << 16);
+      *reinterpret_cast<uint2*>(dstl + (kg * 8 + w) * ROWB + c0 * ESZ) = make_uint2(lo, hi);
+    }
+  } else {
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+      *reinterpret_cast<uint4*>(dstl + (kg * 4 + w) * ROWB + c0 * ESZ) = make_uint4(d0[w], d1[w], d2[w], d3[w]);
+  }
+}
+
+// ------------------------------------------------------------ segment sums
+
+struct OuterArgs {
+  int64_t n_seg;               // segments: destinations (S) or sources (T)
+  const int32_t* seg_ptr;      // [n_seg + 1] positions of each segment's edges
+  const int32_t* pos_eid;      // NULL: edge id = position; else edge id = pos_eid[position]
+  const int32_t* row_of;       // gathered row of edge e
+  const unsigned char* zE;     // [E][h2] layer dtype, stored order
+  const unsigned char* u;      // gathered rows [*][d] layer dtype
+  unsigned char* out;          // [n_seg][ktot] layer dtype
+};
+
+template <typename T, int DL, int H2>
+struct OuterShape {
+  static constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL, ESZ = sizeof(T);
+  static constexpr int ECH = 64;                          // edges per staged chunk
+  static constexpr int NKT = H2 / 32, NCT = DL / 32, NTILE = NKT * NCT, TPW = (NTILE + 3) / 4;
+  static constexpr int ROWB = (ECH + 16 / ESZ) * ESZ;     // LDS row pitch (bytes)
+  static constexpr int ZU = (ECH / 4) * (H2 * ESZ / 16);  // transposed staging units
+  static constexpr int UU = (ECH / 4) * (DL * ESZ / 16);
+  static constexpr int LDS = (H2 + DL) * ROWB;
+  static constexpr int64_t KTOT = (int64_t)H2 * DL + DL;
+};
+
+// One workgroup per segment: stage up to 64 of its edges at a time, z~ and
+// the gathered rows both transposed to [element][edge], and accumulate the
+// outer-product sum tile by tile on MFMA (edges are the contraction index).
+template <typename T, int DL, int H2>
+__global__ __launch_bounds__(256) void k_outer_sum(OuterArgs a) {
+  using S = OuterShape<T, DL, H2>;
+  using M = MT<T>;
+  constexpr int KS = S::KS, EPL = S::EPL, ESZ = S::ESZ, ECH = S::ECH;
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* zt = smem;
+  unsigned char* ut = smem + H2 * S::ROWB;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int64_t n = blockIdx.x;
+  const int64_t pa = a.seg_ptr[n], pb = a.seg_ptr[n + 1];
+
+  f32x16 acc[S::TPW];
+#pragma unroll
+  for (int j = 0; j < S::TPW; ++j) acc[j] = f32x16{};
+  float hs = 0.0f;   // z~ = 1 row: sum of the gathered rows (threads tid < DL)
+
+  for (int64_t c0 = pa; c0 < pb; c0 += ECH) {
+    const int cnt = (int)(pb - c0 < ECH ? pb - c0 : ECH);
+    __syncthreads();   // previous chunk fully consumed
+    for (int x = tid; x < S::ZU + S::UU; x += 256) {
+      const bool isz = x < S::ZU;
+      const int y = isz ? x : x - S::ZU;
+      const int eq = y % (ECH / 4), kg = y / (ECH / 4);
+      const unsigned char* r[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int sl = 4 * eq + i;
+        r[i] = nullptr;
+        if (sl < cnt) {
+          const int64_t pos = c0 + sl;
+          const int64_t e = a.pos_eid ? (int64_t)a.pos_eid[pos] : pos;
+          r[i] = isz ? a.zE + (size_t)e * H2 * ESZ : a.u + (size_t)a.row_of[e] * DL * ESZ;
+        }
+      }
+      if (isz) put4_transposed<T, S::ROWB>(r, kg, 4 * eq, zt);
+      else put4_transposed<T, S::ROWB>(r, kg, 4 * eq, ut);
+    }
+    __syncthreads();
+    const int nks = (cnt + KS - 1) / KS;
+    for (int ks = 0; ks < nks; ++ks) {
+      const int col = (ks * KS + hh * EPL) * ESZ;
+#pragma unroll
+      for (int j = 0; j < S::TPW; ++j) {
+        const int ti = wv + 4 * j;
+        if (ti < S::NTILE) {
+          const int kt = ti / S::NCT, ct = ti % S::NCT;
+          const auto A = ldf<T>(zt + (kt * 32 + l32) * S::ROWB + col);
+          const auto B = ldf<T>(ut + (ct * 32 + l32) * S::ROWB + col);
+          acc[j] = M::mma(A, B, acc[j]);
+        }
+      }
+    }
+    if (tid < DL) {
+      const T* row = reinterpret_cast<const T*>(ut + tid * S::ROWB);
+      for (int s = 0; s < cnt; ++s) hs += (float)row[s];
+    }
+  }
+
+  unsigned char* o = a.out + (size_t)n * S::KTOT * ESZ;
+#pragma unroll
+  for (int j = 0; j < S::TPW; ++j) {
+    const int ti = wv + 4 * j;
+    if (ti < S::NTILE) {
+      unsigned char* dst = o + ((size_t)ti * 1024 + lane * 16) * ESZ;
+      if constexpr (ESZ == 2) {
+        float v[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = acc[j][r];
+        *reinterpret_cast<bf16x8*>(dst) = pack_frag<__bf16>(v);
+        *reinterpret_cast<bf16x8*>(dst + 16) = pack_frag<__bf16>(v + 8);
+      } else {
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+          *reinterpret_cast<f32x4*>(dst + r4 * 16) =
+              f32x4{acc[j][4 * r4], acc[j][4 * r4 + 1], acc[j][4 * r4 + 2], acc[j][4 * r4 + 3]};
+      }
+    }
+  }
+  if (tid < DL) reinterpret_cast<T*>(o)[(size_t)H2 * DL + tid] = (T)hs;
+}
+
+// ------------------------------------------------------------ GEMM with W3~
+
+struct GemmArgs {
+  int64_t n_rows, ktot;
+  const unsigned char* A;    // [n_rows][ktot] layer dtype (segment sums)
+  const unsigned char* BT;   // [DL][ktot] layer dtype (packed W3~ in the sum order)
+  int nsl;                   // K slices
+  int64_t ksl;               // K steps per slice
+  float* part;               // [nsl][n_rows][DL] partial products
+};
+
+// part[s][n][c] = sum over slice s of K:  A[n][K] * BT[c][K].  Each wave owns
+// 32 rows and all d columns; a workgroup is 4 row tiles of one K slice.
+template <typename T, int DL>
+__global__ __launch_bounds__(256) void k_w3_gemm(GemmArgs a) {
+  using M = MT<T>;
+  constexpr int KS = M::KS, EPL = M::EPL, ESZ = sizeof(T), NCT = DL / 32;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int64_t r0 = ((int64_t)blockIdx.x * 4 + wv) * 32;
+  if (r0 >= a.n_rows) return;
+  const int s = blockIdx.y;
+  const int64_t nstep = a.ktot / KS;
+  const int64_t k0 = s * a.ksl, k1 = (s + 1) * a.ksl < nstep ? (s + 1) * a.ksl : nstep;
+  int64_t row = r0 + l32;
+  if (row >= a.n_rows) row = a.n_rows - 1;
+  const unsigned char* pa = a.A + ((size_t)row * a.ktot + hh * EPL) * ESZ;
+  const unsigned char* pb[NCT];
+#pragma unroll
+  for (int ct = 0; ct < NCT; ++ct) pb[ct] = a.BT + ((size_t)(ct * 32 + l32) * a.ktot + hh * EPL) * ESZ;
+  f32x16 acc[NCT];
+#pragma unroll
+  for (int ct = 0; ct < NCT; ++ct) acc[ct] = f32x16{};
+  constexpr int U = 8;
+  int64_t ks = k0;
+  for (; ks + U <= k1; ks += U) {
+    typename M::frag A[U], B[U][NCT];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      A[u] = ldf<T>(pa + (size_t)(ks + u) * KS * ESZ);
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) B[u][ct] = ldf<T>(pb[ct] + (size_t)(ks + u) * KS * ESZ);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) acc[ct] = M::mma(A[u], B[u][ct], acc[ct]);
+  }
+  for (; ks < k1; ++ks) {
+    const auto A = ldf<T>(pa + (size_t)ks * KS * ESZ);
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) acc[ct] = M::mma(A, ldf<T>(pb[ct] + (size_t)ks * KS * ESZ), acc[ct]);
+  }
+  float* out = a.part + (size_t)s * a.n_rows * DL;
+#pragma unroll
+  for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int64_t rr = r0 + 8 * (r / 4) + 4 * hh + (r % 4);
+      if (rr < a.n_rows) out[rr * DL + ct * 32 + l32] = acc[ct][r];
+    }
+}
+
+// ------------------------------------------------------------ dW3 from S
+
+struct DW3AggArgs {
+  int64_t n_rows, ktot, kcols;
+  const unsigned char* OS;   // [n_rows][ktot] layer dtype
+  const unsigned char* G;    // [n_rows][DL] layer dtype (g_i)
+  int nsl;
+  int64_t rows_per_sl;       // multiple of 64
+  float* part;               // [nsl][DL][kcols]
+};
+
+template <typename T, int DL>
+struct DW3AggShape {
+  static constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL, ESZ = sizeof(T);
+  static constexpr int NCH = 64, KR = 256;              // rows per chunk, K columns per workgroup
+  static constexpr int NQT = DL / 32, NKT = KR / 32, NTILE = NQT * NKT, TPW = NTILE / 4;
+  static constexpr int ROWB = (NCH + 16 / ESZ) * ESZ;
+  static constexpr int OU = (NCH / 4) * (KR * ESZ / 16), GU = (NCH / 4) * (DL * ESZ / 16);
+  static constexpr int LDS = (KR + DL) * ROWB;
+  static_assert(NTILE % 4 == 0, "tiles split over four waves");
+};
+
+// part[s][q][K] = sum over the rows of slice s of g[i][q] * S[i][K]: rows of
+// S and g staged transposed to [column][row], rows are the contraction index.
+template <typename T, int DL>
+__global__ __launch_bounds__(256) void k_dw3_agg(DW3AggArgs a) {
+  using S = DW3AggShape<T, DL>;
+  using M = MT<T>;
+  constexpr int KS = S::KS, EPL = S::EPL, ESZ = S::ESZ, NCH = S::NCH;
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* ot = smem;
+  unsigned char* gt = smem + S::KR * S::ROWB;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int64_t kc0 = (int64_t)blockIdx.x * S::KR;
+  const int s = blockIdx.y;
+  const int64_t rb = s * a.rows_per_sl;
+  const int64_t re = rb + a.rows_per_sl < a.n_rows ? rb + a.rows_per_sl : a.n_rows;
+  f32x16 acc[S::TPW];
+#pragma unroll
+  for (int j = 0; j < S::TPW; ++j) acc[j] = f32x16{};
+  for (int64_t c0 = rb; c0 < re; c0 += NCH) {
+    const int cnt = (int)(re - c0 < NCH ? re - c0 : NCH);
+    __syncthreads();
+    for (int x = tid; x < S::OU + S::GU; x += 256) {
+      const bool iso = x < S::OU;
+      const int y = iso ? x : x - S::OU;
+      const int eq = y % (NCH / 4), kg = y / (NCH / 4);
+      const unsigned char* r[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int sl = 4 * eq + i;
+        r[i] = sl < cnt ? (iso ? a.OS + ((size_t)(c0 + sl) * a.ktot + kc0) * ESZ : a.G + (size_t)(c0 + sl) * DL * ESZ)
+                        : nullptr;
+      }
+      if (iso) put4_transposed<T, S::ROWB>(r, kg, 4 * eq, ot);
+      else put4_transposed<T, S::ROWB>(r, kg, 4 * eq, gt);
+    }
+    __syncthreads();
+    const int nks = (cnt + KS - 1) / KS;
+    for (int ks = 0; ks < nks; ++ks) {
+      const int col = (ks * KS + hh * EPL) * ESZ;
+#pragma unroll
+      for (int j = 0; j < S::TPW; ++j) {
+        const int ti = wv * S::TPW + j, qt = ti / S::NKT, kt = ti % S::NKT;
+        acc[j] = M::mma(ldf<T>(gt + (qt * 32 + l32) * S::ROWB + col), ldf<T>(ot + (kt * 32 + l32) * S::ROWB + col),
+                        acc[j]);
+      }
+    }
+  }
+  float* out = a.part + (size_t)s * DL * a.kcols;
+#pragma unroll
+  for (int j = 0; j < S::TPW; ++j) {
+    const int ti = wv * S::TPW + j, qt = ti / S::NKT, kt = ti % S::NKT;
+    const int64_t kc = kc0 + kt * 32 + l32;
+    if (kc < a.kcols)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) out[(size_t)(qt * 32 + 8 * (r / 4) + 4 * hh + (r % 4)) * a.kcols + kc] = acc[j][r];
+  }
+}
+
+// dW3[p*d+q][k] (+)= sum_s part[s][q][K(k, p)], K in the sum order above.
+template <typename T>
+__global__ __launch_bounds__(256) void k_dw3_agg_final(int d, int h2, int nsl, const float* __restrict__ part,
+                                                       float* __restrict__ dW3, int accumulate) {
+  const int64_t kcols = (int64_t)h2 * d, total = (int64_t)d * d * h2;
+  const int nct = d / 32;
+  for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < total; x += (int64_t)gridDim.x * blockDim.x) {
+    // x enumerates (q, K) with K fastest, so the reads of part are contiguous
+    const int q = (int)(x / kcols);
+    const int64_t K = x % kcols;
+    const int ti = K / 1024, rem = K % 1024, l = rem / 16, r = rem % 16;
+    const int kt = ti / nct, ct = ti % nct;
+    const int kpos = kt * 32 + 8 * (r / 4) + 4 * (l / 32) + (r % 4), p = ct * 32 + (l % 32);
+    float v = 0.0f;
+    for (int s = 0; s < nsl; ++s) v += part[((int64_t)s * d + q) * kcols + K];
+    float* o = dW3 + ((int64_t)p * d + q) * h2 + kperm<T>(kpos);
+    *o = accumulate ? *o + v : v;
+  }
+}
+
+template <typename K>
+dsmp_status set_lds_bytes(dsmp_handle* h, K kernel, int bytes) {
+  DSMP_HIP(h, hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, bytes));
+  return DSMP_OK;
+}
+
+template <typename T, int DL, int H2>
+dsmp_status outer_shape(dsmp_handle* h, const OuterArgs& a) {
+  using S = OuterShape<T, DL, H2>;
+  auto kern = k_outer_sum<T, DL, H2>;
+  dsmp_status st = set_lds_bytes(h, kern, S::LDS);
+  if (st != DSMP_OK) return st;
+  hipLaunchKernelGGL(kern, dim3((unsigned)a.n_seg), dim3(256), S::LDS, h->stream, a);
+  DSMP_LAUNCHED(h, "segment outer-product sums");
+  return DSMP_OK;
+}
+
+template <typename T, int DL>
+dsmp_status dw3_shape(dsmp_handle* h, const DW3AggArgs& a) {
+  using S = DW3AggShape<T, DL>;
+  auto kern = k_dw3_agg<T, DL>;
+  dsmp_status st = set_lds_bytes(h, kern, S::LDS);
+  if (st != DSMP_OK) return st;
+  hipLaunchKernelGGL(kern, dim3((unsigned)ceil_div(a.kcols, S::KR), (unsigned)a.nsl), dim3(256), S::LDS, h->stream,
+                     a);
+  DSMP_LAUNCHED(h, "dW3 from segment sums");
+  return DSMP_OK;
+}
+
+}  // namespace
+
+namespace dsmp {
+
+int64_t agg_ktot(const dsmp_layer_desc& d) { return (int64_t)d.h2 * d.d + d.d; }
+
+bool use_aggregate(const dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_dst, int64_t E) {
+  if (h->edge_algo == DSMP_EDGE_PER_EDGE) return false;
+  if (h->edge_algo == DSMP_EDGE_AGGREGATE) return true;
+  return n_dst > 0 && E * d.d >= 512 * n_dst;
+}
+
+int agg_gemm_slices(int64_t n_rows, const dsmp_layer_desc& d) {
+  const int64_t waves = ceil_div(n_rows, 32);
+  int nsl = (int)(2048 / (waves > 0 ? waves : 1));
+  if (nsl < 1) nsl = 1;
+  if (nsl > 16) nsl = 16;
+  return nsl;
+}
+
+dsmp_status launch_outer_sum(dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_seg, const int32_t* seg_ptr,
+                             const int32_t* pos_eid, const int32_t* row_of, const unsigned char* zE,
+                             const unsigned char* u, unsigned char* out) {
+  if (n_seg == 0) return DSMP_OK;
+  OuterArgs a{n_seg, seg_ptr, pos_eid, row_of, zE, u, out};
+  if (d.dtype == DSMP_F32) {
+    if (d.d == 32) return outer_shape<float, 32, 64>(h, a);
+    if (d.d == 64) return outer_shape<float, 64, 128>(h, a);
+  } else {
+    if (d.d == 32) return outer_shape<__bf16, 32, 64>(h, a);
+    if (d.d == 64) return outer_shape<__bf16, 64, 128>(h, a);
+    if (d.d == 128) return outer_shape<__bf16, 128, 256>(h, a);
+  }
+  return fail(h, DSMP_UNSUPPORTED, "unsupported layer shape");
+}
+
+dsmp_status launch_w3_gemm(dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_rows, const unsigned char* A,
+                           const unsigned char* BT, int nsl, float* part) {
+  if (n_rows == 0) return DSMP_OK;
+  const int64_t ktot = agg_ktot(d);
+  const int64_t nstep = ktot / (d.dtype == DSMP_F32 ? MT<float>::KS : MT<__bf16>::KS);
+  GemmArgs a{n_rows, ktot, A, BT, nsl, ceil_div(nstep, nsl), part};
+  dim3 grid((unsigned)ceil_div(n_rows, 128), (unsigned)nsl);
+  if (d.dtype == DSMP_F32) {
+    if (d.d == 32) hipLaunchKernelGGL((k_w3_gemm<float, 32>), grid, dim3(256), 0, h->stream, a);
+    if (d.d == 64) hipLaunchKernelGGL((k_w3_gemm<float, 64>), grid, dim3(256), 0, h->stream, a);
+  } else {
+    if (d.d == 32) hipLaunchKernelGGL((k_w3_gemm<__bf16, 32>), grid, dim3(256), 0, h->stream, a);
+    if (d.d == 64) hipLaunchKernelGGL((k_w3_gemm<__bf16, 64>), grid, dim3(256), 0, h->stream, a);
+    if (d.d == 128) hipLaunchKernelGGL((k_w3_gemm<__bf16, 128>), grid, dim3(256), 0, h->stream, a);
+  }
+  DSMP_LAUNCHED(h, "W3 GEMM over segment sums");
+  return DSMP_OK;
+}
+
+int agg_dw3_slices(int64_t n_rows) {
+  int nsl = (int)ceil_div(n_rows, 512);
+  if (nsl < 1) nsl = 1;
+  if (nsl > 32) nsl = 32;
+  return nsl;
+}
+
+dsmp_status launch_dw3_agg(dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_rows, const unsigned char* OS,
+                           const unsigned char* G, float* part, float* dW3, int accumulate) {
+  const int nsl = agg_dw3_slices(n_rows);
+  const int64_t kcols = (int64_t)d.h2 * d.d;
+  if (n_rows > 0) {
+    DW3AggArgs a{n_rows, agg_ktot(d), kcols, OS, G, nsl, ceil_div(ceil_div(n_rows, nsl), 64) * 64, part};
+    dsmp_status st = DSMP_UNSUPPORTED;
+    if (d.dtype == DSMP_F32) {
+      if (d.d == 32) st = dw3_shape<float, 32>(h, a);
+      if (d.d == 64) st = dw3_shape<float, 64>(h, a);
+    } else {
+      if (d.d == 32) st = dw3_shape<__bf16, 32>(h, a);
+      if (d.d == 64) st = dw3_shape<__bf16, 64>(h, a);
+      if (d.d == 128) st = dw3_shape<__bf16, 128>(h, a);
+    }
+    if (st != DSMP_OK) return st;
+  }
+  const int nuse = n_rows > 0 ? nsl : 0;
+  const int64_t total = (int64_t)d.d * d.d * d.h2;
+  unsigned grid = (unsigned)ceil_div(total, 256);
+  if (grid > 8192) grid = 8192;
+  if (d.dtype == DSMP_F32)
+    hipLaunchKernelGGL(k_dw3_agg_final<float>, dim3(grid), dim3(256), 0, h->stream, d.d, d.h2, nuse, part, dW3,
+                       accumulate);
+  else
+    hipLaunchKernelGGL(k_dw3_agg_final<__bf16>, dim3(grid), dim3(256), 0, h->stream, d.d, d.h2, nuse, part, dW3,
+                       accumulate);
+  DSMP_LAUNCHED(h, "dW3 assembly");
+  return DSMP_OK;
+}
+
+}  // namespace dsmp

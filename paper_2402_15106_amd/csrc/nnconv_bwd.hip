@@ -790,14 +790,21 @@ __device__ __forceinline__ float segment_sum(const int32_t* __restrict__ ptr, in
 }
 
 // grad_h[j] = [root/residual terms if j is a destination] + sum over the edges leaving j
+// (aggregate form: the edge sum is the nsl K-slices of the W3 GEMM over T)
 __global__ void k_bwd_dh_final(int64_t n_src, int64_t n_dst, int DL, const int32_t* __restrict__ csc_ptr,
-                               const float* __restrict__ direct, const float* __restrict__ part,
-                               const float* __restrict__ dh_node, float* __restrict__ grad_h) {
+                               const float* __restrict__ direct, const float* __restrict__ part, int nsl,
+                               const float* __restrict__ slices, const float* __restrict__ dh_node,
+                               float* __restrict__ grad_h) {
   const int64_t total = n_src * DL;
   for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < total; x += (int64_t)gridDim.x * blockDim.x) {
     const int64_t j = x / DL;
     const int c = (int)(x % DL);
-    float s = segment_sum(csc_ptr, j, c, DL, direct, part);
+    float s = 0.0f;
+    if (nsl > 0) {
+      for (int sl = 0; sl < nsl; ++sl) s += slices[(int64_t)sl * total + x];
+    } else {
+      s = segment_sum(csc_ptr, j, c, DL, direct, part);
+    }
     if (j < n_dst) s += dh_node[x];
     grad_h[x] = s;
   }
@@ -811,8 +818,9 @@ __global__ void k_jof(int* out, int h1, int isbf16) {
 // ------------------------------------------------------------ workspace
 
 struct BwdWs {
-  float *ybar, *gF, *dh_node, *dh_direct, *dh_part, *da1E;
-  unsigned char *gT, *da2E;
+  float *ybar, *gF, *dh_node, *dh_direct, *dh_part, *da1E, *dh_sl;
+  unsigned char *gT, *da2E, *ot;
+  int nslh;
   float *p_root, *p_db3, *p_w3, *p_w2, *p_w1;
   int* jof;
   int nr, nb3, n3, n2, n1;
@@ -849,6 +857,10 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   w.dh_node = c.take<float>((size_t)n_dst * d.d);
   w.dh_direct = c.take<float>((size_t)n_src * d.d);
   w.dh_part = c.take<float>((size_t)(ceil_div(E, EDGE_TILE) + 1) * 2 * d.d);
+  // aggregate form: per-source sums T and the K-slices of their W3 GEMM
+  w.ot = c.take<unsigned char>((size_t)n_src * agg_ktot(d) * esz);
+  w.nslh = agg_gemm_slices(n_src, d);
+  w.dh_sl = c.take<float>((size_t)w.nslh * n_src * d.d);
   w.da2E = c.take<unsigned char>((size_t)E * d.h2 * esz);
   w.da1E = c.take<float>((size_t)E * d.h1);
   w.nr = (int)(n_dst > 0 ? (ceil_div(n_dst, 32) < 1024 ? ceil_div(n_dst, 32) : 1024) : 1);
@@ -860,7 +872,9 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   w.n3 = w3_nchunk(d.d, d.h2, E);
   w.pc3 = ((E + w.n3 - 1) / w.n3 + 63) / 64 * 64;
   if (w.pc3 < 64) w.pc3 = 64;
-  w.p_w3 = c.take<float>((size_t)w.n3 * d.d * d.d * d.h2);
+  // dW3 partials: per-edge chunks, or the node slices of the aggregate form
+  const int n3a = agg_dw3_slices(n_dst);
+  w.p_w3 = c.take<float>((size_t)(w.n3 > n3a ? w.n3 : n3a) * d.d * d.d * d.h2);
   w.n2 = (int)(E > 0 ? (ceil_div(E, 2048) < 512 ? ceil_div(E, 2048) : 512) : 1);
   w.pc2 = ((E + w.n2 - 1) / w.n2 + 63) / 64 * 64;
   if (w.pc2 < 64) w.pc2 = 64;
@@ -892,7 +906,7 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
     hipLaunchKernelGGL(kz, dim3(ceil_div(dz.E, S::TILE)), dim3(256), S::LDS, s, dz);
     DSMP_LAUNCHED(h, "dz");
   }
-  {
+  if (w3.nchunk > 0) {
     using S = W3Shape<T, DL, H2>;
     auto k3 = k_bwd_dW3<T, DL, H2>;
     if ((st = set_lds(h, k3, S::LDS)) != DSMP_OK) return st;
@@ -1000,6 +1014,8 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   DSMP_LAUNCHED(h, "backward node kernels");
   prof_node.end();
 
+  const bool agg = use_aggregate(h, d, n_dst, E);
+
   // feature gradient through the edges (edge contraction in source order)
   EdgeArgs ea{};
   ea.E = E; ea.n_dst = n_dst; ea.n_src = n_src;
@@ -1009,20 +1025,34 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   ea.zE = const_cast<unsigned char*>(sv + sl.zE);
   ea.z1E = nullptr;
   ea.out_direct = w.dh_direct; ea.out_part = w.dh_part;
-  if ((st = launch_edge_contract(h, d, MODE_DH, ea)) != DSMP_OK) return st;
+  if (agg) {
+    // per-source sums T_j = sum_e [z_e; 1] (x) g_e, then one GEMM with W3~
+    {
+      ProfScope prof(h, DSMP_K_OUTER_DH);
+      st = launch_outer_sum(h, d, n_src, g->csc_ptr, g->csc_eid, g->dst, sv + sl.zE, w.gT, w.ot);
+    }
+    if (st != DSMP_OK) return st;
+    {
+      ProfScope prof(h, DSMP_K_GEMM_DH);
+      st = launch_w3_gemm(h, d, n_src, w.ot, pk + L.wht, w.nslh, w.dh_sl);
+    }
+    if (st != DSMP_OK) return st;
+  } else {
+    if ((st = launch_edge_contract(h, d, MODE_DH, ea)) != DSMP_OK) return st;
+  }
   if (n_src > 0) {
     unsigned grid = ceil_div(n_src * d.d, 256);
     if (grid > 4096) grid = 4096;
     ProfScope prof(h, DSMP_K_DH_FINAL);
     hipLaunchKernelGGL(k_bwd_dh_final, dim3(grid), dim3(256), 0, s, n_src, n_dst, d.d, g->csc_ptr, w.dh_direct,
-                       w.dh_part, w.dh_node, grad_h);
+                       w.dh_part, agg ? w.nslh : 0, w.dh_sl, w.dh_node, grad_h);
     DSMP_LAUNCHED(h, "grad_h");
   }
 
   // kernel-MLP gradients
   if (E > 0) {
     DzArgs dz{E, g->col, g->dst, hin, w.gF, pk, L, sv + sl.zE, sv + sl.z1E, w.da2E, w.da1E};
-    W3Args w3{E, w.pc3, w.n3, g->col, g->dst, hin, w.gF, sv + sl.zE, w.p_w3};
+    W3Args w3{E, w.pc3, agg ? 0 : w.n3, g->col, g->dst, hin, w.gF, sv + sl.zE, w.p_w3};
     W2Args w2{E, w.pc2, 1, w.da2E, sv + sl.z1E, w.p_w2};
     if ((st = dispatch_edge_grads(h, d, dz, w3, w2)) != DSMP_OK) return st;
     hipLaunchKernelGGL(k_jof, dim3(ceil_div(d.h1, 256)), dim3(256), 0, s, w.jof, d.h1, d.dtype == DSMP_BF16);
@@ -1040,6 +1070,12 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
     DSMP_LAUNCHED(h, "dW1");
   }
 
+  if (agg) {
+    // dW3[p*d+q][k] = sum_i g_i[q] S_i[k][p] from the forward's sums
+    ProfScope prof(h, DSMP_K_DW3);
+    if ((st = launch_dw3_agg(h, d, n_dst, sv + sl.os, w.gT, w.p_w3, grads->dW3, acc)) != DSMP_OK) return st;
+  }
+
   // fixed-order reductions into the caller's gradients
   auto red = [&](const float* part, int nchunk, int64_t stride, int64_t off, int64_t n, float* out) {
     unsigned grid = ceil_div(n, 64);
@@ -1048,7 +1084,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
     hipLaunchKernelGGL(k_reduce, dim3(grid), dim3(256), 0, s, part, nchunk, stride, off, n, out, acc);
   };
   const int64_t dd = (int64_t)d.d * d.d;
-  const int n3 = E > 0 ? w.n3 : 0;
+  const int n3 = E > 0 && !agg ? w.n3 : 0;
   const int n2 = E > 0 ? (int)((E + w.pc2 - 1) / w.pc2) : 0;
   const int n1 = E > 0 ? (int)((E + w.pc1 - 1) / w.pc1) : 0;
   const int nr = n_dst > 0 ? w.nr : 0;
@@ -1056,7 +1092,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   red(w.p_root, nr, dd + d.d, 0, dd, grads->dWr);
   red(w.p_root, nr, dd + d.d, dd, d.d, grads->dbr);
   red(w.p_db3, nr, dd, 0, dd, grads->db3);
-  red(w.p_w3, n3, dd * d.h2, 0, dd * d.h2, grads->dW3);
+  if (!agg) red(w.p_w3, n3, dd * d.h2, 0, dd * d.h2, grads->dW3);
   red(w.p_w2, n2, (int64_t)d.h2 * d.h1 + d.h2, 0, (int64_t)d.h2 * d.h1, grads->dW2);
   red(w.p_w2, n2, (int64_t)d.h2 * d.h1 + d.h2, (int64_t)d.h2 * d.h1, d.h2, grads->db2);
   red(w.p_w1, n1, (int64_t)d.h1 * de + d.h1, 0, (int64_t)d.h1 * de, grads->dW1);

@@ -129,7 +129,8 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
   // attribute loads: the tile's gathered rows (h_j in the forward, g_i for
   // the feature gradient; rows past E take row 0 and are never read back),
   // then the first-layer weights and W2 (forward) or the first W3 chunk.
-  {
+  // The kernel-MLP-only form (z and z1 for the aggregate form) stops after z.
+  if constexpr (MODE != MODE_MLP) {
     constexpr int HU = DL * ESZ / 16, PITCH = HU + 1, UNITS = TILE * PITCH;
     const int wbase = tid & ~63;
 #pragma unroll
@@ -146,7 +147,7 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
       }
     }
   }
-  if constexpr (MODE == MODE_FWD) {
+  if constexpr (MODE != MODE_DH) {
     lds_copy_async(P + a.L.w1l, reinterpret_cast<unsigned char*>(w1s), H1 * 8 * 4 / 16);
     lds_copy_async(P + a.L.b1l, reinterpret_cast<unsigned char*>(w1s + H1 * 8), H1 * 4 / 16);
     LdsStage<S::W2R, H1 * ESZ> w2st;
@@ -164,7 +165,7 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
     hrow[t] = (wv * NT + t) * 32 + l32;
     int64_t s = t0 + hrow[t];
     valid[t] = s < a.E;
-    int64_t e = valid[t] ? (MODE == MODE_FWD ? s : (int64_t)a.csc_eid[s]) : 0;
+    int64_t e = valid[t] ? (MODE != MODE_DH ? s : (int64_t)a.csc_eid[s]) : 0;
     eid[t] = e;
     dnode[t] = valid[t] ? a.dst[e] : 0;
     snode[t] = valid[t] ? a.col[e] : 0;
@@ -172,7 +173,7 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
 
   // B operand of the contraction: z_e, in the permuted register order
   frag zB[NT][S::SK2];
-  if constexpr (MODE == MODE_FWD) {
+  if constexpr (MODE != MODE_DH) {
     float x[NT][8];
 #pragma unroll
     for (int t = 0; t < NT; ++t) edge_attr(a.node_attr, a.dim, a.attr_mode, dnode[t], snode[t], x[t]);
@@ -263,6 +264,7 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
           for (int s = 0; s < S::SK2; ++s)
             *reinterpret_cast<frag*>(a.zE + ((size_t)eid[t] * H2 + s * KS + hh * EPL) * ESZ) = zB[t][s];
     }
+    if constexpr (MODE == MODE_MLP) return;
     __syncthreads();   // every wave is done with W2: the first W3 chunk takes its place
     stg.issue(chunk(0), stage0);
   } else {
@@ -432,6 +434,8 @@ struct NodeArgs {
   unsigned char* h_out_lp;
   float* y_saved;
   int act, residual;
+  int nsl;                     // > 0: aggregate form, sums are the nsl slices below
+  const float* slices;         // [nsl][n_dst][d]
 };
 
 // y_i = mean_i + Wr h_i + br;  out_i = [h_i +] act(y_i)
@@ -452,7 +456,15 @@ __global__ __launch_bounds__(256) void k_fwd_node(NodeArgs a) {
     if (!ok) continue;
     const int32_t deg = a.row_ptr[i + 1] - a.row_ptr[i];
     float y = 0.0f;
-    if (deg > 0) y = segment_sum(a.row_ptr, i, q, DL, a.direct, a.part) / (float)deg;
+    if (deg > 0) {
+      float sum = 0.0f;
+      if (a.nsl > 0) {
+        for (int sl = 0; sl < a.nsl; ++sl) sum += a.slices[((int64_t)sl * a.n_dst + i) * DL + q];
+      } else {
+        sum = segment_sum(a.row_ptr, i, q, DL, a.direct, a.part);
+      }
+      y = sum / (float)deg;
+    }
     float r = 0.0f;
 #pragma unroll 8
     for (int p = 0; p < DL; ++p) r += wr[q][p] * hs[li][p];
@@ -523,6 +535,28 @@ __global__ void k_pack(PackArgs a) {
   }
   float* br = reinterpret_cast<float*>(a.out + a.L.br);
   for (int64_t x = t0; x < d; x += stride) br[x] = a.br[x];
+  // W3~ in the segment-sum K order: K < h2*d is (k stored position, c) of a
+  // 32x32 accumulator tile, K = h2*d + c is the bias row.
+  T* wgt = reinterpret_cast<T*>(a.out + a.L.wgt);
+  T* wht = reinterpret_cast<T*>(a.out + a.L.wht);
+  const int64_t ktot = (int64_t)h2 * d + d;
+  const int nct = d / 32;
+  for (int64_t x = t0; x < (int64_t)d * ktot; x += stride) {
+    const int o = (int)(x / ktot);
+    const int64_t K = x % ktot;
+    if (K < (int64_t)h2 * d) {
+      const int ti = (int)(K / 1024), rem = (int)(K % 1024), l = rem / 16, r = rem % 16;
+      const int kpos = (ti / nct) * 32 + 8 * (r / 4) + 4 * (l / 32) + (r % 4);
+      const int c = (ti % nct) * 32 + (l % 32);
+      const int k = kperm<T>(kpos);
+      wgt[x] = (T)a.W3[((int64_t)c * d + o) * h2 + k];   // output q = o, sum column p = c
+      wht[x] = (T)a.W3[((int64_t)o * d + c) * h2 + k];   // output p = o, sum column q = c
+    } else {
+      const int c = (int)(K - (int64_t)h2 * d);
+      wgt[x] = (T)a.b3[c * d + o];
+      wht[x] = (T)a.b3[o * d + c];
+    }
+  }
 }
 
 template <typename K>
@@ -535,12 +569,18 @@ dsmp_status set_lds(dsmp_handle* h, K kernel, int bytes) {
 template <typename T, int DL, int H1, int H2>
 dsmp_status launch_edge_shape(dsmp_handle* h, int mode, const EdgeArgs& a) {
   using S = Shape<T, DL, H1, H2>;
-  const unsigned grid = ceil_div(mode == MODE_FWD ? a.E : a.E, S::TILE);
+  const unsigned grid = ceil_div(a.E, S::TILE);
   if (mode == MODE_FWD) {
     auto kern = k_edge_contract<T, DL, H1, H2, MODE_FWD>;
     dsmp_status st = set_lds(h, kern, S::LDS);
     if (st != DSMP_OK) return st;
     ProfScope prof(h, DSMP_K_EDGE_FWD);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), S::LDS, h->stream, a);
+  } else if (mode == MODE_MLP) {
+    auto kern = k_edge_contract<T, DL, H1, H2, MODE_MLP>;
+    dsmp_status st = set_lds(h, kern, S::LDS);
+    if (st != DSMP_OK) return st;
+    ProfScope prof(h, DSMP_K_EDGE_MLP);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(256), S::LDS, h->stream, a);
   } else {
     auto kern = k_edge_contract<T, DL, H1, H2, MODE_DH>;
@@ -618,15 +658,20 @@ SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E) {
   s.y = (size_t)c.take<float>((size_t)n_dst * d.d) ;
   s.zE = (size_t)c.take<unsigned char>((size_t)E * d.h2 * esz);
   s.z1E = (size_t)c.take<unsigned char>((size_t)E * d.h1 * esz);
+  s.os = (size_t)c.take<unsigned char>((size_t)n_dst * agg_ktot(d) * esz);
   s.total = c.used();
   return s;
 }
 
 size_t fwd_ws_bytes(const dsmp_layer_desc& d, int64_t n_dst, int64_t E) {
+  // per-edge form: direct sums and tile partials; aggregate form: GEMM slices
   Carve c(nullptr);
   c.take<float>((size_t)n_dst * d.d);
   c.take<float>((size_t)(ceil_div(E, EDGE_TILE) + 1) * 2 * d.d);
-  return c.used();
+  const size_t per_edge = c.used();
+  Carve c2(nullptr);
+  c2.take<float>((size_t)agg_gemm_slices(n_dst, d) * n_dst * d.d);
+  return per_edge > c2.used() ? per_edge : c2.used();
 }
 
 dsmp_status check_graph(dsmp_handle* h, const dsmp_graph* g, bool need_csc) {
@@ -695,9 +740,17 @@ extern "C" dsmp_status dsmp_nnconv_forward(dsmp_handle* h, const dsmp_layer_desc
   const int esz = d.dtype == DSMP_BF16 ? 2 : 4;
   PackLayout L = pack_layout(d.d, d.h1, d.h2, esz);
   unsigned char* sv = static_cast<unsigned char*>(saved);
+  const bool agg = use_aggregate(h, d, g->n_dst, g->n_edges);
   Carve c(ws);
-  float* direct = c.take<float>((size_t)g->n_dst * d.d);
-  float* part = c.take<float>((size_t)(ceil_div(g->n_edges, EDGE_TILE) + 1) * 2 * d.d);
+  float *direct = nullptr, *part = nullptr, *slices = nullptr;
+  int nsl = 0;
+  if (agg) {
+    nsl = agg_gemm_slices(g->n_dst, d);
+    slices = c.take<float>((size_t)nsl * g->n_dst * d.d);
+  } else {
+    direct = c.take<float>((size_t)g->n_dst * d.d);
+    part = c.take<float>((size_t)(ceil_div(g->n_edges, EDGE_TILE) + 1) * 2 * d.d);
+  }
   EdgeArgs ea{};
   ea.E = g->n_edges; ea.n_dst = g->n_dst; ea.n_src = g->n_src;
   ea.row_ptr = g->row_ptr; ea.col = g->col; ea.dst = g->dst;
@@ -706,13 +759,30 @@ extern "C" dsmp_status dsmp_nnconv_forward(dsmp_handle* h, const dsmp_layer_desc
   ea.packed = static_cast<const unsigned char*>(packed); ea.L = L;
   ea.zE = sv + sl.zE; ea.z1E = sv + sl.z1E;
   ea.out_direct = direct; ea.out_part = part;
-  if ((st = launch_edge_contract(h, d, MODE_FWD, ea)) != DSMP_OK) return st;
+  if (agg) {
+    // z and z1 per edge, the per-destination sums S (kept for the backward),
+    // then one GEMM with W3~ into nsl K-slices
+    if ((st = launch_edge_contract(h, d, MODE_MLP, ea)) != DSMP_OK) return st;
+    {
+      ProfScope prof(h, DSMP_K_OUTER_FWD);
+      st = launch_outer_sum(h, d, g->n_dst, g->row_ptr, nullptr, g->col, sv + sl.zE,
+                            static_cast<const unsigned char*>(h_in), sv + sl.os);
+    }
+    if (st != DSMP_OK) return st;
+    {
+      ProfScope prof(h, DSMP_K_GEMM_FWD);
+      st = launch_w3_gemm(h, d, g->n_dst, sv + sl.os, ea.packed + L.wgt, nsl, slices);
+    }
+    if (st != DSMP_OK) return st;
+  } else {
+    if ((st = launch_edge_contract(h, d, MODE_FWD, ea)) != DSMP_OK) return st;
+  }
   if (g->n_dst > 0) {
     NodeArgs na{g->n_dst, g->row_ptr, static_cast<const unsigned char*>(h_in), direct, part,
                 reinterpret_cast<const float*>(ea.packed + L.wr),
                 reinterpret_cast<const float*>(ea.packed + L.br), h_out,
                 static_cast<unsigned char*>(h_out_lp), reinterpret_cast<float*>(sv + sl.y), d.act,
-                d.residual};
+                d.residual, nsl, slices};
     unsigned grid = ceil_div(g->n_dst, 256 / d.d);
     if (grid > 2048) grid = 2048;
     ProfScope prof(h, DSMP_K_NODE_FWD);

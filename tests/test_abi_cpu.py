@@ -52,7 +52,10 @@ def test_host_side_queries(lib):
         s, f, b = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
         assert lib.dsmp_nnconv_workspace(ctypes.byref(desc), ctypes.byref(g), ctypes.byref(s),
                                          ctypes.byref(f), ctypes.byref(b)) == dm.OK
-        assert s.value >= 5000 * (h1 + h2) * (2 if dtype == dm.BF16 else 4)
+        esz = 2 if dtype == dm.BF16 else 4
+        # z and z1 per edge, plus the per-destination sums of the aggregate form
+        assert s.value >= 5000 * (h1 + h2) * esz + 100 * (h2 + 1) * d * esz
+    assert lib.dsmp_set_edge_algorithm(None, dm.EDGE_AGGREGATE) == dm.INVALID_ARG
 
 
 def test_unsupported_and_invalid_descriptors(lib):

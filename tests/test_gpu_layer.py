@@ -27,6 +27,19 @@ def env():
     return gpu_lib()
 
 
+# Both evaluations of the edge contraction (per edge, and aggregate-first
+# over the per-destination sums) are checked against the same oracle.
+ALGOS = ("per_edge", "aggregate")
+
+
+@pytest.fixture(params=ALGOS)
+def algo(request, env):
+    dm, lib, _ = env
+    lib.dsmp_set_edge_algorithm(dm.EDGE_PER_EDGE if request.param == "per_edge" else dm.EDGE_AGGREGATE)
+    yield request.param
+    lib.dsmp_set_edge_algorithm(dm.EDGE_AUTO)
+
+
 class Case:
     """A layer problem on the host plus its device copies."""
 
@@ -123,9 +136,9 @@ FWD_CASES = {
 
 
 @pytest.mark.parametrize("name", sorted(FWD_CASES))
-def test_forward_parity(env, name):
+def test_forward_parity(env, algo, name):
     kw = FWD_CASES[name]
-    announce("forward", name)
+    announce("forward", name, algo)
     c = random_case(env, seed=zlib.crc32(name.encode()) % 1000, **kw)
     got = c.forward()
     ref = c.oracle_forward()
@@ -134,14 +147,14 @@ def test_forward_parity(env, name):
     assert err <= TOL[c.dtype], err
 
 
-def test_forward_no_edges(env):
-    announce("forward no edges")
+def test_forward_no_edges(env, algo):
+    announce("forward no edges", algo)
     c = random_case(env, "bf16_64", n=50, r=1e-6)
     assert c.col.size == 0
     assert rel_err(c.forward(), c.oracle_forward()) <= TOL["bf16"]
 
 
-def test_forward_deterministic(env):
+def test_forward_deterministic(env, algo):
     c = random_case(env, "bf16_64", n=3000, seed=5)
     a = c.forward()
     b = c.forward()
@@ -165,8 +178,8 @@ def workload_case(env, k, layer=0, rows=None):
 
 
 @pytest.mark.parametrize("k", [1, 2])
-def test_forward_workload_full(env, k):
-    announce("forward workload", k)
+def test_forward_workload_full(env, algo, k):
+    announce("forward workload", k, algo)
     c = workload_case(env, k)
     err = rel_err(c.forward(), c.oracle_forward())
     print("E=%d err=%.3e" % (c.col.size, err))
@@ -174,8 +187,8 @@ def test_forward_workload_full(env, k):
 
 
 @pytest.mark.parametrize("k", [3, 4, 5])
-def test_forward_workload_rows(env, k):
-    announce("forward workload rows", k)
+def test_forward_workload_rows(env, algo, k):
+    announce("forward workload rows", k, algo)
     rows = np.sort(np.random.default_rng(k).choice(make_config(k).n_dst, 256, replace=False))
     c = workload_case(env, k, rows=rows)
     got = c.forward()
@@ -202,21 +215,21 @@ def _check_backward(c, label):
 
 
 @pytest.mark.parametrize("name", sorted(FWD_CASES))
-def test_backward_parity(env, name):
+def test_backward_parity(env, algo, name):
     kw = FWD_CASES[name]
-    announce("backward", name)
+    announce("backward", name, algo)
     c = random_case(env, seed=zlib.crc32(name.encode()) % 1000, **kw)
     _check_backward(c, "E=%d" % c.col.size)
 
 
-def test_backward_no_edges(env):
-    announce("backward no edges")
+def test_backward_no_edges(env, algo):
+    announce("backward no edges", algo)
     c = random_case(env, "bf16_64", n=50, r=1e-6)
     _check_backward(c, "E=0")
 
 
-def test_backward_accumulate_and_determinism(env):
-    announce("backward accumulate")
+def test_backward_accumulate_and_determinism(env, algo):
+    announce("backward accumulate", algo)
     dm, lib, torch = env
     c = random_case(env, "bf16_64", n=2000, seed=11)
     c.forward()
@@ -235,17 +248,17 @@ def test_backward_accumulate_and_determinism(env):
 
 
 @pytest.mark.parametrize("k", [1, 2])
-def test_backward_workload_full(env, k):
-    announce("backward workload", k)
+def test_backward_workload_full(env, algo, k):
+    announce("backward workload", k, algo)
     c = workload_case(env, k)
     _check_backward(c, "E=%d" % c.col.size)
 
 
 @pytest.mark.parametrize("k", [3, 4, 5])
-def test_backward_workload_rows(env, k):
+def test_backward_workload_rows(env, algo, k):
     """Sparse upstream gradient (rows only): every gradient is an exact sum
     over those rows' edges, while the GPU runs the full-size kernels."""
-    announce("backward workload rows", k)
+    announce("backward workload rows", k, algo)
     rows = np.sort(np.random.default_rng(k + 10).choice(make_config(k).n_dst, 128, replace=False))
     c = workload_case(env, k, rows=rows)
     _check_backward(c, "E=%d" % c.col.size)
