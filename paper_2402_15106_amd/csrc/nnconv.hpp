@@ -129,7 +129,7 @@ __device__ __forceinline__ void stage_wait() { __builtin_amdgcn_s_waitcnt(0x0F70
 
 // Byte offsets of the sections of a packed parameter buffer.
 struct PackLayout {
-  size_t w1l, b1l, w2p, b2, w3f, w3q, w3t, b3t, b3n, w2t, wr, br, wgt, wht, total;
+  size_t w1l, b1l, w2p, b2, w3f, w3q, w3t, b3t, b3n, w2t, wr, br, wgt, wht, w3u, total;
 };
 
 inline PackLayout pack_layout(int d, int h1, int h2, int esz) {
@@ -156,6 +156,7 @@ inline PackLayout pack_layout(int d, int h1, int h2, int esz) {
   // W3~ for the aggregate form, in the segment-sum K order (K = h2*d + d):
   L.wgt = take((size_t)d * (h2 + 1) * d * esz);   // T [q][K(k, p)]
   L.wht = take((size_t)d * (h2 + 1) * d * esz);   // T [p][K(k, q)]
+  L.w3u = take((size_t)h2 * d * d * esz);         // T [k*d + p][q] (U GEMM of the aggregate dz)
   L.total = (off + 255) & ~size_t(255);
   return L;
 }
@@ -181,6 +182,7 @@ struct EdgeArgs {
   PackLayout L;
   unsigned char* zE;             // [E][h2] layer dtype: FWD writes (if set), DH reads
   unsigned char* z1E;            // [E][h1] layer dtype: FWD writes (if set)
+  unsigned char* zmask;          // [E][(h1+h2)/8] ReLU mask bits of z1 and z: FWD writes (if set)
   float* out_direct;             // [segments][d]
   float* out_part;               // [tiles][2][d]
 };
@@ -189,10 +191,11 @@ dsmp_status launch_edge_contract(dsmp_handle* h, const dsmp_layer_desc& desc, in
                                  const EdgeArgs& a);
 
 // Per-layer buffer the forward fills for the backward: y [n_dst][d] fp32,
-// z [E][h2] and z1 [E][h1] in the layer dtype and the permuted order, and
-// the per-destination sums S [n_dst][(h2+1)d] of the aggregate form.
+// z [E][h2] and z1 [E][h1] in the layer dtype and the permuted order, their
+// ReLU mask bits [E][(h1+h2)/8], and the per-destination sums
+// S [n_dst][(h2+1)d] of the aggregate form.
 struct SavedLayout {
-  size_t y, zE, z1E, os, total;
+  size_t y, zE, z1E, zmask, os, total;
 };
 SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E);
 size_t fwd_ws_bytes(const dsmp_layer_desc& d, int64_t n_dst, int64_t E);
@@ -211,6 +214,6 @@ dsmp_status launch_outer_sum(dsmp_handle* h, const dsmp_layer_desc& d, int64_t n
 dsmp_status launch_w3_gemm(dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_rows, const unsigned char* A,
                            const unsigned char* BT, int nsl, float* part);
 dsmp_status launch_dw3_agg(dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_rows, const unsigned char* OS,
-                           const unsigned char* G, float* part, float* dW3, int accumulate);
+                           const unsigned char* G, float* part, float* dW3, float* db3, int accumulate);
 
 }  // namespace dsmp

@@ -278,11 +278,14 @@ __global__ __launch_bounds__(256) void k_dw3_agg(DW3AggArgs a) {
       const int y = iso ? x : x - S::OU;
       const int eq = y % (NCH / 4), kg = y / (NCH / 4);
       const unsigned char* r[4];
+      // columns past the end of a row (last K block) read as zeros
+      const bool inrow = !iso || kc0 + (int64_t)kg * (16 / ESZ) < a.kcols;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int sl = 4 * eq + i;
-        r[i] = sl < cnt ? (iso ? a.OS + ((size_t)(c0 + sl) * a.ktot + kc0) * ESZ : a.G + (size_t)(c0 + sl) * DL * ESZ)
-                        : nullptr;
+        r[i] = sl < cnt && inrow
+                   ? (iso ? a.OS + ((size_t)(c0 + sl) * a.ktot + kc0) * ESZ : a.G + (size_t)(c0 + sl) * DL * ESZ)
+                   : nullptr;
       }
       if (iso) put4_transposed<T, S::ROWB>(r, kg, 4 * eq, ot);
       else put4_transposed<T, S::ROWB>(r, kg, 4 * eq, gt);
@@ -310,22 +313,29 @@ __global__ __launch_bounds__(256) void k_dw3_agg(DW3AggArgs a) {
   }
 }
 
-// dW3[p*d+q][k] (+)= sum_s part[s][q][K(k, p)], K in the sum order above.
+// dW3[p*d+q][k] (+)= sum_s part[s][q][K(k, p)], K in the sum order above;
+// the bias rows K = h2*d + p give db3[p*d+q].
 template <typename T>
 __global__ __launch_bounds__(256) void k_dw3_agg_final(int d, int h2, int nsl, const float* __restrict__ part,
-                                                       float* __restrict__ dW3, int accumulate) {
-  const int64_t kcols = (int64_t)h2 * d, total = (int64_t)d * d * h2;
+                                                       float* __restrict__ dW3, float* __restrict__ db3,
+                                                       int accumulate) {
+  const int64_t kcols = (int64_t)h2 * d + d, total = (int64_t)d * kcols;
   const int nct = d / 32;
   for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < total; x += (int64_t)gridDim.x * blockDim.x) {
     // x enumerates (q, K) with K fastest, so the reads of part are contiguous
     const int q = (int)(x / kcols);
     const int64_t K = x % kcols;
-    const int ti = K / 1024, rem = K % 1024, l = rem / 16, r = rem % 16;
-    const int kt = ti / nct, ct = ti % nct;
-    const int kpos = kt * 32 + 8 * (r / 4) + 4 * (l / 32) + (r % 4), p = ct * 32 + (l % 32);
     float v = 0.0f;
     for (int s = 0; s < nsl; ++s) v += part[((int64_t)s * d + q) * kcols + K];
-    float* o = dW3 + ((int64_t)p * d + q) * h2 + kperm<T>(kpos);
+    float* o;
+    if (K < (int64_t)h2 * d) {
+      const int ti = K / 1024, rem = K % 1024, l = rem / 16, r = rem % 16;
+      const int kt = ti / nct, ct = ti % nct;
+      const int kpos = kt * 32 + 8 * (r / 4) + 4 * (l / 32) + (r % 4), p = ct * 32 + (l % 32);
+      o = dW3 + ((int64_t)p * d + q) * h2 + kperm<T>(kpos);
+    } else {
+      o = db3 + (K - (int64_t)h2 * d) * d + q;
+    }
     *o = accumulate ? *o + v : v;
   }
 }
@@ -423,9 +433,9 @@ int agg_dw3_slices(int64_t n_rows) {
 }
 
 dsmp_status launch_dw3_agg(dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_rows, const unsigned char* OS,
-                           const unsigned char* G, float* part, float* dW3, int accumulate) {
+                           const unsigned char* G, float* part, float* dW3, float* db3, int accumulate) {
   const int nsl = agg_dw3_slices(n_rows);
-  const int64_t kcols = (int64_t)d.h2 * d.d;
+  const int64_t kcols = agg_ktot(d);
   if (n_rows > 0) {
     DW3AggArgs a{n_rows, agg_ktot(d), kcols, OS, G, nsl, ceil_div(ceil_div(n_rows, nsl), 64) * 64, part};
     dsmp_status st = DSMP_UNSUPPORTED;
@@ -440,14 +450,14 @@ dsmp_status launch_dw3_agg(dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_r
     if (st != DSMP_OK) return st;
   }
   const int nuse = n_rows > 0 ? nsl : 0;
-  const int64_t total = (int64_t)d.d * d.d * d.h2;
+  const int64_t total = (int64_t)d.d * kcols;
   unsigned grid = (unsigned)ceil_div(total, 256);
   if (grid > 8192) grid = 8192;
   if (d.dtype == DSMP_F32)
-    hipLaunchKernelGGL(k_dw3_agg_final<float>, dim3(grid), dim3(256), 0, h->stream, d.d, d.h2, nuse, part, dW3,
+    hipLaunchKernelGGL(k_dw3_agg_final<float>, dim3(grid), dim3(256), 0, h->stream, d.d, d.h2, nuse, part, dW3, db3,
                        accumulate);
   else
-    hipLaunchKernelGGL(k_dw3_agg_final<__bf16>, dim3(grid), dim3(256), 0, h->stream, d.d, d.h2, nuse, part, dW3,
+    hipLaunchKernelGGL(k_dw3_agg_final<__bf16>, dim3(grid), dim3(256), 0, h->stream, d.d, d.h2, nuse, part, dW3, db3,
                        accumulate);
   DSMP_LAUNCHED(h, "dW3 assembly");
   return DSMP_OK;

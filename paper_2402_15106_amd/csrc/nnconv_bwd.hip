@@ -197,9 +197,13 @@ struct DzArgs {
   const unsigned char* packed;
   PackLayout L;
   const unsigned char* zE;     // [E][h2] permuted order
-  const unsigned char* z1E;    // [E][h1] permuted order
+  const unsigned char* zmask;  // [E][(h1+h2)/8] ReLU mask bits of z1 and z (forward)
   unsigned char* da2E;         // [E][h2] permuted order, layer dtype
-  float* da1E;                 // [E][h1] permuted order
+  unsigned char* da1E;         // [E][h1] permuted order, layer dtype
+  const unsigned char* U;      // aggregate form: [n_dst][h2][d] layer dtype, U_i[k][p]
+  const unsigned char* gT;     // aggregate form: g_i [n_dst][d] layer dtype
+  int64_t n_dst;
+  const int32_t* row_ptr;      // aggregate form: edges of each destination
 };
 
 template <typename T, int DL, int H1, int H2>
@@ -214,6 +218,67 @@ struct DzShape {
   static constexpr int STAGE = RCH * ROWB, HROWB = DL * ESZ + 16;
   static constexpr int LDS = 2 * STAGE + TILE * HROWB;
 };
+
+// Epilogue of the dz kernels: acc[t][kt] holds dz of the lane's edge (tile t)
+// for k in tile kt (register i is permuted position 16*kt + i).  Writes
+// da2 = dz * [z > 0] (permuted order), then dz1 = W2^T da2 on MFMA and
+// da1 = dz1 * [z1 > 0].
+template <typename T, int DL, int H1, int H2, int NT, int KT>
+__device__ __forceinline__ void dz_finish(const DzArgs& a, const f32x16 (&acc)[NT][KT], const int64_t (&eid)[NT],
+                                          const bool (&valid)[NT], int hh) {
+  using S = DzShape<T, DL, H1, H2>;
+  using M = MT<T>;
+  using frag = typename M::frag;
+  constexpr int KS = S::KS, EPL = S::EPL, ESZ = S::ESZ;
+  const int l32 = threadIdx.x & 31;
+  const unsigned char* P = a.packed;
+  const unsigned char* w2t = P + a.L.w2t;
+  constexpr int MW1 = H1 / 64, MW2 = H2 / 64;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const size_t e = valid[t] ? (size_t)eid[t] : 0;
+    // the lane's mask bits: bit b of its half <-> position (b/EPL)*KS + hh*EPL + b%EPL
+    uint32_t m1[MW1], m2[MW2];
+    {
+      const uint32_t* mb = reinterpret_cast<const uint32_t*>(a.zmask + e * ((H1 + H2) / 8));
+#pragma unroll
+      for (int w = 0; w < MW1; ++w) m1[w] = mb[hh * MW1 + w];
+#pragma unroll
+      for (int w = 0; w < MW2; ++w) m2[w] = mb[2 * MW1 + hh * MW2 + w];
+    }
+    frag da2B[S::SK2];
+#pragma unroll
+    for (int s = 0; s < S::SK2; ++s) {
+      float v[EPL];
+#pragma unroll
+      for (int u = 0; u < EPL; ++u) {
+        const int n = s * EPL + u;
+        v[u] = (m2[n / 32] >> (n % 32)) & 1u ? acc[t][n / 16][n % 16] : 0.0f;
+      }
+      da2B[s] = pack_frag<T>(v);
+      if (valid[t]) *reinterpret_cast<frag*>(a.da2E + (e * H2 + s * KS + hh * EPL) * ESZ) = da2B[s];
+    }
+#pragma unroll
+    for (int jt = 0; jt < S::JT; ++jt) {
+      f32x16 C = f32x16{};
+#pragma unroll
+      for (int s = 0; s < S::SK2; ++s) {
+        frag A = ld_frag<T>(w2t + ((size_t)(jt * 32 + l32) * H2 + s * KS + hh * EPL) * ESZ);
+        C = M::mma(A, da2B[s], C);
+      }
+      // register i of tile jt is permuted position n = 16*jt + i
+#pragma unroll
+      for (int i = 0; i < 16; i += EPL) {
+        const int n = 16 * jt + i;
+        const int pos = (n / EPL) * KS + hh * EPL;
+        float v[EPL];
+#pragma unroll
+        for (int u = 0; u < EPL; ++u) v[u] = (m1[(n + u) / 32] >> ((n + u) % 32)) & 1u ? C[i + u] : 0.0f;
+        if (valid[t]) *reinterpret_cast<frag*>(a.da1E + (e * H1 + pos) * ESZ) = pack_frag<T>(v);
+      }
+    }
+  }
+}
 
 // dz_e[k] = sum_p h_j[p] sum_q W3[p*d+q][k] g_e[q], accumulated as
 // sum_p W3T[p] (h_j[p] g_e): the scale is folded into the B operand, so the
@@ -332,49 +397,100 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
     }
   }
 
-  // da2 = dz * [z > 0] in the permuted order, then dz1 = W2^T da2 and da1
-  const unsigned char* w2t = P + a.L.w2t;
+  dz_finish<T, DL, H1, H2, NT, S::KT>(a, acc, eid, valid, hh);
+}
+
+// Aggregate form of dz.  With U_i[k][p] = sum_q W3[p*d+q][k] g_i[q] for
+// every destination (one GEMM, k_u_gemm), dz_e[k] = sum_p U_i[k][p] h_j[p]
+// for each edge e into i.  One wave per destination: its edges in chunks of
+// two 32-edge tiles, the A operand is U_i^T read once per chunk, the B
+// operand the lane's own gathered row h_j (zero past the destination's last
+// edge).
+template <typename T, int DL, int H1, int H2>
+__global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) void k_bwd_dz_agg(DzArgs a) {
+  using S = DzShape<T, DL, H1, H2>;
+  using M = MT<T>;
+  using frag = typename M::frag;
+  constexpr int KS = S::KS, EPL = S::EPL, ESZ = S::ESZ, KT = S::KT, SKD = S::SKD, NT = S::NT;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int64_t i = (int64_t)blockIdx.x * 4 + wv;
+  if (i >= a.n_dst) return;
+  const int64_t pa = a.row_ptr[i], pb = a.row_ptr[i + 1];
+  const unsigned char* ur = a.U + ((size_t)i * H2 + l32) * DL * ESZ + hh * EPL * ESZ;
+  for (int64_t c0 = pa; c0 < pb; c0 += 32 * NT) {
+    int64_t eid[NT];
+    bool valid[NT];
+    frag hB[NT][SKD];
 #pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    const size_t e = valid[t] ? (size_t)eid[t] : 0;
-    frag da2B[S::SK2];
+    for (int t = 0; t < NT; ++t) {
+      eid[t] = c0 + t * 32 + l32;
+      valid[t] = eid[t] < pb;
+      const unsigned char* hr = a.h_in + (size_t)(valid[t] ? a.col[eid[t]] : 0) * DL * ESZ;
 #pragma unroll
-    for (int s = 0; s < S::SK2; ++s) {
-      const frag zf = ld_frag<T>(a.zE + (e * H2 + s * KS + hh * EPL) * ESZ);
-      float v[EPL];
-#pragma unroll
-      for (int u = 0; u < EPL; ++u) {
-        const int n = s * EPL + u;
-        v[u] = get_el<T>(zf, u) > 0.0f ? acc[t][n / 16][n % 16] : 0.0f;
-      }
-      da2B[s] = pack_frag<T>(v);
-      if (valid[t]) *reinterpret_cast<frag*>(a.da2E + (e * H2 + s * KS + hh * EPL) * ESZ) = da2B[s];
+      for (int s = 0; s < SKD; ++s) hB[t][s] = valid[t] ? ld_frag<T>(hr + (s * KS + hh * EPL) * ESZ) : frag{};
     }
+    f32x16 acc[NT][KT];
 #pragma unroll
-    for (int jt = 0; jt < S::JT; ++jt) {
-      f32x16 C = f32x16{};
+    for (int kt = 0; kt < KT; ++kt) {
+      frag A[SKD];
 #pragma unroll
-      for (int s = 0; s < S::SK2; ++s) {
-        frag A = ld_frag<T>(w2t + ((size_t)(jt * 32 + l32) * H2 + s * KS + hh * EPL) * ESZ);
-        C = M::mma(A, da2B[s], C);
+      for (int s = 0; s < SKD; ++s) A[s] = ld_frag<T>(ur + ((size_t)kt * 32 * DL + s * KS) * ESZ);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        acc[t][kt] = f32x16{};
+        if (t == 0 || c0 + 32 * t < pb)   // wave-uniform: tile t has edges
+#pragma unroll
+          for (int s = 0; s < SKD; ++s) acc[t][kt] = M::mma(A[s], hB[t][s], acc[t][kt]);
       }
-      // register i of tile jt is permuted position n = 16*jt + i
+    }
+    dz_finish<T, DL, H1, H2, NT, KT>(a, acc, eid, valid, hh);
+  }
+}
+
+struct UArgs {
+  int64_t n_rows;
+  const unsigned char* G;    // [n_rows][DL] layer dtype (g_i)
+  const unsigned char* W;    // [h2*DL][DL] layer dtype: W[k*DL + p][q] = W3[p*DL+q][k]
+  unsigned char* U;          // [n_rows][h2*DL] layer dtype
+};
+
+// U[i][c] = sum_q W[c][q] g_i[q] for c = k*DL + p, as tiles C[c][i] (A = W
+// rows, B = the g rows, lane = destination), so each lane writes runs of four
+// consecutive c.  A wave covers 32 destinations and 256 columns.
+template <typename T, int DL, int H2>
+__global__ __launch_bounds__(256) void k_u_gemm(UArgs a) {
+  using M = MT<T>;
+  using frag = typename M::frag;
+  constexpr int KS = M::KS, EPL = M::EPL, ESZ = sizeof(T), SKD = DL / KS, NC = H2 * DL;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int64_t i0 = (int64_t)blockIdx.x * 32;
+  const int64_t c0 = ((int64_t)blockIdx.y * 4 + wv) * 256;
+  if (c0 >= NC) return;
+  const int64_t row = i0 + l32 < a.n_rows ? i0 + l32 : a.n_rows - 1;
+  frag B[SKD];
 #pragma unroll
-      for (int i = 0; i < 16; i += EPL) {
-        const int n = 16 * jt + i;
-        const int pos = (n / EPL) * KS + hh * EPL;
-        const frag z1f = ld_frag<T>(a.z1E + (e * H1 + pos) * ESZ);
-        float v[EPL];
+  for (int s = 0; s < SKD; ++s) B[s] = ld_frag<T>(a.G + ((size_t)row * DL + s * KS + hh * EPL) * ESZ);
+  T* out = reinterpret_cast<T*>(a.U) + (size_t)(i0 + l32) * NC;
+  const bool ok = i0 + l32 < a.n_rows;
+#pragma unroll 2
+  for (int ct = 0; ct < 8; ++ct) {
+    const int64_t c = c0 + ct * 32;
+    frag A[SKD];
 #pragma unroll
-        for (int u = 0; u < EPL; ++u) v[u] = get_el<T>(z1f, u) > 0.0f ? C[i + u] : 0.0f;
-        if (valid[t]) {
-          float* dst = a.da1E + e * H1 + pos;
-          if constexpr (EPL == 8) {
-            *reinterpret_cast<f32x4*>(dst) = f32x4{v[0], v[1], v[2], v[3]};
-            *reinterpret_cast<f32x4*>(dst + 4) = f32x4{v[4], v[5], v[6], v[7]};
-          } else {
-            dst[0] = v[0];
-          }
+    for (int s = 0; s < SKD; ++s) A[s] = ld_frag<T>(a.W + ((size_t)(c + l32) * DL + s * KS + hh * EPL) * ESZ);
+    f32x16 C = f32x16{};
+#pragma unroll
+    for (int s = 0; s < SKD; ++s) C = M::mma(A[s], B[s], C);
+    if (ok) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        T* o = out + c + 8 * g + 4 * hh;
+        if constexpr (ESZ == 2) {
+          const bf16x2 lo = __builtin_convertvector((f32x2){C[4 * g], C[4 * g + 1]}, bf16x2);
+          const bf16x2 hi = __builtin_convertvector((f32x2){C[4 * g + 2], C[4 * g + 3]}, bf16x2);
+          *reinterpret_cast<uint2*>(o) = make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+        } else {
+          *reinterpret_cast<f32x4*>(o) = f32x4{C[4 * g], C[4 * g + 1], C[4 * g + 2], C[4 * g + 3]};
         }
       }
     }
@@ -702,10 +818,10 @@ __global__ __launch_bounds__(256, 1) void k_bwd_dW2(W2Args a) {
 
 // ------------------------------------------------------------ dW1 / db1 (split over edges)
 
-template <int H1>
+template <typename T, int H1>
 __global__ __launch_bounds__(256) void k_bwd_dW1(int64_t E, int64_t per_chunk, const int32_t* __restrict__ col,
                                                  const int32_t* __restrict__ dst, const float* __restrict__ node_attr,
-                                                 int dim, int attr_mode, int de, const float* __restrict__ da1E,
+                                                 int dim, int attr_mode, int de, const T* __restrict__ da1E,
                                                  const int* __restrict__ jof, float* __restrict__ part) {
   constexpr int SUB = 256 / H1, XB = 256;
   __shared__ float xs[XB][9];
@@ -731,7 +847,7 @@ __global__ __launch_bounds__(256) void k_bwd_dW1(int64_t E, int64_t per_chunk, c
     const int n = e1 - eb < XB ? (int)(e1 - eb) : XB;
 #pragma unroll 4
     for (int u = sub; u < n; u += SUB) {
-      const float v = da1E[(eb + u) * H1 + kk];
+      const float v = to_f(da1E[(eb + u) * H1 + kk]);
 #pragma unroll
       for (int c = 0; c < 9; ++c) acc[c] += v * xs[u][c];
     }
@@ -818,8 +934,8 @@ __global__ void k_jof(int* out, int h1, int isbf16) {
 // ------------------------------------------------------------ workspace
 
 struct BwdWs {
-  float *ybar, *gF, *dh_node, *dh_direct, *dh_part, *da1E, *dh_sl;
-  unsigned char *gT, *da2E, *ot;
+  float *ybar, *gF, *dh_node, *dh_direct, *dh_part, *dh_sl;
+  unsigned char *gT, *da2E, *da1E, *ot, *U;
   int nslh;
   float *p_root, *p_db3, *p_w3, *p_w2, *p_w1;
   int* jof;
@@ -861,8 +977,9 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   w.ot = c.take<unsigned char>((size_t)n_src * agg_ktot(d) * esz);
   w.nslh = agg_gemm_slices(n_src, d);
   w.dh_sl = c.take<float>((size_t)w.nslh * n_src * d.d);
+  w.U = c.take<unsigned char>((size_t)n_dst * d.h2 * d.d * esz);
   w.da2E = c.take<unsigned char>((size_t)E * d.h2 * esz);
-  w.da1E = c.take<float>((size_t)E * d.h1);
+  w.da1E = c.take<unsigned char>((size_t)E * d.h1 * esz);
   w.nr = (int)(n_dst > 0 ? (ceil_div(n_dst, 32) < 1024 ? ceil_div(n_dst, 32) : 1024) : 1);
   w.pr = n_dst > 0 ? ceil_div(n_dst, w.nr) : 1;
   w.p_root = c.take<float>((size_t)w.nr * (d.d * d.d + d.d));
@@ -873,8 +990,9 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   w.pc3 = ((E + w.n3 - 1) / w.n3 + 63) / 64 * 64;
   if (w.pc3 < 64) w.pc3 = 64;
   // dW3 partials: per-edge chunks, or the node slices of the aggregate form
-  const int n3a = agg_dw3_slices(n_dst);
-  w.p_w3 = c.take<float>((size_t)(w.n3 > n3a ? w.n3 : n3a) * d.d * d.d * d.h2);
+  const size_t p3e = (size_t)w.n3 * d.d * d.d * d.h2;
+  const size_t p3a = (size_t)agg_dw3_slices(n_dst) * d.d * agg_ktot(d);
+  w.p_w3 = c.take<float>(p3e > p3a ? p3e : p3a);
   w.n2 = (int)(E > 0 ? (ceil_div(E, 2048) < 512 ? ceil_div(E, 2048) : 512) : 1);
   w.pc2 = ((E + w.n2 - 1) / w.n2 + 63) / 64 * 64;
   if (w.pc2 < 64) w.pc2 = 64;
@@ -898,7 +1016,16 @@ template <typename T, int DL, int H1, int H2>
 dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, const W2Args& w2) {
   hipStream_t s = h->stream;
   dsmp_status st;
-  if (dz.E > 0) {
+  if (dz.E > 0 && dz.U) {
+    // aggregate form: U = g W3 for every destination, then the masked per-tile products
+    using S = DzShape<T, DL, H1, H2>;
+    ProfScope prof(h, DSMP_K_DZ);
+    UArgs ua{dz.n_dst, dz.gT, dz.packed + dz.L.w3u, const_cast<unsigned char*>(dz.U)};
+    hipLaunchKernelGGL((k_u_gemm<T, DL, H2>), dim3((unsigned)ceil_div(dz.n_dst, 32), (unsigned)ceil_div(H2 * DL, 1024)),
+                       dim3(256), 0, s, ua);
+    hipLaunchKernelGGL((k_bwd_dz_agg<T, DL, H1, H2>), dim3((unsigned)ceil_div(dz.n_dst, 4)), dim3(256), 0, s, dz);
+    DSMP_LAUNCHED(h, "dz (aggregate form)");
+  } else if (dz.E > 0) {
     using S = DzShape<T, DL, H1, H2>;
     auto kz = k_bwd_dz<T, DL, H1, H2>;
     if ((st = set_lds(h, kz, S::LDS)) != DSMP_OK) return st;
@@ -942,15 +1069,16 @@ dsmp_status dispatch_edge_grads(dsmp_handle* h, const dsmp_layer_desc& d, const 
 
 template <typename T, int DL>
 void launch_node_kernels(dsmp_handle* h, const BNodeArgs& na, int64_t n_dst, const BwdWs& w,
-                         const unsigned char* h_in, const int32_t* row_ptr, const int32_t* col) {
+                         const unsigned char* h_in, const int32_t* row_ptr, const int32_t* col, bool db3) {
   hipStream_t s = h->stream;
   if (n_dst == 0) return;
   unsigned grid = ceil_div(n_dst, 256 / DL);
   if (grid > 2048) grid = 2048;
   hipLaunchKernelGGL((k_bwd_node<T, DL>), dim3(grid), dim3(256), 0, s, na);
   hipLaunchKernelGGL((k_bwd_root<T, DL>), dim3(w.nr), dim3(256), 0, s, n_dst, w.pr, w.ybar, h_in, w.p_root);
-  hipLaunchKernelGGL((k_bwd_db3<T, DL>), dim3(w.nb3), dim3(256), 0, s, n_dst, w.pb3, row_ptr, col, h_in, w.gF,
-                     w.p_db3);
+  if (db3)
+    hipLaunchKernelGGL((k_bwd_db3<T, DL>), dim3(w.nb3), dim3(256), 0, s, n_dst, w.pb3, row_ptr, col, h_in, w.gF,
+                       w.p_db3);
 }
 
 }  // namespace
@@ -999,22 +1127,23 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   const int acc = flags & DSMP_GRAD_ACCUMULATE;
   const int64_t E = g->n_edges, n_dst = g->n_dst, n_src = g->n_src;
 
-  // node pre-pass, root grads, db3 partials
+  const bool agg = use_aggregate(h, d, n_dst, E);
+
+  // node pre-pass, root grads, db3 partials (the aggregate form takes db3
+  // from the bias rows of its dW3 product)
   ProfScope prof_node(h, DSMP_K_NODE_BWD);
   BNodeArgs na{n_dst, g->row_ptr, grad_out, reinterpret_cast<const float*>(sv + sl.y),
                reinterpret_cast<const float*>(pk + L.wr), w.ybar, w.gT, w.gF, w.dh_node, d.act, d.residual};
   if (d.dtype == DSMP_BF16) {
-    if (d.d == 32) launch_node_kernels<__bf16, 32>(h, na, n_dst, w, hin, g->row_ptr, g->col);
-    if (d.d == 64) launch_node_kernels<__bf16, 64>(h, na, n_dst, w, hin, g->row_ptr, g->col);
-    if (d.d == 128) launch_node_kernels<__bf16, 128>(h, na, n_dst, w, hin, g->row_ptr, g->col);
+    if (d.d == 32) launch_node_kernels<__bf16, 32>(h, na, n_dst, w, hin, g->row_ptr, g->col, !agg);
+    if (d.d == 64) launch_node_kernels<__bf16, 64>(h, na, n_dst, w, hin, g->row_ptr, g->col, !agg);
+    if (d.d == 128) launch_node_kernels<__bf16, 128>(h, na, n_dst, w, hin, g->row_ptr, g->col, !agg);
   } else {
-    if (d.d == 32) launch_node_kernels<float, 32>(h, na, n_dst, w, hin, g->row_ptr, g->col);
-    if (d.d == 64) launch_node_kernels<float, 64>(h, na, n_dst, w, hin, g->row_ptr, g->col);
+    if (d.d == 32) launch_node_kernels<float, 32>(h, na, n_dst, w, hin, g->row_ptr, g->col, !agg);
+    if (d.d == 64) launch_node_kernels<float, 64>(h, na, n_dst, w, hin, g->row_ptr, g->col, !agg);
   }
   DSMP_LAUNCHED(h, "backward node kernels");
   prof_node.end();
-
-  const bool agg = use_aggregate(h, d, n_dst, E);
 
   // feature gradient through the edges (edge contraction in source order)
   EdgeArgs ea{};
@@ -1051,29 +1180,39 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
 
   // kernel-MLP gradients
   if (E > 0) {
-    DzArgs dz{E, g->col, g->dst, hin, w.gF, pk, L, sv + sl.zE, sv + sl.z1E, w.da2E, w.da1E};
+    DzArgs dz{E, g->col, g->dst, hin, w.gF, pk, L, sv + sl.zE, sv + sl.zmask, w.da2E, w.da1E,
+              agg ? w.U : nullptr, w.gT, n_dst, g->row_ptr};
     W3Args w3{E, w.pc3, agg ? 0 : w.n3, g->col, g->dst, hin, w.gF, sv + sl.zE, w.p_w3};
     W2Args w2{E, w.pc2, 1, w.da2E, sv + sl.z1E, w.p_w2};
     if ((st = dispatch_edge_grads(h, d, dz, w3, w2)) != DSMP_OK) return st;
     hipLaunchKernelGGL(k_jof, dim3(ceil_div(d.h1, 256)), dim3(256), 0, s, w.jof, d.h1, d.dtype == DSMP_BF16);
     int n1 = (int)((E + w.pc1 - 1) / w.pc1);
     ProfScope prof(h, DSMP_K_DW1);
-    if (d.h1 == 64)
-      hipLaunchKernelGGL((k_bwd_dW1<64>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr, d.dim,
-                         d.attr_mode, de, w.da1E, w.jof, w.p_w1);
+    const __bf16* da1b = reinterpret_cast<const __bf16*>(w.da1E);
+    const float* da1f = reinterpret_cast<const float*>(w.da1E);
+    if (d.dtype == DSMP_F32 && d.h1 == 64)
+      hipLaunchKernelGGL((k_bwd_dW1<float, 64>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
+                         d.dim, d.attr_mode, de, da1f, w.jof, w.p_w1);
+    else if (d.dtype == DSMP_F32)
+      hipLaunchKernelGGL((k_bwd_dW1<float, 128>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
+                         d.dim, d.attr_mode, de, da1f, w.jof, w.p_w1);
+    else if (d.h1 == 64)
+      hipLaunchKernelGGL((k_bwd_dW1<__bf16, 64>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
+                         d.dim, d.attr_mode, de, da1b, w.jof, w.p_w1);
     else if (d.h1 == 128)
-      hipLaunchKernelGGL((k_bwd_dW1<128>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr, d.dim,
-                         d.attr_mode, de, w.da1E, w.jof, w.p_w1);
+      hipLaunchKernelGGL((k_bwd_dW1<__bf16, 128>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
+                         d.dim, d.attr_mode, de, da1b, w.jof, w.p_w1);
     else
-      hipLaunchKernelGGL((k_bwd_dW1<256>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr, d.dim,
-                         d.attr_mode, de, w.da1E, w.jof, w.p_w1);
+      hipLaunchKernelGGL((k_bwd_dW1<__bf16, 256>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
+                         d.dim, d.attr_mode, de, da1b, w.jof, w.p_w1);
     DSMP_LAUNCHED(h, "dW1");
   }
 
   if (agg) {
     // dW3[p*d+q][k] = sum_i g_i[q] S_i[k][p] from the forward's sums
     ProfScope prof(h, DSMP_K_DW3);
-    if ((st = launch_dw3_agg(h, d, n_dst, sv + sl.os, w.gT, w.p_w3, grads->dW3, acc)) != DSMP_OK) return st;
+    if ((st = launch_dw3_agg(h, d, n_dst, sv + sl.os, w.gT, w.p_w3, grads->dW3, grads->db3, acc)) != DSMP_OK)
+      return st;
   }
 
   // fixed-order reductions into the caller's gradients
@@ -1091,7 +1230,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   ProfScope prof_red(h, DSMP_K_REDUCE);
   red(w.p_root, nr, dd + d.d, 0, dd, grads->dWr);
   red(w.p_root, nr, dd + d.d, dd, d.d, grads->dbr);
-  red(w.p_db3, nr, dd, 0, dd, grads->db3);
+  if (!agg) red(w.p_db3, nr, dd, 0, dd, grads->db3);
   if (!agg) red(w.p_w3, n3, dd * d.h2, 0, dd * d.h2, grads->dW3);
   red(w.p_w2, n2, (int64_t)d.h2 * d.h1 + d.h2, 0, (int64_t)d.h2 * d.h1, grads->dW2);
   red(w.p_w2, n2, (int64_t)d.h2 * d.h1 + d.h2, (int64_t)d.h2 * d.h1, d.h2, grads->db2);

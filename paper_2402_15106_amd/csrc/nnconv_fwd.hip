@@ -180,6 +180,17 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
     stage_wait();
     __syncthreads();   // rows, W1 and W2 are in LDS
     frag z1B[NT][S::SK1];
+    // ReLU masks for the backward: bit s*EPL+u of the lane's half is
+    // [value at position s*KS + hh*EPL + u > 0] (z1 words, then z words)
+    constexpr int MW1 = H1 / 64, MW2 = H2 / 64;
+    uint32_t m1[NT][MW1], m2[NT][MW2];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+#pragma unroll
+      for (int w = 0; w < MW1; ++w) m1[t][w] = 0u;
+#pragma unroll
+      for (int w = 0; w < MW2; ++w) m2[t][w] = 0u;
+    }
     const float* w1h = w1s + hh * (H1 / 2) * 8;
     const float* b1h = w1s + H1 * 8 + hh * (H1 / 2);
 #pragma unroll
@@ -200,6 +211,7 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
           v = __builtin_fmaf(wb[0], x[t][4], v); v = __builtin_fmaf(wb[1], x[t][5], v);
           v = __builtin_fmaf(wb[2], x[t][6], v); v = __builtin_fmaf(wb[3], x[t][7], v);
           zv[t][u] = v > 0.0f ? v : 0.0f;
+          if (v > 0.0f) m1[t][(s * EPL + u) / 32] |= 1u << ((s * EPL + u) % 32);
         }
       }
 #pragma unroll
@@ -251,6 +263,8 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
             for (int u = 0; u < EPL; ++u) {
               const float v = C[t][i0 + u] + bb[i0 + u];
               zv[u] = v > 0.0f ? v : 0.0f;
+              const int b = 16 * kt + i0 + u;
+              if (v > 0.0f) m2[t][b / 32] |= 1u << (b % 32);
             }
             zB[t][(16 * kt + i0) / EPL] = pack_frag<T>(zv);
           }
@@ -263,6 +277,17 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
 #pragma unroll
           for (int s = 0; s < S::SK2; ++s)
             *reinterpret_cast<frag*>(a.zE + ((size_t)eid[t] * H2 + s * KS + hh * EPL) * ESZ) = zB[t][s];
+    }
+    if (a.zmask) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        if (valid[t]) {
+          uint32_t* mb = reinterpret_cast<uint32_t*>(a.zmask + (size_t)eid[t] * ((H1 + H2) / 8));
+#pragma unroll
+          for (int w = 0; w < MW1; ++w) mb[hh * MW1 + w] = m1[t][w];
+#pragma unroll
+          for (int w = 0; w < MW2; ++w) mb[2 * MW1 + hh * MW2 + w] = m2[t][w];
+        }
     }
     if constexpr (MODE == MODE_MLP) return;
     __syncthreads();   // every wave is done with W2: the first W3 chunk takes its place
@@ -557,6 +582,13 @@ __global__ void k_pack(PackArgs a) {
       wht[x] = (T)a.b3[o * d + c];
     }
   }
+  T* w3u = reinterpret_cast<T*>(a.out + a.L.w3u);
+  for (int64_t x = t0; x < (int64_t)h2 * d * d; x += stride) {
+    const int q = (int)(x % d);
+    const int64_t c = x / d;
+    const int k = (int)(c / d), p = (int)(c % d);
+    w3u[x] = (T)a.W3[((int64_t)p * d + q) * h2 + k];
+  }
 }
 
 template <typename K>
@@ -658,6 +690,7 @@ SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E) {
   s.y = (size_t)c.take<float>((size_t)n_dst * d.d) ;
   s.zE = (size_t)c.take<unsigned char>((size_t)E * d.h2 * esz);
   s.z1E = (size_t)c.take<unsigned char>((size_t)E * d.h1 * esz);
+  s.zmask = (size_t)c.take<unsigned char>((size_t)E * (d.h1 + d.h2) / 8);
   s.os = (size_t)c.take<unsigned char>((size_t)n_dst * agg_ktot(d) * esz);
   s.total = c.used();
   return s;
@@ -757,7 +790,7 @@ extern "C" dsmp_status dsmp_nnconv_forward(dsmp_handle* h, const dsmp_layer_desc
   ea.node_attr = node_attr; ea.dim = d.dim; ea.attr_mode = d.attr_mode;
   ea.gath = static_cast<const unsigned char*>(h_in);
   ea.packed = static_cast<const unsigned char*>(packed); ea.L = L;
-  ea.zE = sv + sl.zE; ea.z1E = sv + sl.z1E;
+  ea.zE = sv + sl.zE; ea.z1E = sv + sl.z1E; ea.zmask = sv + sl.zmask;
   ea.out_direct = direct; ea.out_part = part;
   if (agg) {
     // z and z1 per edge, the per-destination sums S (kept for the backward),
