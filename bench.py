@@ -14,6 +14,14 @@ with fp32 accumulation.  Prints one JSON line.
 
 value = edges/s = E * layers / (seconds per step), i.e. edge-layer passes
 (forward + backward) per second, sampling and graph build included.
+
+Per kernel class the line carries the algorithmic work of one launch (flops,
+and the compulsory HBM bytes: inputs read once, outputs written once), the
+rates these give over the HIP-event launch time, and the bound (MFMA or HBM
+by arithmetic intensity).  `roofline` is that of the class taking the most
+time per step.  `method_tflops_step` is the nominal flop count of eq. (1)
+per edge (the per-edge evaluation's) over the step time: a yardstick only,
+the aggregate form does far fewer operations.
 """
 
 import argparse
@@ -36,6 +44,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2)")
+    ap.add_argument("--algo", choices=["auto", "per_edge", "aggregate"], default="auto",
+                    help="edge-contraction form (default: the library's automatic choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=1536,
                     help="destination rows of the oracle's timed layer sample")
@@ -43,27 +53,35 @@ def parse():
 
 
 TRAFFIC_TABLE = os.path.join(ROOT, "profiles", "darcy256_bf16_traffic.md")
+SRC_FWD = ["nnconv_fwd.hip", "nnconv.hpp", "common.hpp"]
+SRC_BWD = ["nnconv_bwd.hip", "nnconv.hpp", "common.hpp"]
+SRC_AGG = ["nnconv_agg.hip", "nnconv.hpp", "common.hpp"]
 KERNEL_SOURCES = {
-    "edge_fwd": ["nnconv_fwd.hip", "nnconv.hpp", "common.hpp"],
-    "edge_dh": ["nnconv_fwd.hip", "nnconv.hpp", "common.hpp"],
-    "dz": ["nnconv_bwd.hip", "nnconv.hpp", "common.hpp"],
-    "dW3": ["nnconv_bwd.hip", "nnconv.hpp", "common.hpp"],
-    "dW2": ["nnconv_bwd.hip", "nnconv.hpp", "common.hpp"],
+    "edge_fwd": SRC_FWD, "edge_dh": SRC_FWD, "edge_mlp": SRC_FWD,
+    "dz": SRC_BWD, "u_gemm": SRC_BWD, "dW2": SRC_BWD, "dW1": SRC_BWD,
+    "dW3": SRC_BWD + ["nnconv_agg.hip"],
+    "outer_fwd": SRC_AGG, "gemm_fwd": SRC_AGG, "outer_dh": SRC_AGG, "gemm_dh": SRC_AGG,
 }
+HBM_TBPS = 8.0                 # MI355X HBM3E peak (8 TB/s published)
+RIDGE = PEAK_BF16_TFLOPS / HBM_TBPS   # flop/byte where the two rooflines meet (bf16)
+
+
+def source_digest(cls):
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[cls]:
+        with open(os.path.join(ROOT, "paper_2402_15106_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(cls, workload):
     """HBM bytes per launch of kernel class ``cls`` from the committed
     rocprofv3 FETCH_SIZE/WRITE_SIZE table, or None when the table covers
     another workload or the kernel's sources changed since it was taken."""
-    import hashlib
     if workload != "darcy256-bf16" or cls not in KERNEL_SOURCES or not os.path.exists(TRAFFIC_TABLE):
         return None
-    h = hashlib.sha256()
-    for f in KERNEL_SOURCES[cls]:
-        with open(os.path.join(ROOT, "paper_2402_15106_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    digest = h.hexdigest()[:16]
+    digest = source_digest(cls)
     for line in open(TRAFFIC_TABLE):
         cells = [c.strip() for c in line.strip().strip("|").split("|")]
         if len(cells) == 6 and cells[0] == cls:
@@ -71,16 +89,68 @@ def measured_traffic(cls, workload):
     return None
 
 
-def per_edge_flops(w):
-    """Nominal method work per retained edge (one kernel evaluation, eq. (1))."""
+def method_flops_per_edge(w):
+    """Nominal work of eq. (1) per retained edge, forward + backward, as the
+    per-edge evaluation does it (the aggregate form reaches the same result
+    with far fewer operations; this is the yardstick, not its count)."""
     d, H1, H2, de = w.d, w.H1, w.H2, w.de
+    return (8 * H2 + 6) * d * d + 6 * H1 * H2 + 4 * de * H1
+
+
+def gemm_slices(n_rows):
+    """K slices of the library's W3 GEMM over segment sums (agg_gemm_slices)."""
+    waves = max(1, -(-n_rows // 32))
+    return max(1, min(16, 2048 // waves))
+
+
+def work_model(w, E, n_src):
+    """Algorithmic work of one launch of each kernel class: flops and the
+    compulsory HBM bytes (every input read once, every output written once)."""
+    d, H1, H2, de, D = w.d, w.H1, w.H2, w.de, w.D
+    n = w.n_dst
+    esz = 2 if w.dtype == "bf16" else 4
+    kt = (H2 + 1) * d                  # length of a segment-sum row
+    mask = (H1 + H2) // 8              # ReLU mask bytes per edge
+    idx = 8                            # two int32 indices per edge
+    attr = 2 * (D + 1) * 4             # node attribute rows of both ends
+    m = {
+        # per-edge form
+        "edge_fwd": (2 * E * (de * H1 + H1 * H2) + 2 * E * (H2 + 1) * d * d,
+                     E * (idx + attr + d * esz + (H1 + H2) * esz + mask) + n * d * 4),
+        "edge_dh": (2 * E * (H2 + 1) * d * d, E * (idx + d * esz + H2 * esz) + n_src * d * 4),
+        # aggregate form
+        "edge_mlp": (2 * E * (de * H1 + H1 * H2), E * (idx + attr + (H1 + H2) * esz + mask)),
+        "outer_fwd": (2 * E * H2 * d, E * (4 + H2 * esz + d * esz) + n * kt * esz),
+        "gemm_fwd": (2 * n * kt * d, n * kt * esz + gemm_slices(n) * n * d * 4),
+        "outer_dh": (2 * E * H2 * d, E * (idx + H2 * esz + d * esz) + n_src * kt * esz),
+        "gemm_dh": (2 * n_src * kt * d, n_src * kt * esz + gemm_slices(n_src) * n_src * d * 4),
+        "u_gemm": (2 * n * d * H2 * d, n * d * esz + n * H2 * d * esz),
+        "dW2": (2 * E * H1 * H2, E * (H1 + H2) * esz),
+    }
+    return m
+
+
+def agg_work(w, E, n_src):
+    """Work of the classes whose kernels differ between the two forms."""
+    d, H1, H2 = w.d, w.H1, w.H2
+    n = w.n_dst
+    esz = 2 if w.dtype == "bf16" else 4
+    kt = (H2 + 1) * d
+    mask = (H1 + H2) // 8
     return {
-        "edge_fwd": 2 * (de * H1 + H1 * H2) + 2 * (H2 + 1) * d * d,
-        "edge_dh": 2 * (H2 + 1) * d * d,
-        "dz": 2 * H2 * d * d + 2 * H1 * H2,
-        "dW3": 2 * H2 * d * d,
-        "dW2": 2 * H1 * H2,
-        "fwd+bwd": (8 * H2 + 6) * d * d + 6 * H1 * H2 + 4 * de * H1,
+        "dz": (2 * E * (d * H2 + H1 * H2), n * H2 * d * esz + E * (4 + d * esz + mask + (H1 + H2) * esz)),
+        "dW3": (2 * n * kt * d, n * kt * esz + n * d * esz),
+    }
+
+
+def per_edge_work(w, E, n_src):
+    d, H1, H2 = w.d, w.H1, w.H2
+    n = w.n_dst
+    esz = 2 if w.dtype == "bf16" else 4
+    mask = (H1 + H2) // 8
+    return {
+        "dz": (2 * E * (H2 * d * d + H1 * H2), E * (8 + d * esz + mask + (H1 + H2) * esz) + n * d * 4),
+        "dW3": (2 * E * H2 * d * d, E * (8 + d * esz + H2 * esz) + n * d * 4),
     }
 
 
@@ -209,6 +279,8 @@ def main():
 
     w = make_config(args.config)
     lib = dm.Dsmp(0)
+    lib.dsmp_set_edge_algorithm({"auto": dm.EDGE_AUTO, "per_edge": dm.EDGE_PER_EDGE,
+                                 "aggregate": dm.EDGE_AGGREGATE}[args.algo])
     pipe = Pipeline(w, lib, dm, torch)
     print("workload %s: n_dst=%d n_src=%d E=%d layers=%d" % (w.name, w.n_dst, w.n_src, pipe.E, w.layers),
           file=sys.stderr, flush=True)
@@ -232,8 +304,10 @@ def main():
     lib.dsmp_profile_enable(False)
 
     E, L = pipe.E, w.layers
-    fl = per_edge_flops(w)
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_TFLOPS
+    agg = "edge_mlp" in prof and prof["edge_mlp"][1] > 0
+    work = work_model(w, E, w.n_src)
+    work.update(agg_work(w, E, w.n_src) if agg else per_edge_work(w, E, w.n_src))
     kernels = {}
     for name, (tot, n) in prof.items():
         if n == 0:
@@ -241,16 +315,25 @@ def main():
         avg = tot / n
         ent = {"ms_avg": round(avg, 5), "launches_per_step": n / args.steps,
                "ms_per_step": round(tot / args.steps, 4)}
-        if name in fl:
-            tf = E * fl[name] / (avg * 1e-3) / 1e12
-            ent["tflops"] = round(tf, 2)
-            ent["frac_peak"] = round(tf / peak, 4)
+        if name in work:
+            fl, by = work[name]
+            tf = fl / (avg * 1e-3) / 1e12
+            gbs = by / (avg * 1e-3) / 1e9
+            bound = "mfma" if fl / by > (peak / HBM_TBPS) else "hbm"
+            ent.update({"flops": fl, "bytes": by, "tflops": round(tf, 2), "gbps": round(gbs, 1), "bound": bound,
+                        "frac": round(tf / peak if bound == "mfma" else gbs / (HBM_TBPS * 1e3), 4)})
         kernels[name] = ent
-    mfma = {k: v for k, v in kernels.items() if "tflops" in v}
-    dom = max(mfma, key=lambda k: mfma[k]["ms_per_step"])
+    modeled = {k: v for k, v in kernels.items() if "bound" in v}
+    dom = max(modeled, key=lambda k: modeled[k]["ms_per_step"])
     dk = kernels[dom]
-    achieved = dk["tflops"]
-    flops_step = L * (E * fl["fwd+bwd"] + w.n_dst * 6 * w.d * w.d)
+    if dk["bound"] == "mfma":
+        roof = {"bound": "mfma", "achieved": dk["tflops"], "peak": peak, "unit": "TFLOP/s", "frac": dk["frac"],
+                "algorithmic": dk["flops"]}
+    else:
+        roof = {"bound": "hbm", "achieved": dk["gbps"], "peak": HBM_TBPS * 1e3, "unit": "GB/s", "frac": dk["frac"],
+                "algorithmic": dk["bytes"]}
+    roof.update({"kernel": dom, "traffic": measured_traffic(dom, w.name), "ms_per_launch": dk["ms_avg"]})
+    flops_step = L * (E * method_flops_per_edge(w) + w.n_dst * 6 * w.d * w.d)
     res = {
         "metric": METRIC,
         "value": round(E * L / (ms * 1e-3), 1),
@@ -265,10 +348,9 @@ def main():
                                   w.d, w.de, w.H1, w.H2, w.d * w.d, L),
                    "n_dst": w.n_dst, "n_src": w.n_src, "edges": E, "layers": L, "d": w.d, "h1": w.H1,
                    "h2": w.H2},
-        "tflops_step": round(flops_step / (ms * 1e-3) / 1e12, 2),
-        "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(achieved / peak, 4), "traffic": measured_traffic(dom, w.name),
-                     "flops_per_launch": E * fl[dom], "ms_per_launch": dk["ms_avg"]},
+        "edge_algorithm": "aggregate" if agg else "per_edge",
+        "method_tflops_step": round(flops_step / (ms * 1e-3) / 1e12, 2),
+        "roofline": roof,
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:

@@ -266,7 +266,7 @@ enum {
   DSMP_K_NODE_BWD = 5,  /* backward node, root and db3 kernels */
   DSMP_K_EDGE_DH = 6,   /* feature-gradient edge contraction kernel */
   DSMP_K_DH_FINAL = 7,  /* feature-gradient assembly kernel */
-  DSMP_K_DZ = 8,        /* dz / da2 / da1 kernel */
+  DSMP_K_DZ = 8,        /* dz / da2 / da1 kernel (either form) */
   DSMP_K_DW3 = 9,       /* dW3 kernels (split over edges, or over S) */
   DSMP_K_DW2 = 10,      /* dW2 split-over-edges kernel */
   DSMP_K_DW1 = 11,      /* dW1 kernel */
@@ -276,7 +276,8 @@ enum {
   DSMP_K_GEMM_FWD = 15, /* W3 GEMM over S (aggregate form) */
   DSMP_K_OUTER_DH = 16, /* per-source sums T_j (aggregate form) */
   DSMP_K_GEMM_DH = 17,  /* W3 GEMM over T (aggregate form) */
-  DSMP_K_COUNT = 18
+  DSMP_K_U_GEMM = 18,   /* U = g W3 GEMM of the aggregate dz */
+  DSMP_K_COUNT = 19
 };
 dsmp_status dsmp_profile_enable(dsmp_handle* h, int enable);
 dsmp_status dsmp_profile_reset(dsmp_handle* h);

@@ -170,7 +170,7 @@ __global__ __launch_bounds__(256) void k_nbr_count(const float* __restrict__ pos
                                                    const float4* __restrict__ spos,
                                                    const int32_t* __restrict__ sidx,
                                                    uint32_t* __restrict__ rcnt,
-                                                   GraphStats* __restrict__ st) {
+                                                   uint32_t* __restrict__ rraw) {
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (i >= n_dst) return;
@@ -187,10 +187,36 @@ __global__ __launch_bounds__(256) void k_nbr_count(const float* __restrict__ pos
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
   if (lane == 0) {
-    uint32_t kept = (cap > 0 && cnt > (uint32_t)cap) ? (uint32_t)cap : cnt;
-    rcnt[i] = kept;
-    atomicAdd(&st->total, (unsigned long long)kept);
-    atomicMax(&st->maxraw, cnt);
+    rcnt[i] = (cap > 0 && cnt > (uint32_t)cap) ? (uint32_t)cap : cnt;
+    rraw[i] = cnt;
+  }
+}
+
+// Edge total (64-bit) and largest pre-cap row count, one block.
+__global__ __launch_bounds__(1024) void k_graph_stats(const uint32_t* __restrict__ rcnt,
+                                                      const uint32_t* __restrict__ rraw, int64_t n_dst,
+                                                      GraphStats* __restrict__ st) {
+  __shared__ unsigned long long ssum[1024];
+  __shared__ uint32_t smax[1024];
+  unsigned long long s = 0;
+  uint32_t m = 0;
+  for (int64_t i = threadIdx.x; i < n_dst; i += 1024) {
+    s += rcnt[i];
+    m = rraw[i] > m ? rraw[i] : m;
+  }
+  ssum[threadIdx.x] = s;
+  smax[threadIdx.x] = m;
+  __syncthreads();
+  for (int o = 512; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) {
+      ssum[threadIdx.x] += ssum[threadIdx.x + o];
+      smax[threadIdx.x] = smax[threadIdx.x + o] > smax[threadIdx.x] ? smax[threadIdx.x + o] : smax[threadIdx.x];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    st->total = ssum[0];
+    st->maxraw = smax[0];
   }
 }
 
@@ -361,6 +387,7 @@ struct GraphWs {
   float4* spos;
   int32_t* sidx;
   uint32_t* rcnt;
+  uint32_t* rraw;
   int32_t* rowptr_tmp;
   uint32_t* indeg;
   uint32_t* scur;
@@ -382,6 +409,7 @@ GraphWs carve_graph_ws(void* base, int64_t n_src, int64_t n_dst, size_t* used) {
   w.spos = c.take<float4>(n_src);
   w.sidx = c.take<int32_t>(n_src);
   w.rcnt = c.take<uint32_t>(n_dst);
+  w.rraw = c.take<uint32_t>(n_dst);
   w.rowptr_tmp = c.take<int32_t>(n_dst + 1);
   w.indeg = c.take<uint32_t>(n_src);
   w.scur = c.take<uint32_t>(n_src);
@@ -434,7 +462,8 @@ dsmp_status count_phase(dsmp_handle* h, const dsmp_graph_query* q, const GraphWs
   }
   if (q->n_dst > 0) {
     hipLaunchKernelGGL(k_nbr_count, dim3(ceil_div(q->n_dst, 4)), dim3(256), 0, s, q->pos, q->n_dst, D,
-                       r2, q->cap, w.grid, w.cstart, w.spos, w.sidx, w.rcnt, w.stats);
+                       r2, q->cap, w.grid, w.cstart, w.spos, w.sidx, w.rcnt, w.rraw);
+    hipLaunchKernelGGL(k_graph_stats, dim3(1), dim3(1024), 0, s, w.rcnt, w.rraw, q->n_dst, w.stats);
     DSMP_LAUNCHED(h, "neighbour count");
   }
   if ((st = exclusive_scan_u32(h, w.rcnt, row_ptr, q->n_dst, w.scan_tmp)) != DSMP_OK) return st;

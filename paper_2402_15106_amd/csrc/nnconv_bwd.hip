@@ -455,13 +455,16 @@ struct UArgs {
 };
 
 // U[i][c] = sum_q W[c][q] g_i[q] for c = k*DL + p, as tiles C[c][i] (A = W
-// rows, B = the g rows, lane = destination), so each lane writes runs of four
-// consecutive c.  A wave covers 32 destinations and 256 columns.
+// rows, B = the g rows, lane = destination).  Each 32x32 tile goes through a
+// per-wave LDS square so that the stores are 16-byte runs along c.  A wave
+// covers 32 destinations and 256 columns.
 template <typename T, int DL, int H2>
 __global__ __launch_bounds__(256) void k_u_gemm(UArgs a) {
   using M = MT<T>;
   using frag = typename M::frag;
   constexpr int KS = M::KS, EPL = M::EPL, ESZ = sizeof(T), SKD = DL / KS, NC = H2 * DL;
+  constexpr int TROW = 32 * ESZ + 16;                    // LDS row pitch of the square (bytes)
+  __shared__ __align__(16) unsigned char sq[4][32 * TROW];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
   const int64_t i0 = (int64_t)blockIdx.x * 32;
   const int64_t c0 = ((int64_t)blockIdx.y * 4 + wv) * 256;
@@ -470,8 +473,8 @@ __global__ __launch_bounds__(256) void k_u_gemm(UArgs a) {
   frag B[SKD];
 #pragma unroll
   for (int s = 0; s < SKD; ++s) B[s] = ld_frag<T>(a.G + ((size_t)row * DL + s * KS + hh * EPL) * ESZ);
-  T* out = reinterpret_cast<T*>(a.U) + (size_t)(i0 + l32) * NC;
-  const bool ok = i0 + l32 < a.n_rows;
+  unsigned char* t = sq[wv];
+  constexpr int CH = 32 * ESZ / 16;                      // 16-byte chunks per row of the square
 #pragma unroll 2
   for (int ct = 0; ct < 8; ++ct) {
     const int64_t c = c0 + ct * 32;
@@ -481,19 +484,26 @@ __global__ __launch_bounds__(256) void k_u_gemm(UArgs a) {
     f32x16 C = f32x16{};
 #pragma unroll
     for (int s = 0; s < SKD; ++s) C = M::mma(A[s], B[s], C);
-    if (ok) {
+    // square row = destination (lane), columns 8(r/4) + 4hh + r%4
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        T* o = out + c + 8 * g + 4 * hh;
-        if constexpr (ESZ == 2) {
-          const bf16x2 lo = __builtin_convertvector((f32x2){C[4 * g], C[4 * g + 1]}, bf16x2);
-          const bf16x2 hi = __builtin_convertvector((f32x2){C[4 * g + 2], C[4 * g + 3]}, bf16x2);
-          *reinterpret_cast<uint2*>(o) = make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
-        } else {
-          *reinterpret_cast<f32x4*>(o) = f32x4{C[4 * g], C[4 * g + 1], C[4 * g + 2], C[4 * g + 3]};
-        }
+    for (int g = 0; g < 4; ++g) {
+      unsigned char* o = t + l32 * TROW + (8 * g + 4 * hh) * ESZ;
+      if constexpr (ESZ == 2) {
+        const bf16x2 lo = __builtin_convertvector((f32x2){C[4 * g], C[4 * g + 1]}, bf16x2);
+        const bf16x2 hi = __builtin_convertvector((f32x2){C[4 * g + 2], C[4 * g + 3]}, bf16x2);
+        *reinterpret_cast<uint2*>(o) = make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+      } else {
+        *reinterpret_cast<f32x4*>(o) = f32x4{C[4 * g], C[4 * g + 1], C[4 * g + 2], C[4 * g + 3]};
       }
     }
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int it = 0; it < 32 * CH / 64; ++it) {
+      const int id = it * 64 + lane, r = id / CH, ch = id % CH;
+      const uint4 v = *reinterpret_cast<const uint4*>(t + r * TROW + ch * 16);
+      if (i0 + r < a.n_rows) *reinterpret_cast<uint4*>(a.U + ((size_t)(i0 + r) * NC + c) * ESZ + ch * 16) = v;
+    }
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
@@ -1018,11 +1028,13 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
   dsmp_status st;
   if (dz.E > 0 && dz.U) {
     // aggregate form: U = g W3 for every destination, then the masked per-tile products
-    using S = DzShape<T, DL, H1, H2>;
+    {
+      ProfScope prof(h, DSMP_K_U_GEMM);
+      UArgs ua{dz.n_dst, dz.gT, dz.packed + dz.L.w3u, const_cast<unsigned char*>(dz.U)};
+      hipLaunchKernelGGL((k_u_gemm<T, DL, H2>), dim3((unsigned)ceil_div(dz.n_dst, 32), (unsigned)ceil_div(H2 * DL, 1024)),
+                         dim3(256), 0, s, ua);
+    }
     ProfScope prof(h, DSMP_K_DZ);
-    UArgs ua{dz.n_dst, dz.gT, dz.packed + dz.L.w3u, const_cast<unsigned char*>(dz.U)};
-    hipLaunchKernelGGL((k_u_gemm<T, DL, H2>), dim3((unsigned)ceil_div(dz.n_dst, 32), (unsigned)ceil_div(H2 * DL, 1024)),
-                       dim3(256), 0, s, ua);
     hipLaunchKernelGGL((k_bwd_dz_agg<T, DL, H1, H2>), dim3((unsigned)ceil_div(dz.n_dst, 4)), dim3(256), 0, s, dz);
     DSMP_LAUNCHED(h, "dz (aggregate form)");
   } else if (dz.E > 0) {
