@@ -832,7 +832,7 @@ template <typename T, int H1>
 __global__ __launch_bounds__(256) void k_bwd_dW1(int64_t E, int64_t per_chunk, const int32_t* __restrict__ col,
                                                  const int32_t* __restrict__ dst, const float* __restrict__ node_attr,
                                                  int dim, int attr_mode, int de, const T* __restrict__ da1E,
-                                                 const int* __restrict__ jof, float* __restrict__ part) {
+                                                 float* __restrict__ part) {
   constexpr int SUB = 256 / H1, XB = 256;
   __shared__ float xs[XB][9];
   __shared__ float red[SUB][H1][9];
@@ -869,7 +869,7 @@ __global__ __launch_bounds__(256) void k_bwd_dW1(int64_t E, int64_t per_chunk, c
     for (int s = 1; s < SUB; ++s)
 #pragma unroll
       for (int c = 0; c < 9; ++c) acc[c] += red[s][kk][c];
-    const int j = jof[kk];
+    const int j = sizeof(T) == 2 ? kperm<__bf16>(kk) : kperm<float>(kk);
     float* out = part + (size_t)blockIdx.x * (H1 * de + H1);
     for (int c = 0; c < de; ++c) out[j * de + c] = acc[c];
     out[H1 * de + j] = acc[8];
@@ -878,28 +878,41 @@ __global__ __launch_bounds__(256) void k_bwd_dW1(int64_t E, int64_t per_chunk, c
 
 // ------------------------------------------------------------ reductions and finals
 
-// out[x] = [out[x] +] sum_c part[c*stride + off + x].  A block owns 64
-// consecutive outputs; four thread groups sum the chunks c = g, g+4, ... in
-// order, and the four group sums are added in group order (deterministic).
-__global__ __launch_bounds__(256) void k_reduce(const float* __restrict__ part, int nchunk, int64_t stride,
-                                                int64_t off, int64_t n, float* __restrict__ out, int accumulate) {
+// Fixed-order reductions out[x] = [out[x] +] sum_c part[c*stride + off + x]
+// for several segments in one launch: block b serves the 64 outputs starting
+// at (b - first[s]) * 64 of segment s; four thread groups sum the chunks
+// c = g, g+4, ... in order and the group sums are added in group order
+// (deterministic).
+struct RedSeg {
+  const float* part;
+  float* out;
+  int64_t stride, off, n;
+  int nchunk;
+};
+struct RedArgs {
+  RedSeg seg[8];
+  int64_t first[9];
+  int nseg, accumulate;
+};
+
+__global__ __launch_bounds__(256) void k_reduce_multi(RedArgs a) {
   __shared__ float sh[4][64];
+  int sidx = 0;
+  while (sidx + 1 < a.nseg && (int64_t)blockIdx.x >= a.first[sidx + 1]) ++sidx;
+  const RedSeg& sg = a.seg[sidx];
   const int c0 = threadIdx.x & 63, g = threadIdx.x >> 6;
-  for (int64_t x0 = (int64_t)blockIdx.x * 64; x0 < n; x0 += (int64_t)gridDim.x * 64) {
-    const int64_t x = x0 + c0;
-    float s = 0.0f;
-    if (x < n) {
-      const float* p = part + off + x;
+  const int64_t x = ((int64_t)blockIdx.x - a.first[sidx]) * 64 + c0;
+  float sum = 0.0f;
+  if (x < sg.n) {
+    const float* p = sg.part + sg.off + x;
 #pragma unroll 8
-      for (int c = g; c < nchunk; c += 4) s += p[(int64_t)c * stride];
-    }
-    sh[g][c0] = s;
-    __syncthreads();
-    if (g == 0 && x < n) {
-      const float t = ((sh[0][c0] + sh[1][c0]) + sh[2][c0]) + sh[3][c0];
-      out[x] = accumulate ? out[x] + t : t;
-    }
-    __syncthreads();
+    for (int c = g; c < sg.nchunk; c += 4) sum += p[(int64_t)c * sg.stride];
+  }
+  sh[g][c0] = sum;
+  __syncthreads();
+  if (g == 0 && x < sg.n) {
+    const float t = ((sh[0][c0] + sh[1][c0]) + sh[2][c0]) + sh[3][c0];
+    sg.out[x] = a.accumulate ? sg.out[x] + t : t;
   }
 }
 
@@ -936,10 +949,6 @@ __global__ void k_bwd_dh_final(int64_t n_src, int64_t n_dst, int DL, const int32
   }
 }
 
-__global__ void k_jof(int* out, int h1, int isbf16) {
-  int kk = blockIdx.x * blockDim.x + threadIdx.x;
-  if (kk < h1) out[kk] = isbf16 ? kperm<__bf16>(kk) : kperm<float>(kk);
-}
 
 // ------------------------------------------------------------ workspace
 
@@ -948,7 +957,6 @@ struct BwdWs {
   unsigned char *gT, *da2E, *da1E, *ot, *U;
   int nslh;
   float *p_root, *p_db3, *p_w3, *p_w2, *p_w1;
-  int* jof;
   int nr, nb3, n3, n2, n1;
   int64_t pc3, pc2, pc1, pr, pb3;
   size_t total;
@@ -1010,7 +1018,6 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   w.n1 = (int)(E > 0 ? (ceil_div(E, 512) < 2048 ? ceil_div(E, 512) : 2048) : 1);
   w.pc1 = E > 0 ? (E + w.n1 - 1) / w.n1 : 1;
   w.p_w1 = c.take<float>((size_t)w.n1 * (d.h1 * de + d.h1));
-  w.jof = c.take<int>(d.h1);
   w.total = c.used();
   return w;
 }
@@ -1197,26 +1204,25 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
     W3Args w3{E, w.pc3, agg ? 0 : w.n3, g->col, g->dst, hin, w.gF, sv + sl.zE, w.p_w3};
     W2Args w2{E, w.pc2, 1, w.da2E, sv + sl.z1E, w.p_w2};
     if ((st = dispatch_edge_grads(h, d, dz, w3, w2)) != DSMP_OK) return st;
-    hipLaunchKernelGGL(k_jof, dim3(ceil_div(d.h1, 256)), dim3(256), 0, s, w.jof, d.h1, d.dtype == DSMP_BF16);
     int n1 = (int)((E + w.pc1 - 1) / w.pc1);
     ProfScope prof(h, DSMP_K_DW1);
     const __bf16* da1b = reinterpret_cast<const __bf16*>(w.da1E);
     const float* da1f = reinterpret_cast<const float*>(w.da1E);
     if (d.dtype == DSMP_F32 && d.h1 == 64)
       hipLaunchKernelGGL((k_bwd_dW1<float, 64>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
-                         d.dim, d.attr_mode, de, da1f, w.jof, w.p_w1);
+                         d.dim, d.attr_mode, de, da1f, w.p_w1);
     else if (d.dtype == DSMP_F32)
       hipLaunchKernelGGL((k_bwd_dW1<float, 128>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
-                         d.dim, d.attr_mode, de, da1f, w.jof, w.p_w1);
+                         d.dim, d.attr_mode, de, da1f, w.p_w1);
     else if (d.h1 == 64)
       hipLaunchKernelGGL((k_bwd_dW1<__bf16, 64>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
-                         d.dim, d.attr_mode, de, da1b, w.jof, w.p_w1);
+                         d.dim, d.attr_mode, de, da1b, w.p_w1);
     else if (d.h1 == 128)
       hipLaunchKernelGGL((k_bwd_dW1<__bf16, 128>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
-                         d.dim, d.attr_mode, de, da1b, w.jof, w.p_w1);
+                         d.dim, d.attr_mode, de, da1b, w.p_w1);
     else
       hipLaunchKernelGGL((k_bwd_dW1<__bf16, 256>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
-                         d.dim, d.attr_mode, de, da1b, w.jof, w.p_w1);
+                         d.dim, d.attr_mode, de, da1b, w.p_w1);
     DSMP_LAUNCHED(h, "dW1");
   }
 
@@ -1227,12 +1233,14 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
       return st;
   }
 
-  // fixed-order reductions into the caller's gradients
+  // fixed-order reductions into the caller's gradients, one launch
+  RedArgs ra{};
+  ra.accumulate = acc;
   auto red = [&](const float* part, int nchunk, int64_t stride, int64_t off, int64_t n, float* out) {
-    unsigned grid = ceil_div(n, 64);
-    if (grid > 8192) grid = 8192;
-    if (grid == 0) return;
-    hipLaunchKernelGGL(k_reduce, dim3(grid), dim3(256), 0, s, part, nchunk, stride, off, n, out, acc);
+    if (n == 0) return;
+    ra.seg[ra.nseg] = RedSeg{part, out, stride, off, n, nchunk};
+    ra.first[ra.nseg + 1] = ra.first[ra.nseg] + ceil_div(n, 64);
+    ++ra.nseg;
   };
   const int64_t dd = (int64_t)d.d * d.d;
   const int n3 = E > 0 && !agg ? w.n3 : 0;
@@ -1248,6 +1256,8 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   red(w.p_w2, n2, (int64_t)d.h2 * d.h1 + d.h2, (int64_t)d.h2 * d.h1, d.h2, grads->db2);
   red(w.p_w1, n1, (int64_t)d.h1 * de + d.h1, 0, (int64_t)d.h1 * de, grads->dW1);
   red(w.p_w1, n1, (int64_t)d.h1 * de + d.h1, (int64_t)d.h1 * de, d.h1, grads->db1);
+  if (ra.nseg > 0)
+    hipLaunchKernelGGL(k_reduce_multi, dim3((unsigned)ra.first[ra.nseg]), dim3(256), 0, s, ra);
   DSMP_LAUNCHED(h, "gradient reductions");
   return DSMP_OK;
 }
