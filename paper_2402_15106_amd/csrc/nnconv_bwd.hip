@@ -475,12 +475,19 @@ __global__ __launch_bounds__(256) void k_u_gemm(UArgs a) {
   for (int s = 0; s < SKD; ++s) B[s] = ld_frag<T>(a.G + ((size_t)row * DL + s * KS + hh * EPL) * ESZ);
   unsigned char* t = sq[wv];
   constexpr int CH = 32 * ESZ / 16;                      // 16-byte chunks per row of the square
+  // the next column tile's W rows are in flight while this tile is multiplied and stored
+  frag An[SKD];
+#pragma unroll
+  for (int s = 0; s < SKD; ++s) An[s] = ld_frag<T>(a.W + ((size_t)(c0 + l32) * DL + s * KS + hh * EPL) * ESZ);
 #pragma unroll 2
   for (int ct = 0; ct < 8; ++ct) {
     const int64_t c = c0 + ct * 32;
     frag A[SKD];
 #pragma unroll
-    for (int s = 0; s < SKD; ++s) A[s] = ld_frag<T>(a.W + ((size_t)(c + l32) * DL + s * KS + hh * EPL) * ESZ);
+    for (int s = 0; s < SKD; ++s) A[s] = An[s];
+    if (ct + 1 < 8)
+#pragma unroll
+      for (int s = 0; s < SKD; ++s) An[s] = ld_frag<T>(a.W + ((size_t)(c + 32 + l32) * DL + s * KS + hh * EPL) * ESZ);
     f32x16 C = f32x16{};
 #pragma unroll
     for (int s = 0; s < SKD; ++s) C = M::mma(A[s], B[s], C);
@@ -507,41 +514,54 @@ __global__ __launch_bounds__(256) void k_u_gemm(UArgs a) {
   }
 }
 
-// Copy a chunk of ECH edge rows of a [E][W] array (layer dtype, permuted
-// register order) into LDS transposed to [W][ECH] (rows still in the permuted
-// order), four edges per thread: 8-byte (bf16) or 16-byte (fp32) LDS writes,
-// zero rows past e_end.  ROWB is the LDS row pitch in bytes.
-template <typename T, int W, int ECH, int ROWB>
-__device__ __forceinline__ void stage_transposed(const unsigned char* __restrict__ src, int64_t eb, int64_t e_end,
-                                                 unsigned char* __restrict__ dstl) {
-  constexpr int ESZ = sizeof(T), KPU = 16 / ESZ, EQ = ECH / 4, NU = EQ * (W / KPU);
-  for (int u = threadIdx.x; u < NU; u += 256) {
-    const int eq = u % EQ, kg = u / EQ;
-    uint4 v[4];
+// Transposed staging of a chunk of ECH edge rows of a [E][W] array (layer
+// dtype, permuted register order) into LDS as [W][ECH] (rows still in the
+// permuted order), four edges per thread: 8-byte (bf16) or 16-byte (fp32)
+// LDS writes, zero rows past e_end.  fetch() loads a chunk into registers
+// (issued before the current chunk's products), store() writes it to LDS
+// with row pitch ROWB bytes after the barrier.
+template <typename T, int W, int ECH>
+struct TStage {
+  static constexpr int ESZ = sizeof(T), KPU = 16 / ESZ, EQ = ECH / 4, NU = EQ * (W / KPU), UPT = (NU + 255) / 256;
+  uint4 v[UPT][4];
+  __device__ __forceinline__ void fetch(const unsigned char* __restrict__ src, int64_t eb, int64_t e_end) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t e = eb + 4 * eq + i;
-      v[i] = e < e_end ? *reinterpret_cast<const uint4*>(src + ((size_t)e * W) * ESZ + kg * 16) : make_uint4(0, 0, 0, 0);
-    }
-    const uint32_t* d0 = reinterpret_cast<const uint32_t*>(&v[0]);
-    const uint32_t* d1 = reinterpret_cast<const uint32_t*>(&v[1]);
-    const uint32_t* d2 = reinterpret_cast<const uint32_t*>(&v[2]);
-    const uint32_t* d3 = reinterpret_cast<const uint32_t*>(&v[3]);
-    if constexpr (ESZ == 2) {
+    for (int x = 0; x < UPT; ++x) {
+      const int u = (int)threadIdx.x + x * 256, eq = u % EQ, kg = u / EQ;
 #pragma unroll
-      for (int w = 0; w < 8; ++w) {
-        const int sh = (w & 1) * 16, dw = w >> 1;
-        const uint32_t lo = ((d0[dw] >> sh) & 0xFFFFu) | (((d1[dw] >> sh) & 0xFFFFu) << 16);
-        const uint32_t hi = ((d2[dw] >> sh) & 0xFFFFu) | (((d3[dw] >> sh) & 0xFFFFu) << 16);
-        *reinterpret_cast<uint2*>(dstl + (kg * 8 + w) * ROWB + 4 * eq * ESZ) = make_uint2(lo, hi);
+      for (int i = 0; i < 4; ++i) {
+        const int64_t e = eb + 4 * eq + i;
+        v[x][i] = (u < NU && e < e_end) ? *reinterpret_cast<const uint4*>(src + ((size_t)e * W) * ESZ + kg * 16)
+                                       : make_uint4(0, 0, 0, 0);
       }
-    } else {
-#pragma unroll
-      for (int w = 0; w < 4; ++w)
-        *reinterpret_cast<uint4*>(dstl + (kg * 4 + w) * ROWB + 4 * eq * ESZ) = make_uint4(d0[w], d1[w], d2[w], d3[w]);
     }
   }
-}
+  template <int ROWB>
+  __device__ __forceinline__ void store(unsigned char* __restrict__ dstl) const {
+#pragma unroll
+    for (int x = 0; x < UPT; ++x) {
+      const int u = (int)threadIdx.x + x * 256, eq = u % EQ, kg = u / EQ;
+      if (u >= NU) continue;
+      const uint32_t* d0 = reinterpret_cast<const uint32_t*>(&v[x][0]);
+      const uint32_t* d1 = reinterpret_cast<const uint32_t*>(&v[x][1]);
+      const uint32_t* d2 = reinterpret_cast<const uint32_t*>(&v[x][2]);
+      const uint32_t* d3 = reinterpret_cast<const uint32_t*>(&v[x][3]);
+      if constexpr (ESZ == 2) {
+#pragma unroll
+        for (int w = 0; w < 8; ++w) {
+          const int sh = (w & 1) * 16, dw = w >> 1;
+          const uint32_t lo = ((d0[dw] >> sh) & 0xFFFFu) | (((d1[dw] >> sh) & 0xFFFFu) << 16);
+          const uint32_t hi = ((d2[dw] >> sh) & 0xFFFFu) | (((d3[dw] >> sh) & 0xFFFFu) << 16);
+          *reinterpret_cast<uint2*>(dstl + (kg * 8 + w) * ROWB + 4 * eq * ESZ) = make_uint2(lo, hi);
+        }
+      } else {
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          *reinterpret_cast<uint4*>(dstl + (kg * 4 + w) * ROWB + 4 * eq * ESZ) = make_uint4(d0[w], d1[w], d2[w], d3[w]);
+      }
+    }
+  }
+};
 
 // ------------------------------------------------------------ dW3 (split over edges)
 
@@ -768,7 +788,7 @@ struct W2Shape {
 };
 
 template <typename T, int H1, int H2>
-__global__ __launch_bounds__(256, 1) void k_bwd_dW2(W2Args a) {
+__global__ __launch_bounds__(256, 2) void k_bwd_dW2(W2Args a) {
   using S = W2Shape<T, H1, H2>;
   using M = MT<T>;
   using frag = typename M::frag;
@@ -789,10 +809,18 @@ __global__ __launch_bounds__(256, 1) void k_bwd_dW2(W2Args a) {
 #pragma unroll
     for (int jj = 0; jj < S::JT_W; ++jj) acc[kk][jj] = f32x16{};
   float bsum = 0.0f;
+  TStage<T, H2, ECH> sa;
+  TStage<T, H1, ECH> sz;
+  sa.fetch(a.da2E, e_begin, e_end);
+  sz.fetch(a.z1E, e_begin, e_end);
   for (int64_t eb = e_begin; eb < e_end; eb += ECH) {
     __syncthreads();
-    stage_transposed<T, H2, ECH, S::ROW>(a.da2E, eb, e_end, dl);
-    stage_transposed<T, H1, ECH, S::ROW>(a.z1E, eb, e_end, zl);
+    sa.template store<S::ROW>(dl);
+    sz.template store<S::ROW>(zl);
+    if (eb + ECH < e_end) {   // next chunk in flight while this one is multiplied
+      sa.fetch(a.da2E, eb + ECH, e_end);
+      sz.fetch(a.z1E, eb + ECH, e_end);
+    }
     __syncthreads();
     if (split == 0 && tid < H2)
       for (int el = 0; el < ECH; ++el) bsum += to_f(*reinterpret_cast<const T*>(dl + tid * S::ROW + el * ESZ));
@@ -1011,7 +1039,7 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   const size_t p3e = (size_t)w.n3 * d.d * d.d * d.h2;
   const size_t p3a = (size_t)agg_dw3_slices(n_dst) * d.d * agg_ktot(d);
   w.p_w3 = c.take<float>(p3e > p3a ? p3e : p3a);
-  w.n2 = (int)(E > 0 ? (ceil_div(E, 2048) < 512 ? ceil_div(E, 2048) : 512) : 1);
+  w.n2 = (int)(E > 0 ? (ceil_div(E, 1024) < 512 ? ceil_div(E, 1024) : 512) : 1);
   w.pc2 = ((E + w.n2 - 1) / w.n2 + 63) / 64 * 64;
   if (w.pc2 < 64) w.pc2 = 64;
   w.p_w2 = c.take<float>((size_t)w.n2 * (d.h2 * d.h1 + d.h2));
