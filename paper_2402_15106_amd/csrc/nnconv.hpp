@@ -154,8 +154,9 @@ inline PackLayout pack_layout(int d, int h1, int h2, int esz) {
   L.wr = take((size_t)d * d * 4);             // fp32 [q][p] (rounded to the layer dtype)
   L.br = take((size_t)d * 4);                 // fp32 [d]
   // W3~ for the aggregate form, in the segment-sum K order (K = h2*d + d):
-  L.wgt = take((size_t)d * (h2 + 1) * d * esz);   // T [q][K(k, p)]
-  L.wht = take((size_t)d * (h2 + 1) * d * esz);   // T [p][K(k, q)]
+  // (+128: the GEMM reads rows in whole 128-byte pieces)
+  L.wgt = take((size_t)d * (h2 + 1) * d * esz + 128);   // T [q][K(k, p)]
+  L.wht = take((size_t)d * (h2 + 1) * d * esz + 128);   // T [p][K(k, q)]
   L.w3u = take((size_t)h2 * d * d * esz);         // T [k*d + p][q] (U GEMM of the aggregate dz)
   L.total = (off + 255) & ~size_t(255);
   return L;

@@ -175,57 +175,111 @@ struct GemmArgs {
   const unsigned char* A;    // [n_rows][ktot] layer dtype (segment sums)
   const unsigned char* BT;   // [DL][ktot] layer dtype (packed W3~ in the sum order)
   int nsl;                   // K slices
-  int64_t ksl;               // K steps per slice
+  int64_t csl;               // K chunks per slice
   float* part;               // [nsl][n_rows][DL] partial products
 };
 
-// part[s][n][c] = sum over slice s of K:  A[n][K] * BT[c][K].  Each wave owns
-// 32 rows and all d columns; a workgroup is 4 row tiles of one K slice.
+// Direct global-to-LDS staging of one 128-byte piece of each of ROWS rows
+// (row stride in bytes given at init): every wave-wide load covers whole
+// cache lines.  LDS rows have a pitch of 144 bytes; a unit in the padding slot
+// re-reads its row's first unit, rows at or past nvalid re-read the last valid
+// row, and lanes past the end of the block are masked off.
+template <int ROWS>
+struct RowStage {
+  static constexpr int PITCH = 144, NU = 8, PU = 9, UNITS = ROWS * PU, PER = (UNITS + 255) / 256;
+  uint32_t off[PER];
+  __device__ __forceinline__ void init(int64_t stride, int nvalid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int U = i * 256 + (int)threadIdx.x;
+      int r = U / PU;
+      const int u = U % PU;
+      if (r > nvalid - 1) r = nvalid - 1;
+      off[i] = (uint32_t)(r * stride + (u < NU ? u : 0) * 16);
+    }
+  }
+  __device__ __forceinline__ void issue(const unsigned char* src, unsigned char* dst) const {
+    const int wbase = (int)(threadIdx.x & ~63u);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      if (UNITS % 256 == 0 || i + 1 < PER || i * 256 + (int)threadIdx.x < UNITS) {
+        uint32_t o = off[i];
+        asm volatile("" : "+v"(o));
+        __builtin_amdgcn_global_load_lds((gbl_void_t*)(src + o),
+                                         (lds_void_t*)(dst + (size_t)(i * 256 + wbase) * 16), 16, 0, 0);
+      }
+    }
+  }
+};
+
+template <typename T, int DL>
+struct GemmShape {
+  static constexpr int ESZ = sizeof(T), KS = MT<T>::KS;
+  static constexpr int CB = 128, SPC = CB / (KS * ESZ);   // bytes of a row per chunk, K steps per chunk
+  static constexpr int AB = 128 * RowStage<128>::PITCH, BB = DL * RowStage<DL>::PITCH;
+  static constexpr int BUF = AB + BB, LDS = 2 * BUF;
+};
+
+// part[s][n][c] = sum over slice s of K:  A[n][K] * BT[c][K].  A workgroup
+// owns 128 rows (32 per wave) and all d columns of one K slice.  K advances
+// in chunks of 128 bytes per row: the chunk of the 128 A rows and the d BT
+// rows is copied to LDS by whole cache lines while the previous chunk is
+// multiplied (two buffers).
 template <typename T, int DL>
 __global__ __launch_bounds__(256) void k_w3_gemm(GemmArgs a) {
   using M = MT<T>;
-  constexpr int KS = M::KS, EPL = M::EPL, ESZ = sizeof(T), NCT = DL / 32;
+  using G = GemmShape<T, DL>;
+  constexpr int KS = M::KS, EPL = M::EPL, ESZ = sizeof(T), NCT = DL / 32, SPC = G::SPC;
+  constexpr int PITCH = RowStage<128>::PITCH;
+  extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
-  const int64_t r0 = ((int64_t)blockIdx.x * 4 + wv) * 32;
-  if (r0 >= a.n_rows) return;
+  const int64_t r0 = (int64_t)blockIdx.x * 128;
   const int s = blockIdx.y;
-  const int64_t nstep = a.ktot / KS;
-  const int64_t k0 = s * a.ksl, k1 = (s + 1) * a.ksl < nstep ? (s + 1) * a.ksl : nstep;
-  int64_t row = r0 + l32;
-  if (row >= a.n_rows) row = a.n_rows - 1;
-  const unsigned char* pa = a.A + ((size_t)row * a.ktot + hh * EPL) * ESZ;
-  const unsigned char* pb[NCT];
-#pragma unroll
-  for (int ct = 0; ct < NCT; ++ct) pb[ct] = a.BT + ((size_t)(ct * 32 + l32) * a.ktot + hh * EPL) * ESZ;
+  const int64_t nstep = a.ktot / KS, nchunk = (nstep + SPC - 1) / SPC;
+  const int64_t c0 = s * a.csl, c1 = c0 + a.csl < nchunk ? c0 + a.csl : nchunk;
   f32x16 acc[NCT];
 #pragma unroll
   for (int ct = 0; ct < NCT; ++ct) acc[ct] = f32x16{};
-  constexpr int U = 8;
-  int64_t ks = k0;
-  for (; ks + U <= k1; ks += U) {
-    typename M::frag A[U], B[U][NCT];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      A[u] = ldf<T>(pa + (size_t)(ks + u) * KS * ESZ);
-#pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) B[u][ct] = ldf<T>(pb[ct] + (size_t)(ks + u) * KS * ESZ);
+  if (c0 < c1) {   // uniform over the workgroup; an empty slice writes zeros
+  const int nvalid = (int)(a.n_rows - r0 < 128 ? a.n_rows - r0 : 128);
+  RowStage<128> sa;
+  RowStage<DL> sb;
+  sa.init(a.ktot * ESZ, nvalid);
+  sb.init(a.ktot * ESZ, DL);
+  const unsigned char* ga = a.A + (size_t)r0 * a.ktot * ESZ;
+  sa.issue(ga + c0 * G::CB, smem);
+  sb.issue(a.BT + c0 * G::CB, smem + G::AB);
+  stage_wait();
+  __syncthreads();
+  for (int64_t c = c0; c < c1; ++c) {
+    unsigned char* cur = smem + ((c - c0) & 1) * G::BUF;
+    if (c + 1 < c1) {
+      unsigned char* nxt = smem + ((c + 1 - c0) & 1) * G::BUF;
+      sa.issue(ga + (c + 1) * G::CB, nxt);
+      sb.issue(a.BT + (c + 1) * G::CB, nxt + G::AB);
     }
+    const int nst = (int)(nstep - c * SPC < SPC ? nstep - c * SPC : SPC);
+    const unsigned char* la = cur + (wv * 32 + l32) * PITCH + hh * EPL * ESZ;
+    const unsigned char* lb = cur + G::AB + l32 * PITCH + hh * EPL * ESZ;
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int st = 0; st < SPC; ++st) {
+      if (st < nst) {
+        const auto A = ldf<T>(la + st * KS * ESZ);
 #pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) acc[ct] = M::mma(A[u], B[u][ct], acc[ct]);
+        for (int ct = 0; ct < NCT; ++ct)
+          acc[ct] = M::mma(A, ldf<T>(lb + ct * 32 * PITCH + st * KS * ESZ), acc[ct]);
+      }
+    }
+    stage_wait();
+    __syncthreads();
   }
-  for (; ks < k1; ++ks) {
-    const auto A = ldf<T>(pa + (size_t)ks * KS * ESZ);
-#pragma unroll
-    for (int ct = 0; ct < NCT; ++ct) acc[ct] = M::mma(A, ldf<T>(pb[ct] + (size_t)ks * KS * ESZ), acc[ct]);
   }
   float* out = a.part + (size_t)s * a.n_rows * DL;
 #pragma unroll
   for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int64_t rr = r0 + 8 * (r / 4) + 4 * hh + (r % 4);
+      const int64_t rr = r0 + wv * 32 + 8 * (r / 4) + 4 * hh + (r % 4);
       if (rr < a.n_rows) out[rr * DL + ct * 32 + l32] = acc[ct][r];
     }
 }
@@ -359,6 +413,17 @@ dsmp_status outer_shape(dsmp_handle* h, const OuterArgs& a) {
 }
 
 template <typename T, int DL>
+dsmp_status gemm_shape(dsmp_handle* h, const GemmArgs& a) {
+  using G = GemmShape<T, DL>;
+  auto kern = k_w3_gemm<T, DL>;
+  dsmp_status st = set_lds_bytes(h, kern, G::LDS);
+  if (st != DSMP_OK) return st;
+  hipLaunchKernelGGL(kern, dim3((unsigned)ceil_div(a.n_rows, 128), (unsigned)a.nsl), dim3(256), G::LDS, h->stream, a);
+  DSMP_LAUNCHED(h, "W3 GEMM over segment sums");
+  return DSMP_OK;
+}
+
+template <typename T, int DL>
 dsmp_status dw3_shape(dsmp_handle* h, const DW3AggArgs& a) {
   using S = DW3AggShape<T, DL>;
   auto kern = k_dw3_agg<T, DL>;
@@ -410,19 +475,18 @@ dsmp_status launch_w3_gemm(dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_r
                            const unsigned char* BT, int nsl, float* part) {
   if (n_rows == 0) return DSMP_OK;
   const int64_t ktot = agg_ktot(d);
-  const int64_t nstep = ktot / (d.dtype == DSMP_F32 ? MT<float>::KS : MT<__bf16>::KS);
-  GemmArgs a{n_rows, ktot, A, BT, nsl, ceil_div(nstep, nsl), part};
-  dim3 grid((unsigned)ceil_div(n_rows, 128), (unsigned)nsl);
+  const int esz = d.dtype == DSMP_F32 ? 4 : 2;
+  const int64_t nchunk = ceil_div(ktot * esz, 128);
+  GemmArgs a{n_rows, ktot, A, BT, nsl, ceil_div(nchunk, nsl), part};
   if (d.dtype == DSMP_F32) {
-    if (d.d == 32) hipLaunchKernelGGL((k_w3_gemm<float, 32>), grid, dim3(256), 0, h->stream, a);
-    if (d.d == 64) hipLaunchKernelGGL((k_w3_gemm<float, 64>), grid, dim3(256), 0, h->stream, a);
+    if (d.d == 32) return gemm_shape<float, 32>(h, a);
+    if (d.d == 64) return gemm_shape<float, 64>(h, a);
   } else {
-    if (d.d == 32) hipLaunchKernelGGL((k_w3_gemm<__bf16, 32>), grid, dim3(256), 0, h->stream, a);
-    if (d.d == 64) hipLaunchKernelGGL((k_w3_gemm<__bf16, 64>), grid, dim3(256), 0, h->stream, a);
-    if (d.d == 128) hipLaunchKernelGGL((k_w3_gemm<__bf16, 128>), grid, dim3(256), 0, h->stream, a);
+    if (d.d == 32) return gemm_shape<__bf16, 32>(h, a);
+    if (d.d == 64) return gemm_shape<__bf16, 64>(h, a);
+    if (d.d == 128) return gemm_shape<__bf16, 128>(h, a);
   }
-  DSMP_LAUNCHED(h, "W3 GEMM over segment sums");
-  return DSMP_OK;
+  return fail(h, DSMP_UNSUPPORTED, "unsupported layer shape");
 }
 
 int agg_dw3_slices(int64_t n_rows) {

@@ -1020,7 +1020,7 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   w.dh_direct = c.take<float>((size_t)n_src * d.d);
   w.dh_part = c.take<float>((size_t)(ceil_div(E, EDGE_TILE) + 1) * 2 * d.d);
   // aggregate form: per-source sums T and the K-slices of their W3 GEMM
-  w.ot = c.take<unsigned char>((size_t)n_src * agg_ktot(d) * esz);
+  w.ot = c.take<unsigned char>((size_t)n_src * agg_ktot(d) * esz + 128);   // + whole last GEMM piece
   w.nslh = agg_gemm_slices(n_src, d);
   w.dh_sl = c.take<float>((size_t)w.nslh * n_src * d.d);
   w.U = c.take<unsigned char>((size_t)n_dst * d.h2 * d.d * esz);

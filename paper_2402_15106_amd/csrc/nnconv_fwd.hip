@@ -691,7 +691,7 @@ SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E) {
   s.zE = (size_t)c.take<unsigned char>((size_t)E * d.h2 * esz);
   s.z1E = (size_t)c.take<unsigned char>((size_t)E * d.h1 * esz);
   s.zmask = (size_t)c.take<unsigned char>((size_t)E * (d.h1 + d.h2) / 8);
-  s.os = (size_t)c.take<unsigned char>((size_t)n_dst * agg_ktot(d) * esz);
+  s.os = (size_t)c.take<unsigned char>((size_t)n_dst * agg_ktot(d) * esz + 128);   // + whole last GEMM piece
   s.total = c.used();
   return s;
 }
