@@ -6,6 +6,7 @@
 #include <stddef.h>
 #include <string>
 #include <vector>
+#include <algorithm>
 #include <cstdio>
 #include <cstdarg>
 
@@ -15,6 +16,7 @@ struct dsmp_handle {
   int device = 0;
   hipStream_t stream = nullptr;
   int edge_algo = 0;   // DSMP_EDGE_AUTO / PER_EDGE / AGGREGATE
+  int n_cu = 256;      // compute units of the device (sizes persistent grids)
   std::string err;
   // kernel timing (opt-in)
   struct Mark {

@@ -125,6 +125,8 @@ extern "C" dsmp_status dsmp_create(dsmp_handle** out, int device) {
   dsmp_handle* h = new (std::nothrow) dsmp_handle();
   if (!h) return DSMP_HIP_ERROR;
   h->device = device;
+  int cu = 0;
+  if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, device) == hipSuccess && cu > 0) h->n_cu = cu;
   *out = h;
   return DSMP_OK;
 }

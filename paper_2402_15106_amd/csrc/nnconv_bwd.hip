@@ -222,17 +222,16 @@ struct DzShape {
 // Epilogue of the dz kernels: acc[t][kt] holds dz of the lane's edge (tile t)
 // for k in tile kt (register i is permuted position 16*kt + i).  Writes
 // da2 = dz * [z > 0] (permuted order), then dz1 = W2^T da2 on MFMA and
-// da1 = dz1 * [z1 > 0].
-template <typename T, int DL, int H1, int H2, int NT, int KT>
+// da1 = dz1 * [z1 > 0].  w2t: W2^T rows [h1][h2 permuted] with a row pitch of
+// W2P bytes (the packed copy in global memory, or a copy in LDS).
+template <typename T, int DL, int H1, int H2, int NT, int KT, int W2P = H2 * (int)sizeof(T)>
 __device__ __forceinline__ void dz_finish(const DzArgs& a, const f32x16 (&acc)[NT][KT], const int64_t (&eid)[NT],
-                                          const bool (&valid)[NT], int hh) {
+                                          const bool (&valid)[NT], int hh, const unsigned char* w2t) {
   using S = DzShape<T, DL, H1, H2>;
   using M = MT<T>;
   using frag = typename M::frag;
   constexpr int KS = S::KS, EPL = S::EPL, ESZ = S::ESZ;
   const int l32 = threadIdx.x & 31;
-  const unsigned char* P = a.packed;
-  const unsigned char* w2t = P + a.L.w2t;
   constexpr int MW1 = H1 / 64, MW2 = H2 / 64;
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
@@ -260,10 +259,13 @@ __device__ __forceinline__ void dz_finish(const DzArgs& a, const f32x16 (&acc)[N
     }
 #pragma unroll
     for (int jt = 0; jt < S::JT; ++jt) {
+      // from LDS the W2^T fragments are cheap to fetch per tile: keep the
+      // scheduler from hoisting all of them (registers)
+      if constexpr (W2P != H2 * (int)sizeof(T)) __builtin_amdgcn_sched_barrier(0);
       f32x16 C = f32x16{};
 #pragma unroll
       for (int s = 0; s < S::SK2; ++s) {
-        frag A = ld_frag<T>(w2t + ((size_t)(jt * 32 + l32) * H2 + s * KS + hh * EPL) * ESZ);
+        frag A = ld_frag<T>(w2t + (size_t)(jt * 32 + l32) * W2P + (s * KS + hh * EPL) * ESZ);
         C = M::mma(A, da2B[s], C);
       }
       // register i of tile jt is permuted position n = 16*jt + i
@@ -397,53 +399,68 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
     }
   }
 
-  dz_finish<T, DL, H1, H2, NT, S::KT>(a, acc, eid, valid, hh);
+  dz_finish<T, DL, H1, H2, NT, S::KT>(a, acc, eid, valid, hh, a.packed + a.L.w2t);
 }
 
 // Aggregate form of dz.  With U_i[k][p] = sum_q W3[p*d+q][k] g_i[q] for
 // every destination (one GEMM, k_u_gemm), dz_e[k] = sum_p U_i[k][p] h_j[p]
-// for each edge e into i.  One wave per destination: its edges in chunks of
-// two 32-edge tiles, the A operand is U_i^T read once per chunk, the B
-// operand the lane's own gathered row h_j (zero past the destination's last
-// edge).
+// for each edge e into i.  One wave per destination: its edges in 32-edge
+// tiles, the A operand is U_i^T, the B operand the lane's own gathered row
+// h_j (zero past the destination's last edge).  Workgroups are persistent
+// (as many as fit on the device, destinations taken in turn), so W2^T of the
+// epilogue is copied to LDS once per workgroup.
+template <typename T, int H1, int H2>
+struct DzAggShape {
+  static constexpr int W2P = H2 * (int)sizeof(T) + 16;   // LDS row pitch of W2^T
+  static constexpr int LDS = H1 * W2P;
+};
+
 template <typename T, int DL, int H1, int H2>
-__global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) void k_bwd_dz_agg(DzArgs a) {
+__global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 3 : 1) void k_bwd_dz_agg(DzArgs a) {
   using S = DzShape<T, DL, H1, H2>;
+  using SA = DzAggShape<T, H1, H2>;
   using M = MT<T>;
   using frag = typename M::frag;
-  constexpr int KS = S::KS, EPL = S::EPL, ESZ = S::ESZ, KT = S::KT, SKD = S::SKD, NT = S::NT;
+  constexpr int KS = S::KS, EPL = S::EPL, ESZ = S::ESZ, KT = S::KT, SKD = S::SKD, NT = 1;
+  extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
-  const int64_t i = (int64_t)blockIdx.x * 4 + wv;
-  if (i >= a.n_dst) return;
-  const int64_t pa = a.row_ptr[i], pb = a.row_ptr[i + 1];
-  const unsigned char* ur = a.U + ((size_t)i * H2 + l32) * DL * ESZ + hh * EPL * ESZ;
-  for (int64_t c0 = pa; c0 < pb; c0 += 32 * NT) {
-    int64_t eid[NT];
-    bool valid[NT];
-    frag hB[NT][SKD];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      eid[t] = c0 + t * 32 + l32;
-      valid[t] = eid[t] < pb;
-      const unsigned char* hr = a.h_in + (size_t)(valid[t] ? a.col[eid[t]] : 0) * DL * ESZ;
-#pragma unroll
-      for (int s = 0; s < SKD; ++s) hB[t][s] = valid[t] ? ld_frag<T>(hr + (s * KS + hh * EPL) * ESZ) : frag{};
-    }
-    f32x16 acc[NT][KT];
-#pragma unroll
-    for (int kt = 0; kt < KT; ++kt) {
-      frag A[SKD];
-#pragma unroll
-      for (int s = 0; s < SKD; ++s) A[s] = ld_frag<T>(ur + ((size_t)kt * 32 * DL + s * KS) * ESZ);
+  {
+    LdsStage<H1, H2 * ESZ> stg;
+    stg.init();
+    stg.issue(a.packed + a.L.w2t, smem);
+    stage_wait();
+    __syncthreads();
+  }
+  for (int64_t i = (int64_t)blockIdx.x * 4 + wv; i < a.n_dst; i += (int64_t)gridDim.x * 4) {
+    const int64_t pa = a.row_ptr[i], pb = a.row_ptr[i + 1];
+    const unsigned char* ur = a.U + ((size_t)i * H2 + l32) * DL * ESZ + hh * EPL * ESZ;
+    for (int64_t c0 = pa; c0 < pb; c0 += 32 * NT) {
+      int64_t eid[NT];
+      bool valid[NT];
+      frag hB[NT][SKD];
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        acc[t][kt] = f32x16{};
-        if (t == 0 || c0 + 32 * t < pb)   // wave-uniform: tile t has edges
+        eid[t] = c0 + t * 32 + l32;
+        valid[t] = eid[t] < pb;
+        const unsigned char* hr = a.h_in + (size_t)(valid[t] ? a.col[eid[t]] : 0) * DL * ESZ;
+#pragma unroll
+        for (int s = 0; s < SKD; ++s) hB[t][s] = valid[t] ? ld_frag<T>(hr + (s * KS + hh * EPL) * ESZ) : frag{};
+      }
+      f32x16 acc[NT][KT];
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt) {
+        frag A[SKD];
+#pragma unroll
+        for (int s = 0; s < SKD; ++s) A[s] = ld_frag<T>(ur + ((size_t)kt * 32 * DL + s * KS) * ESZ);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          acc[t][kt] = f32x16{};
 #pragma unroll
           for (int s = 0; s < SKD; ++s) acc[t][kt] = M::mma(A[s], hB[t][s], acc[t][kt]);
+        }
       }
+      dz_finish<T, DL, H1, H2, NT, KT, SA::W2P>(a, acc, eid, valid, hh, smem);
     }
-    dz_finish<T, DL, H1, H2, NT, KT>(a, acc, eid, valid, hh);
   }
 }
 
@@ -1069,8 +1086,14 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
       hipLaunchKernelGGL((k_u_gemm<T, DL, H2>), dim3((unsigned)ceil_div(dz.n_dst, 32), (unsigned)ceil_div(H2 * DL, 1024)),
                          dim3(256), 0, s, ua);
     }
+    using SA = DzAggShape<T, H1, H2>;
+    auto kz = k_bwd_dz_agg<T, DL, H1, H2>;
+    if ((st = set_lds(h, kz, SA::LDS)) != DSMP_OK) return st;
+    int per_cu = 0;
+    DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kz, 256, SA::LDS));
+    const int64_t grid = std::min<int64_t>(ceil_div(dz.n_dst, 4), (int64_t)h->n_cu * std::max(per_cu, 1));
     ProfScope prof(h, DSMP_K_DZ);
-    hipLaunchKernelGGL((k_bwd_dz_agg<T, DL, H1, H2>), dim3((unsigned)ceil_div(dz.n_dst, 4)), dim3(256), 0, s, dz);
+    hipLaunchKernelGGL(kz, dim3((unsigned)grid), dim3(256), SA::LDS, s, dz);
     DSMP_LAUNCHED(h, "dz (aggregate form)");
   } else if (dz.E > 0) {
     using S = DzShape<T, DL, H1, H2>;
