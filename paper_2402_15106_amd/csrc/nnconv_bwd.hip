@@ -472,16 +472,24 @@ struct UArgs {
 };
 
 // U[i][c] = sum_q W[c][q] g_i[q] for c = k*DL + p, as tiles C[c][i] (A = W
-// rows, B = the g rows, lane = destination).  Each 32x32 tile goes through a
-// per-wave LDS square so that the stores are 16-byte runs along c.  A wave
-// covers 32 destinations and 256 columns.
+// rows, B = the g rows, lane = destination).  A wave covers 32 destinations
+// and 256 columns; four 32x32 tiles at a time are collected in a per-wave LDS
+// block [destination][128 columns], which is then stored by rows of 128
+// columns (whole cache lines).
+template <typename T, int DL, int H2>
+struct UShape {
+  static constexpr int ESZ = sizeof(T), FC = 128;          // columns per flush
+  static constexpr int TROW = FC * ESZ + 16;               // LDS row pitch (bytes)
+  static constexpr int WAVE = 32 * TROW;
+};
+
 template <typename T, int DL, int H2>
 __global__ __launch_bounds__(256) void k_u_gemm(UArgs a) {
   using M = MT<T>;
   using frag = typename M::frag;
-  constexpr int KS = M::KS, EPL = M::EPL, ESZ = sizeof(T), SKD = DL / KS, NC = H2 * DL;
-  constexpr int TROW = 32 * ESZ + 16;                    // LDS row pitch of the square (bytes)
-  __shared__ __align__(16) unsigned char sq[4][32 * TROW];
+  using US = UShape<T, DL, H2>;
+  constexpr int KS = M::KS, EPL = M::EPL, ESZ = sizeof(T), SKD = DL / KS, NC = H2 * DL, TROW = US::TROW;
+  __shared__ __align__(16) unsigned char sq[4][US::WAVE];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
   const int64_t i0 = (int64_t)blockIdx.x * 32;
   const int64_t c0 = ((int64_t)blockIdx.y * 4 + wv) * 256;
@@ -491,7 +499,7 @@ __global__ __launch_bounds__(256) void k_u_gemm(UArgs a) {
 #pragma unroll
   for (int s = 0; s < SKD; ++s) B[s] = ld_frag<T>(a.G + ((size_t)row * DL + s * KS + hh * EPL) * ESZ);
   unsigned char* t = sq[wv];
-  constexpr int CH = 32 * ESZ / 16;                      // 16-byte chunks per row of the square
+  constexpr int CH = US::FC * ESZ / 16;                    // 16-byte chunks per LDS row
   // the next column tile's W rows are in flight while this tile is multiplied and stored
   frag An[SKD];
 #pragma unroll
@@ -508,10 +516,10 @@ __global__ __launch_bounds__(256) void k_u_gemm(UArgs a) {
     f32x16 C = f32x16{};
 #pragma unroll
     for (int s = 0; s < SKD; ++s) C = M::mma(A[s], B[s], C);
-    // square row = destination (lane), columns 8(r/4) + 4hh + r%4
+    // LDS row = destination (lane), columns 32 (ct % 4) + 8(r/4) + 4hh + r%4
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      unsigned char* o = t + l32 * TROW + (8 * g + 4 * hh) * ESZ;
+      unsigned char* o = t + l32 * TROW + (32 * (ct % 4) + 8 * g + 4 * hh) * ESZ;
       if constexpr (ESZ == 2) {
         const bf16x2 lo = __builtin_convertvector((f32x2){C[4 * g], C[4 * g + 1]}, bf16x2);
         const bf16x2 hi = __builtin_convertvector((f32x2){C[4 * g + 2], C[4 * g + 3]}, bf16x2);
@@ -520,14 +528,17 @@ __global__ __launch_bounds__(256) void k_u_gemm(UArgs a) {
         *reinterpret_cast<f32x4*>(o) = f32x4{C[4 * g], C[4 * g + 1], C[4 * g + 2], C[4 * g + 3]};
       }
     }
-    __builtin_amdgcn_wave_barrier();
+    if (ct % 4 == 3) {
+      const int64_t cf = c - 96;   // first column of this flush
+      __builtin_amdgcn_wave_barrier();
 #pragma unroll
-    for (int it = 0; it < 32 * CH / 64; ++it) {
-      const int id = it * 64 + lane, r = id / CH, ch = id % CH;
-      const uint4 v = *reinterpret_cast<const uint4*>(t + r * TROW + ch * 16);
-      if (i0 + r < a.n_rows) *reinterpret_cast<uint4*>(a.U + ((size_t)(i0 + r) * NC + c) * ESZ + ch * 16) = v;
+      for (int it = 0; it < 32 * CH / 64; ++it) {
+        const int id = it * 64 + lane, r = id / CH, ch = id % CH;
+        const uint4 v = *reinterpret_cast<const uint4*>(t + r * TROW + ch * 16);
+        if (i0 + r < a.n_rows) *reinterpret_cast<uint4*>(a.U + ((size_t)(i0 + r) * NC + cf) * ESZ + ch * 16) = v;
+      }
+      __builtin_amdgcn_wave_barrier();
     }
-    __builtin_amdgcn_wave_barrier();
   }
 }
 
