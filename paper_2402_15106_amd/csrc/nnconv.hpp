@@ -124,8 +124,99 @@ __device__ __forceinline__ void lds_copy_async(const unsigned char* src, unsigne
   }
 }
 
+// Direct global-to-LDS staging of one RB-byte piece of each of ROWS rows (row
+// stride in bytes given at init; with RB a multiple of 128 every wave-wide
+// load covers whole cache lines).  LDS rows have a pitch of RB + 16 * PADU
+// bytes; units in the padding slots re-read their row's first unit, rows at
+// or past nvalid re-read the last valid row, and lanes past the end of the
+// block are masked off.  Complete for the workgroup after stage_wait() and a
+// barrier.
+template <int ROWS, int RB = 128, int PADU = 1>
+struct RowStage {
+  static constexpr int PITCH = RB + 16 * PADU, NU = RB / 16, PU = NU + PADU, UNITS = ROWS * PU;
+  static constexpr int PER = (UNITS + 255) / 256;
+  uint32_t off[PER];
+  __device__ __forceinline__ void init(int64_t stride, int nvalid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int U = i * 256 + (int)threadIdx.x;
+      int r = U / PU;
+      const int u = U % PU;
+      if (r > nvalid - 1) r = nvalid - 1;
+      off[i] = (uint32_t)(r * stride + (u < NU ? u : 0) * 16);
+    }
+  }
+  __device__ __forceinline__ void issue(const unsigned char* src, unsigned char* dst) const {
+    const int wbase = (int)(threadIdx.x & ~63u);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      if (UNITS % 256 == 0 || i + 1 < PER || i * 256 + (int)threadIdx.x < UNITS) {
+        uint32_t o = off[i];
+        asm volatile("" : "+v"(o));
+        __builtin_amdgcn_global_load_lds((gbl_void_t*)(src + o),
+                                         (lds_void_t*)(dst + (size_t)(i * 256 + wbase) * 16), 16, 0, 0);
+      }
+    }
+  }
+};
+
+// A bf16 32x32x16 operand fragment whose contraction index runs down the rows
+// of a row-major 16-bit matrix X in LDS (row pitch in bytes, a multiple of 8):
+// lane (n = l%32, h = l/32) receives X[r0 + 8h + t][c0 + n], t < 8 (c0 a
+// multiple of 4).  Two transposing LDS reads: in each, lane 4j + q of a
+// 16-lane group names the 8 bytes X[r + j][c + 4q .. c + 4q + 3], and lane m
+// of the group receives column c + m of the four rows r .. r + 3.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+__device__ __forceinline__ bf16x8 lds_frag_rows(const unsigned char* X, int pitch, int r0, int c0) {
+  const int l = threadIdx.x & 63, g = l >> 4, j = (l >> 2) & 3, q = l & 3;
+  const unsigned char* p = X + (r0 + 8 * (g >> 1) + j) * pitch + (c0 + 16 * (g & 1) + 4 * q) * 2;
+  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 4 * pitch));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
 // Wait for this thread's outstanding global loads, the LDS stages included.
 __device__ __forceinline__ void stage_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Edge attributes of edge (i <- j): concat [p_i, p_j, s_i, s_j] or diff
+// v_i - v_j, zero-padded to 8 (Sec. 2.1).
+__device__ __forceinline__ void edge_attr(const float* __restrict__ na, int dim, int mode, int i, int j,
+                                          float x[8]) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) x[c] = 0.0f;
+  const float* vi = na + (size_t)i * (dim + 1);
+  const float* vj = na + (size_t)j * (dim + 1);
+  if (dim == 2) {
+    if (mode == DSMP_ATTR_CONCAT) {
+      x[0] = vi[0]; x[1] = vi[1]; x[2] = vj[0]; x[3] = vj[1]; x[4] = vi[2]; x[5] = vj[2];
+    } else {
+      x[0] = vi[0] - vj[0]; x[1] = vi[1] - vj[1]; x[2] = vi[2] - vj[2];
+    }
+  } else {
+    if (mode == DSMP_ATTR_CONCAT) {
+      x[0] = vi[0]; x[1] = vi[1]; x[2] = vi[2]; x[3] = vj[0]; x[4] = vj[1]; x[5] = vj[2];
+      x[6] = vi[3]; x[7] = vj[3];
+    } else {
+      x[0] = vi[0] - vj[0]; x[1] = vi[1] - vj[1]; x[2] = vi[2] - vj[2]; x[3] = vi[3] - vj[3];
+    }
+  }
+}
+
+// Pre-activation of the first kernel-MLP layer for one output: b1 + W1 x as
+// a chain of fused multiply-adds in attribute order (w: the 8 weights of the
+// output, zero past de).
+__device__ __forceinline__ float layer1_pre(const float* __restrict__ w, float b, const float x[8]) {
+  const f32x4 wa = *reinterpret_cast<const f32x4*>(w);
+  const f32x4 wb = *reinterpret_cast<const f32x4*>(w + 4);
+  float v = b;
+  v = __builtin_fmaf(wa[0], x[0], v); v = __builtin_fmaf(wa[1], x[1], v);
+  v = __builtin_fmaf(wa[2], x[2], v); v = __builtin_fmaf(wa[3], x[3], v);
+  v = __builtin_fmaf(wb[0], x[4], v); v = __builtin_fmaf(wb[1], x[5], v);
+  v = __builtin_fmaf(wb[2], x[6], v); v = __builtin_fmaf(wb[3], x[7], v);
+  return v;
+}
 
 // Byte offsets of the sections of a packed parameter buffer.
 struct PackLayout {

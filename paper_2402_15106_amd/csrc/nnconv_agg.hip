@@ -179,39 +179,6 @@ struct GemmArgs {
   float* part;               // [nsl][n_rows][DL] partial products
 };
 
-// Direct global-to-LDS staging of one 128-byte piece of each of ROWS rows
-// (row stride in bytes given at init): every wave-wide load covers whole
-// cache lines.  LDS rows have a pitch of 144 bytes; a unit in the padding slot
-// re-reads its row's first unit, rows at or past nvalid re-read the last valid
-// row, and lanes past the end of the block are masked off.
-template <int ROWS>
-struct RowStage {
-  static constexpr int PITCH = 144, NU = 8, PU = 9, UNITS = ROWS * PU, PER = (UNITS + 255) / 256;
-  uint32_t off[PER];
-  __device__ __forceinline__ void init(int64_t stride, int nvalid) {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int U = i * 256 + (int)threadIdx.x;
-      int r = U / PU;
-      const int u = U % PU;
-      if (r > nvalid - 1) r = nvalid - 1;
-      off[i] = (uint32_t)(r * stride + (u < NU ? u : 0) * 16);
-    }
-  }
-  __device__ __forceinline__ void issue(const unsigned char* src, unsigned char* dst) const {
-    const int wbase = (int)(threadIdx.x & ~63u);
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      if (UNITS % 256 == 0 || i + 1 < PER || i * 256 + (int)threadIdx.x < UNITS) {
-        uint32_t o = off[i];
-        asm volatile("" : "+v"(o));
-        __builtin_amdgcn_global_load_lds((gbl_void_t*)(src + o),
-                                         (lds_void_t*)(dst + (size_t)(i * 256 + wbase) * 16), 16, 0, 0);
-      }
-    }
-  }
-};
-
 template <typename T, int DL>
 struct GemmShape {
   static constexpr int ESZ = sizeof(T), KS = MT<T>::KS;

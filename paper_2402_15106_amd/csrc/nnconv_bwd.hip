@@ -40,27 +40,6 @@ __device__ __forceinline__ typename MT<T>::frag ld_frag(const void* p) {
 __device__ __forceinline__ float to_f(__bf16 x) { return (float)x; }
 __device__ __forceinline__ float to_f(float x) { return x; }
 
-__device__ __forceinline__ void edge_attr(const float* __restrict__ na, int dim, int mode, int i, int j,
-                                          float x[8]) {
-#pragma unroll
-  for (int c = 0; c < 8; ++c) x[c] = 0.0f;
-  const float* vi = na + (size_t)i * (dim + 1);
-  const float* vj = na + (size_t)j * (dim + 1);
-  if (dim == 2) {
-    if (mode == DSMP_ATTR_CONCAT) {
-      x[0] = vi[0]; x[1] = vi[1]; x[2] = vj[0]; x[3] = vj[1]; x[4] = vi[2]; x[5] = vj[2];
-    } else {
-      x[0] = vi[0] - vj[0]; x[1] = vi[1] - vj[1]; x[2] = vi[2] - vj[2];
-    }
-  } else {
-    if (mode == DSMP_ATTR_CONCAT) {
-      x[0] = vi[0]; x[1] = vi[1]; x[2] = vi[2]; x[3] = vj[0]; x[4] = vj[1]; x[5] = vj[2];
-      x[6] = vi[3]; x[7] = vj[3];
-    } else {
-      x[0] = vi[0] - vj[0]; x[1] = vi[1] - vj[1]; x[2] = vi[2] - vj[2]; x[3] = vi[3] - vj[3];
-    }
-  }
-}
 
 // ------------------------------------------------------------ node pre-pass
 
@@ -1048,7 +1027,7 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   w.dh_direct = c.take<float>((size_t)n_src * d.d);
   w.dh_part = c.take<float>((size_t)(ceil_div(E, EDGE_TILE) + 1) * 2 * d.d);
   // aggregate form: per-source sums T and the K-slices of their W3 GEMM
-  w.ot = c.take<unsigned char>((size_t)n_src * agg_ktot(d) * esz + 128);   // + whole last GEMM piece
+  w.ot = c.take<unsigned char>((size_t)n_src * agg_ktot(d) * esz + 256);   // + whole last staged piece
   w.nslh = agg_gemm_slices(n_src, d);
   w.dh_sl = c.take<float>((size_t)w.nslh * n_src * d.d);
   w.U = c.take<unsigned char>((size_t)n_dst * d.h2 * d.d * esz);

@@ -75,28 +75,6 @@ struct Shape {
   static constexpr int LDS = LDS_MAIN > LDS_MSG ? LDS_MAIN : LDS_MSG;
 };
 
-// Edge attributes of edge (i <- j): concat [p_i, p_j, s_i, s_j] or diff v_i - v_j.
-__device__ __forceinline__ void edge_attr(const float* __restrict__ na, int dim, int mode, int i,
-                                          int j, float x[8]) {
-#pragma unroll
-  for (int c = 0; c < 8; ++c) x[c] = 0.0f;
-  const float* vi = na + (size_t)i * (dim + 1);
-  const float* vj = na + (size_t)j * (dim + 1);
-  if (dim == 2) {
-    if (mode == DSMP_ATTR_CONCAT) {
-      x[0] = vi[0]; x[1] = vi[1]; x[2] = vj[0]; x[3] = vj[1]; x[4] = vi[2]; x[5] = vj[2];
-    } else {
-      x[0] = vi[0] - vj[0]; x[1] = vi[1] - vj[1]; x[2] = vi[2] - vj[2];
-    }
-  } else {
-    if (mode == DSMP_ATTR_CONCAT) {
-      x[0] = vi[0]; x[1] = vi[1]; x[2] = vi[2]; x[3] = vj[0]; x[4] = vj[1]; x[5] = vj[2];
-      x[6] = vi[3]; x[7] = vj[3];
-    } else {
-      x[0] = vi[0] - vj[0]; x[1] = vi[1] - vj[1]; x[2] = vi[2] - vj[2]; x[3] = vi[3] - vj[3];
-    }
-  }
-}
 
 // Two workgroups per CU when registers and LDS allow (d <= 64), so one
 // workgroup's MFMA chains overlap the other's barriers and epilogues.
@@ -199,17 +177,10 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
 #pragma unroll
       for (int u = 0; u < EPL; ++u) {
         const int n = s * EPL + u;
-        const f32x4 wa = *reinterpret_cast<const f32x4*>(w1h + n * 8);
-        const f32x4 wb = *reinterpret_cast<const f32x4*>(w1h + n * 8 + 4);
         const float bn = b1h[n];
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-          // b1 + W1 x as a chain of fused multiply-adds in attribute order
-          float v = bn;
-          v = __builtin_fmaf(wa[0], x[t][0], v); v = __builtin_fmaf(wa[1], x[t][1], v);
-          v = __builtin_fmaf(wa[2], x[t][2], v); v = __builtin_fmaf(wa[3], x[t][3], v);
-          v = __builtin_fmaf(wb[0], x[t][4], v); v = __builtin_fmaf(wb[1], x[t][5], v);
-          v = __builtin_fmaf(wb[2], x[t][6], v); v = __builtin_fmaf(wb[3], x[t][7], v);
+          const float v = layer1_pre(w1h + n * 8, bn, x[t]);
           zv[t][u] = v > 0.0f ? v : 0.0f;
           if (v > 0.0f) m1[t][(s * EPL + u) / 32] |= 1u << ((s * EPL + u) % 32);
         }
@@ -691,7 +662,7 @@ SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E) {
   s.zE = (size_t)c.take<unsigned char>((size_t)E * d.h2 * esz);
   s.z1E = (size_t)c.take<unsigned char>((size_t)E * d.h1 * esz);
   s.zmask = (size_t)c.take<unsigned char>((size_t)E * (d.h1 + d.h2) / 8);
-  s.os = (size_t)c.take<unsigned char>((size_t)n_dst * agg_ktot(d) * esz + 128);   // + whole last GEMM piece
+  s.os = (size_t)c.take<unsigned char>((size_t)n_dst * agg_ktot(d) * esz + 256);   // + whole last staged piece
   s.total = c.used();
   return s;
 }
