@@ -383,11 +383,16 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
 
 // Aggregate form of dz.  With U_i[k][p] = sum_q W3[p*d+q][k] g_i[q] for
 // every destination (one GEMM, k_u_gemm), dz_e[k] = sum_p U_i[k][p] h_j[p]
-// for each edge e into i.  One wave per destination: its edges in 32-edge
-// tiles, the A operand is U_i^T, the B operand the lane's own gathered row
-// h_j (zero past the destination's last edge).  Workgroups are persistent
-// (as many as fit on the device, destinations taken in turn), so W2^T of the
-// epilogue is copied to LDS once per workgroup.
+// for each edge e into i.  The work items are 32-edge tiles of one
+// destination: the A operand is U_i^T, the B operand the lane's own gathered
+// row h_j (zero past the destination's last edge).  Workgroups are persistent
+// (as many as fit on the device), so W2^T of the epilogue is copied to LDS
+// once per workgroup; each takes blocks of DZ_NB consecutive destinations in
+// turn and lists their tiles in LDS, and its four waves take consecutive
+// tiles, so the tiles of one destination run side by side and U_i comes from
+// HBM once.
+constexpr int DZ_NB = 16;
+
 template <typename T, int H1, int H2>
 struct DzAggShape {
   static constexpr int W2P = H2 * (int)sizeof(T) + 16;   // LDS row pitch of W2^T
@@ -410,10 +415,32 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 3 : 1) v
     stage_wait();
     __syncthreads();
   }
-  for (int64_t i = (int64_t)blockIdx.x * 4 + wv; i < a.n_dst; i += (int64_t)gridDim.x * 4) {
-    const int64_t pa = a.row_ptr[i], pb = a.row_ptr[i + 1];
-    const unsigned char* ur = a.U + ((size_t)i * H2 + l32) * DL * ESZ + hh * EPL * ESZ;
-    for (int64_t c0 = pa; c0 < pb; c0 += 32 * NT) {
+  __shared__ int tstart[DZ_NB + 1];   // first tile of each destination of the block
+  const int64_t nblk = (a.n_dst + DZ_NB - 1) / DZ_NB;
+  for (int64_t blk = blockIdx.x; blk < nblk; blk += gridDim.x) {
+    const int64_t d0 = blk * DZ_NB;
+    const int nd = (int)(a.n_dst - d0 < DZ_NB ? a.n_dst - d0 : DZ_NB);
+    if (wv == 0) {
+      // tiles per destination, inclusive prefix over the block's lanes
+      int nt = 0;
+      if (lane < nd) nt = (a.row_ptr[d0 + lane + 1] - a.row_ptr[d0 + lane] + 31) / 32;
+#pragma unroll
+      for (int o = 1; o < DZ_NB; o <<= 1) {
+        const int v = __shfl_up(nt, o, 64);
+        if (lane >= o) nt += v;
+      }
+      if (lane < DZ_NB) tstart[lane + 1] = nt;
+      if (lane == 0) tstart[0] = 0;
+    }
+    __syncthreads();
+    const int ntile = tstart[nd];
+    for (int tau = wv; tau < ntile; tau += 4) {
+      int k = 0;
+      while (tstart[k + 1] <= tau) ++k;   // destination of tile tau (k < nd)
+      const int64_t i = d0 + k;
+      const int64_t pa = a.row_ptr[i], pb = a.row_ptr[i + 1];
+      const int64_t c0 = pa + (int64_t)(tau - tstart[k]) * 32;
+      const unsigned char* ur = a.U + ((size_t)i * H2 + l32) * DL * ESZ + hh * EPL * ESZ;
       int64_t eid[NT];
       bool valid[NT];
       frag hB[NT][SKD];
@@ -440,6 +467,7 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 3 : 1) v
       }
       dz_finish<T, DL, H1, H2, NT, KT, SA::W2P>(a, acc, eid, valid, hh, smem);
     }
+    __syncthreads();   // the block's tile list is read until every wave is done
   }
 }
 
