@@ -168,6 +168,104 @@ __global__ __launch_bounds__(256) void k_outer_sum(OuterArgs a) {
   if (tid < DL) reinterpret_cast<T*>(o)[(size_t)H2 * DL + tid] = (T)hs;
 }
 
+// bf16: the chunk's rows of z~ and of the gathered rows are copied to LDS as
+// they are (each wave-wide load covers four whole z rows or eight gathered
+// rows), and the fragments, whose contraction index is the edge, come from
+// transposing LDS reads.  Slots past the segment's last edge re-read its last
+// edge and are zeroed in the A fragment.
+template <int DL, int H2>
+struct OuterTrShape {
+  static constexpr int ECH = 64;
+  static constexpr int ZP = H2 * 2 + 32, UP = DL * 2 + 32;     // LDS row pitches (two padding units)
+  static constexpr int ZNU = H2 * 2 / 16, UNU = DL * 2 / 16;   // 16-byte units per row
+  static constexpr int ZU = ECH * (ZNU + 2), UU = ECH * (UNU + 2);
+  static constexpr int NKT = H2 / 32, NCT = DL / 32, NTILE = NKT * NCT, TPW = (NTILE + 3) / 4;
+  static constexpr int LDS = ECH * (ZP + UP);
+  static constexpr int64_t KTOT = (int64_t)H2 * DL + DL;
+};
+
+template <int DL, int H2>
+__global__ __launch_bounds__(256) void k_outer_sum_tr(OuterArgs a) {
+  using S = OuterTrShape<DL, H2>;
+  using M = MT<__bf16>;
+  constexpr int ECH = S::ECH;
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int rz[ECH], ru[ECH];   // source rows of the chunk's z and gathered rows
+  unsigned char* zl = smem;
+  unsigned char* ul = smem + ECH * S::ZP;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int64_t n = blockIdx.x;
+  const int64_t pa = a.seg_ptr[n], pb = a.seg_ptr[n + 1];
+
+  f32x16 acc[S::TPW];
+#pragma unroll
+  for (int j = 0; j < S::TPW; ++j) acc[j] = f32x16{};
+  float hs = 0.0f;   // z~ = 1 row: sum of the gathered rows (threads tid < DL)
+
+  for (int64_t c0 = pa; c0 < pb; c0 += ECH) {
+    const int cnt = (int)(pb - c0 < ECH ? pb - c0 : ECH);
+    __syncthreads();   // previous chunk fully consumed
+    if (tid < ECH) {
+      const int64_t pos = c0 + (tid < cnt ? tid : cnt - 1);
+      const int64_t e = a.pos_eid ? (int64_t)a.pos_eid[pos] : pos;
+      rz[tid] = (int)e;
+      ru[tid] = a.row_of[e];
+    }
+    __syncthreads();
+    const int wbase = tid & ~63;
+    for (int U0 = 0; U0 < S::ZU; U0 += 256) {
+      const int U = U0 + tid, r = U / (S::ZNU + 2), u = U % (S::ZNU + 2);
+      if (U < S::ZU)
+        __builtin_amdgcn_global_load_lds(
+            (gbl_void_t*)(a.zE + (size_t)rz[r < ECH ? r : ECH - 1] * H2 * 2 + (u < S::ZNU ? u : 0) * 16),
+            (lds_void_t*)(zl + (size_t)(U0 + wbase) * 16), 16, 0, 0);
+    }
+    for (int U0 = 0; U0 < S::UU; U0 += 256) {
+      const int U = U0 + tid, r = U / (S::UNU + 2), u = U % (S::UNU + 2);
+      if (U < S::UU)
+        __builtin_amdgcn_global_load_lds(
+            (gbl_void_t*)(a.u + (size_t)ru[r < ECH ? r : ECH - 1] * DL * 2 + (u < S::UNU ? u : 0) * 16),
+            (lds_void_t*)(ul + (size_t)(U0 + wbase) * 16), 16, 0, 0);
+    }
+    stage_wait();
+    __syncthreads();
+    const int nks = (cnt + 15) / 16;
+    for (int ks = 0; ks < nks; ++ks) {
+#pragma unroll
+      for (int j = 0; j < S::TPW; ++j) {
+        const int ti = wv + 4 * j;
+        if (ti < S::NTILE) {
+          const int kt = ti / S::NCT, ct = ti % S::NCT;
+          bf16x8 A = lds_frag_rows(zl, S::ZP, ks * 16, kt * 32);
+          if (ks * 16 + 16 > cnt) {   // slots past the last edge
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+              if (ks * 16 + 8 * hh + t >= cnt) A[t] = (__bf16)0.0f;
+          }
+          acc[j] = M::mma(A, lds_frag_rows(ul, S::UP, ks * 16, ct * 32), acc[j]);
+        }
+      }
+    }
+    if (tid < DL)
+      for (int e = 0; e < cnt; ++e) hs += (float)*reinterpret_cast<const __bf16*>(ul + e * S::UP + tid * 2);
+  }
+
+  unsigned char* o = a.out + (size_t)n * S::KTOT * 2;
+#pragma unroll
+  for (int j = 0; j < S::TPW; ++j) {
+    const int ti = wv + 4 * j;
+    if (ti < S::NTILE) {
+      unsigned char* dst = o + ((size_t)ti * 1024 + lane * 16) * 2;
+      float v[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) v[r] = acc[j][r];
+      *reinterpret_cast<bf16x8*>(dst) = pack_frag<__bf16>(v);
+      *reinterpret_cast<bf16x8*>(dst + 16) = pack_frag<__bf16>(v + 8);
+    }
+  }
+  if (tid < DL) reinterpret_cast<__bf16*>(o)[(size_t)H2 * DL + tid] = (__bf16)hs;
+}
+
 // ------------------------------------------------------------ GEMM with W3~
 
 struct GemmArgs {
@@ -370,6 +468,15 @@ dsmp_status set_lds_bytes(dsmp_handle* h, K kernel, int bytes) {
 
 template <typename T, int DL, int H2>
 dsmp_status outer_shape(dsmp_handle* h, const OuterArgs& a) {
+  if constexpr (sizeof(T) == 2) {
+    using S = OuterTrShape<DL, H2>;
+    auto kern = k_outer_sum_tr<DL, H2>;
+    dsmp_status st = set_lds_bytes(h, kern, S::LDS);
+    if (st != DSMP_OK) return st;
+    hipLaunchKernelGGL(kern, dim3((unsigned)a.n_seg), dim3(256), S::LDS, h->stream, a);
+    DSMP_LAUNCHED(h, "segment outer-product sums");
+    return DSMP_OK;
+  }
   using S = OuterShape<T, DL, H2>;
   auto kern = k_outer_sum<T, DL, H2>;
   dsmp_status st = set_lds_bytes(h, kern, S::LDS);
