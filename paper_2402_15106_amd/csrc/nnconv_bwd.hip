@@ -889,6 +889,99 @@ __global__ __launch_bounds__(256, 2) void k_bwd_dW2(W2Args a) {
   if (split == 0 && tid < H2) out[H2 * H1 + kperm<T>(tid)] = bsum;
 }
 
+// bf16: chunks of 64 edge rows of da2 and z1 are copied to LDS as they are
+// (whole cache lines, the next chunk in flight while this one is multiplied)
+// and the fragments, whose contraction index is the edge, come from
+// transposing LDS reads.  Rows past the range re-read its last row and are
+// zeroed in the A fragment.
+template <int H1, int H2>
+struct W2TrShape {
+  static constexpr int ECH = 64;
+  using DS = RowStage<ECH, H2 * 2, 2>;
+  using ZS = RowStage<ECH, H1 * 2, 2>;
+  static constexpr int DB = ECH * DS::PITCH, BUF = DB + ECH * ZS::PITCH, LDS = 2 * BUF;
+};
+
+template <int H1, int H2>
+__global__ __launch_bounds__(256, 2) void k_bwd_dW2_tr(W2Args a) {
+  using S = W2Shape<__bf16, H1, H2>;
+  using TS = W2TrShape<H1, H2>;
+  using M = MT<__bf16>;
+  constexpr int ECH = TS::ECH;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int split = blockIdx.x % S::NSPLIT, chunk = blockIdx.x / S::NSPLIT;
+  const int kt0 = (wv / S::JGRP) * S::KT_W;
+  const int jt0 = split * S::JT_WG + (wv % S::JGRP) * S::JT_W;
+  const int64_t e_begin = (int64_t)chunk * a.per_chunk;
+  int64_t e_end = e_begin + a.per_chunk;
+  if (e_end > a.E) e_end = a.E;
+  f32x16 acc[S::KT_W][S::JT_W];
+#pragma unroll
+  for (int kk = 0; kk < S::KT_W; ++kk)
+#pragma unroll
+    for (int jj = 0; jj < S::JT_W; ++jj) acc[kk][jj] = f32x16{};
+  float bsum = 0.0f;
+  if (e_begin < e_end) {   // uniform over the workgroup
+    const int nch = (int)((e_end - e_begin + ECH - 1) / ECH);
+    typename TS::DS sd;
+    typename TS::ZS sz;
+    auto issue = [&](int c, unsigned char* buf) {
+      const int64_t e0 = e_begin + (int64_t)c * ECH;
+      const int nv = (int)(e_end - e0 < ECH ? e_end - e0 : ECH);
+      sd.init(H2 * 2, nv);
+      sz.init(H1 * 2, nv);
+      sd.issue(a.da2E + (size_t)e0 * H2 * 2, buf);
+      sz.issue(a.z1E + (size_t)e0 * H1 * 2, buf + TS::DB);
+    };
+    issue(0, smem);
+    stage_wait();
+    __syncthreads();
+    for (int c = 0; c < nch; ++c) {
+      const unsigned char* cur = smem + (c & 1) * TS::BUF;
+      if (c + 1 < nch) issue(c + 1, smem + ((c + 1) & 1) * TS::BUF);
+      const int64_t e0 = e_begin + (int64_t)c * ECH;
+      const int cnt = (int)(e_end - e0 < ECH ? e_end - e0 : ECH);
+      if (split == 0 && tid < H2)
+        for (int e = 0; e < cnt; ++e) bsum += (float)*reinterpret_cast<const __bf16*>(cur + e * TS::DS::PITCH + tid * 2);
+      for (int ks = 0; ks < (cnt + 15) / 16; ++ks) {
+        bf16x8 A[S::KT_W];
+#pragma unroll
+        for (int kk = 0; kk < S::KT_W; ++kk) {
+          A[kk] = lds_frag_rows(cur, TS::DS::PITCH, ks * 16, (kt0 + kk) * 32);
+          if (ks * 16 + 16 > cnt) {
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+              if (ks * 16 + 8 * hh + t >= cnt) A[kk][t] = (__bf16)0.0f;
+          }
+        }
+#pragma unroll
+        for (int jj = 0; jj < S::JT_W; ++jj) {
+          const bf16x8 B = lds_frag_rows(cur + TS::DB, TS::ZS::PITCH, ks * 16, (jt0 + jj) * 32);
+#pragma unroll
+          for (int kk = 0; kk < S::KT_W; ++kk) acc[kk][jj] = M::mma(A[kk], B, acc[kk][jj]);
+        }
+      }
+      stage_wait();
+      __syncthreads();
+    }
+  }
+  float* out = a.part + (size_t)chunk * (H2 * H1 + H2);
+  // tile rows and columns are stored-order positions; map them back to (k, j)
+#pragma unroll
+  for (int jj = 0; jj < S::JT_W; ++jj) {
+    const int j = kperm<__bf16>((jt0 + jj) * 32 + l32);
+#pragma unroll
+    for (int kk = 0; kk < S::KT_W; ++kk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int k = kperm<__bf16>((kt0 + kk) * 32 + 8 * (i / 4) + 4 * hh + (i % 4));
+        out[(size_t)k * H1 + j] = acc[kk][jj][i];
+      }
+  }
+  if (split == 0 && tid < H2) out[H2 * H1 + kperm<__bf16>(tid)] = bsum;
+}
+
 // ------------------------------------------------------------ dW1 / db1 (split over edges)
 
 template <typename T, int H1>
@@ -1131,12 +1224,20 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
   }
   {
     using S = W2Shape<T, H1, H2>;
-    auto k2 = k_bwd_dW2<T, H1, H2>;
-    if ((st = set_lds(h, k2, S::LDS)) != DSMP_OK) return st;
     int nchunk = (int)((w2.E + w2.per_chunk - 1) / w2.per_chunk);
     if (nchunk < 1) nchunk = 1;
-    ProfScope prof(h, DSMP_K_DW2);
-    hipLaunchKernelGGL(k2, dim3(nchunk * S::NSPLIT), dim3(256), S::LDS, s, w2);
+    if constexpr (sizeof(T) == 2) {
+      using TS = W2TrShape<H1, H2>;
+      auto k2 = k_bwd_dW2_tr<H1, H2>;
+      if ((st = set_lds(h, k2, TS::LDS)) != DSMP_OK) return st;
+      ProfScope prof(h, DSMP_K_DW2);
+      hipLaunchKernelGGL(k2, dim3(nchunk * S::NSPLIT), dim3(256), TS::LDS, s, w2);
+    } else {
+      auto k2 = k_bwd_dW2<T, H1, H2>;
+      if ((st = set_lds(h, k2, S::LDS)) != DSMP_OK) return st;
+      ProfScope prof(h, DSMP_K_DW2);
+      hipLaunchKernelGGL(k2, dim3(nchunk * S::NSPLIT), dim3(256), S::LDS, s, w2);
+    }
     DSMP_LAUNCHED(h, "dW2");
   }
   return DSMP_OK;
