@@ -275,6 +275,7 @@ struct EdgeArgs {
   unsigned char* zE;             // [E][h2] layer dtype: FWD writes (if set), DH reads
   unsigned char* z1E;            // [E][h1] layer dtype: FWD writes (if set)
   unsigned char* zmask;          // [E][(h1+h2)/8] ReLU mask bits of z1 and z: FWD writes (if set)
+  unsigned char* xE;             // [E][16] bf16 edge attributes, high then low parts: FWD writes (if set)
   float* out_direct;             // [segments][d]
   float* out_part;               // [tiles][2][d]
 };
@@ -284,10 +285,11 @@ dsmp_status launch_edge_contract(dsmp_handle* h, const dsmp_layer_desc& desc, in
 
 // Per-layer buffer the forward fills for the backward: y [n_dst][d] fp32,
 // z [E][h2] and z1 [E][h1] in the layer dtype and the permuted order, their
-// ReLU mask bits [E][(h1+h2)/8], and the per-destination sums
-// S [n_dst][(h2+1)d] of the aggregate form.
+// ReLU mask bits [E][(h1+h2)/8], the per-destination sums S [n_dst][(h2+1)d]
+// of the aggregate form, and (bf16 layers) the edge attributes split into
+// bf16 high and low parts [E][16] for the dW1 product.
 struct SavedLayout {
-  size_t y, zE, z1E, zmask, os, total;
+  size_t y, zE, z1E, zmask, os, xE, total;
 };
 SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E);
 size_t fwd_ws_bytes(const dsmp_layer_desc& d, int64_t n_dst, int64_t E);

@@ -1032,6 +1032,96 @@ __global__ __launch_bounds__(256) void k_bwd_dW1(int64_t E, int64_t per_chunk, c
   }
 }
 
+// bf16 layers: dW1[j][c] = sum_e da1[e][j] x_e[c] on MFMA.  Chunks of 64 edge
+// rows of da1 and of the saved attributes (bf16 high parts in columns 0..7,
+// low parts in 8..15) are copied to LDS by whole rows, double-buffered; the
+// two column halves added restore the attributes to about 16 bits.  Rows
+// past the range re-read its last row and are zeroed in the A fragment.
+// db1 sums the da1 rows.
+template <int H1>
+struct W1TrShape {
+  static constexpr int ECH = 64;
+  using AS = RowStage<ECH, H1 * 2, 2>;
+  using XS = RowStage<ECH, 32, 4>;   // 32 bytes of attributes per row, pitch 96
+  static constexpr int AB = ECH * AS::PITCH, BUF = AB + ECH * XS::PITCH, LDS = 2 * BUF;
+  static constexpr int JT = H1 / 32, JTW = (JT + 3) / 4;
+};
+
+template <int H1>
+__global__ __launch_bounds__(256) void k_bwd_dW1_tr(int64_t E, int64_t per_chunk, const unsigned char* __restrict__ da1E,
+                                                    const unsigned char* __restrict__ xE, int de,
+                                                    float* __restrict__ part) {
+  using S = W1TrShape<H1>;
+  using M = MT<__bf16>;
+  constexpr int ECH = S::ECH;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int64_t e_begin = (int64_t)blockIdx.x * per_chunk;
+  int64_t e_end = e_begin + per_chunk;
+  if (e_end > E) e_end = E;
+  f32x16 acc[S::JTW];
+#pragma unroll
+  for (int jw = 0; jw < S::JTW; ++jw) acc[jw] = f32x16{};
+  float bsum = 0.0f;
+  if (e_begin < e_end) {   // uniform over the workgroup
+    const int nch = (int)((e_end - e_begin + ECH - 1) / ECH);
+    typename S::AS sa;
+    typename S::XS sx;
+    auto issue = [&](int c, unsigned char* buf) {
+      const int64_t e0 = e_begin + (int64_t)c * ECH;
+      const int nv = (int)(e_end - e0 < ECH ? e_end - e0 : ECH);
+      sa.init(H1 * 2, nv);
+      sx.init(32, nv);
+      sa.issue(da1E + (size_t)e0 * H1 * 2, buf);
+      sx.issue(xE + (size_t)e0 * 32, buf + S::AB);
+    };
+    issue(0, smem);
+    stage_wait();
+    __syncthreads();
+    for (int c = 0; c < nch; ++c) {
+      const unsigned char* cur = smem + (c & 1) * S::BUF;
+      if (c + 1 < nch) issue(c + 1, smem + ((c + 1) & 1) * S::BUF);
+      const int64_t e0 = e_begin + (int64_t)c * ECH;
+      const int cnt = (int)(e_end - e0 < ECH ? e_end - e0 : ECH);
+      if (tid < H1)
+        for (int e = 0; e < cnt; ++e) bsum += (float)*reinterpret_cast<const __bf16*>(cur + e * S::AS::PITCH + tid * 2);
+      for (int ks = 0; ks < (cnt + 15) / 16; ++ks) {
+        const bf16x8 B = lds_frag_rows(cur + S::AB, S::XS::PITCH, ks * 16, 0);
+#pragma unroll
+        for (int jw = 0; jw < S::JTW; ++jw) {
+          const int jt = wv + 4 * jw;
+          if (jt < S::JT) {
+            bf16x8 A = lds_frag_rows(cur, S::AS::PITCH, ks * 16, jt * 32);
+            if (ks * 16 + 16 > cnt) {
+#pragma unroll
+              for (int t = 0; t < 8; ++t)
+                if (ks * 16 + 8 * hh + t >= cnt) A[t] = (__bf16)0.0f;
+            }
+            acc[jw] = M::mma(A, B, acc[jw]);
+          }
+        }
+      }
+      stage_wait();
+      __syncthreads();
+    }
+  }
+  float* out = part + (size_t)blockIdx.x * (H1 * de + H1);
+  // column c of a tile holds the high-part sums, column c + 8 the low-part sums
+#pragma unroll
+  for (int jw = 0; jw < S::JTW; ++jw) {
+    const int jt = wv + 4 * jw;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float lo = __shfl_down(acc[jw][i], 8, 64);
+      if (jt < S::JT && l32 < de) {
+        const int j = kperm<__bf16>(jt * 32 + 8 * (i / 4) + 4 * hh + (i % 4));
+        out[(size_t)j * de + l32] = acc[jw][i] + lo;
+      }
+    }
+  }
+  if (tid < H1) out[H1 * de + kperm<__bf16>(tid)] = bsum;
+}
+
 // ------------------------------------------------------------ reductions and finals
 
 // Fixed-order reductions out[x] = [out[x] +] sum_c part[c*stride + off + x]
@@ -1243,6 +1333,17 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
   return DSMP_OK;
 }
 
+template <int H1>
+dsmp_status launch_dw1_tr(dsmp_handle* h, int n1, int64_t E, int64_t pc1, const unsigned char* da1E,
+                          const unsigned char* xE, int de, float* part) {
+  using S = W1TrShape<H1>;
+  auto k1 = k_bwd_dW1_tr<H1>;
+  dsmp_status st = set_lds(h, k1, S::LDS);
+  if (st != DSMP_OK) return st;
+  hipLaunchKernelGGL(k1, dim3(n1), dim3(256), S::LDS, h->stream, E, pc1, da1E, xE, de, part);
+  return DSMP_OK;
+}
+
 dsmp_status dispatch_edge_grads(dsmp_handle* h, const dsmp_layer_desc& d, const DzArgs& dz, const W3Args& w3,
                                 const W2Args& w2) {
   if (d.dtype == DSMP_F32) {
@@ -1385,14 +1486,12 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
       hipLaunchKernelGGL((k_bwd_dW1<float, 128>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
                          d.dim, d.attr_mode, de, da1f, w.p_w1);
     else if (d.h1 == 64)
-      hipLaunchKernelGGL((k_bwd_dW1<__bf16, 64>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
-                         d.dim, d.attr_mode, de, da1b, w.p_w1);
+      st = launch_dw1_tr<64>(h, n1, E, w.pc1, w.da1E, sv + sl.xE, de, w.p_w1);
     else if (d.h1 == 128)
-      hipLaunchKernelGGL((k_bwd_dW1<__bf16, 128>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
-                         d.dim, d.attr_mode, de, da1b, w.p_w1);
+      st = launch_dw1_tr<128>(h, n1, E, w.pc1, w.da1E, sv + sl.xE, de, w.p_w1);
     else
-      hipLaunchKernelGGL((k_bwd_dW1<__bf16, 256>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
-                         d.dim, d.attr_mode, de, da1b, w.p_w1);
+      st = launch_dw1_tr<256>(h, n1, E, w.pc1, w.da1E, sv + sl.xE, de, w.p_w1);
+    if (st != DSMP_OK) return st;
     DSMP_LAUNCHED(h, "dW1");
   }
 

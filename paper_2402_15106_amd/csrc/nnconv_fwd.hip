@@ -155,6 +155,21 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
     float x[NT][8];
 #pragma unroll
     for (int t = 0; t < NT; ++t) edge_attr(a.node_attr, a.dim, a.attr_mode, dnode[t], snode[t], x[t]);
+    if constexpr (sizeof(T) == 2) {
+      if (a.xE) {   // for the backward: bf16 high parts (lane half 0), then low parts (half 1)
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          if (valid[t]) {
+            float v[8];
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+              const float hi = (float)(__bf16)x[t][c];
+              v[c] = hh ? x[t][c] - hi : hi;
+            }
+            *reinterpret_cast<bf16x8*>(a.xE + (size_t)eid[t] * 32 + hh * 16) = pack_frag<__bf16>(v);
+          }
+      }
+    }
     stage_wait();
     __syncthreads();   // rows, W1 and W2 are in LDS
     frag z1B[NT][S::SK1];
@@ -662,6 +677,7 @@ SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E) {
   s.zE = (size_t)c.take<unsigned char>((size_t)E * d.h2 * esz);
   s.z1E = (size_t)c.take<unsigned char>((size_t)E * d.h1 * esz);
   s.zmask = (size_t)c.take<unsigned char>((size_t)E * (d.h1 + d.h2) / 8);
+  s.xE = (size_t)c.take<unsigned char>(d.dtype == DSMP_BF16 ? (size_t)E * 32 : 0);
   s.os = (size_t)c.take<unsigned char>((size_t)n_dst * agg_ktot(d) * esz + 256);   // + whole last staged piece
   s.total = c.used();
   return s;
@@ -762,6 +778,7 @@ extern "C" dsmp_status dsmp_nnconv_forward(dsmp_handle* h, const dsmp_layer_desc
   ea.gath = static_cast<const unsigned char*>(h_in);
   ea.packed = static_cast<const unsigned char*>(packed); ea.L = L;
   ea.zE = sv + sl.zE; ea.z1E = sv + sl.z1E; ea.zmask = sv + sl.zmask;
+  ea.xE = d.dtype == DSMP_BF16 ? sv + sl.xE : nullptr;
   ea.out_direct = direct; ea.out_part = part;
   if (agg) {
     // z and z1 per edge, the per-destination sums S (kept for the backward),
