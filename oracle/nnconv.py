@@ -239,9 +239,11 @@ def backward(P, x_e, h, row_ptr, col, n_dst: int, grad_out, act: int = ACT_IDENT
 
     If ``rows`` is given, grad_out must vanish outside those rows; only their
     edges are visited, and the result is still exact.
-    Returns a dict with grad_h [n_src, d] and dW1, db1, dW2, db2, dW3, db3,
-    dWr, dbr in the parameter layouts, plus "allow": elementwise bounds on
-    how far ambiguous a1/a2 ReLU decisions can move dW1, db1, dW2, db2.
+    Returns a dict with grad_h [n_src, d], dW1, db1, dW2, db2, dW3, db3,
+    dWr, dbr in the parameter layouts, grad_x [E, de] (the gradient with
+    respect to the edge attributes, W1^T da1 per edge, zero for edges not
+    visited), plus "allow": elementwise bounds on how far ambiguous a1/a2
+    ReLU decisions can move dW1, db1, dW2, db2 and grad_x.
     """
     P = _as64(P)
     h = np.asarray(h, dtype=np.float64)
@@ -265,6 +267,8 @@ def backward(P, x_e, h, row_ptr, col, n_dst: int, grad_out, act: int = ACT_IDENT
     out = {k: np.zeros_like(P[k]) for k in ("W1", "b1", "W2", "b2", "W3", "b3", "Wr", "br")}
     allow = {k: np.zeros_like(P[k]) for k in ("W1", "b1", "W2", "b2")}
     grad_h = np.zeros((n_src, d))
+    grad_x = np.zeros_like(x_e)
+    allow_x = np.zeros_like(x_e)
     # root, bias and residual terms (destinations are nodes [0, n_dst))
     out["Wr"] = ybar.T @ h[:n_dst]
     out["br"] = ybar.sum(0)
@@ -294,6 +298,7 @@ def backward(P, x_e, h, row_ptr, col, n_dst: int, grad_out, act: int = ACT_IDENT
         da1 = dz1 * m1
         out["W1"] += da1.T @ x
         out["b1"] += da1.sum(0)
+        grad_x[e] = da1 @ P["W1"]
         if amb1.any() or amb2.any():
             # an ambiguous a2 decision moves da2[e,k] by dz[e,k]; an ambiguous a1
             # decision moves da1[e,j] by dz1[e,j]
@@ -303,8 +308,10 @@ def backward(P, x_e, h, row_ptr, col, n_dst: int, grad_out, act: int = ACT_IDENT
             d1 = (d2 @ np.abs(P["W2"])) * m1 + np.abs(dz1) * amb1
             allow["W1"] += d1.T @ np.abs(x)
             allow["b1"] += d1.sum(0)
-    res = {"grad_h": grad_h}
+            allow_x[e] = d1 @ np.abs(P["W1"])
+    res = {"grad_h": grad_h, "grad_x": grad_x}
     for k in ("W1", "b1", "W2", "b2", "W3", "b3", "Wr", "br"):
         res["d" + k] = out[k]
     res["allow"] = {"d" + k: v for k, v in allow.items()}
+    res["allow"]["grad_x"] = allow_x
     return res

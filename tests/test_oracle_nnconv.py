@@ -162,9 +162,9 @@ def test_backward_central_differences(act, res):
     G = np.random.default_rng(2).normal(size=(nd, h.shape[1]))
     grads = nn.backward(P, x, h, rp, col, nd, G, act, res)
     eps = 1e-6
-    for key in ["h", "W1", "b1", "W2", "b2", "W3", "b3", "Wr", "br"]:
-        base = h if key == "h" else P[key]
-        gkey = "grad_h" if key == "h" else "d" + key
+    for key in ["h", "x", "W1", "b1", "W2", "b2", "W3", "b3", "Wr", "br"]:
+        base = {"h": h, "x": x}.get(key, P.get(key))
+        gkey = {"h": "grad_h", "x": "grad_x"}.get(key, "d" + key)
         flat = base.reshape(-1)
         idx = np.random.default_rng(7).choice(flat.size, size=min(flat.size, 12), replace=False)
         for t in idx:
@@ -229,7 +229,7 @@ def test_backward_matches_torch_autograd():
     for act in (nn.ACT_IDENTITY, nn.ACT_RELU):
         T = {k: torch.tensor(v, dtype=torch.float64, requires_grad=True) for k, v in P.items()}
         th = torch.tensor(h, dtype=torch.float64, requires_grad=True)
-        tx = torch.tensor(x, dtype=torch.float64)
+        tx = torch.tensor(x, dtype=torch.float64, requires_grad=True)
         dst = torch.tensor(rg.dst_of_edges(rp), dtype=torch.long)
         src = torch.tensor(col, dtype=torch.long)
         d = h.shape[1]
@@ -244,6 +244,7 @@ def test_backward_matches_torch_autograd():
         ref = nn.backward(P, x, h, rp, col, nd, G, act)
         assert np.allclose(out.detach().numpy(), nn.forward(P, x, h, rp, col, nd, act)[0], atol=1e-10)
         assert np.allclose(th.grad.numpy(), ref["grad_h"], atol=1e-9)
+        assert np.allclose(tx.grad.numpy(), ref["grad_x"], atol=1e-9)
         for k in T:
             assert np.allclose(T[k].grad.numpy(), ref["d" + k], atol=1e-9), k
 
