@@ -170,7 +170,11 @@ dsmp_status dsmp_radius_graph_build(dsmp_handle* h, const dsmp_graph_query* q, v
 enum { DSMP_F32 = 0, DSMP_BF16 = 1 };
 enum { DSMP_ACT_IDENTITY = 0, DSMP_ACT_RELU = 1 };
 enum { DSMP_ATTR_CONCAT = 0, DSMP_ATTR_DIFF = 1 };
-enum { DSMP_GRAD_ACCUMULATE = 1 };
+/* Backward flags: DSMP_GRAD_ACCUMULATE adds parameter gradients to the
+ * caller's arrays (parameters shared by several layers or hops);
+ * DSMP_GRAD_X_ACCUMULATE does the same for the input-side gradients that a
+ * call documents as optional (a layer's dattr, a perceptron's grad_x). */
+enum { DSMP_GRAD_ACCUMULATE = 1, DSMP_GRAD_X_ACCUMULATE = 2 };
 
 typedef struct dsmp_layer_desc {
   int32_t dim;        /* spatial dimension D */
@@ -189,9 +193,18 @@ typedef struct dsmp_layer_params {
   const float *W1, *b1, *W2, *b2, *W3, *b3, *Wr, *br;
 } dsmp_layer_params;
 
-/* Gradients, device float32, same layouts as the parameters. */
+/* Gradients, device float32, same layouts as the parameters.  dattr is
+ * optional (NULL: not computed): for DSMP_ATTR_DIFF layers, device float32
+ * [n_src, dim+1], the gradient with respect to the node attribute rows v
+ * through the edge attributes x_e = v_i - v_j (row i gains the sum of W1^T da1
+ * over its incoming edges, row j loses it over its outgoing ones; the step
+ * that carries a hop's decoder outputs into the next hop's edge attributes,
+ * eq. (iv) and Algorithm 1), overwritten, or added to when the backward's
+ * flags have DSMP_GRAD_X_ACCUMULATE; UNSUPPORTED for DSMP_ATTR_CONCAT
+ * layers. */
 typedef struct dsmp_layer_grads {
   float *dW1, *db1, *dW2, *db2, *dW3, *db3, *dWr, *dbr;
+  float* dattr;
 } dsmp_layer_grads;
 
 /* Bytes of the packed parameter buffer (the layouts the kernels read). */
@@ -233,6 +246,61 @@ dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_desc* desc, co
                                  const void* saved, size_t saved_bytes, const float* grad_out,
                                  float* grad_h, const dsmp_layer_grads* grads, int32_t flags,
                                  void* ws, size_t ws_bytes);
+
+/* ---------------------------------------------------- encoder and decoder
+ * The node-wise networks of the hop loop (eq. (i) encoder N_e, eq. (iii)
+ * decoder N_d; Algorithm 1, node encoding and decoding steps): a three-layer
+ * perceptron applied to every row,
+ *     y = W3 ReLU(W2 ReLU(W1 x + b1) + b2) + b3,
+ * float32 throughout, parameters in the [out, in] layout of a linear layer:
+ * W1 [d_hid, d_in], b1 [d_hid], W2 [d_hid, d_hid], b2 [d_hid],
+ * W3 [d_out, d_hid], b3 [d_out].  Widths 1..256 (d_hid a multiple of 4);
+ * others give UNSUPPORTED. */
+typedef struct dsmp_mlp_desc {
+  int32_t d_in, d_hid, d_out;
+} dsmp_mlp_desc;
+
+typedef struct dsmp_mlp_params {
+  const float *W1, *b1, *W2, *b2, *W3, *b3;
+} dsmp_mlp_params;
+
+typedef struct dsmp_mlp_grads {
+  float *dW1, *db1, *dW2, *db2, *dW3, *db3;
+} dsmp_mlp_grads;
+
+/* Byte sizes for n rows: saved (written by forward, read by backward) and
+ * the backward workspace. */
+dsmp_status dsmp_mlp_workspace(const dsmp_mlp_desc* desc, int64_t n, size_t* saved_bytes,
+                               size_t* bwd_ws_bytes);
+
+/* Forward on n rows.  x: device float32 [n, d_in]; y: device float32
+ * [n, d_out], overwritten; y_bf16: NULL or device bfloat16 [n, d_out] (y
+ * rounded to nearest-even, e.g. the feature input of a bf16 layer); saved:
+ * device, dsmp_mlp_workspace long. */
+dsmp_status dsmp_mlp_forward(dsmp_handle* h, const dsmp_mlp_desc* desc, const dsmp_mlp_params* p,
+                             const float* x, int64_t n, float* y, void* y_bf16, void* saved,
+                             size_t saved_bytes);
+
+/* Backward of the forward that filled `saved`: gradients of sum(grad_y * y).
+ * grad_x: NULL or device float32 [n, d_in], overwritten, or added to when
+ * flags has DSMP_GRAD_X_ACCUMULATE.  Parameter gradients (every pointer
+ * non-NULL) are overwritten, or added to with DSMP_GRAD_ACCUMULATE (one
+ * network applied at several hops). */
+dsmp_status dsmp_mlp_backward(dsmp_handle* h, const dsmp_mlp_desc* desc, const dsmp_mlp_params* p,
+                              const float* x, int64_t n, const void* saved, size_t saved_bytes,
+                              const float* grad_y, float* grad_x, const dsmp_mlp_grads* grads,
+                              int32_t flags, void* ws, size_t ws_bytes);
+
+/* ------------------------------------------------------------ loss
+ * Mean squared error on the interior points (Algorithm 1, local loss): the
+ * mean of (pred - target)^2 over the rows with mask[i] != 0 and all c
+ * components.  pred, target: device float32 [n, c]; mask: device uint8 [n];
+ * loss: device float32 scalar, overwritten (0 when no row is interior);
+ * grad: NULL or device float32 [n, c], overwritten with d loss / d pred
+ * (zero on the other rows).  The sums run in a fixed order. */
+dsmp_status dsmp_masked_mse_workspace(int64_t n, size_t* bytes);
+dsmp_status dsmp_masked_mse(dsmp_handle* h, const float* pred, const float* target, const uint8_t* mask,
+                            int64_t n, int32_t c, float* loss, float* grad, void* ws, size_t ws_bytes);
 
 /* How the layer evaluates the edge contraction.  DSMP_EDGE_PER_EDGE forms
  * each message m_e on MFMA (edge tiles against streamed W3 chunks) and sums
@@ -277,7 +345,10 @@ enum {
   DSMP_K_OUTER_DH = 16, /* per-source sums T_j (aggregate form) */
   DSMP_K_GEMM_DH = 17,  /* W3 GEMM over T (aggregate form) */
   DSMP_K_U_GEMM = 18,   /* U = g W3 GEMM of the aggregate dz */
-  DSMP_K_COUNT = 19
+  DSMP_K_ATTR = 19,     /* edge-attribute gradient of a layer (dattr) */
+  DSMP_K_MLP = 20,      /* encoder / decoder perceptrons, forward and backward */
+  DSMP_K_LOSS = 21,     /* masked mean squared error */
+  DSMP_K_COUNT = 22
 };
 dsmp_status dsmp_profile_enable(dsmp_handle* h, int enable);
 dsmp_status dsmp_profile_reset(dsmp_handle* h);

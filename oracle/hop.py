@@ -111,7 +111,10 @@ def train_step(Pe, Pk, Pd, v0, Y, mask, row_ptr, col, n_hops: int, dtype: str = 
     (row_ptr, col) joins the n nodes (every node is a destination).
     Returns a dict: loss, v (final decoder output), vL (final latent), the
     gradients "enc", "conv", "dec" (dicts keyed like the parameters with a
-    leading "d"), and "margin" (the smallest relative ReLU margin met).
+    leading "d"), "conv_allow" (per convolution gradient, the sum over the
+    hops of the layer backward's bound on how far its ambiguous ReLU
+    decisions can move it), "margin" (the smallest relative ReLU margin met)
+    and "mlp_margin" (the same over the encoder and decoder only).
     """
     v0 = np.asarray(v0, dtype=np.float64)
     n = v0.shape[0]
@@ -120,7 +123,8 @@ def train_step(Pe, Pk, Pd, v0, Y, mask, row_ptr, col, n_hops: int, dtype: str = 
     decide = "bf16" if dtype == "bf16" else "f32"
     # forward
     vL, enc_cache = mlp3_forward(Pe, v0)
-    margin = enc_cache["margin"]
+    mlp_margin = enc_cache["margin"]
+    margin = mlp_margin
     v = v0
     hops = []
     for _ in range(n_hops):
@@ -130,6 +134,7 @@ def train_step(Pe, Pk, Pd, v0, Y, mask, row_ptr, col, n_hops: int, dtype: str = 
         margin = min(margin, _conv_margin(Pk, x, dtype))
         v_new, dec_cache = mlp3_forward(Pd, out)
         margin = min(margin, dec_cache["margin"])
+        mlp_margin = min(mlp_margin, dec_cache["margin"])
         hops.append({"x": x, "h_in": h_in, "out": out, "dec": dec_cache})
         vL, v = out, v_new
     loss, gv = masked_mse(v, Y, mask)
@@ -138,6 +143,7 @@ def train_step(Pe, Pk, Pd, v0, Y, mask, row_ptr, col, n_hops: int, dtype: str = 
     # next hop's latent input
     g_conv = {"d" + k: np.zeros_like(np.asarray(Pk[k], dtype=np.float64))
               for k in ("W1", "b1", "W2", "b2", "W3", "b3", "Wr", "br")}
+    conv_allow = {k: np.zeros_like(v) for k, v in g_conv.items()}
     g_dec = None
     g_lat = np.zeros_like(hops[-1]["out"]) if hops else None
     dst = np.repeat(np.arange(n), np.diff(row_ptr))
@@ -148,12 +154,15 @@ def train_step(Pe, Pk, Pd, v0, Y, mask, row_ptr, col, n_hops: int, dtype: str = 
         gc = nnconv.backward(Pk, hp["x"], hp["h_in"], row_ptr, col, n, g_out + g_lat, decide=decide)
         for k in g_conv:
             g_conv[k] += gc[k]
+            if k in gc["allow"]:
+                conv_allow[k] += gc["allow"][k]
         g_lat = gc["grad_h"]                 # with respect to the latent input vL^l
         gv = np.zeros_like(v0)               # with respect to v^l, through x^l = v_i - v_j
         np.add.at(gv, dst, gc["grad_x"])
         np.add.at(gv, col, -gc["grad_x"])
     _, g_enc = mlp3_backward(Pe, enc_cache, g_lat if n_hops else np.zeros_like(vL))
-    return {"loss": loss, "v": v, "vL": vL, "enc": g_enc, "conv": g_conv, "dec": g_dec, "margin": margin}
+    return {"loss": loss, "v": v, "vL": vL, "enc": g_enc, "conv": g_conv, "dec": g_dec, "conv_allow": conv_allow,
+            "margin": margin, "mlp_margin": mlp_margin}
 
 
 def _conv_margin(Pk, x, dtype):

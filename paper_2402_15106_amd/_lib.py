@@ -26,6 +26,7 @@ F32, BF16 = 0, 1
 ACT_IDENTITY, ACT_RELU = 0, 1
 ATTR_CONCAT, ATTR_DIFF = 0, 1
 GRAD_ACCUMULATE = 1
+GRAD_X_ACCUMULATE = 2
 EDGE_AUTO, EDGE_PER_EDGE, EDGE_AGGREGATE = 0, 1, 2
 
 EXPORTED = ["dsmp_version", "dsmp_create", "dsmp_destroy", "dsmp_set_stream", "dsmp_last_error",
@@ -33,12 +34,13 @@ EXPORTED = ["dsmp_version", "dsmp_create", "dsmp_destroy", "dsmp_set_stream", "d
             "dsmp_radius_graph_workspace", "dsmp_radius_graph_count", "dsmp_radius_graph_build",
             "dsmp_nnconv_packed_bytes", "dsmp_nnconv_pack", "dsmp_nnconv_workspace",
             "dsmp_nnconv_forward", "dsmp_nnconv_backward", "dsmp_profile_enable", "dsmp_profile_reset",
-            "dsmp_profile_read", "dsmp_set_edge_algorithm"]
+            "dsmp_profile_read", "dsmp_set_edge_algorithm", "dsmp_mlp_workspace", "dsmp_mlp_forward",
+            "dsmp_mlp_backward", "dsmp_masked_mse_workspace", "dsmp_masked_mse"]
 
 # kernel classes of the opt-in timing (dsmp_profile_*)
 KERNEL_CLASSES = ["sample", "gather", "graph", "edge_fwd", "node_fwd", "node_bwd", "edge_dh", "dh_final",
                   "dz", "dW3", "dW2", "dW1", "reduce", "edge_mlp", "outer_fwd", "gemm_fwd", "outer_dh",
-                  "gemm_dh", "u_gemm"]
+                  "gemm_dh", "u_gemm", "attr", "mlp", "loss"]
 
 
 class DsmpError(RuntimeError):
@@ -70,7 +72,19 @@ class LayerParams(ctypes.Structure):
 
 
 class LayerGrads(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in ("dW1", "db1", "dW2", "db2", "dW3", "db3", "dWr", "dbr")]
+    _fields_ = [(n, ctypes.c_void_p) for n in ("dW1", "db1", "dW2", "db2", "dW3", "db3", "dWr", "dbr", "dattr")]
+
+
+class MlpDesc(ctypes.Structure):
+    _fields_ = [("d_in", ctypes.c_int32), ("d_hid", ctypes.c_int32), ("d_out", ctypes.c_int32)]
+
+
+class MlpParams(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("W1", "b1", "W2", "b2", "W3", "b3")]
+
+
+class MlpGrads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("dW1", "db1", "dW2", "db2", "dW3", "db3")]
 
 
 _P = ctypes.c_void_p
@@ -100,6 +114,15 @@ _SIG = {
     "dsmp_nnconv_backward": (ctypes.c_int, [_P, ctypes.POINTER(LayerDesc), _P, ctypes.POINTER(CGraph), _P, _P,
                                             _P, ctypes.c_size_t, _P, _P, ctypes.POINTER(LayerGrads),
                                             ctypes.c_int32, _P, ctypes.c_size_t]),
+    "dsmp_mlp_workspace": (ctypes.c_int, [ctypes.POINTER(MlpDesc), ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t),
+                                          ctypes.POINTER(ctypes.c_size_t)]),
+    "dsmp_mlp_forward": (ctypes.c_int, [_P, ctypes.POINTER(MlpDesc), ctypes.POINTER(MlpParams), _P, ctypes.c_int64,
+                                        _P, _P, _P, ctypes.c_size_t]),
+    "dsmp_mlp_backward": (ctypes.c_int, [_P, ctypes.POINTER(MlpDesc), ctypes.POINTER(MlpParams), _P, ctypes.c_int64,
+                                         _P, ctypes.c_size_t, _P, _P, ctypes.POINTER(MlpGrads), ctypes.c_int32, _P,
+                                         ctypes.c_size_t]),
+    "dsmp_masked_mse_workspace": (ctypes.c_int, [ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]),
+    "dsmp_masked_mse": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P, _P, ctypes.c_size_t]),
     "dsmp_profile_enable": (ctypes.c_int, [_P, ctypes.c_int]),
     "dsmp_profile_reset": (ctypes.c_int, [_P]),
     "dsmp_profile_read": (ctypes.c_int, [_P, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
@@ -327,7 +350,8 @@ class Dsmp:
                      "dW2": torch.empty(h2, h1, **f32), "db2": torch.empty(h2, **f32),
                      "dW3": torch.empty(d * d, h2, **f32), "db3": torch.empty(d * d, **f32),
                      "dWr": torch.empty(d, d, **f32), "dbr": torch.empty(d, **f32)}
-        lg = LayerGrads(*[grads[k].data_ptr() for k in ("dW1", "db1", "dW2", "db2", "dW3", "db3", "dWr", "dbr")])
+        lg = LayerGrads(*[grads[k].data_ptr() for k in ("dW1", "db1", "dW2", "db2", "dW3", "db3", "dWr", "dbr")],
+                        grads["dattr"].data_ptr() if grads.get("dattr") is not None else None)
         if ws is None:
             ws = self.workspace("bwd", bb)
         cg = g.c()
@@ -337,3 +361,56 @@ class Dsmp:
                                                   _ptr(grad_out), _ptr(grad_h), ctypes.byref(lg), flags,
                                                   _ptr(ws), ws.numel()), self.h)
         return grad_h, grads
+
+    # ------------------------------------------------------------ encoder / decoder and loss
+    def dsmp_mlp_workspace(self, desc: "MlpDesc", n: int):
+        sb, wb = ctypes.c_size_t(), ctypes.c_size_t()
+        self._check(self.lib.dsmp_mlp_workspace(ctypes.byref(desc), n, ctypes.byref(sb), ctypes.byref(wb)), None)
+        return sb.value, wb.value
+
+    def dsmp_mlp_forward(self, desc: "MlpDesc", params: dict, x, y=None, y_bf16=None, saved=None):
+        """Three-layer perceptron on the rows of x (float32 [n, d_in]); returns (y, saved)."""
+        n = x.shape[0]
+        sb, _ = self.dsmp_mlp_workspace(desc, n)
+        if y is None:
+            y = torch.empty(n, desc.d_out, dtype=torch.float32, device=self.device)
+        if saved is None:
+            saved = torch.empty(max(sb, 256), dtype=torch.uint8, device=self.device)
+        mp = MlpParams(*[params[k].data_ptr() for k in ("W1", "b1", "W2", "b2", "W3", "b3")])
+        self._bind()
+        self._check(self.lib.dsmp_mlp_forward(self.h, ctypes.byref(desc), ctypes.byref(mp), _ptr(x), n, _ptr(y),
+                                              _ptr(y_bf16), _ptr(saved), saved.numel()), self.h)
+        return y, saved
+
+    def dsmp_mlp_backward(self, desc: "MlpDesc", params: dict, x, saved, grad_y, grad_x=None,
+                          grads: Optional[dict] = None, flags: int = 0, ws=None):
+        """Gradients of sum(grad_y * y); grad_x optional (None: not computed).  Returns grads."""
+        n = x.shape[0]
+        _, wb = self.dsmp_mlp_workspace(desc, n)
+        f32 = dict(dtype=torch.float32, device=self.device)
+        if grads is None:
+            grads = {"dW1": torch.empty(desc.d_hid, desc.d_in, **f32), "db1": torch.empty(desc.d_hid, **f32),
+                     "dW2": torch.empty(desc.d_hid, desc.d_hid, **f32), "db2": torch.empty(desc.d_hid, **f32),
+                     "dW3": torch.empty(desc.d_out, desc.d_hid, **f32), "db3": torch.empty(desc.d_out, **f32)}
+        mp = MlpParams(*[params[k].data_ptr() for k in ("W1", "b1", "W2", "b2", "W3", "b3")])
+        mg = MlpGrads(*[grads[k].data_ptr() for k in ("dW1", "db1", "dW2", "db2", "dW3", "db3")])
+        if ws is None:
+            ws = self.workspace("mlp_bwd", wb)
+        self._bind()
+        self._check(self.lib.dsmp_mlp_backward(self.h, ctypes.byref(desc), ctypes.byref(mp), _ptr(x), n, _ptr(saved),
+                                               saved.numel(), _ptr(grad_y), _ptr(grad_x), ctypes.byref(mg), flags,
+                                               _ptr(ws), ws.numel()), self.h)
+        return grads
+
+    def dsmp_masked_mse(self, pred, target, mask, loss=None, grad=None):
+        """Mean squared error over interior rows (mask uint8 [n]); returns (loss [1] device, grad)."""
+        n, c = pred.shape
+        nb = ctypes.c_size_t()
+        self._check(self.lib.dsmp_masked_mse_workspace(n, ctypes.byref(nb)), None)
+        ws = self.workspace("mse", nb.value)
+        if loss is None:
+            loss = torch.empty(1, dtype=torch.float32, device=self.device)
+        self._bind()
+        self._check(self.lib.dsmp_masked_mse(self.h, _ptr(pred), _ptr(target), _ptr(mask), n, c, _ptr(loss),
+                                             _ptr(grad), _ptr(ws), ws.numel()), self.h)
+        return loss, grad

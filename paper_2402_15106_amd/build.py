@@ -17,7 +17,7 @@ OUT_DIR = os.path.join(HERE, "lib")
 LIB = os.path.join(OUT_DIR, "libdsmpnn.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 
-SOURCES = ["core.hip", "graph.hip", "nnconv_fwd.hip", "nnconv_bwd.hip", "nnconv_agg.hip"]
+SOURCES = ["core.hip", "graph.hip", "nnconv_fwd.hip", "nnconv_bwd.hip", "nnconv_agg.hip", "hop.hip"]
 COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 PER_FILE = {"graph.hip": ["-ffp-contract=off"]}

@@ -1,0 +1,301 @@
+// Node-wise networks and loss of the hop loop (Algorithm 1): the encoder and
+// decoder perceptrons of eqs. (i) and (iii), forward and backward, and the
+// masked mean squared error on the interior points.  Everything is float32
+// with sums in a fixed order (block partials reduced in block order), so the
+// results are bitwise reproducible.
+#include <algorithm>
+
+#include "common.hpp"
+
+using namespace dsmp;
+
+namespace {
+
+constexpr int ROWS_PER_PART = 256;   // rows per partial of a weight-gradient sum
+
+// out[n][o] = act(b[o] + sum_i in[n][i] W[o][i]), the sum as a chain of fused
+// multiply-adds in input order; optional bf16 copy of the output.
+__global__ __launch_bounds__(256) void k_dense(int64_t n, int din, int dout, const float* __restrict__ in,
+                                               const float* __restrict__ W, const float* __restrict__ b, int relu,
+                                               float* __restrict__ out, __bf16* __restrict__ out_bf16) {
+  const int64_t total = n * dout;
+  for (int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x; x < total; x += (int64_t)gridDim.x * 256) {
+    const int64_t r = x / dout;
+    const int o = (int)(x % dout);
+    const float* xi = in + r * din;
+    const float* wo = W + (int64_t)o * din;
+    float v = b[o];
+    for (int i = 0; i < din; ++i) v = __builtin_fmaf(xi[i], wo[i], v);
+    if (relu && !(v > 0.0f)) v = 0.0f;
+    out[x] = v;
+    if (out_bf16) out_bf16[x] = (__bf16)v;
+  }
+}
+
+// gin[n][i] (+)= [h[n][i] > 0] * sum_o g[n][o] W[o][i]   (mask h optional)
+__global__ __launch_bounds__(256) void k_dense_back(int64_t n, int din, int dout, const float* __restrict__ g,
+                                                    const float* __restrict__ W, const float* __restrict__ h,
+                                                    float* __restrict__ gin, int accumulate) {
+  const int64_t total = n * din;
+  for (int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x; x < total; x += (int64_t)gridDim.x * 256) {
+    const int64_t r = x / din;
+    const int i = (int)(x % din);
+    const float* gr = g + r * dout;
+    float v = 0.0f;
+    for (int o = 0; o < dout; ++o) v = __builtin_fmaf(gr[o], W[(int64_t)o * din + i], v);
+    if (h && !(h[x] > 0.0f)) v = 0.0f;
+    gin[x] = accumulate ? gin[x] + v : v;
+  }
+}
+
+// part[c][o][i] = sum over rows r of part c of g[r][o] * in[r][i] for i < din,
+// and part[c][o][din] = sum of g[r][o] (the bias gradient), rows in order.
+__global__ __launch_bounds__(256) void k_outer_rows(int64_t n, int din, int dout, const float* __restrict__ g,
+                                                    const float* __restrict__ in, float* __restrict__ part) {
+  const int64_t r0 = (int64_t)blockIdx.x * ROWS_PER_PART;
+  const int64_t r1 = std::min<int64_t>(r0 + ROWS_PER_PART, n);
+  const int pairs = dout * (din + 1);
+  float* out = part + (int64_t)blockIdx.x * pairs;
+  for (int p = threadIdx.x; p < pairs; p += 256) {
+    const int o = p / (din + 1), i = p % (din + 1);
+    float v = 0.0f;
+    if (i < din)
+      for (int64_t r = r0; r < r1; ++r) v = __builtin_fmaf(g[r * dout + o], in[r * din + i], v);
+    else
+      for (int64_t r = r0; r < r1; ++r) v += g[r * dout + o];
+    out[p] = v;
+  }
+}
+
+// dW[o][i] (+)= sum_c part[c][o][i], db[o] (+)= sum_c part[c][o][din], c in order.
+__global__ __launch_bounds__(256) void k_outer_final(int nparts, int din, int dout, const float* __restrict__ part,
+                                                     float* __restrict__ dW, float* __restrict__ db, int accumulate) {
+  const int pairs = dout * (din + 1);
+  const int p = blockIdx.x * 256 + threadIdx.x;
+  if (p >= pairs) return;
+  float v = 0.0f;
+  for (int c = 0; c < nparts; ++c) v += part[(int64_t)c * pairs + p];
+  const int o = p / (din + 1), i = p % (din + 1);
+  float* t = i < din ? dW + (int64_t)o * din + i : db + o;
+  *t = accumulate ? *t + v : v;
+}
+
+// Masked MSE: per-block partial sums (squared error, interior rows), a
+// single-block final sum, then the gradient.
+__global__ __launch_bounds__(256) void k_mse_partial(int64_t n, int c, const float* __restrict__ pred,
+                                                     const float* __restrict__ target,
+                                                     const uint8_t* __restrict__ mask, float2* __restrict__ part) {
+  __shared__ float ss[256], sk[256];
+  const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  float s = 0.0f, k = 0.0f;
+  if (r < n && mask[r]) {
+    for (int j = 0; j < c; ++j) {
+      const float dlt = pred[r * c + j] - target[r * c + j];
+      s = __builtin_fmaf(dlt, dlt, s);
+    }
+    k = 1.0f;
+  }
+  ss[threadIdx.x] = s;
+  sk[threadIdx.x] = k;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+      ss[threadIdx.x] += ss[threadIdx.x + w];
+      sk[threadIdx.x] += sk[threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) part[blockIdx.x] = make_float2(ss[0], sk[0]);
+}
+
+__global__ __launch_bounds__(256) void k_mse_final(int nparts, int c, const float2* __restrict__ part,
+                                                   float* __restrict__ loss, float* __restrict__ scale) {
+  __shared__ double ss[256], sk[256];
+  double s = 0.0, k = 0.0;
+  for (int p = threadIdx.x; p < nparts; p += 256) {
+    s += part[p].x;
+    k += part[p].y;
+  }
+  ss[threadIdx.x] = s;
+  sk[threadIdx.x] = k;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+      ss[threadIdx.x] += ss[threadIdx.x + w];
+      sk[threadIdx.x] += sk[threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double cnt = sk[0] * c;
+    *loss = cnt > 0 ? (float)(ss[0] / cnt) : 0.0f;
+    *scale = cnt > 0 ? (float)(2.0 / cnt) : 0.0f;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_mse_grad(int64_t n, int c, const float* __restrict__ pred,
+                                                  const float* __restrict__ target, const uint8_t* __restrict__ mask,
+                                                  const float* __restrict__ scale, float* __restrict__ grad) {
+  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (x >= n * c) return;
+  grad[x] = mask[x / c] ? (pred[x] - target[x]) * *scale : 0.0f;
+}
+
+struct MlpSaved {
+  float *h1, *h2;
+  size_t total;
+};
+
+MlpSaved mlp_saved(const dsmp_mlp_desc& d, int64_t n, void* base) {
+  Carve c(base);
+  MlpSaved s;
+  s.h1 = c.take<float>((size_t)n * d.d_hid);
+  s.h2 = c.take<float>((size_t)n * d.d_hid);
+  s.total = c.used();
+  return s;
+}
+
+struct MlpWs {
+  float *g2, *g1, *p3, *p2, *p1;
+  int nparts;
+  size_t total;
+};
+
+MlpWs mlp_ws(const dsmp_mlp_desc& d, int64_t n, void* base) {
+  Carve c(base);
+  MlpWs w;
+  w.nparts = (int)std::max<int64_t>(1, ceil_div(n, ROWS_PER_PART));
+  w.g2 = c.take<float>((size_t)n * d.d_hid);
+  w.g1 = c.take<float>((size_t)n * d.d_hid);
+  w.p3 = c.take<float>((size_t)w.nparts * d.d_out * (d.d_hid + 1));
+  w.p2 = c.take<float>((size_t)w.nparts * d.d_hid * (d.d_hid + 1));
+  w.p1 = c.take<float>((size_t)w.nparts * d.d_hid * (d.d_in + 1));
+  w.total = c.used();
+  return w;
+}
+
+dsmp_status check_mlp(dsmp_handle* h, const dsmp_mlp_desc* d) {
+  DSMP_CHECK(h, d, DSMP_INVALID_ARG, "desc is NULL");
+  DSMP_CHECK(h, d->d_in >= 1 && d->d_in <= 256 && d->d_out >= 1 && d->d_out <= 256 && d->d_hid >= 4 &&
+                    d->d_hid <= 256 && d->d_hid % 4 == 0,
+             DSMP_UNSUPPORTED, "unsupported perceptron widths %d -> %d -> %d", d->d_in, d->d_hid, d->d_out);
+  return DSMP_OK;
+}
+
+unsigned grid_for(int64_t total) { return (unsigned)std::min<int64_t>(ceil_div(total, 256), 65536); }
+
+}  // namespace
+
+extern "C" dsmp_status dsmp_mlp_workspace(const dsmp_mlp_desc* desc, int64_t n, size_t* saved_bytes,
+                                          size_t* bwd_ws_bytes) {
+  if (!desc || !saved_bytes || !bwd_ws_bytes || n < 0) return DSMP_INVALID_ARG;
+  if (check_mlp(nullptr, desc) != DSMP_OK) return DSMP_UNSUPPORTED;
+  *saved_bytes = mlp_saved(*desc, n, nullptr).total;
+  *bwd_ws_bytes = mlp_ws(*desc, n, nullptr).total;
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_mlp_forward(dsmp_handle* h, const dsmp_mlp_desc* desc, const dsmp_mlp_params* p,
+                                        const float* x, int64_t n, float* y, void* y_bf16, void* saved,
+                                        size_t saved_bytes) {
+  if (!h) return DSMP_INVALID_ARG;
+  dsmp_status st = check_mlp(h, desc);
+  if (st != DSMP_OK) return st;
+  const dsmp_mlp_desc& d = *desc;
+  DSMP_CHECK(h, n >= 0 && n < (int64_t)1 << 31, DSMP_INVALID_ARG, "row count out of range");
+  DSMP_CHECK(h, p && p->W1 && p->b1 && p->W2 && p->b2 && p->W3 && p->b3, DSMP_INVALID_ARG, "a parameter is NULL");
+  DSMP_CHECK(h, n == 0 || (x && y && saved), DSMP_INVALID_ARG, "a data pointer is NULL");
+  const MlpSaved s = mlp_saved(d, n, saved);
+  DSMP_CHECK(h, saved_bytes >= s.total, DSMP_WORKSPACE_TOO_SMALL, "saved buffer needs %zu bytes", s.total);
+  if (n == 0) return DSMP_OK;
+  ProfScope prof(h, DSMP_K_MLP);
+  hipStream_t st_ = h->stream;
+  hipLaunchKernelGGL(k_dense, dim3(grid_for(n * d.d_hid)), dim3(256), 0, st_, n, d.d_in, d.d_hid, x, p->W1, p->b1, 1,
+                     s.h1, (__bf16*)nullptr);
+  hipLaunchKernelGGL(k_dense, dim3(grid_for(n * d.d_hid)), dim3(256), 0, st_, n, d.d_hid, d.d_hid, s.h1, p->W2, p->b2,
+                     1, s.h2, (__bf16*)nullptr);
+  hipLaunchKernelGGL(k_dense, dim3(grid_for(n * d.d_out)), dim3(256), 0, st_, n, d.d_hid, d.d_out, s.h2, p->W3, p->b3,
+                     0, y, static_cast<__bf16*>(y_bf16));
+  DSMP_LAUNCHED(h, "perceptron forward");
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_mlp_backward(dsmp_handle* h, const dsmp_mlp_desc* desc, const dsmp_mlp_params* p,
+                                         const float* x, int64_t n, const void* saved, size_t saved_bytes,
+                                         const float* grad_y, float* grad_x, const dsmp_mlp_grads* grads,
+                                         int32_t flags, void* ws, size_t ws_bytes) {
+  if (!h) return DSMP_INVALID_ARG;
+  dsmp_status st = check_mlp(h, desc);
+  if (st != DSMP_OK) return st;
+  const dsmp_mlp_desc& d = *desc;
+  DSMP_CHECK(h, n >= 0 && n < (int64_t)1 << 31, DSMP_INVALID_ARG, "row count out of range");
+  DSMP_CHECK(h, p && p->W1 && p->b1 && p->W2 && p->b2 && p->W3 && p->b3, DSMP_INVALID_ARG, "a parameter is NULL");
+  DSMP_CHECK(h, grads && grads->dW1 && grads->db1 && grads->dW2 && grads->db2 && grads->dW3 && grads->db3,
+             DSMP_INVALID_ARG, "a gradient pointer is NULL");
+  DSMP_CHECK(h, n == 0 || (x && saved && grad_y), DSMP_INVALID_ARG, "a data pointer is NULL");
+  DSMP_CHECK(h, (flags & ~(DSMP_GRAD_ACCUMULATE | DSMP_GRAD_X_ACCUMULATE)) == 0, DSMP_INVALID_ARG, "unknown flags");
+  const MlpSaved s = mlp_saved(d, n, const_cast<void*>(saved));
+  DSMP_CHECK(h, saved_bytes >= s.total, DSMP_WORKSPACE_TOO_SMALL, "saved buffer needs %zu bytes", s.total);
+  const MlpWs need = mlp_ws(d, n, nullptr);
+  DSMP_CHECK(h, ws && ws_bytes >= need.total, DSMP_WORKSPACE_TOO_SMALL, "backward workspace needs %zu bytes",
+             need.total);
+  const MlpWs w = mlp_ws(d, n, ws);
+  const int acc = flags & DSMP_GRAD_ACCUMULATE;
+  ProfScope prof(h, DSMP_K_MLP);
+  hipStream_t q = h->stream;
+  const int np = n > 0 ? w.nparts : 0;
+  if (n > 0) {
+    // layer 3 (no activation): weights from grad_y and h2, then back to h2's pre-activation
+    hipLaunchKernelGGL(k_outer_rows, dim3(np), dim3(256), 0, q, n, d.d_hid, d.d_out, grad_y, s.h2, w.p3);
+    hipLaunchKernelGGL(k_dense_back, dim3(grid_for(n * d.d_hid)), dim3(256), 0, q, n, d.d_hid, d.d_out, grad_y, p->W3,
+                       s.h2, w.g2, 0);
+    hipLaunchKernelGGL(k_outer_rows, dim3(np), dim3(256), 0, q, n, d.d_hid, d.d_hid, w.g2, s.h1, w.p2);
+    hipLaunchKernelGGL(k_dense_back, dim3(grid_for(n * d.d_hid)), dim3(256), 0, q, n, d.d_hid, d.d_hid, w.g2, p->W2,
+                       s.h1, w.g1, 0);
+    hipLaunchKernelGGL(k_outer_rows, dim3(np), dim3(256), 0, q, n, d.d_in, d.d_hid, w.g1, x, w.p1);
+    if (grad_x)
+      hipLaunchKernelGGL(k_dense_back, dim3(grid_for(n * d.d_in)), dim3(256), 0, q, n, d.d_in, d.d_hid, w.g1, p->W1,
+                         (const float*)nullptr, grad_x, (flags & DSMP_GRAD_X_ACCUMULATE) ? 1 : 0);
+  }
+  // with no rows the partial count is 0 and the finals write zeros (or add nothing)
+  hipLaunchKernelGGL(k_outer_final, dim3(ceil_div(d.d_out * (d.d_hid + 1), 256)), dim3(256), 0, q, np, d.d_hid,
+                     d.d_out, w.p3, grads->dW3, grads->db3, acc);
+  hipLaunchKernelGGL(k_outer_final, dim3(ceil_div(d.d_hid * (d.d_hid + 1), 256)), dim3(256), 0, q, np, d.d_hid,
+                     d.d_hid, w.p2, grads->dW2, grads->db2, acc);
+  hipLaunchKernelGGL(k_outer_final, dim3(ceil_div(d.d_hid * (d.d_in + 1), 256)), dim3(256), 0, q, np, d.d_in,
+                     d.d_hid, w.p1, grads->dW1, grads->db1, acc);
+  DSMP_LAUNCHED(h, "perceptron backward");
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_masked_mse_workspace(int64_t n, size_t* bytes) {
+  if (!bytes || n < 0) return DSMP_INVALID_ARG;
+  Carve c(nullptr);
+  c.take<float2>((size_t)std::max<int64_t>(1, ceil_div(n, 256)));
+  c.take<float>(1);
+  *bytes = c.used();
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_masked_mse(dsmp_handle* h, const float* pred, const float* target, const uint8_t* mask,
+                                       int64_t n, int32_t c, float* loss, float* grad, void* ws, size_t ws_bytes) {
+  if (!h) return DSMP_INVALID_ARG;
+  DSMP_CHECK(h, n >= 0 && n < (int64_t)1 << 31 && c >= 1 && c <= 1024, DSMP_INVALID_ARG, "sizes out of range");
+  DSMP_CHECK(h, loss && (n == 0 || (pred && target && mask)), DSMP_INVALID_ARG, "a pointer is NULL");
+  size_t need = 0;
+  dsmp_masked_mse_workspace(n, &need);
+  DSMP_CHECK(h, ws && ws_bytes >= need, DSMP_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes", need);
+  Carve cv(ws);
+  const int nparts = (int)(n > 0 ? ceil_div(n, 256) : 0);
+  float2* part = cv.take<float2>((size_t)std::max(nparts, 1));
+  float* scale = cv.take<float>(1);
+  ProfScope prof(h, DSMP_K_LOSS);
+  if (nparts > 0)
+    hipLaunchKernelGGL(k_mse_partial, dim3(nparts), dim3(256), 0, h->stream, n, (int)c, pred, target, mask, part);
+  hipLaunchKernelGGL(k_mse_final, dim3(1), dim3(256), 0, h->stream, nparts, (int)c, part, loss, scale);
+  if (grad && n > 0)
+    hipLaunchKernelGGL(k_mse_grad, dim3(ceil_div(n * c, 256)), dim3(256), 0, h->stream, n, (int)c, pred, target,
+                       mask, scale, grad);
+  DSMP_LAUNCHED(h, "masked mean squared error");
+  return DSMP_OK;
+}

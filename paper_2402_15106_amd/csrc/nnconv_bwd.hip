@@ -1122,6 +1122,73 @@ __global__ __launch_bounds__(256) void k_bwd_dW1_tr(int64_t E, int64_t per_chunk
   if (tid < H1) out[H1 * de + kperm<__bf16>(tid)] = bsum;
 }
 
+// ------------------------------------------------------------ attribute gradient
+
+// Diff-mode edge attributes x_e = v_i - v_j: dL/dx_e = W1^T da1_e.  Sixteen
+// lanes per edge, each over H1/16 consecutive stored positions of the edge's
+// da1 row; W1 in the packed lane order (stored position kk is lane-order
+// entry ((kk % KS) / EPL) * H1/2 + (kk / KS) * EPL + kk % EPL), in LDS.
+template <typename T, int H1>
+__global__ __launch_bounds__(256) void k_attr_dx(int64_t E, const unsigned char* __restrict__ da1E,
+                                                 const float* __restrict__ w1l, float4* __restrict__ dx) {
+  constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL, PER = H1 / 16;
+  __shared__ float w1s[H1 * 8];
+  for (int x = threadIdx.x; x < H1 * 8; x += 256) w1s[x] = w1l[x];
+  __syncthreads();
+  const int g = threadIdx.x & 15;
+  // the 16 lanes of an edge are active together, so the shuffles stay within live lanes
+  for (int64_t e = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 4; e < E; e += (int64_t)gridDim.x * 16) {
+    const T* row = reinterpret_cast<const T*>(da1E) + e * H1 + g * PER;
+    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int t = 0; t < PER; ++t) {
+      const int kk = g * PER + t;
+      const int hn = ((kk % KS) / EPL) * (H1 / 2) + (kk / KS) * EPL + kk % EPL;
+      const float v = to_f(row[t]);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[c] = __builtin_fmaf(w1s[hn * 8 + c], v, acc[c]);
+    }
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[c] += __shfl_xor(acc[c], o, 16);
+    if (g == 0) dx[e] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  }
+}
+
+// dattr[n] (+)= sum of dx over the edges into n, minus the sum over the edges
+// out of n (in CSR, then CSC order).
+__global__ __launch_bounds__(256) void k_attr_seg(int64_t n_src, int64_t n_dst, int de,
+                                                  const int32_t* __restrict__ row_ptr,
+                                                  const int32_t* __restrict__ csc_ptr,
+                                                  const int32_t* __restrict__ csc_eid, const float4* __restrict__ dx,
+                                                  float* __restrict__ dattr, int accumulate) {
+  const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (n >= n_src) return;
+  float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (n < n_dst)
+    for (int32_t e = row_ptr[n]; e < row_ptr[n + 1]; ++e) {
+      const float4 v = dx[e];
+      s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
+    }
+  for (int32_t k = csc_ptr[n]; k < csc_ptr[n + 1]; ++k) {
+    const float4 v = dx[csc_eid[k]];
+    s[0] -= v.x; s[1] -= v.y; s[2] -= v.z; s[3] -= v.w;
+  }
+  for (int c = 0; c < de; ++c) {
+    float* o = dattr + n * de + c;
+    *o = accumulate ? *o + s[c] : s[c];
+  }
+}
+
+template <typename T, int H1>
+dsmp_status launch_attr_dx(dsmp_handle* h, int64_t E, const unsigned char* da1E, const float* w1l, float4* dx) {
+  const int64_t grid = std::min<int64_t>(ceil_div(E, 16), (int64_t)h->n_cu * 8);
+  hipLaunchKernelGGL((k_attr_dx<T, H1>), dim3((unsigned)grid), dim3(256), 0, h->stream, E, da1E, w1l, dx);
+  DSMP_LAUNCHED(h, "edge-attribute gradient");
+  return DSMP_OK;
+}
+
 // ------------------------------------------------------------ reductions and finals
 
 // Fixed-order reductions out[x] = [out[x] +] sum_c part[c*stride + off + x]
@@ -1201,6 +1268,7 @@ __global__ void k_bwd_dh_final(int64_t n_src, int64_t n_dst, int DL, const int32
 struct BwdWs {
   float *ybar, *gF, *dh_node, *dh_direct, *dh_part, *dh_sl;
   unsigned char *gT, *da2E, *da1E, *ot, *U;
+  float4* dx;                  // [E] edge-attribute gradients (diff attributes)
   int nslh;
   float *p_root, *p_db3, *p_w3, *p_w2, *p_w1;
   int nr, nb3, n3, n2, n1;
@@ -1244,6 +1312,7 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   w.U = c.take<unsigned char>((size_t)n_dst * d.h2 * d.d * esz);
   w.da2E = c.take<unsigned char>((size_t)E * d.h2 * esz);
   w.da1E = c.take<unsigned char>((size_t)E * d.h1 * esz);
+  w.dx = c.take<float4>((size_t)E);
   w.nr = (int)(n_dst > 0 ? (ceil_div(n_dst, 32) < 1024 ? ceil_div(n_dst, 32) : 1024) : 1);
   w.pr = n_dst > 0 ? ceil_div(n_dst, w.nr) : 1;
   w.p_root = c.take<float>((size_t)w.nr * (d.d * d.d + d.d));
@@ -1400,7 +1469,9 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
                     grads->dbr, DSMP_INVALID_ARG, "a gradient pointer is NULL");
   DSMP_CHECK(h, (g->n_dst == 0 || grad_out) && (g->n_src == 0 || (grad_h && h_in && node_attr)),
              DSMP_INVALID_ARG, "a backward pointer is NULL");
-  DSMP_CHECK(h, (flags & ~DSMP_GRAD_ACCUMULATE) == 0, DSMP_INVALID_ARG, "unknown flags");
+  DSMP_CHECK(h, (flags & ~(DSMP_GRAD_ACCUMULATE | DSMP_GRAD_X_ACCUMULATE)) == 0, DSMP_INVALID_ARG, "unknown flags");
+  DSMP_CHECK(h, !grads->dattr || desc->attr_mode == DSMP_ATTR_DIFF, DSMP_UNSUPPORTED,
+             "the attribute gradient needs difference edge attributes");
   const SavedLayout sl = saved_layout(d, g->n_dst, g->n_edges);
   DSMP_CHECK(h, saved_bytes >= sl.total, DSMP_WORKSPACE_TOO_SMALL, "saved buffer needs %zu bytes", sl.total);
   const BwdWs need = carve_bwd(d, g->n_dst, g->n_src, g->n_edges, nullptr);
@@ -1493,6 +1564,25 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
       st = launch_dw1_tr<256>(h, n1, E, w.pc1, w.da1E, sv + sl.xE, de, w.p_w1);
     if (st != DSMP_OK) return st;
     DSMP_LAUNCHED(h, "dW1");
+  }
+
+  if (grads->dattr && n_src > 0) {
+    // node-attribute gradient through the difference edge attributes
+    ProfScope prof(h, DSMP_K_ATTR);
+    if (E > 0) {
+      const float* w1l = reinterpret_cast<const float*>(pk + L.w1l);
+      if (d.dtype == DSMP_BF16)
+        st = d.h1 == 64 ? launch_attr_dx<__bf16, 64>(h, E, w.da1E, w1l, w.dx)
+             : d.h1 == 128 ? launch_attr_dx<__bf16, 128>(h, E, w.da1E, w1l, w.dx)
+                           : launch_attr_dx<__bf16, 256>(h, E, w.da1E, w1l, w.dx);
+      else
+        st = d.h1 == 64 ? launch_attr_dx<float, 64>(h, E, w.da1E, w1l, w.dx)
+                        : launch_attr_dx<float, 128>(h, E, w.da1E, w1l, w.dx);
+      if (st != DSMP_OK) return st;
+    }
+    hipLaunchKernelGGL(k_attr_seg, dim3(ceil_div(n_src, 256)), dim3(256), 0, s, n_src, n_dst, de, g->row_ptr,
+                       g->csc_ptr, g->csc_eid, w.dx, grads->dattr, (flags & DSMP_GRAD_X_ACCUMULATE) ? 1 : 0);
+    DSMP_LAUNCHED(h, "attribute gradient sums");
   }
 
   if (agg) {

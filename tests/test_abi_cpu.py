@@ -77,3 +77,17 @@ def test_null_handle_is_rejected(lib):
     assert lib.dsmp_set_stream(None, None) == dm.INVALID_ARG
     assert lib.dsmp_last_error(None) == b""
     assert lib.dsmp_create(None, 0) == dm.INVALID_ARG
+
+
+def test_hop_loop_host_side_queries(lib):
+    import paper_2402_15106_amd as dm
+    sb, wb = ctypes.c_size_t(), ctypes.c_size_t()
+    desc = dm.MlpDesc(3, 64, 32)
+    assert lib.dsmp_mlp_workspace(ctypes.byref(desc), 1000, ctypes.byref(sb), ctypes.byref(wb)) == dm.OK
+    assert sb.value >= 2 * 1000 * 64 * 4 and wb.value >= 2 * 1000 * 64 * 4
+    assert lib.dsmp_mlp_workspace(ctypes.byref(dm.MlpDesc(3, 6, 32)), 10, ctypes.byref(sb),
+                                  ctypes.byref(wb)) == dm.UNSUPPORTED          # hidden width not a multiple of 4
+    assert lib.dsmp_mlp_workspace(ctypes.byref(desc), -1, ctypes.byref(sb), ctypes.byref(wb)) == dm.INVALID_ARG
+    assert lib.dsmp_masked_mse_workspace(5000, ctypes.byref(sb)) == dm.OK and sb.value >= 20 * 8
+    assert lib.dsmp_masked_mse_workspace(-1, ctypes.byref(sb)) == dm.INVALID_ARG
+    assert lib.dsmp_mlp_forward(None, ctypes.byref(desc), None, None, 0, None, None, None, 0) == dm.INVALID_ARG
