@@ -25,6 +25,7 @@ __global__ __launch_bounds__(256) void k_dense(int64_t n, int din, int dout, con
     const float* xi = in + r * din;
     const float* wo = W + (int64_t)o * din;
     float v = b[o];
+#pragma unroll 8
     for (int i = 0; i < din; ++i) v = __builtin_fmaf(xi[i], wo[i], v);
     if (relu && !(v > 0.0f)) v = 0.0f;
     out[x] = v;
@@ -42,6 +43,7 @@ __global__ __launch_bounds__(256) void k_dense_back(int64_t n, int din, int dout
     const int i = (int)(x % din);
     const float* gr = g + r * dout;
     float v = 0.0f;
+#pragma unroll 8
     for (int o = 0; o < dout; ++o) v = __builtin_fmaf(gr[o], W[(int64_t)o * din + i], v);
     if (h && !(h[x] > 0.0f)) v = 0.0f;
     gin[x] = accumulate ? gin[x] + v : v;
@@ -49,35 +51,193 @@ __global__ __launch_bounds__(256) void k_dense_back(int64_t n, int din, int dout
 }
 
 // part[c][o][i] = sum over rows r of part c of g[r][o] * in[r][i] for i < din,
-// and part[c][o][din] = sum of g[r][o] (the bias gradient), rows in order.
+// and part[c][o][din] = sum of g[r][o] (the bias gradient, against a column of
+// ones), rows in order.  Block (c, b) serves the 256 (o, i) pairs starting at
+// 256 b; the rows pass through LDS 32 at a time.
+constexpr int OUTER_RC = 32;
+
 __global__ __launch_bounds__(256) void k_outer_rows(int64_t n, int din, int dout, const float* __restrict__ g,
                                                     const float* __restrict__ in, float* __restrict__ part) {
+  __shared__ float gs[OUTER_RC * 256], xs[OUTER_RC * 257];
   const int64_t r0 = (int64_t)blockIdx.x * ROWS_PER_PART;
   const int64_t r1 = std::min<int64_t>(r0 + ROWS_PER_PART, n);
+  const int pairs = dout * (din + 1), xw = din + 1;
+  const int p = blockIdx.y * 256 + threadIdx.x;
+  const int o = p / xw, i = p % xw;
+  float v = 0.0f;
+  for (int64_t rc = r0; rc < r1; rc += OUTER_RC) {
+    const int cnt = (int)std::min<int64_t>(OUTER_RC, r1 - rc);
+    __syncthreads();
+    for (int t = threadIdx.x; t < cnt * dout; t += 256) gs[t] = g[rc * dout + t];
+    for (int t = threadIdx.x; t < cnt * xw; t += 256) {
+      const int k = t / xw, c = t % xw;
+      xs[t] = c < din ? in[(rc + k) * din + c] : 1.0f;
+    }
+    __syncthreads();
+    if (p < pairs)
+      for (int k = 0; k < cnt; ++k) v = __builtin_fmaf(gs[k * dout + o], xs[k * xw + i], v);
+  }
+  if (p < pairs) part[(int64_t)blockIdx.x * pairs + p] = v;
+}
+
+dim3 outer_grid(int np, int din, int dout) { return dim3(np, ceil_div(dout * (din + 1), 256)); }
+
+// dW[o][i] (+)= sum_c part[c][o][i], db[o] (+)= sum_c part[c][o][din].  A
+// block serves 64 pairs; its four waves sum the partials c = g, g+4, ... in
+// order and the four sums are added in wave order (a fixed order).
+__global__ __launch_bounds__(256) void k_outer_final(int nparts, int din, int dout, const float* __restrict__ part,
+                                                     float* __restrict__ dW, float* __restrict__ db, int accumulate) {
+  __shared__ float sh[4][64];
   const int pairs = dout * (din + 1);
-  float* out = part + (int64_t)blockIdx.x * pairs;
-  for (int p = threadIdx.x; p < pairs; p += 256) {
+  const int p = blockIdx.x * 64 + (threadIdx.x & 63), g = threadIdx.x >> 6;
+  float v = 0.0f;
+  if (p < pairs) {
+#pragma unroll 8
+    for (int c = g; c < nparts; c += 4) v += part[(int64_t)c * pairs + p];
+  }
+  sh[g][threadIdx.x & 63] = v;
+  __syncthreads();
+  if (g == 0 && p < pairs) {
+    v = sh[0][threadIdx.x] + sh[1][threadIdx.x] + sh[2][threadIdx.x] + sh[3][threadIdx.x];
     const int o = p / (din + 1), i = p % (din + 1);
-    float v = 0.0f;
-    if (i < din)
-      for (int64_t r = r0; r < r1; ++r) v = __builtin_fmaf(g[r * dout + o], in[r * din + i], v);
-    else
-      for (int64_t r = r0; r < r1; ++r) v += g[r * dout + o];
-    out[p] = v;
+    float* t = i < din ? dW + (int64_t)o * din + i : db + o;
+    *t = accumulate ? *t + v : v;
   }
 }
 
-// dW[o][i] (+)= sum_c part[c][o][i], db[o] (+)= sum_c part[c][o][din], c in order.
-__global__ __launch_bounds__(256) void k_outer_final(int nparts, int din, int dout, const float* __restrict__ part,
-                                                     float* __restrict__ dW, float* __restrict__ db, int accumulate) {
-  const int pairs = dout * (din + 1);
-  const int p = blockIdx.x * 256 + threadIdx.x;
-  if (p >= pairs) return;
-  float v = 0.0f;
-  for (int c = 0; c < nparts; ++c) v += part[(int64_t)c * pairs + p];
-  const int o = p / (din + 1), i = p % (din + 1);
-  float* t = i < din ? dW + (int64_t)o * din + i : db + o;
-  *t = accumulate ? *t + v : v;
+// Fused perceptron passes over blocks of FR rows, activations in LDS (used
+// when they fit, see fused_lds).  A dense step out[r][o] = act(b[o] +
+// sum_k in[r][k] W[o][k]) over the block's rows, in LDS, with optional copies
+// to global memory.
+constexpr int FR = 32;
+
+// WT: the layer's weights transposed, [K][O], in LDS.
+__device__ __forceinline__ void dense_rows(int cnt, int K, int O, const float* __restrict__ in_s,
+                                           const float* __restrict__ WT, const float* __restrict__ b, int relu,
+                                           float* __restrict__ out_s, float* __restrict__ out_g,
+                                           __bf16* __restrict__ out_bf16) {
+  for (int t = threadIdx.x; t < cnt * O; t += 256) {
+    const int r = t / O, o = t % O;
+    const float* xi = in_s + r * K;
+    float v = b[o];
+#pragma unroll 8
+    for (int k = 0; k < K; ++k) v = __builtin_fmaf(xi[k], WT[k * O + o], v);
+    if (relu && !(v > 0.0f)) v = 0.0f;
+    if (out_s) out_s[t] = v;
+    if (out_g) out_g[t] = v;
+    if (out_bf16) out_bf16[t] = (__bf16)v;
+  }
+}
+
+// g_in[r][k] = [mask[r][k] > 0] * sum_o g[r][o] W[o][k] over the block's rows (in LDS)
+__device__ __forceinline__ void dense_back_rows(int cnt, int K, int O, const float* __restrict__ g_s,
+                                                const float* __restrict__ W, const float* __restrict__ mask_s,
+                                                float* __restrict__ out_s, float* __restrict__ out_g, int accumulate) {
+  for (int t = threadIdx.x; t < cnt * K; t += 256) {
+    const int r = t / K, k = t % K;
+    const float* gr = g_s + r * O;
+    float v = 0.0f;
+#pragma unroll 8
+    for (int o = 0; o < O; ++o) v = __builtin_fmaf(gr[o], W[(int64_t)o * K + k], v);
+    if (mask_s && !(mask_s[t] > 0.0f)) v = 0.0f;
+    if (out_s) out_s[t] = v;
+    if (out_g) out_g[t] = accumulate ? out_g[t] + v : v;
+  }
+}
+
+// part[o][k] = sum over the block's rows of g[r][o] * in[r][k] (k < K), part[o][K] = sum of g[r][o]
+__device__ __forceinline__ void outer_block(int cnt, int K, int O, const float* __restrict__ g_s,
+                                            const float* __restrict__ in_s, float* __restrict__ part) {
+  for (int p = threadIdx.x; p < O * (K + 1); p += 256) {
+    const int o = p / (K + 1), k = p % (K + 1);
+    float v = 0.0f;
+    if (k < K)
+      for (int r = 0; r < cnt; ++r) v = __builtin_fmaf(g_s[r * O + o], in_s[r * K + k], v);
+    else
+      for (int r = 0; r < cnt; ++r) v += g_s[r * O + o];
+    part[p] = v;
+  }
+}
+
+struct MlpArgs {
+  int64_t n;
+  int din, dh, dout;
+  const float *W1, *b1, *W2, *b2, *W3, *b3;
+  const float* x;
+  float *h1, *h2;        // saved activations [n][dh]
+  float* y;              // forward output [n][dout]
+  __bf16* y_bf16;
+  const float* gy;       // backward input [n][dout]
+  float* gx;             // backward output [n][din] (nullable)
+  int gx_acc;
+  float *p3, *p2, *p1;   // per-block partials of the weight gradients
+};
+
+// Persistent blocks: the three weight matrices are copied transposed into LDS
+// once, then the blocks take FR-row tiles in turn.
+__global__ __launch_bounds__(256) void k_mlp_fwd(MlpArgs a) {
+  extern __shared__ float sm[];
+  float* t1 = sm;                        // W1^T [din][dh]
+  float* t2 = t1 + a.din * a.dh;         // W2^T [dh][dh]
+  float* t3 = t2 + a.dh * a.dh;          // W3^T [dh][dout]
+  float* xs = t3 + a.dh * a.dout;
+  float* s1 = xs + FR * a.din;
+  float* s2 = s1 + FR * a.dh;
+  for (int t = threadIdx.x; t < a.din * a.dh; t += 256) t1[(t % a.din) * a.dh + t / a.din] = a.W1[t];
+  for (int t = threadIdx.x; t < a.dh * a.dh; t += 256) t2[(t % a.dh) * a.dh + t / a.dh] = a.W2[t];
+  for (int t = threadIdx.x; t < a.dout * a.dh; t += 256) t3[(t % a.dh) * a.dout + t / a.dh] = a.W3[t];
+  const int64_t ntile = (a.n + FR - 1) / FR;
+  for (int64_t tile = blockIdx.x; tile < ntile; tile += gridDim.x) {
+    const int64_t r0 = tile * FR;
+    const int cnt = (int)std::min<int64_t>(FR, a.n - r0);
+    __syncthreads();   // weights staged / the previous tile's rows consumed
+    for (int t = threadIdx.x; t < cnt * a.din; t += 256) xs[t] = a.x[r0 * a.din + t];
+    __syncthreads();
+    dense_rows(cnt, a.din, a.dh, xs, t1, a.b1, 1, s1, a.h1 + r0 * a.dh, nullptr);
+    __syncthreads();
+    dense_rows(cnt, a.dh, a.dh, s1, t2, a.b2, 1, s2, a.h2 + r0 * a.dh, nullptr);
+    __syncthreads();
+    dense_rows(cnt, a.dh, a.dout, s2, t3, a.b3, 0, nullptr, a.y + r0 * a.dout,
+               a.y_bf16 ? a.y_bf16 + r0 * a.dout : nullptr);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_mlp_bwd(MlpArgs a) {
+  extern __shared__ float sm[];
+  float* xs = sm;                     // [FR][din]
+  float* g3 = xs + FR * a.din;        // [FR][dout]
+  float* s1 = g3 + FR * a.dout;       // h1 [FR][dh]
+  float* s2 = s1 + FR * a.dh;         // h2
+  float* g2 = s2 + FR * a.dh;
+  float* g1 = g2 + FR * a.dh;
+  const int64_t r0 = (int64_t)blockIdx.x * FR;
+  const int cnt = (int)std::min<int64_t>(FR, a.n - r0);
+  for (int t = threadIdx.x; t < cnt * a.din; t += 256) xs[t] = a.x[r0 * a.din + t];
+  for (int t = threadIdx.x; t < cnt * a.dout; t += 256) g3[t] = a.gy[r0 * a.dout + t];
+  for (int t = threadIdx.x; t < cnt * a.dh; t += 256) {
+    s1[t] = a.h1[r0 * a.dh + t];
+    s2[t] = a.h2[r0 * a.dh + t];
+  }
+  __syncthreads();
+  dense_back_rows(cnt, a.dh, a.dout, g3, a.W3, s2, g2, nullptr, 0);
+  __syncthreads();
+  dense_back_rows(cnt, a.dh, a.dh, g2, a.W2, s1, g1, nullptr, 0);
+  __syncthreads();
+  if (a.gx) dense_back_rows(cnt, a.din, a.dh, g1, a.W1, nullptr, nullptr, a.gx + r0 * a.din, a.gx_acc);
+  const int64_t b = blockIdx.x;
+  outer_block(cnt, a.dh, a.dout, g3, s2, a.p3 + b * a.dout * (a.dh + 1));
+  outer_block(cnt, a.dh, a.dh, g2, s1, a.p2 + b * a.dh * (a.dh + 1));
+  outer_block(cnt, a.din, a.dh, g1, xs, a.p1 + b * a.dh * (a.din + 1));
+}
+
+// LDS bytes of the fused passes; 0 when either does not fit (64 KB)
+int fused_fwd_lds(const dsmp_mlp_desc& d) {
+  return (int)(((size_t)d.d_in * d.d_hid + (size_t)d.d_hid * d.d_hid + (size_t)d.d_hid * d.d_out +
+                (size_t)FR * (d.d_in + 2 * d.d_hid)) * sizeof(float));
+}
+int fused_lds(const dsmp_mlp_desc& d) {
+  const size_t bytes = (size_t)FR * (d.d_in + d.d_out + 4 * d.d_hid) * sizeof(float);
+  return bytes <= 64 * 1024 && fused_fwd_lds(d) <= 64 * 1024 ? (int)bytes : 0;
 }
 
 // Masked MSE: per-block partial sums (squared error, interior rows), a
@@ -164,7 +324,7 @@ struct MlpWs {
 MlpWs mlp_ws(const dsmp_mlp_desc& d, int64_t n, void* base) {
   Carve c(base);
   MlpWs w;
-  w.nparts = (int)std::max<int64_t>(1, ceil_div(n, ROWS_PER_PART));
+  w.nparts = (int)std::max<int64_t>(1, ceil_div(n, fused_lds(d) ? FR : ROWS_PER_PART));
   w.g2 = c.take<float>((size_t)n * d.d_hid);
   w.g1 = c.take<float>((size_t)n * d.d_hid);
   w.p3 = c.take<float>((size_t)w.nparts * d.d_out * (d.d_hid + 1));
@@ -210,6 +370,15 @@ extern "C" dsmp_status dsmp_mlp_forward(dsmp_handle* h, const dsmp_mlp_desc* des
   if (n == 0) return DSMP_OK;
   ProfScope prof(h, DSMP_K_MLP);
   hipStream_t st_ = h->stream;
+  if (const int lds = fused_lds(d)) {
+    MlpArgs a{n, d.d_in, d.d_hid, d.d_out, p->W1, p->b1, p->W2, p->b2, p->W3, p->b3, x, s.h1, s.h2, y,
+              static_cast<__bf16*>(y_bf16), nullptr, nullptr, 0, nullptr, nullptr, nullptr};
+    (void)lds;
+    const int64_t grid = std::min<int64_t>(ceil_div(n, FR), (int64_t)h->n_cu * 2);
+    hipLaunchKernelGGL(k_mlp_fwd, dim3((unsigned)grid), dim3(256), fused_fwd_lds(d), st_, a);
+    DSMP_LAUNCHED(h, "perceptron forward");
+    return DSMP_OK;
+  }
   hipLaunchKernelGGL(k_dense, dim3(grid_for(n * d.d_hid)), dim3(256), 0, st_, n, d.d_in, d.d_hid, x, p->W1, p->b1, 1,
                      s.h1, (__bf16*)nullptr);
   hipLaunchKernelGGL(k_dense, dim3(grid_for(n * d.d_hid)), dim3(256), 0, st_, n, d.d_hid, d.d_hid, s.h1, p->W2, p->b2,
@@ -244,25 +413,32 @@ extern "C" dsmp_status dsmp_mlp_backward(dsmp_handle* h, const dsmp_mlp_desc* de
   ProfScope prof(h, DSMP_K_MLP);
   hipStream_t q = h->stream;
   const int np = n > 0 ? w.nparts : 0;
-  if (n > 0) {
+  if (n > 0 && fused_lds(d)) {
+    MlpArgs a{n, d.d_in, d.d_hid, d.d_out, p->W1, p->b1, p->W2, p->b2, p->W3, p->b3, x, s.h1, s.h2, nullptr,
+              nullptr, grad_y, grad_x, (flags & DSMP_GRAD_X_ACCUMULATE) ? 1 : 0, w.p3, w.p2, w.p1};
+    hipLaunchKernelGGL(k_mlp_bwd, dim3(np), dim3(256), fused_lds(d), q, a);
+  } else if (n > 0) {
     // layer 3 (no activation): weights from grad_y and h2, then back to h2's pre-activation
-    hipLaunchKernelGGL(k_outer_rows, dim3(np), dim3(256), 0, q, n, d.d_hid, d.d_out, grad_y, s.h2, w.p3);
+    hipLaunchKernelGGL(k_outer_rows, outer_grid(np, d.d_hid, d.d_out), dim3(256), 0, q, n, d.d_hid, d.d_out, grad_y,
+                       s.h2, w.p3);
     hipLaunchKernelGGL(k_dense_back, dim3(grid_for(n * d.d_hid)), dim3(256), 0, q, n, d.d_hid, d.d_out, grad_y, p->W3,
                        s.h2, w.g2, 0);
-    hipLaunchKernelGGL(k_outer_rows, dim3(np), dim3(256), 0, q, n, d.d_hid, d.d_hid, w.g2, s.h1, w.p2);
+    hipLaunchKernelGGL(k_outer_rows, outer_grid(np, d.d_hid, d.d_hid), dim3(256), 0, q, n, d.d_hid, d.d_hid, w.g2,
+                       s.h1, w.p2);
     hipLaunchKernelGGL(k_dense_back, dim3(grid_for(n * d.d_hid)), dim3(256), 0, q, n, d.d_hid, d.d_hid, w.g2, p->W2,
                        s.h1, w.g1, 0);
-    hipLaunchKernelGGL(k_outer_rows, dim3(np), dim3(256), 0, q, n, d.d_in, d.d_hid, w.g1, x, w.p1);
+    hipLaunchKernelGGL(k_outer_rows, outer_grid(np, d.d_in, d.d_hid), dim3(256), 0, q, n, d.d_in, d.d_hid, w.g1, x,
+                       w.p1);
     if (grad_x)
       hipLaunchKernelGGL(k_dense_back, dim3(grid_for(n * d.d_in)), dim3(256), 0, q, n, d.d_in, d.d_hid, w.g1, p->W1,
                          (const float*)nullptr, grad_x, (flags & DSMP_GRAD_X_ACCUMULATE) ? 1 : 0);
   }
   // with no rows the partial count is 0 and the finals write zeros (or add nothing)
-  hipLaunchKernelGGL(k_outer_final, dim3(ceil_div(d.d_out * (d.d_hid + 1), 256)), dim3(256), 0, q, np, d.d_hid,
+  hipLaunchKernelGGL(k_outer_final, dim3(ceil_div(d.d_out * (d.d_hid + 1), 64)), dim3(256), 0, q, np, d.d_hid,
                      d.d_out, w.p3, grads->dW3, grads->db3, acc);
-  hipLaunchKernelGGL(k_outer_final, dim3(ceil_div(d.d_hid * (d.d_hid + 1), 256)), dim3(256), 0, q, np, d.d_hid,
+  hipLaunchKernelGGL(k_outer_final, dim3(ceil_div(d.d_hid * (d.d_hid + 1), 64)), dim3(256), 0, q, np, d.d_hid,
                      d.d_hid, w.p2, grads->dW2, grads->db2, acc);
-  hipLaunchKernelGGL(k_outer_final, dim3(ceil_div(d.d_hid * (d.d_in + 1), 256)), dim3(256), 0, q, np, d.d_in,
+  hipLaunchKernelGGL(k_outer_final, dim3(ceil_div(d.d_hid * (d.d_in + 1), 64)), dim3(256), 0, q, np, d.d_in,
                      d.d_hid, w.p1, grads->dW1, grads->db1, acc);
   DSMP_LAUNCHED(h, "perceptron backward");
   return DSMP_OK;

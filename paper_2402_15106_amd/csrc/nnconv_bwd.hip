@@ -1157,27 +1157,34 @@ __global__ __launch_bounds__(256) void k_attr_dx(int64_t E, const unsigned char*
 }
 
 // dattr[n] (+)= sum of dx over the edges into n, minus the sum over the edges
-// out of n (in CSR, then CSC order).
+// out of n.  Sixteen lanes per node: lane g takes every 16th edge of each
+// list, then a fixed butterfly adds the lanes (a fixed order).
 __global__ __launch_bounds__(256) void k_attr_seg(int64_t n_src, int64_t n_dst, int de,
                                                   const int32_t* __restrict__ row_ptr,
                                                   const int32_t* __restrict__ csc_ptr,
                                                   const int32_t* __restrict__ csc_eid, const float4* __restrict__ dx,
                                                   float* __restrict__ dattr, int accumulate) {
-  const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (n >= n_src) return;
+  const int64_t n = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 4;
+  const int g = threadIdx.x & 15;
+  if (n >= n_src) return;   // whole 16-lane groups leave together
   float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (n < n_dst)
-    for (int32_t e = row_ptr[n]; e < row_ptr[n + 1]; ++e) {
+    for (int32_t e = row_ptr[n] + g; e < row_ptr[n + 1]; e += 16) {
       const float4 v = dx[e];
       s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
     }
-  for (int32_t k = csc_ptr[n]; k < csc_ptr[n + 1]; ++k) {
+  for (int32_t k = csc_ptr[n] + g; k < csc_ptr[n + 1]; k += 16) {
     const float4 v = dx[csc_eid[k]];
     s[0] -= v.x; s[1] -= v.y; s[2] -= v.z; s[3] -= v.w;
   }
-  for (int c = 0; c < de; ++c) {
-    float* o = dattr + n * de + c;
-    *o = accumulate ? *o + s[c] : s[c];
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) s[c] += __shfl_xor(s[c], o, 16);
+  if (g < de) {
+    const float v = g == 0 ? s[0] : g == 1 ? s[1] : g == 2 ? s[2] : s[3];
+    float* o = dattr + n * de + g;
+    *o = accumulate ? *o + v : v;
   }
 }
 
@@ -1580,7 +1587,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
                         : launch_attr_dx<float, 128>(h, E, w.da1E, w1l, w.dx);
       if (st != DSMP_OK) return st;
     }
-    hipLaunchKernelGGL(k_attr_seg, dim3(ceil_div(n_src, 256)), dim3(256), 0, s, n_src, n_dst, de, g->row_ptr,
+    hipLaunchKernelGGL(k_attr_seg, dim3(ceil_div(n_src * 16, 256)), dim3(256), 0, s, n_src, n_dst, de, g->row_ptr,
                        g->csc_ptr, g->csc_eid, w.dx, grads->dattr, (flags & DSMP_GRAD_X_ACCUMULATE) ? 1 : 0);
     DSMP_LAUNCHED(h, "attribute gradient sums");
   }

@@ -285,3 +285,27 @@ def make_config(k: int, n_sample: int = None, layers: int = None) -> Workload:
     return Workload(k=k, name=spec["name"], D=D, d=d, de=de, H1=spec["H1"], H2=spec["H2"],
                     layers=L, dtype=spec["dtype"], r=r, cap=spec["cap"], cap_mode=CAP_KNN,
                     parts=parts, params=params, grad_out=G)
+
+
+def hop_setup(w: Workload, hid: int = 64):
+    """Parameters and targets of the hop-loop training step on workload w
+    (seed 5000 + k): the encoder (dim+1 -> hid -> hid -> d) and decoder
+    (d -> hid -> hid -> dim+1) perceptrons, U(+-1/sqrt(fan_in)); one layer with
+    difference edge attributes (de = dim+1) serving every hop; targets
+    Y ~ N(0, 1) for every node value.  Returns (enc, conv, dec, Y)."""
+    rng = np.random.Generator(np.random.PCG64(5000 + w.k))
+    c = w.D + 1
+
+    def mlp(din, dout):
+        return {"W1": _uniform(rng, (hid, din), din).astype(np.float32),
+                "b1": _uniform(rng, (hid,), din).astype(np.float32),
+                "W2": _uniform(rng, (hid, hid), hid).astype(np.float32),
+                "b2": _uniform(rng, (hid,), hid).astype(np.float32),
+                "W3": _uniform(rng, (dout, hid), hid).astype(np.float32),
+                "b3": _uniform(rng, (dout,), hid).astype(np.float32)}
+
+    enc = mlp(c, w.d)
+    dec = mlp(w.d, c)
+    conv = layer_params(rng, w.d, c, w.H1, w.H2, w.dtype)
+    Y = rng.standard_normal((w.n_src, c)).astype(np.float32)
+    return enc, conv, dec, Y
