@@ -136,15 +136,24 @@ def work_model(w, E, n_src):
     return m
 
 
-def agg_work(w, E, n_src):
-    """Work of the classes whose kernels differ between the two forms."""
-    d, H1, H2 = w.d, w.H1, w.H2
+def agg_work(w, E, n_src, fused=False):
+    """Work of the classes whose kernels differ between the two forms.  With
+    ``fused`` the dz class is the one-pass kernel that also forms the dW2 and
+    dW1 sums: it reads U_i, the gathered rows, the ReLU mask bits and both
+    endpoints' node attributes, and writes no per-edge array (its per-workgroup
+    partial sums are not counted)."""
+    d, H1, H2, D, de = w.d, w.H1, w.H2, w.D, w.de
     n = w.n_dst
     esz = 2 if w.dtype == "bf16" else 4
     kt = (H2 + 1) * d
     mask = (H1 + H2) // 8
+    if fused:
+        dz = (2 * E * (d * H2 + H1 * H2 + H1 * H2 + H1 * de),
+              n * H2 * d * esz + E * (4 + d * esz + mask + 2 * (D + 1) * 4))
+    else:
+        dz = (2 * E * (d * H2 + H1 * H2), n * H2 * d * esz + E * (4 + d * esz + mask + (H1 + H2) * esz))
     return {
-        "dz": (2 * E * (d * H2 + H1 * H2), n * H2 * d * esz + E * (4 + d * esz + mask + (H1 + H2) * esz)),
+        "dz": dz,
         "dW3": (2 * n * kt * d, n * kt * esz + n * d * esz),
     }
 
@@ -390,7 +399,8 @@ def main():
         import dataclasses
         w = dataclasses.replace(w, de=w.D + 1)
     work = work_model(w, E, w.n_src)
-    work.update(agg_work(w, E, w.n_src) if agg else per_edge_work(w, E, w.n_src))
+    fused = agg and not ("dW2" in prof and prof["dW2"][1] > 0)
+    work.update(agg_work(w, E, w.n_src, fused) if agg else per_edge_work(w, E, w.n_src))
     kernels = {}
     for name, (tot, n) in prof.items():
         if n == 0:

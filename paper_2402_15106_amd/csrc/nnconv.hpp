@@ -180,14 +180,13 @@ __device__ __forceinline__ bf16x8 lds_frag_rows(const unsigned char* X, int pitc
 // Wait for this thread's outstanding global loads, the LDS stages included.
 __device__ __forceinline__ void stage_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-// Edge attributes of edge (i <- j): concat [p_i, p_j, s_i, s_j] or diff
-// v_i - v_j, zero-padded to 8 (Sec. 2.1).
-__device__ __forceinline__ void edge_attr(const float* __restrict__ na, int dim, int mode, int i, int j,
-                                          float x[8]) {
+// Edge attributes of edge (i <- j) from the node attribute rows v_i, v_j
+// (dim + 1 values each): concat [p_i, p_j, s_i, s_j] or diff v_i - v_j,
+// zero-padded to 8 (Sec. 2.1).
+template <typename V>
+__device__ __forceinline__ void edge_attr_rows(const V& vi, const V& vj, int dim, int mode, float x[8]) {
 #pragma unroll
   for (int c = 0; c < 8; ++c) x[c] = 0.0f;
-  const float* vi = na + (size_t)i * (dim + 1);
-  const float* vj = na + (size_t)j * (dim + 1);
   if (dim == 2) {
     if (mode == DSMP_ATTR_CONCAT) {
       x[0] = vi[0]; x[1] = vi[1]; x[2] = vj[0]; x[3] = vj[1]; x[4] = vi[2]; x[5] = vj[2];
@@ -202,6 +201,20 @@ __device__ __forceinline__ void edge_attr(const float* __restrict__ na, int dim,
       x[0] = vi[0] - vj[0]; x[1] = vi[1] - vj[1]; x[2] = vi[2] - vj[2]; x[3] = vi[3] - vj[3];
     }
   }
+}
+
+__device__ __forceinline__ void edge_attr(const float* __restrict__ na, int dim, int mode, int i, int j,
+                                          float x[8]) {
+  edge_attr_rows(na + (size_t)i * (dim + 1), na + (size_t)j * (dim + 1), dim, mode, x);
+}
+
+// Workgroup barrier for LDS traffic only: the workgroup's LDS writes are
+// complete and visible after it, while global loads issued before it stay
+// in flight (a full __syncthreads() waits for them as well).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 // Pre-activation of the first kernel-MLP layer for one output: b1 + W1 x as

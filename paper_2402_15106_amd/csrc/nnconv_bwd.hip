@@ -14,6 +14,8 @@
 // are added in chunk order: no atomics, bitwise-reproducible results.
 #include "nnconv.hpp"
 
+#include <type_traits>
+
 using namespace dsmp;
 
 namespace {
@@ -468,6 +470,373 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 3 : 1) v
       dz_finish<T, DL, H1, H2, NT, KT, SA::W2P>(a, acc, eid, valid, hh, smem);
     }
     __syncthreads();   // the block's tile list is read until every wave is done
+  }
+}
+
+// Fused edge gradients of the aggregate form (bf16 layers, h1 = h2 <= 128).
+// One pass over the 32-edge tiles of k_bwd_dz_agg computes dz = U_i h_j, the
+// masked da2, dz1 = W2^T da2 and da1 (as there), and folds the per-edge
+// weight gradients straight into per-workgroup sums, so da2 and da1 never go
+// to HBM:
+//   dW2[k][j] = sum_e da2_e[k] z1_e[j],  db2 = sum_e da2_e,
+//   dW1[j][c] = sum_e da1_e[j] x_e[c],   db1 = sum_e da1_e.
+// A workgroup of eight waves takes four tiles per round; the two waves of a
+// pair share one tile and its LDS slot (dz split by k tiles, dz1 by j tiles,
+// the z1 row by halves).  The slot receives the tile's rows of da2, da1 and
+// z1 and its split attributes; z1 is recomputed from the attributes with the
+// forward's own multiply-add chain, so it is the forward's value bit for bit.
+// The attributes enter dW1 as bf16 high and low parts (columns 0..7 and
+// 8..15, about 16 significant bits together) next to a column of ones (16)
+// that gives db1; db2 sums the da2 fragments of the products.  After a
+// barrier the four slots are contracted over their edges with transposing
+// LDS reads, each wave taking its share of the dW2 tiles.  While those
+// products run, the loads of the wave's next tile are in flight (its source
+// index one round earlier still); the barriers order LDS traffic only.
+// Partial sums go to slot blockIdx.x of the dW2/db2 and dW1/db1 partial
+// buffers, summed later in a fixed order.
+struct EdgeGradArgs {
+  DzArgs dz;
+  const float* node_attr;
+  int dim, attr_mode, de;
+  unsigned char* da1_out;   // [E][h1] bf16 permuted order, or null (needed for the attribute gradient)
+  float* p_w2;              // [gridDim.x][h2*h1 + h2]
+  float* p_w1;              // [gridDim.x][h1*de + h1]
+};
+
+template <int DL, int H1, int H2>
+struct EdgeGradShape {
+  static_assert(H1 == H2 && (H1 == 64 || H1 == 128), "fused edge gradients: h1 = h2 = 64 or 128");
+  static constexpr int NW = 8, NT = NW * 64;                    // waves, threads
+  static constexpr int W2P = H2 * 2 + 16;                       // LDS pitch of W2^T rows
+  // LDS pitches of the slot rows: four consecutive rows of a transposing read
+  // land 8 banks apart (pitch = 8 dwords mod 64), so its 16-lane groups are
+  // free of bank conflicts
+  static constexpr int DA2P = H2 * 2 + 32, DA1P = H1 * 2 + 32;  // da2 / da1 / z1 rows
+  static constexpr int XSP = 96;                                // 32 bf16 attribute columns
+  static constexpr int OD1 = 32 * DA2P, OZ1 = OD1 + 32 * DA1P, OXS = OZ1 + 32 * DA1P;
+  static constexpr int SLOT = OXS + 32 * XSP;
+  static constexpr int W2B = H1 * W2P, W1B = H1 * 9 * 4;
+  static constexpr int LDS = W2B + W1B + 4 * SLOT;
+  static_assert(LDS <= 160 * 1024 - 256, "LDS of the fused edge-gradient kernel");
+  static constexpr int KT = H2 / 32, JT = H1 / 32;
+  static constexpr int TPW = KT * JT >= NW ? KT * JT / NW : 1;   // dW2 tiles per wave
+  static constexpr int ACTIVE = KT * JT / TPW;                     // waves with dW2 tiles
+};
+
+template <int DL, int H1, int H2>
+__global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
+  using S = DzShape<__bf16, DL, H1, H2>;
+  using G = EdgeGradShape<DL, H1, H2>;
+  using M = MT<__bf16>;
+  using frag = bf16x8;
+  constexpr int KS = S::KS, EPL = S::EPL, KT = S::KT, SKD = S::SKD, SK2 = S::SK2, JT = S::JT;
+  constexpr int SK1 = H1 / KS, MW1 = H1 / 64, MW2 = H2 / 64;
+  constexpr int KTH = KT / 2, JTH = JT / 2, SK1H = SK1 / 2, SK2H = SK2 / 2;   // per half of a pair
+  const DzArgs& a = g.dz;
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* w2s = smem;
+  float* w1s = reinterpret_cast<float*>(smem + G::W2B);   // [H1][8] lane order, then b1 [H1]
+  unsigned char* slots = smem + G::W2B + G::W1B;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int pr = wv & 3, hf = wv >> 2;   // tile (slot) of the wave's pair, half of the pair
+  if (tid < 256) {   // the staging helpers are written for 256 threads
+    LdsStage<H1, H2 * 2> stg;
+    stg.init();
+    stg.issue(a.packed + a.L.w2t, w2s);
+    lds_copy_async(a.packed + a.L.w1l, reinterpret_cast<unsigned char*>(w1s), H1 * 8 * 4 / 16);
+    lds_copy_async(a.packed + a.L.b1l, reinterpret_cast<unsigned char*>(w1s + H1 * 8), H1 * 4 / 16);
+  }
+  // products: dW2 tiles (kt(m), jt) of this wave, db2 of kt(m) where kt(m) % JT == jt
+  const int jt = wv % JT;
+  const bool active = wv < G::ACTIVE;
+  auto kt_of = [&](int m) { return (wv / JT) * G::TPW + m; };
+  f32x16 acc2[G::TPW], acc1 = f32x16{};
+#pragma unroll
+  for (int m = 0; m < G::TPW; ++m) acc2[m] = f32x16{};
+  int bm = -1;   // the tile m whose db2 this wave forms
+#pragma unroll
+  for (int m = 0; m < G::TPW; ++m)
+    if (active && kt_of(m) % JT == jt) bm = m;
+  float db2 = 0.0f;   // the lane's half of the edges, column kt(bm)*32 + l32
+  stage_wait();
+  __syncthreads();   // W2^T and the layer-1 weights are in LDS
+
+  __shared__ int tstart[DZ_NB + 1], rps[DZ_NB + 1];
+  __shared__ int slot_cnt[4];
+  unsigned char* myslot = slots + pr * G::SLOT;
+  const float* w1h = w1s + hh * (H1 / 2) * 8;
+  const float* b1h = w1s + H1 * 8 + hh * (H1 / 2);
+
+  // a tile of the current block: destination, first edge, the lane's edge
+  struct Tile {
+    int i, c0, eid, cnt, jn;   // graph indices are int32
+    bool has, valid;
+  };
+  // the operands of a tile: gathered row, the half's rows of U_i, mask bits, node attribute rows
+  struct Ops {
+    frag hB[SKD], UA[KTH][SKD];
+    uint32_t m1[MW1], m2[MW2];
+    float ri[4], rj[4];
+  };
+  int d0 = 0;
+  int ntile = 0;
+  auto locate = [&](int tau, Tile& t) {
+    t.has = tau < ntile;
+    t.i = d0; t.c0 = 0; t.eid = 0; t.cnt = 0; t.valid = false;
+    if (!t.has) return;
+    int k = 0;
+    while (tstart[k + 1] <= tau) ++k;
+    const int pa = rps[k], pb = rps[k + 1];
+    t.i = d0 + k;
+    t.c0 = pa + (tau - tstart[k]) * 32;
+    t.eid = t.c0 + l32;
+    t.valid = t.eid < pb;
+    t.cnt = pb - t.c0 < 32 ? pb - t.c0 : 32;
+  };
+  // Loads are unconditional (lanes past the tile read edge 0) so that no
+  // select waits on them; the dz part zeroes those lanes.
+  auto load_col = [&](Tile& t) { t.jn = a.col[t.valid ? t.eid : 0]; };
+  auto load_rest = [&](const Tile& t, Ops& o) {
+    if (!t.has) return;
+    const unsigned char* ur = a.U + ((size_t)t.i * H2 + l32) * DL * 2 + hh * EPL * 2;
+    const unsigned char* hr = a.h_in + (size_t)t.jn * DL * 2;
+#pragma unroll
+    for (int s = 0; s < SKD; ++s) o.hB[s] = ld_frag<__bf16>(hr + (s * KS + hh * EPL) * 2);
+#pragma unroll
+    for (int q = 0; q < KTH; ++q)
+#pragma unroll
+      for (int s = 0; s < SKD; ++s)
+        o.UA[q][s] = ld_frag<__bf16>(ur + ((size_t)(hf * KTH + q) * 32 * DL + s * KS) * 2);
+    const size_t e = t.valid ? (size_t)t.eid : 0;
+    const uint32_t* mb = reinterpret_cast<const uint32_t*>(a.zmask + e * ((H1 + H2) / 8));
+#pragma unroll
+    for (int w = 0; w < MW1; ++w) o.m1[w] = mb[hh * MW1 + w];
+#pragma unroll
+    for (int w = 0; w < MW2; ++w) o.m2[w] = mb[2 * MW1 + hh * MW2 + w];
+    const int nw = g.dim + 1;
+    const float* vi = g.node_attr + (size_t)t.i * nw;
+    const float* vj = g.node_attr + (size_t)t.jn * nw;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int cc = c < nw ? c : nw - 1;   // in the row; unused past dim
+      o.ri[c] = vi[cc];
+      o.rj[c] = vj[cc];
+    }
+  };
+
+  // ---- dz part, first step: the half's k tiles of dz, its da2 columns, z1
+  // columns and (half 0) the split attribute row go into the pair's slot
+  frag da2B[SK2];
+  auto dz_part1 = [&](auto half, const Tile& t, Ops& o) {
+    constexpr int hf = decltype(half)::value;
+#pragma unroll
+    for (int s = 0; s < SKD; ++s)
+      if (!t.valid) o.hB[s] = frag{};
+    f32x16 acc[KTH];
+#pragma unroll
+    for (int q = 0; q < KTH; ++q) {
+      acc[q] = f32x16{};
+#pragma unroll
+      for (int s = 0; s < SKD; ++s) acc[q] = M::mma(o.UA[q][s], o.hB[s], acc[q]);
+    }
+    float x[8];
+    edge_attr_rows(o.ri, o.rj, g.dim, g.attr_mode, x);
+#pragma unroll
+    for (int c = 0; c < 8; ++c) x[c] = t.valid ? x[c] : 0.0f;
+    unsigned char* zrow = myslot + G::OZ1 + l32 * G::DA1P;
+#pragma unroll
+    for (int q = 0; q < SK1H; ++q) {
+      const int s = hf * SK1H + q;
+      float zv[EPL];
+#pragma unroll
+      for (int u = 0; u < EPL; ++u) {
+        const int n = s * EPL + u;
+        const float v = layer1_pre(w1h + n * 8, b1h[n], x);
+        zv[u] = v > 0.0f ? v : 0.0f;
+      }
+      *reinterpret_cast<frag*>(zrow + (s * KS + hh * EPL) * 2) = pack_frag<__bf16>(zv);
+    }
+    if (hf == 0) {
+      // columns 16hh .. 16hh+15: high parts (0..7), low parts (8..15), ones (16), zeros
+      float xv[16];
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const float hi = (float)(__bf16)x[c];
+        xv[c] = hh ? (c == 0 && t.valid ? 1.0f : 0.0f) : hi;
+        xv[8 + c] = hh ? 0.0f : x[c] - hi;
+      }
+      unsigned char* xrow = myslot + G::OXS + l32 * G::XSP + hh * 32;
+      *reinterpret_cast<frag*>(xrow) = pack_frag<__bf16>(xv);
+      *reinterpret_cast<frag*>(xrow + 16) = pack_frag<__bf16>(xv + 8);
+      if (lane == 0) slot_cnt[pr] = t.cnt;
+    }
+    // da2 = dz [z > 0] for the half's positions n = 16 kt + i (frags s = n / EPL)
+    unsigned char* d2row = myslot + l32 * G::DA2P;
+#pragma unroll
+    for (int q = 0; q < SK2H; ++q) {
+      const int s = hf * SK2H + q;
+      float v[EPL];
+#pragma unroll
+      for (int u = 0; u < EPL; ++u) {
+        const int n = s * EPL + u;
+        v[u] = (o.m2[n / 32] >> (n % 32)) & 1u ? acc[n / 16 - hf * KTH][n % 16] : 0.0f;
+      }
+      da2B[s] = pack_frag<__bf16>(v);
+      *reinterpret_cast<frag*>(d2row + (s * KS + hh * EPL) * 2) = da2B[s];
+    }
+  };
+  // ---- dz part, second step (da2 of the whole tile is in the slot): the
+  // half's j tiles of dz1 = W2^T da2 and da1 = dz1 [z1 > 0]
+  auto dz_part2 = [&](auto half, const Tile& t, const Ops& o) {
+    constexpr int hf = decltype(half)::value;
+    const unsigned char* d2row = myslot + l32 * G::DA2P;
+#pragma unroll
+    for (int q = 0; q < SK2H; ++q) {
+      const int s = (1 - hf) * SK2H + q;
+      da2B[s] = *reinterpret_cast<const frag*>(d2row + (s * KS + hh * EPL) * 2);
+    }
+    unsigned char* d1row = myslot + G::OD1 + l32 * G::DA1P;
+    const size_t e = t.valid ? (size_t)t.eid : 0;
+#pragma unroll
+    for (int q = 0; q < JTH; ++q) {
+      const int t1 = hf * JTH + q;
+      f32x16 C = f32x16{};
+#pragma unroll
+      for (int s = 0; s < SK2; ++s) {
+        frag A = ld_frag<__bf16>(w2s + (size_t)(t1 * 32 + l32) * G::W2P + (s * KS + hh * EPL) * 2);
+        C = M::mma(A, da2B[s], C);
+      }
+#pragma unroll
+      for (int i0 = 0; i0 < 16; i0 += EPL) {
+        const int n = 16 * t1 + i0;
+        const int pos = (n / EPL) * KS + hh * EPL;
+        float v[EPL];
+#pragma unroll
+        for (int u = 0; u < EPL; ++u) v[u] = (o.m1[(n + u) / 32] >> ((n + u) % 32)) & 1u ? C[i0 + u] : 0.0f;
+        const frag f = pack_frag<__bf16>(v);
+        *reinterpret_cast<frag*>(d1row + pos * 2) = f;
+        if (g.da1_out && t.valid) *reinterpret_cast<frag*>(g.da1_out + (e * H1 + pos) * 2) = f;
+      }
+    }
+  };
+
+  // ---- products over a round's slots
+  auto products = [&](int nslot) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      if (v < nslot) {
+        const unsigned char* st = slots + v * G::SLOT;
+        const int cnt = slot_cnt[v];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          if (ks * 16 < cnt) {
+            if (active) {
+              const frag Bz = lds_frag_rows(st + G::OZ1, G::DA1P, 16 * ks, 32 * jt);
+              frag A[G::TPW];
+#pragma unroll
+              for (int m = 0; m < G::TPW; ++m) A[m] = lds_frag_rows(st, G::DA2P, 16 * ks, 32 * kt_of(m));
+#pragma unroll
+              for (int m = 0; m < G::TPW; ++m) {
+                acc2[m] = M::mma(A[m], Bz, acc2[m]);
+                if (m == bm) {
+#pragma unroll
+                  for (int t = 0; t < 8; ++t) db2 += (float)A[m][t];
+                }
+              }
+            }
+            if (wv < JT) {
+              const frag A1 = lds_frag_rows(st + G::OD1, G::DA1P, 16 * ks, 32 * jt);
+              const frag Bx = lds_frag_rows(st + G::OXS, G::XSP, 16 * ks, 0);
+              acc1 = M::mma(A1, Bx, acc1);
+            }
+          }
+        }
+      }
+    }
+  };
+
+  // One round: the pair contracts its tile into the slot (two steps around
+  // an LDS barrier); the next round's operands go out into the same
+  // registers (its source index came a round earlier), the tile two rounds
+  // ahead takes the place of `cur` and its source index goes out; then the
+  // round's slots are contracted while those loads are in flight.
+  Ops op;
+  auto round = [&](int r0, Tile& cur, const Tile& nxt) {
+    if (cur.has) {
+      if (hf == 0) dz_part1(std::integral_constant<int, 0>{}, cur, op);
+      else dz_part1(std::integral_constant<int, 1>{}, cur, op);
+    }
+    lds_barrier();   // the pairs' da2 rows are complete
+    if (cur.has) {
+      if (hf == 0) dz_part2(std::integral_constant<int, 0>{}, cur, op);
+      else dz_part2(std::integral_constant<int, 1>{}, cur, op);
+    }
+    load_rest(nxt, op);
+    locate(r0 + 8 + pr, cur);
+    load_col(cur);
+    lds_barrier();   // the round's slots are complete
+    products(ntile - r0 < 4 ? ntile - r0 : 4);
+    lds_barrier();   // slots are free for the next round
+  };
+
+  const int64_t nblk = (a.n_dst + DZ_NB - 1) / DZ_NB;
+  for (int64_t blk = blockIdx.x; blk < nblk; blk += gridDim.x) {
+    d0 = (int)(blk * DZ_NB);
+    const int nd = (int)(a.n_dst - d0 < DZ_NB ? a.n_dst - d0 : DZ_NB);
+    if (wv == 0) {
+      int nt = 0, rp = 0;
+      if (lane <= nd) rp = a.row_ptr[d0 + lane];
+      if (lane < nd) nt = (a.row_ptr[d0 + lane + 1] - rp + 31) / 32;
+#pragma unroll
+      for (int o = 1; o < DZ_NB; o <<= 1) {
+        const int v = __shfl_up(nt, o, 64);
+        if (lane >= o) nt += v;
+      }
+      if (lane < DZ_NB) tstart[lane + 1] = nt;
+      if (lane == 0) tstart[0] = 0;
+      if (lane <= nd) rps[lane] = rp;
+    }
+    lds_barrier();
+    ntile = tstart[nd];
+    Tile tA, tB;
+    locate(pr, tA);
+    load_col(tA);
+    locate(4 + pr, tB);
+    load_col(tB);
+    load_rest(tA, op);
+    for (int r0 = 0; r0 < ntile; r0 += 8) {
+      round(r0, tA, tB);
+      if (r0 + 4 < ntile) round(r0 + 4, tB, tA);
+    }
+    lds_barrier();   // the block's lists are read until every wave is done
+  }
+  // ---- partial sums of this workgroup (stored positions mapped back to k, j)
+  float* o2 = g.p_w2 + (size_t)blockIdx.x * (H2 * H1 + H2);
+  if (active) {
+    const int j = kperm<__bf16>(jt * 32 + l32);
+#pragma unroll
+    for (int m = 0; m < G::TPW; ++m) {
+      const int kt = kt_of(m);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int k = kperm<__bf16>(kt * 32 + 8 * (i / 4) + 4 * hh + (i % 4));
+        o2[(size_t)k * H1 + j] = acc2[m][i];
+      }
+    }
+  }
+  {
+    const float bs = db2 + __shfl_xor(db2, 32, 64);
+    if (bm >= 0 && hh == 0) o2[H2 * H1 + kperm<__bf16>(kt_of(bm) * 32 + l32)] = bs;
+  }
+  if (wv < JT) {
+    float* o1 = g.p_w1 + (size_t)blockIdx.x * (H1 * g.de + H1);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float lo = __shfl_down(acc1[i], 8, 64);
+      const int jj = kperm<__bf16>(jt * 32 + 8 * (i / 4) + 4 * hh + (i % 4));
+      if (l32 < g.de) o1[(size_t)jj * g.de + l32] = acc1[i] + lo;
+      if (l32 == 16) o1[(size_t)H1 * g.de + jj] = acc1[i];
+    }
   }
 }
 
@@ -1433,6 +1802,48 @@ dsmp_status dispatch_edge_grads(dsmp_handle* h, const dsmp_layer_desc& d, const 
   return fail(h, DSMP_UNSUPPORTED, "unsupported layer shape");
 }
 
+// Aggregate form, bf16, h1 = h2 <= 128: U = g W3 for every destination, then
+// one fused pass for dz, da2, da1 and the dW2/db2/dW1/db1 partial sums
+// (one partial per workgroup, at most cap workgroups).
+bool fused_edge_grads(const dsmp_layer_desc& d) {
+  return d.dtype == DSMP_BF16 && d.h1 == d.h2 && (d.h1 == 64 || d.h1 == 128) && (d.d == 32 || d.d == 64);
+}
+
+template <int DL, int H1, int H2>
+dsmp_status run_edge_grads_fused(dsmp_handle* h, const EdgeGradArgs& eg, int cap, int* nchunk) {
+  hipStream_t s = h->stream;
+  const DzArgs& dz = eg.dz;
+  {
+    ProfScope prof(h, DSMP_K_U_GEMM);
+    UArgs ua{dz.n_dst, dz.gT, dz.packed + dz.L.w3u, const_cast<unsigned char*>(dz.U)};
+    hipLaunchKernelGGL((k_u_gemm<__bf16, DL, H2>),
+                       dim3((unsigned)ceil_div(dz.n_dst, 32), (unsigned)ceil_div(H2 * DL, 1024)), dim3(256), 0, s, ua);
+    DSMP_LAUNCHED(h, "U GEMM");
+  }
+  using G = EdgeGradShape<DL, H1, H2>;
+  auto kf = k_bwd_edge_agg<DL, H1, H2>;
+  dsmp_status st = set_lds(h, kf, G::LDS);
+  if (st != DSMP_OK) return st;
+  int per_cu = 0;
+  DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kf, G::NT, G::LDS));
+  int64_t grid = std::min<int64_t>((dz.n_dst + DZ_NB - 1) / DZ_NB, (int64_t)h->n_cu * std::max(per_cu, 1));
+  grid = std::max<int64_t>(1, std::min<int64_t>(grid, cap));
+  ProfScope prof(h, DSMP_K_DZ);
+  hipLaunchKernelGGL(kf, dim3((unsigned)grid), dim3(G::NT), G::LDS, s, eg);
+  DSMP_LAUNCHED(h, "fused edge gradients");
+  *nchunk = (int)grid;
+  return DSMP_OK;
+}
+
+dsmp_status dispatch_edge_grads_fused(dsmp_handle* h, const dsmp_layer_desc& d, const EdgeGradArgs& eg, int cap,
+                                      int* nchunk) {
+  if (d.d == 32 && d.h1 == 64) return run_edge_grads_fused<32, 64, 64>(h, eg, cap, nchunk);
+  if (d.d == 64 && d.h1 == 64) return run_edge_grads_fused<64, 64, 64>(h, eg, cap, nchunk);
+  if (d.d == 32 && d.h1 == 128) return run_edge_grads_fused<32, 128, 128>(h, eg, cap, nchunk);
+  if (d.d == 64 && d.h1 == 128) return run_edge_grads_fused<64, 128, 128>(h, eg, cap, nchunk);
+  return fail(h, DSMP_UNSUPPORTED, "unsupported layer shape for the fused edge gradients");
+}
+
 template <typename T, int DL>
 void launch_node_kernels(dsmp_handle* h, const BNodeArgs& na, int64_t n_dst, const BwdWs& w,
                          const unsigned char* h_in, const int32_t* row_ptr, const int32_t* col, bool db3) {
@@ -1547,7 +1958,13 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   }
 
   // kernel-MLP gradients
-  if (E > 0) {
+  int nfused = 0;   // workgroups of the fused edge-gradient pass (their partials replace dW2's and dW1's)
+  if (E > 0 && agg && fused_edge_grads(d)) {
+    DzArgs dz{E, g->col, g->dst, hin, w.gF, pk, L, sv + sl.zE, sv + sl.zmask, w.da2E, w.da1E,
+              w.U, w.gT, n_dst, g->row_ptr};
+    EdgeGradArgs eg{dz, node_attr, d.dim, d.attr_mode, de, grads->dattr ? w.da1E : nullptr, w.p_w2, w.p_w1};
+    if ((st = dispatch_edge_grads_fused(h, d, eg, std::min(w.n2, w.n1), &nfused)) != DSMP_OK) return st;
+  } else if (E > 0) {
     DzArgs dz{E, g->col, g->dst, hin, w.gF, pk, L, sv + sl.zE, sv + sl.zmask, w.da2E, w.da1E,
               agg ? w.U : nullptr, w.gT, n_dst, g->row_ptr};
     W3Args w3{E, w.pc3, agg ? 0 : w.n3, g->col, g->dst, hin, w.gF, sv + sl.zE, w.p_w3};
@@ -1610,8 +2027,8 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   };
   const int64_t dd = (int64_t)d.d * d.d;
   const int n3 = E > 0 && !agg ? w.n3 : 0;
-  const int n2 = E > 0 ? (int)((E + w.pc2 - 1) / w.pc2) : 0;
-  const int n1 = E > 0 ? (int)((E + w.pc1 - 1) / w.pc1) : 0;
+  const int n2 = nfused ? nfused : E > 0 ? (int)((E + w.pc2 - 1) / w.pc2) : 0;
+  const int n1 = nfused ? nfused : E > 0 ? (int)((E + w.pc1 - 1) / w.pc1) : 0;
   const int nr = n_dst > 0 ? w.nr : 0;
   ProfScope prof_red(h, DSMP_K_REDUCE);
   red(w.p_root, nr, dd + d.d, 0, dd, grads->dWr);
