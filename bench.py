@@ -109,9 +109,11 @@ def gemm_slices(n_rows):
     return max(1, min(16, 2048 // waves))
 
 
-def work_model(w, E, n_src):
+def work_model(w, E, n_src, fused=False):
     """Algorithmic work of one launch of each kernel class: flops and the
-    compulsory HBM bytes (every input read once, every output written once)."""
+    compulsory HBM bytes (every input read once, every output written once).
+    With ``fused`` (the one-pass edge gradients) the kernel-MLP pass stores z
+    and the mask bits only: the backward recomputes z1."""
     d, H1, H2, de, D = w.d, w.H1, w.H2, w.de, w.D
     n = w.n_dst
     esz = 2 if w.dtype == "bf16" else 4
@@ -125,7 +127,7 @@ def work_model(w, E, n_src):
                      E * (idx + attr + d * esz + (H1 + H2) * esz + mask) + n * d * 4),
         "edge_dh": (2 * E * (H2 + 1) * d * d, E * (idx + d * esz + H2 * esz) + n_src * d * 4),
         # aggregate form
-        "edge_mlp": (2 * E * (de * H1 + H1 * H2), E * (idx + attr + (H1 + H2) * esz + mask)),
+        "edge_mlp": (2 * E * (de * H1 + H1 * H2), E * (idx + attr + (H2 if fused else H1 + H2) * esz + mask)),
         "outer_fwd": (2 * E * H2 * d, E * (4 + H2 * esz + d * esz) + n * kt * esz),
         "gemm_fwd": (2 * n * kt * d, n * kt * esz + gemm_slices(n) * n * d * 4),
         "outer_dh": (2 * E * H2 * d, E * (idx + H2 * esz + d * esz) + n_src * kt * esz),
@@ -398,8 +400,8 @@ def main():
     if hop:   # the layer of the hop loop reads difference attributes (dim+1 per edge)
         import dataclasses
         w = dataclasses.replace(w, de=w.D + 1)
-    work = work_model(w, E, w.n_src)
     fused = agg and not ("dW2" in prof and prof["dW2"][1] > 0)
+    work = work_model(w, E, w.n_src, fused)
     work.update(agg_work(w, E, w.n_src, fused) if agg else per_edge_work(w, E, w.n_src))
     kernels = {}
     for name, (tot, n) in prof.items():

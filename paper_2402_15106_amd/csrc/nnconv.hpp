@@ -310,6 +310,11 @@ dsmp_status check_layer_desc(dsmp_handle* h, const dsmp_layer_desc* d);
 dsmp_status check_graph(dsmp_handle* h, const dsmp_graph* g, bool need_csc);
 int layer_attr_width(const dsmp_layer_desc& d);
 
+// Whether the backward of an aggregate-form layer runs the fused edge-gradient
+// pass (bf16, h1 = h2 in {64, 128}, d in {32, 64}).  That pass recomputes z1
+// and the edge attributes, so the forward then stores neither.
+bool fused_edge_grads(const dsmp_layer_desc& d);
+
 // Aggregate form of the edge contraction (nnconv_agg.hip).
 bool use_aggregate(const dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_dst, int64_t E);
 int64_t agg_ktot(const dsmp_layer_desc& d);

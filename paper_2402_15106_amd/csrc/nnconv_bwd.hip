@@ -483,11 +483,14 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 3 : 1) v
 // A workgroup of eight waves takes four tiles per round; the two waves of a
 // pair share one tile and its LDS slot (dz split by k tiles, dz1 by j tiles,
 // the z1 row by halves).  The slot receives the tile's rows of da2, da1 and
-// z1 and its split attributes; z1 is recomputed from the attributes with the
-// forward's own multiply-add chain, so it is the forward's value bit for bit.
-// The attributes enter dW1 as bf16 high and low parts (columns 0..7 and
-// 8..15, about 16 significant bits together) next to a column of ones (16)
-// that gives db1; db2 sums the da2 fragments of the products.  After a
+// z1 and its split attributes.  z1 = ReLU(W1 x + b1) is recomputed on the
+// matrix cores from bf16 high and low parts, W1h xh + W1h xl + W1l xh + b1h
+// + b1l with fp32 accumulation: within about 2^-16 of the forward's fp32
+// value, far inside the bf16 rounding that z1 and da2 then take, and a ReLU
+// decision can only differ where z1 is about zero.  The attributes enter dW1
+// the same way (high parts in columns 0..7, low parts in 8..15) next to a
+// column of ones (16) that gives db1; db2 sums the da2 fragments of the
+// products.  After a
 // barrier the four slots are contracted over their edges with transposing
 // LDS reads, each wave taking its share of the dW2 tiles.  While those
 // products run, the loads of the wave's next tile are in flight (its source
@@ -532,6 +535,7 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
   constexpr int KS = S::KS, EPL = S::EPL, KT = S::KT, SKD = S::SKD, SK2 = S::SK2, JT = S::JT;
   constexpr int SK1 = H1 / KS, MW1 = H1 / 64, MW2 = H2 / 64;
   constexpr int KTH = KT / 2, JTH = JT / 2, SK1H = SK1 / 2, SK2H = SK2 / 2;   // per half of a pair
+  constexpr int ZB = SK1H / 2;   // 32-row blocks of z1 per half
   const DzArgs& a = g.dz;
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* w2s = smem;
@@ -564,8 +568,33 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
   __shared__ int tstart[DZ_NB + 1], rps[DZ_NB + 1];
   __shared__ int slot_cnt[4];
   unsigned char* myslot = slots + pr * G::SLOT;
-  const float* w1h = w1s + hh * (H1 / 2) * 8;
-  const float* b1h = w1s + H1 * 8 + hh * (H1 / 2);
+  // A operands of the z1 product, built each round from the fp32 weights in
+  // LDS: row R of block zb holds the layer-1 weights of stored position
+  // (hf*SK1H + 2zb + i/8)*16 + hh'*8 + i%8 with R = 8(i/4) + 4hh' + i%4; K
+  // slots 0..7 W1h, 8..15 W1h, 16..23 W1l, 24 b1h, 25 b1l
+  auto w1_frags = [&](int zb, frag& f0, frag& f1) {
+    const int R = l32, i = 4 * (R / 8) + R % 4, hr = (R % 8) / 4;
+    const int pos = (hf * SK1H + 2 * zb + i / 8) * KS + hr * EPL + i % 8;
+    const int hn = ((pos % KS) / EPL) * (H1 / 2) + (pos / KS) * EPL + pos % EPL;
+    const f32x4 wa = *reinterpret_cast<const f32x4*>(w1s + hn * 8);
+    const f32x4 wb = *reinterpret_cast<const f32x4*>(w1s + hn * 8 + 4);
+    const float wv[8] = {wa[0], wa[1], wa[2], wa[3], wb[0], wb[1], wb[2], wb[3]};
+    const float bb = w1s[H1 * 8 + hn];
+    float v0[8], v1[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const float whi = (float)(__bf16)wv[c];
+      v0[c] = whi;                        // slots 0..7 (times xh) and 8..15 (times xl)
+      v1[c] = hh ? 0.0f : wv[c] - whi;    // slots 16..23 (times xh)
+    }
+    if (hh) {
+      const float bhi = (float)(__bf16)bb;
+      v1[0] = bhi;
+      v1[1] = bb - bhi;
+    }
+    f0 = pack_frag<__bf16>(v0);
+    f1 = pack_frag<__bf16>(v1);
+  };
 
   // a tile of the current block: destination, first edge, the lane's edge
   struct Tile {
@@ -584,8 +613,9 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
     t.has = tau < ntile;
     t.i = d0; t.c0 = 0; t.eid = 0; t.cnt = 0; t.valid = false;
     if (!t.has) return;
-    int k = 0;
-    while (tstart[k + 1] <= tau) ++k;
+    // destination of tile tau: the number of tile-list starts at or below it, minus one
+    const int ts = lane < DZ_NB ? tstart[lane + 1] : 0x7fffffff;
+    const int k = __popcll(__ballot(ts <= tau));
     const int pa = rps[k], pb = rps[k + 1];
     t.i = d0 + k;
     t.c0 = pa + (tau - tstart[k]) * 32;
@@ -596,9 +626,12 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
   // Loads are unconditional (lanes past the tile read edge 0) so that no
   // select waits on them; the dz part zeroes those lanes.
   auto load_col = [&](Tile& t) { t.jn = a.col[t.valid ? t.eid : 0]; };
-  auto load_rest = [&](const Tile& t, Ops& o) {
+  // the gathered row and the half's rows of U_i (issued as soon as the
+  // previous tile's products have read those registers) ...
+  auto load_uh = [&](const Tile& t, Ops& o) {
     if (!t.has) return;
-    const unsigned char* ur = a.U + ((size_t)t.i * H2 + l32) * DL * 2 + hh * EPL * 2;
+    const int i = __builtin_amdgcn_readfirstlane(t.i);   // one destination per tile
+    const unsigned char* ur = a.U + ((size_t)i * H2 + l32) * DL * 2 + hh * EPL * 2;
     const unsigned char* hr = a.h_in + (size_t)t.jn * DL * 2;
 #pragma unroll
     for (int s = 0; s < SKD; ++s) o.hB[s] = ld_frag<__bf16>(hr + (s * KS + hh * EPL) * 2);
@@ -607,14 +640,15 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
 #pragma unroll
       for (int s = 0; s < SKD; ++s)
         o.UA[q][s] = ld_frag<__bf16>(ur + ((size_t)(hf * KTH + q) * 32 * DL + s * KS) * 2);
-    const size_t e = t.valid ? (size_t)t.eid : 0;
-    const uint32_t* mb = reinterpret_cast<const uint32_t*>(a.zmask + e * ((H1 + H2) / 8));
-#pragma unroll
-    for (int w = 0; w < MW1; ++w) o.m1[w] = mb[hh * MW1 + w];
-#pragma unroll
-    for (int w = 0; w < MW2; ++w) o.m2[w] = mb[2 * MW1 + hh * MW2 + w];
+  };
+  // ... the node attribute rows and z's mask bits (after their use in the
+  // first step) and z1's mask bits (after the second step); each load goes
+  // out once its registers are free
+  auto load_attr = [&](const Tile& t, Ops& o) {
+    if (!t.has) return;
     const int nw = g.dim + 1;
-    const float* vi = g.node_attr + (size_t)t.i * nw;
+    const int i = __builtin_amdgcn_readfirstlane(t.i);
+    const float* vi = g.node_attr + (size_t)i * nw;
     const float* vj = g.node_attr + (size_t)t.jn * nw;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
@@ -623,12 +657,81 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
       o.rj[c] = vj[cc];
     }
   };
+  auto load_m2 = [&](const Tile& t, Ops& o) {
+    if (!t.has) return;
+    const size_t e = t.valid ? (size_t)t.eid : 0;
+    const uint32_t* mb = reinterpret_cast<const uint32_t*>(a.zmask + e * ((H1 + H2) / 8));
+#pragma unroll
+    for (int w = 0; w < MW2; ++w) o.m2[w] = mb[2 * MW1 + hh * MW2 + w];
+  };
+  auto load_m1 = [&](const Tile& t, Ops& o) {
+    if (!t.has) return;
+    const size_t e = t.valid ? (size_t)t.eid : 0;
+    const uint32_t* mb = reinterpret_cast<const uint32_t*>(a.zmask + e * ((H1 + H2) / 8));
+#pragma unroll
+    for (int w = 0; w < MW1; ++w) o.m1[w] = mb[hh * MW1 + w];
+  };
 
   // ---- dz part, first step: the half's k tiles of dz, its da2 columns, z1
   // columns and (half 0) the split attribute row go into the pair's slot
   frag da2B[SK2];
-  auto dz_part1 = [&](auto half, const Tile& t, Ops& o) {
+  auto dz_part1 = [&](auto half, const Tile& t, const Tile& nxt, Ops& o) {
     constexpr int hf = decltype(half)::value;
+    float x[8];
+    edge_attr_rows(o.ri, o.rj, g.dim, g.attr_mode, x);
+#pragma unroll
+    for (int c = 0; c < 8; ++c) x[c] = t.valid ? x[c] : 0.0f;
+    float xh[8], xl[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      xh[c] = (float)(__bf16)x[c];
+      xl[c] = x[c] - xh[c];
+    }
+    // z1 of the half's 32-row blocks on MFMA: B = [xh | xl | xh | 1 1 0..]
+    // (lane = edge), A = the rows prepared in w1A; rows of block zb are the
+    // stored positions of z1 frags s = hf*SK1H + 2zb + i/8 (half hh, element i%8)
+    {
+      frag xb0, xb1;
+      float v0[8], v1[8];
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        v0[c] = hh ? xl[c] : xh[c];
+        v1[c] = hh ? (c < 2 ? 1.0f : 0.0f) : xh[c];
+      }
+      xb0 = pack_frag<__bf16>(v0);
+      xb1 = pack_frag<__bf16>(v1);
+      unsigned char* zrow = myslot + G::OZ1 + l32 * G::DA1P;
+#pragma unroll
+      for (int zb = 0; zb < ZB; ++zb) {
+        frag w0, w1;
+        w1_frags(zb, w0, w1);
+        f32x16 Z = f32x16{};
+        Z = M::mma(w0, xb0, Z);
+        Z = M::mma(w1, xb1, Z);
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int s = hf * SK1H + 2 * zb + q;
+          float zv[EPL];
+#pragma unroll
+          for (int u = 0; u < EPL; ++u) zv[u] = Z[8 * q + u] > 0.0f ? Z[8 * q + u] : 0.0f;
+          *reinterpret_cast<frag*>(zrow + (s * KS + hh * EPL) * 2) = pack_frag<__bf16>(zv);
+        }
+      }
+    }
+    if (hf == 0) {
+      // columns 16hh .. 16hh+15: high parts (0..7), low parts (8..15), ones (16), zeros
+      float xv[16];
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        xv[c] = hh ? (c == 0 && t.valid ? 1.0f : 0.0f) : xh[c];
+        xv[8 + c] = hh ? 0.0f : xl[c];
+      }
+      unsigned char* xrow = myslot + G::OXS + l32 * G::XSP + hh * 32;
+      *reinterpret_cast<frag*>(xrow) = pack_frag<__bf16>(xv);
+      *reinterpret_cast<frag*>(xrow + 16) = pack_frag<__bf16>(xv + 8);
+      if (lane == 0) slot_cnt[pr] = t.cnt;
+    }
+    load_attr(nxt, o);   // the attribute rows have been used
 #pragma unroll
     for (int s = 0; s < SKD; ++s)
       if (!t.valid) o.hB[s] = frag{};
@@ -639,37 +742,7 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
 #pragma unroll
       for (int s = 0; s < SKD; ++s) acc[q] = M::mma(o.UA[q][s], o.hB[s], acc[q]);
     }
-    float x[8];
-    edge_attr_rows(o.ri, o.rj, g.dim, g.attr_mode, x);
-#pragma unroll
-    for (int c = 0; c < 8; ++c) x[c] = t.valid ? x[c] : 0.0f;
-    unsigned char* zrow = myslot + G::OZ1 + l32 * G::DA1P;
-#pragma unroll
-    for (int q = 0; q < SK1H; ++q) {
-      const int s = hf * SK1H + q;
-      float zv[EPL];
-#pragma unroll
-      for (int u = 0; u < EPL; ++u) {
-        const int n = s * EPL + u;
-        const float v = layer1_pre(w1h + n * 8, b1h[n], x);
-        zv[u] = v > 0.0f ? v : 0.0f;
-      }
-      *reinterpret_cast<frag*>(zrow + (s * KS + hh * EPL) * 2) = pack_frag<__bf16>(zv);
-    }
-    if (hf == 0) {
-      // columns 16hh .. 16hh+15: high parts (0..7), low parts (8..15), ones (16), zeros
-      float xv[16];
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const float hi = (float)(__bf16)x[c];
-        xv[c] = hh ? (c == 0 && t.valid ? 1.0f : 0.0f) : hi;
-        xv[8 + c] = hh ? 0.0f : x[c] - hi;
-      }
-      unsigned char* xrow = myslot + G::OXS + l32 * G::XSP + hh * 32;
-      *reinterpret_cast<frag*>(xrow) = pack_frag<__bf16>(xv);
-      *reinterpret_cast<frag*>(xrow + 16) = pack_frag<__bf16>(xv + 8);
-      if (lane == 0) slot_cnt[pr] = t.cnt;
-    }
+    load_uh(nxt, o);   // the products above have read these registers
     // da2 = dz [z > 0] for the half's positions n = 16 kt + i (frags s = n / EPL)
     unsigned char* d2row = myslot + l32 * G::DA2P;
 #pragma unroll
@@ -684,10 +757,11 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
       da2B[s] = pack_frag<__bf16>(v);
       *reinterpret_cast<frag*>(d2row + (s * KS + hh * EPL) * 2) = da2B[s];
     }
+    load_m2(nxt, o);   // z's mask bits have been used
   };
   // ---- dz part, second step (da2 of the whole tile is in the slot): the
   // half's j tiles of dz1 = W2^T da2 and da1 = dz1 [z1 > 0]
-  auto dz_part2 = [&](auto half, const Tile& t, const Ops& o) {
+  auto dz_part2 = [&](auto half, const Tile& t, const Tile& nxt, Ops& o) {
     constexpr int hf = decltype(half)::value;
     const unsigned char* d2row = myslot + l32 * G::DA2P;
 #pragma unroll
@@ -718,6 +792,7 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
         if (g.da1_out && t.valid) *reinterpret_cast<frag*>(g.da1_out + (e * H1 + pos) * 2) = f;
       }
     }
+    load_m1(nxt, o);   // z1's mask bits have been used
   };
 
   // ---- products over a round's slots
@@ -756,22 +831,28 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
   };
 
   // One round: the pair contracts its tile into the slot (two steps around
-  // an LDS barrier); the next round's operands go out into the same
-  // registers (its source index came a round earlier), the tile two rounds
-  // ahead takes the place of `cur` and its source index goes out; then the
-  // round's slots are contracted while those loads are in flight.
+  // an LDS barrier).  The next round's operands go out into the same
+  // registers as soon as they are free (its source index came a round
+  // earlier), the tile two rounds ahead takes the place of `cur` and its
+  // source index goes out; then the round's slots are contracted while
+  // those loads are in flight.
   Ops op;
   auto round = [&](int r0, Tile& cur, const Tile& nxt) {
     if (cur.has) {
-      if (hf == 0) dz_part1(std::integral_constant<int, 0>{}, cur, op);
-      else dz_part1(std::integral_constant<int, 1>{}, cur, op);
+      if (hf == 0) dz_part1(std::integral_constant<int, 0>{}, cur, nxt, op);
+      else dz_part1(std::integral_constant<int, 1>{}, cur, nxt, op);
+    } else {
+      load_attr(nxt, op);
+      load_uh(nxt, op);
+      load_m2(nxt, op);
     }
     lds_barrier();   // the pairs' da2 rows are complete
     if (cur.has) {
-      if (hf == 0) dz_part2(std::integral_constant<int, 0>{}, cur, op);
-      else dz_part2(std::integral_constant<int, 1>{}, cur, op);
+      if (hf == 0) dz_part2(std::integral_constant<int, 0>{}, cur, nxt, op);
+      else dz_part2(std::integral_constant<int, 1>{}, cur, nxt, op);
+    } else {
+      load_m1(nxt, op);
     }
-    load_rest(nxt, op);
     locate(r0 + 8 + pr, cur);
     load_col(cur);
     lds_barrier();   // the round's slots are complete
@@ -803,7 +884,10 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
     load_col(tA);
     locate(4 + pr, tB);
     load_col(tB);
-    load_rest(tA, op);
+    load_uh(tA, op);
+    load_attr(tA, op);
+    load_m2(tA, op);
+    load_m1(tA, op);
     for (int r0 = 0; r0 < ntile; r0 += 8) {
       round(r0, tA, tB);
       if (r0 + 4 < ntile) round(r0 + 4, tB, tA);
@@ -1805,10 +1889,6 @@ dsmp_status dispatch_edge_grads(dsmp_handle* h, const dsmp_layer_desc& d, const 
 // Aggregate form, bf16, h1 = h2 <= 128: U = g W3 for every destination, then
 // one fused pass for dz, da2, da1 and the dW2/db2/dW1/db1 partial sums
 // (one partial per workgroup, at most cap workgroups).
-bool fused_edge_grads(const dsmp_layer_desc& d) {
-  return d.dtype == DSMP_BF16 && d.h1 == d.h2 && (d.h1 == 64 || d.h1 == 128) && (d.d == 32 || d.d == 64);
-}
-
 template <int DL, int H1, int H2>
 dsmp_status run_edge_grads_fused(dsmp_handle* h, const EdgeGradArgs& eg, int cap, int* nchunk) {
   hipStream_t s = h->stream;
@@ -1859,6 +1939,12 @@ void launch_node_kernels(dsmp_handle* h, const BNodeArgs& na, int64_t n_dst, con
 }
 
 }  // namespace
+
+namespace dsmp {
+bool fused_edge_grads(const dsmp_layer_desc& d) {
+  return d.dtype == DSMP_BF16 && d.h1 == d.h2 && (d.h1 == 64 || d.h1 == 128) && (d.d == 32 || d.d == 64);
+}
+}  // namespace dsmp
 
 extern "C" dsmp_status dsmp_nnconv_workspace(const dsmp_layer_desc* desc, const dsmp_graph* g,
                                              size_t* saved_bytes, size_t* fwd_ws, size_t* bwd_ws) {

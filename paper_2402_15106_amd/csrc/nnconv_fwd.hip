@@ -779,6 +779,7 @@ extern "C" dsmp_status dsmp_nnconv_forward(dsmp_handle* h, const dsmp_layer_desc
   ea.packed = static_cast<const unsigned char*>(packed); ea.L = L;
   ea.zE = sv + sl.zE; ea.z1E = sv + sl.z1E; ea.zmask = sv + sl.zmask;
   ea.xE = d.dtype == DSMP_BF16 ? sv + sl.xE : nullptr;
+  if (agg && fused_edge_grads(d)) ea.z1E = ea.xE = nullptr;   // the backward recomputes both
   ea.out_direct = direct; ea.out_part = part;
   if (agg) {
     // z and z1 per edge, the per-destination sums S (kept for the backward),
