@@ -490,11 +490,11 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 3 : 1) v
 // decision can only differ where z1 is about zero.  The attributes enter dW1
 // the same way (high parts in columns 0..7, low parts in 8..15) next to a
 // column of ones (16) that gives db1; db2 sums the da2 fragments of the
-// products.  After a
-// barrier the four slots are contracted over their edges with transposing
-// LDS reads, each wave taking its share of the dW2 tiles.  While those
-// products run, the loads of the wave's next tile are in flight (its source
-// index one round earlier still); the barriers order LDS traffic only.
+// products.  After a barrier the four slots are contracted over their edges
+// with transposing LDS reads, each wave taking its share of the dW2 tiles.
+// Each load of the wave's next tile goes out as soon as its registers are
+// free (its source index one round earlier still), so they are in flight
+// while the products run; the barriers order LDS traffic only.
 // Partial sums go to slot blockIdx.x of the dW2/db2 and dW1/db1 partial
 // buffers, summed later in a fixed order.
 struct EdgeGradArgs {
