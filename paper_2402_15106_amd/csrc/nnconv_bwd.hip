@@ -932,74 +932,90 @@ struct UArgs {
 };
 
 // U[i][c] = sum_q W[c][q] g_i[q] for c = k*DL + p, as tiles C[c][i] (A = W
-// rows, B = the g rows, lane = destination).  A wave covers 32 destinations
-// and 256 columns; four 32x32 tiles at a time are collected in a per-wave LDS
-// block [destination][128 columns], which is then stored by rows of 128
-// columns (whole cache lines).
+// rows, B = the g rows, lane = destination).  A workgroup owns CB
+// consecutive columns (one or two 32-column tiles per wave, whose W rows stay
+// in registers for the whole launch) and a range of destinations, taken 32
+// at a time: the products land in an LDS block [32 destinations][CB columns]
+// (two buffers, one barrier per step) that is stored by whole 512-byte row
+// pieces.
 template <typename T, int DL, int H2>
 struct UShape {
-  static constexpr int ESZ = sizeof(T), FC = 128;          // columns per flush
-  static constexpr int TROW = FC * ESZ + 16;               // LDS row pitch (bytes)
-  static constexpr int WAVE = 32 * TROW;
+  static constexpr int ESZ = sizeof(T), CB = 512 / ESZ;    // 256 bf16 or 128 fp32 columns
+  static constexpr int TPW = CB / 128;                     // column tiles per wave
+  static constexpr int TROW = CB * ESZ + 16;               // LDS row pitch (bytes)
+  static constexpr int BUF = 32 * TROW;
 };
 
 template <typename T, int DL, int H2>
-__global__ __launch_bounds__(256) void k_u_gemm(UArgs a) {
+__global__ __launch_bounds__(256) void k_u_gemm(UArgs a, int64_t rows_per_wg) {
   using M = MT<T>;
   using frag = typename M::frag;
   using US = UShape<T, DL, H2>;
   constexpr int KS = M::KS, EPL = M::EPL, ESZ = sizeof(T), SKD = DL / KS, NC = H2 * DL, TROW = US::TROW;
-  __shared__ __align__(16) unsigned char sq[4][US::WAVE];
+  constexpr int CB = US::CB, CH = CB * ESZ / 16;          // columns, 16-byte units of an LDS row
+  __shared__ __align__(16) unsigned char sq[2][US::BUF];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
-  const int64_t i0 = (int64_t)blockIdx.x * 32;
-  const int64_t c0 = ((int64_t)blockIdx.y * 4 + wv) * 256;
-  if (c0 >= NC) return;
-  const int64_t row = i0 + l32 < a.n_rows ? i0 + l32 : a.n_rows - 1;
-  frag B[SKD];
+  const int64_t cb0 = (int64_t)blockIdx.x * CB;
+  const int64_t i_begin = (int64_t)blockIdx.y * rows_per_wg;
+  const int64_t i_end = i_begin + rows_per_wg < a.n_rows ? i_begin + rows_per_wg : a.n_rows;
+  frag A[US::TPW][SKD];
 #pragma unroll
-  for (int s = 0; s < SKD; ++s) B[s] = ld_frag<T>(a.G + ((size_t)row * DL + s * KS + hh * EPL) * ESZ);
-  unsigned char* t = sq[wv];
-  constexpr int CH = US::FC * ESZ / 16;                    // 16-byte chunks per LDS row
-  // the next column tile's W rows are in flight while this tile is multiplied and stored
-  frag An[SKD];
+  for (int m = 0; m < US::TPW; ++m)
 #pragma unroll
-  for (int s = 0; s < SKD; ++s) An[s] = ld_frag<T>(a.W + ((size_t)(c0 + l32) * DL + s * KS + hh * EPL) * ESZ);
-#pragma unroll 2
-  for (int ct = 0; ct < 8; ++ct) {
-    const int64_t c = c0 + ct * 32;
-    frag A[SKD];
+    for (int s = 0; s < SKD; ++s)
+      A[m][s] = ld_frag<T>(a.W + ((size_t)(cb0 + (wv * US::TPW + m) * 32 + l32) * DL + s * KS + hh * EPL) * ESZ);
+  int buf = 0;
+  for (int64_t i0 = i_begin; i0 < i_end; i0 += 32, buf ^= 1) {
+    const int64_t row = i0 + l32 < i_end ? i0 + l32 : i_end - 1;
+    frag B[SKD];
 #pragma unroll
-    for (int s = 0; s < SKD; ++s) A[s] = An[s];
-    if (ct + 1 < 8)
+    for (int s = 0; s < SKD; ++s) B[s] = ld_frag<T>(a.G + ((size_t)row * DL + s * KS + hh * EPL) * ESZ);
+    unsigned char* t = sq[buf];
 #pragma unroll
-      for (int s = 0; s < SKD; ++s) An[s] = ld_frag<T>(a.W + ((size_t)(c + 32 + l32) * DL + s * KS + hh * EPL) * ESZ);
-    f32x16 C = f32x16{};
+    for (int m = 0; m < US::TPW; ++m) {
+      f32x16 C = f32x16{};
 #pragma unroll
-    for (int s = 0; s < SKD; ++s) C = M::mma(A[s], B[s], C);
-    // LDS row = destination (lane), columns 32 (ct % 4) + 8(r/4) + 4hh + r%4
+      for (int s = 0; s < SKD; ++s) C = M::mma(A[m][s], B[s], C);
+      // LDS row = destination (lane), columns 32 (wave tile) + 8(r/4) + 4hh + r%4
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      unsigned char* o = t + l32 * TROW + (32 * (ct % 4) + 8 * g + 4 * hh) * ESZ;
-      if constexpr (ESZ == 2) {
-        const bf16x2 lo = __builtin_convertvector((f32x2){C[4 * g], C[4 * g + 1]}, bf16x2);
-        const bf16x2 hi = __builtin_convertvector((f32x2){C[4 * g + 2], C[4 * g + 3]}, bf16x2);
-        *reinterpret_cast<uint2*>(o) = make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
-      } else {
-        *reinterpret_cast<f32x4*>(o) = f32x4{C[4 * g], C[4 * g + 1], C[4 * g + 2], C[4 * g + 3]};
+      for (int g = 0; g < 4; ++g) {
+        unsigned char* o = t + l32 * TROW + (32 * (wv * US::TPW + m) + 8 * g + 4 * hh) * ESZ;
+        if constexpr (ESZ == 2) {
+          const bf16x2 lo = __builtin_convertvector((f32x2){C[4 * g], C[4 * g + 1]}, bf16x2);
+          const bf16x2 hi = __builtin_convertvector((f32x2){C[4 * g + 2], C[4 * g + 3]}, bf16x2);
+          *reinterpret_cast<uint2*>(o) = make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+        } else {
+          *reinterpret_cast<f32x4*>(o) = f32x4{C[4 * g], C[4 * g + 1], C[4 * g + 2], C[4 * g + 3]};
+        }
       }
     }
-    if (ct % 4 == 3) {
-      const int64_t cf = c - 96;   // first column of this flush
-      __builtin_amdgcn_wave_barrier();
+    __syncthreads();   // the block is complete; the other buffer's stores are done
 #pragma unroll
-      for (int it = 0; it < 32 * CH / 64; ++it) {
-        const int id = it * 64 + lane, r = id / CH, ch = id % CH;
-        const uint4 v = *reinterpret_cast<const uint4*>(t + r * TROW + ch * 16);
-        if (i0 + r < a.n_rows) *reinterpret_cast<uint4*>(a.U + ((size_t)(i0 + r) * NC + cf) * ESZ + ch * 16) = v;
-      }
-      __builtin_amdgcn_wave_barrier();
+    for (int it = 0; it < 32 * CH / 256; ++it) {
+      const int id = it * 256 + tid, r = id / CH, ch = id % CH;
+      const uint4 v = *reinterpret_cast<const uint4*>(t + r * TROW + ch * 16);
+      if (i0 + r < i_end) *reinterpret_cast<uint4*>(a.U + ((size_t)(i0 + r) * NC + cb0) * ESZ + ch * 16) = v;
     }
   }
+}
+
+// Launch shape of k_u_gemm: column blocks, destinations split into groups of
+// whole 32-row steps so that there are about four workgroups per CU.
+template <typename T, int DL, int H2>
+dsmp_status launch_u_gemm(dsmp_handle* h, const UArgs& ua) {
+  if (ua.n_rows == 0) return DSMP_OK;
+  constexpr int NC = H2 * DL, CB = UShape<T, DL, H2>::CB;
+  static_assert(NC % CB == 0, "U columns are whole column blocks");
+  const int64_t ncb = NC / CB;
+  int64_t groups = ((int64_t)h->n_cu * 4 + ncb - 1) / ncb;
+  const int64_t steps = (ua.n_rows + 31) / 32;
+  if (groups > steps) groups = steps;
+  const int64_t rows_per_wg = ((steps + groups - 1) / groups) * 32;
+  groups = (ua.n_rows + rows_per_wg - 1) / rows_per_wg;
+  hipLaunchKernelGGL((k_u_gemm<T, DL, H2>), dim3((unsigned)ncb, (unsigned)groups), dim3(256), 0, h->stream, ua,
+                     rows_per_wg);
+  DSMP_LAUNCHED(h, "U GEMM");
+  return DSMP_OK;
 }
 
 // Transposed staging of a chunk of ECH edge rows of a [E][W] array (layer
@@ -1813,8 +1829,7 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
     {
       ProfScope prof(h, DSMP_K_U_GEMM);
       UArgs ua{dz.n_dst, dz.gT, dz.packed + dz.L.w3u, const_cast<unsigned char*>(dz.U)};
-      hipLaunchKernelGGL((k_u_gemm<T, DL, H2>), dim3((unsigned)ceil_div(dz.n_dst, 32), (unsigned)ceil_div(H2 * DL, 1024)),
-                         dim3(256), 0, s, ua);
+      if ((st = launch_u_gemm<T, DL, H2>(h, ua)) != DSMP_OK) return st;
     }
     using SA = DzAggShape<T, H1, H2>;
     auto kz = k_bwd_dz_agg<T, DL, H1, H2>;
@@ -1896,9 +1911,8 @@ dsmp_status run_edge_grads_fused(dsmp_handle* h, const EdgeGradArgs& eg, int cap
   {
     ProfScope prof(h, DSMP_K_U_GEMM);
     UArgs ua{dz.n_dst, dz.gT, dz.packed + dz.L.w3u, const_cast<unsigned char*>(dz.U)};
-    hipLaunchKernelGGL((k_u_gemm<__bf16, DL, H2>),
-                       dim3((unsigned)ceil_div(dz.n_dst, 32), (unsigned)ceil_div(H2 * DL, 1024)), dim3(256), 0, s, ua);
-    DSMP_LAUNCHED(h, "U GEMM");
+    dsmp_status su = launch_u_gemm<__bf16, DL, H2>(h, ua);
+    if (su != DSMP_OK) return su;
   }
   using G = EdgeGradShape<DL, H1, H2>;
   auto kf = k_bwd_edge_agg<DL, H1, H2>;
