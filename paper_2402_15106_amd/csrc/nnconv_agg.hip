@@ -432,6 +432,85 @@ __global__ __launch_bounds__(256) void k_dw3_agg(DW3AggArgs a) {
   }
 }
 
+// bf16 layers: the same sums with chunks of 32 rows of S (a 512-byte piece,
+// 256 K columns) and of g copied to LDS by whole cache lines, two buffers,
+// and the fragments read by transposing LDS reads (rows are the contraction
+// index).  Wave w owns the q tile w / (NKT/4) and four consecutive K tiles,
+// so one g fragment feeds four products.  Rows past the slice re-read its
+// last row and are zeroed in the g fragment; columns past the end of a row
+// (last K block) are read from the next row (or the buffer's tail padding)
+// and never stored.
+template <int DL>
+struct DW3TrShape {
+  static constexpr int ECH = 32, KR = 256;
+  using SS = RowStage<ECH, KR * 2, 2>;
+  using GS = RowStage<ECH, DL * 2, 2>;
+  static constexpr int SB = ECH * SS::PITCH, BUF = SB + ECH * GS::PITCH, LDS = 2 * BUF;
+  static constexpr int NQT = DL / 32, NKT = KR / 32, TPW = NQT * NKT / 4;
+  static_assert(TPW % 4 == 0 || TPW == 2, "K tiles per wave");
+};
+
+template <int DL>
+__global__ __launch_bounds__(256) void k_dw3_agg_tr(DW3AggArgs a) {
+  using S = DW3TrShape<DL>;
+  using M = MT<__bf16>;
+  constexpr int ECH = S::ECH, TPW = S::TPW;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int64_t kc0 = (int64_t)blockIdx.x * S::KR;
+  const int s = blockIdx.y;
+  const int64_t rb = s * a.rows_per_sl;
+  const int64_t re = rb + a.rows_per_sl < a.n_rows ? rb + a.rows_per_sl : a.n_rows;
+  // the wave's tiles: ti = wv*TPW + j  ->  qt = ti / NKT, kt = ti % NKT (one qt per wave)
+  const int qt = (wv * TPW) / S::NKT, kt0 = (wv * TPW) % S::NKT;
+  f32x16 acc[TPW];
+#pragma unroll
+  for (int j = 0; j < TPW; ++j) acc[j] = f32x16{};
+  if (rb < re) {   // uniform over the workgroup
+    const int nch = (int)((re - rb + ECH - 1) / ECH);
+    typename S::SS ss;
+    typename S::GS sg;
+    auto issue = [&](int c, unsigned char* buf) {
+      const int64_t r0 = rb + (int64_t)c * ECH;
+      const int nv = (int)(re - r0 < ECH ? re - r0 : ECH);
+      ss.init(a.ktot * 2, nv);
+      sg.init(DL * 2, nv);
+      ss.issue(a.OS + ((size_t)r0 * a.ktot + kc0) * 2, buf);
+      sg.issue(a.G + (size_t)r0 * DL * 2, buf + S::SB);
+    };
+    issue(0, smem);
+    stage_wait();
+    __syncthreads();
+    for (int c = 0; c < nch; ++c) {
+      const unsigned char* cur = smem + (c & 1) * S::BUF;
+      if (c + 1 < nch) issue(c + 1, smem + ((c + 1) & 1) * S::BUF);
+      const int64_t r0 = rb + (int64_t)c * ECH;
+      const int cnt = (int)(re - r0 < ECH ? re - r0 : ECH);
+      for (int ks = 0; ks * 16 < cnt; ++ks) {
+        bf16x8 A = lds_frag_rows(cur + S::SB, S::GS::PITCH, ks * 16, qt * 32);
+        if (ks * 16 + 16 > cnt) {
+#pragma unroll
+          for (int t = 0; t < 8; ++t)
+            if (ks * 16 + 8 * hh + t >= cnt) A[t] = (__bf16)0.0f;
+        }
+#pragma unroll
+        for (int j = 0; j < TPW; ++j)
+          acc[j] = M::mma(A, lds_frag_rows(cur, S::SS::PITCH, ks * 16, (kt0 + j) * 32), acc[j]);
+      }
+      stage_wait();
+      __syncthreads();
+    }
+  }
+  float* out = a.part + (size_t)s * DL * a.kcols;
+#pragma unroll
+  for (int j = 0; j < TPW; ++j) {
+    const int64_t kc = kc0 + (kt0 + j) * 32 + l32;
+    if (kc < a.kcols)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) out[(size_t)(qt * 32 + 8 * (r / 4) + 4 * hh + (r % 4)) * a.kcols + kc] = acc[j][r];
+  }
+}
+
 // dW3[p*d+q][k] (+)= sum_s part[s][q][K(k, p)], K in the sum order above;
 // the bias rows K = h2*d + p give db3[p*d+q].
 template <typename T>
@@ -499,6 +578,16 @@ dsmp_status gemm_shape(dsmp_handle* h, const GemmArgs& a) {
 
 template <typename T, int DL>
 dsmp_status dw3_shape(dsmp_handle* h, const DW3AggArgs& a) {
+  if constexpr (sizeof(T) == 2) {
+    using S = DW3TrShape<DL>;
+    auto kern = k_dw3_agg_tr<DL>;
+    dsmp_status st = set_lds_bytes(h, kern, S::LDS);
+    if (st != DSMP_OK) return st;
+    hipLaunchKernelGGL(kern, dim3((unsigned)ceil_div(a.kcols, S::KR), (unsigned)a.nsl), dim3(256), S::LDS,
+                       h->stream, a);
+    DSMP_LAUNCHED(h, "dW3 from segment sums");
+    return DSMP_OK;
+  }
   using S = DW3AggShape<T, DL>;
   auto kern = k_dw3_agg<T, DL>;
   dsmp_status st = set_lds_bytes(h, kern, S::LDS);

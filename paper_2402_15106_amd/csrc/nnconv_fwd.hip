@@ -678,7 +678,7 @@ SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E) {
   s.z1E = (size_t)c.take<unsigned char>((size_t)E * d.h1 * esz);
   s.zmask = (size_t)c.take<unsigned char>((size_t)E * (d.h1 + d.h2) / 8);
   s.xE = (size_t)c.take<unsigned char>(d.dtype == DSMP_BF16 ? (size_t)E * 32 : 0);
-  s.os = (size_t)c.take<unsigned char>((size_t)n_dst * agg_ktot(d) * esz + 256);   // + whole last staged piece
+  s.os = (size_t)c.take<unsigned char>((size_t)n_dst * agg_ktot(d) * esz + 512);   // + whole last staged piece
   s.total = c.used();
   return s;
 }
