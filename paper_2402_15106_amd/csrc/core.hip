@@ -194,9 +194,11 @@ extern "C" const char* dsmp_last_error(const dsmp_handle* h) { return h ? h->err
 
 // ------------------------------------------------------------------ sampling
 //
-// Selection of the s smallest SplitMix64 keys out of M by an 8-pass MSB-first
-// radix select over 8-bit digits (the keys are recomputed every pass), then a
-// stable compaction of the candidates whose key is <= the s-th smallest.
+// Selection of the s smallest SplitMix64 keys out of M by a 4-pass MSB-first
+// radix select over 16-bit digits (the keys are recomputed every pass), then a
+// stable compaction of the candidates whose key is <= the s-th smallest.  The
+// keys are distinct (the mix is a bijection of the counter), so exactly s are
+// kept.
 
 namespace {
 
@@ -206,40 +208,60 @@ struct SelState {
 };
 
 constexpr int SAMPLE_CHUNK = 1024;   // candidates per block in the compaction
+constexpr int SEL_BINS = 65536;      // 16-bit digits
 
-__global__ __launch_bounds__(256) void k_sel_hist(int64_t M, uint64_t seed, const SelState* st,
-                                                  int shift, uint32_t* __restrict__ hist) {
-  __shared__ uint32_t lh[256];
-  lh[threadIdx.x] = 0;
-  __syncthreads();
+// Histogram of digit (k >> shift) & 0xFFFF over the keys that match the fixed prefix.
+__global__ __launch_bounds__(256) void k_sel_hist(int64_t M, uint64_t seed, const SelState* st, int shift,
+                                                  uint32_t* __restrict__ hist) {
   const uint64_t prefix = st->prefix;
-  const uint64_t himask = shift >= 56 ? 0ull : (~0ull << (shift + 8));
+  const uint64_t himask = shift >= 48 ? 0ull : (~0ull << (shift + 16));
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (; i < M; i += stride) {
-    uint64_t k = splitmix64(seed, (uint64_t)i);
-    if ((k & himask) == (prefix & himask)) atomicAdd(&lh[(k >> shift) & 255u], 1u);
+    const uint64_t k = splitmix64(seed, (uint64_t)i);
+    if ((k & himask) == (prefix & himask)) atomicAdd(&hist[(k >> shift) & 0xFFFFu], 1u);
   }
-  __syncthreads();
-  if (lh[threadIdx.x]) atomicAdd(&hist[threadIdx.x], lh[threadIdx.x]);
 }
 
-__global__ void k_sel_pick(SelState* st, int shift, uint32_t* __restrict__ hist) {
-  if (threadIdx.x != 0) return;
-  uint64_t r = st->rank, acc = 0;
-  int dsel = 255;
-  for (int d = 0; d < 256; ++d) {
-    if (acc + hist[d] >= r) { dsel = d; break; }
-    acc += hist[d];
+// One workgroup: thread t owns bins [64t, 64t + 64); a scan of the per-thread
+// counts finds the thread whose bins hold the wanted rank, which fixes the
+// digit.  Every thread clears its bins for the next pass.
+__global__ __launch_bounds__(1024) void k_sel_pick(SelState* st, int shift, uint32_t* __restrict__ hist) {
+  __shared__ uint32_t sh[32];
+  constexpr int PER = SEL_BINS / 1024;
+  uint4* hb = reinterpret_cast<uint4*>(hist + (size_t)threadIdx.x * PER);
+  uint32_t c[PER];
+  uint32_t sum = 0;
+#pragma unroll
+  for (int v = 0; v < PER / 4; ++v) {
+    const uint4 x = hb[v];
+    c[4 * v] = x.x; c[4 * v + 1] = x.y; c[4 * v + 2] = x.z; c[4 * v + 3] = x.w;
+    sum += x.x + x.y + x.z + x.w;
   }
-  st->rank = r - acc;
-  st->prefix |= (uint64_t)dsel << shift;
-  for (int d = 0; d < 256; ++d) hist[d] = 0;
+  uint32_t tot;
+  const uint32_t ex = block_exclusive_scan_1024(sum, sh, &tot);
+  const uint64_t r = st->rank;
+  __syncthreads();   // every thread has read the rank before it changes
+  if (ex < r && r <= (uint64_t)ex + sum) {
+    uint64_t acc = ex;
+#pragma unroll
+    for (int b = 0; b < PER; ++b) {
+      if (acc + c[b] >= r) {
+        st->rank = r - acc;
+        st->prefix |= (uint64_t)(threadIdx.x * PER + b) << shift;
+        break;
+      }
+      acc += c[b];
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < PER / 4; ++v) hb[v] = make_uint4(0u, 0u, 0u, 0u);
 }
 
-__global__ void k_sel_init(SelState* st, uint64_t s, uint32_t* hist) {
+__global__ __launch_bounds__(1024) void k_sel_init(SelState* st, uint64_t s, uint32_t* hist) {
   if (threadIdx.x == 0) { st->prefix = 0; st->rank = s; }
-  hist[threadIdx.x] = 0;
+  uint4* hb = reinterpret_cast<uint4*>(hist);
+  for (int v = threadIdx.x; v < SEL_BINS / 4; v += 1024) hb[v] = make_uint4(0u, 0u, 0u, 0u);
 }
 
 __global__ __launch_bounds__(1024) void k_sel_count(int64_t M, uint64_t seed, const SelState* st,
@@ -270,7 +292,11 @@ __global__ void k_iota(int32_t* out, int64_t n) {
 
 size_t sample_ws(int64_t M) {
   size_t nb = ceil_div(M, SAMPLE_CHUNK);
-  return 256 + 1024 + 256 * (nb + 2) * 4 / 256 * 4 + (nb + 2) * 4 + 1024;
+  Carve c(nullptr);
+  c.take<SelState>(1);
+  c.take<uint32_t>(SEL_BINS);
+  c.take<uint32_t>(nb + 2);
+  return c.used();
 }
 
 }  // namespace
@@ -299,15 +325,15 @@ extern "C" dsmp_status dsmp_sample_nodes(dsmp_handle* h, int64_t M, int64_t s, u
              "sampling workspace needs %zu bytes", sample_ws(M));
   Carve c(ws);
   SelState* st = c.take<SelState>(1);
-  uint32_t* hist = c.take<uint32_t>(256);
+  uint32_t* hist = c.take<uint32_t>(SEL_BINS);
   int nb = (int)ceil_div(M, SAMPLE_CHUNK);
   uint32_t* cnt = c.take<uint32_t>(nb + 2);
-  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, h->stream, st, (uint64_t)s, hist);
+  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(1024), 0, h->stream, st, (uint64_t)s, hist);
   unsigned g = ceil_div(M, 256);
   if (g > 2048) g = 2048;
-  for (int shift = 56; shift >= 0; shift -= 8) {
+  for (int shift = 48; shift >= 0; shift -= 16) {
     hipLaunchKernelGGL(k_sel_hist, dim3(g), dim3(256), 0, h->stream, M, seed, st, shift, hist);
-    hipLaunchKernelGGL(k_sel_pick, dim3(1), dim3(64), 0, h->stream, st, shift, hist);
+    hipLaunchKernelGGL(k_sel_pick, dim3(1), dim3(1024), 0, h->stream, st, shift, hist);
   }
   hipLaunchKernelGGL(k_sel_count, dim3(nb), dim3(1024), 0, h->stream, M, seed, st, cnt);
   hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(1024), 0, h->stream, cnt, nb);

@@ -349,6 +349,33 @@ __global__ __launch_bounds__(256) void k_csc_scatter(const int32_t* __restrict__
   csc_eid[csc_ptr[j] + (int32_t)atomicAdd(&cur[j], 1u)] = (int32_t)e;
 }
 
+// Uncapped graph over one point set (n_src = n_dst, no cap): j is a source of
+// i exactly when i is a source of j (the float32 distance test is symmetric,
+// fl(a - b) = -fl(b - a)), so the edges leaving j are the edges (i <- j) for i
+// in row j, in row order, which is ascending edge id: csc_ptr = row_ptr, and
+// position e of row j holds the id of edge (col[e] <- j), row_ptr[i] + the
+// position of j in row i (rows are sorted by source).
+__global__ __launch_bounds__(256) void k_csc_symmetric(const int32_t* __restrict__ row_ptr,
+                                                       const int32_t* __restrict__ col,
+                                                       const int32_t* __restrict__ dst, int64_t E,
+                                                       int32_t* __restrict__ csc_eid) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= E) return;
+  const int32_t i = col[e], j = dst[e];
+  int32_t lo = row_ptr[i], hi = row_ptr[i + 1];   // first position in row i with col >= j
+  while (lo < hi) {
+    const int32_t mid = lo + (hi - lo) / 2;
+    if (col[mid] < j) lo = mid + 1;
+    else hi = mid;
+  }
+  csc_eid[e] = lo;
+}
+
+__global__ __launch_bounds__(256) void k_copy_i32(const int32_t* __restrict__ a, int64_t n, int32_t* __restrict__ b) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t < n) b[t] = a[t];
+}
+
 constexpr int CSC_SORT_LDS = 2048;
 
 // One wave per source: sort its edge ids ascending (LDS bitonic; an in-place
@@ -535,6 +562,16 @@ extern "C" dsmp_status dsmp_radius_graph_build(dsmp_handle* h, const dsmp_graph_
   }
   DSMP_CHECK(h, E <= edge_capacity, DSMP_CAPACITY, "graph has %lld edges, capacity %lld",
              (long long)E, (long long)edge_capacity);
+  if (q->cap == 0 && q->n_src == q->n_dst) {
+    // symmetric graph: the transpose is the row structure itself
+    hipLaunchKernelGGL(k_copy_i32, dim3(ceil_div(q->n_dst + 1, 256)), dim3(256), 0, s, g->row_ptr, q->n_dst + 1,
+                       g->csc_ptr);
+    if (E > 0)
+      hipLaunchKernelGGL(k_csc_symmetric, dim3(ceil_div(E, 256)), dim3(256), 0, s, g->row_ptr, g->col, g->dst, E,
+                         g->csc_eid);
+    DSMP_LAUNCHED(h, "csc (symmetric graph)");
+    return DSMP_OK;
+  }
   if ((st = fill_u32(h, w.indeg, q->n_src, 0)) != DSMP_OK) return st;
   if ((st = fill_u32(h, w.scur, q->n_src, 0)) != DSMP_OK) return st;
   if (E > 0) {
