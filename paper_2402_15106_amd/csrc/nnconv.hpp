@@ -231,6 +231,34 @@ __device__ __forceinline__ float layer1_pre(const float* __restrict__ w, float b
   return v;
 }
 
+// Attribute slots that can be nonzero for an attribute mode and dimension
+// (the layouts of edge_attr_rows).
+__host__ __device__ inline int attr_slots(int dim, int mode) {
+  return mode == DSMP_ATTR_DIFF ? 4 : (dim == 2 ? 6 : 8);
+}
+
+// ReLU as one integer maximum over the bits: a positive float is a positive
+// signed integer and keeps its bits; +0, -0 and every negative float give +0.
+// Equal to (v > 0 ? v : +0) for every value that is not a NaN.
+__device__ __forceinline__ float relu_bits(float v) {
+  const int i = __float_as_int(v);
+  return __int_as_float(i > 0 ? i : 0);
+}
+
+// ReLU of v, with its mask bit [v > 0] ORed into position `bit` of `word`.
+// The bit is a clamp of the ReLU output's bits to [0, 1], one vector
+// instruction that leaves no lane mask in scalar registers to keep live.  It
+// is inline assembly and reads the ReLU output, never v itself: v may be a
+// matrix-core result, and the wait states the compiler inserts before the
+// first vector read of such a result are not applied to inline assembly.
+__device__ __forceinline__ float relu_mask(float v, uint32_t& word, int bit) {
+  const float z = relu_bits(v);
+  int r;
+  asm("v_med3_i32 %0, %1, 0, 1" : "=v"(r) : "v"(__float_as_int(z)));
+  word |= (uint32_t)r << bit;
+  return z;
+}
+
 // Byte offsets of the sections of a packed parameter buffer.
 struct PackLayout {
   size_t w1l, b1l, w2p, b2, w3f, w3q, w3t, b3t, b3n, w2t, wr, br, wgt, wht, w3u, total;

@@ -196,12 +196,16 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
           const float v = layer1_pre(w1h + n * 8, bn, x[t]);
-          zv[t][u] = v > 0.0f ? v : 0.0f;
-          if (v > 0.0f) m1[t][(s * EPL + u) / 32] |= 1u << ((s * EPL + u) % 32);
+          zv[t][u] = relu_mask(v, m1[t][n / 32], n % 32);
         }
       }
 #pragma unroll
-      for (int t = 0; t < NT; ++t) z1B[t][s] = pack_frag<T>(zv[t]);
+      for (int t = 0; t < NT; ++t) {
+        z1B[t][s] = pack_frag<T>(zv[t]);
+        // fold the bits into their words here rather than at the store
+#pragma unroll
+        for (int w = 0; w < MW1; ++w) asm("" : "+v"(m1[t][w]));
+      }
     }
     if (a.z1E) {
 #pragma unroll
@@ -248,12 +252,15 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 2 : 1) v
 #pragma unroll
             for (int u = 0; u < EPL; ++u) {
               const float v = C[t][i0 + u] + bb[i0 + u];
-              zv[u] = v > 0.0f ? v : 0.0f;
               const int b = 16 * kt + i0 + u;
-              if (v > 0.0f) m2[t][b / 32] |= 1u << (b % 32);
+              zv[u] = relu_mask(v, m2[t][b / 32], b % 32);
             }
             zB[t][(16 * kt + i0) / EPL] = pack_frag<T>(zv);
           }
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int w = 0; w < MW2; ++w) asm("" : "+v"(m2[t][w]));
       }
     }
     if (a.zE) {
@@ -488,6 +495,187 @@ __global__ __launch_bounds__(256) void k_fwd_node(NodeArgs a) {
   }
 }
 
+// ------------------------------------------------------------------ kernel MLP
+
+// Layers 1 and 2 of the kernel network K_phi (eq. (1)) for every edge, the
+// pass the aggregate form runs ahead of its per-destination sums (bf16
+// layers):  z1 = ReLU(W1 x + b1),  z = ReLU(W2 z1 + b2),  with the ReLU mask
+// bits of both, and z1 and the split attributes when the backward reads them
+// back.  Both layers are matrix-core products over a 32-edge tile:
+//  * layer 1 in fp32, 32x32x2 steps over the attribute slots that can be
+//    nonzero (two per step), with the bias as the accumulator's initial
+//    value: any fp32 evaluation order of the pre-activation is within the
+//    accumulation bound the ReLU decisions are held to;
+//  * layer 2 in bf16, the bias again the accumulator's initial value.
+// W1, W2 (packed columns) and the biases sit in LDS for the workgroup's
+// lifetime.
+// The layer-1 accumulator rows are the neurons in natural order, which is
+// the order the packed-column permutation assigns to the layer-2 B operand:
+// each half of a 32-row tile's accumulators is one B fragment as it stands,
+// and the mask bits come out in the stored format.  Workgroups are
+// persistent; each wave takes every (grid * waves)-th tile.
+template <int H>
+struct MlpShape {
+  static constexpr int WAVES = H <= 128 ? 4 : 8;    // waves per workgroup
+  static constexpr int PER_CU = H <= 128 ? 4 : 1;   // workgroups per CU (LDS and registers)
+  static constexpr int RT = H / 32, SK = H / 16;    // 32-row output tiles; bf16 K steps
+  static constexpr int W2B = H * 2 + 16;            // LDS pitch of a W2 row
+  static constexpr int LDS = H * W2B + 10 * H * 4;  // W2; W1 and b1 (packed halves); b2
+  static constexpr int MW = H / 64;                 // mask words per lane half and layer
+};
+
+template <int H>
+__global__ __launch_bounds__(64 * MlpShape<H>::WAVES, MlpShape<H>::PER_CU) void k_edge_mlp(EdgeArgs a,
+                                                                                         int64_t ntiles) {
+  using S = MlpShape<H>;
+  using M = MT<__bf16>;
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* w2s = smem;
+  float* w1s = reinterpret_cast<float*>(smem + H * S::W2B);
+  float* b1s = w1s + 8 * H;
+  float* b2s = b1s + H;
+  const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
+  const unsigned char* P = a.packed;
+
+  // W2, W1 and the biases to LDS, once per workgroup
+  {
+    constexpr int NU = H * 2 / 16;
+    const uint4* src = reinterpret_cast<const uint4*>(P + a.L.w2p);
+    for (int U = tid; U < H * NU; U += 64 * S::WAVES)
+      *reinterpret_cast<uint4*>(w2s + (U / NU) * S::W2B + (U % NU) * 16) = src[U];
+    const uint4* w1l = reinterpret_cast<const uint4*>(P + a.L.w1l);
+    for (int U = tid; U < 2 * H; U += 64 * S::WAVES) reinterpret_cast<uint4*>(w1s)[U] = w1l[U];
+    const float* b1l = reinterpret_cast<const float*>(P + a.L.b1l);
+    const float* b2 = reinterpret_cast<const float*>(P + a.L.b2);
+    for (int U = tid; U < H; U += 64 * S::WAVES) {
+      b1s[U] = b1l[U];
+      b2s[U] = b2[U];
+    }
+  }
+  // Layer-1 A operand: W1[32 rt + l32][2 ks + hh] from the packed halves
+  // (neuron 32c + r sits in half (r/4)%2 at position 16c + 4(r/8) + r%4).
+  const int nks = attr_slots(a.dim, a.attr_mode) / 2;
+  const float* w1a = w1s + ((((l32 >> 2) & 1) * (H / 2) + 4 * (l32 >> 3) + (l32 & 3)) * 8 + hh);
+  __syncthreads();
+
+  const int64_t stride = (int64_t)gridDim.x * S::WAVES;
+  for (int64_t tile = (int64_t)blockIdx.x * S::WAVES + (tid >> 6); tile < ntiles; tile += stride) {
+    const int64_t e = tile * 32 + l32;
+    const bool valid = e < a.E;
+    const int64_t es = valid ? e : 0;
+    float x[8];
+    edge_attr(a.node_attr, a.dim, a.attr_mode, a.dst[es], a.col[es], x);
+    if (a.xE && valid) {   // bf16 high parts (lane half 0), then low parts (half 1)
+      float v[8];
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const float hi = (float)(__bf16)x[c];
+        v[c] = hh ? x[c] - hi : hi;
+      }
+      *reinterpret_cast<bf16x8*>(a.xE + (size_t)e * 32 + hh * 16) = pack_frag<__bf16>(v);
+    }
+    // B operand of layer 1: slot 2 ks + hh of the lane's edge (the values go
+    // through registers first, so the choice stays a select of values)
+    float xb[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      float x0 = x[2 * ks], x1 = x[2 * ks + 1];
+      asm("" : "+v"(x0), "+v"(x1));
+      xb[ks] = hh ? x1 : x0;
+    }
+
+    // layer 1
+    bf16x8 z1B[S::SK];
+    uint32_t m1[S::MW], m2[S::MW];
+#pragma unroll
+    for (int w = 0; w < S::MW; ++w) m1[w] = m2[w] = 0u;
+#pragma unroll
+    for (int rt = 0; rt < S::RT; ++rt) {
+      f32x16 C;
+      const f32x4* bp = reinterpret_cast<const f32x4*>(b1s + hh * (H / 2) + 16 * rt);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x4 b = bp[q];
+        C[4 * q] = b[0]; C[4 * q + 1] = b[1]; C[4 * q + 2] = b[2]; C[4 * q + 3] = b[3];
+      }
+      const float* w1t = w1a + 16 * rt * 8;
+      C = MT<float>::mma(w1t[0], xb[0], C);
+      C = MT<float>::mma(w1t[2], xb[1], C);
+      if (nks > 2) C = MT<float>::mma(w1t[4], xb[2], C);
+      if (nks > 3) C = MT<float>::mma(w1t[6], xb[3], C);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        float zv[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const int b = (2 * rt + j) * 8 + t;
+          zv[t] = relu_mask(C[8 * j + t], m1[b / 32], b % 32);
+        }
+        z1B[2 * rt + j] = pack_frag<__bf16>(zv);
+      }
+      // fold the tile's mask bits into their words here rather than at the store
+#pragma unroll
+      for (int w = 0; w < S::MW; ++w) asm("" : "+v"(m1[w]));
+    }
+    if (a.z1E && valid) {
+#pragma unroll
+      for (int s = 0; s < S::SK; ++s)
+        *reinterpret_cast<bf16x8*>(a.z1E + ((size_t)e * H + s * 16 + hh * 8) * 2) = z1B[s];
+    }
+
+    // layer 2, one 32-row tile of outputs at a time
+#pragma unroll
+    for (int kt = 0; kt < S::RT; ++kt) {
+      f32x16 C;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x4 b = *reinterpret_cast<const f32x4*>(b2s + kt * 32 + 8 * q + 4 * hh);
+        C[4 * q] = b[0]; C[4 * q + 1] = b[1]; C[4 * q + 2] = b[2]; C[4 * q + 3] = b[3];
+      }
+#pragma unroll
+      for (int s = 0; s < S::SK; ++s) {
+        const bf16x8 A = *reinterpret_cast<const bf16x8*>(w2s + (kt * 32 + l32) * S::W2B + (s * 16 + hh * 8) * 2);
+        C = M::mma(A, z1B[s], C);
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        float zv[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const int b = 16 * kt + 8 * j + t;
+          zv[t] = relu_mask(C[8 * j + t], m2[b / 32], b % 32);
+        }
+        if (a.zE && valid)
+          *reinterpret_cast<bf16x8*>(a.zE + ((size_t)e * H + (2 * kt + j) * 16 + hh * 8) * 2) =
+              pack_frag<__bf16>(zv);
+      }
+#pragma unroll
+      for (int w = 0; w < S::MW; ++w) asm("" : "+v"(m2[w]));
+    }
+    if (a.zmask && valid) {
+      uint32_t* mb = reinterpret_cast<uint32_t*>(a.zmask + (size_t)e * (2 * H / 8));
+#pragma unroll
+      for (int w = 0; w < S::MW; ++w) mb[hh * S::MW + w] = m1[w];
+#pragma unroll
+      for (int w = 0; w < S::MW; ++w) mb[2 * S::MW + hh * S::MW + w] = m2[w];
+    }
+  }
+}
+
+template <int H>
+dsmp_status launch_edge_mlp(dsmp_handle* h, const EdgeArgs& a) {
+  using S = MlpShape<H>;
+  auto kern = k_edge_mlp<H>;
+  DSMP_HIP(h, hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, S::LDS));
+  const int64_t ntiles = ceil_div(a.E, 32);
+  const int64_t grid = std::min<int64_t>(ceil_div(ntiles, S::WAVES), (int64_t)h->n_cu * S::PER_CU);
+  ProfScope prof(h, DSMP_K_EDGE_MLP);
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(64 * S::WAVES), S::LDS, h->stream, a, ntiles);
+  DSMP_LAUNCHED(h, "kernel MLP");
+  return DSMP_OK;
+}
+
 // ------------------------------------------------------------------ packing
 
 struct PackArgs {
@@ -595,11 +783,15 @@ dsmp_status launch_edge_shape(dsmp_handle* h, int mode, const EdgeArgs& a) {
     ProfScope prof(h, DSMP_K_EDGE_FWD);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(256), S::LDS, h->stream, a);
   } else if (mode == MODE_MLP) {
-    auto kern = k_edge_contract<T, DL, H1, H2, MODE_MLP>;
-    dsmp_status st = set_lds(h, kern, S::LDS);
-    if (st != DSMP_OK) return st;
-    ProfScope prof(h, DSMP_K_EDGE_MLP);
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), S::LDS, h->stream, a);
+    if constexpr (sizeof(T) == 2 && H1 == H2) {
+      return launch_edge_mlp<H1>(h, a);
+    } else {
+      auto kern = k_edge_contract<T, DL, H1, H2, MODE_MLP>;
+      dsmp_status st = set_lds(h, kern, S::LDS);
+      if (st != DSMP_OK) return st;
+      ProfScope prof(h, DSMP_K_EDGE_MLP);
+      hipLaunchKernelGGL(kern, dim3(grid), dim3(256), S::LDS, h->stream, a);
+    }
   } else {
     auto kern = k_edge_contract<T, DL, H1, H2, MODE_DH>;
     dsmp_status st = set_lds(h, kern, S::LDS);
