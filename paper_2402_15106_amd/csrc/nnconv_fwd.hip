@@ -524,7 +524,7 @@ struct MlpShape {
   static constexpr int MW = H / 64;                 // mask words per lane half and layer
 };
 
-template <int H>
+template <int H, bool SPLIT>
 __global__ __launch_bounds__(64 * MlpShape<H>::WAVES, MlpShape<H>::PER_CU) void k_edge_mlp(EdgeArgs a,
                                                                                          int64_t ntiles) {
   using S = MlpShape<H>;
@@ -559,13 +559,62 @@ __global__ __launch_bounds__(64 * MlpShape<H>::WAVES, MlpShape<H>::PER_CU) void 
   __syncthreads();
 
   const int64_t stride = (int64_t)gridDim.x * S::WAVES;
-  for (int64_t tile = (int64_t)blockIdx.x * S::WAVES + (tid >> 6); tile < ntiles; tile += stride) {
+  int64_t tile = (int64_t)blockIdx.x * S::WAVES + (tid >> 6);
+  if (tile >= ntiles) return;
+  // Loads run a tile ahead: a tile's attribute rows, and the ids of the tile
+  // after it, are issued before the stores of the tile in hand, so waiting
+  // for them never waits for those stores (loads and stores retire in one
+  // in-order count).  Lanes past E read edge 0 and store into the padding
+  // rows of the last tile.
+  const int rw = a.dim + 1;
+  const float* na = a.node_attr;
+  auto eid = [&](int64_t t) -> int64_t {
+    const int64_t e = t * 32 + l32;
+    return e < a.E ? e : 0;
+  };
+  float ri[4], rj[4];
+  auto load_rows = [&](int i, int j) {
+    const float* pi = na + (size_t)i * rw;
+    const float* pj = na + (size_t)j * rw;
+    ri[0] = pi[0]; ri[1] = pi[1]; ri[2] = pi[2];
+    rj[0] = pj[0]; rj[1] = pj[1]; rj[2] = pj[2];
+    ri[3] = rw == 4 ? pi[3] : 0.0f;
+    rj[3] = rw == 4 ? pj[3] : 0.0f;
+  };
+  {
+    const int64_t e0 = eid(tile);
+    load_rows(a.dst[e0], a.col[e0]);
+  }
+  int ni, nj;
+  {
+    const int64_t e1 = eid(tile + stride);
+    ni = a.dst[e1];
+    nj = a.col[e1];
+  }
+
+  // The loop is re-entered with a tile's stores issued after the next tile's
+  // loads.  The compiler's wait counts at the loop head take the smaller count
+  // of its two ways in, so the way in from here issues as many stores after
+  // those loads, into the spare mask rows past the last tile (never read).
+  {
+    constexpr int NST = 2 * S::RT + 2 + (SPLIT ? S::SK + 1 : 0);
+    constexpr int RW = 2 * H / 32;   // mask words per edge
+    uint32_t* sink = reinterpret_cast<uint32_t*>(a.zmask + (size_t)ntiles * 32 * RW * 4);
+    // a lane-dependent row per store keeps them from merging into wider ones
+#pragma unroll
+    for (int k = 0; k < NST; ++k) sink[((l32 + 5 * k) % 32) * RW + (k / 32) % RW] = 0u;
+  }
+  for (; tile < ntiles; tile += stride) {
     const int64_t e = tile * 32 + l32;
-    const bool valid = e < a.E;
-    const int64_t es = valid ? e : 0;
     float x[8];
-    edge_attr(a.node_attr, a.dim, a.attr_mode, a.dst[es], a.col[es], x);
-    if (a.xE && valid) {   // bf16 high parts (lane half 0), then low parts (half 1)
+    edge_attr_rows(ri, rj, a.dim, a.attr_mode, x);
+    load_rows(ni, nj);
+    {
+      const int64_t e2 = eid(tile + 2 * stride);
+      ni = a.dst[e2];
+      nj = a.col[e2];
+    }
+    if constexpr (SPLIT) {   // bf16 high parts (lane half 0), then low parts (half 1)
       float v[8];
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
@@ -617,7 +666,7 @@ __global__ __launch_bounds__(64 * MlpShape<H>::WAVES, MlpShape<H>::PER_CU) void 
 #pragma unroll
       for (int w = 0; w < S::MW; ++w) asm("" : "+v"(m1[w]));
     }
-    if (a.z1E && valid) {
+    if constexpr (SPLIT) {
 #pragma unroll
       for (int s = 0; s < S::SK; ++s)
         *reinterpret_cast<bf16x8*>(a.z1E + ((size_t)e * H + s * 16 + hh * 8) * 2) = z1B[s];
@@ -645,27 +694,26 @@ __global__ __launch_bounds__(64 * MlpShape<H>::WAVES, MlpShape<H>::PER_CU) void 
           const int b = 16 * kt + 8 * j + t;
           zv[t] = relu_mask(C[8 * j + t], m2[b / 32], b % 32);
         }
-        if (a.zE && valid)
-          *reinterpret_cast<bf16x8*>(a.zE + ((size_t)e * H + (2 * kt + j) * 16 + hh * 8) * 2) =
-              pack_frag<__bf16>(zv);
+        *reinterpret_cast<bf16x8*>(a.zE + ((size_t)e * H + (2 * kt + j) * 16 + hh * 8) * 2) =
+            pack_frag<__bf16>(zv);
       }
 #pragma unroll
       for (int w = 0; w < S::MW; ++w) asm("" : "+v"(m2[w]));
     }
-    if (a.zmask && valid) {
-      uint32_t* mb = reinterpret_cast<uint32_t*>(a.zmask + (size_t)e * (2 * H / 8));
+    uint32_t* mb = reinterpret_cast<uint32_t*>(a.zmask + (size_t)e * (2 * H / 8));
 #pragma unroll
-      for (int w = 0; w < S::MW; ++w) mb[hh * S::MW + w] = m1[w];
+    for (int w = 0; w < S::MW; ++w) mb[hh * S::MW + w] = m1[w];
 #pragma unroll
-      for (int w = 0; w < S::MW; ++w) mb[2 * S::MW + hh * S::MW + w] = m2[w];
-    }
+    for (int w = 0; w < S::MW; ++w) mb[2 * S::MW + hh * S::MW + w] = m2[w];
   }
 }
 
 template <int H>
 dsmp_status launch_edge_mlp(dsmp_handle* h, const EdgeArgs& a) {
   using S = MlpShape<H>;
-  auto kern = k_edge_mlp<H>;
+  DSMP_CHECK(h, a.zE != nullptr && a.zmask != nullptr && (a.z1E == nullptr) == (a.xE == nullptr),
+             DSMP_INVALID_ARG, "kernel MLP: z and the mask bits are always stored, z1 and x together");
+  auto kern = a.z1E ? k_edge_mlp<H, true> : k_edge_mlp<H, false>;
   DSMP_HIP(h, hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                   hipFuncAttributeMaxDynamicSharedMemorySize, S::LDS));
   const int64_t ntiles = ceil_div(a.E, 32);
@@ -675,6 +723,7 @@ dsmp_status launch_edge_mlp(dsmp_handle* h, const EdgeArgs& a) {
   DSMP_LAUNCHED(h, "kernel MLP");
   return DSMP_OK;
 }
+
 
 // ------------------------------------------------------------------ packing
 
@@ -866,10 +915,14 @@ SavedLayout saved_layout(const dsmp_layer_desc& d, int64_t n_dst, int64_t E) {
   int esz = d.dtype == DSMP_BF16 ? 2 : 4;
   SavedLayout s;
   s.y = (size_t)c.take<float>((size_t)n_dst * d.d) ;
-  s.zE = (size_t)c.take<unsigned char>((size_t)E * d.h2 * esz);
-  s.z1E = (size_t)c.take<unsigned char>((size_t)E * d.h1 * esz);
-  s.zmask = (size_t)c.take<unsigned char>((size_t)E * (d.h1 + d.h2) / 8);
-  s.xE = (size_t)c.take<unsigned char>(d.dtype == DSMP_BF16 ? (size_t)E * 32 : 0);
+  // per-edge sections hold whole 32-edge tiles: the kernel-MLP pass stores
+  // its last tile's rows past E without a per-lane condition; the mask bits
+  // have one more tile of rows that it writes and nothing reads
+  const int64_t E32 = (E + 31) / 32 * 32;
+  s.zE = (size_t)c.take<unsigned char>((size_t)E32 * d.h2 * esz);
+  s.z1E = (size_t)c.take<unsigned char>((size_t)E32 * d.h1 * esz);
+  s.zmask = (size_t)c.take<unsigned char>((size_t)(E32 + 32) * (d.h1 + d.h2) / 8);
+  s.xE = (size_t)c.take<unsigned char>(d.dtype == DSMP_BF16 ? (size_t)E32 * 32 : 0);
   s.os = (size_t)c.take<unsigned char>((size_t)n_dst * agg_ktot(d) * esz + 512);   // + whole last staged piece
   s.total = c.used();
   return s;

@@ -262,3 +262,105 @@ def test_backward_workload_rows(env, algo, k):
     rows = np.sort(np.random.default_rng(k + 10).choice(make_config(k).n_dst, 128, replace=False))
     c = workload_case(env, k, rows=rows)
     _check_backward(c, "E=%d" % c.col.size)
+
+
+# ---------------------------------------------------------------- kernel MLP
+# What the forward keeps for the backward, read back from the saved buffer:
+# the ReLU mask bits of both kernel-MLP layers (every layer shape), z1 and the
+# bf16 high/low attribute parts (shapes whose backward reads them back), and
+# z.  Layout of the saved buffer: y [n_dst][d] fp32, z [E][h2], z1 [E][h1],
+# mask bits [E][(h1+h2)/8], split attributes [E][16] bf16, each section at a
+# 256-byte boundary, the per-edge ones with E rounded up to whole 32-edge
+# tiles (the mask bits with one tile more).  z1, z and their bits sit at packed positions: position
+# p = 16 s + 8 g + t (fragment s, lane half g) holds neuron kperm(p) below.
+
+def _kperm(p):
+    n = (p // 16) * 8 + p % 8
+    c, i, g = n // 16, n % 16, (p % 16) // 8
+    return 32 * c + 8 * (i // 4) + 4 * g + i % 4
+
+
+def _saved_sections(c):
+    E, esz = c.col.size, 2
+    E32 = (E + 31) // 32 * 32
+    H1, H2 = c.P["W1"].shape[0], c.P["W2"].shape[0]
+    off, out = 0, {}
+    for name, nb in (("y", c.n_dst * c.h.shape[1] * 4), ("z", E32 * H2 * esz), ("z1", E32 * H1 * esz),
+                     ("mask", (E32 + 32) * (H1 + H2) // 8), ("x", E32 * 32)):
+        off = (off + 255) & ~255
+        out[name] = (off, nb)
+        off += nb
+    return out
+
+
+def _bits_natural(words, H):
+    """[E][2 * H/64] uint32 (lane half 0 words, then half 1) -> [E][H] bool in neuron order."""
+    E = words.shape[0]
+    bits = np.unpackbits(words.view(np.uint8).reshape(E, -1), axis=1, bitorder="little").astype(bool)
+    out = np.zeros((E, H), bool)
+    for g in range(2):
+        for b in range(H // 2):
+            p = (b // 8) * 16 + 8 * g + b % 8
+            out[:, _kperm(p)] = bits[:, g * (H // 2) + b]
+    return out
+
+
+def _positions_natural(vals, H):
+    perm = np.array([_kperm(p) for p in range(H)])
+    out = np.empty_like(vals)
+    out[:, perm] = vals
+    return out
+
+
+def _bf16_bits_to_f64(u16):
+    return (u16.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+@pytest.mark.parametrize("name", ["bf16_128_3d", "bf16_64_2d", "bf16_64_diff_attr", "bf16_32_2d",
+                                  "bf16_64_one_tile_ragged"])
+def test_kernel_mlp_saved(env, name):
+    dm, lib, _ = env
+    announce("kernel MLP saved outputs", name)
+    lib.dsmp_set_edge_algorithm(dm.EDGE_AGGREGATE)
+    try:
+        c = random_case(env, seed=zlib.crc32(name.encode()) % 1000, **FWD_CASES[name])
+        c.forward()
+    finally:
+        lib.dsmp_set_edge_algorithm(dm.EDGE_AUTO)
+    E, H1, H2 = c.col.size, c.P["W1"].shape[0], c.P["W2"].shape[0]
+    sv = c.saved.cpu().numpy().view(np.uint8)
+    sec = _saved_sections(c)
+    part = lambda k: sv[sec[k][0]:sec[k][0] + sec[k][1]]
+    per_edge = {"z": H2 * 2, "z1": H1 * 2, "mask": (H1 + H2) // 8, "x": 32}
+    part_e = lambda k: part(k)[:E * per_edge[k]]
+    assert sv.size >= sec["x"][0] + sec["x"][1]
+    words = part_e("mask").view(np.uint32).reshape(E, -1)
+    m1 = _bits_natural(words[:, :H1 // 32], H1)
+    m2 = _bits_natural(words[:, H1 // 32:], H2)
+    # decisions of the oracle at the kernel's precision: a1 as the float32
+    # chain, a2 from bf16 z1 and W2 (exact products), ambiguous a2 excluded
+    a1 = onn.a1_float32(c.P, c.x)
+    z1q = onn.bf16(np.where(a1 > 0, a1, 0.0))
+    a2 = z1q @ c.P["W2"].T + c.P["b2"]
+    amb2 = np.abs(a2) <= 2.0 ** -16 * (z1q @ np.abs(c.P["W2"]).T + np.abs(c.P["b2"]))
+    print("E=%d ambiguous a2 decisions %d" % (E, int(amb2.sum())))
+    assert np.array_equal(m1, a1 > 0)
+    assert np.array_equal(m2[~amb2], (a2 > 0)[~amb2])
+    # z in bf16: within one rounding of the float32 accumulation of a2
+    z = _positions_natural(_bf16_bits_to_f64(part_e("z").view(np.uint16).reshape(E, H2)), H2)
+    zref = np.where(a2 > 0, a2, 0.0)
+    s2 = z1q @ np.abs(c.P["W2"]).T + np.abs(c.P["b2"])
+    ok = ~amb2
+    assert np.all(np.abs(z - zref)[ok] <= 2.0 ** -8 * np.abs(zref)[ok] + 2.0 ** -15 * s2[ok])
+    fused = H1 == H2 and H1 in (64, 128)
+    if not fused:
+        # z1 bit for bit, and the attributes as bf16 high + low parts
+        z1 = _positions_natural(_bf16_bits_to_f64(part_e("z1").view(np.uint16).reshape(E, H1)), H1)
+        assert np.array_equal(z1, z1q)
+        xs = part_e("x").view(np.uint16).reshape(E, 16)
+        hi, lo = _bf16_bits_to_f64(xs[:, :8]), _bf16_bits_to_f64(xs[:, 8:])
+        de = c.x.shape[1]
+        x32 = c.x.astype(np.float32).astype(np.float64)
+        assert np.array_equal(hi[:, :de], onn.bf16(x32))
+        assert np.array_equal(lo[:, :de], onn.bf16(x32 - onn.bf16(x32)))
+        assert not hi[:, de:].any() and not lo[:, de:].any()
