@@ -223,45 +223,97 @@ __global__ __launch_bounds__(256) void k_sel_hist(int64_t M, uint64_t seed, cons
   }
 }
 
-// One workgroup: thread t owns bins [64t, 64t + 64); a scan of the per-thread
-// counts finds the thread whose bins hold the wanted rank, which fixes the
-// digit.  Every thread clears its bins for the next pass.
-__global__ __launch_bounds__(1024) void k_sel_pick(SelState* st, int shift, uint32_t* __restrict__ hist) {
-  __shared__ uint32_t sh[32];
-  constexpr int PER = SEL_BINS / 1024;
-  uint4* hb = reinterpret_cast<uint4*>(hist + (size_t)threadIdx.x * PER);
-  uint32_t c[PER];
-  uint32_t sum = 0;
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
+  const int lane = threadIdx.x & 63;
 #pragma unroll
-  for (int v = 0; v < PER / 4; ++v) {
-    const uint4 x = hb[v];
-    c[4 * v] = x.x; c[4 * v + 1] = x.y; c[4 * v + 2] = x.z; c[4 * v + 3] = x.w;
-    sum += x.x + x.y + x.z + x.w;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
   }
-  uint32_t tot;
-  const uint32_t ex = block_exclusive_scan_1024(sum, sh, &tot);
-  const uint64_t r = st->rank;
-  __syncthreads();   // every thread has read the rank before it changes
-  if (ex < r && r <= (uint64_t)ex + sum) {
-    uint64_t acc = ex;
+  return x;
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
 #pragma unroll
-    for (int b = 0; b < PER; ++b) {
-      if (acc + c[b] >= r) {
-        st->rank = r - acc;
-        st->prefix |= (uint64_t)(threadIdx.x * PER + b) << shift;
-        break;
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+// One workgroup of 16 waves.  The histogram is read once, in 1 KB pieces
+// that one wave loads whole: piece P = 16 w + v covers bins
+// [256 P, 256 P + 256), lane l of it bins 256 P + 4 l .. + 3.  Every piece's
+// total goes to LDS; wave 0 scans the 256 totals and finds the piece that
+// holds the wanted rank; the wave that read that piece scans its lanes and
+// fixes the digit.  Every wave clears the bins it read for the next pass.
+__global__ __launch_bounds__(1024) void k_sel_pick(SelState* st, int shift, uint32_t* __restrict__ hist) {
+  static_assert(SEL_BINS == 16 * 16 * 256, "16 waves x 16 pieces of 256 bins");
+  __shared__ uint32_t psum[256];
+  __shared__ uint32_t pick[2];   // the piece, and the count of the bins before it
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (threadIdx.x == 0) pick[0] = ~0u;
+  uint4* hb = reinterpret_cast<uint4*>(hist) + (size_t)w * 1024 + lane;
+  uint4 x[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) x[v] = hb[64 * v];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const uint32_t t = wave_sum(x[v].x + x[v].y + x[v].z + x[v].w);
+    if (lane == 0) psum[16 * w + v] = t;
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) hb[64 * v] = make_uint4(0u, 0u, 0u, 0u);
+  const uint64_t r = st->rank;
+  __syncthreads();   // piece totals are in LDS; every thread has read the rank
+  if (w == 0) {
+    const uint32_t a0 = psum[4 * lane], a1 = psum[4 * lane + 1], a2 = psum[4 * lane + 2], a3 = psum[4 * lane + 3];
+    const uint32_t ls = a0 + a1 + a2 + a3;
+    const uint32_t inc = wave_inclusive_scan(ls), ex = inc - ls;
+    if (ex < r && r <= (uint64_t)inc) {
+      uint32_t acc = ex;
+      int P = 4 * lane;
+      if (acc + a0 < r) {
+        acc += a0; ++P;
+        if (acc + a1 < r) {
+          acc += a1; ++P;
+          if (acc + a2 < r) { acc += a2; ++P; }
+        }
       }
-      acc += c[b];
+      pick[0] = (uint32_t)P;
+      pick[1] = acc;
     }
   }
+  __syncthreads();
+  const uint32_t P = pick[0];
+  if (P < 256 && w == (int)(P / 16)) {
+    const int vs = P % 16;
+    uint4 y = x[0];
 #pragma unroll
-  for (int v = 0; v < PER / 4; ++v) hb[v] = make_uint4(0u, 0u, 0u, 0u);
+    for (int v = 1; v < 16; ++v)
+      if (v == vs) y = x[v];
+    const uint32_t ls = y.x + y.y + y.z + y.w;
+    const uint32_t inc = wave_inclusive_scan(ls);
+    const uint64_t base = (uint64_t)pick[1] + (inc - ls);
+    if (base < r && r <= base + ls) {
+      const uint32_t c[4] = {y.x, y.y, y.z, y.w};
+      uint64_t acc = base;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (acc + c[k] >= r) {
+          st->rank = r - acc;
+          st->prefix |= (uint64_t)(256 * P + 4 * lane + k) << shift;
+          break;
+        }
+        acc += c[k];
+      }
+    }
+  }
 }
 
 __global__ __launch_bounds__(1024) void k_sel_init(SelState* st, uint64_t s, uint32_t* hist) {
-  if (threadIdx.x == 0) { st->prefix = 0; st->rank = s; }
+  if (blockIdx.x == 0 && threadIdx.x == 0) { st->prefix = 0; st->rank = s; }
   uint4* hb = reinterpret_cast<uint4*>(hist);
-  for (int v = threadIdx.x; v < SEL_BINS / 4; v += 1024) hb[v] = make_uint4(0u, 0u, 0u, 0u);
+  for (int v = blockIdx.x * 1024 + threadIdx.x; v < SEL_BINS / 4; v += gridDim.x * 1024)
+    hb[v] = make_uint4(0u, 0u, 0u, 0u);
 }
 
 __global__ __launch_bounds__(1024) void k_sel_count(int64_t M, uint64_t seed, const SelState* st,
@@ -328,7 +380,7 @@ extern "C" dsmp_status dsmp_sample_nodes(dsmp_handle* h, int64_t M, int64_t s, u
   uint32_t* hist = c.take<uint32_t>(SEL_BINS);
   int nb = (int)ceil_div(M, SAMPLE_CHUNK);
   uint32_t* cnt = c.take<uint32_t>(nb + 2);
-  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(1024), 0, h->stream, st, (uint64_t)s, hist);
+  hipLaunchKernelGGL(k_sel_init, dim3(SEL_BINS / 4 / 1024), dim3(1024), 0, h->stream, st, (uint64_t)s, hist);
   unsigned g = ceil_div(M, 256);
   if (g > 2048) g = 2048;
   for (int shift = 48; shift >= 0; shift -= 16) {
