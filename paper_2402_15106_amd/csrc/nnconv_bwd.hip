@@ -442,7 +442,8 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 3 : 1) v
       const int64_t i = d0 + k;
       const int64_t pa = a.row_ptr[i], pb = a.row_ptr[i + 1];
       const int64_t c0 = pa + (int64_t)(tau - tstart[k]) * 32;
-      const unsigned char* ur = a.U + ((size_t)i * H2 + l32) * DL * ESZ + hh * EPL * ESZ;
+      // U_i in fragment order: fragment (kt, s) is 64 lanes x EPL elements
+      const unsigned char* ur = a.U + ((size_t)i * H2 * DL + lane * EPL) * ESZ;
       int64_t eid[NT];
       bool valid[NT];
       frag hB[NT][SKD];
@@ -459,7 +460,7 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 3 : 1) v
       for (int kt = 0; kt < KT; ++kt) {
         frag A[SKD];
 #pragma unroll
-        for (int s = 0; s < SKD; ++s) A[s] = ld_frag<T>(ur + ((size_t)kt * 32 * DL + s * KS) * ESZ);
+        for (int s = 0; s < SKD; ++s) A[s] = ld_frag<T>(ur + (size_t)((kt * SKD + s) * 64 * EPL) * ESZ);
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
           acc[t][kt] = f32x16{};
@@ -631,7 +632,7 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
   auto load_uh = [&](const Tile& t, Ops& o) {
     if (!t.has) return;
     const int i = __builtin_amdgcn_readfirstlane(t.i);   // one destination per tile
-    const unsigned char* ur = a.U + ((size_t)i * H2 + l32) * DL * 2 + hh * EPL * 2;
+    const unsigned char* ur = a.U + ((size_t)i * H2 * DL + lane * EPL) * 2;   // fragment order
     const unsigned char* hr = a.h_in + (size_t)t.jn * DL * 2;
 #pragma unroll
     for (int s = 0; s < SKD; ++s) o.hB[s] = ld_frag<__bf16>(hr + (s * KS + hh * EPL) * 2);
@@ -639,7 +640,7 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
     for (int q = 0; q < KTH; ++q)
 #pragma unroll
       for (int s = 0; s < SKD; ++s)
-        o.UA[q][s] = ld_frag<__bf16>(ur + ((size_t)(hf * KTH + q) * 32 * DL + s * KS) * 2);
+        o.UA[q][s] = ld_frag<__bf16>(ur + (size_t)(((hf * KTH + q) * SKD + s) * 64 * EPL) * 2);
   };
   // ... the node attribute rows and z's mask bits (after their use in the
   // first step) and z1's mask bits (after the second step); each load goes
@@ -928,7 +929,7 @@ struct UArgs {
   int64_t n_rows;
   const unsigned char* G;    // [n_rows][DL] layer dtype (g_i)
   const unsigned char* W;    // [h2*DL][DL] layer dtype: W[k*DL + p][q] = W3[p*DL+q][k]
-  unsigned char* U;          // [n_rows][h2*DL] layer dtype
+  unsigned char* U;          // [n_rows][h2*DL] layer dtype, each row in MFMA fragment order
 };
 
 // U[i][c] = sum_q W[c][q] g_i[q] for c = k*DL + p, as tiles C[c][i] (A = W

@@ -805,11 +805,17 @@ __global__ void k_pack(PackArgs a) {
       wht[x] = (T)a.b3[o * d + c];
     }
   }
+  // W3u rows in MFMA fragment order: row c' of the U GEMM is U_i's element
+  // (k, p) that lane l of A fragment (kt, s) holds, c' = ((kt*SKD + s)*64 + l)*EPL + t
+  // with k = 32 kt + l%32 and p = s*KS + (l/32)*EPL + t, so a fragment of U_i
+  // is one contiguous 64-lane piece.
   T* w3u = reinterpret_cast<T*>(a.out + a.L.w3u);
   for (int64_t x = t0; x < (int64_t)h2 * d * d; x += stride) {
     const int q = (int)(x % d);
     const int64_t c = x / d;
-    const int k = (int)(c / d), p = (int)(c % d);
+    const int t = (int)(c % EPL), l = (int)((c / EPL) % 64), fs = (int)(c / (EPL * 64));
+    const int skd = d / KS, kt = fs / skd, sk = fs % skd;
+    const int k = 32 * kt + l % 32, p = sk * KS + (l / 32) * EPL + t;
     w3u[x] = (T)a.W3[((int64_t)p * d + q) * h2 + k];
   }
 }
