@@ -169,6 +169,16 @@ struct RowStage {
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
+typedef __attribute__((address_space(3))) const unsigned char lds_cu8;
+
+__device__ __forceinline__ bf16x8 lds_frag_rows(lds_cu8* X, int pitch, int r0, int c0) {
+  const int l = threadIdx.x & 63, g = l >> 4, j = (l >> 2) & 3, q = l & 3;
+  lds_cu8* p = X + (r0 + 8 * (g >> 1) + j) * pitch + (c0 + 16 * (g & 1) + 4 * q) * 2;
+  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 4 * pitch));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
 __device__ __forceinline__ bf16x8 lds_frag_rows(const unsigned char* X, int pitch, int r0, int c0) {
   const int l = threadIdx.x & 63, g = l >> 4, j = (l >> 2) & 3, q = l & 3;
   const unsigned char* p = X + (r0 + 8 * (g >> 1) + j) * pitch + (c0 + 16 * (g & 1) + 4 * q) * 2;
@@ -243,6 +253,17 @@ __host__ __device__ inline int attr_slots(int dim, int mode) {
 __device__ __forceinline__ float relu_bits(float v) {
   const int i = __float_as_int(v);
   return __int_as_float(i > 0 ? i : 0);
+}
+
+// v where bit `bit` of `word` is set, else +0: the bit, sign-extended to a
+// whole word (one bit-field extract, inline assembly so that it is not
+// turned back into a compare and select), masks the float's bits.  The
+// assembly reads only the mask word; v, which may be a matrix-core result,
+// goes through an ordinary AND.
+__device__ __forceinline__ float keep_if_bit(float v, uint32_t word, int bit) {
+  int m;
+  asm("v_bfe_i32 %0, %1, %2, 1" : "=v"(m) : "v"(word), "i"(bit));
+  return __int_as_float(__float_as_int(v) & m);
 }
 
 // ReLU of v, with its mask bit [v > 0] ORed into position `bit` of `word`.

@@ -233,7 +233,7 @@ __device__ __forceinline__ void dz_finish(const DzArgs& a, const f32x16 (&acc)[N
 #pragma unroll
       for (int u = 0; u < EPL; ++u) {
         const int n = s * EPL + u;
-        v[u] = (m2[n / 32] >> (n % 32)) & 1u ? acc[t][n / 16][n % 16] : 0.0f;
+        v[u] = keep_if_bit(acc[t][n / 16][n % 16], m2[n / 32], n % 32);
       }
       da2B[s] = pack_frag<T>(v);
       if (valid[t]) *reinterpret_cast<frag*>(a.da2E + (e * H2 + s * KS + hh * EPL) * ESZ) = da2B[s];
@@ -256,7 +256,7 @@ __device__ __forceinline__ void dz_finish(const DzArgs& a, const f32x16 (&acc)[N
         const int pos = (n / EPL) * KS + hh * EPL;
         float v[EPL];
 #pragma unroll
-        for (int u = 0; u < EPL; ++u) v[u] = (m1[(n + u) / 32] >> ((n + u) % 32)) & 1u ? C[i + u] : 0.0f;
+        for (int u = 0; u < EPL; ++u) v[u] = keep_if_bit(C[i + u], m1[(n + u) / 32], (n + u) % 32);
         if (valid[t]) *reinterpret_cast<frag*>(a.da1E + (e * H1 + pos) * ESZ) = pack_frag<T>(v);
       }
     }
@@ -714,7 +714,7 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
           const int s = hf * SK1H + 2 * zb + q;
           float zv[EPL];
 #pragma unroll
-          for (int u = 0; u < EPL; ++u) zv[u] = Z[8 * q + u] > 0.0f ? Z[8 * q + u] : 0.0f;
+          for (int u = 0; u < EPL; ++u) zv[u] = relu_bits(Z[8 * q + u]);
           *reinterpret_cast<frag*>(zrow + (s * KS + hh * EPL) * 2) = pack_frag<__bf16>(zv);
         }
       }
@@ -753,7 +753,7 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
 #pragma unroll
       for (int u = 0; u < EPL; ++u) {
         const int n = s * EPL + u;
-        v[u] = (o.m2[n / 32] >> (n % 32)) & 1u ? acc[n / 16 - hf * KTH][n % 16] : 0.0f;
+        v[u] = keep_if_bit(acc[n / 16 - hf * KTH][n % 16], o.m2[n / 32], n % 32);
       }
       da2B[s] = pack_frag<__bf16>(v);
       *reinterpret_cast<frag*>(d2row + (s * KS + hh * EPL) * 2) = da2B[s];
@@ -787,7 +787,7 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
         const int pos = (n / EPL) * KS + hh * EPL;
         float v[EPL];
 #pragma unroll
-        for (int u = 0; u < EPL; ++u) v[u] = (o.m1[(n + u) / 32] >> ((n + u) % 32)) & 1u ? C[i0 + u] : 0.0f;
+        for (int u = 0; u < EPL; ++u) v[u] = keep_if_bit(C[i0 + u], o.m1[(n + u) / 32], (n + u) % 32);
         const frag f = pack_frag<__bf16>(v);
         *reinterpret_cast<frag*>(d1row + pos * 2) = f;
         if (g.da1_out && t.valid) *reinterpret_cast<frag*>(g.da1_out + (e * H1 + pos) * 2) = f;
@@ -801,7 +801,13 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       if (v < nslot) {
-        const unsigned char* st = slots + v * G::SLOT;
+        // The slot's LDS address (past 64 KB, beyond an instruction's offset
+        // field) is formed here from a scalar base, not kept per lane and
+        // region for the whole kernel: that took a register per slot and
+        // region and pushed other values out to scratch.
+        uint32_t sb = (uint32_t)(uintptr_t)(slots + v * G::SLOT);
+        asm volatile("" : "+s"(sb));
+        lds_cu8* st = (lds_cu8*)(uintptr_t)sb;
         const int cnt = slot_cnt[v];
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
