@@ -171,6 +171,19 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 typedef __attribute__((address_space(3))) const unsigned char lds_cu8;
 
+// Padding (16-byte units) after RB bytes of row data that makes the row pitch
+// a bank-conflict-free layout for lds_frag_rows.  LDS has 64 four-byte banks
+// and serves a transposing 8-byte read 32 lanes at a time; those lanes read
+// 16 consecutive dwords of each of 4 consecutive rows, which land on disjoint
+// banks when the pitch is 16 or 48 dwords modulo 64.
+constexpr int tr_pad_units(int rb) {
+  const int d = (rb / 4) % 64;
+  const int a = ((16 - d) % 64 + 64) % 64, b = ((48 - d) % 64 + 64) % 64;
+  return (a < b ? a : b) / 4;
+}
+static_assert(tr_pad_units(512) == 4 && tr_pad_units(128) == 4 && tr_pad_units(64) == 0 &&
+              tr_pad_units(256) == 4 && tr_pad_units(32) == 2, "transposing-read pitches");
+
 __device__ __forceinline__ bf16x8 lds_frag_rows(lds_cu8* X, int pitch, int r0, int c0) {
   const int l = threadIdx.x & 63, g = l >> 4, j = (l >> 2) & 3, q = l & 3;
   lds_cu8* p = X + (r0 + 8 * (g >> 1) + j) * pitch + (c0 + 16 * (g & 1) + 4 * q) * 2;

@@ -176,9 +176,10 @@ __global__ __launch_bounds__(256) void k_outer_sum(OuterArgs a) {
 template <int DL, int H2>
 struct OuterTrShape {
   static constexpr int ECH = 64;
-  static constexpr int ZP = H2 * 2 + 32, UP = DL * 2 + 32;     // LDS row pitches (two padding units)
+  static constexpr int ZPAD = tr_pad_units(H2 * 2), UPAD = tr_pad_units(DL * 2);
+  static constexpr int ZP = H2 * 2 + 16 * ZPAD, UP = DL * 2 + 16 * UPAD;   // LDS row pitches
   static constexpr int ZNU = H2 * 2 / 16, UNU = DL * 2 / 16;   // 16-byte units per row
-  static constexpr int ZU = ECH * (ZNU + 2), UU = ECH * (UNU + 2);
+  static constexpr int ZU = ECH * (ZNU + ZPAD), UU = ECH * (UNU + UPAD);
   static constexpr int NKT = H2 / 32, NCT = DL / 32, NTILE = NKT * NCT, TPW = (NTILE + 3) / 4;
   static constexpr int LDS = ECH * (ZP + UP);
   static constexpr int64_t KTOT = (int64_t)H2 * DL + DL;
@@ -214,14 +215,14 @@ __global__ __launch_bounds__(256) void k_outer_sum_tr(OuterArgs a) {
     __syncthreads();
     const int wbase = tid & ~63;
     for (int U0 = 0; U0 < S::ZU; U0 += 256) {
-      const int U = U0 + tid, r = U / (S::ZNU + 2), u = U % (S::ZNU + 2);
+      const int U = U0 + tid, r = U / (S::ZNU + S::ZPAD), u = U % (S::ZNU + S::ZPAD);
       if (U < S::ZU)
         __builtin_amdgcn_global_load_lds(
             (gbl_void_t*)(a.zE + (size_t)rz[r < ECH ? r : ECH - 1] * H2 * 2 + (u < S::ZNU ? u : 0) * 16),
             (lds_void_t*)(zl + (size_t)(U0 + wbase) * 16), 16, 0, 0);
     }
     for (int U0 = 0; U0 < S::UU; U0 += 256) {
-      const int U = U0 + tid, r = U / (S::UNU + 2), u = U % (S::UNU + 2);
+      const int U = U0 + tid, r = U / (S::UNU + S::UPAD), u = U % (S::UNU + S::UPAD);
       if (U < S::UU)
         __builtin_amdgcn_global_load_lds(
             (gbl_void_t*)(a.u + (size_t)ru[r < ECH ? r : ECH - 1] * DL * 2 + (u < S::UNU ? u : 0) * 16),
@@ -443,8 +444,8 @@ __global__ __launch_bounds__(256) void k_dw3_agg(DW3AggArgs a) {
 template <int DL>
 struct DW3TrShape {
   static constexpr int ECH = 32, KR = 256;
-  using SS = RowStage<ECH, KR * 2, 2>;
-  using GS = RowStage<ECH, DL * 2, 2>;
+  using SS = RowStage<ECH, KR * 2, tr_pad_units(KR * 2)>;
+  using GS = RowStage<ECH, DL * 2, tr_pad_units(DL * 2)>;
   static constexpr int SB = ECH * SS::PITCH, BUF = SB + ECH * GS::PITCH, LDS = 2 * BUF;
   static constexpr int NQT = DL / 32, NKT = KR / 32, TPW = NQT * NKT / 4;
   static_assert(TPW % 4 == 0 || TPW == 2, "K tiles per wave");

@@ -1373,8 +1373,8 @@ __global__ __launch_bounds__(256, 2) void k_bwd_dW2(W2Args a) {
 template <int H1, int H2>
 struct W2TrShape {
   static constexpr int ECH = 64;
-  using DS = RowStage<ECH, H2 * 2, 2>;
-  using ZS = RowStage<ECH, H1 * 2, 2>;
+  using DS = RowStage<ECH, H2 * 2, tr_pad_units(H2 * 2)>;
+  using ZS = RowStage<ECH, H1 * 2, tr_pad_units(H1 * 2)>;
   static constexpr int DB = ECH * DS::PITCH, BUF = DB + ECH * ZS::PITCH, LDS = 2 * BUF;
 };
 
@@ -1517,8 +1517,8 @@ __global__ __launch_bounds__(256) void k_bwd_dW1(int64_t E, int64_t per_chunk, c
 template <int H1>
 struct W1TrShape {
   static constexpr int ECH = 64;
-  using AS = RowStage<ECH, H1 * 2, 2>;
-  using XS = RowStage<ECH, 32, 4>;   // 32 bytes of attributes per row, pitch 96
+  using AS = RowStage<ECH, H1 * 2, tr_pad_units(H1 * 2)>;
+  using XS = RowStage<ECH, 32, tr_pad_units(32)>;   // 32 bytes of attributes per row, pitch 64
   static constexpr int AB = ECH * AS::PITCH, BUF = AB + ECH * XS::PITCH, LDS = 2 * BUF;
   static constexpr int JT = H1 / 32, JTW = (JT + 3) / 4;
 };
