@@ -82,14 +82,27 @@ __global__ __launch_bounds__(256) void k_outer_rows(int64_t n, int din, int dout
 
 dim3 outer_grid(int np, int din, int dout) { return dim3(np, ceil_div(dout * (din + 1), 256)); }
 
-// dW[o][i] (+)= sum_c part[c][o][i], db[o] (+)= sum_c part[c][o][din].  A
-// block serves 64 pairs; its four waves sum the partials c = g, g+4, ... in
-// order and the four sums are added in wave order (a fixed order).
-__global__ __launch_bounds__(256) void k_outer_final(int nparts, int din, int dout, const float* __restrict__ part,
-                                                     float* __restrict__ dW, float* __restrict__ db, int accumulate) {
+// dW[o][i] (+)= sum_c part[c][o][i], db[o] (+)= sum_c part[c][o][din], for
+// the three weight gradients of a perceptron in one launch: segment m takes
+// the blocks [first[m], first[m + 1]).  A block serves 64 pairs; its four
+// waves sum the partials c = g, g+4, ... in order and the four sums are
+// added in wave order (a fixed order).
+struct OuterFinal3 {
+  const float* part[3];
+  float* dW[3];
+  float* db[3];
+  int din[3], dout[3], first[4];
+  int nparts, accumulate;
+};
+
+
+__global__ __launch_bounds__(256) void k_outer_final3(OuterFinal3 a) {
   __shared__ float sh[4][64];
+  const int m = (int)blockIdx.x < a.first[1] ? 0 : (int)blockIdx.x < a.first[2] ? 1 : 2;
+  const int din = a.din[m], dout = a.dout[m], nparts = a.nparts;
+  const float* part = a.part[m];
   const int pairs = dout * (din + 1);
-  const int p = blockIdx.x * 64 + (threadIdx.x & 63), g = threadIdx.x >> 6;
+  const int p = ((int)blockIdx.x - a.first[m]) * 64 + (threadIdx.x & 63), g = threadIdx.x >> 6;
   float v = 0.0f;
   if (p < pairs) {
 #pragma unroll 8
@@ -100,8 +113,8 @@ __global__ __launch_bounds__(256) void k_outer_final(int nparts, int din, int do
   if (g == 0 && p < pairs) {
     v = sh[0][threadIdx.x] + sh[1][threadIdx.x] + sh[2][threadIdx.x] + sh[3][threadIdx.x];
     const int o = p / (din + 1), i = p % (din + 1);
-    float* t = i < din ? dW + (int64_t)o * din + i : db + o;
-    *t = accumulate ? *t + v : v;
+    float* t = i < din ? a.dW[m] + (int64_t)o * din + i : a.db[m] + o;
+    *t = a.accumulate ? *t + v : v;
   }
 }
 
@@ -230,6 +243,216 @@ __global__ __launch_bounds__(256) void k_mlp_bwd(MlpArgs a) {
   outer_block(cnt, a.din, a.dh, g1, xs, a.p1 + b * a.dh * (a.din + 1));
 }
 
+// Matrix-core forms of the fused passes, for hidden widths that are whole
+// 32-column tiles.  Every product is a chain of fp32 32x32x2 MFMA steps in
+// contraction order (the accumulator starting from the bias, or zero), which
+// rounds as the fused multiply-add chains above do.  Matrices sit in LDS in
+// their natural row-major layout with one float of row padding, so both the
+// row-indexed and the column-indexed operand reads are free of bank
+// conflicts; rows of a tile past its end hold zeros.
+typedef float f32x16m __attribute__((ext_vector_type(16)));
+
+// C += sum over k < K of A(r, k) B(k, c) for the 32x32 block of rows
+// [0, 32) and columns [c0, c0 + 32): A row-major with pitch pa, B given as
+// Bt row-major [c][k] (pitch pb, rows >= nc read as zero), two k per step.
+__device__ __forceinline__ f32x16m mchain_rows(f32x16m C, int K, const float* A, int pa, const float* Bt, int pb,
+                                              int c0, int nc) {
+  const int l = threadIdx.x & 63, r = l & 31, h = l >> 5;
+  const bool cv = c0 + r < nc;
+  for (int kk = 0; kk < K; kk += 2) {
+    const int k = kk + h;
+    const float av = k < K ? A[r * pa + k] : 0.0f;
+    const float bv = k < K && cv ? Bt[(c0 + r) * pb + k] : 0.0f;
+    C = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, C, 0, 0, 0);
+  }
+  return C;
+}
+
+// The same with B row-major [k][c] (pitch pb, columns >= nc read as zero).
+__device__ __forceinline__ f32x16m mchain_cols(f32x16m C, int K, const float* A, int pa, const float* B, int pb,
+                                              int c0, int nc) {
+  const int l = threadIdx.x & 63, r = l & 31, h = l >> 5;
+  const bool cv = c0 + r < nc;
+  for (int kk = 0; kk < K; kk += 2) {
+    const int k = kk + h;
+    const float av = k < K ? A[r * pa + k] : 0.0f;
+    const float bv = k < K && cv ? B[k * pb + c0 + r] : 0.0f;
+    C = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, C, 0, 0, 0);
+  }
+  return C;
+}
+
+// out[r][o] = act(b[o] + sum_k in[r][k] W[o][k]) for the tile's rows, one
+// 32-column block per wave in turn; to LDS (pitch O + 1) and global memory.
+__device__ __forceinline__ void mdense(int cnt, int K, int O, const float* in_s, const float* W_s, const float* b,
+                                       int relu, float* out_s, float* out_g, __bf16* out_bf16) {
+  const int l = threadIdx.x & 63, wv = threadIdx.x >> 6, r = l & 31, h = l >> 5;
+  for (int ob = wv; ob * 32 < O; ob += 4) {
+    const int c = ob * 32 + r;
+    const float bc = c < O ? b[c] : 0.0f;
+    f32x16m C;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) C[i] = bc;
+    C = mchain_rows(C, K, in_s, K + 1, W_s, K + 1, ob * 32, O);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int row = 8 * (i / 4) + 4 * h + (i % 4);
+      float v = C[i];
+      if (relu && !(v > 0.0f)) v = 0.0f;
+      if (c < O) {
+        if (out_s) out_s[row * (O + 1) + c] = row < cnt ? v : 0.0f;
+        if (row < cnt) {
+          if (out_g) out_g[(int64_t)row * O + c] = v;
+          if (out_bf16) out_bf16[(int64_t)row * O + c] = (__bf16)v;
+        }
+      }
+    }
+  }
+}
+
+// gin[r][k] = [mask[r][k] > 0] * sum_o g[r][o] W[o][k]: A = g (pitch O + 1),
+// B = W row-major [o][k] (pitch K + 1); to LDS (pitch K + 1) and/or global.
+__device__ __forceinline__ void mdense_back(int cnt, int K, int O, const float* g_s, const float* W_s,
+                                            const float* mask_s, float* out_s, float* out_g, int accumulate) {
+  const int l = threadIdx.x & 63, wv = threadIdx.x >> 6, r = l & 31, h = l >> 5;
+  for (int kb = wv; kb * 32 < K; kb += 4) {
+    const int c = kb * 32 + r;
+    f32x16m C = f32x16m{};
+    C = mchain_cols(C, O, g_s, O + 1, W_s, K + 1, kb * 32, K);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int row = 8 * (i / 4) + 4 * h + (i % 4);
+      if (c >= K) continue;
+      float v = C[i];
+      if (mask_s && !(mask_s[row * (K + 1) + c] > 0.0f)) v = 0.0f;
+      if (out_s) out_s[row * (K + 1) + c] = row < cnt ? v : 0.0f;
+      if (out_g && row < cnt) {
+        float* t = out_g + (int64_t)row * K + c;
+        *t = accumulate ? *t + v : v;
+      }
+    }
+  }
+}
+
+// part[o][k] = sum over the tile's rows r of g[r][o] in[r][k] (k < K) and
+// part[o][K] = sum of g[r][o]: rows of the product are o (A = g transposed,
+// read as g[r][o]), its contraction index the tile's rows.
+__device__ __forceinline__ void mouter(int K, int O, const float* g_s, const float* in_s, float* part) {
+  const int l = threadIdx.x & 63, wv = threadIdx.x >> 6, r = l & 31, h = l >> 5;
+  const int nob = (O + 31) / 32, nkb = (K + 1 + 31) / 32;
+  for (int t = wv; t < nob * nkb; t += 4) {
+    const int ob = t / nkb, kb = t % nkb;
+    const int o = ob * 32 + r, c = kb * 32 + r;
+    f32x16m C = f32x16m{};
+    for (int kk = 0; kk < FR; kk += 2) {
+      const int rr = kk + h;
+      const float av = o < O ? g_s[rr * (O + 1) + o] : 0.0f;
+      const float bv = c < K ? in_s[rr * (K + 1) + c] : (c == K ? 1.0f : 0.0f);
+      C = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, C, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int oo = ob * 32 + 8 * (i / 4) + 4 * h + (i % 4);
+      if (oo < O && c <= K) part[oo * (K + 1) + c] = C[i];
+    }
+  }
+}
+
+// A [rows][w] row-major global matrix (w <= 256) to LDS with pitch w + 1,
+// rows past `valid` as zeros: each thread keeps one column and steps over
+// the rows 256 / w at a time (one division per thread, none per element).
+__device__ __forceinline__ void stage_mat(float* dst, const float* src, int rows, int w, int valid) {
+  const int per = 256 / w, t = threadIdx.x, r0 = t / w, c = t - r0 * w;
+  if (r0 >= per) return;
+  for (int rr = r0; rr < rows; rr += per)
+    dst[rr * (w + 1) + c] = rr < valid ? src[(int64_t)rr * w + c] : 0.0f;
+}
+
+// Rows [0, cnt) of a [*][w] global matrix to LDS with pitch w + 1, zeros past cnt.
+__device__ __forceinline__ void stage_rows(float* dst, const float* src, int cnt, int w) {
+  stage_mat(dst, src, FR, w, cnt);
+}
+
+struct MlpLdsM {
+  int w1, w2, w3, x, s1, s2, g3, g2, g1, fwd, bwd;   // float offsets / totals
+};
+
+__host__ __device__ inline MlpLdsM mlp_lds_m(int din, int dh, int dout) {
+  MlpLdsM m;
+  m.w1 = 0;
+  m.w2 = m.w1 + dh * (din + 1);
+  m.w3 = m.w2 + dh * (dh + 1);
+  m.x = m.w3 + dout * (dh + 1);
+  m.s1 = m.x + FR * (din + 1);
+  m.s2 = m.s1 + FR * (dh + 1);
+  m.fwd = m.s2 + FR * (dh + 1);
+  m.g3 = m.fwd;
+  m.g2 = m.g3 + FR * (dout + 1);
+  m.g1 = m.g2 + FR * (dh + 1);
+  m.bwd = m.g1 + FR * (dh + 1);
+  return m;
+}
+
+__global__ __launch_bounds__(256) void k_mlp_fwd_m(MlpArgs a) {
+  extern __shared__ float sm[];
+  const MlpLdsM m = mlp_lds_m(a.din, a.dh, a.dout);
+  stage_mat(sm + m.w1, a.W1, a.dh, a.din, a.dh);
+  stage_mat(sm + m.w2, a.W2, a.dh, a.dh, a.dh);
+  stage_mat(sm + m.w3, a.W3, a.dout, a.dh, a.dout);
+  const int64_t ntile = (a.n + FR - 1) / FR;
+  for (int64_t tile = blockIdx.x; tile < ntile; tile += gridDim.x) {
+    const int64_t r0 = tile * FR;
+    const int cnt = (int)std::min<int64_t>(FR, a.n - r0);
+    __syncthreads();   // weights staged / the previous tile consumed
+    stage_rows(sm + m.x, a.x + r0 * a.din, cnt, a.din);
+    __syncthreads();
+    mdense(cnt, a.din, a.dh, sm + m.x, sm + m.w1, a.b1, 1, sm + m.s1, a.h1 + r0 * a.dh, nullptr);
+    __syncthreads();
+    mdense(cnt, a.dh, a.dh, sm + m.s1, sm + m.w2, a.b2, 1, sm + m.s2, a.h2 + r0 * a.dh, nullptr);
+    __syncthreads();
+    mdense(cnt, a.dh, a.dout, sm + m.s2, sm + m.w3, a.b3, 0, nullptr, a.y + r0 * a.dout,
+           a.y_bf16 ? a.y_bf16 + r0 * a.dout : nullptr);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_mlp_bwd_m(MlpArgs a) {
+  extern __shared__ float sm[];
+  const MlpLdsM m = mlp_lds_m(a.din, a.dh, a.dout);
+  const int64_t r0 = (int64_t)blockIdx.x * FR;
+  const int cnt = (int)std::min<int64_t>(FR, a.n - r0);
+  stage_mat(sm + m.w1, a.W1, a.dh, a.din, a.dh);
+  stage_mat(sm + m.w2, a.W2, a.dh, a.dh, a.dh);
+  stage_mat(sm + m.w3, a.W3, a.dout, a.dh, a.dout);
+  stage_rows(sm + m.x, a.x + r0 * a.din, cnt, a.din);
+  stage_rows(sm + m.g3, a.gy + r0 * a.dout, cnt, a.dout);
+  stage_rows(sm + m.s1, a.h1 + r0 * a.dh, cnt, a.dh);
+  stage_rows(sm + m.s2, a.h2 + r0 * a.dh, cnt, a.dh);
+  __syncthreads();
+  mdense_back(cnt, a.dh, a.dout, sm + m.g3, sm + m.w3, sm + m.s2, sm + m.g2, nullptr, 0);
+  __syncthreads();
+  mdense_back(cnt, a.dh, a.dh, sm + m.g2, sm + m.w2, sm + m.s1, sm + m.g1, nullptr, 0);
+  __syncthreads();
+  if (a.gx) mdense_back(cnt, a.din, a.dh, sm + m.g1, sm + m.w1, nullptr, nullptr, a.gx + r0 * a.din, a.gx_acc);
+  const int64_t b = blockIdx.x;
+  mouter(a.dh, a.dout, sm + m.g3, sm + m.s2, a.p3 + b * a.dout * (a.dh + 1));
+  mouter(a.dh, a.dh, sm + m.g2, sm + m.s1, a.p2 + b * a.dh * (a.dh + 1));
+  mouter(a.din, a.dh, sm + m.g1, sm + m.x, a.p1 + b * a.dh * (a.din + 1));
+}
+
+// LDS bytes of the matrix-core passes (at most 96 KB: two workgroups per
+// CU); 0 when they do not apply
+int mfma_lds(const dsmp_mlp_desc& d) {
+  if (d.d_hid % 32 != 0) return 0;
+  const MlpLdsM m = mlp_lds_m(d.d_in, d.d_hid, d.d_out);
+  const size_t bytes = (size_t)std::max(m.fwd, m.bwd) * sizeof(float);
+  return bytes <= 96 * 1024 ? (int)bytes : 0;
+}
+
+dsmp_status allow_lds(dsmp_handle* h, const void* kern, int bytes) {
+  DSMP_HIP(h, hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes));
+  return DSMP_OK;
+}
+
 // LDS bytes of the fused passes; 0 when either does not fit (64 KB)
 int fused_fwd_lds(const dsmp_mlp_desc& d) {
   return (int)(((size_t)d.d_in * d.d_hid + (size_t)d.d_hid * d.d_hid + (size_t)d.d_hid * d.d_out +
@@ -324,7 +547,7 @@ struct MlpWs {
 MlpWs mlp_ws(const dsmp_mlp_desc& d, int64_t n, void* base) {
   Carve c(base);
   MlpWs w;
-  w.nparts = (int)std::max<int64_t>(1, ceil_div(n, fused_lds(d) ? FR : ROWS_PER_PART));
+  w.nparts = (int)std::max<int64_t>(1, ceil_div(n, (mfma_lds(d) || fused_lds(d)) ? FR : ROWS_PER_PART));
   w.g2 = c.take<float>((size_t)n * d.d_hid);
   w.g1 = c.take<float>((size_t)n * d.d_hid);
   w.p3 = c.take<float>((size_t)w.nparts * d.d_out * (d.d_hid + 1));
@@ -370,6 +593,15 @@ extern "C" dsmp_status dsmp_mlp_forward(dsmp_handle* h, const dsmp_mlp_desc* des
   if (n == 0) return DSMP_OK;
   ProfScope prof(h, DSMP_K_MLP);
   hipStream_t st_ = h->stream;
+  if (const int lds = mfma_lds(d)) {
+    MlpArgs a{n, d.d_in, d.d_hid, d.d_out, p->W1, p->b1, p->W2, p->b2, p->W3, p->b3, x, s.h1, s.h2, y,
+              static_cast<__bf16*>(y_bf16), nullptr, nullptr, 0, nullptr, nullptr, nullptr};
+    const int64_t grid = std::min<int64_t>(ceil_div(n, FR), (int64_t)h->n_cu * 2);
+    if ((st = allow_lds(h, reinterpret_cast<const void*>(k_mlp_fwd_m), lds)) != DSMP_OK) return st;
+    hipLaunchKernelGGL(k_mlp_fwd_m, dim3((unsigned)grid), dim3(256), lds, st_, a);
+    DSMP_LAUNCHED(h, "perceptron forward");
+    return DSMP_OK;
+  }
   if (const int lds = fused_lds(d)) {
     MlpArgs a{n, d.d_in, d.d_hid, d.d_out, p->W1, p->b1, p->W2, p->b2, p->W3, p->b3, x, s.h1, s.h2, y,
               static_cast<__bf16*>(y_bf16), nullptr, nullptr, 0, nullptr, nullptr, nullptr};
@@ -413,7 +645,12 @@ extern "C" dsmp_status dsmp_mlp_backward(dsmp_handle* h, const dsmp_mlp_desc* de
   ProfScope prof(h, DSMP_K_MLP);
   hipStream_t q = h->stream;
   const int np = n > 0 ? w.nparts : 0;
-  if (n > 0 && fused_lds(d)) {
+  if (n > 0 && mfma_lds(d)) {
+    MlpArgs a{n, d.d_in, d.d_hid, d.d_out, p->W1, p->b1, p->W2, p->b2, p->W3, p->b3, x, s.h1, s.h2, nullptr,
+              nullptr, grad_y, grad_x, (flags & DSMP_GRAD_X_ACCUMULATE) ? 1 : 0, w.p3, w.p2, w.p1};
+    if ((st = allow_lds(h, reinterpret_cast<const void*>(k_mlp_bwd_m), mfma_lds(d))) != DSMP_OK) return st;
+    hipLaunchKernelGGL(k_mlp_bwd_m, dim3(np), dim3(256), mfma_lds(d), q, a);
+  } else if (n > 0 && fused_lds(d)) {
     MlpArgs a{n, d.d_in, d.d_hid, d.d_out, p->W1, p->b1, p->W2, p->b2, p->W3, p->b3, x, s.h1, s.h2, nullptr,
               nullptr, grad_y, grad_x, (flags & DSMP_GRAD_X_ACCUMULATE) ? 1 : 0, w.p3, w.p2, w.p1};
     hipLaunchKernelGGL(k_mlp_bwd, dim3(np), dim3(256), fused_lds(d), q, a);
@@ -434,12 +671,10 @@ extern "C" dsmp_status dsmp_mlp_backward(dsmp_handle* h, const dsmp_mlp_desc* de
                          (const float*)nullptr, grad_x, (flags & DSMP_GRAD_X_ACCUMULATE) ? 1 : 0);
   }
   // with no rows the partial count is 0 and the finals write zeros (or add nothing)
-  hipLaunchKernelGGL(k_outer_final, dim3(ceil_div(d.d_out * (d.d_hid + 1), 64)), dim3(256), 0, q, np, d.d_hid,
-                     d.d_out, w.p3, grads->dW3, grads->db3, acc);
-  hipLaunchKernelGGL(k_outer_final, dim3(ceil_div(d.d_hid * (d.d_hid + 1), 64)), dim3(256), 0, q, np, d.d_hid,
-                     d.d_hid, w.p2, grads->dW2, grads->db2, acc);
-  hipLaunchKernelGGL(k_outer_final, dim3(ceil_div(d.d_hid * (d.d_in + 1), 64)), dim3(256), 0, q, np, d.d_in,
-                     d.d_hid, w.p1, grads->dW1, grads->db1, acc);
+  OuterFinal3 f{{w.p3, w.p2, w.p1}, {grads->dW3, grads->dW2, grads->dW1}, {grads->db3, grads->db2, grads->db1},
+                {d.d_hid, d.d_hid, d.d_in}, {d.d_out, d.d_hid, d.d_hid}, {0, 0, 0, 0}, np, acc};
+  for (int m = 0; m < 3; ++m) f.first[m + 1] = f.first[m] + (int)ceil_div(f.dout[m] * (f.din[m] + 1), 64);
+  hipLaunchKernelGGL(k_outer_final3, dim3((unsigned)f.first[3]), dim3(256), 0, q, f);
   DSMP_LAUNCHED(h, "perceptron backward");
   return DSMP_OK;
 }
