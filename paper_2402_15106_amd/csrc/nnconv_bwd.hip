@@ -475,10 +475,14 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 3 : 1) v
 }
 
 // Fused edge gradients of the aggregate form (bf16 layers, h1 = h2 <= 128).
-// One pass over the 32-edge tiles of k_bwd_dz_agg computes dz = U_i h_j, the
-// masked da2, dz1 = W2^T da2 and da1 (as there), and folds the per-edge
+// One pass over 32-edge tiles computes dz = U_i h_j, the masked da2,
+// dz1 = W2^T da2 and da1 (as k_bwd_dz_agg does), and folds the per-edge
 // weight gradients straight into per-workgroup sums, so da2 and da1 never go
-// to HBM:
+// to HBM.  A workgroup takes blocks of 16 destinations; a tile is 32
+// consecutive edges of the block's rows, so it may cross destinations: dz
+// runs once per destination in the tile, with the B operand restricted to
+// that destination's lanes (every tile is full but the block's last, where a
+// tile per destination would leave most tails part-empty).  The sums:
 //   dW2[k][j] = sum_e da2_e[k] z1_e[j],  db2 = sum_e da2_e,
 //   dW1[j][c] = sum_e da1_e[j] x_e[c],   db1 = sum_e da1_e.
 // A workgroup of eight waves takes four tiles per round; the two waves of a
@@ -566,7 +570,7 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
   stage_wait();
   __syncthreads();   // W2^T and the layer-1 weights are in LDS
 
-  __shared__ int tstart[DZ_NB + 1], rps[DZ_NB + 1];
+  __shared__ int rps[DZ_NB + 1];
   __shared__ int slot_cnt[4];
   unsigned char* myslot = slots + pr * G::SLOT;
   // A operands of the z1 product, built each round from the fp32 weights in
@@ -597,9 +601,12 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
     f1 = pack_frag<__bf16>(v1);
   };
 
-  // a tile of the current block: destination, first edge, the lane's edge
+  // a tile of the current block: 32 consecutive edges of the block's edge
+  // range (destinations d0 .. d0 + nd - 1, rows in order), which may span
+  // several destinations: the first and last of them, the first edge, the
+  // lane's edge, its source and its destination
   struct Tile {
-    int i, c0, eid, cnt, jn;   // graph indices are int32
+    int i0, i1, c0, eid, cnt, jn, dn;   // graph indices are int32
     bool has, valid;
   };
   // the operands of a tile: gathered row, the half's rows of U_i, mask bits, node attribute rows
@@ -610,29 +617,34 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
   };
   int d0 = 0;
   int ntile = 0;
+  int nd = 0;
   auto locate = [&](int tau, Tile& t) {
     t.has = tau < ntile;
-    t.i = d0; t.c0 = 0; t.eid = 0; t.cnt = 0; t.valid = false;
+    t.i0 = t.i1 = d0; t.c0 = 0; t.eid = 0; t.cnt = 0; t.valid = false;
     if (!t.has) return;
-    // destination of tile tau: the number of tile-list starts at or below it, minus one
-    const int ts = lane < DZ_NB ? tstart[lane + 1] : 0x7fffffff;
-    const int k = __popcll(__ballot(ts <= tau));
-    const int pa = rps[k], pb = rps[k + 1];
-    t.i = d0 + k;
-    t.c0 = pa + (tau - tstart[k]) * 32;
+    const int pe = rps[nd];
+    t.c0 = rps[0] + tau * 32;
     t.eid = t.c0 + l32;
-    t.valid = t.eid < pb;
-    t.cnt = pb - t.c0 < 32 ? pb - t.c0 : 32;
+    t.valid = t.eid < pe;
+    t.cnt = pe - t.c0 < 32 ? pe - t.c0 : 32;
+    // destination of an edge of the block: the number of row ends at or below it
+    const int re = lane < nd ? rps[lane + 1] : 0x7fffffff;
+    t.i0 = d0 + __popcll(__ballot(re <= t.c0));
+    t.i1 = d0 + __popcll(__ballot(re <= t.c0 + t.cnt - 1));
   };
   // Loads are unconditional (lanes past the tile read edge 0) so that no
   // select waits on them; the dz part zeroes those lanes.
-  auto load_col = [&](Tile& t) { t.jn = a.col[t.valid ? t.eid : 0]; };
+  auto load_col = [&](Tile& t) {
+    const int e = t.valid ? t.eid : 0;
+    t.jn = a.col[e];
+    t.dn = a.dst[e];
+  };
   // the gathered row and the half's rows of U_i (issued as soon as the
   // previous tile's products have read those registers) ...
   auto load_uh = [&](const Tile& t, Ops& o) {
     if (!t.has) return;
-    const int i = __builtin_amdgcn_readfirstlane(t.i);   // one destination per tile
-    const unsigned char* ur = a.U + ((size_t)i * H2 * DL + lane * EPL) * 2;   // fragment order
+    const int i = __builtin_amdgcn_readfirstlane(t.i0);   // the tile's first destination
+    const unsigned char* ub = a.U + (size_t)i * (H2 * DL * 2);   // fragment order
     const unsigned char* hr = a.h_in + (size_t)t.jn * DL * 2;
 #pragma unroll
     for (int s = 0; s < SKD; ++s) o.hB[s] = ld_frag<__bf16>(hr + (s * KS + hh * EPL) * 2);
@@ -640,7 +652,7 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
     for (int q = 0; q < KTH; ++q)
 #pragma unroll
       for (int s = 0; s < SKD; ++s)
-        o.UA[q][s] = ld_frag<__bf16>(ur + (size_t)(((hf * KTH + q) * SKD + s) * 64 * EPL) * 2);
+        o.UA[q][s] = ld_frag<__bf16>(ub + (uint32_t)((((hf * KTH + q) * SKD + s) * 64 + lane) * EPL * 2));
   };
   // ... the node attribute rows and z's mask bits (after their use in the
   // first step) and z1's mask bits (after the second step); each load goes
@@ -648,8 +660,7 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
   auto load_attr = [&](const Tile& t, Ops& o) {
     if (!t.has) return;
     const int nw = g.dim + 1;
-    const int i = __builtin_amdgcn_readfirstlane(t.i);
-    const float* vi = g.node_attr + (size_t)i * nw;
+    const float* vi = g.node_attr + (size_t)t.dn * nw;
     const float* vj = g.node_attr + (size_t)t.jn * nw;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
@@ -736,12 +747,31 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
 #pragma unroll
     for (int s = 0; s < SKD; ++s)
       if (!t.valid) o.hB[s] = frag{};
+    // dz = U_i h_j, one destination of the tile at a time: the B operand
+    // keeps the lanes whose edge goes into that destination (U of the first
+    // one was loaded a round ahead, the others are loaded here)
     f32x16 acc[KTH];
 #pragma unroll
-    for (int q = 0; q < KTH; ++q) {
-      acc[q] = f32x16{};
+    for (int q = 0; q < KTH; ++q) acc[q] = f32x16{};
+    for (int i = t.i0; i <= t.i1; ++i) {
+      const bool mine = t.dn == i;
+      if (__ballot(mine) == 0) continue;   // a destination without edges
+      if (i != t.i0) {
+        // a scalar row base and 32-bit lane offsets
+        const unsigned char* ub = a.U + (size_t)__builtin_amdgcn_readfirstlane(i) * (H2 * DL * 2);
 #pragma unroll
-      for (int s = 0; s < SKD; ++s) acc[q] = M::mma(o.UA[q][s], o.hB[s], acc[q]);
+        for (int q = 0; q < KTH; ++q)
+#pragma unroll
+          for (int s = 0; s < SKD; ++s)
+            o.UA[q][s] = ld_frag<__bf16>(ub + (uint32_t)((((hf * KTH + q) * SKD + s) * 64 + lane) * EPL * 2));
+      }
+      frag hBm[SKD];
+#pragma unroll
+      for (int s = 0; s < SKD; ++s) hBm[s] = mine ? o.hB[s] : frag{};
+#pragma unroll
+      for (int q = 0; q < KTH; ++q)
+#pragma unroll
+        for (int s = 0; s < SKD; ++s) acc[q] = M::mma(o.UA[q][s], hBm[s], acc[q]);
     }
     load_uh(nxt, o);   // the products above have read these registers
     // da2 = dz [z > 0] for the half's positions n = 16 kt + i (frags s = n / EPL)
@@ -870,22 +900,10 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
   const int64_t nblk = (a.n_dst + DZ_NB - 1) / DZ_NB;
   for (int64_t blk = blockIdx.x; blk < nblk; blk += gridDim.x) {
     d0 = (int)(blk * DZ_NB);
-    const int nd = (int)(a.n_dst - d0 < DZ_NB ? a.n_dst - d0 : DZ_NB);
-    if (wv == 0) {
-      int nt = 0, rp = 0;
-      if (lane <= nd) rp = a.row_ptr[d0 + lane];
-      if (lane < nd) nt = (a.row_ptr[d0 + lane + 1] - rp + 31) / 32;
-#pragma unroll
-      for (int o = 1; o < DZ_NB; o <<= 1) {
-        const int v = __shfl_up(nt, o, 64);
-        if (lane >= o) nt += v;
-      }
-      if (lane < DZ_NB) tstart[lane + 1] = nt;
-      if (lane == 0) tstart[0] = 0;
-      if (lane <= nd) rps[lane] = rp;
-    }
+    nd = (int)(a.n_dst - d0 < DZ_NB ? a.n_dst - d0 : DZ_NB);
+    if (wv == 0 && lane <= nd) rps[lane] = a.row_ptr[d0 + lane];
     lds_barrier();
-    ntile = tstart[nd];
+    ntile = (rps[nd] - rps[0] + 31) / 32;
     Tile tA, tB;
     locate(pr, tA);
     load_col(tA);
