@@ -917,7 +917,7 @@ __global__ __launch_bounds__(512, 1) void k_bwd_edge_agg(EdgeGradArgs g) {
       round(r0, tA, tB);
       if (r0 + 4 < ntile) round(r0 + 4, tB, tA);
     }
-    lds_barrier();   // the block's lists are read until every wave is done
+    lds_barrier();   // the block's row pointers are read until every wave is done
   }
   // ---- partial sums of this workgroup (stored positions mapped back to k, j)
   float* o2 = g.p_w2 + (size_t)blockIdx.x * (H2 * H1 + H2);
