@@ -75,6 +75,31 @@ __global__ __launch_bounds__(1024) void k_scan_final(const uint32_t* __restrict_
   if (blockIdx.x == 0 && threadIdx.x == 0) out[n] = (int32_t)sums[nb];
 }
 
+// Exclusive scan of up to 16 * 1024 values by one workgroup in one launch:
+// thread t takes SCAN_PER consecutive values, the per-thread totals are
+// scanned across the block, and each thread writes its values' prefixes;
+// out[n] = total.
+constexpr int SCAN_PER = 16;
+__global__ __launch_bounds__(1024) void k_scan_single(const uint32_t* __restrict__ in, int64_t n,
+                                                      int32_t* __restrict__ out) {
+  __shared__ uint32_t sh[32];
+  const int64_t b = (int64_t)threadIdx.x * SCAN_PER;
+  uint32_t v[SCAN_PER], sum = 0;
+#pragma unroll
+  for (int k = 0; k < SCAN_PER; ++k) {
+    v[k] = b + k < n ? in[b + k] : 0u;
+    sum += v[k];
+  }
+  uint32_t tot;
+  uint32_t run = block_exclusive_scan_1024(sum, sh, &tot);
+#pragma unroll
+  for (int k = 0; k < SCAN_PER; ++k) {
+    if (b + k < n) out[b + k] = (int32_t)run;
+    run += v[k];
+  }
+  if (threadIdx.x == 0) out[n] = (int32_t)tot;
+}
+
 __global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -88,6 +113,11 @@ namespace dsmp {
 dsmp_status exclusive_scan_u32(dsmp_handle* h, const uint32_t* in, int32_t* out, int64_t n,
                                uint32_t* tmp) {
   int nb = (int)ceil_div(n, SCAN_BLOCK);
+  if (n <= (int64_t)SCAN_PER * 1024) {   // one launch
+    hipLaunchKernelGGL(k_scan_single, dim3(1), dim3(1024), 0, h->stream, in, n, out);
+    DSMP_LAUNCHED(h, "scan");
+    return DSMP_OK;
+  }
   if (nb == 0) {
     hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(1024), 0, h->stream, tmp, 0);
     hipLaunchKernelGGL(k_scan_final, dim3(1), dim3(1024), 0, h->stream, in, (int64_t)0, tmp, out, 0);
