@@ -965,7 +965,8 @@ struct UArgs {
 // pieces.
 template <typename T, int DL, int H2>
 struct UShape {
-  static constexpr int ESZ = sizeof(T), CB = 512 / ESZ;    // 256 bf16 or 128 fp32 columns
+  // columns per workgroup: row pieces of 1 KB where U rows are long enough, else 512 bytes
+  static constexpr int ESZ = sizeof(T), CB = (H2 * DL >= 8192 ? 1024 : 512) / ESZ;
   static constexpr int TPW = CB / 128;                     // column tiles per wave
   static constexpr int TROW = CB * ESZ + 16;               // LDS row pitch (bytes)
   static constexpr int BUF = 32 * TROW;
@@ -978,7 +979,8 @@ __global__ __launch_bounds__(256) void k_u_gemm(UArgs a, int64_t rows_per_wg) {
   using US = UShape<T, DL, H2>;
   constexpr int KS = M::KS, EPL = M::EPL, ESZ = sizeof(T), SKD = DL / KS, NC = H2 * DL, TROW = US::TROW;
   constexpr int CB = US::CB, CH = CB * ESZ / 16;          // columns, 16-byte units of an LDS row
-  __shared__ __align__(16) unsigned char sq[2][US::BUF];
+  extern __shared__ __align__(16) unsigned char sqm[];
+  unsigned char (*sq)[US::BUF] = reinterpret_cast<unsigned char (*)[US::BUF]>(sqm);
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
   const int64_t cb0 = (int64_t)blockIdx.x * CB;
   const int64_t i_begin = (int64_t)blockIdx.y * rows_per_wg;
@@ -1037,7 +1039,10 @@ dsmp_status launch_u_gemm(dsmp_handle* h, const UArgs& ua) {
   if (groups > steps) groups = steps;
   const int64_t rows_per_wg = ((steps + groups - 1) / groups) * 32;
   groups = (ua.n_rows + rows_per_wg - 1) / rows_per_wg;
-  hipLaunchKernelGGL((k_u_gemm<T, DL, H2>), dim3((unsigned)ncb, (unsigned)groups), dim3(256), 0, h->stream, ua,
+  constexpr int lds = 2 * UShape<T, DL, H2>::BUF;
+  DSMP_HIP(h, hipFuncSetAttribute(reinterpret_cast<const void*>(k_u_gemm<T, DL, H2>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, lds));
+  hipLaunchKernelGGL((k_u_gemm<T, DL, H2>), dim3((unsigned)ncb, (unsigned)groups), dim3(256), lds, h->stream, ua,
                      rows_per_wg);
   DSMP_LAUNCHED(h, "U GEMM");
   return DSMP_OK;
