@@ -293,6 +293,41 @@ __device__ __forceinline__ float relu_mask(float v, uint32_t& word, int bit) {
   return z;
 }
 
+// p[0] + p[stride] + ... + p[(n-1) stride], added in index order starting
+// from +0 (the same bits as the plain loop), with the loads issued eight at a
+// time ahead of their additions instead of one load-wait-add per term.
+__device__ __forceinline__ float ordered_sum(const float* __restrict__ p, int64_t stride, int n) {
+  float s = 0.0f;
+  for (int c0 = 0; c0 < n; c0 += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = c0 + u < n ? p[(int64_t)(c0 + u) * stride] : 0.0f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (c0 + u < n) s += v[u];
+  }
+  return s;
+}
+
+// A DL x DL fp32 matrix (16-byte aligned) into LDS rows of pitch DL + 1 by a
+// 256-thread workgroup, every load issued before the first LDS write.
+template <int DL>
+__device__ __forceinline__ void stage_square(float (*dst)[DL + 1], const float* __restrict__ src) {
+  constexpr int N4 = DL * DL / 4 / 256;
+  static_assert(N4 >= 1 && DL * DL % 1024 == 0, "whole float4 per thread");
+  float4 v[N4];
+#pragma unroll
+  for (int u = 0; u < N4; ++u) v[u] = reinterpret_cast<const float4*>(src)[threadIdx.x + 256 * u];
+#pragma unroll
+  for (int u = 0; u < N4; ++u) {
+    const int e = 4 * (threadIdx.x + 256 * u), r = e / DL, c = e % DL;
+    dst[r][c] = v[u].x;
+    dst[r][c + 1] = v[u].y;
+    dst[r][c + 2] = v[u].z;
+    dst[r][c + 3] = v[u].w;
+  }
+}
+
 // Byte offsets of the sections of a packed parameter buffer.
 struct PackLayout {
   size_t w1l, b1l, w2p, b2, w3f, w3q, w3t, b3t, b3n, w2t, wr, br, wgt, wht, w3u, total;

@@ -524,8 +524,7 @@ __global__ __launch_bounds__(256) void k_dw3_agg_final(int d, int h2, int nsl, c
     // x enumerates (q, K) with K fastest, so the reads of part are contiguous
     const int q = (int)(x / kcols);
     const int64_t K = x % kcols;
-    float v = 0.0f;
-    for (int s = 0; s < nsl; ++s) v += part[((int64_t)s * d + q) * kcols + K];
+    const float v = ordered_sum(part + (int64_t)q * kcols + K, (int64_t)d * kcols, nsl);
     float* o;
     if (K < (int64_t)h2 * d) {
       const int ti = K / 1024, rem = K % 1024, l = rem / 16, r = rem % 16;

@@ -63,21 +63,23 @@ __global__ __launch_bounds__(256) void k_bwd_node(BNodeArgs a) {
   constexpr int NPB = 256 / DL;
   __shared__ float wr[DL][DL + 1];
   __shared__ float yb[NPB][DL];
-  for (int u = threadIdx.x; u < DL * DL; u += 256) wr[u / DL][u % DL] = a.wr[u];
+  stage_square<DL>(wr, a.wr);
   const int li = threadIdx.x / DL, c = threadIdx.x % DL;
   for (int64_t base = (int64_t)blockIdx.x * NPB; base < a.n_dst; base += (int64_t)gridDim.x * NPB) {
     const int64_t i = base + li;
     const bool ok = i < a.n_dst;
     float g = 0.0f, v = 0.0f;
+    int32_t deg = 0;
     if (ok) {
       g = a.G[i * DL + c];
-      v = a.act == DSMP_ACT_RELU ? (a.y[i * DL + c] > 0.0f ? g : 0.0f) : g;
+      const float yv = a.y[i * DL + c];
+      deg = a.row_ptr[i + 1] - a.row_ptr[i];
+      v = a.act == DSMP_ACT_RELU ? (yv > 0.0f ? g : 0.0f) : g;
     }
     __syncthreads();
     yb[li][c] = v;
     __syncthreads();
     if (!ok) continue;
-    const int32_t deg = a.row_ptr[i + 1] - a.row_ptr[i];
     const float gm = deg > 0 ? v / (float)deg : 0.0f;
     a.ybar[i * DL + c] = v;
     a.gF[i * DL + c] = gm;
@@ -105,13 +107,23 @@ __global__ __launch_bounds__(256) void k_bwd_root(int64_t n_dst, int64_t per_blo
   float accb = 0.0f;
   const int64_t i0 = (int64_t)blockIdx.x * per_block;
   const int64_t i1 = i0 + per_block < n_dst ? i0 + per_block : n_dst;
+  constexpr int NU = NB * DL / 256;
   for (int64_t b = i0; b < i1; b += NB) {
+    float yv[NU], hv[NU];
+#pragma unroll
+    for (int k = 0; k < NU; ++k) {
+      const int u = threadIdx.x + 256 * k;
+      const int64_t i = b + u / DL;
+      const bool ok = i < i1;
+      yv[k] = ok ? ybar[i * DL + u % DL] : 0.0f;
+      hv[k] = ok ? to_f(hin[i * DL + u % DL]) : 0.0f;
+    }
     __syncthreads();
-    for (int u = threadIdx.x; u < NB * DL; u += 256) {
-      int64_t i = b + u / DL;
-      bool ok = i < i1;
-      ys[u / DL][u % DL] = ok ? ybar[i * DL + u % DL] : 0.0f;
-      hs[u / DL][u % DL] = ok ? to_f(hin[i * DL + u % DL]) : 0.0f;
+#pragma unroll
+    for (int k = 0; k < NU; ++k) {
+      const int u = threadIdx.x + 256 * k;
+      ys[u / DL][u % DL] = yv[k];
+      hs[u / DL][u % DL] = hv[k];
     }
     __syncthreads();
     for (int n = 0; n < NB; ++n) {
@@ -1699,8 +1711,8 @@ dsmp_status launch_attr_dx(dsmp_handle* h, int64_t E, const unsigned char* da1E,
 
 // Fixed-order reductions out[x] = [out[x] +] sum_c part[c*stride + off + x]
 // for several segments in one launch: block b serves the 64 outputs starting
-// at (b - first[s]) * 64 of segment s; four thread groups sum the chunks
-// c = g, g+4, ... in order and the group sums are added in group order
+// at (b - first[s]) * 64 of segment s; sixteen thread groups sum the chunks
+// c = g, g+16, ... in order and the group sums are added in group order
 // (deterministic).
 struct RedSeg {
   const float* part;
@@ -1714,23 +1726,25 @@ struct RedArgs {
   int nseg, accumulate;
 };
 
-__global__ __launch_bounds__(256) void k_reduce_multi(RedArgs a) {
-  __shared__ float sh[4][64];
+constexpr int RED_GROUPS = 16;
+
+__global__ __launch_bounds__(64 * RED_GROUPS) void k_reduce_multi(RedArgs a) {
+  __shared__ float sh[RED_GROUPS][64];
   int sidx = 0;
   while (sidx + 1 < a.nseg && (int64_t)blockIdx.x >= a.first[sidx + 1]) ++sidx;
   const RedSeg& sg = a.seg[sidx];
   const int c0 = threadIdx.x & 63, g = threadIdx.x >> 6;
   const int64_t x = ((int64_t)blockIdx.x - a.first[sidx]) * 64 + c0;
   float sum = 0.0f;
-  if (x < sg.n) {
-    const float* p = sg.part + sg.off + x;
-#pragma unroll 8
-    for (int c = g; c < sg.nchunk; c += 4) sum += p[(int64_t)c * sg.stride];
-  }
+  if (x < sg.n && g < sg.nchunk)
+    sum = ordered_sum(sg.part + sg.off + x + (int64_t)g * sg.stride, RED_GROUPS * sg.stride,
+                      (sg.nchunk - g + RED_GROUPS - 1) / RED_GROUPS);
   sh[g][c0] = sum;
   __syncthreads();
   if (g == 0 && x < sg.n) {
-    const float t = ((sh[0][c0] + sh[1][c0]) + sh[2][c0]) + sh[3][c0];
+    float t = sh[0][c0];
+#pragma unroll
+    for (int u = 1; u < RED_GROUPS; ++u) t += sh[u][c0];
     sg.out[x] = a.accumulate ? sg.out[x] + t : t;
   }
 }
@@ -1759,7 +1773,7 @@ __global__ void k_bwd_dh_final(int64_t n_src, int64_t n_dst, int DL, const int32
     const int c = (int)(x % DL);
     float s = 0.0f;
     if (nsl > 0) {
-      for (int sl = 0; sl < nsl; ++sl) s += slices[(int64_t)sl * total + x];
+      s = ordered_sum(slices + x, total, nsl);
     } else {
       s = segment_sum(csc_ptr, j, c, DL, direct, part);
     }
@@ -2170,7 +2184,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   red(w.p_w1, n1, (int64_t)d.h1 * de + d.h1, 0, (int64_t)d.h1 * de, grads->dW1);
   red(w.p_w1, n1, (int64_t)d.h1 * de + d.h1, (int64_t)d.h1 * de, d.h1, grads->db1);
   if (ra.nseg > 0)
-    hipLaunchKernelGGL(k_reduce_multi, dim3((unsigned)ra.first[ra.nseg]), dim3(256), 0, s, ra);
+    hipLaunchKernelGGL(k_reduce_multi, dim3((unsigned)ra.first[ra.nseg]), dim3(64 * RED_GROUPS), 0, s, ra);
   DSMP_LAUNCHED(h, "gradient reductions");
   return DSMP_OK;
 }

@@ -462,33 +462,32 @@ __global__ __launch_bounds__(256) void k_fwd_node(NodeArgs a) {
   constexpr int NPB = 256 / DL;
   __shared__ float wr[DL][DL + 1];
   __shared__ float hs[NPB][DL];
-  for (int u = threadIdx.x; u < DL * DL; u += 256) wr[u / DL][u % DL] = a.wr[u];
+  stage_square<DL>(wr, a.wr);
   const int li = threadIdx.x / DL, q = threadIdx.x % DL;
   const T* hin = reinterpret_cast<const T*>(a.h_in);
   for (int64_t base = (int64_t)blockIdx.x * NPB; base < a.n_dst; base += (int64_t)gridDim.x * NPB) {
     const int64_t i = base + li;
     const bool ok = i < a.n_dst;
+    // every global read of the node is issued ahead of the barriers
+    float hv = 0.0f, sum = 0.0f;
+    int32_t deg = 0;
+    if (ok) {
+      hv = to_f(hin[i * DL + q]);
+      deg = a.row_ptr[i + 1] - a.row_ptr[i];
+      sum = a.nsl > 0 ? ordered_sum(a.slices + i * DL + q, a.n_dst * DL, a.nsl)
+                      : segment_sum(a.row_ptr, i, q, DL, a.direct, a.part);
+    }
     __syncthreads();
-    hs[li][q] = ok ? to_f(hin[i * DL + q]) : 0.0f;
+    hs[li][q] = hv;
     __syncthreads();
     if (!ok) continue;
-    const int32_t deg = a.row_ptr[i + 1] - a.row_ptr[i];
-    float y = 0.0f;
-    if (deg > 0) {
-      float sum = 0.0f;
-      if (a.nsl > 0) {
-        for (int sl = 0; sl < a.nsl; ++sl) sum += a.slices[((int64_t)sl * a.n_dst + i) * DL + q];
-      } else {
-        sum = segment_sum(a.row_ptr, i, q, DL, a.direct, a.part);
-      }
-      y = sum / (float)deg;
-    }
+    float y = deg > 0 ? sum / (float)deg : 0.0f;
     float r = 0.0f;
 #pragma unroll 8
     for (int p = 0; p < DL; ++p) r += wr[q][p] * hs[li][p];
     y += r + a.br[q];
     const float act = a.act == DSMP_ACT_RELU ? (y > 0.0f ? y : 0.0f) : y;
-    const float out = a.residual ? hs[li][q] + act : act;
+    const float out = a.residual ? hv + act : act;
     a.h_out[i * DL + q] = out;
     if (a.h_out_lp) reinterpret_cast<T*>(a.h_out_lp)[i * DL + q] = (T)out;
     a.y_saved[i * DL + q] = y;
@@ -760,7 +759,6 @@ __global__ void k_pack(PackArgs a) {
   for (int64_t x = t0; x < h2; x += stride) b2[x] = a.b2[x];
   T* w3f = reinterpret_cast<T*>(a.out + a.L.w3f);
   T* w3q = reinterpret_cast<T*>(a.out + a.L.w3q);
-  T* w3t = reinterpret_cast<T*>(a.out + a.L.w3t);
   for (int64_t x = t0; x < (int64_t)d * d * h2; x += stride) {
     int64_t r = x / h2;
     int kk = x % h2;
@@ -768,9 +766,6 @@ __global__ void k_pack(PackArgs a) {
     // w3f[p=i0][q=i1][kk], w3q[q=i0][p=i1][kk]
     w3f[x] = (T)a.W3[((int64_t)i0 * d + i1) * h2 + kperm<T>(kk)];
     w3q[x] = (T)a.W3[((int64_t)i1 * d + i0) * h2 + kperm<T>(kk)];
-    // w3t[p][k][q]
-    int p = x / ((int64_t)h2 * d), rem = x % ((int64_t)h2 * d), k = rem / d, q = rem % d;
-    w3t[x] = (T)a.W3[((int64_t)p * d + q) * h2 + k];
   }
   T* b3t = reinterpret_cast<T*>(a.out + a.L.b3t);
   T* b3n = reinterpret_cast<T*>(a.out + a.L.b3n);
@@ -805,18 +800,36 @@ __global__ void k_pack(PackArgs a) {
       wht[x] = (T)a.b3[o * d + c];
     }
   }
-  // W3u rows in MFMA fragment order: row c' of the U GEMM is U_i's element
-  // (k, p) that lane l of A fragment (kt, s) holds, c' = ((kt*SKD + s)*64 + l)*EPL + t
-  // with k = 32 kt + l%32 and p = s*KS + (l/32)*EPL + t, so a fragment of U_i
-  // is one contiguous 64-lane piece.
-  T* w3u = reinterpret_cast<T*>(a.out + a.L.w3u);
-  for (int64_t x = t0; x < (int64_t)h2 * d * d; x += stride) {
-    const int q = (int)(x % d);
-    const int64_t c = x / d;
-    const int t = (int)(c % EPL), l = (int)((c / EPL) % 64), fs = (int)(c / (EPL * 64));
-    const int skd = d / KS, kt = fs / skd, sk = fs % skd;
-    const int k = 32 * kt + l % 32, p = sk * KS + (l / 32) * EPL + t;
-    w3u[x] = (T)a.W3[((int64_t)p * d + q) * h2 + k];
+}
+
+// The two packed forms of W3 [p][q][k] that put q fastest, through an LDS
+// tile so that both the reads (rows of k) and the writes (rows of q) are
+// whole cache lines; one workgroup per (32 values of k, p):
+//  * w3t [p][k][q];
+//  * W3u, the U GEMM's B operand, rows in MFMA fragment order: row c of W3u
+//    is U_i's element (k, p) that lane l of A fragment (kt, s) holds,
+//    c = ((kt*SKD + s)*64 + l)*EPL + t, with k = 32 kt + l%32 and
+//    p = s*KS + (l/32)*EPL + t, so a fragment of U_i is one contiguous
+//    64-lane piece.
+template <typename T>
+__global__ __launch_bounds__(256) void k_pack_w3_tr(const float* __restrict__ W3, int d, int h2,
+                                                    T* __restrict__ w3t, T* __restrict__ w3u) {
+  constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL;
+  __shared__ float tile[32][129];   // [k - k0][q], d <= 128
+  const int k0 = blockIdx.x * 32, p = blockIdx.y;
+  for (int u = threadIdx.x; u < d * 32; u += 256) {
+    const int q = u / 32, kk = u % 32;
+    tile[kk][q] = k0 + kk < h2 ? W3[((int64_t)p * d + q) * h2 + k0 + kk] : 0.0f;
+  }
+  __syncthreads();
+  const int skd = d / KS, t = p % EPL, s = p / KS, lh = (p % KS) / EPL;
+  for (int u = threadIdx.x; u < d * 32; u += 256) {
+    const int kk = u / d, q = u % d, k = k0 + kk;
+    if (k >= h2) continue;
+    const T v = (T)tile[kk][q];
+    w3t[((int64_t)p * h2 + k) * d + q] = v;
+    const int l = lh * 32 + k % 32, fs = (k / 32) * skd + s;
+    w3u[((int64_t)(fs * 64 + l) * EPL + t) * d + q] = v;
   }
 }
 
@@ -982,10 +995,17 @@ extern "C" dsmp_status dsmp_nnconv_pack(dsmp_handle* h, const dsmp_layer_desc* d
              desc->d, desc->h1, desc->h2, attr_width(*desc),
              pack_layout(desc->d, desc->h1, desc->h2, desc->dtype == DSMP_BF16 ? 2 : 4),
              static_cast<unsigned char*>(packed)};
-  if (desc->dtype == DSMP_BF16)
+  const dim3 gt((unsigned)ceil_div(desc->h2, 32), (unsigned)desc->d);
+  unsigned char* out = static_cast<unsigned char*>(packed);
+  if (desc->dtype == DSMP_BF16) {
     hipLaunchKernelGGL(k_pack<__bf16>, dim3(1024), dim3(256), 0, h->stream, a);
-  else
+    hipLaunchKernelGGL(k_pack_w3_tr<__bf16>, gt, dim3(256), 0, h->stream, p->W3, desc->d, desc->h2,
+                       reinterpret_cast<__bf16*>(out + a.L.w3t), reinterpret_cast<__bf16*>(out + a.L.w3u));
+  } else {
     hipLaunchKernelGGL(k_pack<float>, dim3(1024), dim3(256), 0, h->stream, a);
+    hipLaunchKernelGGL(k_pack_w3_tr<float>, gt, dim3(256), 0, h->stream, p->W3, desc->d, desc->h2,
+                       reinterpret_cast<float*>(out + a.L.w3t), reinterpret_cast<float*>(out + a.L.w3u));
+  }
   DSMP_LAUNCHED(h, "pack");
   return DSMP_OK;
 }
