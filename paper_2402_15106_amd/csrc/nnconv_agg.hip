@@ -185,7 +185,7 @@ struct OuterTrShape {
   static constexpr int64_t KTOT = (int64_t)H2 * DL + DL;
 };
 
-template <int DL, int H2>
+template <int DL, int H2, bool AHEAD>
 __global__ __launch_bounds__(256) void k_outer_sum_tr(OuterArgs a) {
   using S = OuterTrShape<DL, H2>;
   using M = MT<__bf16>;
@@ -194,77 +194,120 @@ __global__ __launch_bounds__(256) void k_outer_sum_tr(OuterArgs a) {
   __shared__ int rz[ECH], ru[ECH];   // source rows of the chunk's z and gathered rows
   unsigned char* zl = smem;
   unsigned char* ul = smem + ECH * S::ZP;
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
-  const int64_t n = blockIdx.x;
-  const int64_t pa = a.seg_ptr[n], pb = a.seg_ptr[n + 1];
-
-  f32x16 acc[S::TPW];
-#pragma unroll
-  for (int j = 0; j < S::TPW; ++j) acc[j] = f32x16{};
-  float hs = 0.0f;   // z~ = 1 row: sum of the gathered rows (threads tid < DL)
-
-  for (int64_t c0 = pa; c0 < pb; c0 += ECH) {
-    const int cnt = (int)(pb - c0 < ECH ? pb - c0 : ECH);
-    __syncthreads();   // previous chunk fully consumed
-    if (tid < ECH) {
-      const int64_t pos = c0 + (tid < cnt ? tid : cnt - 1);
-      const int64_t e = a.pos_eid ? (int64_t)a.pos_eid[pos] : pos;
-      rz[tid] = (int)e;
-      ru[tid] = a.row_of[e];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5;
+  const int64_t G = gridDim.x;
+  // AHEAD: workgroup b takes segments b, b + G, ..., and the next segment's
+  // bounds, edge ids and gathered-row ids are read while this segment's rows
+  // are copied and multiplied, so that a segment waits for the copy of its
+  // rows alone, not for the chain of index reads ahead of it.  Otherwise
+  // workgroup b takes segment b alone (G = n_seg).
+  // Slot tid < ECH of a chunk takes the chunk's edge min(tid, cnt - 1).
+  auto slot_pos = [&](int64_t c0, int64_t end) {
+    const int cnt = (int)(end - c0 < ECH ? end - c0 : ECH);
+    return c0 + (tid < cnt ? tid : cnt - 1);
+  };
+  int64_t n = blockIdx.x, pa = 0, pb = 0;
+  int pz = 0, pu = 0;   // first chunk of segment n: edge id and gathered row of slot tid
+  if (n < a.n_seg) {
+    pa = a.seg_ptr[n];
+    pb = a.seg_ptr[n + 1];
+    if (AHEAD && tid < ECH && pb > pa) {
+      const int64_t pos = slot_pos(pa, pb);
+      pz = a.pos_eid ? a.pos_eid[pos] : (int)pos;
+      pu = a.row_of[pz];
     }
-    __syncthreads();
-    const int wbase = tid & ~63;
-    for (int U0 = 0; U0 < S::ZU; U0 += 256) {
-      const int U = U0 + tid, r = U / (S::ZNU + S::ZPAD), u = U % (S::ZNU + S::ZPAD);
-      if (U < S::ZU)
-        __builtin_amdgcn_global_load_lds(
-            (gbl_void_t*)(a.zE + (size_t)rz[r < ECH ? r : ECH - 1] * H2 * 2 + (u < S::ZNU ? u : 0) * 16),
-            (lds_void_t*)(zl + (size_t)(U0 + wbase) * 16), 16, 0, 0);
-    }
-    for (int U0 = 0; U0 < S::UU; U0 += 256) {
-      const int U = U0 + tid, r = U / (S::UNU + S::UPAD), u = U % (S::UNU + S::UPAD);
-      if (U < S::UU)
-        __builtin_amdgcn_global_load_lds(
-            (gbl_void_t*)(a.u + (size_t)ru[r < ECH ? r : ECH - 1] * DL * 2 + (u < S::UNU ? u : 0) * 16),
-            (lds_void_t*)(ul + (size_t)(U0 + wbase) * 16), 16, 0, 0);
-    }
-    stage_wait();
-    __syncthreads();
-    const int nks = (cnt + 15) / 16;
-    for (int ks = 0; ks < nks; ++ks) {
+  }
+  for (; n < a.n_seg; n += G) {
+    // the next segment's bounds (an empty range past the last segment)
+    const int64_t nn = AHEAD ? n + G : a.n_seg;
+    const int64_t qa = AHEAD ? a.seg_ptr[nn < a.n_seg ? nn : a.n_seg] : 0;
+    const int64_t qb = AHEAD ? a.seg_ptr[nn < a.n_seg ? nn + 1 : a.n_seg] : 0;
+    f32x16 acc[S::TPW];
 #pragma unroll
-      for (int j = 0; j < S::TPW; ++j) {
-        const int ti = wv + 4 * j;
-        if (ti < S::NTILE) {
-          const int kt = ti / S::NCT, ct = ti % S::NCT;
-          bf16x8 A = lds_frag_rows(zl, S::ZP, ks * 16, kt * 32);
-          if (ks * 16 + 16 > cnt) {   // slots past the last edge
+    for (int j = 0; j < S::TPW; ++j) acc[j] = f32x16{};
+    float hs = 0.0f;   // z~ = 1 row: sum of the gathered rows (threads tid < DL)
+    const bool ahead = AHEAD && tid < ECH && qb > qa;   // this thread reads ahead a slot of the next segment
+    for (int64_t c0 = pa; c0 < pb; c0 += ECH) {
+      const int cnt = (int)(pb - c0 < ECH ? pb - c0 : ECH);
+      const bool first = c0 == pa;
+      __syncthreads();   // previous chunk fully consumed
+      if (tid < ECH) {
+        int z = pz, u = pu;
+        if (!AHEAD || !first) {
+          const int64_t pos = slot_pos(c0, pb);
+          z = a.pos_eid ? a.pos_eid[pos] : (int)pos;
+          u = a.row_of[z];
+        }
+        rz[tid] = z;
+        ru[tid] = u;
+      }
+      if (first && ahead) {   // the next segment's edge ids, in flight with this chunk's copy
+        const int64_t pos = slot_pos(qa, qb);
+        pz = a.pos_eid ? a.pos_eid[pos] : (int)pos;
+      }
+      __syncthreads();
+      const int wbase = tid & ~63;
+      for (int U0 = 0; U0 < S::ZU; U0 += 256) {
+        const int U = U0 + tid, r = U / (S::ZNU + S::ZPAD), u = U % (S::ZNU + S::ZPAD);
+        if (U < S::ZU)
+          __builtin_amdgcn_global_load_lds(
+              (gbl_void_t*)(a.zE + (size_t)rz[r < ECH ? r : ECH - 1] * H2 * 2 + (u < S::ZNU ? u : 0) * 16),
+              (lds_void_t*)(zl + (size_t)(U0 + wbase) * 16), 16, 0, 0);
+      }
+      for (int U0 = 0; U0 < S::UU; U0 += 256) {
+        const int U = U0 + tid, r = U / (S::UNU + S::UPAD), u = U % (S::UNU + S::UPAD);
+        if (U < S::UU)
+          __builtin_amdgcn_global_load_lds(
+              (gbl_void_t*)(a.u + (size_t)ru[r < ECH ? r : ECH - 1] * DL * 2 + (u < S::UNU ? u : 0) * 16),
+              (lds_void_t*)(ul + (size_t)(U0 + wbase) * 16), 16, 0, 0);
+      }
+      stage_wait();
+      __syncthreads();
+      if (first && ahead) pu = a.row_of[pz];   // in flight with this chunk's products
+      const int nks = (cnt + 15) / 16;
+      for (int ks = 0; ks < nks; ++ks) {
 #pragma unroll
-            for (int t = 0; t < 8; ++t)
-              if (ks * 16 + 8 * hh + t >= cnt) A[t] = (__bf16)0.0f;
+        for (int j = 0; j < S::TPW; ++j) {
+          const int ti = wv + 4 * j;
+          if (ti < S::NTILE) {
+            const int kt = ti / S::NCT, ct = ti % S::NCT;
+            bf16x8 A = lds_frag_rows(zl, S::ZP, ks * 16, kt * 32);
+            if (ks * 16 + 16 > cnt) {   // slots past the last edge
+#pragma unroll
+              for (int t = 0; t < 8; ++t)
+                if (ks * 16 + 8 * hh + t >= cnt) A[t] = (__bf16)0.0f;
+            }
+            acc[j] = M::mma(A, lds_frag_rows(ul, S::UP, ks * 16, ct * 32), acc[j]);
           }
-          acc[j] = M::mma(A, lds_frag_rows(ul, S::UP, ks * 16, ct * 32), acc[j]);
         }
       }
+      if (tid < DL)
+        for (int e = 0; e < cnt; ++e) hs += (float)*reinterpret_cast<const __bf16*>(ul + e * S::UP + tid * 2);
     }
-    if (tid < DL)
-      for (int e = 0; e < cnt; ++e) hs += (float)*reinterpret_cast<const __bf16*>(ul + e * S::UP + tid * 2);
-  }
+    if (pb <= pa && ahead) {   // a segment with no edges: nothing to overlap with
+      const int64_t pos = slot_pos(qa, qb);
+      pz = a.pos_eid ? a.pos_eid[pos] : (int)pos;
+      pu = a.row_of[pz];
+    }
 
-  unsigned char* o = a.out + (size_t)n * S::KTOT * 2;
+    unsigned char* o = a.out + (size_t)n * S::KTOT * 2;
 #pragma unroll
-  for (int j = 0; j < S::TPW; ++j) {
-    const int ti = wv + 4 * j;
-    if (ti < S::NTILE) {
-      unsigned char* dst = o + ((size_t)ti * 1024 + lane * 16) * 2;
-      float v[16];
+    for (int j = 0; j < S::TPW; ++j) {
+      const int ti = wv + 4 * j;
+      if (ti < S::NTILE) {
+        unsigned char* dst = o + ((size_t)ti * 1024 + lane * 16) * 2;
+        float v[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) v[r] = acc[j][r];
-      *reinterpret_cast<bf16x8*>(dst) = pack_frag<__bf16>(v);
-      *reinterpret_cast<bf16x8*>(dst + 16) = pack_frag<__bf16>(v + 8);
+        for (int r = 0; r < 16; ++r) v[r] = acc[j][r];
+        *reinterpret_cast<bf16x8*>(dst) = pack_frag<__bf16>(v);
+        *reinterpret_cast<bf16x8*>(dst + 16) = pack_frag<__bf16>(v + 8);
+      }
     }
+    if (tid < DL) reinterpret_cast<__bf16*>(o)[(size_t)H2 * DL + tid] = (__bf16)hs;
+    if (!AHEAD) break;
+    pa = qa;
+    pb = qb;
   }
-  if (tid < DL) reinterpret_cast<__bf16*>(o)[(size_t)H2 * DL + tid] = (__bf16)hs;
 }
 
 // ------------------------------------------------------------ GEMM with W3~
@@ -549,10 +592,21 @@ template <typename T, int DL, int H2>
 dsmp_status outer_shape(dsmp_handle* h, const OuterArgs& a) {
   if constexpr (sizeof(T) == 2) {
     using S = OuterTrShape<DL, H2>;
-    auto kern = k_outer_sum_tr<DL, H2>;
-    dsmp_status st = set_lds_bytes(h, kern, S::LDS);
+    // persistent workgroups that read the next segment's indices ahead where
+    // fewer than four fit on a CU; with four or more, one segment per
+    // workgroup, which lets the dispatcher balance segments of uneven length
+    auto ahead = k_outer_sum_tr<DL, H2, true>;
+    auto single = k_outer_sum_tr<DL, H2, false>;
+    dsmp_status st = set_lds_bytes(h, ahead, S::LDS);
+    if (st == DSMP_OK) st = set_lds_bytes(h, single, S::LDS);
     if (st != DSMP_OK) return st;
-    hipLaunchKernelGGL(kern, dim3((unsigned)a.n_seg), dim3(256), S::LDS, h->stream, a);
+    int per_cu = 0;
+    DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ahead, 256, S::LDS));
+    if (per_cu >= 4)
+      hipLaunchKernelGGL(single, dim3((unsigned)a.n_seg), dim3(256), S::LDS, h->stream, a);
+    else
+      hipLaunchKernelGGL(ahead, dim3((unsigned)std::min<int64_t>(a.n_seg, (int64_t)h->n_cu * std::max(per_cu, 1))),
+                         dim3(256), S::LDS, h->stream, a);
     DSMP_LAUNCHED(h, "segment outer-product sums");
     return DSMP_OK;
   }
