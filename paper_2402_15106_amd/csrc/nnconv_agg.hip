@@ -476,17 +476,18 @@ __global__ __launch_bounds__(256) void k_dw3_agg(DW3AggArgs a) {
   }
 }
 
-// bf16 layers: the same sums with chunks of 32 rows of S (a 512-byte piece,
-// 256 K columns) and of g copied to LDS by whole cache lines, two buffers,
-// and the fragments read by transposing LDS reads (rows are the contraction
-// index).  Wave w owns the q tile w / (NKT/4) and four consecutive K tiles,
-// so one g fragment feeds four products.  Rows past the slice re-read its
-// last row and are zeroed in the g fragment; columns past the end of a row
-// (last K block) are read from the next row (or the buffer's tail padding)
-// and never stored.
+// bf16 layers: the same sums with chunks of 32 rows of S (a piece of KR K
+// columns: 256, or 128 at d = 128, which halves the accumulators per wave and
+// measured 1.5x faster there) and of g copied to LDS by whole cache lines,
+// two buffers, and the fragments read by transposing LDS reads (rows are the
+// contraction index).  Wave w owns TPW consecutive K tiles of one q tile, so
+// one g fragment feeds TPW products.  Rows past the slice re-read its last
+// row and are zeroed in the g fragment; columns past the end of a row (last
+// K block) are read from the next row (or the buffer's tail padding) and
+// never stored.
 template <int DL>
 struct DW3TrShape {
-  static constexpr int ECH = 32, KR = 256;
+  static constexpr int ECH = 32, KR = DL == 128 ? 128 : 256;
   using SS = RowStage<ECH, KR * 2, tr_pad_units(KR * 2)>;
   using GS = RowStage<ECH, DL * 2, tr_pad_units(DL * 2)>;
   static constexpr int SB = ECH * SS::PITCH, BUF = SB + ECH * GS::PITCH, LDS = 2 * BUF;
