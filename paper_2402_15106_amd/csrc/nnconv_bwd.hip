@@ -46,86 +46,88 @@ __device__ __forceinline__ float to_f(float x) { return x; }
 // ------------------------------------------------------------ node pre-pass
 
 struct BNodeArgs {
-  int64_t n_dst;
+  int64_t n_dst, per_block;    // destinations, and destinations per workgroup
   const int32_t* row_ptr;
   const float* G;
   const float* y;
   const float* wr;       // [q][p]
-  float* ybar;
+  const unsigned char* h_in;   // [n_src][d] layer dtype
   unsigned char* gT;     // [n_dst][d] layer dtype
   float* gF;             // [n_dst][d]
   float* dh_node;
+  float* p_root;         // [grid][d*d + d] partial sums of dWr and dbr
   int act, residual;
 };
 
+// The node terms of the backward for a chunk of per_block destinations per
+// workgroup, 32 at a time:  ybar_i = G_i * act'(y_i), the message gradient
+// g_i = ybar_i / deg_i (fp32 and layer dtype), dh_node_i = [G_i] + Wr^T ybar_i,
+// and the workgroup's partial sums dWr = sum_i ybar_i h_i^T, dbr = sum_i ybar_i
+// (added over workgroups in a fixed order later).
 template <typename T, int DL>
 __global__ __launch_bounds__(256) void k_bwd_node(BNodeArgs a) {
-  constexpr int NPB = 256 / DL;
+  constexpr int NB = 32, NU = NB * DL / 256, PP = DL * DL / 256, NPW = 256 / DL;
   __shared__ float wr[DL][DL + 1];
-  __shared__ float yb[NPB][DL];
-  stage_square<DL>(wr, a.wr);
-  const int li = threadIdx.x / DL, c = threadIdx.x % DL;
-  for (int64_t base = (int64_t)blockIdx.x * NPB; base < a.n_dst; base += (int64_t)gridDim.x * NPB) {
-    const int64_t i = base + li;
-    const bool ok = i < a.n_dst;
-    float g = 0.0f, v = 0.0f;
-    int32_t deg = 0;
-    if (ok) {
-      g = a.G[i * DL + c];
-      const float yv = a.y[i * DL + c];
-      deg = a.row_ptr[i + 1] - a.row_ptr[i];
-      v = a.act == DSMP_ACT_RELU ? (yv > 0.0f ? g : 0.0f) : g;
-    }
-    __syncthreads();
-    yb[li][c] = v;
-    __syncthreads();
-    if (!ok) continue;
-    const float gm = deg > 0 ? v / (float)deg : 0.0f;
-    a.ybar[i * DL + c] = v;
-    a.gF[i * DL + c] = gm;
-    reinterpret_cast<T*>(a.gT)[i * DL + c] = (T)gm;
-    float s = a.residual ? g : 0.0f;
-#pragma unroll 8
-    for (int q = 0; q < DL; ++q) s += wr[q][c] * yb[li][q];
-    a.dh_node[i * DL + c] = s;
-  }
-}
-
-// dWr = sum_i ybar_i h_i^T, dbr = sum_i ybar_i over a chunk of nodes.
-template <typename T, int DL>
-__global__ __launch_bounds__(256) void k_bwd_root(int64_t n_dst, int64_t per_block, const float* __restrict__ ybar,
-                                                  const unsigned char* __restrict__ h_in,
-                                                  float* __restrict__ part) {
-  constexpr int PP = DL * DL / 256, NB = 32;
   __shared__ float ys[NB][DL];
   __shared__ float hs[NB][DL];
-  const int q = threadIdx.x % DL, p0 = (threadIdx.x / DL) * PP;
-  const T* hin = reinterpret_cast<const T*>(h_in);
+  stage_square<DL>(wr, a.wr);
+  const int tid = threadIdx.x, c = tid % DL, li = tid / DL;   // element k: node li + NPW*k, column c
+  const int q = tid % DL, p0 = (tid / DL) * PP;               // partial sums dWr[q][p0 .. p0+PP)
+  const T* hin = reinterpret_cast<const T*>(a.h_in);
   float acc[PP];
 #pragma unroll
   for (int u = 0; u < PP; ++u) acc[u] = 0.0f;
   float accb = 0.0f;
-  const int64_t i0 = (int64_t)blockIdx.x * per_block;
-  const int64_t i1 = i0 + per_block < n_dst ? i0 + per_block : n_dst;
-  constexpr int NU = NB * DL / 256;
+  const int64_t i0 = (int64_t)blockIdx.x * a.per_block;
+  const int64_t i1 = i0 + a.per_block < a.n_dst ? i0 + a.per_block : a.n_dst;
   for (int64_t b = i0; b < i1; b += NB) {
-    float yv[NU], hv[NU];
+    float g[NU], v[NU], hv[NU];
+    int32_t deg[NU];
 #pragma unroll
     for (int k = 0; k < NU; ++k) {
-      const int u = threadIdx.x + 256 * k;
-      const int64_t i = b + u / DL;
-      const bool ok = i < i1;
-      yv[k] = ok ? ybar[i * DL + u % DL] : 0.0f;
-      hv[k] = ok ? to_f(hin[i * DL + u % DL]) : 0.0f;
+      const int64_t i = b + li + NPW * k;
+      g[k] = 0.0f; v[k] = 0.0f; hv[k] = 0.0f; deg[k] = 0;
+      if (i < i1) {
+        g[k] = a.G[i * DL + c];
+        const float yv = a.y[i * DL + c];
+        hv[k] = to_f(hin[i * DL + c]);
+        deg[k] = a.row_ptr[i + 1] - a.row_ptr[i];
+        v[k] = a.act == DSMP_ACT_RELU ? (yv > 0.0f ? g[k] : 0.0f) : g[k];
+      }
+    }
+    __syncthreads();   // the previous chunk's rows are consumed
+#pragma unroll
+    for (int k = 0; k < NU; ++k) {
+      ys[li + NPW * k][c] = v[k];
+      hs[li + NPW * k][c] = hv[k];
     }
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < NU; ++k) {
-      const int u = threadIdx.x + 256 * k;
-      ys[u / DL][u % DL] = yv[k];
-      hs[u / DL][u % DL] = hv[k];
+      const int64_t i = b + li + NPW * k;
+      if (i < i1) {
+        const float gm = deg[k] > 0 ? v[k] / (float)deg[k] : 0.0f;
+        a.gF[i * DL + c] = gm;
+        reinterpret_cast<T*>(a.gT)[i * DL + c] = (T)gm;
+      }
     }
-    __syncthreads();
+    // dh_node = [G] + Wr^T ybar, each output summed over q in order
+    float sdh[NU];
+#pragma unroll
+    for (int k = 0; k < NU; ++k) sdh[k] = a.residual ? g[k] : 0.0f;
+#pragma unroll 4
+    for (int qq = 0; qq < DL; ++qq) {
+      const float w = wr[qq][c];
+#pragma unroll
+      for (int k = 0; k < NU; ++k) sdh[k] += w * ys[li + NPW * k][qq];
+    }
+#pragma unroll
+    for (int k = 0; k < NU; ++k) {
+      const int64_t i = b + li + NPW * k;
+      if (i < i1) a.dh_node[i * DL + c] = sdh[k];
+    }
+    // partial sums of dWr and dbr over the chunk's nodes in order (rows past
+    // the end are zero)
     for (int n = 0; n < NB; ++n) {
       const float yv = ys[n][q];
 #pragma unroll
@@ -133,10 +135,10 @@ __global__ __launch_bounds__(256) void k_bwd_root(int64_t n_dst, int64_t per_blo
       accb += yv;
     }
   }
-  float* out = part + (size_t)blockIdx.x * (DL * DL + DL);
+  float* out = a.p_root + (size_t)blockIdx.x * (DL * DL + DL);
 #pragma unroll
   for (int u = 0; u < PP; ++u) out[q * DL + p0 + u] = acc[u];
-  if (threadIdx.x < DL) out[DL * DL + q] = accb;
+  if (tid < DL) out[DL * DL + q] = accb;
 }
 
 // db3[p*d+q] = sum_i (sum_{e in E_i} h_{src(e)}[p]) g_i[q] over a chunk of destinations.
@@ -1786,7 +1788,7 @@ __global__ void k_bwd_dh_final(int64_t n_src, int64_t n_dst, int DL, const int32
 // ------------------------------------------------------------ workspace
 
 struct BwdWs {
-  float *ybar, *gF, *dh_node, *dh_direct, *dh_part, *dh_sl;
+  float *gF, *dh_node, *dh_direct, *dh_part, *dh_sl;
   unsigned char *gT, *da2E, *da1E, *ot, *U;
   float4* dx;                  // [E] edge-attribute gradients (diff attributes)
   int nslh;
@@ -1819,7 +1821,6 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   BwdWs w;
   const int esz = d.dtype == DSMP_BF16 ? 2 : 4;
   const int de = layer_attr_width(d);
-  w.ybar = c.take<float>((size_t)n_dst * d.d);
   w.gF = c.take<float>((size_t)n_dst * d.d);
   w.gT = c.take<unsigned char>((size_t)n_dst * d.d * esz);
   w.dh_node = c.take<float>((size_t)n_dst * d.d);
@@ -1987,10 +1988,7 @@ void launch_node_kernels(dsmp_handle* h, const BNodeArgs& na, int64_t n_dst, con
                          const unsigned char* h_in, const int32_t* row_ptr, const int32_t* col, bool db3) {
   hipStream_t s = h->stream;
   if (n_dst == 0) return;
-  unsigned grid = ceil_div(n_dst, 256 / DL);
-  if (grid > 2048) grid = 2048;
-  hipLaunchKernelGGL((k_bwd_node<T, DL>), dim3(grid), dim3(256), 0, s, na);
-  hipLaunchKernelGGL((k_bwd_root<T, DL>), dim3(w.nr), dim3(256), 0, s, n_dst, w.pr, w.ybar, h_in, w.p_root);
+  hipLaunchKernelGGL((k_bwd_node<T, DL>), dim3(w.nr), dim3(256), 0, s, na);
   if (db3)
     hipLaunchKernelGGL((k_bwd_db3<T, DL>), dim3(w.nb3), dim3(256), 0, s, n_dst, w.pb3, row_ptr, col, h_in, w.gF,
                        w.p_db3);
@@ -2055,8 +2053,8 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   // node pre-pass, root grads, db3 partials (the aggregate form takes db3
   // from the bias rows of its dW3 product)
   ProfScope prof_node(h, DSMP_K_NODE_BWD);
-  BNodeArgs na{n_dst, g->row_ptr, grad_out, reinterpret_cast<const float*>(sv + sl.y),
-               reinterpret_cast<const float*>(pk + L.wr), w.ybar, w.gT, w.gF, w.dh_node, d.act, d.residual};
+  BNodeArgs na{n_dst, w.pr, g->row_ptr, grad_out, reinterpret_cast<const float*>(sv + sl.y),
+               reinterpret_cast<const float*>(pk + L.wr), hin, w.gT, w.gF, w.dh_node, w.p_root, d.act, d.residual};
   if (d.dtype == DSMP_BF16) {
     if (d.d == 32) launch_node_kernels<__bf16, 32>(h, na, n_dst, w, hin, g->row_ptr, g->col, !agg);
     if (d.d == 64) launch_node_kernels<__bf16, 64>(h, na, n_dst, w, hin, g->row_ptr, g->col, !agg);
