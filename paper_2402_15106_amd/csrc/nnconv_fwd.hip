@@ -731,13 +731,58 @@ struct PackArgs {
   int d, h1, h2, de;
   PackLayout L;
   unsigned char* out;
+  int nloop;   // workgroups of the element loops; d * ceil(h2/32) more transpose W3 tiles
 };
+
+// The two packed forms of W3 [p][q][k] that put q fastest, through an LDS
+// tile so that both the reads (rows of k) and the writes (rows of q) are
+// whole cache lines; one workgroup per tile (32 values of k, p), tb:
+//  * w3t [p][k][q];
+//  * W3u, the U GEMM's B operand, rows in MFMA fragment order: row c of W3u
+//    is U_i's element (k, p) that lane l of A fragment (kt, s) holds,
+//    c = ((kt*SKD + s)*64 + l)*EPL + t, with k = 32 kt + l%32 and
+//    p = s*KS + (l/32)*EPL + t, so a fragment of U_i is one contiguous
+//    64-lane piece.
+template <typename T>
+__device__ __forceinline__ void pack_w3_tile(const float* __restrict__ W3, int d, int h2, int tb,
+                                             T* __restrict__ w3t, T* __restrict__ w3u) {
+  constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL, MAXU = 128 * 32 / 256;   // d <= 128
+  __shared__ float tile[32][129];   // [k - k0][q]
+  const int nkb = (h2 + 31) / 32, tid = threadIdx.x;
+  const int k0 = (tb % nkb) * 32, p = tb / nkb;
+  float v[MAXU];   // every load of the tile issued before the first LDS write
+#pragma unroll
+  for (int i = 0; i < MAXU; ++i) {
+    const int u = tid + 256 * i, q = u / 32, kk = u % 32;
+    v[i] = u < d * 32 && k0 + kk < h2 ? W3[((int64_t)p * d + q) * h2 + k0 + kk] : 0.0f;
+  }
+#pragma unroll
+  for (int i = 0; i < MAXU; ++i) {
+    const int u = tid + 256 * i;
+    if (u < d * 32) tile[u % 32][u / 32] = v[i];
+  }
+  __syncthreads();
+  const int skd = d / KS, t = p % EPL, s = p / KS, lh = (p % KS) / EPL;
+  for (int u = tid; u < d * 32; u += 256) {
+    const int kk = u / d, q = u % d, k = k0 + kk;
+    if (k >= h2) continue;
+    const T x = (T)tile[kk][q];
+    w3t[((int64_t)p * h2 + k) * d + q] = x;
+    const int l = lh * 32 + k % 32, fs = (k / 32) * skd + s;
+    w3u[((int64_t)(fs * 64 + l) * EPL + t) * d + q] = x;
+  }
+}
 
 template <typename T>
 __global__ void k_pack(PackArgs a) {
   constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL;
   const int d = a.d, h1 = a.h1, h2 = a.h2;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  if ((int)blockIdx.x >= a.nloop) {   // the blocks past the element loops' grid transpose one W3 tile each
+    pack_w3_tile<T>(a.W3, d, h2, (int)blockIdx.x - a.nloop, reinterpret_cast<T*>(a.out + a.L.w3t),
+                    reinterpret_cast<T*>(a.out + a.L.w3u));
+    return;
+  }
+  const int64_t stride = (int64_t)a.nloop * blockDim.x;
   const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   float* w1l = reinterpret_cast<float*>(a.out + a.L.w1l);
   float* b1l = reinterpret_cast<float*>(a.out + a.L.b1l);
@@ -799,37 +844,6 @@ __global__ void k_pack(PackArgs a) {
       wgt[x] = (T)a.b3[c * d + o];
       wht[x] = (T)a.b3[o * d + c];
     }
-  }
-}
-
-// The two packed forms of W3 [p][q][k] that put q fastest, through an LDS
-// tile so that both the reads (rows of k) and the writes (rows of q) are
-// whole cache lines; one workgroup per (32 values of k, p):
-//  * w3t [p][k][q];
-//  * W3u, the U GEMM's B operand, rows in MFMA fragment order: row c of W3u
-//    is U_i's element (k, p) that lane l of A fragment (kt, s) holds,
-//    c = ((kt*SKD + s)*64 + l)*EPL + t, with k = 32 kt + l%32 and
-//    p = s*KS + (l/32)*EPL + t, so a fragment of U_i is one contiguous
-//    64-lane piece.
-template <typename T>
-__global__ __launch_bounds__(256) void k_pack_w3_tr(const float* __restrict__ W3, int d, int h2,
-                                                    T* __restrict__ w3t, T* __restrict__ w3u) {
-  constexpr int KS = MT<T>::KS, EPL = MT<T>::EPL;
-  __shared__ float tile[32][129];   // [k - k0][q], d <= 128
-  const int k0 = blockIdx.x * 32, p = blockIdx.y;
-  for (int u = threadIdx.x; u < d * 32; u += 256) {
-    const int q = u / 32, kk = u % 32;
-    tile[kk][q] = k0 + kk < h2 ? W3[((int64_t)p * d + q) * h2 + k0 + kk] : 0.0f;
-  }
-  __syncthreads();
-  const int skd = d / KS, t = p % EPL, s = p / KS, lh = (p % KS) / EPL;
-  for (int u = threadIdx.x; u < d * 32; u += 256) {
-    const int kk = u / d, q = u % d, k = k0 + kk;
-    if (k >= h2) continue;
-    const T v = (T)tile[kk][q];
-    w3t[((int64_t)p * h2 + k) * d + q] = v;
-    const int l = lh * 32 + k % 32, fs = (k / 32) * skd + s;
-    w3u[((int64_t)(fs * 64 + l) * EPL + t) * d + q] = v;
   }
 }
 
@@ -994,18 +1008,12 @@ extern "C" dsmp_status dsmp_nnconv_pack(dsmp_handle* h, const dsmp_layer_desc* d
   PackArgs a{p->W1, p->b1, p->W2, p->b2, p->W3, p->b3, p->Wr, p->br,
              desc->d, desc->h1, desc->h2, attr_width(*desc),
              pack_layout(desc->d, desc->h1, desc->h2, desc->dtype == DSMP_BF16 ? 2 : 4),
-             static_cast<unsigned char*>(packed)};
-  const dim3 gt((unsigned)ceil_div(desc->h2, 32), (unsigned)desc->d);
-  unsigned char* out = static_cast<unsigned char*>(packed);
-  if (desc->dtype == DSMP_BF16) {
-    hipLaunchKernelGGL(k_pack<__bf16>, dim3(1024), dim3(256), 0, h->stream, a);
-    hipLaunchKernelGGL(k_pack_w3_tr<__bf16>, gt, dim3(256), 0, h->stream, p->W3, desc->d, desc->h2,
-                       reinterpret_cast<__bf16*>(out + a.L.w3t), reinterpret_cast<__bf16*>(out + a.L.w3u));
-  } else {
-    hipLaunchKernelGGL(k_pack<float>, dim3(1024), dim3(256), 0, h->stream, a);
-    hipLaunchKernelGGL(k_pack_w3_tr<float>, gt, dim3(256), 0, h->stream, p->W3, desc->d, desc->h2,
-                       reinterpret_cast<float*>(out + a.L.w3t), reinterpret_cast<float*>(out + a.L.w3u));
-  }
+             static_cast<unsigned char*>(packed), 1024};
+  const dim3 grid((unsigned)(a.nloop + desc->d * ceil_div(desc->h2, 32)));
+  if (desc->dtype == DSMP_BF16)
+    hipLaunchKernelGGL(k_pack<__bf16>, grid, dim3(256), 0, h->stream, a);
+  else
+    hipLaunchKernelGGL(k_pack<float>, grid, dim3(256), 0, h->stream, a);
   DSMP_LAUNCHED(h, "pack");
   return DSMP_OK;
 }
