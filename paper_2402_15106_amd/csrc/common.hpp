@@ -117,7 +117,8 @@ dsmp_status exclusive_scan_u32(dsmp_handle* h, const uint32_t* in, int32_t* out,
                                uint32_t* tmp);
 
 // Fill n uint32 words with a value (a kernel, not a memset node).
-dsmp_status fill_u32(dsmp_handle* h, uint32_t* p, int64_t n, uint32_t v);
+// p[0..n) = v, and q[0..n) = v in the same launch when q is given
+dsmp_status fill_u32(dsmp_handle* h, uint32_t* p, int64_t n, uint32_t v, uint32_t* q = nullptr);
 
 // SplitMix64 output number c+1 after seeding the state with `seed`
 // (Steele, Lea, Flood, OOPSLA 2014; Stafford's Mix13 finaliser).

@@ -100,10 +100,14 @@ __global__ __launch_bounds__(1024) void k_scan_single(const uint32_t* __restrict
   if (threadIdx.x == 0) out[n] = (int32_t)tot;
 }
 
-__global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v) {
+// p[0..n) = v, and q[0..n) = v too when q is not null (two arrays, one launch)
+__global__ void k_fill_u32(uint32_t* p, uint32_t* q, int64_t n, uint32_t v) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (; i < n; i += stride) p[i] = v;
+  for (; i < n; i += stride) {
+    p[i] = v;
+    if (q) q[i] = v;
+  }
 }
 
 }  // namespace
@@ -131,11 +135,11 @@ dsmp_status exclusive_scan_u32(dsmp_handle* h, const uint32_t* in, int32_t* out,
   return DSMP_OK;
 }
 
-dsmp_status fill_u32(dsmp_handle* h, uint32_t* p, int64_t n, uint32_t v) {
+dsmp_status fill_u32(dsmp_handle* h, uint32_t* p, int64_t n, uint32_t v, uint32_t* q) {
   if (n <= 0) return DSMP_OK;
   unsigned g = ceil_div(n, 256);
   if (g > 4096) g = 4096;
-  hipLaunchKernelGGL(k_fill_u32, dim3(g), dim3(256), 0, h->stream, p, n, v);
+  hipLaunchKernelGGL(k_fill_u32, dim3(g), dim3(256), 0, h->stream, p, q, n, v);
   DSMP_LAUNCHED(h, "fill");
   return DSMP_OK;
 }

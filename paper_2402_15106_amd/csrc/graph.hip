@@ -355,11 +355,14 @@ __global__ __launch_bounds__(256) void k_csc_scatter(const int32_t* __restrict__
 // in row j, in row order, which is ascending edge id: csc_ptr = row_ptr, and
 // position e of row j holds the id of edge (col[e] <- j), row_ptr[i] + the
 // position of j in row i (rows are sorted by source).
-__global__ __launch_bounds__(256) void k_csc_symmetric(const int32_t* __restrict__ row_ptr,
+// The same launch copies row_ptr (n_ptr entries) to csc_ptr.
+__global__ __launch_bounds__(256) void k_csc_symmetric(const int32_t* __restrict__ row_ptr, int64_t n_ptr,
                                                        const int32_t* __restrict__ col,
                                                        const int32_t* __restrict__ dst, int64_t E,
+                                                       int32_t* __restrict__ csc_ptr,
                                                        int32_t* __restrict__ csc_eid) {
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e < n_ptr) csc_ptr[e] = row_ptr[e];
   if (e >= E) return;
   const int32_t i = col[e], j = dst[e];
   int32_t lo = row_ptr[i], hi = row_ptr[i + 1];   // first position in row i with col >= j
@@ -369,11 +372,6 @@ __global__ __launch_bounds__(256) void k_csc_symmetric(const int32_t* __restrict
     else hi = mid;
   }
   csc_eid[e] = lo;
-}
-
-__global__ __launch_bounds__(256) void k_copy_i32(const int32_t* __restrict__ a, int64_t n, int32_t* __restrict__ b) {
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t < n) b[t] = a[t];
 }
 
 constexpr int CSC_SORT_LDS = 2048;
@@ -474,8 +472,7 @@ dsmp_status count_phase(dsmp_handle* h, const dsmp_graph_query* q, const GraphWs
                      w.stats);
   DSMP_LAUNCHED(h, "grid setup");
   dsmp_status st;
-  if ((st = fill_u32(h, w.ccount, w.ncap, 0)) != DSMP_OK) return st;
-  if ((st = fill_u32(h, w.ccur, w.ncap, 0)) != DSMP_OK) return st;
+  if ((st = fill_u32(h, w.ccount, w.ncap, 0, w.ccur)) != DSMP_OK) return st;
   if (n > 0) {
     hipLaunchKernelGGL(k_cell_hash, dim3(ceil_div(n, 256)), dim3(256), 0, s, q->pos, n, D, w.grid,
                        w.cellid, w.ccount);
@@ -564,16 +561,13 @@ extern "C" dsmp_status dsmp_radius_graph_build(dsmp_handle* h, const dsmp_graph_
              (long long)E, (long long)edge_capacity);
   if (q->cap == 0 && q->n_src == q->n_dst) {
     // symmetric graph: the transpose is the row structure itself
-    hipLaunchKernelGGL(k_copy_i32, dim3(ceil_div(q->n_dst + 1, 256)), dim3(256), 0, s, g->row_ptr, q->n_dst + 1,
-                       g->csc_ptr);
-    if (E > 0)
-      hipLaunchKernelGGL(k_csc_symmetric, dim3(ceil_div(E, 256)), dim3(256), 0, s, g->row_ptr, g->col, g->dst, E,
-                         g->csc_eid);
+    const int64_t n_ptr = q->n_dst + 1;
+    hipLaunchKernelGGL(k_csc_symmetric, dim3((unsigned)ceil_div(std::max<int64_t>(E, n_ptr), 256)), dim3(256), 0, s,
+                       g->row_ptr, n_ptr, g->col, g->dst, E, g->csc_ptr, g->csc_eid);
     DSMP_LAUNCHED(h, "csc (symmetric graph)");
     return DSMP_OK;
   }
-  if ((st = fill_u32(h, w.indeg, q->n_src, 0)) != DSMP_OK) return st;
-  if ((st = fill_u32(h, w.scur, q->n_src, 0)) != DSMP_OK) return st;
+  if ((st = fill_u32(h, w.indeg, q->n_src, 0, w.scur)) != DSMP_OK) return st;
   if (E > 0) {
     hipLaunchKernelGGL(k_csc_count, dim3(ceil_div(E, 256)), dim3(256), 0, s, g->col, E, w.indeg);
     DSMP_LAUNCHED(h, "csc count");
