@@ -8,23 +8,27 @@ all inputs resident in HBM before timing starts:
   forward, then the backward through every layer in reverse (the feature
   gradient of layer l is the upstream gradient of layer l-1).
 
-Default workload: the Darcy-like case -- 8,192 nodes sampled from a 256x256
-grid, r = 0.04, d = 64, kernel MLP 6->128->128->4096, 4 layers, bf16 operands
-with fp32 accumulation.  Prints one JSON line.
+Default workload: one GPU's share of the 3-D step domain decomposition -- a
+262,144-node slab plus a halo of ghost nodes (23,420 sampled), r = 0.06,
+kNN cap 24, d = 128, kernel MLP 8->256->256->16384, 4 layers, bf16 operands
+with fp32 accumulation (the largest workload that fits one GPU).  Prints one
+JSON line.
 
 value = edges/s = E * layers / (seconds per step), i.e. edge-layer passes
 (forward + backward) per second, sampling and graph build included.
 
 Per kernel class the line carries the algorithmic work of one launch (flops,
 and the compulsory HBM bytes: inputs read once, outputs written once), the
-rates these give over the HIP-event launch time, and the bound (MFMA or HBM
-by arithmetic intensity).  `roofline` is that of the class taking the most
-time per step.  `executed_tflops_step` is the flops the kernels of the step
-actually perform (the modelled classes) over the step time.
-`per_edge_equivalent_tflops_step` is the nominal flop count of eq. (1) for
-one kernel evaluation per edge over the step time: a yardstick for comparing
-with per-edge implementations, not work done (the aggregate form reaches the
-same result with far fewer operations).
+rates these give over the HIP-event launch time (mean, median and minimum over
+the steps of a second, profiled pass), and the bound (MFMA or HBM by
+arithmetic intensity).  `roofline` is that of the class taking the most time
+per step.  `executed_tflops_step` is the flops the kernels of the step
+actually perform (the modelled classes) over the step time, and
+`executed_frac_peak` its fraction of the dense MFMA peak.  The nominal work of
+eq. (1) per edge (one kernel evaluation per retained edge, as a per-edge
+implementation performs it) is given as a count, `nominal_flops_per_edge_layer`,
+not as a rate: the aggregate form reaches the same result with far fewer
+operations.
 """
 
 import argparse
@@ -46,23 +50,26 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2)")
+    ap.add_argument("--config", type=int, default=5, help="workload 1..5 (default 5)")
     ap.add_argument("--algo", choices=["auto", "per_edge", "aggregate"], default="auto",
                     help="edge-contraction form (default: the library's automatic choice)")
     ap.add_argument("--model", choices=["layer", "hop"], default="layer",
                     help="layer: the NNConv layer stack (default); hop: the hop-loop training step "
                          "(encoder, layer + decoder per hop, masked MSE, backward)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=1536,
-                    help="destination rows of the oracle's timed layer sample")
+    ap.add_argument("--cpu-rows", type=int, default=None,
+                    help="destination rows of the oracle's timed sample (default: about 10-30 s of host work)")
     return ap.parse_args()
 
 
-TRAFFIC_TABLE = os.path.join(ROOT, "profiles", "darcy256_bf16_traffic.md")
+CPU_ROWS = {1: 1024, 2: 4096, 3: 2048, 4: 2048, 5: 4096}
+SRC_CORE = ["core.hip", "common.hpp"]
+SRC_GRAPH = ["graph.hip", "common.hpp"]
 SRC_FWD = ["nnconv_fwd.hip", "nnconv.hpp", "common.hpp"]
 SRC_BWD = ["nnconv_bwd.hip", "nnconv.hpp", "common.hpp"]
 SRC_AGG = ["nnconv_agg.hip", "nnconv.hpp", "common.hpp"]
 KERNEL_SOURCES = {
+    "sample": SRC_CORE, "gather": SRC_CORE, "graph": SRC_GRAPH,
     "edge_fwd": SRC_FWD, "edge_dh": SRC_FWD, "edge_mlp": SRC_FWD,
     "dz": SRC_BWD, "u_gemm": SRC_BWD, "dW2": SRC_BWD, "dW1": SRC_BWD,
     "dW3": SRC_BWD + ["nnconv_agg.hip"],
@@ -81,14 +88,19 @@ def source_digest(cls):
     return h.hexdigest()[:16]
 
 
+def traffic_table(workload):
+    return os.path.join(ROOT, "profiles", workload.replace("-", "_") + "_traffic.md")
+
+
 def measured_traffic(cls, workload):
     """HBM bytes per launch of kernel class ``cls`` from the committed
-    rocprofv3 FETCH_SIZE/WRITE_SIZE table, or None when the table covers
-    another workload or the kernel's sources changed since it was taken."""
-    if workload != "darcy256-bf16" or cls not in KERNEL_SOURCES or not os.path.exists(TRAFFIC_TABLE):
+    rocprofv3 FETCH_SIZE/WRITE_SIZE table of this workload, or None when
+    there is none or the kernel's sources changed since it was taken."""
+    table = traffic_table(workload)
+    if cls not in KERNEL_SOURCES or not os.path.exists(table):
         return None
     digest = source_digest(cls)
-    for line in open(TRAFFIC_TABLE):
+    for line in open(table):
         cells = [c.strip() for c in line.strip().strip("|").split("|")]
         if len(cells) == 6 and cells[0] == cls:
             return int(float(cells[5])) if cells[2] == digest else None
@@ -157,6 +169,22 @@ def agg_work(w, E, n_src, fused=False):
     return {
         "dz": dz,
         "dW3": (2 * n * kt * d, n * kt * esz + n * d * esz),
+    }
+
+
+def prep_work_step(w, E):
+    """Algorithmic work per step of the data-preparation classes (no flops):
+    sampling writes the kept indices (the keys are recomputed, nothing is
+    read); the gathers read and write every sampled row of positions,
+    attributes and features plus its index; the graph build reads the
+    positions once and writes row_ptr, col, dst, csc_ptr and csc_eid."""
+    esz = 2 if w.dtype == "bf16" else 4
+    s_all = sum(p.s for p in w.parts)
+    row = 4 * w.D + 4 * (w.D + 1) + w.d * esz
+    return {
+        "sample": (0, 4 * s_all),
+        "gather": (0, s_all * (2 * row + 3 * 4)),
+        "graph": (0, w.n_src * 4 * w.D + 12 * E + 4 * (w.n_dst + 1) + 4 * (w.n_src + 1)),
     }
 
 
@@ -314,10 +342,12 @@ def hop_cpu_baseline(w, E_gpu, m=1536):
 
 
 def cpu_baseline(w, rows_n, E_gpu):
-    """Time the oracle, as it stands, on the host: sampling and the radius
-    graph of the whole workload, and one layer forward+backward on a fixed
-    subset of destination rows (sparse upstream gradient), extrapolated to the
-    step's E * layers."""
+    """Time the oracle, as it stands, on the host, on a bounded sample of the
+    workload: the sampling of every part (whole), then, for a fixed set of
+    destination rows, their radius-graph rows and one layer forward+backward
+    (sparse upstream gradient: only their edges are visited).  The per-step
+    time of the whole workload is extrapolated from the sample by its share
+    of the edges: t_sample + (t_graph_rows + layers * t_layer_rows) * E / E_rows."""
     import numpy as np
     import oracle
     from threadpoolctl import threadpool_info
@@ -328,29 +358,33 @@ def cpu_baseline(w, rows_n, E_gpu):
         pos.append(p.pos[idx]); attr.append(p.attr[idx]); h.append(p.h[idx])
     t_sample = time.perf_counter() - t
     pos, attr, h = np.concatenate(pos), np.concatenate(attr), np.concatenate(h).astype(np.float64)
-    t = time.perf_counter()
-    rp, col = oracle.radius_graph.radius_graph(pos, w.n_dst, w.r, w.cap, w.cap_mode)
-    t_graph = time.perf_counter() - t
     rows = np.sort(np.random.default_rng(0).choice(w.n_dst, min(rows_n, w.n_dst), replace=False))
-    E_sub = int(sum(rp[i + 1] - rp[i] for i in rows))
+    t = time.perf_counter()
+    lists = oracle.radius_graph.rows_subset(pos, rows, w.n_dst, w.r, w.cap, w.cap_mode)
+    t_graph = time.perf_counter() - t
+    deg = np.zeros(w.n_dst, np.int64)
+    deg[rows] = [len(c) for c in lists]
+    rp = np.zeros(w.n_dst + 1, np.int64)
+    np.cumsum(deg, out=rp[1:])
+    col = np.concatenate(lists) if lists else np.zeros(0, np.int32)
+    E_sub = int(rp[-1])
     G = np.zeros((w.n_dst, w.d))
     G[rows] = w.grad_out[rows]
-    decide = w.dtype
     t = time.perf_counter()
     x = oracle.nnconv.edge_attr(attr, rp, col)
-    oracle.nnconv.forward(w.params[0], x, h, rp, col, w.n_dst, rows=rows, decide=decide)
-    oracle.nnconv.backward(w.params[0], x, h, rp, col, w.n_dst, G, rows=rows, decide=decide)
+    oracle.nnconv.forward(w.params[0], x, h, rp, col, w.n_dst, rows=rows)
+    oracle.nnconv.backward(w.params[0], x, h, rp, col, w.n_dst, G, rows=rows)
     t_layer_sub = time.perf_counter() - t
-    E = int(rp[-1])
-    t_step = t_sample + t_graph + w.layers * t_layer_sub * E / max(E_sub, 1)
+    t_step = t_sample + (t_graph + w.layers * t_layer_sub) * E_gpu / max(E_sub, 1)
     threads = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
     return {
-        "value": E * w.layers / t_step, "unit": "edges/s", "cores": int(threads), "kind": "oracle",
-        "sample": ("sampling and radius graph of the whole workload (%.2f s + %.2f s), one layer forward+"
-                   "backward on %d destination rows = %d of %d edges (%.2f s), extrapolated to %d layers; "
-                   "%d BLAS threads, %d cores in affinity; E matches the GPU's: %s"
-                   % (t_sample, t_graph, len(rows), E_sub, E, t_layer_sub, w.layers, threads,
-                      len(os.sched_getaffinity(0)), E == E_gpu)),
+        "value": E_gpu * w.layers / t_step, "unit": "edges/s", "cores": int(threads), "kind": "oracle",
+        "sample": ("subset-extrapolated: sampling of every part (%.2f s), then %d fixed destination rows "
+                   "(%d of the %d edges): their radius-graph rows (%.2f s) and one layer forward+backward "
+                   "(%.2f s); the step time of the whole workload extrapolated by the edge share to %d layers; "
+                   "%d BLAS threads, %d cores in affinity"
+                   % (t_sample, len(rows), E_sub, E_gpu, t_graph, t_layer_sub, w.layers, threads,
+                      len(os.sched_getaffinity(0)))),
         "seconds": round(t_sample + t_graph + t_layer_sub, 2),
     }
 
@@ -386,16 +420,20 @@ def main():
     ms = (t1 - t0) * 1e3 / args.steps
     print("timed %d steps: %.3f ms/step" % (args.steps, ms), file=sys.stderr, flush=True)
 
-    # per-kernel durations: HIP events recorded by the library on its stream
+    # per-kernel durations: HIP events recorded by the library on its stream,
+    # read after every step of a second pass (mean, median and minimum)
+    import statistics
     lib.dsmp_profile_enable(True)
-    lib.dsmp_profile_reset()
+    per_step = []
     for _ in range(args.steps):
+        lib.dsmp_profile_reset()
         pipe.step()
-    prof = lib.dsmp_profile_read()
+        per_step.append(lib.dsmp_profile_read())
     lib.dsmp_profile_enable(False)
 
     E, L = pipe.E, w.layers
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_TFLOPS
+    prof = {k: (sum(p[k][0] for p in per_step), sum(p[k][1] for p in per_step)) for k in per_step[0]}
     agg = "edge_mlp" in prof and prof["edge_mlp"][1] > 0
     if hop:   # the layer of the hop loop reads difference attributes (dim+1 per edge)
         import dataclasses
@@ -403,12 +441,18 @@ def main():
     fused = agg and not ("dW2" in prof and prof["dW2"][1] > 0)
     work = work_model(w, E, w.n_src, fused)
     work.update(agg_work(w, E, w.n_src, fused) if agg else per_edge_work(w, E, w.n_src))
+    for name, (fl, by) in prep_work_step(w, E).items():
+        if name in prof and prof[name][1] > 0:
+            nper = prof[name][1] / args.steps
+            work[name] = (fl / nper, by / nper)
     kernels = {}
     for name, (tot, n) in prof.items():
         if n == 0:
             continue
         avg = tot / n
-        ent = {"ms_avg": round(avg, 5), "launches_per_step": n / args.steps,
+        launch_ms = [p[name][0] / p[name][1] for p in per_step if p[name][1] > 0]
+        ent = {"ms_avg": round(avg, 5), "ms_median": round(statistics.median(launch_ms), 5),
+               "ms_min": round(min(launch_ms), 5), "launches_per_step": n / args.steps,
                "ms_per_step": round(tot / args.steps, 4)}
         if name in work:
             fl, by = work[name]
@@ -427,8 +471,8 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": dk["gbps"], "peak": HBM_TBPS * 1e3, "unit": "GB/s", "frac": dk["frac"],
                 "algorithmic": dk["bytes"]}
-    roof.update({"kernel": dom, "traffic": measured_traffic(dom, w.name), "ms_per_launch": dk["ms_avg"]})
-    flops_step = L * (E * method_flops_per_edge(w) + w.n_dst * 6 * w.d * w.d)
+    roof.update({"kernel": dom, "traffic": measured_traffic(dom, w.name), "ms_per_launch": dk["ms_avg"],
+                 "ms_per_launch_median": dk["ms_median"], "ms_per_launch_min": dk["ms_min"]})
     executed = sum(v["flops"] * v["launches_per_step"] for v in modeled.values())
     if hop:
         METRIC_RUN = ("edges/sec of the hop-loop training step (encoder, layer + decoder per hop, masked MSE, "
@@ -443,21 +487,24 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic (seeded stand-in for the paper's mesh datasets)",
-        "config": {"workload": "%s: %d nodes sampled from %d candidates, radius %.3g, cap %s, d=%d, kernel MLP "
+        "config": {"workload": "%s: %d nodes sampled from %d candidates%s, radius %.3g, cap %s, d=%d, kernel MLP "
                                "%d->%d->%d->%d, %d %s, sample+graph+forward+backward per step"
-                               % (w.name, w.n_dst, sum(p.pos.shape[0] for p in w.parts), w.r, w.cap or "none",
+                               % (w.name, w.n_dst, sum(p.pos.shape[0] for p in w.parts),
+                                  " (plus %d halo nodes)" % (w.n_src - w.n_dst) if w.n_src > w.n_dst else "",
+                                  w.r, w.cap or "none",
                                   w.d, w.de, w.H1, w.H2, w.d * w.d, L,
                                   "hops (encoder and decoder 64 wide, difference attributes)" if hop else "layers"),
                    "n_dst": w.n_dst, "n_src": w.n_src, "edges": E, "layers": L, "d": w.d, "h1": w.H1,
-                   "h2": w.H2},
+                   "h2": w.H2, "nominal_flops_per_edge_layer": method_flops_per_edge(w)},
         "edge_algorithm": "aggregate" if agg else "per_edge",
         "executed_tflops_step": round(executed / (ms * 1e-3) / 1e12, 2),
-        "per_edge_equivalent_tflops_step": round(flops_step / (ms * 1e-3) / 1e12, 2),
+        "executed_frac_peak": round(executed / (ms * 1e-3) / 1e12 / peak, 4),
         "roofline": roof,
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = hop_cpu_baseline(w, E) if hop else cpu_baseline(w, args.cpu_rows, E)
+        rows_n = args.cpu_rows if args.cpu_rows is not None else CPU_ROWS[args.config]
+        res["cpu_baseline"] = hop_cpu_baseline(w, E) if hop else cpu_baseline(w, rows_n, E)
     print(json.dumps(res), flush=True)
 
 

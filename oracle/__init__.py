@@ -22,10 +22,12 @@ Contents, each following the paper passage named in its module docstring:
 * ``hop``          -- encoder / decoder perceptrons, the masked MSE and the
                       hop loop of Algorithm 1 (eqs. (i)-(iv)) on one
                       sub-domain, forward and backward.
+* ``infer``        -- sub-domain inference with reassembly (Sec. 3, testing
+                      procedure).
 
 Floating point: the layer runs in float64.  The radius test runs in float32
 in a fixed evaluation order (no fused multiply-add), because the paper fixes
 no precision and the GPU must reproduce the edge set bit for bit.
 """
 
-from . import rng, sampling, radius_graph, nnconv, hop  # noqa: F401
+from . import rng, sampling, radius_graph, nnconv, hop, infer  # noqa: F401

@@ -125,7 +125,7 @@ def test_layer_attribute_gradient(env, shape, algo):
         lib.dsmp_nnconv_backward(desc, packed, G, t_attr, t_h, saved, _dev(torch, Gout), grads=grads)
         torch.cuda.synchronize()
         x = onn.edge_attr(attr, rp, col, "diff")
-        ref = onn.backward(P, x, h.astype(np.float64), rp, col, n, Gout, decide=dtype)
+        ref = onn.backward(P, x, h.astype(np.float64), rp, col, n, Gout, precision=dtype)
         dst = org.dst_of_edges(rp)
         want = np.zeros((n, D + 1))
         allow = np.zeros((n, D + 1))
@@ -189,24 +189,14 @@ def _hop_case(seed, n, D, d, h1, h2, hid, dtype, r, cap):
 
 # (seed, n, D, d, h1, h2, hidden, dtype, r, cap, hops).
 #
-# Float32 steps are compared in full (loss, outputs, every gradient) at 1e-4
-# over several hops.  Their seeds are chosen on the oracle alone so that no
-# ReLU decision sits within a relative margin of 1e-5 of its kink, where
-# float32 and float64 could decide differently.
-#
-# bf16 steps: from the second hop on, the layer's edge attributes are
-# differences of decoder outputs, which the two sides round differently
-# (float32 against float64).  A kernel-MLP decision or a bf16 rounding of z1
-# near its boundary can then go either way, and a gradient is discontinuous
-# in such a choice, while the forward values are not.  So every bf16 step
-# compares the loss and the outputs, and the gradients are compared for
-# one-hop steps, whose attributes are the input values on both sides.  Their
-# encoder and decoder decisions are kept 1e-5 away from the kinks as above.
-# A composed step's gradients carry the layer's bf16 roundings (g, z, the
-# products h_j g_i or the sums S_i and U_i, da2, da1: up to about 3 * 2^-9
-# per term) through the float32 perceptrons on either side, so they are held
-# to 3e-2 (the layer alone: 2e-2).
-TOL_STEP = {"f32": TOL["f32"], "bf16": 3e-2}
+# Every step is compared in full: loss, outputs and every gradient, at the
+# layer's bar (1e-4 float32, 2e-2 bf16) beyond the allowances of the oracle's
+# precision model.  The model carries the spread of every value through the
+# hops (from the second hop on, the edge attributes are differences of
+# decoder outputs that a kernel rounds its own way), gives every ReLU
+# decision of the perceptrons and the layer a band and a flip probability,
+# and propagates the effect of flips back through the loop.  The number of
+# decisions inside their bands and the size of the allowances are printed.
 HOP_CASES = {
     "f32_32_1hop": (16, 120, 2, 32, 64, 64, 32, "f32", 0.2, 10, 1),
     "f32_32_2hops": (39, 96, 2, 32, 64, 64, 32, "f32", 0.2, 8, 2),
@@ -226,7 +216,6 @@ def test_hop_train_step(env, name):
     announce("hop", name)
     Pe, Pk, Pd, v0, Y, mask, rp, col = _hop_case(seed, n, D, d, h1, h2, hid, dtype, r, cap)
     ref = ohop.train_step(Pe, Pk, Pd, v0, Y, mask.astype(bool), rp, col, hops, dtype)
-    assert (ref["margin"] if dtype == "f32" else ref["mlp_margin"]) >= 1e-5
     cp, ceid = org.transpose(rp, col, n)
     i32 = lambda a: _dev(torch, a.astype(np.int32))
     G = dm.Graph(n, n, col.size, i32(rp), i32(col), i32(org.dst_of_edges(rp)), i32(cp), i32(ceid))
@@ -238,16 +227,17 @@ def test_hop_train_step(env, name):
     tPd = {k: _dev(torch, v) for k, v in Pd.items()}
     loss, grads = st.step(tPe, packed, tPd, _dev(torch, v0), _dev(torch, Y), _dev(torch, mask))
     torch.cuda.synchronize()
-    tol = TOL_STEP[dtype]
-    print("E=%d loss gpu %.6e oracle %.6e margin %.2e" % (col.size, loss.item(), ref["loss"], ref["margin"]))
-    assert abs(loss.item() - ref["loss"]) <= tol * abs(ref["loss"])
-    assert rel_err(st.v[hops - 1].cpu().numpy(), ref["v"]) <= tol
-    assert rel_err(st.out[hops - 1].cpu().numpy(), ref["vL"]) <= tol
-    if dtype == "bf16" and hops > 1:
-        return
+    tol = TOL[dtype]
+    A = ref["allow"]
+    print("E=%d loss gpu %.6e oracle %.6e (allowance %.2e), decisions inside their bands: %d"
+          % (col.size, loss.item(), ref["loss"], A["loss"], ref["ambiguous"]))
+    assert abs(loss.item() - ref["loss"]) <= A["loss"] + tol * abs(ref["loss"])
+    assert rel_err(st.v[hops - 1].cpu().numpy(), ref["v"], A["v"]) <= tol
+    assert rel_err(st.out[hops - 1].cpu().numpy(), ref["vL"], A["vL"]) <= tol
     for group in ("enc", "conv", "dec"):
         for k, want in ref[group].items():
-            allow = ref["conv_allow"][k] if group == "conv" else None
+            allow = A[group][k]
             err = rel_err(grads[group][k].cpu().numpy().reshape(want.shape), want, allow)
-            print("  %s %s err %.3e" % (group, k, err))
+            print("  %s %s err %.3e (allowance/max %.3f)" % (group, k, err,
+                                                            allow.max() / max(np.abs(want).max(), 1e-300)))
             assert err <= tol, (group, k, err)

@@ -137,14 +137,29 @@ def test_train_step_matches_torch_autograd():
             assert np.allclose(t.grad.numpy(), res[g]["d" + k], atol=1e-10), (g, k)
 
 
-def test_margin_reports_smallest_relu_margin():
+def test_ambiguous_decisions_are_counted_and_allowed_for():
     Pe, Pk, Pd, v0, Y, mask, rp, col = _case(5)
     res = hop.train_step(Pe, Pk, Pd, v0, Y, mask, rp, col, 2)
-    assert 0.0 <= res["margin"] < 1.0
-    # pushing one encoder pre-activation onto its kink drives the margin to 0
+    base = res["ambiguous"]
+    for g in ("enc", "conv", "dec"):
+        for k, v in res[g].items():
+            assert res["allow"][g][k].shape == v.shape and np.all(res["allow"][g][k] >= 0), (g, k)
+    # pushing one encoder pre-activation onto its kink adds an ambiguous decision
     a1 = v0[0] @ Pe["W1"][0]
     Pe["b1"][0] = -a1
-    assert hop.train_step(Pe, Pk, Pd, v0, Y, mask, rp, col, 2)["margin"] == 0.0
+    res2 = hop.train_step(Pe, Pk, Pd, v0, Y, mask, rp, col, 2)
+    assert res2["ambiguous"] >= base + 1
+    assert res2["allow"]["enc"]["dW1"][0].max() > 0
+
+
+def test_model_does_not_change_the_step():
+    """The allowances ride along: a bfloat16 step differs from the float32
+    one only in the rounding of the layer's input features."""
+    Pe, Pk, Pd, v0, Y, mask, rp, col = _case(8)
+    a = hop.train_step(Pe, Pk, Pd, v0, Y, mask, rp, col, 2, "f32")
+    b = hop.train_step(Pe, Pk, Pd, v0, Y, mask, rp, col, 2, "bf16")
+    assert abs(a["loss"] - b["loss"]) <= 1e-2 * abs(a["loss"])
+    assert b["allow"]["loss"] > a["allow"]["loss"]
 
 
 def test_zero_hops_is_decoder_free_encoder_loss():

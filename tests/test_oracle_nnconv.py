@@ -261,67 +261,199 @@ def test_bf16_rounding_known_values():
     assert np.array_equal(nn.bf16(r), lib.astype(np.float64))
 
 
-def test_a1_float32_chain_bounds_and_exact_cases():
-    g = np.random.default_rng(3)
-    P = {"W1": g.normal(size=(16, 6)).astype(np.float32), "b1": g.normal(size=16).astype(np.float32)}
-    x = g.uniform(0, 2, (500, 6)).astype(np.float32)
-    a64 = x.astype(np.float64) @ P["W1"].astype(np.float64).T + P["b1"]
-    a32 = nn.a1_float32(P, x)
-    s1 = np.abs(x) @ np.abs(P["W1"]).T.astype(np.float64) + np.abs(P["b1"])
-    assert np.all(np.abs(a32 - a64) <= 6 * 2.0 ** -24 * s1)
-    assert np.all(a32 == a32.astype(np.float32))           # representable in float32
-    # small integers: no rounding anywhere, so the chain is exact
-    Pi = {"W1": g.integers(-3, 4, (8, 4)).astype(np.float32), "b1": g.integers(-3, 4, 8).astype(np.float32)}
-    xi = g.integers(-3, 4, (50, 4)).astype(np.float32)
-    assert np.array_equal(nn.a1_float32(Pi, xi), xi.astype(np.float64) @ Pi["W1"].T.astype(np.float64) + Pi["b1"])
+# A plain evaluation in the workloads' precision, written here for the pins
+# only: float32 arithmetic, operands of bfloat16 products rounded to bfloat16
+# where they are formed, sums in the order numpy's float32 routines take
+# (forward) or in reverse attribute / neuron order.  It is one of the many
+# evaluations a correct kernel may perform; the precision model must cover it.
+
+def _bf(a):
+    return nn.bf16(a).astype(np.float32)
 
 
-@pytest.mark.parametrize("decide", ["f32", "bf16"])
-def test_decided_layer_matches_float64_away_from_kinks(decide):
-    na, rp, col, P, h, x = _random_case(12, n=60, n_dst=50, cap=8)
-    P32 = {k: v.astype(np.float32) for k, v in P.items()}
-    G = np.random.default_rng(1).normal(size=(50, h.shape[1]))
-    ref = nn.backward(P32, x, h, rp, col, 50, G)
-    got = nn.backward(P32, x, h, rp, col, 50, G, decide=decide)
-    a1, z1, a2, z = nn._edge_mlp(nn._as64(P32), x)
-    # the decided masks agree with float64 signs except within the rounding band
-    a1d = nn.a1_float32(P32, x)
-    assert np.all((a1d > 0) == (a1 > 0))
-    if decide == "f32":
-        for k in ref:
-            if k != "allow":
-                assert np.allclose(got[k], ref[k], rtol=1e-9, atol=1e-9), k
+def _eval_lowp(P, x, h, rp, col, n_dst, precision, reverse=False):
+    f = np.float32
+    P32 = {k: np.asarray(v, dtype=f) for k, v in P.items()}
+    x32, h32 = np.asarray(x, dtype=f), np.asarray(h, dtype=f)
+    rd = (lambda a: _bf(a)) if precision == "bf16" else (lambda a: a.astype(f))
+    if reverse:
+        a1 = np.broadcast_to(P32["b1"], (x32.shape[0], P32["b1"].size)).astype(f).copy()
+        for c in reversed(range(x32.shape[1])):
+            a1 = (a1 + x32[:, c:c + 1] * P32["W1"][None, :, c]).astype(f)
+    else:
+        a1 = (x32 @ P32["W1"].T + P32["b1"]).astype(f)
+    z1 = rd(np.maximum(a1, f(0)))
+    if reverse:
+        a2 = np.broadcast_to(P32["b2"], (x32.shape[0], P32["b2"].size)).astype(f).copy()
+        for j in reversed(range(z1.shape[1])):
+            a2 = (a2 + z1[:, j:j + 1] * P32["W2"][None, :, j]).astype(f)
+    else:
+        a2 = (z1 @ P32["W2"].T + P32["b2"]).astype(f)
+    z = rd(np.maximum(a2, f(0)))
+    d = h32.shape[1]
+    theta = (z @ P32["W3"].T + P32["b3"]).astype(f).reshape(-1, d, d)
+    m = np.einsum("epq,ep->eq", theta, h32[col]).astype(f)
+    deg = np.diff(rp)[:n_dst]
+    agg = np.zeros((n_dst, d), f)
+    np.add.at(agg, np.repeat(np.arange(n_dst), deg), m)
+    agg[deg > 0] /= deg[deg > 0][:, None].astype(f)
+    y = (agg + h32[:n_dst] @ P32["Wr"].T + P32["br"]).astype(f)
+    return a1.astype(np.float64), a2.astype(np.float64), y.astype(np.float64)
 
 
-@pytest.mark.parametrize("layer", ["a1", "a2"])
-def test_allowance_covers_flipped_decisions(monkeypatch, layer):
-    """Plant flips of every decision of one layer that the oracle calls
-    ambiguous (with that layer's band widened so there are many); the change
-    must stay within the allowance.  Flipping a1 also moves z1 inside the
-    band, a second-order effect on dW2 that is negligible at the real band
-    width but not at this one, so that case checks dW1 and db1 only."""
-    na, rp, col, P, h, x = _random_case(13, n=80, n_dst=70, cap=10)
-    P32 = {k: v.astype(np.float32) for k, v in P.items()}
-    G = np.random.default_rng(2).normal(size=(70, h.shape[1]))
-    monkeypatch.setattr(nn, "_EPS_A1" if layer == "a1" else "_EPS_A2", 0.05)
-    base = nn.backward(P32, x, h, rp, col, 70, G, decide="f32")
-    orig = nn._edge_mlp_decided
+def _lowp_case(seed, precision, n=300, d=16, H1=32, H2=32):
+    from workloads import layer_params
+    g = np.random.default_rng(seed)
+    na = g.uniform(0, 1, (n, 3)).astype(np.float32)
+    rp, col = rg.radius_graph(na[:, :2], n, 0.12, 16)
+    P = layer_params(g, d, 6, H1, H2, precision)
+    h = g.normal(size=(n, d)).astype(np.float32)
+    if precision == "bf16":
+        h = _bf(h)
+    return na, rp, col, P, h.astype(np.float64), nn.edge_attr(na, rp, col)
 
-    def flipped(P_, x_, decide):
-        a1, z1, a2, z, m1, m2, zq, amb1, amb2 = orig(P_, x_, decide)
-        m1 = np.where(amb1, ~m1, m1)
-        m2 = np.where(amb2, ~m2, m2)
-        z1 = np.where(m1, a1, 0.0)
-        a2 = z1 @ P_["W2"].T + P_["b2"]
-        z = np.where(m2, a2, 0.0)
-        return a1, z1, a2, z, m1, m2, zq, amb1, amb2
 
-    monkeypatch.setattr(nn, "_edge_mlp_decided", flipped)
-    alt = nn.backward(P32, x, h, rp, col, 70, G, decide="f32")
-    keys = ("dW2", "db2", "dW1", "db1") if layer == "a2" else ("dW1", "db1")
-    nflip = 0
-    for k in keys:
-        diff = np.abs(alt[k] - base[k])
-        nflip += int((diff > 1e-12).sum())
-        assert np.all(diff <= base["allow"][k] + 1e-9 * np.abs(base[k]).max()), k
-    assert nflip > 0
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
+@pytest.mark.parametrize("reverse", [False, True])
+def test_precision_model_covers_a_low_precision_evaluation(precision, reverse):
+    """The deviations of a float32 / bfloat16 evaluation from the float64
+    values stay within the modelled spread (root mean square below one
+    standard deviation, none beyond the band), and its decisions agree with
+    the float64 decisions outside the band."""
+    na, rp, col, P, h, x = _lowp_case(21 + reverse, precision)
+    n = len(rp) - 1
+    em = nn.edge_mlp(P, x, precision)
+    _, y, st = nn.forward(P, x, h, rp, col, n, nn.ACT_RELU, precision=precision, return_stats=True)
+    a1, a2, yl = _eval_lowp(P, x, h, rp, col, n, precision, reverse)
+    for got, want, var in ((a1, em["a1"], em["v1"]), (a2, em["a2"], em["v2"]), (yl, y, st["y_var"])):
+        t = (got - want) / np.sqrt(var)
+        assert np.sqrt(np.mean(t * t)) <= 1.0
+        assert np.abs(t).max() <= nn.BAND_SIGMAS
+        band = nn.ambiguous(want, var)
+        assert np.array_equal((got > 0)[~band], (want > 0)[~band])
+
+
+def test_exact_arithmetic_has_no_band():
+    na, rp, col, P, h, x = _lowp_case(23, "f32", n=80)
+    em = nn.edge_mlp(P, x, None)
+    assert "v1" not in em
+    ref = nn.backward(P, x, h, rp, col, 80, np.ones((80, 16)))
+    assert ref["allow"] == {}
+    # a small-integer layer in float32 is computed exactly, and the model's
+    # spread of a1 is within one rounding of its largest partial sum
+    Pi = {"W1": np.arange(-6, 6).reshape(2, 6).astype(np.float64), "b1": np.array([1.0, -2.0]),
+          "W2": np.eye(2), "b2": np.zeros(2)}
+    xi = np.array([[1, 0, 2, 0, 1, 1], [0, 1, 1, 1, 0, 0]], np.float64)
+    em = nn.edge_mlp(Pi, xi, "f32")
+    s1 = np.abs(xi) @ np.abs(Pi["W1"]).T + np.abs(Pi["b1"])
+    assert np.all(np.sqrt(em["v1"]) <= 7 * nn.U_F32 * s1)
+    assert np.array_equal(em["a1"], xi @ Pi["W1"].T + Pi["b1"])
+
+
+def test_flip_probability_closed_form():
+    from math import erfc, sqrt
+    assert nn.flip_probability(0.0, 1.0) == pytest.approx(0.5)
+    assert nn.flip_probability(1.0, 1.0) == pytest.approx(0.5 * erfc(1 / sqrt(2)))
+    assert nn.flip_probability(-3.0, 4.0) == pytest.approx(0.5 * erfc(1.5 / sqrt(2)))
+    assert nn.flip_probability(1.0, 0.0) == 0.0
+    assert nn.flip_probability(50.0, 1.0) < 1e-300 or nn.flip_probability(50.0, 1.0) == 0.0
+
+
+def test_bernstein_allowance_closed_form():
+    L = 0.5 * nn.ALLOW_SIGMAS ** 2
+    # no single-flip bound: the Gaussian case, ALLOW_SIGMAS standard deviations
+    assert nn.bernstein_allowance(np.array(4.0), np.array(0.0), np.array(0.0)) == pytest.approx(2 * nn.ALLOW_SIGMAS)
+    # no variance: 2 L b / 3 (one flip of size b is covered for ALLOW_SIGMAS >= 2)
+    assert nn.bernstein_allowance(np.array(0.0), np.array(3.0), np.array(-1.0)) == pytest.approx(1 + 2 * L)
+    t = nn.bernstein_allowance(np.array(2.0), np.array(0.5), np.array(0.0))
+    assert t * t / 2 == pytest.approx(L * (2.0 + 0.5 * t / 3))
+
+
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
+def test_values_do_not_depend_on_the_model(precision):
+    na, rp, col, P, h, x = _lowp_case(24, precision, n=120)
+    G = np.random.default_rng(1).normal(size=(120, 16))
+    a = nn.backward(P, x, h, rp, col, 120, G, nn.ACT_RELU)
+    b = nn.backward(P, x, h, rp, col, 120, G, nn.ACT_RELU, precision=precision)
+    for k in a:
+        if k != "allow":
+            assert np.array_equal(a[k], b[k]), k
+    assert np.array_equal(nn.forward(P, x, h, rp, col, 120)[0],
+                          nn.forward(P, x, h, rp, col, 120, precision=precision)[0])
+
+
+def _flipped_backward(monkeypatch, P, x, h, rp, col, n, G, precision, choose):
+    """Backward with masks changed where ``choose(em)`` says (values kept):
+    a kernel that took those decisions the other way."""
+    orig = nn.edge_mlp
+
+    def patched(P_, x_, precision_=None, x_var=None):
+        em = orig(P_, x_, precision_, x_var)
+        if precision_ is not None:
+            f1, f2 = choose(em)
+            em = dict(em, m1=em["m1"] ^ f1, m2=em["m2"] ^ f2)
+        return em
+
+    monkeypatch.setattr(nn, "edge_mlp", patched)
+    try:
+        return nn.backward(P, x, h, rp, col, n, G, precision=precision)
+    finally:
+        monkeypatch.setattr(nn, "edge_mlp", orig)
+
+
+def test_allowance_covers_random_flips(monkeypatch):
+    """Flip each decision with its modelled probability (several draws): the
+    weight gradients move by less than their allowance."""
+    na, rp, col, P, h, x = _lowp_case(25, "bf16", n=400, d=16, H1=64, H2=64)
+    n = len(rp) - 1
+    G = np.random.default_rng(3).normal(size=(n, 16))
+    base = nn.backward(P, x, h, rp, col, n, G, precision="bf16")
+    em = nn.edge_mlp(P, x, "bf16")
+    assert em["amb1"].sum() + em["amb2"].sum() > 20        # the draws do flip decisions
+    rng = np.random.default_rng(4)
+    moved = 0
+    for _ in range(4):
+        alt = _flipped_backward(monkeypatch, P, x, h, rp, col, n, G, "bf16",
+                                lambda e: (rng.uniform(size=e["p1"].shape) < e["p1"],
+                                           rng.uniform(size=e["p2"].shape) < e["p2"]))
+        for k in ("dW1", "db1", "dW2", "db2"):
+            diff = np.abs(alt[k] - base[k])
+            moved += int((diff > 0).sum())
+            assert np.all(diff <= base["allow"][k]), k
+    assert moved > 0
+
+
+def test_worst_case_covers_every_ambiguous_flip(monkeypatch):
+    """grad_x of an edge moves by at most its worst-case allowance when every
+    ambiguous decision of the edge is flipped."""
+    na, rp, col, P, h, x = _lowp_case(26, "bf16", n=300, d=16, H1=64, H2=64)
+    n = len(rp) - 1
+    G = np.random.default_rng(5).normal(size=(n, 16))
+    base = nn.backward(P, x, h, rp, col, n, G, precision="bf16")
+    alt = _flipped_backward(monkeypatch, P, x, h, rp, col, n, G, "bf16", lambda e: (e["amb1"], e["amb2"]))
+    diff = np.abs(alt["grad_x"] - base["grad_x"])
+    assert diff.max() > 0
+    assert np.all(diff <= base["allow"]["grad_x"] * (1 + 1e-9) + 1e-15)
+
+
+def test_allowance_propagates_an_upstream_variance():
+    """A variance of grad_out reaches every gradient linear in it; with unit
+    variance on one row the dWr allowance is ALLOW_SIGMAS * |h_i| per column."""
+    na, rp, col, P, h, x = _lowp_case(27, "f32", n=60)
+    G = np.random.default_rng(6).normal(size=(60, 16))
+    Gv = np.zeros_like(G)
+    Gv[7] = 1.0
+    a = nn.backward(P, x, h, rp, col, 60, G, precision="f32")
+    b = nn.backward(P, x, h, rp, col, 60, G, precision="f32", grad_var=Gv)
+    assert np.allclose(b["var"]["dWr"] - a["var"]["dWr"], np.outer(Gv[7], h[7] ** 2))
+    for k in ("dW3", "db3", "grad_h"):
+        assert b["allow"][k].max() > a["allow"][k].max(), k
+
+
+def test_model_pin_catches_a_dropped_rounding(monkeypatch):
+    """Planted mistake: a model that forgets the bfloat16 rounding of the
+    product operands underestimates the spread, and the coverage pin fails."""
+    orig = nn.units
+    monkeypatch.setattr(nn, "units", lambda p: (nn.U_F32, nn.U_F32) if p == "bf16" else orig(p))
+    with pytest.raises(AssertionError):
+        test_precision_model_covers_a_low_precision_evaluation("bf16", False)

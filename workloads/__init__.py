@@ -33,4 +33,4 @@ Seeds: geometry and features 1000+k, parameters 2000+k, upstream gradient
 3000+k, the sampler seed handed to the library 4000+k; numpy PCG64.
 """
 
-from .configs import Workload, make_config, bf16_round, layer_params, hop_setup, CONFIG_IDS  # noqa: F401
+from .configs import Workload, make_config, bf16_round, layer_params, hop_setup, subdomain_boxes, CONFIG_IDS  # noqa: F401

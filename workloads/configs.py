@@ -20,10 +20,9 @@ def bf16_round(x: np.ndarray) -> np.ndarray:
     so both sides start from identical values.
     """
     a = np.ascontiguousarray(x, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    lsb = (u >> np.uint64(16)) & np.uint64(1)
-    u = (u + np.uint64(0x7FFF) + lsb) & np.uint64(0xFFFF0000)
-    out = u.astype(np.uint32).view(np.float32)
+    u = a.view(np.uint32)
+    # uint32 arithmetic: no finite value carries past bit 31
+    out = ((u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) & np.uint32(0xFFFF0000)).view(np.float32)
     nan = np.isnan(a)
     if nan.any():
         out = out.copy()
@@ -309,3 +308,27 @@ def hop_setup(w: Workload, hid: int = 64):
     conv = layer_params(rng, w.d, c, w.H1, w.H2, w.dtype)
     Y = rng.standard_normal((w.n_src, c)).astype(np.float32)
     return enc, conv, dec, Y
+
+
+def subdomain_boxes(w: Workload, cuts_per_axis=None, seed_offset: int = 0):
+    """Random sub-domains for the inference of workload w (seed 6000 + k):
+    boxes [lo, hi) that tile space, cut at uniformly drawn positions inside
+    the extent of the candidate points along each axis (the outermost sides
+    are infinite, so every node has exactly one owning box).  cuts_per_axis
+    [D] gives the number of cuts per axis (default: the 2-D squares 1 x 1, the
+    3-D channels 7 cuts along x)."""
+    rng = np.random.Generator(np.random.PCG64(6000 + w.k + seed_offset))
+    if cuts_per_axis is None:
+        cuts_per_axis = [1, 1] if w.D == 2 else [7, 0, 0]
+    allpos = np.concatenate([p.pos for p in w.parts])
+    lo_ext, hi_ext = allpos.min(0).astype(np.float64), allpos.max(0).astype(np.float64)
+    edges = []
+    for a in range(w.D):
+        c = np.sort(rng.uniform(lo_ext[a], hi_ext[a], cuts_per_axis[a])).astype(np.float32)
+        edges.append(np.concatenate([[-np.inf], c, [np.inf]]).astype(np.float32))
+    boxes = []
+    for cell in np.ndindex(*[len(e) - 1 for e in edges]):
+        lo = [float(edges[a][cell[a]]) for a in range(w.D)]
+        hi = [float(edges[a][cell[a] + 1]) for a in range(w.D)]
+        boxes.append((lo, hi))
+    return boxes
