@@ -53,9 +53,11 @@ def parse():
     ap.add_argument("--config", type=int, default=5, help="workload 1..5 (default 5)")
     ap.add_argument("--algo", choices=["auto", "per_edge", "aggregate"], default="auto",
                     help="edge-contraction form (default: the library's automatic choice)")
-    ap.add_argument("--model", choices=["layer", "hop"], default="layer",
+    ap.add_argument("--model", choices=["layer", "hop", "infer"], default="layer",
                     help="layer: the NNConv layer stack (default); hop: the hop-loop training step "
-                         "(encoder, layer + decoder per hop, masked MSE, backward)")
+                         "(encoder, layer + decoder per hop, masked MSE, backward); infer: sub-domain "
+                         "inference (random boxes with overlap r, the layer stack forward on each, "
+                         "owned outputs reassembled)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=None,
                     help="destination rows of the oracle's timed sample (default: about 10-30 s of host work)")
@@ -121,13 +123,13 @@ def gemm_slices(n_rows):
     return max(1, min(16, 2048 // waves))
 
 
-def work_model(w, E, n_src, fused=False):
+def work_model(w, E, n_src, fused=False, n_dst=None):
     """Algorithmic work of one launch of each kernel class: flops and the
     compulsory HBM bytes (every input read once, every output written once).
     With ``fused`` (the one-pass edge gradients) the kernel-MLP pass stores z
     and the mask bits only: the backward recomputes z1."""
     d, H1, H2, de, D = w.d, w.H1, w.H2, w.de, w.D
-    n = w.n_dst
+    n = w.n_dst if n_dst is None else n_dst
     esz = 2 if w.dtype == "bf16" else 4
     kt = (H2 + 1) * d                  # length of a segment-sum row
     mask = (H1 + H2) // 8              # ReLU mask bytes per edge
@@ -316,6 +318,53 @@ class HopPipeline:
         self.st.step(self.enc, self.packed, self.dec, self.attr, self.Y, self.mask)
 
 
+class InferPipeline:
+    """Sub-domain inference on a workload: sample and gather the nodes, then
+    for every random box (overlap r) select its nodes, build its radius graph,
+    run the layer stack forward and scatter the owned outputs back."""
+
+    def __init__(self, w, lib, dm, torch):
+        from workloads import subdomain_boxes
+        self.w, self.lib, self.dm, self.torch = w, lib, dm, torch
+        self.layer = Pipeline.__new__(Pipeline)
+        Pipeline.__init__(self.layer, w, lib, dm, torch)
+        self.boxes = subdomain_boxes(w)
+        self.inf = dm.SubdomainInference(lib, self.layer.desc, self.layer.packed, w.r, w.cap, w.cap_mode)
+        self.out = torch.zeros(w.n_src, w.d, dtype=torch.float32, device=torch.device("cuda", 0))
+        self.step()
+        self.E = sum(st[2] for st in self.inf.stats)
+
+    def step(self):
+        self.layer.sample_and_gather()
+        self.inf.run(self.layer.pos, self.layer.attr, self.layer.h[0], self.boxes, self.w.r, out=self.out)
+
+
+def infer_cpu_baseline(w, E_gpu):
+    """The oracle's sub-domain inference on the smallest box of the workload,
+    extrapolated to all boxes by their share of the edges."""
+    import numpy as np
+    import oracle
+    from threadpoolctl import threadpool_info
+    from workloads import subdomain_boxes
+    pos, attr, h = [], [], []
+    for p in w.parts:
+        idx = oracle.sampling.sample_nodes(p.pos.shape[0], p.s, p.seed)
+        pos.append(p.pos[idx]); attr.append(p.attr[idx]); h.append(p.h[idx])
+    pos, attr, h = np.concatenate(pos), np.concatenate(attr), np.concatenate(h)
+    boxes = subdomain_boxes(w)
+    sizes = [oracle.infer.subdomain_nodes(pos, lo, hi, w.r)[0].size for lo, hi in boxes]
+    b = int(np.argmin(sizes))
+    t = time.perf_counter()
+    _, st = oracle.infer.infer(w.params, pos, attr, h, boxes, w.r, w.r, w.cap, w.cap_mode, w.dtype, only=[b])
+    sec = time.perf_counter() - t
+    E_b = st[b][2]
+    threads = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
+    return {"value": E_b * w.layers / sec, "unit": "edges/s", "cores": int(threads), "kind": "oracle",
+            "sample": "subset-extrapolated: the oracle's inference of the smallest of %d boxes (%d edges, %d layers, "
+                      "%.2f s); the rate carries to all boxes' %d edges" % (len(boxes), E_b, w.layers, sec, E_gpu),
+            "seconds": round(sec, 2)}
+
+
 def hop_cpu_baseline(w, E_gpu, m=1536):
     """The oracle's hop-loop step on the sub-graph of the first m sampled nodes
     (hops couple every row, so rows cannot be subsampled), extrapolated to the
@@ -406,7 +455,9 @@ def main():
     lib.dsmp_set_edge_algorithm({"auto": dm.EDGE_AUTO, "per_edge": dm.EDGE_PER_EDGE,
                                  "aggregate": dm.EDGE_AGGREGATE}[args.algo])
     hop = args.model == "hop"
-    pipe = HopPipeline(w, lib, dm, torch) if hop else Pipeline(w, lib, dm, torch)
+    infer = args.model == "infer"
+    pipe = HopPipeline(w, lib, dm, torch) if hop else InferPipeline(w, lib, dm, torch) if infer \
+        else Pipeline(w, lib, dm, torch)
     print("workload %s: n_dst=%d n_src=%d E=%d layers=%d" % (w.name, w.n_dst, w.n_src, pipe.E, w.layers),
           file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -439,7 +490,13 @@ def main():
         import dataclasses
         w = dataclasses.replace(w, de=w.D + 1)
     fused = agg and not ("dW2" in prof and prof["dW2"][1] > 0)
-    work = work_model(w, E, w.n_src, fused)
+    if infer:   # no backward ran: the forward's stores follow the shape's backward
+        fused = agg and w.dtype == "bf16" and w.H1 == w.H2 and w.H1 in (64, 128)
+    if infer:   # every box is a graph of its own: the layer runs over all their nodes
+        n_box = sum(st[1] for st in pipe.inf.stats)
+        work = work_model(w, E, n_box, fused, n_dst=n_box)
+    else:
+        work = work_model(w, E, w.n_src, fused)
     work.update(agg_work(w, E, w.n_src, fused) if agg else per_edge_work(w, E, w.n_src))
     for name, (fl, by) in prep_work_step(w, E).items():
         if name in prof and prof[name][1] > 0:
@@ -477,6 +534,9 @@ def main():
     if hop:
         METRIC_RUN = ("edges/sec of the hop-loop training step (encoder, layer + decoder per hop, masked MSE, "
                       "backward) on 1 MI355X")
+    elif infer:
+        METRIC_RUN = ("edges/sec of sub-domain inference (the layer stack forward on random boxes with overlap r, "
+                      "owned outputs reassembled) on 1 MI355X")
     else:
         METRIC_RUN = METRIC
     res = {
@@ -493,7 +553,8 @@ def main():
                                   " (plus %d halo nodes)" % (w.n_src - w.n_dst) if w.n_src > w.n_dst else "",
                                   w.r, w.cap or "none",
                                   w.d, w.de, w.H1, w.H2, w.d * w.d, L,
-                                  "hops (encoder and decoder 64 wide, difference attributes)" if hop else "layers"),
+                                  "hops (encoder and decoder 64 wide, difference attributes)" if hop else "layers")
+                   + (" (inference: %d random boxes with overlap r, forward only)" % len(pipe.boxes) if infer else ""),
                    "n_dst": w.n_dst, "n_src": w.n_src, "edges": E, "layers": L, "d": w.d, "h1": w.H1,
                    "h2": w.H2, "nominal_flops_per_edge_layer": method_flops_per_edge(w)},
         "edge_algorithm": "aggregate" if agg else "per_edge",
@@ -504,7 +565,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         rows_n = args.cpu_rows if args.cpu_rows is not None else CPU_ROWS[args.config]
-        res["cpu_baseline"] = hop_cpu_baseline(w, E) if hop else cpu_baseline(w, rows_n, E)
+        res["cpu_baseline"] = (hop_cpu_baseline(w, E) if hop else infer_cpu_baseline(w, E) if infer
+                               else cpu_baseline(w, rows_n, E))
     print(json.dumps(res), flush=True)
 
 

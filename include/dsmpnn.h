@@ -87,6 +87,41 @@ dsmp_status dsmp_sample_nodes(dsmp_handle* h, int64_t M, int64_t s, uint64_t see
 dsmp_status dsmp_gather_rows(dsmp_handle* h, const void* src, int64_t n_src_rows,
                              int64_t row_bytes, const int32_t* idx, int64_t n, void* dst);
 
+/* ------------------------------------------------------------- sub-domains
+ * Sub-domain inference (Sec. 3, Methodology, testing procedure): the domain
+ * is cut into smaller sub-domains, each with an overlap region; each is run
+ * through the trained model as a graph of its own, and the outputs of its
+ * own (interior) nodes are put back into the output over the whole domain.
+ *
+ * dsmp_subdomain_select picks the nodes of the box [lo, hi) (half-open in
+ * every axis) with overlap l:
+ *     owned   : lo[a] <= p[a] < hi[a] for every axis a
+ *     overlap : not owned, and (lo[a] - l) <= p[a] < (hi[a] + l) for every a,
+ *               the two bounds rounded to float32
+ * pos     : device float32 [n, dim]; lo, hi: host float32 [dim]; overlap >= 0.
+ * idx_out : device int32 [n] (capacity n); receives the owned nodes in
+ *           ascending order at [0, *n_owned), then the overlap nodes in
+ *           ascending order up to *n_total -- the layout the radius graph and
+ *           the layer expect (destinations first).
+ * ws      : device workspace of dsmp_subdomain_workspace(n) bytes.
+ * SYNCHRONISES the stream; *n_owned and *n_total are host int64.
+ * Errors  : INVALID_ARG for NULL pointers, n < 0 or overlap < 0;
+ *           UNSUPPORTED for dim not 2 or 3; WORKSPACE_TOO_SMALL.
+ * The kernels are timed in the DSMP_K_GATHER class. */
+dsmp_status dsmp_subdomain_workspace(int64_t n, size_t* bytes);
+dsmp_status dsmp_subdomain_select(dsmp_handle* h, const float* pos, int64_t n, int32_t dim,
+                                  const float* lo, const float* hi, float overlap,
+                                  int32_t* idx_out, void* ws, size_t ws_bytes,
+                                  int64_t* n_owned, int64_t* n_total);
+
+/* Scatter rows, the inverse of dsmp_gather_rows: dst[idx[i], :] = src[i, :]
+ * for i < n (reassembly of a sub-domain's owned outputs).  src: device
+ * [n, row_bytes]; idx: device int32 [n], distinct (two equal indices leave
+ * either row); dst: device [n_dst_rows, row_bytes].  Indices outside
+ * [0, n_dst_rows) are skipped.  row_bytes is a multiple of 4. */
+dsmp_status dsmp_scatter_rows(dsmp_handle* h, const void* src, int64_t n, int64_t row_bytes,
+                              const int32_t* idx, void* dst, int64_t n_dst_rows);
+
 /* ------------------------------------------------------------- radius graph
  * Graph kernels of Sec. 2.1: every destination i in [0, n_dst) is joined to
  * every source j in [0, n_src), j != i, within radius r; when more than `cap`

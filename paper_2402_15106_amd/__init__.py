@@ -12,3 +12,4 @@ from ._lib import (  # noqa: F401
     GRAD_ACCUMULATE, GRAD_X_ACCUMULATE, MlpDesc, EDGE_AUTO, EDGE_PER_EDGE, EDGE_AGGREGATE, OK, INVALID_ARG, CAPACITY, HIP_ERROR, UNSUPPORTED, WORKSPACE_TOO_SMALL,
 )
 from .hop import HopShapes, HopStep  # noqa: F401,E402
+from .infer import SubdomainInference  # noqa: F401,E402

@@ -30,7 +30,8 @@ GRAD_X_ACCUMULATE = 2
 EDGE_AUTO, EDGE_PER_EDGE, EDGE_AGGREGATE = 0, 1, 2
 
 EXPORTED = ["dsmp_version", "dsmp_create", "dsmp_destroy", "dsmp_set_stream", "dsmp_last_error",
-            "dsmp_sample_workspace", "dsmp_sample_nodes", "dsmp_gather_rows",
+            "dsmp_sample_workspace", "dsmp_sample_nodes", "dsmp_gather_rows", "dsmp_scatter_rows",
+            "dsmp_subdomain_workspace", "dsmp_subdomain_select",
             "dsmp_radius_graph_workspace", "dsmp_radius_graph_count", "dsmp_radius_graph_build",
             "dsmp_nnconv_packed_bytes", "dsmp_nnconv_pack", "dsmp_nnconv_workspace",
             "dsmp_nnconv_forward", "dsmp_nnconv_backward", "dsmp_profile_enable", "dsmp_profile_reset",
@@ -99,6 +100,11 @@ _SIG = {
     "dsmp_sample_nodes": (ctypes.c_int, [_P, ctypes.c_int64, ctypes.c_int64, ctypes.c_uint64, _P, _P,
                                          ctypes.c_size_t]),
     "dsmp_gather_rows": (ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.c_int64, _P, ctypes.c_int64, _P]),
+    "dsmp_scatter_rows": (ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.c_int64, _P, _P, ctypes.c_int64]),
+    "dsmp_subdomain_workspace": (ctypes.c_int, [ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]),
+    "dsmp_subdomain_select": (ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.c_int32, ctypes.POINTER(ctypes.c_float),
+                                             ctypes.POINTER(ctypes.c_float), ctypes.c_float, _P, _P, ctypes.c_size_t,
+                                             ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64)]),
     "dsmp_radius_graph_workspace": (ctypes.c_int, [ctypes.POINTER(GraphQuery), ctypes.POINTER(ctypes.c_size_t)]),
     "dsmp_radius_graph_count": (ctypes.c_int, [_P, ctypes.POINTER(GraphQuery), _P, ctypes.c_size_t,
                                                ctypes.POINTER(ctypes.c_int64)]),
@@ -259,6 +265,36 @@ class Dsmp:
         self._check(self.lib.dsmp_gather_rows(self.h, _ptr(src), src.shape[0], row_bytes, _ptr(idx), n,
                                               _ptr(out)), self.h)
         return out
+
+    def dsmp_scatter_rows(self, src: torch.Tensor, idx: torch.Tensor, out: torch.Tensor):
+        """out[idx[i]] = src[i] (the inverse of dsmp_gather_rows)."""
+        src = src.contiguous()
+        n = idx.numel()
+        row_bytes = out[0].numel() * out.element_size() if out.shape[0] > 0 else 4
+        self._bind()
+        self._check(self.lib.dsmp_scatter_rows(self.h, _ptr(src), n, row_bytes, _ptr(idx), _ptr(out),
+                                               out.shape[0]), self.h)
+        return out
+
+    # ------------------------------------------------------------ sub-domains
+    def dsmp_subdomain_select(self, pos: torch.Tensor, lo, hi, overlap: float,
+                              out: Optional[torch.Tensor] = None):
+        """Nodes of the box [lo, hi) with overlap: (idx [n_total] int32 with the
+        owned nodes first, n_owned).  Synchronises."""
+        pos = pos.contiguous()
+        n, D = pos.shape
+        out = torch.empty(max(n, 1), dtype=torch.int32, device=self.device) if out is None else out
+        nb = ctypes.c_size_t()
+        self._check(self.lib.dsmp_subdomain_workspace(n, ctypes.byref(nb)), None)
+        ws = self.workspace("subdomain", nb.value)
+        clo = (ctypes.c_float * D)(*[float(v) for v in lo])
+        chi = (ctypes.c_float * D)(*[float(v) for v in hi])
+        n_own, n_tot = ctypes.c_int64(), ctypes.c_int64()
+        self._bind()
+        self._check(self.lib.dsmp_subdomain_select(self.h, _ptr(pos), n, D, clo, chi, float(overlap), _ptr(out),
+                                                   _ptr(ws), ws.numel(), ctypes.byref(n_own),
+                                                   ctypes.byref(n_tot)), self.h)
+        return out[:n_tot.value], n_own.value
 
     # ------------------------------------------------------------ graph
     def _query(self, pos, n_dst, r, cap, cap_mode, seed):

@@ -461,3 +461,132 @@ extern "C" dsmp_status dsmp_gather_rows(dsmp_handle* h, const void* src, int64_t
   DSMP_LAUNCHED(h, "gather_rows");
   return DSMP_OK;
 }
+
+// ------------------------------------------------------------ sub-domains
+
+namespace {
+struct Box {
+  float lo[3], hi[3], elo[3], ehi[3];
+};
+
+// own[i] = 1 for nodes inside [lo, hi) in every axis; ovl[i] = 1 for the
+// other nodes inside [lo - l, hi + l) (bounds rounded to float32 on the host)
+__global__ void k_sub_flags(const float* __restrict__ pos, int64_t n, int D, Box b,
+                            uint32_t* __restrict__ own, uint32_t* __restrict__ ovl) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  bool in = true, ext = true;
+  for (int a = 0; a < D; ++a) {
+    float p = pos[i * D + a];
+    in = in && p >= b.lo[a] && p < b.hi[a];
+    ext = ext && p >= b.elo[a] && p < b.ehi[a];
+  }
+  own[i] = in ? 1u : 0u;
+  ovl[i] = (ext && !in) ? 1u : 0u;
+}
+
+// owned nodes to idx[0, n_owned), overlap nodes to idx[n_owned, n_total),
+// each in ascending order (positions from the two exclusive scans)
+__global__ void k_sub_scatter(int64_t n, const uint32_t* __restrict__ own, const uint32_t* __restrict__ ovl,
+                              const int32_t* __restrict__ own_pos, const int32_t* __restrict__ ovl_pos,
+                              int32_t* __restrict__ idx) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  if (own[i]) idx[own_pos[i]] = (int32_t)i;
+  else if (ovl[i]) idx[own_pos[n] + ovl_pos[i]] = (int32_t)i;
+}
+
+__global__ void k_scatter_rows(const uint32_t* __restrict__ src, int64_t words, const int32_t* __restrict__ idx,
+                               int64_t n, uint32_t* __restrict__ dst, int64_t n_dst_rows) {
+  int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t total = n * words;
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (; t < total; t += stride) {
+    int64_t r = t / words, w = t - r * words;
+    int32_t d = idx[r];
+    if (d >= 0 && d < n_dst_rows) dst[(int64_t)d * words + w] = src[t];
+  }
+}
+
+struct SubWs {
+  uint32_t *own, *ovl, *tmp;
+  int32_t *own_pos, *ovl_pos;
+};
+
+SubWs carve_sub(void* ws, int64_t n, size_t* used) {
+  Carve c(ws);
+  SubWs w;
+  w.own = c.take<uint32_t>(n + 1);
+  w.ovl = c.take<uint32_t>(n + 1);
+  w.own_pos = c.take<int32_t>(n + 1);
+  w.ovl_pos = c.take<int32_t>(n + 1);
+  w.tmp = c.take<uint32_t>(scan_tmp_elems(n));
+  *used = c.used();
+  return w;
+}
+}  // namespace
+
+extern "C" dsmp_status dsmp_subdomain_workspace(int64_t n, size_t* bytes) {
+  if (!bytes || n < 0) return DSMP_INVALID_ARG;
+  carve_sub(nullptr, n, bytes);
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_subdomain_select(dsmp_handle* h, const float* pos, int64_t n, int32_t dim,
+                                             const float* lo, const float* hi, float overlap,
+                                             int32_t* idx_out, void* ws, size_t ws_bytes,
+                                             int64_t* n_owned, int64_t* n_total) {
+  if (!h) return DSMP_INVALID_ARG;
+  DSMP_CHECK(h, n >= 0 && n <= INT32_MAX, n < 0 ? DSMP_INVALID_ARG : DSMP_UNSUPPORTED, "bad node count");
+  DSMP_CHECK(h, dim == 2 || dim == 3, DSMP_UNSUPPORTED, "dim must be 2 or 3");
+  DSMP_CHECK(h, lo && hi && n_owned && n_total, DSMP_INVALID_ARG, "sub-domain pointer is NULL");
+  DSMP_CHECK(h, overlap >= 0.0f, DSMP_INVALID_ARG, "overlap must be >= 0");
+  *n_owned = 0;
+  *n_total = 0;
+  if (n == 0) return DSMP_OK;
+  DSMP_CHECK(h, pos && idx_out && ws, DSMP_INVALID_ARG, "sub-domain pointer is NULL");
+  size_t need;
+  SubWs w = carve_sub(ws, n, &need);
+  DSMP_CHECK(h, ws_bytes >= need, DSMP_WORKSPACE_TOO_SMALL, "sub-domain workspace %zu < %zu", ws_bytes, need);
+  Box b{};
+  for (int a = 0; a < dim; ++a) {
+    b.lo[a] = lo[a];
+    b.hi[a] = hi[a];
+    b.elo[a] = lo[a] - overlap;   // float32 rounding, as the bounds are defined
+    b.ehi[a] = hi[a] + overlap;
+  }
+  ProfScope prof(h, DSMP_K_GATHER);
+  hipStream_t s = h->stream;
+  hipLaunchKernelGGL(k_sub_flags, dim3(ceil_div(n, 256)), dim3(256), 0, s, pos, n, (int)dim, b, w.own, w.ovl);
+  DSMP_LAUNCHED(h, "sub-domain flags");
+  dsmp_status st;
+  if ((st = exclusive_scan_u32(h, w.own, w.own_pos, n, w.tmp)) != DSMP_OK) return st;
+  if ((st = exclusive_scan_u32(h, w.ovl, w.ovl_pos, n, w.tmp)) != DSMP_OK) return st;
+  hipLaunchKernelGGL(k_sub_scatter, dim3(ceil_div(n, 256)), dim3(256), 0, s, n, w.own, w.ovl, w.own_pos,
+                     w.ovl_pos, idx_out);
+  DSMP_LAUNCHED(h, "sub-domain scatter");
+  int32_t tot[2];
+  DSMP_HIP(h, hipMemcpyAsync(&tot[0], w.own_pos + n, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  DSMP_HIP(h, hipMemcpyAsync(&tot[1], w.ovl_pos + n, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  DSMP_HIP(h, hipStreamSynchronize(s));
+  *n_owned = tot[0];
+  *n_total = (int64_t)tot[0] + tot[1];
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_scatter_rows(dsmp_handle* h, const void* src, int64_t n, int64_t row_bytes,
+                                         const int32_t* idx, void* dst, int64_t n_dst_rows) {
+  if (!h) return DSMP_INVALID_ARG;
+  DSMP_CHECK(h, n >= 0 && n_dst_rows >= 0 && row_bytes > 0 && row_bytes % 4 == 0, DSMP_INVALID_ARG,
+             "bad scatter sizes");
+  if (n == 0) return DSMP_OK;
+  DSMP_CHECK(h, src && idx && dst, DSMP_INVALID_ARG, "scatter pointer is NULL");
+  ProfScope prof(h, DSMP_K_GATHER);
+  int64_t words = row_bytes / 4;
+  unsigned g = ceil_div(n * words, 256);
+  if (g > 8192) g = 8192;
+  hipLaunchKernelGGL(k_scatter_rows, dim3(g), dim3(256), 0, h->stream, static_cast<const uint32_t*>(src), words,
+                     idx, n, static_cast<uint32_t*>(dst), n_dst_rows);
+  DSMP_LAUNCHED(h, "scatter_rows");
+  return DSMP_OK;
+}
