@@ -79,6 +79,19 @@ dsmp_status dsmp_sample_workspace(int64_t M, size_t* bytes);
 dsmp_status dsmp_sample_nodes(dsmp_handle* h, int64_t M, int64_t s, uint64_t seed,
                               int32_t* idx_out, void* ws, size_t ws_bytes);
 
+/* Allocation-free variant of dsmp_sample_nodes, for callers that cannot
+ * allocate or pass workspace (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation).  Same arguments and result,
+ * without ws: the selection runs on a scratch array the library holds in
+ * device memory, one per GPU for the life of the process (328 KB), sized for
+ * at most 16,777,216 candidates; M beyond that gives UNSUPPORTED before
+ * anything is enqueued.  Calls no allocating routine.  Every call on a GPU
+ * uses that GPU's one array (its state and histogram are cleared by a kernel
+ * at the start of each call), so calls that overlap on one GPU -- on two
+ * streams, or from two threads -- race; serialise them. */
+dsmp_status dsmp_sample_nodes_noalloc(dsmp_handle* h, int64_t M, int64_t s, uint64_t seed,
+                                      int32_t* idx_out);
+
 /* Gather rows: dst[i, :] = src[idx[i], :] for i < n.  Rows are row_bytes long
  * (a multiple of 4).  src: device [n_src_rows, row_bytes]; idx: device
  * int32 [n]; dst: device [n, row_bytes].  Indices out of [0, n_src_rows)

@@ -30,7 +30,8 @@ GRAD_X_ACCUMULATE = 2
 EDGE_AUTO, EDGE_PER_EDGE, EDGE_AGGREGATE = 0, 1, 2
 
 EXPORTED = ["dsmp_version", "dsmp_create", "dsmp_destroy", "dsmp_set_stream", "dsmp_last_error",
-            "dsmp_sample_workspace", "dsmp_sample_nodes", "dsmp_gather_rows", "dsmp_scatter_rows",
+            "dsmp_sample_workspace", "dsmp_sample_nodes", "dsmp_sample_nodes_noalloc", "dsmp_gather_rows",
+            "dsmp_scatter_rows",
             "dsmp_subdomain_workspace", "dsmp_subdomain_select",
             "dsmp_radius_graph_workspace", "dsmp_radius_graph_count", "dsmp_radius_graph_build",
             "dsmp_nnconv_packed_bytes", "dsmp_nnconv_pack", "dsmp_nnconv_workspace",
@@ -99,6 +100,7 @@ _SIG = {
     "dsmp_sample_workspace": (ctypes.c_int, [ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]),
     "dsmp_sample_nodes": (ctypes.c_int, [_P, ctypes.c_int64, ctypes.c_int64, ctypes.c_uint64, _P, _P,
                                          ctypes.c_size_t]),
+    "dsmp_sample_nodes_noalloc": (ctypes.c_int, [_P, ctypes.c_int64, ctypes.c_int64, ctypes.c_uint64, _P]),
     "dsmp_gather_rows": (ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.c_int64, _P, ctypes.c_int64, _P]),
     "dsmp_scatter_rows": (ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.c_int64, _P, _P, ctypes.c_int64]),
     "dsmp_subdomain_workspace": (ctypes.c_int, [ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]),
@@ -254,6 +256,13 @@ class Dsmp:
         self._bind()
         self._check(self.lib.dsmp_sample_nodes(self.h, M, s, ctypes.c_uint64(seed & (2 ** 64 - 1)),
                                                _ptr(out), _ptr(ws), ws.numel()), self.h)
+        return out
+
+    def dsmp_sample_nodes_noalloc(self, M: int, s: int, seed: int, out: torch.Tensor):
+        """dsmp_sample_nodes on the library's own scratch (no workspace); out
+        is the caller's int32 [s] device buffer."""
+        self._bind()
+        self._check(self.lib.dsmp_sample_nodes_noalloc(self.h, M, s, seed & (2 ** 64 - 1), _ptr(out)), self.h)
         return out
 
     def dsmp_gather_rows(self, src: torch.Tensor, idx: torch.Tensor, out: Optional[torch.Tensor] = None):

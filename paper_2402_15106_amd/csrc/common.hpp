@@ -17,6 +17,7 @@ struct dsmp_handle {
   hipStream_t stream = nullptr;
   int edge_algo = 0;   // DSMP_EDGE_AUTO / PER_EDGE / AGGREGATE
   int n_cu = 256;      // compute units of the device (sizes persistent grids)
+  void* sample_scratch = nullptr;   // device address of the allocation-free sampling scratch
   std::string err;
   // kernel timing (opt-in)
   struct Mark {

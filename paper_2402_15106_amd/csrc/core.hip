@@ -1,6 +1,8 @@
 // Handle management, scan and fill utilities, node sampling and row gather.
 #include "common.hpp"
 
+#include <map>
+#include <mutex>
 #include <new>
 
 using namespace dsmp;
@@ -150,6 +152,10 @@ dsmp_status fill_u32(dsmp_handle* h, uint32_t* p, int64_t n, uint32_t v, uint32_
 
 extern "C" int dsmp_version(void) { return 10000; }
 
+// device address of the sampling scratch array on the current device (set-up
+// of the allocation-free sampling entry point; defined with the array below)
+static dsmp_status sample_scratch_setup(dsmp_handle* h);
+
 extern "C" dsmp_status dsmp_create(dsmp_handle** out, int device) {
   if (!out) return DSMP_INVALID_ARG;
   *out = nullptr;
@@ -161,6 +167,11 @@ extern "C" dsmp_status dsmp_create(dsmp_handle** out, int device) {
   h->device = device;
   int cu = 0;
   if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, device) == hipSuccess && cu > 0) h->n_cu = cu;
+  const dsmp_status st = sample_scratch_setup(h);
+  if (st != DSMP_OK) {
+    delete h;
+    return st;
+  }
   *out = h;
   return DSMP_OK;
 }
@@ -393,27 +404,21 @@ extern "C" dsmp_status dsmp_sample_workspace(int64_t M, size_t* bytes) {
   return DSMP_OK;
 }
 
-extern "C" dsmp_status dsmp_sample_nodes(dsmp_handle* h, int64_t M, int64_t s, uint64_t seed,
-                                         int32_t* idx_out, void* ws, size_t ws_bytes) {
-  if (!h) return DSMP_INVALID_ARG;
-  DSMP_CHECK(h, M >= 0 && s >= 0 && s <= M, DSMP_INVALID_ARG, "need 0 <= s <= M (M=%lld s=%lld)",
-             (long long)M, (long long)s);
-  DSMP_CHECK(h, M <= INT32_MAX, DSMP_UNSUPPORTED, "M exceeds int32 range");
-  if (s == 0) return DSMP_OK;
-  DSMP_CHECK(h, idx_out != nullptr, DSMP_INVALID_ARG, "idx_out is NULL");
+namespace {
+// The selection on a workspace of at least sample_ws(M) bytes (checked by the callers).
+dsmp_status sample_run(dsmp_handle* h, int64_t M, int64_t s, uint64_t seed, int32_t* idx_out, void* ws) {
   ProfScope prof(h, DSMP_K_SAMPLE);
   if (s == M) {
     hipLaunchKernelGGL(k_iota, dim3(ceil_div(M, 256)), dim3(256), 0, h->stream, idx_out, M);
     DSMP_LAUNCHED(h, "iota");
     return DSMP_OK;
   }
-  DSMP_CHECK(h, ws != nullptr && ws_bytes >= sample_ws(M), DSMP_WORKSPACE_TOO_SMALL,
-             "sampling workspace needs %zu bytes", sample_ws(M));
   Carve c(ws);
   SelState* st = c.take<SelState>(1);
   uint32_t* hist = c.take<uint32_t>(SEL_BINS);
   int nb = (int)ceil_div(M, SAMPLE_CHUNK);
   uint32_t* cnt = c.take<uint32_t>(nb + 2);
+  // the state and the histogram are cleared by a kernel on every call
   hipLaunchKernelGGL(k_sel_init, dim3(SEL_BINS / 4 / 1024), dim3(1024), 0, h->stream, st, (uint64_t)s, hist);
   unsigned g = ceil_div(M, 256);
   if (g > 2048) g = 2048;
@@ -426,6 +431,66 @@ extern "C" dsmp_status dsmp_sample_nodes(dsmp_handle* h, int64_t M, int64_t s, u
   hipLaunchKernelGGL(k_sel_write, dim3(nb), dim3(1024), 0, h->stream, M, seed, st, cnt, idx_out);
   DSMP_LAUNCHED(h, "sample");
   return DSMP_OK;
+}
+
+dsmp_status sample_check(dsmp_handle* h, int64_t M, int64_t s, const int32_t* idx_out) {
+  DSMP_CHECK(h, M >= 0 && s >= 0 && s <= M, DSMP_INVALID_ARG, "need 0 <= s <= M (M=%lld s=%lld)",
+             (long long)M, (long long)s);
+  DSMP_CHECK(h, M <= INT32_MAX, DSMP_UNSUPPORTED, "M exceeds int32 range");
+  DSMP_CHECK(h, s == 0 || idx_out != nullptr, DSMP_INVALID_ARG, "idx_out is NULL");
+  return DSMP_OK;
+}
+
+// Allocation-free sampling: the workspace is a file-scope device array of a
+// fixed size, enough for SAMPLE_NOALLOC_MAX_M candidates.  Host code never
+// passes the array's name to a kernel: the device address comes from
+// hipGetSymbolAddress, taken once per device at handle creation.
+constexpr int64_t SAMPLE_NOALLOC_MAX_M = 1ll << 24;
+constexpr size_t round256(size_t b) { return (b + 255) & ~size_t(255); }
+constexpr size_t SAMPLE_SCRATCH_BYTES = round256(sizeof(SelState)) + round256(sizeof(uint32_t) * SEL_BINS) +
+                                        round256(sizeof(uint32_t) * ((SAMPLE_NOALLOC_MAX_M + SAMPLE_CHUNK - 1) /
+                                                                     SAMPLE_CHUNK + 2));
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[SAMPLE_SCRATCH_BYTES];
+
+static dsmp_status sample_scratch_setup(dsmp_handle* h) {
+  static std::mutex mu;
+  static std::map<int, void*> addr;   // device -> address of its copy of the array
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = addr.find(h->device);
+  if (it == addr.end()) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || ptr == nullptr)
+      return fail(h, DSMP_HIP_ERROR, "hipGetSymbolAddress of the sampling scratch failed: %s", hipGetErrorString(e));
+    it = addr.emplace(h->device, ptr).first;
+  }
+  h->sample_scratch = it->second;
+  return DSMP_OK;
+}
+
+extern "C" dsmp_status dsmp_sample_nodes(dsmp_handle* h, int64_t M, int64_t s, uint64_t seed,
+                                         int32_t* idx_out, void* ws, size_t ws_bytes) {
+  if (!h) return DSMP_INVALID_ARG;
+  dsmp_status st = sample_check(h, M, s, idx_out);
+  if (st != DSMP_OK || s == 0) return st;
+  DSMP_CHECK(h, s == M || (ws != nullptr && ws_bytes >= sample_ws(M)), DSMP_WORKSPACE_TOO_SMALL,
+             "sampling workspace needs %zu bytes", sample_ws(M));
+  return sample_run(h, M, s, seed, idx_out, ws);
+}
+
+extern "C" dsmp_status dsmp_sample_nodes_noalloc(dsmp_handle* h, int64_t M, int64_t s, uint64_t seed,
+                                                 int32_t* idx_out) {
+  if (!h) return DSMP_INVALID_ARG;
+  dsmp_status st = sample_check(h, M, s, idx_out);
+  if (st != DSMP_OK || s == 0) return st;
+  DSMP_CHECK(h, M <= SAMPLE_NOALLOC_MAX_M, DSMP_UNSUPPORTED,
+             "allocation-free sampling takes at most %lld candidates (M=%lld)", (long long)SAMPLE_NOALLOC_MAX_M,
+             (long long)M);
+  DSMP_CHECK(h, h->sample_scratch != nullptr, DSMP_HIP_ERROR, "sampling scratch address not set up");
+  DSMP_CHECK(h, sample_ws(M) <= SAMPLE_SCRATCH_BYTES, DSMP_UNSUPPORTED, "sampling scratch too small");
+  return sample_run(h, M, s, seed, idx_out, h->sample_scratch);
 }
 
 // ------------------------------------------------------------------ gather
