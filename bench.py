@@ -73,7 +73,7 @@ SRC_AGG = ["nnconv_agg.hip", "nnconv.hpp", "common.hpp"]
 KERNEL_SOURCES = {
     "sample": SRC_CORE, "gather": SRC_CORE, "graph": SRC_GRAPH,
     "edge_fwd": SRC_FWD, "edge_dh": SRC_FWD, "edge_mlp": SRC_FWD,
-    "dz": SRC_BWD, "u_gemm": SRC_BWD, "dW2": SRC_BWD, "dW1": SRC_BWD,
+    "dz": SRC_BWD, "u_gemm": SRC_BWD, "dW2": SRC_BWD, "dW1": SRC_BWD, "dh_u": SRC_BWD, "dh_final": SRC_BWD,
     "dW3": SRC_BWD + ["nnconv_agg.hip"],
     "outer_fwd": SRC_AGG, "gemm_fwd": SRC_AGG, "outer_dh": SRC_AGG, "gemm_dh": SRC_AGG,
 }
@@ -168,10 +168,16 @@ def agg_work(w, E, n_src, fused=False):
               n * H2 * d * esz + E * (4 + d * esz + mask + 2 * (D + 1) * 4))
     else:
         dz = (2 * E * (d * H2 + H1 * H2), n * H2 * d * esz + E * (4 + d * esz + mask + (H1 + H2) * esz))
-    return {
+    out = {
         "dz": dz,
         "dW3": (2 * n * kt * d, n * kt * esz + n * d * esz),
     }
+    if w.dtype == "bf16":
+        # the feature gradient from U: per-edge terms from U_i, z_e and the bias
+        # row, then their sums over the edges leaving each source
+        out["dh_u"] = (2 * E * H2 * d + 2 * n * d * d, n * H2 * d * esz + E * (H2 * esz + d * esz) + n * (d * esz + 4))
+        out["dh_final"] = (0, E * (d * esz + 4) + n_src * (d * 4 + 4) + n * d * 4)
+    return out
 
 
 def prep_work_step(w, E):

@@ -396,7 +396,8 @@ enum {
   DSMP_K_ATTR = 19,     /* edge-attribute gradient of a layer (dattr) */
   DSMP_K_MLP = 20,      /* encoder / decoder perceptrons, forward and backward */
   DSMP_K_LOSS = 21,     /* masked mean squared error */
-  DSMP_K_COUNT = 22
+  DSMP_K_DH_U = 22,     /* per-edge feature-gradient terms from U (aggregate form, bf16) */
+  DSMP_K_COUNT = 23
 };
 dsmp_status dsmp_profile_enable(dsmp_handle* h, int enable);
 dsmp_status dsmp_profile_reset(dsmp_handle* h);

@@ -1785,11 +1785,220 @@ __global__ void k_bwd_dh_final(int64_t n_src, int64_t n_dst, int DL, const int32
 }
 
 
+// ------------------------------------------------------------ feature gradient from U
+// The feature gradient of the aggregate form (bf16) without per-source sums:
+// for the edge e = (i <- j),
+//   sum_q Theta_e[p][q] g_i[q] = sum_k z~_e[k] U~_i[k][p],
+// U~_i[k][p] = sum_q W3~[p*d+q][k] g_i[q] -- the same U_i the dz pass reads,
+// plus the bias row k = h2, sum_q b3[p*d+q] g_i[q].  k_dh_u forms these
+// per-edge terms m_e[p] for every edge of a destination, U_i staged once in
+// LDS (rows in the stored order of z, so the z rows load as they are);
+// k_dh_gather then sums them over the edges leaving each source, in edge
+// order, and adds the node terms.
+struct DhuArgs {
+  int64_t n_dst;
+  const int32_t* row_ptr;
+  const unsigned char* U;     // [n_dst][h2*d] bf16, each row in MFMA fragment order
+  const unsigned char* gT;    // [n_dst][d] bf16
+  const unsigned char* b3n;   // [d][d] bf16, b3[p*d + q]
+  const unsigned char* zE;    // [E][h2] bf16, stored positions
+  unsigned char* mE;          // [E][d] bf16 out
+};
+
+template <int DL, int H2>
+struct DhuShape {
+  static constexpr int UB = H2 * DL * 2;   // bytes of one U_i (bf16, MFMA fragment order)
+  static constexpr int LDS = 2 * UB;       // two destinations' U_i: one in use, the next one arriving
+  static_assert(UB % (256 * 16) == 0, "U_i is whole rounds of 256 16-byte units");
+};
+
+// U row R of a 32-row tile holds the neuron of z position swap(R): the dz
+// pass's accumulator row 8(i/4) + 4h + i%4 is stored at 16(i/8) + 8h + i%8,
+// which exchanges bits 2 and 3 of the row within its tile.
+__device__ __forceinline__ int swap_bits23(int r) { return (r & ~12) | ((r >> 2) & 1) << 3 | ((r >> 3) & 1) << 2; }
+
+// Byte offset of U_i[R][p .. p+3] (p a multiple of 4) in the fragment order
+// of the U GEMM: fragment (kt, s) = 64 lanes x 8 elements, lane r + 32 h
+// holding row 32 kt + r, columns 16 s + 8 h .. + 7.
+template <int DL>
+__device__ __forceinline__ int u_offset(int R, int p) {
+  constexpr int SKD = DL / 16;
+  return ((((R >> 5) * SKD + (p >> 4)) * 64 + (R & 31) + 32 * ((p >> 3) & 1)) * 8 + (p & 7)) * 2;
+}
+
+// A operand of m_e = U_i^T z~_e: lane (n = l%32, h = l/32) receives
+// U_i[R(P)][c0 + n] for P = P0 + 8h + t, t < 8, with R(P) the U row of z
+// position P -- two transposing LDS reads whose lanes name their own rows in
+// the fragment-order copy of U_i (see lds_frag_rows for the lane pattern).
+template <int DL>
+__device__ __forceinline__ bf16x8 lds_frag_ut(const unsigned char* X, int P0, int c0) {
+  const int l = threadIdx.x & 63, g = l >> 4, j = (l >> 2) & 3, q = l & 3;
+  const int Plo = P0 + 8 * (g >> 1) + j, Phi = Plo + 4, p = c0 + 16 * (g & 1) + 4 * q;
+  const int Rlo = (Plo & ~31) | swap_bits23(Plo & 31), Rhi = (Phi & ~31) | swap_bits23(Phi & 31);
+  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(X + u_offset<DL>(Rlo, p)));
+  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(X + u_offset<DL>(Rhi, p)));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// Persistent workgroups walk destinations i = blockIdx.x, + gridDim.x, ...:
+// U_i is copied to LDS as it stands (direct global-to-LDS loads).  Each wave
+// takes (32-row column tile pt of p, 32-edge tile) items of a destination;
+// pt is the same for every item of a wave (4 waves, PT divides 4), so the
+// bias fragments of b3 are loaded once.  While destination i is multiplied,
+// the next destination's U and the operands of the wave's first item of it
+// (its z rows and g) are already on their way, so the loop waits on one
+// round of loads per destination.
+template <int DL, int H2>
+__global__ __launch_bounds__(256) void k_dh_u(DhuArgs a) {
+  using S = DhuShape<DL, H2>;
+  using M = MT<__bf16>;
+  constexpr int SKD = DL / 16, SK2 = H2 / 16, PT = DL / 32, NU = S::UB / 16, EPW = 4 / PT;
+  static_assert(4 % PT == 0, "column tiles divide the waves");
+  extern __shared__ __align__(16) unsigned char X[];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int pt = wv % PT, et0 = wv / PT;   // the wave's column tile and first edge tile
+  bf16x8 ba[SKD];
+#pragma unroll
+  for (int sf = 0; sf < SKD; ++sf)
+    ba[sf] = ld_frag<__bf16>(a.b3n + ((size_t)(32 * pt + l32) * DL + 16 * sf + 8 * hh) * 2);
+  // operands of the wave's first item of destination i: z rows of edge tile et0, and g_i
+  auto load_ops = [&](int64_t i, int64_t pa, int64_t pb, bf16x8 (&zb)[SK2], bf16x8 (&gb)[SKD]) {
+    const int64_t e = pa + (int64_t)et0 * 32 + l32;
+    const bool valid = e < pb;
+    const unsigned char* zr = a.zE + (size_t)(valid ? e : 0) * H2 * 2;
+#pragma unroll
+    for (int s2 = 0; s2 < SK2; ++s2) zb[s2] = valid ? ld_frag<__bf16>(zr + (16 * s2 + 8 * hh) * 2) : bf16x8{};
+#pragma unroll
+    for (int sf = 0; sf < SKD; ++sf) gb[sf] = ld_frag<__bf16>(a.gT + ((size_t)i * DL + 16 * sf + 8 * hh) * 2);
+  };
+  auto item = [&](const unsigned char* Xb, int64_t pa, int64_t pb, int et, const bf16x8 (&zb)[SK2],
+                  const bf16x8 (&gb)[SKD]) {
+    const int64_t e = pa + (int64_t)et * 32 + l32;
+    f32x16 acc = f32x16{};
+    // bias row: sum_q b3[p*d+q] g_i[q], the same for every edge column
+#pragma unroll
+    for (int sf = 0; sf < SKD; ++sf) acc = M::mma(ba[sf], gb[sf], acc);
+#pragma unroll
+    for (int s2 = 0; s2 < SK2; ++s2) acc = M::mma(lds_frag_ut<DL>(Xb, 16 * s2, 32 * pt), zb[s2], acc);
+    if (e < pb) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const bf16x2 lo = __builtin_convertvector((f32x2){acc[4 * g], acc[4 * g + 1]}, bf16x2);
+        const bf16x2 hi = __builtin_convertvector((f32x2){acc[4 * g + 2], acc[4 * g + 3]}, bf16x2);
+        *reinterpret_cast<uint2*>(a.mE + ((size_t)e * DL + 32 * pt + 8 * g + 4 * hh) * 2) =
+            make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+      }
+    }
+  };
+  int64_t i = blockIdx.x;
+  if (i >= a.n_dst) return;
+  int64_t pa = a.row_ptr[i], pb = a.row_ptr[i + 1];
+  bf16x8 zb[SK2], gb[SKD];
+  lds_copy_async(a.U + (size_t)i * S::UB, X, NU);
+  load_ops(i, pa, pb, zb, gb);
+  for (int buf = 0; i < a.n_dst; i += gridDim.x, buf ^= 1) {
+    stage_wait();
+    __syncthreads();   // U_i is in X[buf]; every wave is done with X[buf ^ 1]
+    const unsigned char* Xb = X + buf * S::UB;
+    const int64_t inext = i + gridDim.x;
+    int64_t pa2 = 0, pb2 = 0;
+    bf16x8 zn[SK2], gn[SKD];
+    if (inext < a.n_dst) {
+      lds_copy_async(a.U + (size_t)inext * S::UB, X + (buf ^ 1) * S::UB, NU);
+      pa2 = a.row_ptr[inext];
+      pb2 = a.row_ptr[inext + 1];
+      load_ops(inext, pa2, pb2, zn, gn);
+    }
+    const int net = (int)((pb - pa + 31) / 32);
+    if (et0 < net) item(Xb, pa, pb, et0, zb, gb);
+    for (int et = et0 + EPW; et < net; et += EPW) {   // destinations of more than 4 / PT edge tiles
+      bf16x8 zx[SK2];
+      const int64_t e = pa + (int64_t)et * 32 + l32;
+      const unsigned char* zr = a.zE + (size_t)(e < pb ? e : 0) * H2 * 2;
+#pragma unroll
+      for (int s2 = 0; s2 < SK2; ++s2) zx[s2] = e < pb ? ld_frag<__bf16>(zr + (16 * s2 + 8 * hh) * 2) : bf16x8{};
+      item(Xb, pa, pb, et, zx, gb);
+    }
+#pragma unroll
+    for (int s2 = 0; s2 < SK2; ++s2) zb[s2] = zn[s2];
+#pragma unroll
+    for (int sf = 0; sf < SKD; ++sf) gb[sf] = gn[sf];
+    pa = pa2;
+    pb = pb2;
+  }
+}
+
+// grad_h[j] = sum over the edges leaving j (edge order) of m_e, plus the root
+// and residual terms when j is a destination; two channels per thread (a
+// wave covers one source at d = 128).  The edge ids and rows of eight edges
+// are loaded before they are added (in edge order).
+__global__ void k_dh_gather(int64_t n_src, int64_t n_dst, int DL, const int32_t* __restrict__ csc_ptr,
+                            const int32_t* __restrict__ csc_eid, const unsigned char* __restrict__ mE,
+                            const float* __restrict__ dh_node, float* __restrict__ grad_h) {
+  const int hw = DL / 2;
+  const int64_t total = n_src * hw;
+  for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < total; x += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t j = x / hw;
+    const int c = 2 * (int)(x % hw);
+    float s0 = 0.0f, s1 = 0.0f;
+    const int t0 = csc_ptr[j], t1 = csc_ptr[j + 1];
+    float node0 = 0.0f, node1 = 0.0f;
+    if (j < n_dst) {
+      node0 = dh_node[j * DL + c];
+      node1 = dh_node[j * DL + c + 1];
+    }
+    for (int t = t0; t < t1; t += 8) {
+      int32_t id[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) id[u] = t + u < t1 ? csc_eid[t + u] : -1;
+      bf16x2 m[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        m[u] = id[u] >= 0 ? *reinterpret_cast<const bf16x2*>(mE + ((size_t)id[u] * DL + c) * 2) : bf16x2{};
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        s0 += (float)m[u][0];
+        s1 += (float)m[u][1];
+      }
+    }
+    *reinterpret_cast<f32x2*>(grad_h + j * DL + c) = f32x2{s0 + node0, s1 + node1};
+  }
+}
+
+template <int DL, int H2>
+dsmp_status launch_dh_u(dsmp_handle* h, const DhuArgs& a) {
+  using S = DhuShape<DL, H2>;
+  auto k = k_dh_u<DL, H2>;
+  DSMP_HIP(h, hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  S::LDS));
+  int per_cu = 0;
+  DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, 256, S::LDS));
+  const int64_t grid = std::min<int64_t>(a.n_dst, (int64_t)h->n_cu * std::max(per_cu, 1));
+  if (grid == 0) return DSMP_OK;
+  hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(256), S::LDS, h->stream, a);
+  DSMP_LAUNCHED(h, "feature gradient from U");
+  return DSMP_OK;
+}
+
+dsmp_status dispatch_dh_u(dsmp_handle* h, const dsmp_layer_desc& d, const DhuArgs& a) {
+  if (d.d == 32 && d.h2 == 64) return launch_dh_u<32, 64>(h, a);
+  if (d.d == 32 && d.h2 == 128) return launch_dh_u<32, 128>(h, a);
+  if (d.d == 64 && d.h2 == 64) return launch_dh_u<64, 64>(h, a);
+  if (d.d == 64 && d.h2 == 128) return launch_dh_u<64, 128>(h, a);
+  if (d.d == 128 && d.h2 == 256) return launch_dh_u<128, 256>(h, a);
+  return fail(h, DSMP_UNSUPPORTED, "unsupported layer shape for the feature gradient from U");
+}
+
+// The feature gradient comes from U (and no per-source sums are formed) for
+// bf16 layers of the aggregate form.
+bool dh_from_u(const dsmp_layer_desc& d, bool agg) { return agg && d.dtype == DSMP_BF16; }
+
+
 // ------------------------------------------------------------ workspace
 
 struct BwdWs {
   float *gF, *dh_node, *dh_direct, *dh_part, *dh_sl;
-  unsigned char *gT, *da2E, *da1E, *ot, *U;
+  unsigned char *gT, *da2E, *da1E, *ot, *U, *mE;
   float4* dx;                  // [E] edge-attribute gradients (diff attributes)
   int nslh;
   float *p_root, *p_db3, *p_w3, *p_w2, *p_w1;
@@ -1831,6 +2040,7 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   w.nslh = agg_gemm_slices(n_src, d);
   w.dh_sl = c.take<float>((size_t)w.nslh * n_src * d.d);
   w.U = c.take<unsigned char>((size_t)n_dst * d.h2 * d.d * esz);
+  w.mE = c.take<unsigned char>((size_t)E * d.d * esz);   // per-edge feature-gradient terms (from U)
   w.da2E = c.take<unsigned char>((size_t)E * d.h2 * esz);
   w.da1E = c.take<unsigned char>((size_t)E * d.h1 * esz);
   w.dx = c.take<float4>((size_t)E);
@@ -2075,7 +2285,10 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   ea.zE = const_cast<unsigned char*>(sv + sl.zE);
   ea.z1E = nullptr;
   ea.out_direct = w.dh_direct; ea.out_part = w.dh_part;
-  if (agg) {
+  const bool dhu = dh_from_u(d, agg);
+  if (dhu) {
+    // after the kernel-MLP gradients, from U (below)
+  } else if (agg) {
     // per-source sums T_j = sum_e [z_e; 1] (x) g_e, then one GEMM with W3~
     {
       ProfScope prof(h, DSMP_K_OUTER_DH);
@@ -2090,7 +2303,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   } else {
     if ((st = launch_edge_contract(h, d, MODE_DH, ea)) != DSMP_OK) return st;
   }
-  if (n_src > 0) {
+  if (n_src > 0 && !dhu) {
     unsigned grid = ceil_div(n_src * d.d, 256);
     if (grid > 4096) grid = 4096;
     ProfScope prof(h, DSMP_K_DH_FINAL);
@@ -2130,6 +2343,22 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
       st = launch_dw1_tr<256>(h, n1, E, w.pc1, w.da1E, sv + sl.xE, de, w.p_w1);
     if (st != DSMP_OK) return st;
     DSMP_LAUNCHED(h, "dW1");
+  }
+
+  if (dhu) {
+    if (E > 0) {
+      ProfScope prof(h, DSMP_K_DH_U);
+      DhuArgs da{n_dst, g->row_ptr, w.U, w.gT, pk + L.b3n, sv + sl.zE, w.mE};
+      if ((st = dispatch_dh_u(h, d, da)) != DSMP_OK) return st;
+    }
+    if (n_src > 0) {
+      unsigned grid = ceil_div(n_src * d.d / 2, 256);
+      if (grid > 4096) grid = 4096;
+      ProfScope prof(h, DSMP_K_DH_FINAL);
+      hipLaunchKernelGGL(k_dh_gather, dim3(grid), dim3(256), 0, s, n_src, n_dst, d.d, g->csc_ptr, g->csc_eid, w.mE,
+                         w.dh_node, grad_h);
+      DSMP_LAUNCHED(h, "grad_h from the edge terms");
+    }
   }
 
   if (grads->dattr && n_src > 0) {
