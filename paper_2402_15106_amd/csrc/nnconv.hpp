@@ -203,6 +203,12 @@ __device__ __forceinline__ bf16x8 lds_frag_rows(const unsigned char* X, int pitc
 // Wait for this thread's outstanding global loads, the LDS stages included.
 __device__ __forceinline__ void stage_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// s_waitcnt immediate that waits until at most N vector memory operations of
+// this thread are outstanding (N < 64; expcnt and lgkmcnt not waited for).
+// Operations retire in issue order, so every one issued before the N youngest
+// has completed.
+constexpr int vmcnt_imm(int N) { return (N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+
 // Edge attributes of edge (i <- j) from the node attribute rows v_i, v_j
 // (dim + 1 values each): concat [p_i, p_j, s_i, s_j] or diff v_i - v_j,
 // zero-padded to 8 (Sec. 2.1).

@@ -1005,12 +1005,17 @@ __global__ __launch_bounds__(256) void k_u_gemm(UArgs a, int64_t rows_per_wg) {
 #pragma unroll
     for (int s = 0; s < SKD; ++s)
       A[m][s] = ld_frag<T>(a.W + ((size_t)(cb0 + (wv * US::TPW + m) * 32 + l32) * DL + s * KS + hh * EPL) * ESZ);
-  int buf = 0;
-  for (int64_t i0 = i_begin; i0 < i_end; i0 += 32, buf ^= 1) {
-    const int64_t row = i0 + l32 < i_end ? i0 + l32 : i_end - 1;
-    frag B[SKD];
+  // the g rows of a step are loaded one step ahead, ahead of the previous
+  // step's stores: loads and stores retire in order, so a load issued after
+  // the stores would wait for them too
+  frag B[SKD];
+  {
+    const int64_t row = i_begin + l32 < i_end ? i_begin + l32 : i_end - 1;
 #pragma unroll
     for (int s = 0; s < SKD; ++s) B[s] = ld_frag<T>(a.G + ((size_t)row * DL + s * KS + hh * EPL) * ESZ);
+  }
+  int buf = 0;
+  for (int64_t i0 = i_begin; i0 < i_end; i0 += 32, buf ^= 1) {
     unsigned char* t = sq[buf];
 #pragma unroll
     for (int m = 0; m < US::TPW; ++m) {
@@ -1031,6 +1036,11 @@ __global__ __launch_bounds__(256) void k_u_gemm(UArgs a, int64_t rows_per_wg) {
       }
     }
     __syncthreads();   // the block is complete; the other buffer's stores are done
+    if (i0 + 32 < i_end) {
+      const int64_t row = i0 + 32 + l32 < i_end ? i0 + 32 + l32 : i_end - 1;
+#pragma unroll
+      for (int s = 0; s < SKD; ++s) B[s] = ld_frag<T>(a.G + ((size_t)row * DL + s * KS + hh * EPL) * ESZ);
+    }
 #pragma unroll
     for (int it = 0; it < 32 * CH / 256; ++it) {
       const int id = it * 256 + tid, r = id / CH, ch = id % CH;
@@ -1896,8 +1906,12 @@ __global__ __launch_bounds__(256) void k_dh_u(DhuArgs a) {
   bf16x8 zb[SK2], gb[SKD];
   lds_copy_async(a.U + (size_t)i * S::UB, X, NU);
   load_ops(i, pa, pb, zb, gb);
+  static_assert(SK2 + SKD < 64, "wait count");
   for (int buf = 0; i < a.n_dst; i += gridDim.x, buf ^= 1) {
-    stage_wait();
+    // the copy of U_i was followed by at least SK2 + SKD loads of this thread
+    // (its operands): once no more than those are outstanding the copy is in
+    // (the item's stores need not have completed)
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(SK2 + SKD));
     __syncthreads();   // U_i is in X[buf]; every wave is done with X[buf ^ 1]
     const unsigned char* Xb = X + buf * S::UB;
     const int64_t inext = i + gridDim.x;
