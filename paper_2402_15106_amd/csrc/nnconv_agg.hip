@@ -185,11 +185,11 @@ struct OuterTrShape {
   static constexpr int64_t KTOT = (int64_t)H2 * DL + DL;
 };
 
-template <int DL, int H2, bool AHEAD>
-__global__ __launch_bounds__(256) void k_outer_sum_tr(OuterArgs a) {
+template <int DL, int H2, bool AHEAD, int NW = 4>
+__global__ __launch_bounds__(64 * NW) void k_outer_sum_tr(OuterArgs a) {
   using S = OuterTrShape<DL, H2>;
   using M = MT<__bf16>;
-  constexpr int ECH = S::ECH;
+  constexpr int ECH = S::ECH, NT = 64 * NW, TPW = (S::NTILE + NW - 1) / NW;   // threads, tiles per wave
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int rz[ECH], ru[ECH];   // source rows of the chunk's z and gathered rows
   unsigned char* zl = smem;
@@ -222,9 +222,9 @@ __global__ __launch_bounds__(256) void k_outer_sum_tr(OuterArgs a) {
     const int64_t nn = AHEAD ? n + G : a.n_seg;
     const int64_t qa = AHEAD ? a.seg_ptr[nn < a.n_seg ? nn : a.n_seg] : 0;
     const int64_t qb = AHEAD ? a.seg_ptr[nn < a.n_seg ? nn + 1 : a.n_seg] : 0;
-    f32x16 acc[S::TPW];
+    f32x16 acc[TPW];
 #pragma unroll
-    for (int j = 0; j < S::TPW; ++j) acc[j] = f32x16{};
+    for (int j = 0; j < TPW; ++j) acc[j] = f32x16{};
     float hs = 0.0f;   // z~ = 1 row: sum of the gathered rows (threads tid < DL)
     const bool ahead = AHEAD && tid < ECH && qb > qa;   // this thread reads ahead a slot of the next segment
     for (int64_t c0 = pa; c0 < pb; c0 += ECH) {
@@ -247,14 +247,14 @@ __global__ __launch_bounds__(256) void k_outer_sum_tr(OuterArgs a) {
       }
       __syncthreads();
       const int wbase = tid & ~63;
-      for (int U0 = 0; U0 < S::ZU; U0 += 256) {
+      for (int U0 = 0; U0 < S::ZU; U0 += NT) {
         const int U = U0 + tid, r = U / (S::ZNU + S::ZPAD), u = U % (S::ZNU + S::ZPAD);
         if (U < S::ZU)
           __builtin_amdgcn_global_load_lds(
               (gbl_void_t*)(a.zE + (size_t)rz[r < ECH ? r : ECH - 1] * H2 * 2 + (u < S::ZNU ? u : 0) * 16),
               (lds_void_t*)(zl + (size_t)(U0 + wbase) * 16), 16, 0, 0);
       }
-      for (int U0 = 0; U0 < S::UU; U0 += 256) {
+      for (int U0 = 0; U0 < S::UU; U0 += NT) {
         const int U = U0 + tid, r = U / (S::UNU + S::UPAD), u = U % (S::UNU + S::UPAD);
         if (U < S::UU)
           __builtin_amdgcn_global_load_lds(
@@ -267,8 +267,8 @@ __global__ __launch_bounds__(256) void k_outer_sum_tr(OuterArgs a) {
       const int nks = (cnt + 15) / 16;
       for (int ks = 0; ks < nks; ++ks) {
 #pragma unroll
-        for (int j = 0; j < S::TPW; ++j) {
-          const int ti = wv + 4 * j;
+        for (int j = 0; j < TPW; ++j) {
+          const int ti = wv + NW * j;
           if (ti < S::NTILE) {
             const int kt = ti / S::NCT, ct = ti % S::NCT;
             bf16x8 A = lds_frag_rows(zl, S::ZP, ks * 16, kt * 32);
@@ -292,8 +292,8 @@ __global__ __launch_bounds__(256) void k_outer_sum_tr(OuterArgs a) {
 
     unsigned char* o = a.out + (size_t)n * S::KTOT * 2;
 #pragma unroll
-    for (int j = 0; j < S::TPW; ++j) {
-      const int ti = wv + 4 * j;
+    for (int j = 0; j < TPW; ++j) {
+      const int ti = wv + NW * j;
       if (ti < S::NTILE) {
         unsigned char* dst = o + ((size_t)ti * 1024 + lane * 16) * 2;
         float v[16];
@@ -603,11 +603,18 @@ dsmp_status outer_shape(dsmp_handle* h, const OuterArgs& a) {
     if (st != DSMP_OK) return st;
     int per_cu = 0;
     DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ahead, 256, S::LDS));
-    if (per_cu >= 4)
+    if (per_cu >= 4) {
       hipLaunchKernelGGL(single, dim3((unsigned)a.n_seg), dim3(256), S::LDS, h->stream, a);
-    else
-      hipLaunchKernelGGL(ahead, dim3((unsigned)std::min<int64_t>(a.n_seg, (int64_t)h->n_cu * std::max(per_cu, 1))),
-                         dim3(256), S::LDS, h->stream, a);
+    } else {
+      // few workgroups fit: eight waves per workgroup, half the tiles per wave
+      auto ahead8 = k_outer_sum_tr<DL, H2, true, 8>;
+      if ((st = set_lds_bytes(h, ahead8, S::LDS)) != DSMP_OK) return st;
+      int per_cu8 = 0;
+      DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu8, ahead8, 512, S::LDS));
+      hipLaunchKernelGGL(ahead8,
+                         dim3((unsigned)std::min<int64_t>(a.n_seg, (int64_t)h->n_cu * std::max(per_cu8, 1))),
+                         dim3(512), S::LDS, h->stream, a);
+    }
     DSMP_LAUNCHED(h, "segment outer-product sums");
     return DSMP_OK;
   }
