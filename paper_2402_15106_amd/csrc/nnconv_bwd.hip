@@ -1425,17 +1425,29 @@ struct W2TrShape {
   static constexpr int DB = ECH * DS::PITCH, BUF = DB + ECH * ZS::PITCH, LDS = 2 * BUF;
 };
 
-template <int H1, int H2>
-__global__ __launch_bounds__(256, 2) void k_bwd_dW2_tr(W2Args a) {
+// W8: eight waves per workgroup cover all (k, j) tiles of a 256 x 256 dW2
+// (two k tiles by four j tiles each), so each chunk of edges is read once
+// instead of once per half of the j tiles.
+template <int H1, int H2, bool W8 = false>
+struct W2TrTiles {
   using S = W2Shape<__bf16, H1, H2>;
+  static constexpr int NW = W8 ? 8 : 4, NSPLIT = W8 ? 1 : S::NSPLIT;
+  static constexpr int KT_W = W8 ? 2 : S::KT_W, JT_W = W8 ? 4 : S::JT_W;
+  static_assert(!W8 || (S::KT == 8 && S::JT == 8), "eight waves: h1 = h2 = 256");
+};
+
+template <int H1, int H2, bool W8 = false>
+__global__ __launch_bounds__(W8 ? 512 : 256, W8 ? 1 : 2) void k_bwd_dW2_tr(W2Args a) {
+  using S0 = W2Shape<__bf16, H1, H2>;
+  using S = W2TrTiles<H1, H2, W8>;
   using TS = W2TrShape<H1, H2>;
   using M = MT<__bf16>;
   constexpr int ECH = TS::ECH;
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
   const int split = blockIdx.x % S::NSPLIT, chunk = blockIdx.x / S::NSPLIT;
-  const int kt0 = (wv / S::JGRP) * S::KT_W;
-  const int jt0 = split * S::JT_WG + (wv % S::JGRP) * S::JT_W;
+  const int kt0 = W8 ? (wv / 2) * 2 : (wv / S0::JGRP) * S0::KT_W;
+  const int jt0 = W8 ? (wv % 2) * 4 : split * S0::JT_WG + (wv % S0::JGRP) * S0::JT_W;
   const int64_t e_begin = (int64_t)chunk * a.per_chunk;
   int64_t e_end = e_begin + a.per_chunk;
   if (e_end > a.E) e_end = a.E;
@@ -1450,6 +1462,7 @@ __global__ __launch_bounds__(256, 2) void k_bwd_dW2_tr(W2Args a) {
     typename TS::DS sd;
     typename TS::ZS sz;
     auto issue = [&](int c, unsigned char* buf) {
+      if (tid >= 256) return;   // the row stages are laid out for 256 threads
       const int64_t e0 = e_begin + (int64_t)c * ECH;
       const int nv = (int)(e_end - e0 < ECH ? e_end - e0 : ECH);
       sd.init(H2 * 2, nv);
@@ -2131,10 +2144,17 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
     if (nchunk < 1) nchunk = 1;
     if constexpr (sizeof(T) == 2) {
       using TS = W2TrShape<H1, H2>;
-      auto k2 = k_bwd_dW2_tr<H1, H2>;
-      if ((st = set_lds(h, k2, TS::LDS)) != DSMP_OK) return st;
-      ProfScope prof(h, DSMP_K_DW2);
-      hipLaunchKernelGGL(k2, dim3(nchunk * S::NSPLIT), dim3(256), TS::LDS, s, w2);
+      if constexpr (S::NSPLIT > 1 && H1 == 256 && H2 == 256) {
+        auto k2 = k_bwd_dW2_tr<H1, H2, true>;
+        if ((st = set_lds(h, k2, TS::LDS)) != DSMP_OK) return st;
+        ProfScope prof(h, DSMP_K_DW2);
+        hipLaunchKernelGGL(k2, dim3(nchunk), dim3(512), TS::LDS, s, w2);
+      } else {
+        auto k2 = k_bwd_dW2_tr<H1, H2>;
+        if ((st = set_lds(h, k2, TS::LDS)) != DSMP_OK) return st;
+        ProfScope prof(h, DSMP_K_DW2);
+        hipLaunchKernelGGL(k2, dim3(nchunk * S::NSPLIT), dim3(256), TS::LDS, s, w2);
+      }
     } else {
       auto k2 = k_bwd_dW2<T, H1, H2>;
       if ((st = set_lds(h, k2, S::LDS)) != DSMP_OK) return st;
