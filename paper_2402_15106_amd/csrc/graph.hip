@@ -20,9 +20,9 @@ constexpr int BBOX_BLOCKS = 256;
 
 struct GridParams {
   float lo[3];
-  float inv_c;
   int dims[3];
   int ncell;
+  double inv_c;   // 1 / cell width
 };
 
 struct GraphStats {
@@ -72,8 +72,9 @@ __global__ __launch_bounds__(256) void k_bbox_partial(const float* __restrict__ 
 
 // One thread: reduce the partial boxes and choose the cell size.  Cells are
 // at least r*(1 + 2^-10) wide, so two points that pass the float32 radius
-// test always sit in the same or adjacent cells; the grid is coarsened by
-// doubling until it has at most `cap` cells.
+// test always sit in the same or adjacent cells (cell coordinates are formed
+// in double, see cell_coord); the grid is coarsened by doubling until it has
+// at most `cap` cells.
 __global__ void k_grid_setup(const float* __restrict__ part, int nb, int D, float r, int64_t cap,
                              GridParams* __restrict__ g, GraphStats* __restrict__ st) {
   if (threadIdx.x != 0) return;
@@ -99,14 +100,20 @@ __global__ void k_grid_setup(const float* __restrict__ part, int nb, int D, floa
     c *= 2.0;
   }
   for (int a = 0; a < 3; ++a) { g->lo[a] = lo[a]; g->dims[a] = (int)dims[a]; }
-  g->inv_c = (float)(1.0 / c);
+  g->inv_c = 1.0 / c;
   g->ncell = g->dims[0] * g->dims[1] * g->dims[2];
   st->total = 0;
   st->maxraw = 0;
 }
 
-__device__ __forceinline__ int cell_coord(float v, float lo, float inv_c, int dim) {
-  int c = (int)floorf((v - lo) * inv_c);
+// Cell of coordinate v, in double: v - lo is exact there and the product
+// with 1/c is within 2^-52 of the cell coordinate, so the cell margin of
+// 2^-10 covers the rounding however many cells an axis has (in float32 the
+// worst-case error grows with the coordinate and reaches the margin at a few
+// thousand cells on an axis, which a long, thin point set can have).
+__device__ __forceinline__ int cell_coord(float v, float lo, double inv_c, int dim) {
+  const double t = ((double)v - (double)lo) * inv_c;
+  int c = (int)floor(t);
   return c < 0 ? 0 : (c >= dim ? dim - 1 : c);
 }
 

@@ -69,6 +69,32 @@ def _rand(n, D, seed):
     return np.random.default_rng(seed).uniform(0, 1, (n, D)).astype(np.float32)
 
 
+def _long_line(r=0.02, length=300.0, pairs=4000, seed=17):
+    """Points along a line 15,000 cells long (one cell across) with pairs at
+    the largest float32 distance that passes the radius test, the first point
+    just past a cell bound, far from the origin, where the rounding of a cell
+    coordinate is largest against the cell margin of 2^-10."""
+    g = np.random.default_rng(seed)
+    f32 = np.float32
+    r2 = f32(r) * f32(r)
+    c = r * (1.0 + 2.0 ** -10)
+    k = g.integers(int(0.6 * length / c), int(length / c) - 2, pairs)
+    x1 = ((k + g.uniform(0.9e-3, 1.5e-3, pairs)) * c).astype(f32)
+    x2 = (x1 + f32(r)).astype(f32)
+    for _ in range(8):   # the largest x2 with fl(fl(x2 - x1)^2) <= fl(r^2)
+        d = (x2 - x1).astype(f32)
+        over = (d * d).astype(f32) > r2
+        x2 = np.where(over, np.nextafter(x2, f32(-np.inf)), x2)
+    up = np.nextafter(x2, f32(np.inf))
+    du = (up - x1).astype(f32)
+    x2 = np.where((du * du).astype(f32) <= r2, up, x2)
+    y = np.full(pairs, 5e-4, f32)
+    pts = [np.array([[0.0, 0.0], [length, 1e-3]], f32),
+           np.stack([x1, y], 1), np.stack([x2, y], 1),
+           np.stack([g.uniform(0, length, 2000), g.uniform(0, 1e-3, 2000)], 1).astype(f32)]
+    return np.concatenate(pts)
+
+
 CASES = {
     "2d_uncapped": (lambda: _rand(3000, 2, 1), 2500, 0.03, 0, 0),
     "2d_knn5": (lambda: _rand(3000, 2, 2), 3000, 0.05, 5, 0),
@@ -90,6 +116,7 @@ CASES = {
     "no_destinations": (lambda: _rand(100, 2, 13), 0, 0.1, 0, 0),
     "single_point": (lambda: _rand(1, 3, 14), 1, 0.1, 0, 0),
     "halo_far": (lambda: np.concatenate([_rand(500, 2, 15), _rand(500, 2, 16) + 5.0]), 500, 0.08, 0, 0),
+    "long_line_15k_cells": (lambda: _long_line(), 10002, 0.02, 0, 0),
 }
 
 
