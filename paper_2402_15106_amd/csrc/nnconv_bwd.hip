@@ -1955,40 +1955,54 @@ __global__ __launch_bounds__(256) void k_dh_u(DhuArgs a) {
   }
 }
 
-// grad_h[j] = sum over the edges leaving j (edge order) of m_e, plus the root
-// and residual terms when j is a destination; two channels per thread (a
-// wave covers one source at d = 128).  The edge ids and rows of eight edges
-// are loaded before they are added (in edge order).
-__global__ void k_dh_gather(int64_t n_src, int64_t n_dst, int DL, const int32_t* __restrict__ csc_ptr,
-                            const int32_t* __restrict__ csc_eid, const unsigned char* __restrict__ mE,
-                            const float* __restrict__ dh_node, float* __restrict__ grad_h) {
-  const int hw = DL / 2;
-  const int64_t total = n_src * hw;
-  for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < total; x += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t j = x / hw;
-    const int c = 2 * (int)(x % hw);
-    float s0 = 0.0f, s1 = 0.0f;
+// grad_h[j] = sum over the edges leaving j of m_e, plus the root and residual
+// terms when j is a destination.  One wave per source: the edge ids come in
+// with one load per 64 edges and are passed round by shuffles; lanes take two
+// channels each, and at d < 128 the wave's lanes form G = 128 / d groups that
+// take every G-th edge, their sums then added in group order (a fixed order).
+template <int DL>
+__global__ __launch_bounds__(256) void k_dh_gather(int64_t n_src, int64_t n_dst, const int32_t* __restrict__ csc_ptr,
+                                                   const int32_t* __restrict__ csc_eid,
+                                                   const unsigned char* __restrict__ mE,
+                                                   const float* __restrict__ dh_node, float* __restrict__ grad_h) {
+  constexpr int HW = DL / 2, G = 64 / HW, UN = 8;
+  const int lane = threadIdx.x & 63, cp = lane % HW, grp = lane / HW;
+  for (int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); j < n_src; j += (int64_t)gridDim.x * 4) {
     const int t0 = csc_ptr[j], t1 = csc_ptr[j + 1];
-    float node0 = 0.0f, node1 = 0.0f;
-    if (j < n_dst) {
-      node0 = dh_node[j * DL + c];
-      node1 = dh_node[j * DL + c + 1];
-    }
-    for (int t = t0; t < t1; t += 8) {
-      int32_t id[8];
+    float s0 = 0.0f, s1 = 0.0f;
+    for (int base = t0; base < t1; base += 64) {
+      const int cnt = t1 - base < 64 ? t1 - base : 64;
+      const int my = lane < cnt ? csc_eid[base + lane] : 0;
+      for (int k = 0; k < cnt; k += G * UN) {
+        bf16x2 m[UN];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) id[u] = t + u < t1 ? csc_eid[t + u] : -1;
-      bf16x2 m[8];
+        for (int u = 0; u < UN; ++u) {
+          const int idx = k + u * G + grp;
+          const int eid = __shfl(my, idx < 64 ? idx : 0, 64);
+          m[u] = idx < cnt ? *reinterpret_cast<const bf16x2*>(mE + ((size_t)eid * DL + 2 * cp) * 2) : bf16x2{};
+        }
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        m[u] = id[u] >= 0 ? *reinterpret_cast<const bf16x2*>(mE + ((size_t)id[u] * DL + c) * 2) : bf16x2{};
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        s0 += (float)m[u][0];
-        s1 += (float)m[u][1];
+        for (int u = 0; u < UN; ++u) {
+          s0 += (float)m[u][0];
+          s1 += (float)m[u][1];
+        }
       }
     }
-    *reinterpret_cast<f32x2*>(grad_h + j * DL + c) = f32x2{s0 + node0, s1 + node1};
+    // groups in order: group 0 adds group 1's sums, then group 2's, ...
+    const float g0 = s0, g1 = s1;
+#pragma unroll
+    for (int g = 1; g < G; ++g) {
+      const float o0 = __shfl(g0, cp + g * HW, 64), o1 = __shfl(g1, cp + g * HW, 64);
+      s0 += o0;
+      s1 += o1;
+    }
+    if (grp == 0) {
+      if (j < n_dst) {
+        s0 += dh_node[j * DL + 2 * cp];
+        s1 += dh_node[j * DL + 2 * cp + 1];
+      }
+      *reinterpret_cast<f32x2*>(grad_h + j * DL + 2 * cp) = f32x2{s0, s1};
+    }
   }
 }
 
@@ -2386,11 +2400,12 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
       if ((st = dispatch_dh_u(h, d, da)) != DSMP_OK) return st;
     }
     if (n_src > 0) {
-      unsigned grid = ceil_div(n_src * d.d / 2, 256);
-      if (grid > 4096) grid = 4096;
+      unsigned grid = ceil_div(n_src, 4);
+      if (grid > 8192) grid = 8192;
       ProfScope prof(h, DSMP_K_DH_FINAL);
-      hipLaunchKernelGGL(k_dh_gather, dim3(grid), dim3(256), 0, s, n_src, n_dst, d.d, g->csc_ptr, g->csc_eid, w.mE,
-                         w.dh_node, grad_h);
+      auto kg = d.d == 32 ? k_dh_gather<32> : d.d == 64 ? k_dh_gather<64> : k_dh_gather<128>;
+      hipLaunchKernelGGL(kg, dim3(grid), dim3(256), 0, s, n_src, n_dst, g->csc_ptr, g->csc_eid, w.mE, w.dh_node,
+                         grad_h);
       DSMP_LAUNCHED(h, "grad_h from the edge terms");
     }
   }
