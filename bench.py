@@ -74,6 +74,7 @@ KERNEL_SOURCES = {
     "sample": SRC_CORE, "gather": SRC_CORE, "graph": SRC_GRAPH,
     "edge_fwd": SRC_FWD, "edge_dh": SRC_FWD, "edge_mlp": SRC_FWD,
     "dz": SRC_BWD, "u_gemm": SRC_BWD, "dW2": SRC_BWD, "dW1": SRC_BWD, "dh_u": SRC_BWD, "dh_final": SRC_BWD,
+    "da1": SRC_BWD,
     "dW3": SRC_BWD + ["nnconv_agg.hip"],
     "outer_fwd": SRC_AGG, "gemm_fwd": SRC_AGG, "outer_dh": SRC_AGG, "gemm_dh": SRC_AGG,
 }
@@ -163,19 +164,31 @@ def agg_work(w, E, n_src, fused=False):
     esz = 2 if w.dtype == "bf16" else 4
     kt = (H2 + 1) * d
     mask = (H1 + H2) // 8
+    dz_m = w.dtype == "bf16" and not fused and (d, H1, H2) == (128, 256, 256)
     if fused:
         dz = (2 * E * (d * H2 + H1 * H2 + H1 * H2 + H1 * de),
               n * H2 * d * esz + E * (4 + d * esz + mask + 2 * (D + 1) * 4))
+    elif dz_m:
+        # dz masked into da2 and the feature-gradient terms m_e from one read
+        # of U_i and g_i: reads the source index, h_j, z and z's mask bits,
+        # writes da2 and m_e
+        dz = (2 * E * (d * H2 + H2 * d) + 2 * n * d * d,
+              n * (H2 * d + d) * esz + E * (4 + d * esz + H2 * esz + H2 // 8 + H2 * esz + d * esz))
     else:
         dz = (2 * E * (d * H2 + H1 * H2), n * H2 * d * esz + E * (4 + d * esz + mask + (H1 + H2) * esz))
     out = {
         "dz": dz,
         "dW3": (2 * n * kt * d, n * kt * esz + n * d * esz),
     }
+    if dz_m:
+        # da1 = [z1 > 0] W2^T da2 from the stored da2 rows
+        out["da1"] = (2 * E * H1 * H2, E * (H2 * esz + H1 // 8 + H1 * esz))
     if w.dtype == "bf16":
         # the feature gradient from U: per-edge terms from U_i, z_e and the bias
         # row, then their sums over the edges leaving each source
-        out["dh_u"] = (2 * E * H2 * d + 2 * n * d * d, n * H2 * d * esz + E * (H2 * esz + d * esz) + n * (d * esz + 4))
+        if not dz_m:
+            out["dh_u"] = (2 * E * H2 * d + 2 * n * d * d,
+                           n * H2 * d * esz + E * (H2 * esz + d * esz) + n * (d * esz + 4))
         out["dh_final"] = (0, E * (d * esz + 4) + n_src * (d * 4 + 4) + n * d * 4)
     return out
 

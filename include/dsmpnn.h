@@ -382,7 +382,7 @@ enum {
   DSMP_K_NODE_BWD = 5,  /* backward node, root and db3 kernels */
   DSMP_K_EDGE_DH = 6,   /* feature-gradient edge contraction kernel */
   DSMP_K_DH_FINAL = 7,  /* feature-gradient assembly kernel */
-  DSMP_K_DZ = 8,        /* dz / da2 / da1 kernel (either form) */
+  DSMP_K_DZ = 8,        /* dz / da2 / da1 kernel (either form; with the terms of DSMP_K_DH_U at h = 256) */
   DSMP_K_DW3 = 9,       /* dW3 kernels (split over edges, or over S) */
   DSMP_K_DW2 = 10,      /* dW2 split-over-edges kernel */
   DSMP_K_DW1 = 11,      /* dW1 kernel */
@@ -397,7 +397,8 @@ enum {
   DSMP_K_MLP = 20,      /* encoder / decoder perceptrons, forward and backward */
   DSMP_K_LOSS = 21,     /* masked mean squared error */
   DSMP_K_DH_U = 22,     /* per-edge feature-gradient terms from U (aggregate form, bf16) */
-  DSMP_K_COUNT = 23
+  DSMP_K_DA1 = 23,      /* da1 from the stored da2 (aggregate form, bf16, h = 256) */
+  DSMP_K_COUNT = 24
 };
 dsmp_status dsmp_profile_enable(dsmp_handle* h, int enable);
 dsmp_status dsmp_profile_reset(dsmp_handle* h);

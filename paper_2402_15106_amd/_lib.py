@@ -42,7 +42,7 @@ EXPORTED = ["dsmp_version", "dsmp_create", "dsmp_destroy", "dsmp_set_stream", "d
 # kernel classes of the opt-in timing (dsmp_profile_*)
 KERNEL_CLASSES = ["sample", "gather", "graph", "edge_fwd", "node_fwd", "node_bwd", "edge_dh", "dh_final",
                   "dz", "dW3", "dW2", "dW1", "reduce", "edge_mlp", "outer_fwd", "gemm_fwd", "outer_dh",
-                  "gemm_dh", "u_gemm", "attr", "mlp", "loss", "dh_u"]
+                  "gemm_dh", "u_gemm", "attr", "mlp", "loss", "dh_u", "da1"]
 
 
 class DsmpError(RuntimeError):

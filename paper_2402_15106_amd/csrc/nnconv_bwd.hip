@@ -2006,6 +2006,222 @@ __global__ __launch_bounds__(256) void k_dh_gather(int64_t n_src, int64_t n_dst,
   }
 }
 
+// ------------------------------------------------------------ dz and feature-gradient terms in one pass
+// The two per-edge products that read U_i, dz_e = U_i h_j and
+// m_e = U~_i^T z~_e, in one pass over each destination's edges (bf16 layers
+// whose kernel-MLP gradients are not fused, h2 = 256), so that U is read from
+// HBM once for both.  U_i and g_i are copied to LDS as they stand (direct
+// global-to-LDS loads, double-buffered over destinations).  Of the four
+// waves, wave w takes, for every 32-edge tile of the destination, the two
+// 32-neuron tiles 2w, 2w + 1 of dz (A = U_i fragments read from LDS as
+// stored, B = h_j rows), which it masks with the forward's ReLU bits of z
+// into da2 (stored positions, as the dz pass does), and the 32-column tile w
+// of m_e (as k_dh_u).  dz1 = W2^T da2 and da1 follow in k_da1, whose W2^T
+// copy would not fit in LDS beside two U_i.
+struct DzDhuArgs {
+  DhuArgs m;
+  const int32_t* col;
+  const unsigned char* h_in;    // [n_src][d] bf16
+  const unsigned char* zmask;   // [E][(h1+h2)/8] ReLU mask bits of z1 and z (forward)
+  unsigned char* da2E;          // [E][h2] bf16 out, stored positions
+};
+
+template <int DL, int H1, int H2>
+struct DzDhuShape {
+  static constexpr int UB = H2 * DL * 2, GB = DL * 2, BUF = UB + GB, LDS = 2 * BUF;
+  static_assert(UB % (256 * 16) == 0 && GB % 16 == 0 && GB / 16 <= 256, "U_i whole rounds, g_i one partial round");
+};
+
+template <int DL, int H1, int H2>
+__global__ __launch_bounds__(256) void k_dz_dh_u(DzDhuArgs a) {
+  using S = DzDhuShape<DL, H1, H2>;
+  using M = MT<__bf16>;
+  constexpr int SKD = DL / 16, SK2 = H2 / 16, PT = DL / 32, KT = H2 / 32, KTW = KT / 4;
+  constexpr int MW1 = H1 / 64, MW2 = H2 / 64, MROW = (H1 + H2) / 8;
+  static_assert(PT == 4 && KTW == 2, "one column tile of p and two neuron tiles per wave");
+  extern __shared__ __align__(16) unsigned char X[];
+  const DhuArgs& d = a.m;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  bf16x8 ba[SKD];
+#pragma unroll
+  for (int sf = 0; sf < SKD; ++sf)
+    ba[sf] = ld_frag<__bf16>(d.b3n + ((size_t)(32 * wv + l32) * DL + 16 * sf + 8 * hh) * 2);
+  // operands of one 32-edge tile: z rows, h_j rows (c: the lane's source) and
+  // the mask word of this wave's neurons
+  struct Ops {
+    bf16x8 z[SK2], h[SKD];
+    uint32_t mw;
+  };
+  auto load_ops = [&](int64_t pa, int64_t pb, int et, int32_t c, Ops& o) {
+    const int64_t e = pa + (int64_t)et * 32 + l32;
+    const bool valid = e < pb;
+    const size_t es = valid ? (size_t)e : 0;
+    const unsigned char* zr = d.zE + es * H2 * 2;
+#pragma unroll
+    for (int s2 = 0; s2 < SK2; ++s2) o.z[s2] = valid ? ld_frag<__bf16>(zr + (16 * s2 + 8 * hh) * 2) : bf16x8{};
+    const unsigned char* hr = a.h_in + (size_t)(valid ? c : 0) * DL * 2;
+#pragma unroll
+    for (int s = 0; s < SKD; ++s) o.h[s] = valid ? ld_frag<__bf16>(hr + (16 * s + 8 * hh) * 2) : bf16x8{};
+    o.mw = valid ? reinterpret_cast<const uint32_t*>(a.zmask + es * MROW)[2 * MW1 + hh * MW2 + wv] : 0u;
+  };
+  auto first_col = [&](int64_t i) -> int32_t {
+    const int64_t q = d.row_ptr[i] + l32;
+    return q < d.row_ptr[i + 1] ? a.col[q] : 0;
+  };
+  auto item = [&](const unsigned char* Xb, int64_t pa, int64_t pb, int et, const Ops& o) {
+    const int64_t e = pa + (int64_t)et * 32 + l32;
+    f32x16 acc = f32x16{};
+    // m_e: the bias row sum_q b3[p*d+q] g_i[q], then the z~ . U_i terms
+#pragma unroll
+    for (int sf = 0; sf < SKD; ++sf)
+      acc = M::mma(ba[sf], *reinterpret_cast<const bf16x8*>(Xb + S::UB + (16 * sf + 8 * hh) * 2), acc);
+#pragma unroll
+    for (int s2 = 0; s2 < SK2; ++s2) acc = M::mma(lds_frag_ut<DL>(Xb, 16 * s2, 32 * wv), o.z[s2], acc);
+    // dz_e on neuron tiles 2w, 2w + 1: fragment (kt, s) of U_i is 64 lanes x 16 bytes
+    f32x16 dz[KTW];
+#pragma unroll
+    for (int kk = 0; kk < KTW; ++kk) {
+      dz[kk] = f32x16{};
+#pragma unroll
+      for (int s = 0; s < SKD; ++s)
+        dz[kk] = M::mma(*reinterpret_cast<const bf16x8*>(Xb + (((KTW * wv + kk) * SKD + s) * 64 + lane) * 16),
+                        o.h[s], dz[kk]);
+    }
+    if (e < pb) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const bf16x2 lo = __builtin_convertvector((f32x2){acc[4 * g], acc[4 * g + 1]}, bf16x2);
+        const bf16x2 hi = __builtin_convertvector((f32x2){acc[4 * g + 2], acc[4 * g + 3]}, bf16x2);
+        *reinterpret_cast<uint2*>(d.mE + ((size_t)e * DL + 32 * wv + 8 * g + 4 * hh) * 2) =
+            make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+      }
+      // da2 positions 16 s + 8 hh + u, s = 4w + sl, hold dz register 8 (sl % 2) + u of tile sl / 2
+#pragma unroll
+      for (int sl = 0; sl < 4; ++sl) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = keep_if_bit(dz[sl / 2][8 * (sl % 2) + u], o.mw, 8 * sl + u);
+        *reinterpret_cast<bf16x8*>(a.da2E + ((size_t)e * H2 + 16 * (4 * wv + sl) + 8 * hh) * 2) =
+            pack_frag<__bf16>(v);
+      }
+    }
+  };
+  int64_t i = blockIdx.x;
+  if (i >= d.n_dst) return;
+  const int64_t G = gridDim.x;
+  int64_t pa = d.row_ptr[i], pb = d.row_ptr[i + 1];
+  Ops ops;
+  lds_copy_async(d.U + (size_t)i * S::UB, X, S::UB / 16);
+  lds_copy_async(d.gT + (size_t)i * S::GB, X + S::UB, S::GB / 16);
+  load_ops(pa, pb, 0, first_col(i), ops);
+  // source of the lane's edge in the first tile of the next destination,
+  // loaded a destination ahead of its h row
+  int32_t cnext = i + G < d.n_dst ? first_col(i + G) : 0;
+  static_assert(SK2 + SKD + 1 < 64, "wait count");
+  for (int buf = 0; i < d.n_dst; i += G, buf ^= 1) {
+    // the copies of U_i and g_i were followed by the SK2 + SKD + 1 operand
+    // loads of the destination's first tile (issued whenever it has an edge,
+    // the only case that reads the copy): once no more than those are
+    // outstanding, the copies are in
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(SK2 + SKD + 1));
+    __syncthreads();   // U_i, g_i in buffer buf; every wave is done with buffer buf ^ 1
+    const unsigned char* Xb = X + buf * S::BUF;
+    const int64_t inext = i + G;
+    int64_t pa2 = 0, pb2 = 0;
+    int32_t cnn = 0;
+    Ops on;
+    if (inext < d.n_dst) {
+      unsigned char* Xn = X + (buf ^ 1) * S::BUF;
+      lds_copy_async(d.U + (size_t)inext * S::UB, Xn, S::UB / 16);
+      lds_copy_async(d.gT + (size_t)inext * S::GB, Xn + S::UB, S::GB / 16);
+      pa2 = d.row_ptr[inext];
+      pb2 = d.row_ptr[inext + 1];
+      load_ops(pa2, pb2, 0, cnext, on);
+      if (inext + G < d.n_dst) cnn = first_col(inext + G);
+    }
+    const int net = (int)((pb - pa + 31) / 32);
+    if (net > 0) item(Xb, pa, pb, 0, ops);
+    for (int et = 1; et < net; ++et) {   // destinations of more than 32 edges
+      const int64_t e = pa + (int64_t)et * 32 + l32;
+      Ops ox;
+      load_ops(pa, pb, et, e < pb ? a.col[e] : 0, ox);
+      item(Xb, pa, pb, et, ox);
+    }
+    ops = on;
+    pa = pa2;
+    pb = pb2;
+    cnext = cnn;
+  }
+}
+
+// dz1 = W2^T da2 and da1 = dz1 * [z1 > 0] for 32-edge tiles of the stored da2
+// rows (the second half of the dz epilogue, in the same products and order).
+// W2^T is staged in LDS once per workgroup; each wave takes every
+// (4 x grid)-th tile, the next tile's da2 rows and mask words loaded while the
+// current one is multiplied.
+template <int H1, int H2>
+__global__ __launch_bounds__(256) void k_da1(int64_t E, const unsigned char* __restrict__ w2t,
+                                             const unsigned char* __restrict__ zmask,
+                                             const unsigned char* __restrict__ da2E, unsigned char* __restrict__ da1E) {
+  using SA = DzAggShape<__bf16, H1, H2>;
+  using M = MT<__bf16>;
+  constexpr int SK2 = H2 / 16, JT = H1 / 32, MW1 = H1 / 64, MROW = (H1 + H2) / 8;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  {
+    LdsStage<H1, H2 * 2> stg;
+    stg.init();
+    stg.issue(w2t, smem);
+    stage_wait();
+    __syncthreads();
+  }
+  const int64_t ntile = (E + 31) / 32, stride = (int64_t)gridDim.x * 4;
+  auto load = [&](int64_t t, bf16x8 (&B)[SK2], uint32_t (&m1)[MW1]) {
+    const int64_t e = t * 32 + l32;
+    const bool valid = t < ntile && e < E;
+    const size_t es = valid ? (size_t)e : 0;
+#pragma unroll
+    for (int s = 0; s < SK2; ++s)
+      B[s] = valid ? ld_frag<__bf16>(da2E + (es * H2 + 16 * s + 8 * hh) * 2) : bf16x8{};
+    const uint32_t* mb = reinterpret_cast<const uint32_t*>(zmask + es * MROW);
+#pragma unroll
+    for (int w = 0; w < MW1; ++w) m1[w] = valid ? mb[hh * MW1 + w] : 0u;
+  };
+  int64_t t = (int64_t)blockIdx.x * 4 + wv;
+  bf16x8 B[SK2];
+  uint32_t m1[MW1];
+  load(t, B, m1);
+  for (; t < ntile; t += stride) {
+    bf16x8 Bn[SK2];
+    uint32_t m1n[MW1];
+    load(t + stride, Bn, m1n);
+    const int64_t e = t * 32 + l32;
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      __builtin_amdgcn_sched_barrier(0);
+      f32x16 C = f32x16{};
+#pragma unroll
+      for (int s = 0; s < SK2; ++s) {
+        const bf16x8 A = *reinterpret_cast<const bf16x8*>(smem + (jt * 32 + l32) * SA::W2P + (16 * s + 8 * hh) * 2);
+        C = M::mma(A, B[s], C);
+      }
+      // register i of tile jt is stored position 16 (2 jt + i / 8) + 8 hh + i % 8
+#pragma unroll
+      for (int i = 0; i < 16; i += 8) {
+        const int n = 16 * jt + i;
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = keep_if_bit(C[i + u], m1[(n + u) / 32], (n + u) % 32);
+        if (e < E) *reinterpret_cast<bf16x8*>(da1E + ((size_t)e * H1 + (n / 8) * 16 + 8 * hh) * 2) = pack_frag<__bf16>(v);
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < SK2; ++s) B[s] = Bn[s];
+#pragma unroll
+    for (int w = 0; w < MW1; ++w) m1[w] = m1n[w];
+  }
+}
+
 template <int DL, int H2>
 dsmp_status launch_dh_u(dsmp_handle* h, const DhuArgs& a) {
   using S = DhuShape<DL, H2>;
@@ -2033,6 +2249,12 @@ dsmp_status dispatch_dh_u(dsmp_handle* h, const dsmp_layer_desc& d, const DhuArg
 // The feature gradient comes from U (and no per-source sums are formed) for
 // bf16 layers of the aggregate form.
 bool dh_from_u(const dsmp_layer_desc& d, bool agg) { return agg && d.dtype == DSMP_BF16; }
+
+// Where the kernel-MLP gradients are not fused (bf16, d = 128, h1 = h2 = 256)
+// the dz pass also forms the feature-gradient terms (k_dz_dh_u).
+bool dz_with_m(const dsmp_layer_desc& d, bool agg) {
+  return dh_from_u(d, agg) && d.d == 128 && d.h1 == 256 && d.h2 == 256;
+}
 
 
 // ------------------------------------------------------------ workspace
@@ -2117,7 +2339,8 @@ dsmp_status set_lds(dsmp_handle* h, K kernel, int bytes) {
 }
 
 template <typename T, int DL, int H1, int H2>
-dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, const W2Args& w2) {
+dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, const W2Args& w2,
+                           const DzDhuArgs* fm) {
   hipStream_t s = h->stream;
   dsmp_status st;
   if (dz.E > 0 && dz.U) {
@@ -2127,6 +2350,36 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
       UArgs ua{dz.n_dst, dz.gT, dz.packed + dz.L.w3u, const_cast<unsigned char*>(dz.U)};
       if ((st = launch_u_gemm<T, DL, H2>(h, ua)) != DSMP_OK) return st;
     }
+    if (fm) {
+      if constexpr (sizeof(T) == 2 && DL == 128 && H1 == 256 && H2 == 256) {
+        {
+          // dz (masked into da2) and the feature-gradient terms from one read of U
+          using S = DzDhuShape<DL, H1, H2>;
+          auto kf = k_dz_dh_u<DL, H1, H2>;
+          if ((st = set_lds(h, kf, S::LDS)) != DSMP_OK) return st;
+          int per_cu = 0;
+          DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kf, 256, S::LDS));
+          const int64_t grid = std::min<int64_t>(dz.n_dst, (int64_t)h->n_cu * std::max(per_cu, 1));
+          ProfScope prof(h, DSMP_K_DZ);
+          if (grid > 0) hipLaunchKernelGGL(kf, dim3((unsigned)grid), dim3(256), S::LDS, s, *fm);
+          DSMP_LAUNCHED(h, "dz and feature-gradient terms from U");
+        }
+        {
+          using SA = DzAggShape<T, H1, H2>;
+          auto ka = k_da1<H1, H2>;
+          if ((st = set_lds(h, ka, SA::LDS)) != DSMP_OK) return st;
+          int per_cu = 0;
+          DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ka, 256, SA::LDS));
+          const int64_t grid = std::min<int64_t>(ceil_div(ceil_div(dz.E, 32), 4), (int64_t)h->n_cu * std::max(per_cu, 1));
+          ProfScope prof(h, DSMP_K_DA1);
+          hipLaunchKernelGGL(ka, dim3((unsigned)grid), dim3(256), SA::LDS, s, dz.E, dz.packed + dz.L.w2t, dz.zmask,
+                             dz.da2E, dz.da1E);
+          DSMP_LAUNCHED(h, "da1 from da2");
+        }
+      } else {
+        return fail(h, DSMP_UNSUPPORTED, "dz with the feature-gradient terms is built for d = 128, h = 256 only");
+      }
+    } else {
     using SA = DzAggShape<T, H1, H2>;
     auto kz = k_bwd_dz_agg<T, DL, H1, H2>;
     if ((st = set_lds(h, kz, SA::LDS)) != DSMP_OK) return st;
@@ -2136,6 +2389,7 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
     ProfScope prof(h, DSMP_K_DZ);
     hipLaunchKernelGGL(kz, dim3((unsigned)grid), dim3(256), SA::LDS, s, dz);
     DSMP_LAUNCHED(h, "dz (aggregate form)");
+    }
   } else if (dz.E > 0) {
     using S = DzShape<T, DL, H1, H2>;
     auto kz = k_bwd_dz<T, DL, H1, H2>;
@@ -2192,14 +2446,14 @@ dsmp_status launch_dw1_tr(dsmp_handle* h, int n1, int64_t E, int64_t pc1, const 
 }
 
 dsmp_status dispatch_edge_grads(dsmp_handle* h, const dsmp_layer_desc& d, const DzArgs& dz, const W3Args& w3,
-                                const W2Args& w2) {
+                                const W2Args& w2, const DzDhuArgs* fm) {
   if (d.dtype == DSMP_F32) {
-    if (d.d == 32) return run_edge_grads<float, 32, 64, 64>(h, dz, w3, w2);
-    if (d.d == 64) return run_edge_grads<float, 64, 128, 128>(h, dz, w3, w2);
+    if (d.d == 32) return run_edge_grads<float, 32, 64, 64>(h, dz, w3, w2, fm);
+    if (d.d == 64) return run_edge_grads<float, 64, 128, 128>(h, dz, w3, w2, fm);
   } else {
-    if (d.d == 32) return run_edge_grads<__bf16, 32, 64, 64>(h, dz, w3, w2);
-    if (d.d == 64) return run_edge_grads<__bf16, 64, 128, 128>(h, dz, w3, w2);
-    if (d.d == 128) return run_edge_grads<__bf16, 128, 256, 256>(h, dz, w3, w2);
+    if (d.d == 32) return run_edge_grads<__bf16, 32, 64, 64>(h, dz, w3, w2, fm);
+    if (d.d == 64) return run_edge_grads<__bf16, 64, 128, 128>(h, dz, w3, w2, fm);
+    if (d.d == 128) return run_edge_grads<__bf16, 128, 256, 256>(h, dz, w3, w2, fm);
   }
   return fail(h, DSMP_UNSUPPORTED, "unsupported layer shape");
 }
@@ -2333,7 +2587,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   ea.zE = const_cast<unsigned char*>(sv + sl.zE);
   ea.z1E = nullptr;
   ea.out_direct = w.dh_direct; ea.out_part = w.dh_part;
-  const bool dhu = dh_from_u(d, agg);
+  const bool dhu = dh_from_u(d, agg), dzm = dz_with_m(d, agg);
   if (dhu) {
     // after the kernel-MLP gradients, from U (below)
   } else if (agg) {
@@ -2372,7 +2626,9 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
               agg ? w.U : nullptr, w.gT, n_dst, g->row_ptr};
     W3Args w3{E, w.pc3, agg ? 0 : w.n3, g->col, g->dst, hin, w.gF, sv + sl.zE, w.p_w3};
     W2Args w2{E, w.pc2, 1, w.da2E, sv + sl.z1E, w.p_w2};
-    if ((st = dispatch_edge_grads(h, d, dz, w3, w2)) != DSMP_OK) return st;
+    DzDhuArgs fm{DhuArgs{n_dst, g->row_ptr, w.U, w.gT, pk + L.b3n, sv + sl.zE, w.mE}, g->col, hin, sv + sl.zmask,
+                 w.da2E};
+    if ((st = dispatch_edge_grads(h, d, dz, w3, w2, dzm ? &fm : nullptr)) != DSMP_OK) return st;
     int n1 = (int)((E + w.pc1 - 1) / w.pc1);
     ProfScope prof(h, DSMP_K_DW1);
     const __bf16* da1b = reinterpret_cast<const __bf16*>(w.da1E);
@@ -2394,7 +2650,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   }
 
   if (dhu) {
-    if (E > 0) {
+    if (E > 0 && !dzm) {
       ProfScope prof(h, DSMP_K_DH_U);
       DhuArgs da{n_dst, g->row_ptr, w.U, w.gT, pk + L.b3n, sv + sl.zE, w.mE};
       if ((st = dispatch_dh_u(h, d, da)) != DSMP_OK) return st;

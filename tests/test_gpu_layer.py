@@ -143,6 +143,8 @@ FWD_CASES = {
     "bf16_64_2d": dict(shape="bf16_64"),
     "bf16_64_3d_knn": dict(shape="bf16_64", D=3, cap=12),
     "bf16_128_3d": dict(shape="bf16_128", D=3, cap=24, n=700),
+    "bf16_128_3d_high_degree": dict(shape="bf16_128", D=3, n=300, r=0.35),
+    "bf16_128_halo_isolated": dict(shape="bf16_128", D=3, n=600, n_dst=450, r=0.07),
     "bf16_64_relu_nores": dict(shape="bf16_64", act=1, residual=0),
     "bf16_64_diff_attr": dict(shape="bf16_64", attr_mode=1),
     "f32_32_halo": dict(shape="f32_32", n=1000, n_dst=700),
