@@ -511,12 +511,20 @@ def main():
     fused = agg and not ("dW2" in prof and prof["dW2"][1] > 0)
     if infer:   # no backward ran: the forward's stores follow the shape's backward
         fused = agg and w.dtype == "bf16" and w.H1 == w.H2 and w.H1 in (64, 128)
-    if infer:   # every box is a graph of its own: the layer runs over all their nodes
+    if infer:
+        # every box is a graph of its own and each layer launch runs over one
+        # box: a launch's work is the boxes' total over the number of boxes
+        # (time and work are then both averages over the boxes)
+        import dataclasses
         n_box = sum(st[1] for st in pipe.inf.stats)
-        work = work_model(w, E, n_box, fused, n_dst=n_box)
+        nb = sum(1 for st in pipe.inf.stats if st[1] > 0)
+        wb = dataclasses.replace(w, n_dst=n_box, n_src=n_box)
+        work = work_model(wb, E, n_box, fused, n_dst=n_box)
+        work.update(agg_work(wb, E, n_box, fused) if agg else per_edge_work(wb, E, n_box))
+        work = {k: (fl / nb, by / nb) for k, (fl, by) in work.items()}
     else:
         work = work_model(w, E, w.n_src, fused)
-    work.update(agg_work(w, E, w.n_src, fused) if agg else per_edge_work(w, E, w.n_src))
+        work.update(agg_work(w, E, w.n_src, fused) if agg else per_edge_work(w, E, w.n_src))
     for name, (fl, by) in prep_work_step(w, E).items():
         if name in prof and prof[name][1] > 0:
             nper = prof[name][1] / args.steps
@@ -567,13 +575,15 @@ def main():
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic (seeded stand-in for the paper's mesh datasets)",
         "config": {"workload": "%s: %d nodes sampled from %d candidates%s, radius %.3g, cap %s, d=%d, kernel MLP "
-                               "%d->%d->%d->%d, %d %s, sample+graph+forward+backward per step"
+                               "%d->%d->%d->%d, %d %s, %s per step"
                                % (w.name, w.n_dst, sum(p.pos.shape[0] for p in w.parts),
                                   " (plus %d halo nodes)" % (w.n_src - w.n_dst) if w.n_src > w.n_dst else "",
                                   w.r, w.cap or "none",
                                   w.d, w.de, w.H1, w.H2, w.d * w.d, L,
-                                  "hops (encoder and decoder 64 wide, difference attributes)" if hop else "layers")
-                   + (" (inference: %d random boxes with overlap r, forward only)" % len(pipe.boxes) if infer else ""),
+                                  "hops (encoder and decoder 64 wide, difference attributes)" if hop else "layers",
+                                  "sample, then for each of %d random boxes with overlap r: select, gather, "
+                                  "graph, forward, scatter" % len(pipe.boxes) if infer
+                                  else "sample+graph+forward+backward"),
                    "n_dst": w.n_dst, "n_src": w.n_src, "edges": E, "layers": L, "d": w.d, "h1": w.H1,
                    "h2": w.H2, "nominal_flops_per_edge_layer": method_flops_per_edge(w)},
         "edge_algorithm": "aggregate" if agg else "per_edge",
