@@ -199,6 +199,7 @@ struct DzArgs {
   const unsigned char* gT;     // aggregate form: g_i [n_dst][d] layer dtype
   int64_t n_dst;
   const int32_t* row_ptr;      // aggregate form: edges of each destination
+  int nb;                      // k_bwd_dz_agg: destinations per block, 1 .. DZ_NB (0: DZ_NB)
 };
 
 template <typename T, int DL, int H1, int H2>
@@ -432,10 +433,11 @@ __global__ __launch_bounds__(256, (DL <= 64 && H2 * sizeof(T) <= 256) ? 3 : 1) v
     __syncthreads();
   }
   __shared__ int tstart[DZ_NB + 1];   // first tile of each destination of the block
-  const int64_t nblk = (a.n_dst + DZ_NB - 1) / DZ_NB;
+  const int NB = a.nb > 0 && a.nb < DZ_NB ? a.nb : DZ_NB;
+  const int64_t nblk = (a.n_dst + NB - 1) / NB;
   for (int64_t blk = blockIdx.x; blk < nblk; blk += gridDim.x) {
-    const int64_t d0 = blk * DZ_NB;
-    const int nd = (int)(a.n_dst - d0 < DZ_NB ? a.n_dst - d0 : DZ_NB);
+    const int64_t d0 = blk * NB;
+    const int nd = (int)(a.n_dst - d0 < NB ? a.n_dst - d0 : NB);
     if (wv == 0) {
       // tiles per destination, inclusive prefix over the block's lanes
       int nt = 0;
@@ -2320,11 +2322,14 @@ BwdWs carve_bwd(const dsmp_layer_desc& d, int64_t n_dst, int64_t n_src, int64_t 
   const size_t p3e = (size_t)w.n3 * d.d * d.d * d.h2;
   const size_t p3a = (size_t)agg_dw3_slices(n_dst) * d.d * agg_ktot(d);
   w.p_w3 = c.take<float>(p3e > p3a ? p3e : p3a);
-  w.n2 = (int)(E > 0 ? (ceil_div(E, 1024) < 512 ? ceil_div(E, 1024) : 512) : 1);
+  // edge chunks of the dW2 and dW1 partial sums: 64 edges or more each, at
+  // most 512 (dW2) and 2048 (dW1) chunks, so that small graphs still spread
+  // over the CUs
+  w.n2 = (int)(E > 0 ? (ceil_div(E, 64) < 512 ? ceil_div(E, 64) : 512) : 1);
   w.pc2 = ((E + w.n2 - 1) / w.n2 + 63) / 64 * 64;
   if (w.pc2 < 64) w.pc2 = 64;
   w.p_w2 = c.take<float>((size_t)w.n2 * (d.h2 * d.h1 + d.h2));
-  w.n1 = (int)(E > 0 ? (ceil_div(E, 512) < 2048 ? ceil_div(E, 512) : 2048) : 1);
+  w.n1 = (int)(E > 0 ? (ceil_div(E, 64) < 2048 ? ceil_div(E, 64) : 2048) : 1);
   w.pc1 = E > 0 ? (E + w.n1 - 1) / w.n1 : 1;
   w.p_w1 = c.take<float>((size_t)w.n1 * (d.h1 * de + d.h1));
   w.total = c.used();
@@ -2385,9 +2390,13 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
     if ((st = set_lds(h, kz, SA::LDS)) != DSMP_OK) return st;
     int per_cu = 0;
     DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kz, 256, SA::LDS));
-    const int64_t grid = std::min<int64_t>(ceil_div(dz.n_dst, 4), (int64_t)h->n_cu * std::max(per_cu, 1));
+    // blocks of up to DZ_NB destinations, smaller where that leaves CUs idle
+    const int64_t slots = (int64_t)h->n_cu * std::max(per_cu, 1);
+    DzArgs da = dz;
+    da.nb = (int)std::max<int64_t>(1, std::min<int64_t>(DZ_NB, ceil_div(dz.n_dst, slots)));
+    const int64_t grid = std::min<int64_t>(ceil_div(dz.n_dst, da.nb), slots);
     ProfScope prof(h, DSMP_K_DZ);
-    hipLaunchKernelGGL(kz, dim3((unsigned)grid), dim3(256), SA::LDS, s, dz);
+    hipLaunchKernelGGL(kz, dim3((unsigned)grid), dim3(256), SA::LDS, s, da);
     DSMP_LAUNCHED(h, "dz (aggregate form)");
     }
   } else if (dz.E > 0) {
