@@ -181,8 +181,10 @@ def agg_work(w, E, n_src, fused=False):
         "dW3": (2 * n * kt * d, n * kt * esz + n * d * esz),
     }
     if dz_m:
-        # da1 = [z1 > 0] W2^T da2 from the stored da2 rows
-        out["da1"] = (2 * E * H1 * H2, E * (H2 * esz + H1 // 8 + H1 * esz))
+        # da1 = [z1 > 0] W2^T da2 from the stored da2 rows and the dW1/db1 sums
+        # from it (x as bf16 high and low parts, 32 bytes per edge); da1 itself
+        # stays on chip
+        out["da1"] = (2 * E * H1 * H2 + 2 * E * H1 * (2 * de + 1), E * (H2 * esz + H1 // 8 + 32))
     if w.dtype == "bf16":
         # the feature gradient from U: per-edge terms from U_i, z_e and the bias
         # row, then their sums over the edges leaving each source

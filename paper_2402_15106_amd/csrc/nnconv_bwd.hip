@@ -39,6 +39,16 @@ __device__ __forceinline__ typename MT<T>::frag ld_frag(const void* p) {
   return *reinterpret_cast<const typename MT<T>::frag*>(p);
 }
 
+// A fragment that is zero where !valid.  The load itself is unconditional (p
+// must be readable either way): a load under a condition compiles to a branch
+// around it, and past such joins the compiler's wait counts fall back to
+// waiting for every outstanding load, the loads issued ahead included.
+template <typename T>
+__device__ __forceinline__ typename MT<T>::frag ld_frag_if(const void* p, bool valid) {
+  const typename MT<T>::frag v = ld_frag<T>(p);
+  return valid ? v : typename MT<T>::frag{};
+}
+
 __device__ __forceinline__ float to_f(__bf16 x) { return (float)x; }
 __device__ __forceinline__ float to_f(float x) { return x; }
 
@@ -2041,7 +2051,10 @@ __global__ __launch_bounds__(256) void k_dz_dh_u(DzDhuArgs a) {
   constexpr int SKD = DL / 16, SK2 = H2 / 16, PT = DL / 32, KT = H2 / 32, KTW = KT / 4;
   constexpr int MW1 = H1 / 64, MW2 = H2 / 64, MROW = (H1 + H2) / 8;
   static_assert(PT == 4 && KTW == 2, "one column tile of p and two neuron tiles per wave");
-  extern __shared__ __align__(16) unsigned char X[];
+  // two statically distinct buffers: the compiler can then see that the
+  // copies into one never alias the reads of the other, and does not wait
+  // for the copies before every LDS read
+  __shared__ __align__(16) unsigned char XA[S::BUF], XB[S::BUF];
   const DhuArgs& d = a.m;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
   bf16x8 ba[SKD];
@@ -2060,15 +2073,12 @@ __global__ __launch_bounds__(256) void k_dz_dh_u(DzDhuArgs a) {
     const size_t es = valid ? (size_t)e : 0;
     const unsigned char* zr = d.zE + es * H2 * 2;
 #pragma unroll
-    for (int s2 = 0; s2 < SK2; ++s2) o.z[s2] = valid ? ld_frag<__bf16>(zr + (16 * s2 + 8 * hh) * 2) : bf16x8{};
+    for (int s2 = 0; s2 < SK2; ++s2) o.z[s2] = ld_frag_if<__bf16>(zr + (16 * s2 + 8 * hh) * 2, valid);
     const unsigned char* hr = a.h_in + (size_t)(valid ? c : 0) * DL * 2;
 #pragma unroll
-    for (int s = 0; s < SKD; ++s) o.h[s] = valid ? ld_frag<__bf16>(hr + (16 * s + 8 * hh) * 2) : bf16x8{};
-    o.mw = valid ? reinterpret_cast<const uint32_t*>(a.zmask + es * MROW)[2 * MW1 + hh * MW2 + wv] : 0u;
-  };
-  auto first_col = [&](int64_t i) -> int32_t {
-    const int64_t q = d.row_ptr[i] + l32;
-    return q < d.row_ptr[i + 1] ? a.col[q] : 0;
+    for (int s = 0; s < SKD; ++s) o.h[s] = ld_frag_if<__bf16>(hr + (16 * s + 8 * hh) * 2, valid);
+    const uint32_t w = reinterpret_cast<const uint32_t*>(a.zmask + es * MROW)[2 * MW1 + hh * MW2 + wv];
+    o.mw = valid ? w : 0u;
   };
   auto item = [&](const unsigned char* Xb, int64_t pa, int64_t pb, int et, const Ops& o) {
     const int64_t e = pa + (int64_t)et * 32 + l32;
@@ -2108,119 +2118,218 @@ __global__ __launch_bounds__(256) void k_dz_dh_u(DzDhuArgs a) {
       }
     }
   };
-  int64_t i = blockIdx.x;
-  if (i >= d.n_dst) return;
-  const int64_t G = gridDim.x;
-  int64_t pa = d.row_ptr[i], pb = d.row_ptr[i + 1];
-  Ops ops;
-  lds_copy_async(d.U + (size_t)i * S::UB, X, S::UB / 16);
-  lds_copy_async(d.gT + (size_t)i * S::GB, X + S::UB, S::GB / 16);
-  load_ops(pa, pb, 0, first_col(i), ops);
-  // source of the lane's edge in the first tile of the next destination,
-  // loaded a destination ahead of its h row
-  int32_t cnext = i + G < d.n_dst ? first_col(i + G) : 0;
-  static_assert(SK2 + SKD + 1 < 64, "wait count");
-  for (int buf = 0; i < d.n_dst; i += G, buf ^= 1) {
-    // the copies of U_i and g_i were followed by the SK2 + SKD + 1 operand
-    // loads of the destination's first tile (issued whenever it has an edge,
-    // the only case that reads the copy): once no more than those are
-    // outstanding, the copies are in
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(SK2 + SKD + 1));
-    __syncthreads();   // U_i, g_i in buffer buf; every wave is done with buffer buf ^ 1
-    const unsigned char* Xb = X + buf * S::BUF;
-    const int64_t inext = i + G;
-    int64_t pa2 = 0, pb2 = 0;
-    int32_t cnn = 0;
-    Ops on;
-    if (inext < d.n_dst) {
-      unsigned char* Xn = X + (buf ^ 1) * S::BUF;
+  const int64_t i0 = blockIdx.x, G = gridDim.x;
+  if (i0 >= d.n_dst) return;
+  // Loads and stores retire through one in-order counter, so waiting for a
+  // load also waits for everything issued before it.  Per destination i the
+  // order is: the index loads (edge range of i + 3G, first-tile sources of
+  // i + 2G), the operand loads of i + G, then the copies of U and g of
+  // i + G, then the products of i.  The operand registers are handed on at the
+  // end of the step, which waits for those loads but not for the copies
+  // behind them; the next step waits for everything (the copies) before its
+  // barrier.  Index values are used one step after their loads.
+  // edge range of a destination: scalar loads (row_ptr is not written while
+  // the kernel runs), which count apart from the vector loads and copies
+  typedef __attribute__((address_space(4))) const int32_t cint32_t;
+  cint32_t* rp = (cint32_t*)(d.row_ptr);
+  auto rows = [&](int64_t i, int64_t& p0, int64_t& p1) {
+    const int64_t ic = i < d.n_dst ? i : d.n_dst;
+    p0 = rp[ic];
+    p1 = i < d.n_dst ? (int64_t)rp[ic + 1] : p0;
+  };
+  // source of the lane's edge in the first tile of edges [p0, p1) (0 past
+  // them; the load is unconditional, of edge 0 there)
+  auto first_col = [&](int64_t p0, int64_t p1) -> int32_t {
+    const int64_t q = p0 + l32;
+    const bool valid = q < p1;
+    const int32_t c = a.col[valid ? q : 0];
+    return valid ? c : 0;
+  };
+  int64_t pa, pb, pa1, pb1, pa2, pb2;
+  rows(i0, pa, pb);
+  rows(i0 + G, pa1, pb1);
+  rows(i0 + 2 * G, pa2, pb2);
+  Ops opsA, opsB;
+  load_ops(pa, pb, 0, first_col(pa, pb), opsA);
+  int32_t c1 = first_col(pa1, pb1);
+  lds_copy_async(d.U + (size_t)i0 * S::UB, XA, S::UB / 16);
+  lds_copy_async(d.gT + (size_t)i0 * S::GB, XA + S::UB, S::GB / 16);
+  // one destination: its U_i and g_i in Xc (copied one step earlier), its
+  // operands in cur; the next destination's copies go to Xn, its operands to
+  // nxt.  The loop alternates the two (buffers, operand sets) in code, so no
+  // buffer is chosen at run time and no operand set is copied.
+  auto step = [&](int64_t i, const unsigned char* Xc, unsigned char* Xn, const Ops& cur, Ops& nxt) {
+    stage_wait();      // the copies of U_i and g_i (and every store before them)
+    __syncthreads();   // U_i, g_i in Xc; every wave is done with Xn
+    int64_t pa3, pb3;
+    rows(i + 3 * G, pa3, pb3);
+    const int32_t c2 = first_col(pa2, pb2);
+    load_ops(pa1, pb1, 0, c1, nxt);
+    {
+      // unconditional (the last step copies its own U_i again): the count of
+      // operations after the operand loads then includes these copies
+      const int64_t inext = i + G < d.n_dst ? i + G : i;
       lds_copy_async(d.U + (size_t)inext * S::UB, Xn, S::UB / 16);
       lds_copy_async(d.gT + (size_t)inext * S::GB, Xn + S::UB, S::GB / 16);
-      pa2 = d.row_ptr[inext];
-      pb2 = d.row_ptr[inext + 1];
-      load_ops(pa2, pb2, 0, cnext, on);
-      if (inext + G < d.n_dst) cnn = first_col(inext + G);
     }
     const int net = (int)((pb - pa + 31) / 32);
-    if (net > 0) item(Xb, pa, pb, 0, ops);
+    if (net > 0) item(Xc, pa, pb, 0, cur);
     for (int et = 1; et < net; ++et) {   // destinations of more than 32 edges
       const int64_t e = pa + (int64_t)et * 32 + l32;
+      const bool valid = e < pb;
+      const int32_t c = a.col[valid ? e : pa];
       Ops ox;
-      load_ops(pa, pb, et, e < pb ? a.col[e] : 0, ox);
-      item(Xb, pa, pb, et, ox);
+      load_ops(pa, pb, et, valid ? c : 0, ox);
+      item(Xc, pa, pb, et, ox);
     }
-    ops = on;
-    pa = pa2;
-    pb = pb2;
-    cnext = cnn;
+    pa = pa1; pb = pb1;
+    pa1 = pa2; pb1 = pb2;
+    pa2 = pa3; pb2 = pb3;
+    c1 = c2;
+  };
+  for (int64_t i = i0;;) {
+    step(i, XA, XB, opsA, opsB);
+    if ((i += G) >= d.n_dst) break;
+    step(i, XB, XA, opsB, opsA);
+    if ((i += G) >= d.n_dst) break;
   }
 }
 
 // dz1 = W2^T da2 and da1 = dz1 * [z1 > 0] for 32-edge tiles of the stored da2
-// rows (the second half of the dz epilogue, in the same products and order).
-// W2^T is staged in LDS once per workgroup; each wave takes every
-// (4 x grid)-th tile, the next tile's da2 rows and mask words loaded while the
-// current one is multiplied.
+// rows (the second half of the dz epilogue, in the same products and order),
+// and the layer-1 weight gradients from them in the same pass:
+//   dW1[j][c] = sum_e da1_e[j] x_e[c],  db1[j] = sum_e da1_e[j],
+// with x as its bf16 high parts (columns 0..7) and low parts (8..15) next to
+// a column of ones (16), as the unfused dW1 product takes it.  W2^T is staged
+// in LDS once per workgroup; each wave takes every (4 x grid)-th tile, the
+// next tile's da2 rows, mask words and attribute rows loaded while the current
+// one is multiplied.  Each 32 x 32 block of da1 goes through a small LDS tile
+// of the wave ([edge][stored position]) so that the dW1 product can read it
+// with transposing reads (edges are its contraction index); the wave keeps its
+// dW1 sums in registers over all its tiles and writes them to partial slot
+// 4 blockIdx.x + w.  da1 goes to HBM only when the attribute gradient needs it.
+struct Da1Args {
+  int64_t E;
+  const unsigned char* w2t;     // packed W2^T rows [h1][h2 stored positions] bf16
+  const unsigned char* zmask;   // [E][(h1+h2)/8]
+  const unsigned char* da2E;    // [E][h2] bf16, stored positions
+  const unsigned char* xE;      // [E][32 bytes]: bf16 high parts 0..7, low parts 8..15
+  int de;
+  unsigned char* da1E;          // [E][h1] bf16 out, or null
+  float* p_w1;                  // [4 grid][h1*de + h1] partial sums
+};
+
 template <int H1, int H2>
-__global__ __launch_bounds__(256) void k_da1(int64_t E, const unsigned char* __restrict__ w2t,
-                                             const unsigned char* __restrict__ zmask,
-                                             const unsigned char* __restrict__ da2E, unsigned char* __restrict__ da1E) {
+struct Da1Shape {
+  static constexpr int W2B = H1 * DzAggShape<__bf16, H1, H2>::W2P;
+  static constexpr int TP = 64;                // pitch of the wave's da1 and attribute tiles (bytes)
+  static constexpr int WT = 3 * 32 * TP;       // per wave: two da1 tiles, the attribute tile
+  static constexpr int LDS = W2B + 4 * WT;
+  static_assert(LDS <= 160 * 1024, "LDS of the da1 pass");
+};
+
+template <int H1, int H2>
+__global__ __launch_bounds__(256) void k_da1_dw1(Da1Args a) {
   using SA = DzAggShape<__bf16, H1, H2>;
+  using S = Da1Shape<H1, H2>;
   using M = MT<__bf16>;
-  constexpr int SK2 = H2 / 16, JT = H1 / 32, MW1 = H1 / 64, MROW = (H1 + H2) / 8;
+  constexpr int SK2 = H2 / 16, JT = H1 / 32, MW1 = H1 / 64, MROW = (H1 + H2) / 8, TP = S::TP;
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  unsigned char* dtile = smem + S::W2B + wv * S::WT;
+  unsigned char* xtile = dtile + 2 * 32 * TP;
   {
     LdsStage<H1, H2 * 2> stg;
     stg.init();
-    stg.issue(w2t, smem);
+    stg.issue(a.w2t, smem);
+    // columns 16..31 of the attribute tile: a one in column 16, zeros after it
+    const float one[8] = {hh ? 0.0f : 1.0f, 0, 0, 0, 0, 0, 0, 0};
+    *reinterpret_cast<bf16x8*>(xtile + l32 * TP + 32 + 16 * hh) = pack_frag<__bf16>(one);
     stage_wait();
     __syncthreads();
   }
-  const int64_t ntile = (E + 31) / 32, stride = (int64_t)gridDim.x * 4;
-  auto load = [&](int64_t t, bf16x8 (&B)[SK2], uint32_t (&m1)[MW1]) {
+  const int64_t ntile = (a.E + 31) / 32, stride = (int64_t)gridDim.x * 4;
+  struct Ops {
+    bf16x8 B[SK2];
+    uint32_t m1[MW1];
+    uint4 x;   // bytes 16 hh .. + 15 of the lane's edge's attribute row
+  };
+  auto load = [&](int64_t t, Ops& o) {
     const int64_t e = t * 32 + l32;
-    const bool valid = t < ntile && e < E;
+    const bool valid = t < ntile && e < a.E;
     const size_t es = valid ? (size_t)e : 0;
 #pragma unroll
     for (int s = 0; s < SK2; ++s)
-      B[s] = valid ? ld_frag<__bf16>(da2E + (es * H2 + 16 * s + 8 * hh) * 2) : bf16x8{};
-    const uint32_t* mb = reinterpret_cast<const uint32_t*>(zmask + es * MROW);
+      o.B[s] = valid ? ld_frag<__bf16>(a.da2E + (es * H2 + 16 * s + 8 * hh) * 2) : bf16x8{};
+    const uint32_t* mb = reinterpret_cast<const uint32_t*>(a.zmask + es * MROW);
 #pragma unroll
-    for (int w = 0; w < MW1; ++w) m1[w] = valid ? mb[hh * MW1 + w] : 0u;
+    for (int w = 0; w < MW1; ++w) o.m1[w] = valid ? mb[hh * MW1 + w] : 0u;
+    o.x = valid ? *reinterpret_cast<const uint4*>(a.xE + es * 32 + 16 * hh) : make_uint4(0, 0, 0, 0);
   };
-  int64_t t = (int64_t)blockIdx.x * 4 + wv;
-  bf16x8 B[SK2];
-  uint32_t m1[MW1];
-  load(t, B, m1);
-  for (; t < ntile; t += stride) {
-    bf16x8 Bn[SK2];
-    uint32_t m1n[MW1];
-    load(t + stride, Bn, m1n);
-    const int64_t e = t * 32 + l32;
+  f32x16 acc1[JT];
 #pragma unroll
-    for (int jt = 0; jt < JT; ++jt) {
+  for (int jt = 0; jt < JT; ++jt) acc1[jt] = f32x16{};
+  int64_t t = (int64_t)blockIdx.x * 4 + wv;
+  Ops o, on;
+  load(t, o);
+  load(t + stride, on);
+  for (; t < ntile; t += stride) {
+    // loads run two tiles ahead: one tile's products do not cover their latency
+    Ops onn;
+    load(t + 2 * stride, onn);
+    const int64_t e = t * 32 + l32;
+    *reinterpret_cast<uint4*>(xtile + l32 * TP + 16 * hh) = o.x;
+    const bf16x8 X0 = lds_frag_rows(xtile, TP, 0, 0), X1 = lds_frag_rows(xtile, TP, 16, 0);
+    // two blocks of dz1 at a time, so that two accumulation chains interleave
+#pragma unroll
+    for (int jp = 0; jp < JT; jp += 2) {
       __builtin_amdgcn_sched_barrier(0);
-      f32x16 C = f32x16{};
+      f32x16 C[2] = {f32x16{}, f32x16{}};
 #pragma unroll
       for (int s = 0; s < SK2; ++s) {
-        const bf16x8 A = *reinterpret_cast<const bf16x8*>(smem + (jt * 32 + l32) * SA::W2P + (16 * s + 8 * hh) * 2);
-        C = M::mma(A, B[s], C);
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const bf16x8 A =
+              *reinterpret_cast<const bf16x8*>(smem + ((jp + q) * 32 + l32) * SA::W2P + (16 * s + 8 * hh) * 2);
+          C[q] = M::mma(A, o.B[s], C[q]);
+        }
       }
-      // register i of tile jt is stored position 16 (2 jt + i / 8) + 8 hh + i % 8
 #pragma unroll
-      for (int i = 0; i < 16; i += 8) {
-        const int n = 16 * jt + i;
-        float v[8];
+      for (int q = 0; q < 2; ++q) {
+        const int jt = jp + q;
+        unsigned char* dt = dtile + q * 32 * TP;
+        // register i of block jt is stored position 16 (2 jt + i / 8) + 8 hh + i % 8
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = keep_if_bit(C[i + u], m1[(n + u) / 32], (n + u) % 32);
-        if (e < E) *reinterpret_cast<bf16x8*>(da1E + ((size_t)e * H1 + (n / 8) * 16 + 8 * hh) * 2) = pack_frag<__bf16>(v);
+        for (int i = 0; i < 16; i += 8) {
+          const int n = 16 * jt + i;
+          float v[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) v[u] = keep_if_bit(C[q][i + u], o.m1[(n + u) / 32], (n + u) % 32);
+          const bf16x8 f = pack_frag<__bf16>(v);
+          if (a.da1E && e < a.E)
+            *reinterpret_cast<bf16x8*>(a.da1E + ((size_t)e * H1 + (n / 8) * 16 + 8 * hh) * 2) = f;
+          *reinterpret_cast<bf16x8*>(dt + l32 * TP + (16 * (i / 8) + 8 * hh) * 2) = f;
+        }
+        // dW1 rows of this block: A = da1 [position][edge], B = the attribute columns
+        acc1[jt] = M::mma(lds_frag_rows(dt, TP, 0, 0), X0, acc1[jt]);
+        acc1[jt] = M::mma(lds_frag_rows(dt, TP, 16, 0), X1, acc1[jt]);
       }
     }
+    o = on;
+    on = onn;
+  }
+  // column c of a block holds the high-part sums, column c + 8 the low-part
+  // sums, column 16 the row sums (db1)
+  float* out = a.p_w1 + (size_t)(blockIdx.x * 4 + wv) * (H1 * a.de + H1);
 #pragma unroll
-    for (int s = 0; s < SK2; ++s) B[s] = Bn[s];
+  for (int jt = 0; jt < JT; ++jt) {
 #pragma unroll
-    for (int w = 0; w < MW1; ++w) m1[w] = m1n[w];
+    for (int i = 0; i < 16; ++i) {
+      const float lo = __shfl_down(acc1[jt][i], 8, 64);
+      const int j = kperm<__bf16>(jt * 32 + 8 * (i / 4) + 4 * hh + (i % 4));
+      if (l32 < a.de) out[(size_t)j * a.de + l32] = acc1[jt][i] + lo;
+      if (l32 == 16) out[(size_t)H1 * a.de + j] = acc1[jt][i];
+    }
   }
 }
 
@@ -2345,7 +2454,7 @@ dsmp_status set_lds(dsmp_handle* h, K kernel, int bytes) {
 
 template <typename T, int DL, int H1, int H2>
 dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, const W2Args& w2,
-                           const DzDhuArgs* fm) {
+                           const DzDhuArgs* fm, Da1Args* fa, int n1cap, int* n1_used) {
   hipStream_t s = h->stream;
   dsmp_status st;
   if (dz.E > 0 && dz.U) {
@@ -2359,27 +2468,27 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
       if constexpr (sizeof(T) == 2 && DL == 128 && H1 == 256 && H2 == 256) {
         {
           // dz (masked into da2) and the feature-gradient terms from one read of U
-          using S = DzDhuShape<DL, H1, H2>;
-          auto kf = k_dz_dh_u<DL, H1, H2>;
-          if ((st = set_lds(h, kf, S::LDS)) != DSMP_OK) return st;
+          auto kf = k_dz_dh_u<DL, H1, H2>;   // static LDS: two U_i + g_i buffers
           int per_cu = 0;
-          DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kf, 256, S::LDS));
+          DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kf, 256, 0));
           const int64_t grid = std::min<int64_t>(dz.n_dst, (int64_t)h->n_cu * std::max(per_cu, 1));
           ProfScope prof(h, DSMP_K_DZ);
-          if (grid > 0) hipLaunchKernelGGL(kf, dim3((unsigned)grid), dim3(256), S::LDS, s, *fm);
+          if (grid > 0) hipLaunchKernelGGL(kf, dim3((unsigned)grid), dim3(256), 0, s, *fm);
           DSMP_LAUNCHED(h, "dz and feature-gradient terms from U");
         }
         {
-          using SA = DzAggShape<T, H1, H2>;
-          auto ka = k_da1<H1, H2>;
-          if ((st = set_lds(h, ka, SA::LDS)) != DSMP_OK) return st;
+          // da1 and the dW1/db1 partial sums (four per workgroup, at most n1cap)
+          using SD = Da1Shape<H1, H2>;
+          auto ka = k_da1_dw1<H1, H2>;
+          if ((st = set_lds(h, ka, SD::LDS)) != DSMP_OK) return st;
           int per_cu = 0;
-          DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ka, 256, SA::LDS));
-          const int64_t grid = std::min<int64_t>(ceil_div(ceil_div(dz.E, 32), 4), (int64_t)h->n_cu * std::max(per_cu, 1));
+          DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ka, 256, SD::LDS));
+          int64_t grid = std::min<int64_t>(ceil_div(ceil_div(dz.E, 32), 4), (int64_t)h->n_cu * std::max(per_cu, 1));
+          grid = std::max<int64_t>(1, std::min<int64_t>(grid, n1cap / 4));
           ProfScope prof(h, DSMP_K_DA1);
-          hipLaunchKernelGGL(ka, dim3((unsigned)grid), dim3(256), SA::LDS, s, dz.E, dz.packed + dz.L.w2t, dz.zmask,
-                             dz.da2E, dz.da1E);
-          DSMP_LAUNCHED(h, "da1 from da2");
+          hipLaunchKernelGGL(ka, dim3((unsigned)grid), dim3(256), SD::LDS, s, *fa);
+          DSMP_LAUNCHED(h, "da1 and dW1 from da2");
+          *n1_used = (int)(4 * grid);
         }
       } else {
         return fail(h, DSMP_UNSUPPORTED, "dz with the feature-gradient terms is built for d = 128, h = 256 only");
@@ -2455,14 +2564,14 @@ dsmp_status launch_dw1_tr(dsmp_handle* h, int n1, int64_t E, int64_t pc1, const 
 }
 
 dsmp_status dispatch_edge_grads(dsmp_handle* h, const dsmp_layer_desc& d, const DzArgs& dz, const W3Args& w3,
-                                const W2Args& w2, const DzDhuArgs* fm) {
+                                const W2Args& w2, const DzDhuArgs* fm, Da1Args* fa, int n1cap, int* n1_used) {
   if (d.dtype == DSMP_F32) {
-    if (d.d == 32) return run_edge_grads<float, 32, 64, 64>(h, dz, w3, w2, fm);
-    if (d.d == 64) return run_edge_grads<float, 64, 128, 128>(h, dz, w3, w2, fm);
+    if (d.d == 32) return run_edge_grads<float, 32, 64, 64>(h, dz, w3, w2, fm, fa, n1cap, n1_used);
+    if (d.d == 64) return run_edge_grads<float, 64, 128, 128>(h, dz, w3, w2, fm, fa, n1cap, n1_used);
   } else {
-    if (d.d == 32) return run_edge_grads<__bf16, 32, 64, 64>(h, dz, w3, w2, fm);
-    if (d.d == 64) return run_edge_grads<__bf16, 64, 128, 128>(h, dz, w3, w2, fm);
-    if (d.d == 128) return run_edge_grads<__bf16, 128, 256, 256>(h, dz, w3, w2, fm);
+    if (d.d == 32) return run_edge_grads<__bf16, 32, 64, 64>(h, dz, w3, w2, fm, fa, n1cap, n1_used);
+    if (d.d == 64) return run_edge_grads<__bf16, 64, 128, 128>(h, dz, w3, w2, fm, fa, n1cap, n1_used);
+    if (d.d == 128) return run_edge_grads<__bf16, 128, 256, 256>(h, dz, w3, w2, fm, fa, n1cap, n1_used);
   }
   return fail(h, DSMP_UNSUPPORTED, "unsupported layer shape");
 }
@@ -2625,6 +2734,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
 
   // kernel-MLP gradients
   int nfused = 0;   // workgroups of the fused edge-gradient pass (their partials replace dW2's and dW1's)
+  int n1da = 0;     // dW1 partials of the da1 pass (dz_with_m)
   if (E > 0 && agg && fused_edge_grads(d)) {
     DzArgs dz{E, g->col, g->dst, hin, w.gF, pk, L, sv + sl.zE, sv + sl.zmask, w.da2E, w.da1E,
               w.U, w.gT, n_dst, g->row_ptr};
@@ -2637,10 +2747,11 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
     W2Args w2{E, w.pc2, 1, w.da2E, sv + sl.z1E, w.p_w2};
     DzDhuArgs fm{DhuArgs{n_dst, g->row_ptr, w.U, w.gT, pk + L.b3n, sv + sl.zE, w.mE}, g->col, hin, sv + sl.zmask,
                  w.da2E};
-    if ((st = dispatch_edge_grads(h, d, dz, w3, w2, dzm ? &fm : nullptr)) != DSMP_OK) return st;
+    Da1Args fa{E, pk + L.w2t, sv + sl.zmask, w.da2E, sv + sl.xE, de, grads->dattr ? w.da1E : nullptr, w.p_w1};
+    if ((st = dispatch_edge_grads(h, d, dz, w3, w2, dzm ? &fm : nullptr, &fa, w.n1, &n1da)) != DSMP_OK) return st;
+    if (!dzm) {   // with dz_with_m the da1 pass formed the dW1 partial sums
     int n1 = (int)((E + w.pc1 - 1) / w.pc1);
     ProfScope prof(h, DSMP_K_DW1);
-    const __bf16* da1b = reinterpret_cast<const __bf16*>(w.da1E);
     const float* da1f = reinterpret_cast<const float*>(w.da1E);
     if (d.dtype == DSMP_F32 && d.h1 == 64)
       hipLaunchKernelGGL((k_bwd_dW1<float, 64>), dim3(n1), dim3(256), 0, s, E, w.pc1, g->col, g->dst, node_attr,
@@ -2656,6 +2767,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
       st = launch_dw1_tr<256>(h, n1, E, w.pc1, w.da1E, sv + sl.xE, de, w.p_w1);
     if (st != DSMP_OK) return st;
     DSMP_LAUNCHED(h, "dW1");
+    }
   }
 
   if (dhu) {
@@ -2713,7 +2825,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
   const int64_t dd = (int64_t)d.d * d.d;
   const int n3 = E > 0 && !agg ? w.n3 : 0;
   const int n2 = nfused ? nfused : E > 0 ? (int)((E + w.pc2 - 1) / w.pc2) : 0;
-  const int n1 = nfused ? nfused : E > 0 ? (int)((E + w.pc1 - 1) / w.pc1) : 0;
+  const int n1 = nfused ? nfused : n1da ? n1da : E > 0 ? (int)((E + w.pc1 - 1) / w.pc1) : 0;
   const int nr = n_dst > 0 ? w.nr : 0;
   ProfScope prof_red(h, DSMP_K_REDUCE);
   red(w.p_root, nr, dd + d.d, 0, dd, grads->dWr);
