@@ -2254,17 +2254,20 @@ __global__ __launch_bounds__(256) void k_da1_dw1(Da1Args a) {
     uint32_t m1[MW1];
     uint4 x;   // bytes 16 hh .. + 15 of the lane's edge's attribute row
   };
-  auto load = [&](int64_t t, Ops& o) {
+  auto load = [&](int64_t t, Ops& o) {   // unconditional loads (row 0 past the edges), then zeroed
     const int64_t e = t * 32 + l32;
     const bool valid = t < ntile && e < a.E;
     const size_t es = valid ? (size_t)e : 0;
 #pragma unroll
-    for (int s = 0; s < SK2; ++s)
-      o.B[s] = valid ? ld_frag<__bf16>(a.da2E + (es * H2 + 16 * s + 8 * hh) * 2) : bf16x8{};
+    for (int s = 0; s < SK2; ++s) o.B[s] = ld_frag_if<__bf16>(a.da2E + (es * H2 + 16 * s + 8 * hh) * 2, valid);
     const uint32_t* mb = reinterpret_cast<const uint32_t*>(a.zmask + es * MROW);
 #pragma unroll
-    for (int w = 0; w < MW1; ++w) o.m1[w] = valid ? mb[hh * MW1 + w] : 0u;
-    o.x = valid ? *reinterpret_cast<const uint4*>(a.xE + es * 32 + 16 * hh) : make_uint4(0, 0, 0, 0);
+    for (int w = 0; w < MW1; ++w) {
+      const uint32_t m = mb[hh * MW1 + w];
+      o.m1[w] = valid ? m : 0u;
+    }
+    const uint4 x = *reinterpret_cast<const uint4*>(a.xE + es * 32 + 16 * hh);
+    o.x = valid ? x : make_uint4(0, 0, 0, 0);
   };
   f32x16 acc1[JT];
 #pragma unroll
