@@ -246,6 +246,20 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Workgroup barrier that waits for this wave's LDS instructions alone
+// (lgkmcnt): global loads, stores and global-to-LDS copies in flight stay in
+// flight, so a caller that reads copied data waits for those copies itself
+// (vmcnt) before it.  Even lds_barrier() waits for every outstanding vector
+// memory operation once global-to-LDS copies are in flight (its LDS fence
+// covers them), stores included.  The empty asm statements keep the compiler
+// from moving memory accesses across the barrier.
+__device__ __forceinline__ void lds_sync() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0); vmcnt and expcnt not waited for
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Pre-activation of the first kernel-MLP layer for one output: b1 + W1 x as
 // a chain of fused multiply-adds in attribute order (w: the 8 weights of the
 // output, zero past de).

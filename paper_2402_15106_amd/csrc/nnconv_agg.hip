@@ -582,6 +582,153 @@ __global__ __launch_bounds__(256) void k_dw3_agg_final(int d, int h2, int nsl, c
   }
 }
 
+// Persistent form of the outer-product sums for few workgroups per CU, with
+// the first chunk of the next segment copied while this segment's sums are
+// stored.  Loads and stores retire through one in-order counter, so a copy
+// issued after a segment's stores would wait for them; here the copy goes out
+// first, and the wait at the top of a segment leaves the previous segment's
+// stores in flight.  The index chain runs ahead: edge ids two segments ahead,
+// gathered-row ids one segment ahead, bounds by scalar loads.  Chunks after a
+// segment's first (segments of more than ECH edges) are copied and multiplied
+// in turn.  Barriers wait for LDS instructions only (lds_sync: a full
+// barrier would wait for the stores).  The products, their order and the stored layout are those of
+// k_outer_sum_tr.
+template <int DL, int H2, int NW>
+__global__ __launch_bounds__(64 * NW) void k_outer_sum_pf(OuterArgs a) {
+  using S = OuterTrShape<DL, H2>;
+  using M = MT<__bf16>;
+  constexpr int ECH = S::ECH, NT = 64 * NW, TPW = (S::NTILE + NW - 1) / NW;
+  static_assert(S::NTILE % NW == 0, "every wave holds TPW tiles");
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int rz[ECH], ru[ECH];   // source rows of the chunk's z and gathered rows
+  unsigned char* zl = smem;
+  unsigned char* ul = smem + ECH * S::ZP;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5;
+  const int64_t G = gridDim.x;
+  typedef __attribute__((address_space(4))) const int32_t cint32_t;
+  cint32_t* sp = (cint32_t*)(a.seg_ptr);
+  auto bounds = [&](int64_t n, int64_t& p0, int64_t& p1) {   // empty past the last segment
+    const int64_t nc = n < a.n_seg ? n : a.n_seg;
+    p0 = sp[nc];
+    p1 = n < a.n_seg ? (int64_t)sp[nc + 1] : p0;
+  };
+  // slot tid < ECH of a chunk takes the chunk's edge min(tid, cnt - 1)
+  auto slot_pos = [&](int64_t c0, int64_t end) {
+    const int cnt = (int)(end - c0 < ECH ? end - c0 : ECH);
+    return c0 + (tid < cnt ? tid : cnt - 1);
+  };
+  auto edge_of = [&](int64_t pos) -> int { return a.pos_eid ? a.pos_eid[pos] : (int)pos; };
+  auto copy_chunk = [&]() {
+    const int wbase = tid & ~63;
+    for (int U0 = 0; U0 < S::ZU; U0 += NT) {
+      const int U = U0 + tid, r = U / (S::ZNU + S::ZPAD), u = U % (S::ZNU + S::ZPAD);
+      if (U < S::ZU)
+        __builtin_amdgcn_global_load_lds(
+            (gbl_void_t*)(a.zE + (size_t)rz[r < ECH ? r : ECH - 1] * H2 * 2 + (u < S::ZNU ? u : 0) * 16),
+            (lds_void_t*)(zl + (size_t)(U0 + wbase) * 16), 16, 0, 0);
+    }
+    for (int U0 = 0; U0 < S::UU; U0 += NT) {
+      const int U = U0 + tid, r = U / (S::UNU + S::UPAD), u = U % (S::UNU + S::UPAD);
+      if (U < S::UU)
+        __builtin_amdgcn_global_load_lds(
+            (gbl_void_t*)(a.u + (size_t)ru[r < ECH ? r : ECH - 1] * DL * 2 + (u < S::UNU ? u : 0) * 16),
+            (lds_void_t*)(ul + (size_t)(U0 + wbase) * 16), 16, 0, 0);
+    }
+  };
+  f32x16 acc[TPW];
+  float hs = 0.0f;   // z~ = 1 row: sum of the gathered rows (threads tid < DL)
+  auto multiply = [&](int cnt) {
+    const int nks = (cnt + 15) / 16;
+    for (int ks = 0; ks < nks; ++ks) {
+#pragma unroll
+      for (int j = 0; j < TPW; ++j) {
+        const int ti = wv + NW * j;
+        const int kt = ti / S::NCT, ct = ti % S::NCT;
+        bf16x8 A = lds_frag_rows(zl, S::ZP, ks * 16, kt * 32);
+        if (ks * 16 + 16 > cnt) {   // slots past the last edge
+#pragma unroll
+          for (int t = 0; t < 8; ++t)
+            if (ks * 16 + 8 * hh + t >= cnt) A[t] = (__bf16)0.0f;
+        }
+        acc[j] = M::mma(A, lds_frag_rows(ul, S::UP, ks * 16, ct * 32), acc[j]);
+      }
+    }
+    if (tid < DL)
+      for (int e = 0; e < cnt; ++e) hs += (float)*reinterpret_cast<const __bf16*>(ul + e * S::UP + tid * 2);
+  };
+
+  int64_t n = blockIdx.x;
+  if (n >= a.n_seg) return;
+  int64_t pa, pb, pa1, pb1, pa2, pb2;
+  bounds(n, pa, pb);
+  bounds(n + G, pa1, pb1);
+  bounds(n + 2 * G, pa2, pb2);
+  // the first chunk of segment n, and the ids of segment n + G (and the edge
+  // ids of n + 2G) ahead
+  int pz1 = 0, pu1 = 0, pz2 = 0;
+  if (tid < ECH && pb > pa) {
+    const int z = edge_of(slot_pos(pa, pb));
+    rz[tid] = z;
+    ru[tid] = a.row_of[z];
+  }
+  if (tid < ECH && pb1 > pa1) pz1 = edge_of(slot_pos(pa1, pb1));
+  lds_sync();
+  if (pb > pa) copy_chunk();
+  if (tid < ECH && pb1 > pa1) pu1 = a.row_of[pz1];
+  bool first_iter = true;
+  for (; n < a.n_seg; n += G) {
+    // the copy of this segment's first chunk; after it only the previous
+    // segment's stores (2 TPW per thread) went out
+    if (first_iter) stage_wait();
+    else __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * TPW));
+    first_iter = false;
+    lds_sync();
+    if (tid < ECH && pb2 > pa2) pz2 = edge_of(slot_pos(pa2, pb2));   // two segments ahead
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) acc[j] = f32x16{};
+    hs = 0.0f;
+    if (pb > pa) multiply((int)(pb - pa < ECH ? pb - pa : ECH));
+    for (int64_t c0 = pa + ECH; c0 < pb; c0 += ECH) {   // segments of more than ECH edges
+      lds_sync();
+      if (tid < ECH) {
+        const int z = edge_of(slot_pos(c0, pb));
+        rz[tid] = z;
+        ru[tid] = a.row_of[z];
+      }
+      lds_sync();
+      copy_chunk();
+      stage_wait();
+      lds_sync();
+      multiply((int)(pb - c0 < ECH ? pb - c0 : ECH));
+    }
+    unsigned char* o = a.out + (size_t)n * S::KTOT * 2;
+    // the z~ = 1 row before the next copy, so that exactly 2 TPW stores follow it
+    if (tid < DL) reinterpret_cast<__bf16*>(o)[(size_t)H2 * DL + tid] = (__bf16)hs;
+    lds_sync();   // every wave is done with the chunk buffers and ids
+    if (tid < ECH && pb1 > pa1) {
+      rz[tid] = pz1;
+      ru[tid] = pu1;
+    }
+    lds_sync();
+    if (pb1 > pa1) copy_chunk();   // segment n + G's first chunk, ahead of this segment's stores
+    if (tid < ECH && pb2 > pa2) pu1 = a.row_of[pz2];
+    pz1 = pz2;
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) {
+      const int ti = wv + NW * j;
+      unsigned char* dst = o + ((size_t)ti * 1024 + lane * 16) * 2;
+      float v[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) v[r] = acc[j][r];
+      *reinterpret_cast<bf16x8*>(dst) = pack_frag<__bf16>(v);
+      *reinterpret_cast<bf16x8*>(dst + 16) = pack_frag<__bf16>(v + 8);
+    }
+    pa = pa1; pb = pb1;
+    pa1 = pa2; pb1 = pb2;
+    bounds(n + 3 * G, pa2, pb2);
+  }
+}
+
 template <typename K>
 dsmp_status set_lds_bytes(dsmp_handle* h, K kernel, int bytes) {
   DSMP_HIP(h, hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
@@ -606,8 +753,12 @@ dsmp_status outer_shape(dsmp_handle* h, const OuterArgs& a) {
     if (per_cu >= 4) {
       hipLaunchKernelGGL(single, dim3((unsigned)a.n_seg), dim3(256), S::LDS, h->stream, a);
     } else {
-      // few workgroups fit: eight waves per workgroup, half the tiles per wave
-      auto ahead8 = k_outer_sum_tr<DL, H2, true, 8>;
+      // few workgroups fit: eight waves per workgroup, half the tiles per wave,
+      // the next segment's first chunk copied ahead of this segment's stores
+      auto ahead8 = [] {
+        if constexpr (S::NTILE % 8 == 0) return k_outer_sum_pf<DL, H2, 8>;
+        else return k_outer_sum_tr<DL, H2, true, 8>;
+      }();
       if ((st = set_lds_bytes(h, ahead8, S::LDS)) != DSMP_OK) return st;
       int per_cu8 = 0;
       DSMP_HIP(h, hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu8, ahead8, 512, S::LDS));
