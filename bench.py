@@ -134,6 +134,9 @@ def work_model(w, E, n_src, fused=False, n_dst=None):
     esz = 2 if w.dtype == "bf16" else 4
     kt = (H2 + 1) * d                  # length of a segment-sum row
     mask = (H1 + H2) // 8              # ReLU mask bytes per edge
+    # z1 rows are kept for the backward unless it recomputes them: the fused
+    # edge-gradient pass, or the dW2 pass at d = 128, h1 = h2 = 256 (bf16)
+    keeps_z1 = not fused and not (w.dtype == "bf16" and (d, H1, H2) == (128, 256, 256))
     idx = 8                            # two int32 indices per edge
     attr = 2 * (D + 1) * 4             # node attribute rows of both ends
     m = {
@@ -142,13 +145,16 @@ def work_model(w, E, n_src, fused=False, n_dst=None):
                      E * (idx + attr + d * esz + (H1 + H2) * esz + mask) + n * d * 4),
         "edge_dh": (2 * E * (H2 + 1) * d * d, E * (idx + d * esz + H2 * esz) + n_src * d * 4),
         # aggregate form
-        "edge_mlp": (2 * E * (de * H1 + H1 * H2), E * (idx + attr + (H2 if fused else H1 + H2) * esz + mask)),
+        # the split attributes (32 bytes) are stored for the unfused backward, z1
+        # too where the dW2 pass does not recompute it (d = 128, h = 256)
+        "edge_mlp": (2 * E * (de * H1 + H1 * H2),
+                     E * (idx + attr + H2 * esz + mask + (0 if fused else 32) + (H1 * esz if keeps_z1 else 0))),
         "outer_fwd": (2 * E * H2 * d, E * (4 + H2 * esz + d * esz) + n * kt * esz),
         "gemm_fwd": (2 * n * kt * d, n * kt * esz + gemm_slices(n) * n * d * 4),
         "outer_dh": (2 * E * H2 * d, E * (idx + H2 * esz + d * esz) + n_src * kt * esz),
         "gemm_dh": (2 * n_src * kt * d, n_src * kt * esz + gemm_slices(n_src) * n_src * d * 4),
         "u_gemm": (2 * n * d * H2 * d, n * d * esz + n * H2 * d * esz),
-        "dW2": (2 * E * H1 * H2, E * (H1 + H2) * esz),
+        "dW2": (2 * E * H1 * H2, E * ((H1 if keeps_z1 else 0) + H2) * esz + (0 if keeps_z1 else 32 * E)),
     }
     return m
 

@@ -431,6 +431,9 @@ int layer_attr_width(const dsmp_layer_desc& d);
 // pass (bf16, h1 = h2 in {64, 128}, d in {32, 64}).  That pass recomputes z1
 // and the edge attributes, so the forward then stores neither.
 bool fused_edge_grads(const dsmp_layer_desc& d);
+// bf16 aggregate layers at d = 128, h1 = h2 = 256: dz with the feature-gradient
+// terms in one pass, da1 with the dW1 sums, dW2 with z1 recomputed
+bool dz_with_m(const dsmp_layer_desc& d, bool agg);
 
 // Aggregate form of the edge contraction (nnconv_agg.hip).
 bool use_aggregate(const dsmp_handle* h, const dsmp_layer_desc& d, int64_t n_dst, int64_t E);

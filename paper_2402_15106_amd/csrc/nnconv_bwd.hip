@@ -1339,8 +1339,11 @@ struct W2Args {
   int64_t per_chunk;
   int nsplit;
   const unsigned char* da2E;   // [E][h2] permuted
-  const unsigned char* z1E;    // [E][h1] permuted
+  const unsigned char* z1E;    // [E][h1] permuted, or null: recomputed from xE (k_bwd_dW2_rz)
   float* part;                 // [nchunk][h2*h1 + h2]
+  const unsigned char* xE;     // [E][32 bytes] bf16 high parts 0..7, low parts 8..15 (k_bwd_dW2_rz)
+  const unsigned char* w1l;    // packed W1, fp32 [2][h1/2][8] (k_bwd_dW2_rz)
+  const unsigned char* b1l;    // packed b1, fp32 [2][h1/2] (k_bwd_dW2_rz)
 };
 
 template <typename T, int H1, int H2>
@@ -1528,6 +1531,172 @@ __global__ __launch_bounds__(W8 ? 512 : 256, W8 ? 1 : 2) void k_bwd_dW2_tr(W2Arg
       }
   }
   if (split == 0 && tid < H2) out[H2 * H1 + kperm<__bf16>(tid)] = bsum;
+}
+
+// dW2 and db2 where the forward kept no z1 rows (d = 128, h1 = h2 = 256):
+// z1 = ReLU(W1 x + b1) of each chunk of edges is recomputed on the matrix
+// cores from the saved bf16 high and low parts of x, as the fused
+// edge-gradient pass does (W1h xh + W1h xl + W1l xh + b1h + b1l with fp32
+// accumulation, within about 2^-16 of the forward's fp32 chain), rounded to
+// bf16 into the chunk's z1 rows in LDS; the dW2 products, the waves' tiles
+// and the outputs are those of k_bwd_dW2_tr with eight waves.  Wave w forms
+// the z1 row blocks 2 (w % 4), 2 (w % 4) + 1 of edge block w / 4 of the chunk.
+// Two statically distinct chunk buffers alternate in code; the next chunk's
+// attribute rows are loaded ahead of its da2 copy.
+template <int H1, int H2>
+__global__ __launch_bounds__(512, 1) void k_bwd_dW2_rz(W2Args a) {
+  using S = W2TrTiles<H1, H2, true>;
+  using TS = W2TrShape<H1, H2>;
+  using M = MT<__bf16>;
+  constexpr int ECH = TS::ECH;
+  static_assert(ECH == 64 && H1 == 256, "two 32-edge blocks per chunk, eight 32-row blocks of z1 per block");
+  __shared__ __align__(16) unsigned char XA[TS::BUF], XB[TS::BUF];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hh = lane >> 5, l32 = lane & 31;
+  const int kt0 = (wv / 2) * 2, jt0 = (wv % 2) * 4, sb = wv / 4;
+  const int64_t e_begin = (int64_t)blockIdx.x * a.per_chunk;
+  int64_t e_end = e_begin + a.per_chunk;
+  if (e_end > a.E) e_end = a.E;
+  if (e_begin >= e_end) return;   // uniform over the workgroup (the launch has no empty chunk)
+  // A operands of the z1 products: row R of block zb holds the layer-1
+  // weights of stored position (2 zb + i/8)*16 + hr*8 + i%8, R = 8(i/4) +
+  // 4 hr + i%4; K slots 0..7 W1h, 8..15 W1h, 16..23 W1l, 24 b1h, 25 b1l
+  bf16x8 wa[2], wb[2];
+  {
+    const float* w1 = reinterpret_cast<const float*>(a.w1l);
+    const float* b1 = reinterpret_cast<const float*>(a.b1l);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int zb = 2 * (wv % 4) + q;
+      const int R = l32, i = 4 * (R / 8) + R % 4, hr = (R % 8) / 4;
+      const int pos = (2 * zb + i / 8) * 16 + hr * 8 + i % 8;
+      const int hn = ((pos % 16) / 8) * (H1 / 2) + (pos / 16) * 8 + pos % 8;
+      const f32x4 w0 = *reinterpret_cast<const f32x4*>(w1 + hn * 8);
+      const f32x4 w4 = *reinterpret_cast<const f32x4*>(w1 + hn * 8 + 4);
+      const float wvv[8] = {w0[0], w0[1], w0[2], w0[3], w4[0], w4[1], w4[2], w4[3]};
+      const float bb = b1[hn];
+      float v0[8], v1[8];
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const float whi = (float)(__bf16)wvv[c];
+        v0[c] = whi;                          // slots 0..7 (times xh) and 8..15 (times xl)
+        v1[c] = hh ? 0.0f : wvv[c] - whi;     // slots 16..23 (times xh)
+      }
+      if (hh) {
+        const float bhi = (float)(__bf16)bb;
+        v1[0] = bhi;
+        v1[1] = bb - bhi;
+      }
+      wa[q] = pack_frag<__bf16>(v0);
+      wb[q] = pack_frag<__bf16>(v1);
+    }
+  }
+  f32x16 acc[S::KT_W][S::JT_W];
+#pragma unroll
+  for (int kk = 0; kk < S::KT_W; ++kk)
+#pragma unroll
+    for (int jj = 0; jj < S::JT_W; ++jj) acc[kk][jj] = f32x16{};
+  float bsum = 0.0f;
+  const int nch = (int)((e_end - e_begin + ECH - 1) / ECH);
+  typename TS::DS sd;
+  auto issue = [&](int c, unsigned char* buf) {
+    if (tid >= 256) return;   // the row stage is laid out for 256 threads
+    const int64_t e0 = e_begin + (int64_t)c * ECH;
+    const int nv = (int)(e_end - e0 < ECH ? e_end - e0 : ECH);
+    sd.init(H2 * 2, nv);
+    sd.issue(a.da2E + (size_t)e0 * H2 * 2, buf);
+  };
+  // the lane's attribute half-row of its edge in block sb of chunk c
+  // (rows past the end re-read the last edge: their products are never used)
+  auto xload = [&](int c) -> uint4 {
+    int64_t e = e_begin + (int64_t)c * ECH + 32 * sb + l32;
+    if (e > e_end - 1) e = e_end - 1;
+    return *reinterpret_cast<const uint4*>(a.xE + (size_t)e * 32 + 16 * hh);
+  };
+  auto zfill = [&](const uint4& xr, unsigned char* buf) {
+    const bf16x8 xb0 = __builtin_bit_cast(bf16x8, xr);   // [xh | xl] by lane half
+    float one[8] = {1.0f, 1.0f, 0, 0, 0, 0, 0, 0};
+    const bf16x8 xb1 = hh ? pack_frag<__bf16>(one) : xb0;   // [xh | 1 1 0 ...]
+    unsigned char* zrow = buf + TS::DB + (32 * sb + l32) * TS::ZS::PITCH;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int zb = 2 * (wv % 4) + q;
+      f32x16 Z = f32x16{};
+      Z = M::mma(wa[q], xb0, Z);
+      Z = M::mma(wb[q], xb1, Z);
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        float zv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) zv[u] = relu_bits(Z[8 * r + u]);
+        *reinterpret_cast<bf16x8*>(zrow + ((2 * zb + r) * 16 + hh * 8) * 2) = pack_frag<__bf16>(zv);
+      }
+    }
+  };
+  auto products = [&](int c, const unsigned char* cur) {
+    const int64_t e0 = e_begin + (int64_t)c * ECH;
+    const int cnt = (int)(e_end - e0 < ECH ? e_end - e0 : ECH);
+    if (tid < H2)
+      for (int e = 0; e < cnt; ++e) bsum += (float)*reinterpret_cast<const __bf16*>(cur + e * TS::DS::PITCH + tid * 2);
+    for (int ks = 0; ks < (cnt + 15) / 16; ++ks) {
+      bf16x8 A[S::KT_W];
+#pragma unroll
+      for (int kk = 0; kk < S::KT_W; ++kk) {
+        A[kk] = lds_frag_rows(cur, TS::DS::PITCH, ks * 16, (kt0 + kk) * 32);
+        if (ks * 16 + 16 > cnt) {
+#pragma unroll
+          for (int t = 0; t < 8; ++t)
+            if (ks * 16 + 8 * hh + t >= cnt) A[kk][t] = (__bf16)0.0f;
+        }
+      }
+#pragma unroll
+      for (int jj = 0; jj < S::JT_W; ++jj) {
+        const bf16x8 B = lds_frag_rows(cur + TS::DB, TS::ZS::PITCH, ks * 16, (jt0 + jj) * 32);
+#pragma unroll
+        for (int kk = 0; kk < S::KT_W; ++kk) acc[kk][jj] = M::mma(A[kk], B, acc[kk][jj]);
+      }
+    }
+  };
+  // one chunk: its da2 rows copied and z1 rows written (cur); the next
+  // chunk's attribute rows, then its da2 copy, go out ahead of the products;
+  // its z1 rows are written after them
+  auto step = [&](int c, const unsigned char* cur, unsigned char* nxt) {
+    uint4 xr = make_uint4(0, 0, 0, 0);
+    if (c + 1 < nch) {
+      xr = xload(c + 1);
+      issue(c + 1, nxt);
+    }
+    products(c, cur);
+    if (c + 1 < nch) zfill(xr, nxt);
+    stage_wait();
+    __syncthreads();
+  };
+  {
+    const uint4 xr = xload(0);
+    issue(0, XA);
+    zfill(xr, XA);
+    stage_wait();
+    __syncthreads();
+  }
+  for (int c = 0;;) {
+    step(c, XA, XB);
+    if (++c >= nch) break;
+    step(c, XB, XA);
+    if (++c >= nch) break;
+  }
+  float* out = a.part + (size_t)blockIdx.x * (H2 * H1 + H2);
+  // tile rows and columns are stored-order positions; map them back to (k, j)
+#pragma unroll
+  for (int jj = 0; jj < S::JT_W; ++jj) {
+    const int j = kperm<__bf16>((jt0 + jj) * 32 + l32);
+#pragma unroll
+    for (int kk = 0; kk < S::KT_W; ++kk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int k = kperm<__bf16>((kt0 + kk) * 32 + 8 * (i / 4) + 4 * hh + (i % 4));
+        out[(size_t)k * H1 + j] = acc[kk][jj][i];
+      }
+  }
+  if (tid < H2) out[H2 * H1 + kperm<__bf16>(tid)] = bsum;
 }
 
 // ------------------------------------------------------------ dW1 / db1 (split over edges)
@@ -2364,11 +2533,7 @@ dsmp_status dispatch_dh_u(dsmp_handle* h, const dsmp_layer_desc& d, const DhuArg
 // bf16 layers of the aggregate form.
 bool dh_from_u(const dsmp_layer_desc& d, bool agg) { return agg && d.dtype == DSMP_BF16; }
 
-// Where the kernel-MLP gradients are not fused (bf16, d = 128, h1 = h2 = 256)
-// the dz pass also forms the feature-gradient terms (k_dz_dh_u).
-bool dz_with_m(const dsmp_layer_desc& d, bool agg) {
-  return dh_from_u(d, agg) && d.d == 128 && d.h1 == 256 && d.h2 == 256;
-}
+
 
 
 // ------------------------------------------------------------ workspace
@@ -2534,10 +2699,16 @@ dsmp_status run_edge_grads(dsmp_handle* h, const DzArgs& dz, const W3Args& w3, c
     if constexpr (sizeof(T) == 2) {
       using TS = W2TrShape<H1, H2>;
       if constexpr (S::NSPLIT > 1 && H1 == 256 && H2 == 256) {
-        auto k2 = k_bwd_dW2_tr<H1, H2, true>;
-        if ((st = set_lds(h, k2, TS::LDS)) != DSMP_OK) return st;
-        ProfScope prof(h, DSMP_K_DW2);
-        hipLaunchKernelGGL(k2, dim3(nchunk), dim3(512), TS::LDS, s, w2);
+        if (w2.z1E == nullptr) {   // z1 recomputed from the split attributes
+          auto k2 = k_bwd_dW2_rz<H1, H2>;
+          ProfScope prof(h, DSMP_K_DW2);
+          hipLaunchKernelGGL(k2, dim3(nchunk), dim3(512), 0, s, w2);
+        } else {
+          auto k2 = k_bwd_dW2_tr<H1, H2, true>;
+          if ((st = set_lds(h, k2, TS::LDS)) != DSMP_OK) return st;
+          ProfScope prof(h, DSMP_K_DW2);
+          hipLaunchKernelGGL(k2, dim3(nchunk), dim3(512), TS::LDS, s, w2);
+        }
       } else {
         auto k2 = k_bwd_dW2_tr<H1, H2>;
         if ((st = set_lds(h, k2, TS::LDS)) != DSMP_OK) return st;
@@ -2630,6 +2801,13 @@ void launch_node_kernels(dsmp_handle* h, const BNodeArgs& na, int64_t n_dst, con
 }  // namespace
 
 namespace dsmp {
+// Where the kernel-MLP gradients are not fused (bf16, d = 128, h1 = h2 = 256)
+// the dz pass also forms the feature-gradient terms (k_dz_dh_u), the da1 pass
+// the dW1 sums, and the dW2 pass recomputes z1 (the forward keeps no z1 rows).
+bool dz_with_m(const dsmp_layer_desc& d, bool agg) {
+  return agg && d.dtype == DSMP_BF16 && d.d == 128 && d.h1 == 256 && d.h2 == 256;
+}
+
 bool fused_edge_grads(const dsmp_layer_desc& d) {
   return d.dtype == DSMP_BF16 && d.h1 == d.h2 && (d.h1 == 64 || d.h1 == 128) && (d.d == 32 || d.d == 64);
 }
@@ -2747,7 +2925,7 @@ extern "C" dsmp_status dsmp_nnconv_backward(dsmp_handle* h, const dsmp_layer_des
     DzArgs dz{E, g->col, g->dst, hin, w.gF, pk, L, sv + sl.zE, sv + sl.zmask, w.da2E, w.da1E,
               agg ? w.U : nullptr, w.gT, n_dst, g->row_ptr};
     W3Args w3{E, w.pc3, agg ? 0 : w.n3, g->col, g->dst, hin, w.gF, sv + sl.zE, w.p_w3};
-    W2Args w2{E, w.pc2, 1, w.da2E, sv + sl.z1E, w.p_w2};
+    W2Args w2{E, w.pc2, 1, w.da2E, dzm ? nullptr : sv + sl.z1E, w.p_w2, sv + sl.xE, pk + L.w1l, pk + L.b1l};
     DzDhuArgs fm{DhuArgs{n_dst, g->row_ptr, w.U, w.gT, pk + L.b3n, sv + sl.zE, w.mE}, g->col, hin, sv + sl.zmask,
                  w.da2E};
     Da1Args fa{E, pk + L.w2t, sv + sl.zmask, w.da2E, sv + sl.xE, de, grads->dattr ? w.da1E : nullptr, w.p_w1};

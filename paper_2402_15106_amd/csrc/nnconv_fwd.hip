@@ -743,9 +743,11 @@ __global__ __launch_bounds__(64 * MlpShape<H>::WAVES, MlpShape<H>::PER_CU) void 
       for (int w = 0; w < S::MW; ++w) asm("" : "+v"(m1[w]));
     }
     if constexpr (SPLIT) {
+      if (a.z1E) {   // without z1 rows the backward recomputes z1 from the split attributes
 #pragma unroll
-      for (int s = 0; s < S::SK; ++s)
-        *reinterpret_cast<bf16x8*>(a.z1E + ((size_t)e * H + s * 16 + hh * 8) * 2) = z1B[s];
+        for (int s = 0; s < S::SK; ++s)
+          *reinterpret_cast<bf16x8*>(a.z1E + ((size_t)e * H + s * 16 + hh * 8) * 2) = z1B[s];
+      }
     }
 
     // layer 2, one 32-row tile of outputs at a time
@@ -787,9 +789,9 @@ __global__ __launch_bounds__(64 * MlpShape<H>::WAVES, MlpShape<H>::PER_CU) void 
 template <int H>
 dsmp_status launch_edge_mlp(dsmp_handle* h, const EdgeArgs& a) {
   using S = MlpShape<H>;
-  DSMP_CHECK(h, a.zE != nullptr && a.zmask != nullptr && (a.z1E == nullptr) == (a.xE == nullptr),
-             DSMP_INVALID_ARG, "kernel MLP: z and the mask bits are always stored, z1 and x together");
-  auto kern = a.z1E ? k_edge_mlp<H, true> : k_edge_mlp<H, false>;
+  DSMP_CHECK(h, a.zE != nullptr && a.zmask != nullptr && (a.z1E == nullptr || a.xE != nullptr),
+             DSMP_INVALID_ARG, "kernel MLP: z and the mask bits are always stored, z1 only with x");
+  auto kern = a.xE ? k_edge_mlp<H, true> : k_edge_mlp<H, false>;
   DSMP_HIP(h, hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                   hipFuncAttributeMaxDynamicSharedMemorySize, S::LDS));
   const int64_t ntiles = ceil_div(a.E, 32);
@@ -1136,6 +1138,7 @@ extern "C" dsmp_status dsmp_nnconv_forward(dsmp_handle* h, const dsmp_layer_desc
   ea.zE = sv + sl.zE; ea.z1E = sv + sl.z1E; ea.zmask = sv + sl.zmask;
   ea.xE = d.dtype == DSMP_BF16 ? sv + sl.xE : nullptr;
   if (agg && fused_edge_grads(d)) ea.z1E = ea.xE = nullptr;   // the backward recomputes both
+  if (dz_with_m(d, agg)) ea.z1E = nullptr;                     // the dW2 pass recomputes z1 from x
   ea.out_direct = direct; ea.out_part = part;
   if (agg) {
     // z and z1 per edge, the per-destination sums S (kept for the backward),
