@@ -984,11 +984,11 @@ struct UArgs {
 
 // U[i][c] = sum_q W[c][q] g_i[q] for c = k*DL + p, as tiles C[c][i] (A = W
 // rows, B = the g rows, lane = destination).  A workgroup owns CB
-// consecutive columns (one or two 32-column tiles per wave, whose W rows stay
+// consecutive columns (one to four 32-column tiles per wave, whose W rows stay
 // in registers for the whole launch) and a range of destinations, taken 32
 // at a time: the products land in an LDS block [32 destinations][CB columns]
-// (two buffers, one barrier per step) that is stored by whole 512-byte row
-// pieces.
+// (two buffers, one barrier per step) that is stored by whole row pieces
+// (512 bytes or 1 KB) with streaming stores.
 template <typename T, int DL, int H2>
 struct UShape {
   // columns per workgroup: row pieces of 1 KB where U rows are long enough, else 512 bytes
@@ -1053,11 +1053,15 @@ __global__ __launch_bounds__(256) void k_u_gemm(UArgs a, int64_t rows_per_wg) {
 #pragma unroll
       for (int s = 0; s < SKD; ++s) B[s] = ld_frag<T>(a.G + ((size_t)row * DL + s * KS + hh * EPL) * ESZ);
     }
+    // Each wave-wide store covers whole cache lines of one row piece; U is
+    // far larger than the caches and is next read by another kernel, so the
+    // stores carry the non-temporal (streaming) hint.
 #pragma unroll
     for (int it = 0; it < 32 * CH / 256; ++it) {
       const int id = it * 256 + tid, r = id / CH, ch = id % CH;
-      const uint4 v = *reinterpret_cast<const uint4*>(t + r * TROW + ch * 16);
-      if (i0 + r < i_end) *reinterpret_cast<uint4*>(a.U + ((size_t)(i0 + r) * NC + cb0) * ESZ + ch * 16) = v;
+      const f32x4 v = *reinterpret_cast<const f32x4*>(t + r * TROW + ch * 16);
+      if (i0 + r < i_end)
+        __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(a.U + ((size_t)(i0 + r) * NC + cb0) * ESZ + ch * 16));
     }
   }
 }
