@@ -151,6 +151,182 @@ __global__ __launch_bounds__(256) void k_bwd_node(BNodeArgs a) {
   if (tid < DL) out[DL * DL + q] = accb;
 }
 
+// bf16 layers, d = 64 or 128: the same node terms on matrix cores, with NW
+// waves and a step of NR = 32 NW / (d / 32) destinations.  Wave w holds the
+// 32 x 32 block (row tile w / QT, column tile w % QT) of the step in the
+// accumulator layout
+// (lane = column, register r = row 8(r/4) + 4h + r%4), so that every global
+// load and store covers whole cache lines across the lanes.  ybar, split into
+// bf16 high and low parts (their sum is within 2^-17 of ybar), and h (bf16
+// already) go to LDS transposed, [column][row]; from there
+//   dh_node = [G] + Wr^T ybar : A = ybar rows (transposing reads), B = Wr
+//                               columns (registers; Wr holds bf16 values);
+//   dWr += ybar^T h           : A = ybar columns, B = h columns, K = the
+//                               step's destinations; each wave keeps
+//                               QT*QT/NW tiles of the workgroup's partial sum.
+template <int DL, int NW>
+struct BNodeShape {
+  static constexpr int QT = DL / 32, RT = NW / QT, NR = 32 * RT;  // column tiles, row tiles, rows per step
+  static constexpr int TP = NR * 2 + 16 * tr_pad_units(NR * 2);   // LDS pitch of a transposed row (bytes)
+  static constexpr int NPAIR = QT * QT / NW;                      // dWr tiles per wave
+  static_assert(NPAIR >= 1 && QT * QT % NW == 0, "whole dWr tiles per wave");
+};
+
+template <int DL, int NW>
+__global__ __launch_bounds__(NW * 64, 8 / NW) void k_bwd_node_m(BNodeArgs a) {
+  using M = MT<__bf16>;
+  using S = BNodeShape<DL, NW>;
+  constexpr int QT = S::QT, NR = S::NR, TP = S::TP, SK = DL / 16, KR = NR / 16;
+  __shared__ __align__(16) unsigned char yth[DL * TP], ytl[DL * TP], ht[DL * TP];
+  __shared__ float dbs[NW][32];
+  const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: row bases in scalar registers
+  const int rt = wv / QT, ct = wv % QT, q = 32 * ct + l32;
+  // B operand of dh_node: lane (p, h) holds Wr[16s + 8h + t][32ct + p]
+  bf16x8 bw[SK];
+#pragma unroll
+  for (int s = 0; s < SK; ++s) {
+    float v[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) v[t] = a.wr[(size_t)(16 * s + 8 * hh + t) * DL + q];
+    bw[s] = pack_frag<__bf16>(v);   // exact: the values are bf16 already
+  }
+  f32x16 acc2[S::NPAIR];
+#pragma unroll
+  for (int j = 0; j < S::NPAIR; ++j) acc2[j] = f32x16{};
+  float dbr = 0.0f;
+  // Register r of the accumulator layout is row 8(r/4) + 4h + r%4 of the
+  // block: a scalar base per row group r/4, one lane byte offset and a
+  // constant per register.
+  const uint32_t lo4 = (uint32_t)(4 * hh * DL + q) * 4u, lo2 = lo4 / 2;
+  auto row_of = [&](int r) { return 8 * (r / 4) + 4 * hh + r % 4; };
+  auto at4 = [&](const float* base, int64_t row0, int r) {   // element (row0 + row_of(r), q) of an fp32 array
+    return reinterpret_cast<const float*>(reinterpret_cast<const char*>(base + (row0 + 8 * (r / 4)) * DL) + lo4) +
+           (r % 4) * DL;
+  };
+  auto at2 = [&](const __bf16* base, int64_t row0, int r) {
+    return reinterpret_cast<const __bf16*>(reinterpret_cast<const char*>(base + (row0 + 8 * (r / 4)) * DL) + lo2) +
+           (r % 4) * DL;
+  };
+  const __bf16* hin = reinterpret_cast<const __bf16*>(a.h_in);
+  const int64_t i0 = (int64_t)blockIdx.x * a.per_block;
+  const int64_t i1 = i0 + a.per_block < a.n_dst ? i0 + a.per_block : a.n_dst;
+  for (int64_t b = i0; b < i1; b += NR) {
+    const int64_t rb = b + 32 * rt;   // first row of the wave's block
+    const bool full = rb + 32 <= i1;
+    float invl;   // lane l32: 1 / degree of row rb + l32 (0 without edges or past the end)
+    {
+      const int64_t i = rb + l32 < i1 ? rb + l32 : i1 - 1;
+      const int32_t d0 = a.row_ptr[i], d1 = a.row_ptr[i + 1];
+      const int deg = rb + l32 < i1 ? d1 - d0 : 0;
+      invl = deg > 0 ? 1.0f / (float)deg : 0.0f;
+    }
+    float Y[16], H[16], yb[16];
+    if (full) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        yb[r] = *at4(a.G, rb, r);
+        Y[r] = *at4(a.y, rb, r);
+        H[r] = to_f(*at2(hin, rb, r));
+      }
+    } else {   // rows past the end re-read the last row
+      const int64_t rbl = rb < i1 ? rb : i1 - 1;
+      const int rlast = (int)(i1 - 1 - rbl);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t o = (int64_t)(row_of(r) < rlast ? row_of(r) : rlast) * DL + q;
+        yb[r] = a.G[rbl * DL + o];
+        Y[r] = a.y[rbl * DL + o];
+        H[r] = to_f(hin[rbl * DL + o]);
+      }
+    }
+    float gm[16];
+    const bool relu = a.act == DSMP_ACT_RELU;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const bool ok = full || rb + row_of(r) < i1;
+      const float inv = __shfl(invl, row_of(r), 64);
+      const float v = ok && (!relu || Y[r] > 0.0f) ? yb[r] : 0.0f;
+      yb[r] = v;
+      H[r] = ok ? H[r] : 0.0f;
+      dbr += v;
+      gm[r] = v * inv;
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (full || rb + row_of(r) < i1) {
+        *const_cast<float*>(at4(a.gF, rb, r)) = gm[r];
+        *const_cast<__bf16*>(at2(reinterpret_cast<const __bf16*>(a.gT), rb, r)) = (__bf16)gm[r];
+      }
+    __syncthreads();   // the previous step's LDS reads are done
+    // transposed rows: [column q][row of the step]
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      float vh[4], vl[4], vx[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float y = yb[4 * g + u], yh = (float)(__bf16)y;
+        vh[u] = yh;
+        vl[u] = y - yh;
+        vx[u] = H[4 * g + u];
+      }
+      const int off = q * TP + (32 * rt + 8 * g + 4 * hh) * 2;
+      auto put = [&](unsigned char* base, const float* v) {
+        const bf16x2 p0 = __builtin_convertvector((f32x2){v[0], v[1]}, bf16x2);
+        const bf16x2 p1 = __builtin_convertvector((f32x2){v[2], v[3]}, bf16x2);
+        *reinterpret_cast<uint2*>(base + off) = make_uint2(__builtin_bit_cast(uint32_t, p0), __builtin_bit_cast(uint32_t, p1));
+      };
+      put(yth, vh);
+      put(ytl, vl);
+      put(ht, vx);
+    }
+    __syncthreads();
+    // dh_node of the wave's block
+    f32x16 C = f32x16{};
+#pragma unroll
+    for (int s = 0; s < SK; ++s) {
+      C = M::mma(lds_frag_rows(yth, TP, 16 * s, 32 * rt), bw[s], C);
+      C = M::mma(lds_frag_rows(ytl, TP, 16 * s, 32 * rt), bw[s], C);
+    }
+    // dh_node = [G] + C, G read again (the step's rows are in the cache)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (full || rb + row_of(r) < i1)
+        *const_cast<float*>(at4(a.dh_node, rb, r)) = (a.residual ? *at4(a.G, rb, r) : 0.0f) + C[r];
+    // the wave's dWr tiles over the step's rows
+#pragma unroll
+    for (int j = 0; j < S::NPAIR; ++j) {
+      const int idx = wv * S::NPAIR + j, qt = idx / QT, pt = idx % QT;
+#pragma unroll
+      for (int k = 0; k < KR; ++k) {
+        const int co = (16 * k + 8 * hh) * 2;
+        const bf16x8 ah = *reinterpret_cast<const bf16x8*>(yth + (32 * qt + l32) * TP + co);
+        const bf16x8 al = *reinterpret_cast<const bf16x8*>(ytl + (32 * qt + l32) * TP + co);
+        const bf16x8 bh = *reinterpret_cast<const bf16x8*>(ht + (32 * pt + l32) * TP + co);
+        acc2[j] = M::mma(ah, bh, acc2[j]);
+        acc2[j] = M::mma(al, bh, acc2[j]);
+      }
+    }
+  }
+  float* out = a.p_root + (size_t)blockIdx.x * (DL * DL + DL);
+#pragma unroll
+  for (int j = 0; j < S::NPAIR; ++j) {
+    const int idx = wv * S::NPAIR + j, qt = idx / QT, pt = idx % QT;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) out[(size_t)(32 * qt + 8 * (r / 4) + 4 * hh + r % 4) * DL + 32 * pt + l32] = acc2[j][r];
+  }
+  // dbr: the two lane halves, then the row tiles of each column tile in order
+  dbr += __shfl_xor(dbr, 32, 64);
+  if (lane < 32) dbs[wv][lane] = dbr;
+  __syncthreads();
+  if (tid < DL) {
+    float sb = 0.0f;
+#pragma unroll
+    for (int r = 0; r < S::RT; ++r) sb += dbs[r * QT + tid / 32][tid % 32];
+    out[DL * DL + tid] = sb;
+  }
+}
+
 // db3[p*d+q] = sum_i (sum_{e in E_i} h_{src(e)}[p]) g_i[q] over a chunk of destinations.
 template <typename T, int DL>
 __global__ __launch_bounds__(256) void k_bwd_db3(int64_t n_dst, int64_t per_block, const int32_t* __restrict__ row_ptr,
@@ -2796,7 +2972,12 @@ void launch_node_kernels(dsmp_handle* h, const BNodeArgs& na, int64_t n_dst, con
                          const unsigned char* h_in, const int32_t* row_ptr, const int32_t* col, bool db3) {
   hipStream_t s = h->stream;
   if (n_dst == 0) return;
-  hipLaunchKernelGGL((k_bwd_node<T, DL>), dim3(w.nr), dim3(256), 0, s, na);
+  if constexpr (std::is_same<T, __bf16>::value && DL == 64)
+    hipLaunchKernelGGL((k_bwd_node_m<64, 4>), dim3(w.nr), dim3(256), 0, s, na);
+  else if constexpr (std::is_same<T, __bf16>::value && DL == 128)
+    hipLaunchKernelGGL((k_bwd_node_m<128, 8>), dim3(w.nr), dim3(512), 0, s, na);
+  else
+    hipLaunchKernelGGL((k_bwd_node<T, DL>), dim3(w.nr), dim3(256), 0, s, na);
   if (db3)
     hipLaunchKernelGGL((k_bwd_db3<T, DL>), dim3(w.nb3), dim3(256), 0, s, n_dst, w.pb3, row_ptr, col, h_in, w.gF,
                        w.p_db3);
