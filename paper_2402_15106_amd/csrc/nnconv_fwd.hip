@@ -494,80 +494,109 @@ __global__ __launch_bounds__(256) void k_fwd_node(NodeArgs a) {
   }
 }
 
-// bf16 layers, d = 64 or 128: the root term Wr h_i on matrix cores, 32
-// destinations per wave (C[q][i] = sum_p Wr[q][p] h_i[p]; Wr and h are bf16
-// values, so the products are exact and accumulate in fp32).  Persistent
-// waves keep the Wr fragments in registers; each lane then finishes four
-// consecutive outputs of its destination per register group.
+// bf16 layers, d = 64 or 128: the root term on matrix cores,
+// C[i][q] = sum_p h_i[p] Wr[q][p] (Wr and h are bf16 values, so the products
+// are exact and accumulate in fp32).  A step covers NR = 128 / (d / 32)
+// destinations; wave w takes the 32 x 32 block (row tile w / QT, column tile
+// w % QT) in the accumulator layout (lane = column q, register r = row
+// 8(r/4) + 4h + r%4), so that the sums, h, and the three outputs move as
+// whole cache lines across the lanes.  The wave's Wr rows stay in registers.
 template <int DL>
 __global__ __launch_bounds__(256) void k_fwd_node_m(NodeArgs a) {
   using M = MT<__bf16>;
-  constexpr int QT = DL / 32, SK = DL / 16;
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, hh = lane >> 5, l32 = lane & 31;
-  bf16x8 A[QT][SK];
+  constexpr int QT = DL / 32, RT = 4 / QT, NR = 32 * RT, SK = DL / 16;
+  const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: row bases in scalar registers
+  const int rt = wv / QT, ct = wv % QT, q = 32 * ct + l32;
+  bf16x8 bw[SK];   // B operand: lane (q, h) holds Wr[q][16s + 8h + t]
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-    for (int s = 0; s < SK; ++s) {
-      const float* w = a.wr + (size_t)(32 * qt + l32) * DL + 16 * s + 8 * hh;
-      const float4 lo = *reinterpret_cast<const float4*>(w), hi = *reinterpret_cast<const float4*>(w + 4);
-      const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-      A[qt][s] = pack_frag<__bf16>(v);   // exact: the values are bf16 already
-    }
+  for (int s = 0; s < SK; ++s) {
+    const float* w = a.wr + (size_t)q * DL + 16 * s + 8 * hh;
+    const float4 lo = *reinterpret_cast<const float4*>(w), hi = *reinterpret_cast<const float4*>(w + 4);
+    const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    bw[s] = pack_frag<__bf16>(v);   // exact: the values are bf16 already
+  }
+  const float brq = a.br[q];
   const __bf16* hin = reinterpret_cast<const __bf16*>(a.h_in);
-  const int64_t ntile = (a.n_dst + 31) / 32;
-  for (int64_t tile = (int64_t)blockIdx.x * 4 + wv; tile < ntile; tile += (int64_t)gridDim.x * 4) {
-    const int64_t i = tile * 32 + l32;
-    const bool ok = i < a.n_dst;
-    const int64_t ii = ok ? i : a.n_dst - 1;
-    bf16x8 B[SK];
-#pragma unroll
-    for (int s = 0; s < SK; ++s) B[s] = ld_frag<__bf16>(hin + (size_t)ii * DL + 16 * s + 8 * hh);
-    const int32_t deg = a.row_ptr[ii + 1] - a.row_ptr[ii];
-    f32x16 acc[QT];
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      acc[qt] = f32x16{};
-#pragma unroll
-      for (int s = 0; s < SK; ++s) acc[qt] = M::mma(A[qt][s], B[s], acc[qt]);
+  const uint32_t lo4 = (uint32_t)(4 * hh * DL + q) * 4u, lo2 = lo4 / 2;
+  auto row_of = [&](int r) { return 8 * (r / 4) + 4 * hh + r % 4; };
+  // element (row0 + row_of(r), q): a scalar base per row group, the lane offset, a constant per register
+  auto at4 = [&](const float* base, int64_t row0, int r) {
+    return reinterpret_cast<const float*>(reinterpret_cast<const char*>(base + (row0 + 8 * (r / 4)) * DL) + lo4) +
+           (r % 4) * DL;
+  };
+  auto at2 = [&](const __bf16* base, int64_t row0, int r) {
+    return reinterpret_cast<const __bf16*>(reinterpret_cast<const char*>(base + (row0 + 8 * (r / 4)) * DL) + lo2) +
+           (r % 4) * DL;
+  };
+  const int64_t n = a.n_dst;
+  for (int64_t b = (int64_t)blockIdx.x * NR; b < n; b += (int64_t)gridDim.x * NR) {
+    const int64_t rb = b + 32 * rt;   // first row of the wave's block
+    if (rb >= n) continue;            // (wave-uniform) a step past the end
+    const bool full = rb + 32 <= n;
+    const int rlast = full ? 31 : (int)(n - 1 - rb);
+    int degl;   // lane l32: degree of row rb + l32
+    {
+      const int64_t i = rb + l32 < n ? rb + l32 : n - 1;
+      const int32_t d0 = a.row_ptr[i], d1 = a.row_ptr[i + 1];
+      degl = d1 - d0;
     }
-    if (!ok) continue;
+    bf16x8 A[SK];   // A operand: lane (i, h) holds h_i[16s + 8h + t]
+    {
+      const int64_t i = rb + (l32 < rlast ? l32 : rlast);
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt)
+      for (int s = 0; s < SK; ++s) A[s] = *reinterpret_cast<const bf16x8*>(hin + i * DL + 16 * s + 8 * hh);
+    }
+    // h and the sums (the K slices in order, each slice's 16 loads issued together)
+    float sum[16], hv[16];
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int q0 = 32 * qt + 8 * g + 4 * hh;
-        float y[4], out[4], sum[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-        if (a.nsl > 0) {   // the K slices in order, four outputs at a time
-          for (int k = 0; k < a.nsl; ++k) {
-            const f32x4 v = *reinterpret_cast<const f32x4*>(a.slices + (size_t)k * a.n_dst * DL + i * DL + q0);
+    for (int r = 0; r < 16; ++r) sum[r] = 0.0f;
+    if (full) {
 #pragma unroll
-            for (int u = 0; u < 4; ++u) sum[u] += v[u];
-          }
-        } else {
+      for (int r = 0; r < 16; ++r) hv[r] = (float)*at2(hin, rb, r);
+      for (int k = 0; k < a.nsl; ++k) {
+        const float* sk = a.slices + (size_t)k * n * DL;
+        float v[16];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) sum[u] = segment_sum(a.row_ptr, i, q0 + u, DL, a.direct, a.part);
-        }
-        const uint2 hraw = *reinterpret_cast<const uint2*>(hin + i * DL + q0);
-        const bf16x2 h01 = __builtin_bit_cast(bf16x2, hraw.x), h23 = __builtin_bit_cast(bf16x2, hraw.y);
-        const float hvs[4] = {(float)h01[0], (float)h01[1], (float)h23[0], (float)h23[1]};
+        for (int r = 0; r < 16; ++r) v[r] = *at4(sk, rb, r);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int q = q0 + u;
-          const float hv = hvs[u];
-          y[u] = (deg > 0 ? sum[u] / (float)deg : 0.0f) + (acc[qt][4 * g + u] + a.br[q]);
-          const float act = a.act == DSMP_ACT_RELU ? (y[u] > 0.0f ? y[u] : 0.0f) : y[u];
-          out[u] = a.residual ? hv + act : act;
-        }
-        *reinterpret_cast<f32x4*>(a.h_out + i * DL + q0) = f32x4{out[0], out[1], out[2], out[3]};
-        *reinterpret_cast<f32x4*>(a.y_saved + i * DL + q0) = f32x4{y[0], y[1], y[2], y[3]};
-        if (a.h_out_lp) {
-          const bf16x2 p0 = __builtin_convertvector((f32x2){out[0], out[1]}, bf16x2);
-          const bf16x2 p1 = __builtin_convertvector((f32x2){out[2], out[3]}, bf16x2);
-          *reinterpret_cast<uint2*>(reinterpret_cast<__bf16*>(a.h_out_lp) + i * DL + q0) =
-              make_uint2(__builtin_bit_cast(uint32_t, p0), __builtin_bit_cast(uint32_t, p1));
-        }
+        for (int r = 0; r < 16; ++r) sum[r] += v[r];
       }
+    } else {   // rows past the end re-read the last row
+      auto oi = [&](int r) { return (rb + (row_of(r) < rlast ? row_of(r) : rlast)) * DL + q; };
+#pragma unroll
+      for (int r = 0; r < 16; ++r) hv[r] = (float)hin[oi(r)];
+      for (int k = 0; k < a.nsl; ++k) {
+        const float* sk = a.slices + (size_t)k * n * DL;
+        float v[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = sk[oi(r)];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sum[r] += v[r];
+      }
+    }
+    if (a.nsl == 0) {   // per-edge form: tile partial sums
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t i = rb + (row_of(r) < rlast ? row_of(r) : rlast);
+        sum[r] = segment_sum(a.row_ptr, i, q, DL, a.direct, a.part);
+      }
+    }
+    f32x16 C = f32x16{};
+#pragma unroll
+    for (int s = 0; s < SK; ++s) C = M::mma(A[s], bw[s], C);
+    const bool relu = a.act == DSMP_ACT_RELU;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      if (!full && row_of(r) > rlast) continue;
+      const int deg = __shfl(degl, row_of(r), 64);
+      const float y = (deg > 0 ? sum[r] / (float)deg : 0.0f) + (C[r] + brq);
+      const float act = relu ? (y > 0.0f ? y : 0.0f) : y;
+      const float out = a.residual ? hv[r] + act : act;
+      *const_cast<float*>(at4(a.h_out, rb, r)) = out;
+      *const_cast<float*>(at4(a.y_saved, rb, r)) = y;
+      if (a.h_out_lp) *const_cast<__bf16*>(at2(reinterpret_cast<const __bf16*>(a.h_out_lp), rb, r)) = (__bf16)out;
+    }
   }
 }
 
@@ -1169,11 +1198,11 @@ extern "C" dsmp_status dsmp_nnconv_forward(dsmp_handle* h, const dsmp_layer_desc
     ProfScope prof(h, DSMP_K_NODE_FWD);
     if (d.dtype == DSMP_BF16) {
       if (d.d == 32) hipLaunchKernelGGL((k_fwd_node<__bf16, 32>), dim3(grid), dim3(256), 0, h->stream, na);
-      // matrix-core root term where every wave has several 32-destination
-      // tiles to spread its Wr fragment loads over; the LDS form otherwise
-      const int64_t ntile = ceil_div(g->n_dst, 32);
-      const unsigned gm = (unsigned)std::min<int64_t>(ceil_div(ntile, 4), (int64_t)h->n_cu * 8);
-      const bool mfma_root = ntile >= (int64_t)h->n_cu * 8;
+      // matrix-core root term (steps of 128 / (d / 32) destinations) where
+      // there are enough steps to fill the CUs; the LDS form otherwise
+      const int64_t nstep = ceil_div(g->n_dst, 128 / (d.d / 32));
+      const unsigned gm = (unsigned)std::min<int64_t>(nstep, (int64_t)h->n_cu * 8);
+      const bool mfma_root = nstep >= (int64_t)h->n_cu * 2;
       if (d.d == 64 && mfma_root) hipLaunchKernelGGL((k_fwd_node_m<64>), dim3(gm), dim3(256), 0, h->stream, na);
       if (d.d == 64 && !mfma_root) hipLaunchKernelGGL((k_fwd_node<__bf16, 64>), dim3(grid), dim3(256), 0, h->stream, na);
       if (d.d == 128 && mfma_root) hipLaunchKernelGGL((k_fwd_node_m<128>), dim3(gm), dim3(256), 0, h->stream, na);

@@ -238,6 +238,36 @@ def _check_backward(c, label):
         assert e <= TOL[c.dtype], (k, e)
 
 
+# Sizes at which the node kernels take the matrix-core form (at least 512
+# steps of 128 / (d / 32) destinations) while the forward's per-destination
+# sums still come in several K slices (2 at d = 64, 4 at d = 128); neither
+# size is a whole number of 32-destination blocks.  The upstream gradient is
+# nonzero on sampled rows only (the last rows among them), so the oracle
+# visits only their edges.
+NODE_SIZES = {"bf16_128": 16360, "bf16_64": 32760}
+
+
+def _node_rows_case(env, shape):
+    n = NODE_SIZES[shape]
+    g = np.random.default_rng(n)
+    rows = np.unique(np.concatenate([g.choice(n - 64, 96, replace=False), np.arange(n - 40, n)]))
+    c = random_case(env, shape, n=n, D=3, seed=n % 997)
+    G = np.zeros_like(c.G)
+    G[rows] = c.G[rows]
+    c.G, c.rows, c.key = G, rows, "node-%s" % shape
+    return c, rows
+
+
+@pytest.mark.parametrize("shape", sorted(NODE_SIZES))
+def test_node_terms_sliced_sums(env, algo, shape):
+    announce("node terms, sliced sums", shape, algo)
+    c, rows = _node_rows_case(env, shape)
+    err = rel_err(c.forward()[rows], c.oracle_forward()[rows])
+    print("E=%d forward err=%.3e" % (c.col.size, err))
+    assert err <= TOL[c.dtype]
+    _check_backward(c, "E=%d" % c.col.size)
+
+
 @pytest.mark.parametrize("name", sorted(FWD_CASES))
 def test_backward_parity(env, algo, name):
     kw = FWD_CASES[name]
