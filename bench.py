@@ -74,7 +74,7 @@ KERNEL_SOURCES = {
     "sample": SRC_CORE, "gather": SRC_CORE, "graph": SRC_GRAPH,
     "edge_fwd": SRC_FWD, "edge_dh": SRC_FWD, "edge_mlp": SRC_FWD,
     "dz": SRC_BWD, "u_gemm": SRC_BWD, "dW2": SRC_BWD, "dW1": SRC_BWD, "dh_u": SRC_BWD, "dh_final": SRC_BWD,
-    "da1": SRC_BWD,
+    "da1": SRC_BWD, "node_bwd": SRC_BWD, "node_fwd": SRC_FWD,
     "dW3": SRC_BWD + ["nnconv_agg.hip"],
     "outer_fwd": SRC_AGG, "gemm_fwd": SRC_AGG, "outer_dh": SRC_AGG, "gemm_dh": SRC_AGG,
 }
