@@ -201,6 +201,13 @@ def agg_work(w, E, n_src, fused=False):
     return out
 
 
+def boxes_view(w, n_box):
+    """The workload's shape with the inference boxes' nodes as its nodes
+    (n_dst = n_src = n_box), for the work model of the inference mode."""
+    import dataclasses
+    return dataclasses.replace(w, parts=[dataclasses.replace(w.parts[0], s=n_box)])
+
+
 def prep_work_step(w, E):
     """Algorithmic work per step of the data-preparation classes (no flops):
     sampling writes the kept indices (the keys are recomputed, nothing is
@@ -523,10 +530,9 @@ def main():
         # every box is a graph of its own and each layer launch runs over one
         # box: a launch's work is the boxes' total over the number of boxes
         # (time and work are then both averages over the boxes)
-        import dataclasses
         n_box = sum(st[1] for st in pipe.inf.stats)
         nb = sum(1 for st in pipe.inf.stats if st[1] > 0)
-        wb = dataclasses.replace(w, n_dst=n_box, n_src=n_box)
+        wb = boxes_view(w, n_box)
         work = work_model(wb, E, n_box, fused, n_dst=n_box)
         work.update(agg_work(wb, E, n_box, fused) if agg else per_edge_work(wb, E, n_box))
         work = {k: (fl / nb, by / nb) for k, (fl, by) in work.items()}
