@@ -569,7 +569,9 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": dk["gbps"], "peak": HBM_TBPS * 1e3, "unit": "GB/s", "frac": dk["frac"],
                 "algorithmic": dk["bytes"]}
-    roof.update({"kernel": dom, "traffic": measured_traffic(dom, w.name), "ms_per_launch": dk["ms_avg"],
+    # the traffic tables record the layer bench in the aggregate form
+    traffic = measured_traffic(dom, w.name) if agg and not hop and not infer else None
+    roof.update({"kernel": dom, "traffic": traffic, "ms_per_launch": dk["ms_avg"],
                  "ms_per_launch_median": dk["ms_median"], "ms_per_launch_min": dk["ms_min"]})
     executed = sum(v["flops"] * v["launches_per_step"] for v in modeled.values())
     if hop:
