@@ -2507,9 +2507,13 @@ __global__ __launch_bounds__(256) void k_dz_dh_u(DzDhuArgs a) {
   // operands in cur; the next destination's copies go to Xn, its operands to
   // nxt.  The loop alternates the two (buffers, operand sets) in code, so no
   // buffer is chosen at run time and no operand set is copied.
+  int prev_net = 0;   // edge tiles of the previous destination (its stores follow the copies)
   auto step = [&](int64_t i, const unsigned char* Xc, unsigned char* Xn, const Ops& cur, Ops& nxt) {
-    stage_wait();      // the copies of U_i and g_i (and every store before them)
-    __syncthreads();   // U_i, g_i in Xc; every wave is done with Xn
+    // the copies of U_i and g_i: after them the previous step issued only its
+    // tile's eight stores when it had one tile, which may stay in flight
+    if (prev_net == 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(8));
+    else stage_wait();
+    lds_sync();   // U_i, g_i in Xc; every wave is done with Xn (LDS only: stores stay in flight)
     int64_t pa3, pb3;
     rows(i + 3 * G, pa3, pb3);
     const int32_t c2 = first_col(pa2, pb2);
@@ -2521,6 +2525,8 @@ __global__ __launch_bounds__(256) void k_dz_dh_u(DzDhuArgs a) {
       lds_copy_async(d.U + (size_t)inext * S::UB, Xn, S::UB / 16);
       lds_copy_async(d.gT + (size_t)inext * S::GB, Xn + S::UB, S::GB / 16);
     }
+    asm volatile("" ::: "memory");   // the copies stay ahead of the tile's stores
+    __builtin_amdgcn_sched_barrier(0);
     const int net = (int)((pb - pa + 31) / 32);
     if (net > 0) item(Xc, pa, pb, 0, cur);
     for (int et = 1; et < net; ++et) {   // destinations of more than 32 edges
@@ -2535,6 +2541,7 @@ __global__ __launch_bounds__(256) void k_dz_dh_u(DzDhuArgs a) {
     pa1 = pa2; pb1 = pb2;
     pa2 = pa3; pb2 = pb3;
     c1 = c2;
+    prev_net = net;
   };
   for (int64_t i = i0;;) {
     step(i, XA, XB, opsA, opsB);
