@@ -2448,6 +2448,8 @@ __global__ __launch_bounds__(256) void k_dz_dh_u(DzDhuArgs a) {
         dz[kk] = M::mma(*reinterpret_cast<const bf16x8*>(Xb + (((KTW * wv + kk) * SKD + s) * 64 + lane) * 16),
                         o.h[s], dz[kk]);
     }
+    // The tile's only memory operations after the products: eight stores
+    // (four of m_e, four of da2).  The next step's wait count relies on it.
     if (e < pb) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
