@@ -147,26 +147,84 @@ __global__ __launch_bounds__(256) void k_cell_scatter(const float* __restrict__ 
   sidx[slot] = (int32_t)i;
 }
 
-// Visit the candidate ranges of destination i: for every neighbouring cell
-// row (3 in 2-D, 9 in 3-D) the three cells along x are one contiguous range of
-// the cell-sorted arrays.
-template <typename F>
-__device__ __forceinline__ void for_each_candidate_range(float3 p, int D, const GridParams& g,
-                                                         const int32_t* __restrict__ cstart, F f) {
-  int cx = cell_coord(p.x, g.lo[0], g.inv_c, g.dims[0]);
-  int cy = cell_coord(p.y, g.lo[1], g.inv_c, g.dims[1]);
-  int cz = D == 3 ? cell_coord(p.z, g.lo[2], g.inv_c, g.dims[2]) : 0;
-  int x0 = cx > 0 ? cx - 1 : 0, x1 = cx + 1 < g.dims[0] ? cx + 1 : g.dims[0] - 1;
-  int zlo = D == 3 ? -1 : 0, zhi = D == 3 ? 1 : 0;
-  for (int dz = zlo; dz <= zhi; ++dz) {
-    int z = cz + dz;
-    if (z < 0 || z >= g.dims[2]) continue;
-    for (int dy = -1; dy <= 1; ++dy) {
-      int y = cy + dy;
-      if (y < 0 || y >= g.dims[1]) continue;
-      int base = g.dims[0] * (y + g.dims[1] * z);
-      f(cstart[base + x0], cstart[base + x1 + 1]);
+// The candidates of a destination: for every neighbouring cell row (3 in 2-D,
+// 9 in 3-D) the three cells along x are one contiguous range of the
+// cell-sorted arrays. Lane k < 9 loads the bounds of range k, so that all of
+// them are in flight at once; the ranges are then numbered as one flat list of
+// `total` candidates (wave-uniform starts a[k] and flat offsets off[k]).
+struct Candidates {
+  int a[9];
+  int off[9];
+  int total;
+};
+
+__device__ __forceinline__ Candidates candidate_ranges(float3 p, int D, const GridParams& g,
+                                                       const int32_t* __restrict__ cstart,
+                                                       int lane) {
+  const int cx = cell_coord(p.x, g.lo[0], g.inv_c, g.dims[0]);
+  const int cy = cell_coord(p.y, g.lo[1], g.inv_c, g.dims[1]);
+  const int cz = D == 3 ? cell_coord(p.z, g.lo[2], g.inv_c, g.dims[2]) : 0;
+  const int x0 = cx > 0 ? cx - 1 : 0, x1 = cx + 1 < g.dims[0] ? cx + 1 : g.dims[0] - 1;
+  const int nr = D == 3 ? 9 : 3;
+  int a = 0, len = 0;
+  if (lane < nr) {
+    const int z = cz + (D == 3 ? lane / 3 - 1 : 0);
+    const int y = cy + lane % 3 - 1;
+    if (z >= 0 && z < g.dims[2] && y >= 0 && y < g.dims[1]) {
+      const int base = g.dims[0] * (y + g.dims[1] * z);
+      a = cstart[base + x0];
+      len = cstart[base + x1 + 1] - a;
     }
+  }
+  int inc = len;  // inclusive prefix over lanes 0..15 (lanes past nr hold 0)
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) {
+    const int v = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += v;
+  }
+  Candidates c;
+#pragma unroll
+  for (int k = 0; k < 9; ++k) {
+    c.a[k] = __builtin_amdgcn_readlane(a, k);
+    c.off[k] = __builtin_amdgcn_readlane(inc - len, k);
+  }
+  c.total = __builtin_amdgcn_readlane(inc, 15);
+  return c;
+}
+
+// Position in the cell-sorted arrays of flat candidate t (0 <= t < total).
+// Offsets never decrease, so the last range whose offset is at most t holds it.
+__device__ __forceinline__ int candidate_at(const Candidates& c, int t) {
+  int s = c.a[0] + t;
+#pragma unroll
+  for (int k = 1; k < 9; ++k)
+    if (t >= c.off[k]) s = c.a[k] + (t - c.off[k]);
+  return s;
+}
+
+// Candidates are read CAND_BATCHES x 64 at a time, all loads issued before the
+// first test.
+constexpr int CAND_BATCHES = 4;
+
+// Calls f(t, q, j) for every flat candidate t of a destination, with its
+// position and source index; lanes past the end get t >= total. Every lane of
+// the wave calls f the same number of times.
+template <typename F>
+__device__ __forceinline__ void for_each_candidate(const Candidates& c, int lane,
+                                                   const float4* __restrict__ spos,
+                                                   const int32_t* __restrict__ sidx, F f) {
+  for (int t0 = 0; t0 < c.total; t0 += 64 * CAND_BATCHES) {
+    float4 q[CAND_BATCHES];
+    int32_t j[CAND_BATCHES];
+#pragma unroll
+    for (int u = 0; u < CAND_BATCHES; ++u) {
+      const int t = t0 + 64 * u + lane;
+      const int sidx_pos = candidate_at(c, t < c.total ? t : c.total - 1);
+      q[u] = spos[sidx_pos];
+      j[u] = sidx[sidx_pos];
+    }
+#pragma unroll
+    for (int u = 0; u < CAND_BATCHES; ++u) f(t0 + 64 * u + lane, q[u], j[u]);
   }
 }
 
@@ -183,13 +241,11 @@ __global__ __launch_bounds__(256) void k_nbr_count(const float* __restrict__ pos
   if (i >= n_dst) return;
   const GridParams g = *gp;
   const float3 pi = load_pos(pos, i, D);
+  const Candidates c = candidate_ranges(pi, D, g, cstart, lane);
   uint32_t cnt = 0;
-  for_each_candidate_range(pi, D, g, cstart, [&](int a, int b) {
-    for (int t = a + lane; t < b; t += 64) {
-      float4 q = spos[t];
-      float d2 = dist2(pi, make_float3(q.x, q.y, q.z), D);
-      if (d2 <= r2 && sidx[t] != (int32_t)i) ++cnt;
-    }
+  for_each_candidate(c, lane, spos, sidx, [&](int t, float4 q, int32_t j) {
+    const float d2 = dist2(pi, make_float3(q.x, q.y, q.z), D);
+    if (t < c.total && d2 <= r2 && j != (int32_t)i) ++cnt;
   });
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
@@ -227,12 +283,20 @@ __global__ __launch_bounds__(1024) void k_graph_stats(const uint32_t* __restrict
   }
 }
 
-// Bitonic sort of P (power of two) 64-bit keys with 32-bit payload, by one
-// wave (the block is one wave, so __syncthreads is a wave barrier).
-__device__ void bitonic_kv(uint64_t* key, int32_t* val, int P) {
+// Orders shared-memory accesses between the lanes of one wave: the rows a
+// block holds are independent waves, each with its own slice of shared
+// memory, so they never wait for each other.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Bitonic sort of P (power of two) 64-bit keys with 32-bit payload, by one wave.
+__device__ void bitonic_kv(uint64_t* key, int32_t* val, int P, int lane) {
   for (int k = 2; k <= P; k <<= 1)
     for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int t = threadIdx.x; t < P; t += 64) {
+      for (int t = lane; t < P; t += 64) {
         int u = t ^ j;
         if (u > t) {
           bool up = (t & k) == 0;
@@ -243,14 +307,14 @@ __device__ void bitonic_kv(uint64_t* key, int32_t* val, int P) {
           }
         }
       }
-      __syncthreads();
+      wave_sync();
     }
 }
 
-__device__ void bitonic_u32(uint32_t* key, int P) {
+__device__ void bitonic_u32(uint32_t* key, int P, int lane) {
   for (int k = 2; k <= P; k <<= 1)
     for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int t = threadIdx.x; t < P; t += 64) {
+      for (int t = lane; t < P; t += 64) {
         int u = t ^ j;
         if (u > t) {
           bool up = (t & k) == 0;
@@ -258,8 +322,16 @@ __device__ void bitonic_u32(uint32_t* key, int P) {
           if ((a > b) == up) { key[t] = b; key[u] = a; }
         }
       }
-      __syncthreads();
+      wave_sync();
     }
+}
+
+// Place of each lane's value among the first n lanes' values (n <= 64,
+// values distinct): the number of smaller ones.
+__device__ __forceinline__ int wave_rank(uint32_t v, int n) {
+  int rank = 0;
+  for (int k = 0; k < n; ++k) rank += (uint32_t)__builtin_amdgcn_readlane((int)v, k) < v;
+  return rank;
 }
 
 __device__ __forceinline__ int next_pow2(int n) {
@@ -268,69 +340,162 @@ __device__ __forceinline__ int next_pow2(int n) {
   return p;
 }
 
-// One wave per destination row: gather the sources that pass the test into
-// LDS, apply the cap by sorting on (d2, j) or on the hashed key, sort the kept
-// sources by index and write the row.
-__global__ __launch_bounds__(64) void k_nbr_fill(const float* __restrict__ pos, int64_t n_dst,
-                                                 int64_t n_src, int D, float r2, int cap,
-                                                 int cap_mode, uint64_t seed, int lim,
-                                                 const GridParams* __restrict__ gp,
-                                                 const int32_t* __restrict__ cstart,
-                                                 const float4* __restrict__ spos,
-                                                 const int32_t* __restrict__ sidx,
-                                                 const int32_t* __restrict__ row_ptr,
-                                                 int64_t capacity, int32_t* __restrict__ col,
-                                                 int32_t* __restrict__ dst) {
+// Rows of up to 64 SEL_PER_LANE candidates take the cap by a radix select in
+// registers; longer rows sort their keys in LDS.
+constexpr int SEL_PER_LANE = 8;
+
+// Writes to js the payloads of the cap smallest of the n keys (cap < n <=
+// 64 NT) without sorting them. Keys are distinct: d2 bits with the source
+// index, or a bijective hash of a distinct counter. The cap-th smallest key K
+// is fixed bit by bit from the top (a radix select over the keys held in
+// registers, NT per lane, with counts by ballots) until one key alone matches
+// the fixed bits; the kept keys are those whose fixed bits are at most K's.
+// The high words decide unless two of them are equal at K; only then are the
+// low words visited.
+template <int NT>
+__device__ __forceinline__ void select_cap(const uint64_t* key, const int32_t* val, uint32_t* js,
+                                           int n, int cap, int lane) {
+  uint32_t kh[NT], kl[NT];
+  int32_t vr[NT];
+  uint64_t vm[NT];  // lanes that hold a key (wave-uniform)
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int u = lane + 64 * t;
+    const bool ok = u < n;
+    const uint64_t k = ok ? key[u] : ~0ull;
+    kh[t] = (uint32_t)(k >> 32);
+    kl[t] = (uint32_t)k;
+    vr[t] = ok ? val[u] : 0;
+    vm[t] = __ballot(ok);
+  }
+  int rank = cap - 1;  // K's rank among the keys that match the fixed bits
+  int tot = n;         // how many keys match them
+  uint32_t mh = 0, ph = 0, ml = 0, pl = 0;  // fixed bits of K (masks) and their values
+  for (int b = 31; b >= 0 && tot > 1; --b) {
+    const uint32_t sel = mh | (1u << b);  // bit b of ph is still clear
+    int c = 0;  // matching keys with bit b clear
+#pragma unroll
+    for (int t = 0; t < NT; ++t) c += __popcll(__ballot(((kh[t] ^ ph) & sel) == 0) & vm[t]);
+    if (rank >= c) {
+      ph |= 1u << b;
+      rank -= c;
+      tot -= c;
+    } else {
+      tot = c;
+    }
+    mh = sel;
+  }
+  for (int b = 31; b >= 0 && tot > 1; --b) {
+    const uint32_t sel = ml | (1u << b);
+    int c = 0;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      c += __popcll(__ballot(kh[t] == ph && ((kl[t] ^ pl) & sel) == 0) & vm[t]);
+    if (rank >= c) {
+      pl |= 1u << b;
+      rank -= c;
+      tot -= c;
+    } else {
+      tot = c;
+    }
+    ml = sel;
+  }
+  wave_sync();  // every key is read; js overwrites them
+  int m0 = 0;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const uint32_t h = kh[t] & mh;
+    const bool keep = h < ph || (h == ph && (kl[t] & ml) <= pl);
+    const uint64_t bm = __ballot(keep) & vm[t];
+    const int slot = m0 + __popcll(bm & ((1ull << lane) - 1ull));
+    if (((bm >> lane) & 1ull) && slot < cap) js[slot] = (uint32_t)vr[t];
+    m0 += __popcll(bm);
+  }
+}
+
+// One wave per destination row, up to four rows per block (each wave with
+// its own lim x 12 bytes of shared memory): gather the sources that pass the
+// test, apply the cap (the cap smallest keys: (d2, j) or the hashed key), sort
+// the kept sources by index and write the row.
+__global__ __launch_bounds__(256) void k_nbr_fill(const float* __restrict__ pos, int64_t n_dst,
+                                                  int64_t n_src, int D, float r2, int cap,
+                                                  int cap_mode, uint64_t seed, int lim,
+                                                  const GridParams* __restrict__ gp,
+                                                  const int32_t* __restrict__ cstart,
+                                                  const float4* __restrict__ spos,
+                                                  const int32_t* __restrict__ sidx,
+                                                  const int32_t* __restrict__ row_ptr,
+                                                  int64_t capacity, int32_t* __restrict__ col,
+                                                  int32_t* __restrict__ dst) {
   extern __shared__ __align__(16) unsigned char smem[];
-  uint64_t* key = reinterpret_cast<uint64_t*>(smem);
-  int32_t* val = reinterpret_cast<int32_t*>(smem + (size_t)lim * 8);
-  const int lane = threadIdx.x;
-  const int64_t i = blockIdx.x;
+  const int wv = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  uint64_t* key = reinterpret_cast<uint64_t*>(smem + (size_t)wv * lim * 12);
+  int32_t* val = reinterpret_cast<int32_t*>(smem + (size_t)wv * lim * 12 + (size_t)lim * 8);
+  const int64_t i = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
   if (i >= n_dst) return;
+  const int64_t base = row_ptr[i];
   const GridParams g = *gp;
   const float3 pi = load_pos(pos, i, D);
+  const Candidates c = candidate_ranges(pi, D, g, cstart, lane);
   int n = 0;
-  for_each_candidate_range(pi, D, g, cstart, [&](int a, int b) {
-    for (int t0 = a; t0 < b; t0 += 64) {
-      int t = t0 + lane;
-      bool pass = false;
-      float d2 = 0.0f;
-      int32_t j = -1;
-      if (t < b) {
-        float4 q = spos[t];
-        d2 = dist2(pi, make_float3(q.x, q.y, q.z), D);
-        j = sidx[t];
-        pass = d2 <= r2 && j != (int32_t)i;
-      }
-      uint64_t m = __ballot(pass);
-      if (pass) {
-        int slot = n + __popcll(m & ((1ull << lane) - 1ull));
-        uint64_t k = cap_mode == DSMP_CAP_KNN
-                         ? (((uint64_t)__float_as_uint(d2)) << 32) | (uint32_t)j
-                         : splitmix64(seed, (uint64_t)i * (uint64_t)n_src + (uint64_t)j);
+  for_each_candidate(c, lane, spos, sidx, [&](int t, float4 q, int32_t j) {
+    const float d2 = dist2(pi, make_float3(q.x, q.y, q.z), D);
+    const bool pass = t < c.total && d2 <= r2 && j != (int32_t)i;
+    const uint64_t m = __ballot(pass);
+    if (pass) {
+      const int slot = n + __popcll(m & ((1ull << lane) - 1ull));
+      const uint64_t k = cap_mode == DSMP_CAP_KNN
+                             ? (((uint64_t)__float_as_uint(d2)) << 32) | (uint32_t)j
+                             : splitmix64(seed, (uint64_t)i * (uint64_t)n_src + (uint64_t)j);
+      if (slot < lim) {
         key[slot] = k;
         val[slot] = j;
       }
-      n += __popcll(m);
     }
+    n += __popcll(m);
   });
-  __syncthreads();
-  if (cap > 0 && n > cap) {
-    int P = next_pow2(n);
-    for (int t = n + lane; t < P; t += 64) { key[t] = ~0ull; val[t] = INT32_MAX; }
-    __syncthreads();
-    bitonic_kv(key, val, P);
+  n = n < lim ? n : lim;
+  wave_sync();
+  uint32_t* js = reinterpret_cast<uint32_t*>(key);   // kept sources (the key array reused as uint32 scratch)
+  if (cap > 0 && n > cap && n <= 64 * SEL_PER_LANE) {
+    switch ((n + 63) >> 6) {
+      case 1: select_cap<1>(key, val, js, n, cap, lane); break;
+      case 2: select_cap<2>(key, val, js, n, cap, lane); break;
+      case 3: select_cap<3>(key, val, js, n, cap, lane); break;
+      case 4: select_cap<4>(key, val, js, n, cap, lane); break;
+      case 5: select_cap<5>(key, val, js, n, cap, lane); break;
+      case 6: select_cap<6>(key, val, js, n, cap, lane); break;
+      case 7: select_cap<7>(key, val, js, n, cap, lane); break;
+      default: select_cap<8>(key, val, js, n, cap, lane); break;
+    }
     n = cap;
+  } else {
+    if (cap > 0 && n > cap) {
+      int P = next_pow2(n);
+      for (int t = n + lane; t < P; t += 64) { key[t] = ~0ull; val[t] = INT32_MAX; }
+      wave_sync();
+      bitonic_kv(key, val, P, lane);
+      n = cap;
+    }
+    for (int t = lane; t < n; t += 64) js[t] = (uint32_t)val[t];
   }
-  // sort the kept sources by index (reuse the key array as uint32 scratch)
-  uint32_t* js = reinterpret_cast<uint32_t*>(key);
-  for (int t = lane; t < n; t += 64) js[t] = (uint32_t)val[t];
-  __syncthreads();
-  int P = next_pow2(n > 0 ? n : 1);
+  wave_sync();
+  if (n <= 64) {
+    // Rows of up to 64 kept sources are sorted in registers (the indices of
+    // a row are distinct).
+    const uint32_t mj = lane < n ? js[lane] : 0xFFFFFFFFu;
+    const int64_t e = base + wave_rank(mj, n);
+    if (lane < n && e < capacity) {
+      col[e] = (int32_t)mj;
+      dst[e] = (int32_t)i;
+    }
+    return;
+  }
+  int P = next_pow2(n);
   for (int t = n + lane; t < P; t += 64) js[t] = 0xFFFFFFFFu;
-  __syncthreads();
-  bitonic_u32(js, P);
-  const int64_t base = row_ptr[i];
+  wave_sync();
+  bitonic_u32(js, P, lane);
   for (int t = lane; t < n; t += 64) {
     int64_t e = base + t;
     if (e < capacity) {
@@ -385,20 +550,30 @@ constexpr int CSC_SORT_LDS = 2048;
 
 // One wave per source: sort its edge ids ascending (LDS bitonic; an in-place
 // insertion sort by one lane for the rare longer groups).
-__global__ __launch_bounds__(64) void k_csc_sort(const int32_t* __restrict__ csc_ptr, int64_t n_src,
-                                                 int32_t* __restrict__ csc_eid) {
-  __shared__ uint32_t buf[CSC_SORT_LDS];
-  const int64_t j = blockIdx.x;
+// Sorts each source's incoming edge ids, one wave per source and four per
+// block: up to 64 ids in registers, up to CSC_SORT_LDS in shared memory,
+// longer columns by one lane.
+__global__ __launch_bounds__(256) void k_csc_sort(const int32_t* __restrict__ csc_ptr, int64_t n_src,
+                                                  int32_t* __restrict__ csc_eid) {
+  __shared__ uint32_t sbuf[4][CSC_SORT_LDS];
+  const int wv = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int64_t j = (int64_t)blockIdx.x * 4 + wv;
   if (j >= n_src) return;
+  uint32_t* buf = sbuf[wv];
   const int a = csc_ptr[j], b = csc_ptr[j + 1], n = b - a;
   if (n <= 1) return;
-  if (n <= CSC_SORT_LDS) {
+  if (n <= 64) {
+    const uint32_t v = lane < n ? (uint32_t)csc_eid[a + lane] : 0xFFFFFFFFu;
+    const int rank = wave_rank(v, n);
+    if (lane < n) csc_eid[a + rank] = (int32_t)v;
+  } else if (n <= CSC_SORT_LDS) {
     int P = next_pow2(n);
-    for (int t = threadIdx.x; t < P; t += 64) buf[t] = t < n ? (uint32_t)csc_eid[a + t] : 0xFFFFFFFFu;
-    __syncthreads();
-    bitonic_u32(buf, P);
-    for (int t = threadIdx.x; t < n; t += 64) csc_eid[a + t] = (int32_t)buf[t];
-  } else if (threadIdx.x == 0) {
+    for (int t = lane; t < P; t += 64) buf[t] = t < n ? (uint32_t)csc_eid[a + t] : 0xFFFFFFFFu;
+    wave_sync();
+    bitonic_u32(buf, P, lane);
+    for (int t = lane; t < n; t += 64) csc_eid[a + t] = (int32_t)buf[t];
+  } else if (lane == 0) {
     for (int t = a + 1; t < b; ++t) {
       int32_t v = csc_eid[t];
       int u = t - 1;
@@ -558,8 +733,11 @@ extern "C" dsmp_status dsmp_radius_graph_build(dsmp_handle* h, const dsmp_graph_
   if (q->n_dst > 0 && E > 0) {
     int lim = 64;
     while (lim < (int)maxraw) lim <<= 1;
-    size_t lds = (size_t)lim * 12;
-    hipLaunchKernelGGL(k_nbr_fill, dim3((unsigned)q->n_dst), dim3(64), lds, s, q->pos, q->n_dst,
+    // up to four rows per block within 48 KB of shared memory (lim <= 4096)
+    const int rows = std::min(4, std::max(1, 49152 / (lim * 12)));
+    const size_t lds = (size_t)rows * lim * 12;
+    hipLaunchKernelGGL(k_nbr_fill, dim3((unsigned)ceil_div(q->n_dst, rows)), dim3(64 * rows), lds, s,
+                       q->pos, q->n_dst,
                        q->n_src, q->dim, r2, q->cap, q->cap_mode, q->seed, lim, w.grid, w.cstart,
                        w.spos, w.sidx, g->row_ptr, edge_capacity, g->col, g->dst);
     DSMP_LAUNCHED(h, "neighbour fill");
@@ -583,8 +761,8 @@ extern "C" dsmp_status dsmp_radius_graph_build(dsmp_handle* h, const dsmp_graph_
   if (E > 0) {
     hipLaunchKernelGGL(k_csc_scatter, dim3(ceil_div(E, 256)), dim3(256), 0, s, g->col, E, g->csc_ptr,
                        w.scur, g->csc_eid);
-    hipLaunchKernelGGL(k_csc_sort, dim3((unsigned)q->n_src), dim3(64), 0, s, g->csc_ptr, q->n_src,
-                       g->csc_eid);
+    hipLaunchKernelGGL(k_csc_sort, dim3((unsigned)ceil_div(q->n_src, 4)), dim3(256), 0, s, g->csc_ptr,
+                       q->n_src, g->csc_eid);
     DSMP_LAUNCHED(h, "csc build");
   }
   return DSMP_OK;

@@ -69,6 +69,11 @@ def _rand(n, D, seed):
     return np.random.default_rng(seed).uniform(0, 1, (n, D)).astype(np.float32)
 
 
+def _two_clusters(seed):
+    """513 points within 0.002 of each other, and 514 more far away."""
+    return np.concatenate([_rand(513, 3, seed) * 1e-3, _rand(514, 3, seed + 1) * 1e-3 + 10.0])
+
+
 def _long_line(r=0.02, length=300.0, pairs=4000, seed=17):
     """Points along a line 15,000 cells long (one cell across) with pairs at
     the largest float32 distance that passes the radius test, the first point
@@ -117,6 +122,14 @@ CASES = {
     "single_point": (lambda: _rand(1, 3, 14), 1, 0.1, 0, 0),
     "halo_far": (lambda: np.concatenate([_rand(500, 2, 15), _rand(500, 2, 16) + 5.0]), 500, 0.08, 0, 0),
     "long_line_15k_cells": (lambda: _long_line(), 10002, 0.02, 0, 0),
+    # rows of 65..168 candidates capped at 40: the cap is selected in registers
+    "dense_knn40": (lambda: _rand(4000, 3, 20), 4000, 0.2, 40, 0),
+    # rows of 130..555 candidates, a cap above 64: both the register select
+    # (up to 512 candidates) and the sort in shared memory (beyond)
+    "dense_random80": (lambda: _rand(4000, 2, 21), 4000, 0.2, 80, 1),
+    # two tight clusters: rows of exactly 512 and of 513 candidates
+    "clusters_512_513_knn": (lambda: _two_clusters(22), 1027, 0.01, 30, 0),
+    "clusters_512_513_random": (lambda: _two_clusters(24), 1027, 0.01, 30, 1),
 }
 
 
