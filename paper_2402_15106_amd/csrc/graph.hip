@@ -70,20 +70,26 @@ __global__ __launch_bounds__(256) void k_bbox_partial(const float* __restrict__ 
   if (threadIdx.x < 6) part[blockIdx.x * 6 + threadIdx.x] = sh[threadIdx.x][0];
 }
 
-// One thread: reduce the partial boxes and choose the cell size.  Cells are
+// One wave reduces the partial boxes, one lane chooses the cell size.  Cells are
 // at least r*(1 + 2^-10) wide, so two points that pass the float32 radius
 // test always sit in the same or adjacent cells (cell coordinates are formed
 // in double, see cell_coord); the grid is coarsened by doubling until it has
 // at most `cap` cells.
 __global__ void k_grid_setup(const float* __restrict__ part, int nb, int D, float r, int64_t cap,
                              GridParams* __restrict__ g, GraphStats* __restrict__ st) {
-  if (threadIdx.x != 0) return;
+  const int lane = threadIdx.x;  // one wave
   float lo[3] = {INFINITY, INFINITY, INFINITY}, hi[3] = {-INFINITY, -INFINITY, -INFINITY};
-  for (int b = 0; b < nb; ++b)
+  for (int b = lane; b < nb; b += 64)
     for (int a = 0; a < 3; ++a) {
       lo[a] = fminf(lo[a], part[b * 6 + a]);
       hi[a] = fmaxf(hi[a], part[b * 6 + 3 + a]);
     }
+  for (int o = 32; o > 0; o >>= 1)
+    for (int a = 0; a < 3; ++a) {
+      lo[a] = fminf(lo[a], __shfl_xor(lo[a], o, 64));
+      hi[a] = fmaxf(hi[a], __shfl_xor(hi[a], o, 64));
+    }
+  if (lane != 0) return;
   for (int a = D; a < 3; ++a) { lo[a] = 0.0f; hi[a] = 0.0f; }
   for (int a = 0; a < 3; ++a)
     if (!(hi[a] >= lo[a])) { lo[a] = 0.0f; hi[a] = 0.0f; }   // empty input
@@ -255,31 +261,37 @@ __global__ __launch_bounds__(256) void k_nbr_count(const float* __restrict__ pos
   }
 }
 
-// Edge total (64-bit) and largest pre-cap row count, one block.
-__global__ __launch_bounds__(1024) void k_graph_stats(const uint32_t* __restrict__ rcnt,
-                                                      const uint32_t* __restrict__ rraw, int64_t n_dst,
-                                                      GraphStats* __restrict__ st) {
-  __shared__ unsigned long long ssum[1024];
-  __shared__ uint32_t smax[1024];
+// Edge total (64-bit) and largest pre-cap row count: every block reduces a
+// strided share of the rows and adds its result atomically (grid setup has
+// zeroed both).
+__global__ __launch_bounds__(256) void k_graph_stats(const uint32_t* __restrict__ rcnt,
+                                                     const uint32_t* __restrict__ rraw, int64_t n_dst,
+                                                     GraphStats* __restrict__ st) {
+  __shared__ unsigned long long ssum[4];
+  __shared__ uint32_t smax[4];
   unsigned long long s = 0;
   uint32_t m = 0;
-  for (int64_t i = threadIdx.x; i < n_dst; i += 1024) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n_dst; i += (int64_t)gridDim.x * 256) {
     s += rcnt[i];
     m = rraw[i] > m ? rraw[i] : m;
   }
-  ssum[threadIdx.x] = s;
-  smax[threadIdx.x] = m;
-  __syncthreads();
-  for (int o = 512; o > 0; o >>= 1) {
-    if ((int)threadIdx.x < o) {
-      ssum[threadIdx.x] += ssum[threadIdx.x + o];
-      smax[threadIdx.x] = smax[threadIdx.x + o] > smax[threadIdx.x] ? smax[threadIdx.x + o] : smax[threadIdx.x];
-    }
-    __syncthreads();
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    s += __shfl_xor(s, o, 64);
+    const uint32_t v = __shfl_xor(m, o, 64);
+    m = v > m ? v : m;
   }
+  if ((threadIdx.x & 63) == 0) {
+    ssum[threadIdx.x >> 6] = s;
+    smax[threadIdx.x >> 6] = m;
+  }
+  __syncthreads();
   if (threadIdx.x == 0) {
-    st->total = ssum[0];
-    st->maxraw = smax[0];
+    s = ssum[0] + ssum[1] + ssum[2] + ssum[3];
+    m = smax[0];
+    for (int k = 1; k < 4; ++k) m = smax[k] > m ? smax[k] : m;
+    atomicAdd(&st->total, s);
+    atomicMax(&st->maxraw, m);
   }
 }
 
@@ -343,6 +355,11 @@ __device__ __forceinline__ int next_pow2(int n) {
 // Rows of up to 64 SEL_PER_LANE candidates take the cap by a radix select in
 // registers; longer rows sort their keys in LDS.
 constexpr int SEL_PER_LANE = 8;
+
+// The one-pass select of capped graphs: caps up to FUSE_CAP, rows of up to
+// FUSE_LIM candidates (larger rows are built by the fill kernel).
+constexpr int FUSE_CAP = 64;
+constexpr int FUSE_LIM = 256;
 
 // Writes to js the payloads of the cap smallest of the n keys (cap < n <=
 // 64 NT) without sorting them. Keys are distinct: d2 bits with the source
@@ -416,7 +433,9 @@ __device__ __forceinline__ void select_cap(const uint64_t* key, const int32_t* v
 // One wave per destination row, up to four rows per block (each wave with
 // its own lim x 12 bytes of shared memory): gather the sources that pass the
 // test, apply the cap (the cap smallest keys: (d2, j) or the hashed key), sort
-// the kept sources by index and write the row.
+// the kept sources by index and write the row. When indeg is given, every
+// written edge also adds one to its source's in-degree. When rraw is given,
+// only rows with more than raw_above candidates are filled.
 __global__ __launch_bounds__(256) void k_nbr_fill(const float* __restrict__ pos, int64_t n_dst,
                                                   int64_t n_src, int D, float r2, int cap,
                                                   int cap_mode, uint64_t seed, int lim,
@@ -426,7 +445,9 @@ __global__ __launch_bounds__(256) void k_nbr_fill(const float* __restrict__ pos,
                                                   const int32_t* __restrict__ sidx,
                                                   const int32_t* __restrict__ row_ptr,
                                                   int64_t capacity, int32_t* __restrict__ col,
-                                                  int32_t* __restrict__ dst) {
+                                                  int32_t* __restrict__ dst,
+                                                  uint32_t* __restrict__ indeg,
+                                                  const uint32_t* __restrict__ rraw, int raw_above) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int wv = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
@@ -434,6 +455,7 @@ __global__ __launch_bounds__(256) void k_nbr_fill(const float* __restrict__ pos,
   int32_t* val = reinterpret_cast<int32_t*>(smem + (size_t)wv * lim * 12 + (size_t)lim * 8);
   const int64_t i = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
   if (i >= n_dst) return;
+  if (rraw && rraw[i] <= (uint32_t)raw_above) return;  // placed from the select's slab
   const int64_t base = row_ptr[i];
   const GridParams g = *gp;
   const float3 pi = load_pos(pos, i, D);
@@ -489,6 +511,7 @@ __global__ __launch_bounds__(256) void k_nbr_fill(const float* __restrict__ pos,
     if (lane < n && e < capacity) {
       col[e] = (int32_t)mj;
       dst[e] = (int32_t)i;
+      if (indeg) atomicAdd(&indeg[mj], 1u);
     }
     return;
   }
@@ -501,14 +524,9 @@ __global__ __launch_bounds__(256) void k_nbr_fill(const float* __restrict__ pos,
     if (e < capacity) {
       col[e] = (int32_t)js[t];
       dst[e] = (int32_t)i;
+      if (indeg) atomicAdd(&indeg[js[t]], 1u);
     }
   }
-}
-
-__global__ __launch_bounds__(256) void k_csc_count(const int32_t* __restrict__ col, int64_t E,
-                                                   uint32_t* __restrict__ indeg) {
-  int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e < E) atomicAdd(&indeg[col[e]], 1u);
 }
 
 __global__ __launch_bounds__(256) void k_csc_scatter(const int32_t* __restrict__ col, int64_t E,
@@ -550,35 +568,157 @@ constexpr int CSC_SORT_LDS = 2048;
 
 // One wave per source: sort its edge ids ascending (LDS bitonic; an in-place
 // insertion sort by one lane for the rare longer groups).
-// Sorts each source's incoming edge ids, one wave per source and four per
-// block: up to 64 ids in registers, up to CSC_SORT_LDS in shared memory,
-// longer columns by one lane.
+// Sorts each source's incoming edge ids. A wave takes CSC_COLS consecutive
+// sources (their loads issued together), four waves per block: up to 64 ids
+// are sorted in registers, up to CSC_SORT_LDS in shared memory, longer
+// columns by one lane.
+constexpr int CSC_COLS = 4;
+
 __global__ __launch_bounds__(256) void k_csc_sort(const int32_t* __restrict__ csc_ptr, int64_t n_src,
                                                   int32_t* __restrict__ csc_eid) {
   __shared__ uint32_t sbuf[4][CSC_SORT_LDS];
   const int wv = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  const int64_t j = (int64_t)blockIdx.x * 4 + wv;
-  if (j >= n_src) return;
+  const int64_t j0 = ((int64_t)blockIdx.x * 4 + wv) * CSC_COLS;
+  if (j0 >= n_src) return;
   uint32_t* buf = sbuf[wv];
-  const int a = csc_ptr[j], b = csc_ptr[j + 1], n = b - a;
-  if (n <= 1) return;
-  if (n <= 64) {
-    const uint32_t v = lane < n ? (uint32_t)csc_eid[a + lane] : 0xFFFFFFFFu;
-    const int rank = wave_rank(v, n);
-    if (lane < n) csc_eid[a + rank] = (int32_t)v;
-  } else if (n <= CSC_SORT_LDS) {
-    int P = next_pow2(n);
-    for (int t = lane; t < P; t += 64) buf[t] = t < n ? (uint32_t)csc_eid[a + t] : 0xFFFFFFFFu;
-    wave_sync();
-    bitonic_u32(buf, P, lane);
-    for (int t = lane; t < n; t += 64) csc_eid[a + t] = (int32_t)buf[t];
-  } else if (lane == 0) {
-    for (int t = a + 1; t < b; ++t) {
-      int32_t v = csc_eid[t];
-      int u = t - 1;
-      while (u >= a && csc_eid[u] > v) { csc_eid[u + 1] = csc_eid[u]; --u; }
-      csc_eid[u + 1] = v;
+  int ptr[CSC_COLS + 1];
+#pragma unroll
+  for (int c = 0; c <= CSC_COLS; ++c) ptr[c] = csc_ptr[j0 + c < n_src ? j0 + c : n_src];
+  uint32_t v[CSC_COLS];
+#pragma unroll
+  for (int c = 0; c < CSC_COLS; ++c) {
+    // in bounds for every lane: the column's own ids, else the first edge
+    const int n = ptr[c + 1] - ptr[c];
+    const int at = n > 0 ? ptr[c] + (lane < n ? lane : n - 1) : 0;
+    const uint32_t x = (uint32_t)csc_eid[at];
+    v[c] = lane < n ? x : 0xFFFFFFFFu;
+  }
+#pragma unroll
+  for (int c = 0; c < CSC_COLS; ++c) {
+    const int a = ptr[c], b = ptr[c + 1], n = b - a;
+    if (n <= 1) continue;
+    if (n <= 64) {
+      const int rank = wave_rank(v[c], n);
+      if (lane < n) csc_eid[a + rank] = (int32_t)v[c];
+    } else if (n <= CSC_SORT_LDS) {
+      int P = next_pow2(n);
+      for (int t = lane; t < P; t += 64) buf[t] = t < n ? (uint32_t)csc_eid[a + t] : 0xFFFFFFFFu;
+      wave_sync();
+      bitonic_u32(buf, P, lane);
+      for (int t = lane; t < n; t += 64) csc_eid[a + t] = (int32_t)buf[t];
+      wave_sync();  // buf is free for the next column
+    } else if (lane == 0) {
+      for (int t = a + 1; t < b; ++t) {
+        int32_t x = csc_eid[t];
+        int u = t - 1;
+        while (u >= a && csc_eid[u] > x) { csc_eid[u + 1] = csc_eid[u]; --u; }
+        csc_eid[u + 1] = x;
+      }
+    }
+  }
+}
+
+// One pass per row for capped graphs: gather the sources that pass the test,
+// keep the cap smallest keys and write them, sorted by index, to the row's cap
+// slots of the slab; count the row, and each kept edge into its source's
+// in-degree (zeroed beforehand), keeping the count it found there as the
+// edge's place among its source's edges (in no fixed order; the transpose is
+// sorted afterwards). One wave per row, four per block, each
+// wave with room for FUSE_LIM candidates: a row with more is only counted
+// (the fill kernel builds it after the scan).
+__global__ __launch_bounds__(256) void k_nbr_select(const float* __restrict__ pos, int64_t n_dst,
+                                                    int64_t n_src, int D, float r2, int cap,
+                                                    int cap_mode, uint64_t seed,
+                                                    const GridParams* __restrict__ gp,
+                                                    const int32_t* __restrict__ cstart,
+                                                    const float4* __restrict__ spos,
+                                                    const int32_t* __restrict__ sidx,
+                                                    uint32_t* __restrict__ rcnt,
+                                                    uint32_t* __restrict__ rraw,
+                                                    uint32_t* __restrict__ slab,
+                                                    uint32_t* __restrict__ indeg,
+                                                    uint32_t* __restrict__ eslot) {
+  __shared__ uint64_t skey[4][FUSE_LIM];
+  __shared__ int32_t sval[4][FUSE_LIM];
+  const int wv = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int64_t i = (int64_t)blockIdx.x * 4 + wv;
+  if (i >= n_dst) return;
+  uint64_t* key = skey[wv];
+  int32_t* val = sval[wv];
+  const GridParams g = *gp;
+  const float3 pi = load_pos(pos, i, D);
+  const Candidates c = candidate_ranges(pi, D, g, cstart, lane);
+  int n = 0;
+  for_each_candidate(c, lane, spos, sidx, [&](int t, float4 q, int32_t j) {
+    const float d2 = dist2(pi, make_float3(q.x, q.y, q.z), D);
+    const bool pass = t < c.total && d2 <= r2 && j != (int32_t)i;
+    const uint64_t m = __ballot(pass);
+    if (pass) {
+      const int slot = n + __popcll(m & ((1ull << lane) - 1ull));
+      if (slot < FUSE_LIM) {
+        key[slot] = cap_mode == DSMP_CAP_KNN
+                        ? (((uint64_t)__float_as_uint(d2)) << 32) | (uint32_t)j
+                        : splitmix64(seed, (uint64_t)i * (uint64_t)n_src + (uint64_t)j);
+        val[slot] = j;
+      }
+    }
+    n += __popcll(m);
+  });
+  const int kept = n < cap ? n : cap;
+  if (lane == 0) {
+    rraw[i] = (uint32_t)n;
+    rcnt[i] = (uint32_t)kept;
+  }
+  if (n > FUSE_LIM) return;
+  wave_sync();
+  uint32_t* js = reinterpret_cast<uint32_t*>(key);  // kept sources, over the keys
+  if (n > cap) {
+    switch ((n + 63) >> 6) {
+      case 1: select_cap<1>(key, val, js, n, cap, lane); break;
+      case 2: select_cap<2>(key, val, js, n, cap, lane); break;
+      case 3: select_cap<3>(key, val, js, n, cap, lane); break;
+      default: select_cap<4>(key, val, js, n, cap, lane); break;
+    }
+  } else {
+    for (int t = lane; t < n; t += 64) js[t] = (uint32_t)val[t];
+  }
+  wave_sync();
+  // kept <= cap <= 64: sorted in registers
+  const uint32_t mj = lane < kept ? js[lane] : 0xFFFFFFFFu;
+  const int rank = wave_rank(mj, kept);
+  if (lane < kept) {
+    slab[i * cap + rank] = mj;
+    eslot[i * cap + rank] = atomicAdd(&indeg[mj], 1u);
+  }
+}
+
+// Copies the selected rows from the slab into the CSR arrays, one thread per
+// slab entry, and, given csc_ptr, each edge id into its source's column at the
+// place the select found. Rows with more than FUSE_LIM candidates are left to
+// the fill kernel.
+__global__ __launch_bounds__(256) void k_nbr_place(int64_t n_dst, int cap, const uint32_t* __restrict__ rraw,
+                                                   const int32_t* __restrict__ row_ptr,
+                                                   const uint32_t* __restrict__ slab,
+                                                   const uint32_t* __restrict__ eslot,
+                                                   const int32_t* __restrict__ csc_ptr, int64_t capacity,
+                                                   int32_t* __restrict__ col, int32_t* __restrict__ dst,
+                                                   int32_t* __restrict__ csc_eid) {
+  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (x >= n_dst * cap) return;
+  const int64_t i = x / cap;
+  const int t = (int)(x - i * cap);
+  if (rraw[i] > (uint32_t)FUSE_LIM) return;
+  const int64_t base = row_ptr[i];
+  const int64_t e = base + t;
+  if (e < row_ptr[i + 1] && e < capacity) {
+    const uint32_t j = slab[x];
+    col[e] = (int32_t)j;
+    dst[e] = (int32_t)i;
+    if (csc_ptr) {
+      const int64_t p = (int64_t)csc_ptr[j] + eslot[x];
+      if (p < capacity) csc_eid[p] = (int32_t)e;
     }
   }
 }
@@ -599,10 +739,17 @@ struct GraphWs {
   uint32_t* indeg;
   uint32_t* scur;
   uint32_t* scan_tmp;
+  uint32_t* slab;   // n_dst x cap kept sources per row (capped graphs with cap <= FUSE_CAP)
+  uint32_t* eslot;  // n_dst x cap: each kept edge's place among its source's edges
   int64_t ncap;
 };
 
-GraphWs carve_graph_ws(void* base, int64_t n_src, int64_t n_dst, size_t* used) {
+// Capped graphs with cap <= FUSE_CAP select their rows in one pass over the
+// candidates (k_nbr_select) into a slab of n_dst x cap entries.
+bool fused_select(const dsmp_graph_query* q) { return q->cap > 0 && q->cap <= FUSE_CAP; }
+
+GraphWs carve_graph_ws(void* base, const dsmp_graph_query* q, size_t* used) {
+  const int64_t n_src = q->n_src, n_dst = q->n_dst;
   Carve c(base);
   GraphWs w;
   w.ncap = 2 * n_src + 64;
@@ -622,6 +769,8 @@ GraphWs carve_graph_ws(void* base, int64_t n_src, int64_t n_dst, size_t* used) {
   w.scur = c.take<uint32_t>(n_src);
   int64_t m = w.ncap > n_src ? w.ncap : n_src;
   w.scan_tmp = c.take<uint32_t>(scan_tmp_elems(m));
+  w.slab = fused_select(q) ? c.take<uint32_t>(n_dst * q->cap) : nullptr;
+  w.eslot = fused_select(q) ? c.take<uint32_t>(n_dst * q->cap) : nullptr;
   if (used) *used = c.used();
   return w;
 }
@@ -642,7 +791,7 @@ dsmp_status validate_query(dsmp_handle* h, const dsmp_graph_query* q) {
 // Phases shared by count and build: grid, cell sort, per-row counts, scan
 // into row_ptr.  Then the host reads back E and the largest row.
 dsmp_status count_phase(dsmp_handle* h, const dsmp_graph_query* q, const GraphWs& w, int32_t* row_ptr,
-                        int64_t* E, uint32_t* maxraw) {
+                        int64_t* E, uint32_t* maxraw, bool select) {
   const int D = q->dim;
   const float r2 = __builtin_bit_cast(float, 0) + q->r * q->r;   // fl32(r*r)
   hipStream_t s = h->stream;
@@ -667,9 +816,15 @@ dsmp_status count_phase(dsmp_handle* h, const dsmp_graph_query* q, const GraphWs
     DSMP_LAUNCHED(h, "cell scatter");
   }
   if (q->n_dst > 0) {
-    hipLaunchKernelGGL(k_nbr_count, dim3(ceil_div(q->n_dst, 4)), dim3(256), 0, s, q->pos, q->n_dst, D,
-                       r2, q->cap, w.grid, w.cstart, w.spos, w.sidx, w.rcnt, w.rraw);
-    hipLaunchKernelGGL(k_graph_stats, dim3(1), dim3(1024), 0, s, w.rcnt, w.rraw, q->n_dst, w.stats);
+    if (select)
+      hipLaunchKernelGGL(k_nbr_select, dim3(ceil_div(q->n_dst, 4)), dim3(256), 0, s, q->pos, q->n_dst,
+                         q->n_src, D, r2, q->cap, q->cap_mode, q->seed, w.grid, w.cstart, w.spos, w.sidx,
+                         w.rcnt, w.rraw, w.slab, w.indeg, w.eslot);
+    else
+      hipLaunchKernelGGL(k_nbr_count, dim3(ceil_div(q->n_dst, 4)), dim3(256), 0, s, q->pos, q->n_dst, D,
+                         r2, q->cap, w.grid, w.cstart, w.spos, w.sidx, w.rcnt, w.rraw);
+    hipLaunchKernelGGL(k_graph_stats, dim3((unsigned)std::min<int64_t>(ceil_div(q->n_dst, 2048), 256)),
+                       dim3(256), 0, s, w.rcnt, w.rraw, q->n_dst, w.stats);
     DSMP_LAUNCHED(h, "neighbour count");
   }
   if ((st = exclusive_scan_u32(h, w.rcnt, row_ptr, q->n_dst, w.scan_tmp)) != DSMP_OK) return st;
@@ -688,7 +843,7 @@ dsmp_status count_phase(dsmp_handle* h, const dsmp_graph_query* q, const GraphWs
 
 extern "C" dsmp_status dsmp_radius_graph_workspace(const dsmp_graph_query* q, size_t* bytes) {
   if (!q || !bytes || q->n_src < 0 || q->n_dst < 0) return DSMP_INVALID_ARG;
-  carve_graph_ws(nullptr, q->n_src, q->n_dst, bytes);
+  carve_graph_ws(nullptr, q, bytes);
   return DSMP_OK;
 }
 
@@ -699,11 +854,11 @@ extern "C" dsmp_status dsmp_radius_graph_count(dsmp_handle* h, const dsmp_graph_
   if (st != DSMP_OK) return st;
   DSMP_CHECK(h, n_edges != nullptr, DSMP_INVALID_ARG, "n_edges is NULL");
   size_t need;
-  GraphWs w = carve_graph_ws(ws, q->n_src, q->n_dst, &need);
+  GraphWs w = carve_graph_ws(ws, q, &need);
   DSMP_CHECK(h, ws != nullptr && ws_bytes >= need, DSMP_WORKSPACE_TOO_SMALL,
              "graph workspace needs %zu bytes", need);
   uint32_t maxraw;
-  return count_phase(h, q, w, w.rowptr_tmp, n_edges, &maxraw);
+  return count_phase(h, q, w, w.rowptr_tmp, n_edges, &maxraw, false);
 }
 
 extern "C" dsmp_status dsmp_radius_graph_build(dsmp_handle* h, const dsmp_graph_query* q, void* ws,
@@ -717,20 +872,39 @@ extern "C" dsmp_status dsmp_radius_graph_build(dsmp_handle* h, const dsmp_graph_
   DSMP_CHECK(h, g->csc_ptr != nullptr && (edge_capacity == 0 || g->csc_eid), DSMP_INVALID_ARG,
              "csc arrays are NULL");
   size_t need;
-  GraphWs w = carve_graph_ws(ws, q->n_src, q->n_dst, &need);
+  GraphWs w = carve_graph_ws(ws, q, &need);
   DSMP_CHECK(h, ws != nullptr && ws_bytes >= need, DSMP_WORKSPACE_TOO_SMALL,
              "graph workspace needs %zu bytes", need);
   ProfScope prof(h, DSMP_K_GRAPH);
   int64_t E;
   uint32_t maxraw;
-  st = count_phase(h, q, w, g->row_ptr, &E, &maxraw);
+  const bool select = fused_select(q);
+  // a symmetric graph (no cap, every source a destination) is its own transpose
+  const bool symmetric = q->cap == 0 && q->n_src == q->n_dst;
+  if (!symmetric && (st = fill_u32(h, w.indeg, q->n_src, 0, w.scur)) != DSMP_OK) return st;
+  st = count_phase(h, q, w, g->row_ptr, &E, &maxraw, select);
   g->n_dst = q->n_dst;
   g->n_src = q->n_src;
   g->n_edges = E;
   if (st != DSMP_OK) return st;
   hipStream_t s = h->stream;
   const float r2 = q->r * q->r;
-  if (q->n_dst > 0 && E > 0) {
+  // When every row fit the select pass, the in-degrees are complete and the
+  // transpose is placed with the rows; otherwise the fill kernel builds the
+  // larger rows and the transpose is scattered from col afterwards.
+  const bool overflow = select && maxraw > (uint32_t)FUSE_LIM;
+  const bool place_csc = select && !overflow;
+  if (place_csc && (st = exclusive_scan_u32(h, w.indeg, g->csc_ptr, q->n_src, w.scan_tmp)) != DSMP_OK)
+    return st;
+  if (select && q->n_dst > 0 && E > 0) {
+    const int64_t nslab = q->n_dst * q->cap;
+    hipLaunchKernelGGL(k_nbr_place, dim3((unsigned)ceil_div(nslab, 256)), dim3(256), 0, s, q->n_dst,
+                       q->cap, w.rraw, g->row_ptr, w.slab, w.eslot, place_csc ? g->csc_ptr : nullptr,
+                       edge_capacity, g->col, g->dst, g->csc_eid);
+    DSMP_LAUNCHED(h, "neighbour place");
+  }
+  // every row without the fused select, or with more candidates than it holds
+  if (q->n_dst > 0 && E > 0 && (!select || overflow)) {
     int lim = 64;
     while (lim < (int)maxraw) lim <<= 1;
     // up to four rows per block within 48 KB of shared memory (lim <= 4096)
@@ -739,30 +913,27 @@ extern "C" dsmp_status dsmp_radius_graph_build(dsmp_handle* h, const dsmp_graph_
     hipLaunchKernelGGL(k_nbr_fill, dim3((unsigned)ceil_div(q->n_dst, rows)), dim3(64 * rows), lds, s,
                        q->pos, q->n_dst,
                        q->n_src, q->dim, r2, q->cap, q->cap_mode, q->seed, lim, w.grid, w.cstart,
-                       w.spos, w.sidx, g->row_ptr, edge_capacity, g->col, g->dst);
+                       w.spos, w.sidx, g->row_ptr, edge_capacity, g->col, g->dst,
+                       symmetric ? nullptr : w.indeg, select ? w.rraw : nullptr, FUSE_LIM);
     DSMP_LAUNCHED(h, "neighbour fill");
   }
   DSMP_CHECK(h, E <= edge_capacity, DSMP_CAPACITY, "graph has %lld edges, capacity %lld",
              (long long)E, (long long)edge_capacity);
-  if (q->cap == 0 && q->n_src == q->n_dst) {
-    // symmetric graph: the transpose is the row structure itself
+  if (symmetric) {
     const int64_t n_ptr = q->n_dst + 1;
     hipLaunchKernelGGL(k_csc_symmetric, dim3((unsigned)ceil_div(std::max<int64_t>(E, n_ptr), 256)), dim3(256), 0, s,
                        g->row_ptr, n_ptr, g->col, g->dst, E, g->csc_ptr, g->csc_eid);
     DSMP_LAUNCHED(h, "csc (symmetric graph)");
     return DSMP_OK;
   }
-  if ((st = fill_u32(h, w.indeg, q->n_src, 0, w.scur)) != DSMP_OK) return st;
+  if (!place_csc && (st = exclusive_scan_u32(h, w.indeg, g->csc_ptr, q->n_src, w.scan_tmp)) != DSMP_OK)
+    return st;
   if (E > 0) {
-    hipLaunchKernelGGL(k_csc_count, dim3(ceil_div(E, 256)), dim3(256), 0, s, g->col, E, w.indeg);
-    DSMP_LAUNCHED(h, "csc count");
-  }
-  if ((st = exclusive_scan_u32(h, w.indeg, g->csc_ptr, q->n_src, w.scan_tmp)) != DSMP_OK) return st;
-  if (E > 0) {
-    hipLaunchKernelGGL(k_csc_scatter, dim3(ceil_div(E, 256)), dim3(256), 0, s, g->col, E, g->csc_ptr,
-                       w.scur, g->csc_eid);
-    hipLaunchKernelGGL(k_csc_sort, dim3((unsigned)ceil_div(q->n_src, 4)), dim3(256), 0, s, g->csc_ptr,
-                       q->n_src, g->csc_eid);
+    if (!place_csc)
+      hipLaunchKernelGGL(k_csc_scatter, dim3(ceil_div(E, 256)), dim3(256), 0, s, g->col, E, g->csc_ptr,
+                         w.scur, g->csc_eid);
+    hipLaunchKernelGGL(k_csc_sort, dim3((unsigned)ceil_div(q->n_src, 4 * CSC_COLS)), dim3(256), 0, s,
+                       g->csc_ptr, q->n_src, g->csc_eid);
     DSMP_LAUNCHED(h, "csc build");
   }
   return DSMP_OK;

@@ -130,6 +130,10 @@ CASES = {
     # two tight clusters: rows of exactly 512 and of 513 candidates
     "clusters_512_513_knn": (lambda: _two_clusters(22), 1027, 0.01, 30, 0),
     "clusters_512_513_random": (lambda: _two_clusters(24), 1027, 0.01, 30, 1),
+    # capped graphs select each row in one pass: rows of 58..264 candidates
+    # (the last few beyond what that pass holds), and a cap of exactly 64
+    "dense_random48": (lambda: _rand(4000, 2, 25), 4000, 0.132, 48, 1),
+    "dense_knn64": (lambda: _rand(4000, 3, 26), 4000, 0.2, 64, 0),
 }
 
 
@@ -141,12 +145,13 @@ def test_graph_bit_exact(env, name):
     _check_graph(lib, torch, mk(), n_dst, r, cap, mode, seed=123)
 
 
-def test_graph_capacity_error_reports_E(env):
+@pytest.mark.parametrize("cap", [0, 10])
+def test_graph_capacity_error_reports_E(env, cap):
     dm, lib, torch = env
     pos = torch.from_numpy(_rand(1000, 2, 20)).cuda()
-    E = lib.dsmp_radius_graph_count(pos, 1000, 0.05)
+    E = lib.dsmp_radius_graph_count(pos, 1000, 0.05, cap)
     with pytest.raises(dm.DsmpError) as ei:
-        lib.dsmp_radius_graph_build(pos, 1000, 0.05, capacity=E - 1)
+        lib.dsmp_radius_graph_build(pos, 1000, 0.05, cap, capacity=E - 1)
     assert ei.value.status == dm.CAPACITY
 
 
