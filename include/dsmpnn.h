@@ -178,7 +178,8 @@ typedef struct dsmp_graph {
   int32_t* csc_eid;   /* device [E]  edge ids grouped by source */
 } dsmp_graph;
 
-/* Workspace bytes for count/build of this query. */
+/* Workspace bytes for count/build of this query (for a cap of 1..64 it
+ * includes 8 * n_dst * cap bytes for the rows selected in one pass). */
 dsmp_status dsmp_radius_graph_workspace(const dsmp_graph_query* q, size_t* bytes);
 
 /* Count the edges.  SYNCHRONISES the stream; *n_edges (host) receives E.
@@ -188,8 +189,9 @@ dsmp_status dsmp_radius_graph_count(dsmp_handle* h, const dsmp_graph_query* q, v
                                     size_t ws_bytes, int64_t* n_edges);
 
 /* Build the graph into caller buffers (g->row_ptr ... g->csc_eid, sized for
- * `edge_capacity` edges).  SYNCHRONISES the stream at its end and writes
- * g->n_dst, g->n_src and g->n_edges.  If E > edge_capacity it returns
+ * `edge_capacity` edges).  SYNCHRONISES the stream once, after the row counts
+ * (the host reads E), and writes g->n_dst, g->n_src and g->n_edges; the rows
+ * and the transpose are queued on the stream after it.  If E > edge_capacity it returns
  * DSMP_CAPACITY with g->n_edges = E; then row_ptr is complete, and no edge
  * array has been written past edge_capacity. */
 dsmp_status dsmp_radius_graph_build(dsmp_handle* h, const dsmp_graph_query* q, void* ws,

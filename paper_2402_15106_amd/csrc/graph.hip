@@ -804,6 +804,8 @@ dsmp_status count_phase(dsmp_handle* h, const dsmp_graph_query* q, const GraphWs
   DSMP_LAUNCHED(h, "grid setup");
   dsmp_status st;
   if ((st = fill_u32(h, w.ccount, w.ncap, 0, w.ccur)) != DSMP_OK) return st;
+  // the select pass counts in-degrees (and the scatter's cursors start at zero)
+  if (select && (st = fill_u32(h, w.indeg, q->n_src, 0, w.scur)) != DSMP_OK) return st;
   if (n > 0) {
     hipLaunchKernelGGL(k_cell_hash, dim3(ceil_div(n, 256)), dim3(256), 0, s, q->pos, n, D, w.grid,
                        w.cellid, w.ccount);
@@ -881,7 +883,6 @@ extern "C" dsmp_status dsmp_radius_graph_build(dsmp_handle* h, const dsmp_graph_
   const bool select = fused_select(q);
   // a symmetric graph (no cap, every source a destination) is its own transpose
   const bool symmetric = q->cap == 0 && q->n_src == q->n_dst;
-  if (!symmetric && (st = fill_u32(h, w.indeg, q->n_src, 0, w.scur)) != DSMP_OK) return st;
   st = count_phase(h, q, w, g->row_ptr, &E, &maxraw, select);
   g->n_dst = q->n_dst;
   g->n_src = q->n_src;
@@ -889,6 +890,8 @@ extern "C" dsmp_status dsmp_radius_graph_build(dsmp_handle* h, const dsmp_graph_
   if (st != DSMP_OK) return st;
   hipStream_t s = h->stream;
   const float r2 = q->r * q->r;
+  // in-degrees start at zero (the count phase zeroed them for the select pass)
+  if (!select && !symmetric && (st = fill_u32(h, w.indeg, q->n_src, 0, w.scur)) != DSMP_OK) return st;
   // When every row fit the select pass, the in-degrees are complete and the
   // transpose is placed with the rows; otherwise the fill kernel builds the
   // larger rows and the transpose is scattered from col afterwards.
