@@ -113,14 +113,20 @@ struct LdsStage {
   }
 };
 
-// Copy n16 contiguous 16-byte units from global memory to contiguous LDS.
+// Cache policy of a global-to-LDS copy: the non-temporal (streaming) hint, for
+// whole-kilobyte pieces of data read once and far larger than the caches.
+constexpr int LDS_COPY_STREAM = 2;
+
+// Copy n16 contiguous 16-byte units from global memory to contiguous LDS
+// (each wave-wide load one contiguous kilobyte).
+template <int POLICY = 0>
 __device__ __forceinline__ void lds_copy_async(const unsigned char* src, unsigned char* dst, int n16) {
   const int tid = (int)threadIdx.x, wbase = tid & ~63;
   for (int i = 0; i * 256 < n16; ++i) {
     const int U = i * 256 + tid;
     if (U < n16)
       __builtin_amdgcn_global_load_lds((gbl_void_t*)(src + (size_t)U * 16),
-                                       (lds_void_t*)(dst + (size_t)(i * 256 + wbase) * 16), 16, 0, 0);
+                                       (lds_void_t*)(dst + (size_t)(i * 256 + wbase) * 16), 16, 0, POLICY);
   }
 }
 

@@ -2503,7 +2503,8 @@ __global__ __launch_bounds__(256) void k_dz_dh_u(DzDhuArgs a) {
   Ops opsA, opsB;
   load_ops(pa, pb, 0, first_col(pa, pb), opsA);
   int32_t c1 = first_col(pa1, pb1);
-  lds_copy_async(d.U + (size_t)i0 * S::UB, XA, S::UB / 16);
+  // U_i is read once, here: streaming copies
+  lds_copy_async<LDS_COPY_STREAM>(d.U + (size_t)i0 * S::UB, XA, S::UB / 16);
   lds_copy_async(d.gT + (size_t)i0 * S::GB, XA + S::UB, S::GB / 16);
   // one destination: its U_i and g_i in Xc (copied one step earlier), its
   // operands in cur; the next destination's copies go to Xn, its operands to
@@ -2524,7 +2525,7 @@ __global__ __launch_bounds__(256) void k_dz_dh_u(DzDhuArgs a) {
       // unconditional (the last step copies its own U_i again): the count of
       // operations after the operand loads then includes these copies
       const int64_t inext = i + G < d.n_dst ? i + G : i;
-      lds_copy_async(d.U + (size_t)inext * S::UB, Xn, S::UB / 16);
+      lds_copy_async<LDS_COPY_STREAM>(d.U + (size_t)inext * S::UB, Xn, S::UB / 16);
       lds_copy_async(d.gT + (size_t)inext * S::GB, Xn + S::UB, S::GB / 16);
     }
     asm volatile("" ::: "memory");   // the copies stay ahead of the tile's stores
