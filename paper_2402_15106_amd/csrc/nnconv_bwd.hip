@@ -2278,7 +2278,7 @@ __global__ __launch_bounds__(256) void k_dh_u(DhuArgs a) {
   if (i >= a.n_dst) return;
   int64_t pa = a.row_ptr[i], pb = a.row_ptr[i + 1];
   bf16x8 zb[SK2], gb[SKD];
-  lds_copy_async(a.U + (size_t)i * S::UB, X, NU);
+  lds_copy_async<LDS_COPY_STREAM>(a.U + (size_t)i * S::UB, X, NU);   // U_i: last read, streaming
   load_ops(i, pa, pb, zb, gb);
   static_assert(SK2 + SKD < 64, "wait count");
   for (int buf = 0; i < a.n_dst; i += gridDim.x, buf ^= 1) {
@@ -2292,7 +2292,7 @@ __global__ __launch_bounds__(256) void k_dh_u(DhuArgs a) {
     int64_t pa2 = 0, pb2 = 0;
     bf16x8 zn[SK2], gn[SKD];
     if (inext < a.n_dst) {
-      lds_copy_async(a.U + (size_t)inext * S::UB, X + (buf ^ 1) * S::UB, NU);
+      lds_copy_async<LDS_COPY_STREAM>(a.U + (size_t)inext * S::UB, X + (buf ^ 1) * S::UB, NU);
       pa2 = a.row_ptr[inext];
       pb2 = a.row_ptr[inext + 1];
       load_ops(inext, pa2, pb2, zn, gn);
