@@ -134,6 +134,11 @@ CASES = {
     # (the last few beyond what that pass holds), and a cap of exactly 64
     "dense_random48": (lambda: _rand(4000, 2, 25), 4000, 0.132, 48, 1),
     "dense_knn64": (lambda: _rand(4000, 3, 26), 4000, 0.2, 64, 0),
+    # a cap of one (the select keeps the single smallest key), and a cap above
+    # every row's size (no select; the fill pass, caps above 64)
+    "3d_knn1": (lambda: _rand(3000, 3, 27), 3000, 0.12, 1, 0),
+    "2d_random1": (lambda: _rand(3000, 2, 28), 3000, 0.05, 1, 1),
+    "3d_cap200": (lambda: _rand(3000, 3, 29), 3000, 0.12, 200, 0),
 }
 
 
